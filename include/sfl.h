@@ -1,0 +1,249 @@
+/*
+ * sfl.h - C ABI of libsfl, a gfx950 (MI355X) implementation of the ReLU-sparse
+ * transformer feed-forward layer of "Sparser, Faster, Lighter Transformer
+ * Language Models" (arXiv 2603.23198).
+ *
+ * Notation (the paper's Sec. 2.1, renamed): T tokens (the paper's M), model
+ * width d (the paper's K), hidden width f (the paper's N). X [T,d];
+ * W_up, W_gate [d,f]; W_down [f,d]; Y [T,d]. All matrices are row-major and
+ * contiguous. The TwELL tile width T_n, slots per tile S = T_n / C and the
+ * hybrid ELL width K are runtime parameters (sfl_twell_cfg_t).
+ *
+ * Conventions shared by every entry point:
+ *  - Ownership: every buffer pointer is caller-owned device memory (or a device
+ *    pointer obtained from the caller's allocator). The library never allocates
+ *    or frees device memory on a call path; scratch comes from a caller
+ *    workspace whose size the *_workspace_size queries return.
+ *  - Asynchrony: calls validate their arguments on the host, enqueue kernels on
+ *    the given stream and return; the library never synchronises the stream.
+ *  - Errors: argument and launch failures come back synchronously as an
+ *    sfl_status_t (no C++ exception crosses the ABI). Data-dependent outcomes
+ *    (how many rows overflowed, whether the dense-backup capacity was exceeded)
+ *    are written to device memory (sfl_twell_t.n_ovf, sfl_stats_t) and can be
+ *    read after the caller's own synchronisation.
+ *  - Reentrancy: no global mutable state; concurrent calls on different streams
+ *    with disjoint buffers are safe.
+ *  - Numerics: bf16 inputs are multiplied on MFMA with float32 accumulation;
+ *    activations are stored in the activation dtype, bf16 by round-to-nearest-
+ *    even. A hidden unit is active iff its pre-activation is > 0 (strict; +0,
+ *    -0 and NaN are inactive). Denormals are not flushed.
+ */
+#ifndef SFL_H_
+#define SFL_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* sfl_stream_t; /* a hipStream_t; NULL = the null stream */
+
+typedef enum { SFL_F32 = 0, SFL_BF16 = 1 } sfl_dtype_t;
+
+typedef enum {
+  SFL_OK = 0,
+  SFL_E_ARG = -1,          /* invalid argument (null pointer, bad size, inconsistent config) */
+  SFL_E_UNSUPPORTED = -2,  /* valid request that this build has no kernel for */
+  SFL_E_WORKSPACE = -3,    /* workspace missing or smaller than the size query returned */
+  SFL_E_HIP = -4           /* a HIP runtime call or kernel launch failed */
+} sfl_status_t;
+
+/* TwELL / hybrid parameters (Sec. 3.2 and 3.4 of the paper).
+ *  tile_rows    T_m: row tile of the producing GEMM. The TwELL layout does not
+ *               depend on it (rows are independent); 0 or a power of two <= 256.
+ *  tile_cols    T_n: width of the horizontal column tiles (>= 1).
+ *  tile_slots   S = T_n / C: stored slots per (row, tile), 1 <= S <= T_n.
+ *  ell_width    K: hybrid ELL row width (the paper's N_nz-hat), >= 0.
+ *  ovf_capacity rows of the dense backup (the paper's M^d); 0 means T. */
+typedef struct {
+  int32_t tile_rows;
+  int32_t tile_cols;
+  int32_t tile_slots;
+  int32_t ell_width;
+  int32_t ovf_capacity;
+} sfl_twell_cfg_t;
+
+/* Packed activations: TwELL (Alg. 1 outputs) plus the hybrid format (Sec. 3.4).
+ * With N_T = ceil(f / T_n), all row-major:
+ *  val       [T][N_T*S] activation dtype: val[t][j*S+s] = s-th active value of tile j
+ *  idx       [T][N_T*S] uint16 global column of that value (f <= 65535)
+ *  cnt       [T][N_T]   int32 true count of active columns in tile j (may exceed S)
+ *  row_nnz   [T]        int32 true count of active columns in row t
+ *  row_ovf   [T]        uint8 1 iff row t is a dense-backup row (row_nnz > K or
+ *                       some cnt > S), the paper's h_b
+ *  ovf_rows  [cap]      int32 dense-backup rows in ascending order (the first
+ *                       min(n_ovf, cap) entries are written)
+ *  n_ovf     [1]        int32 number of dense-backup rows (may exceed cap)
+ *  ell_val   [T][K]     activation dtype: compact ELL rows (tile slots concatenated
+ *                       in tile order = ascending columns) for rows with row_ovf = 0
+ *  ell_idx   [T][K]     uint16 columns of ell_val
+ *  ovf_dense [cap][f]   activation dtype: dense ReLU rows of the dense-backup rows,
+ *                       written by sfl_ffn_forward (training state), may be NULL
+ *                       in sfl_pack_twell.
+ * Slots s >= min(cnt, S), ELL entries beyond a row's count and the ELL rows of
+ * dense-backup rows are left unwritten (their contents are unspecified). */
+typedef struct {
+  void* val;
+  uint16_t* idx;
+  int32_t* cnt;
+  int32_t* row_nnz;
+  uint8_t* row_ovf;
+  int32_t* ovf_rows;
+  int32_t* n_ovf;
+  void* ell_val;
+  uint16_t* ell_idx;
+  void* ovf_dense;
+} sfl_twell_t;
+
+/* Buffer indices for sfl_twell_buffer_sizes, in sfl_twell_t field order. */
+enum {
+  SFL_BUF_VAL = 0, SFL_BUF_IDX, SFL_BUF_CNT, SFL_BUF_ROW_NNZ, SFL_BUF_ROW_OVF,
+  SFL_BUF_OVF_ROWS, SFL_BUF_N_OVF, SFL_BUF_ELL_VAL, SFL_BUF_ELL_IDX, SFL_BUF_OVF_DENSE,
+  SFL_NUM_BUFS
+};
+
+/* Device-resident statistics, overwritten by every call that takes them.
+ *  total_nnz          number of active (row, column) pairs
+ *  n_ovf_rows         number of dense-backup rows
+ *  n_tile_ovf         number of (row, tile) pairs with cnt > S
+ *  l1_sum             sum of the stored activation values over sparse rows plus the
+ *                     dense-backup rows that were computed (sfl_ffn_forward); times
+ *                     lambda/(T f) this is the L1 term of eq. l1 for one layer
+ *  capacity_exceeded  1 iff n_ovf_rows > ovf capacity; the outputs of the rows
+ *                     beyond the capacity are then unspecified. */
+typedef struct {
+  int64_t total_nnz;
+  int64_t n_ovf_rows;
+  int64_t n_tile_ovf;
+  double l1_sum;
+  int32_t capacity_exceeded;
+  int32_t reserved;
+} sfl_stats_t;
+
+/* Arguments of the forward entry points.
+ *  dtype     dtype of X, weights, Y and the stored activations (F32 or BF16)
+ *  gated     0: y = ReLU(X W_up + b + s) W_down  (eq. secC:eq:non-gated-mlp)
+ *            1: y = (ReLU(X W_gate + b + s) * (X W_up)) W_down (eq. sec2:eq:gated-mlp)
+ *  W_gate    [d][f], gated only
+ *  W_upT     optional [f][d] copy of W_up transposed (read by the gated up-dot);
+ *            when NULL the gated path transposes W_up into the workspace
+ *  bias_f    optional float32 [f] added to every pre-activation of column n
+ *  shift_t   optional float32 [T] added to every pre-activation of row t
+ *            (both are extensions; NULL/NULL is the paper's bias-free FFN)
+ *  twell     packed activations and hybrid state, written by the call
+ *  stats     optional device pointer
+ *  workspace device scratch of at least sfl_workspace_size() bytes (may be NULL
+ *            when that size is 0)
+ *  events / n_events  optional hipEvent_t array; when n_events >= 2 the forward
+ *            records events[i] at its stage boundaries on the call's stream
+ *            (0: start, 1: after the up projection, 2: after classification,
+ *            3: after the sparse down projection, 4: end). */
+typedef struct {
+  sfl_dtype_t dtype;
+  int32_t gated;
+  int64_t T, d, f;
+  const void* X;
+  const void* W_gate;
+  const void* W_up;
+  const void* W_down;
+  const void* W_upT;
+  const float* bias_f;
+  const float* shift_t;
+  sfl_twell_cfg_t cfg;
+  void* Y;
+  sfl_twell_t twell;
+  sfl_stats_t* stats;
+  void* workspace;
+  size_t workspace_bytes;
+  void* const* events;
+  int32_t n_events;
+} sfl_ffn_args_t;
+
+/* Arguments of the backward entry point (non-gated ReLU FFN, bf16).
+ * Gradients of  sum(dY * Y) + lambda_l1 / (T f) * sum |H|  (eq. l1 with one layer)
+ * through the activity pattern the forward saved in `saved`:
+ *   dH = dY W_down^T + lambda_l1/(T f) on active entries, dZ = dH on the pattern,
+ *   dW_down = H^T dY, dW_up = X^T dZ, dX = dZ W_up^T  (eq. sec3:eq:all_other_gradients,
+ *   non-gated case).
+ *  dX        [T][d] activation dtype (overwritten)
+ *  dW_up     float32 [d][f] (overwritten)
+ *  dW_down   float32 [f][d] (overwritten)
+ *  W_upT     optional [f][d]; transposed into the workspace when NULL. */
+typedef struct {
+  sfl_dtype_t dtype;
+  int64_t T, d, f;
+  const void* X;
+  const void* W_up;
+  const void* W_down;
+  const void* W_upT;
+  const void* dY;
+  sfl_twell_cfg_t cfg;
+  sfl_twell_t saved;
+  double lambda_l1;
+  void* dX;
+  float* dW_up;
+  float* dW_down;
+  void* workspace;
+  size_t workspace_bytes;
+  void* const* events;
+  int32_t n_events;
+} sfl_ffn_bwd_args_t;
+
+/* Human-readable name of a status code (static string). */
+const char* sfl_status_string(sfl_status_t s);
+
+/* Library version string and the offload target it was built for. */
+const char* sfl_version(void);
+
+/* Byte sizes of the ten sfl_twell_t buffers (SFL_BUF_* order) for T rows, f
+ * columns and activation dtype `val_dtype`. bytes[] must hold SFL_NUM_BUFS. */
+sfl_status_t sfl_twell_buffer_sizes(int64_t T, int64_t f, sfl_dtype_t val_dtype,
+                                    const sfl_twell_cfg_t* cfg, size_t* bytes);
+
+/* Standalone TwELL packing (Alg. 1's epilogue fed from memory) plus the hybrid
+ * classification of Sec. 3.4. Z: device float32 [T][f] pre-activations. Writes
+ * val, idx, cnt, row_nnz, row_ovf, ovf_rows, n_ovf and, when ell_val/ell_idx
+ * are non-NULL, the compact ELL rows. Any T >= 0, f in [1, 65535], any
+ * tile_cols >= 1 and 1 <= tile_slots <= tile_cols. stats may be NULL.
+ * Needs no workspace. */
+sfl_status_t sfl_pack_twell(const float* Z, int64_t T, int64_t f, sfl_dtype_t val_dtype,
+                            const sfl_twell_cfg_t* cfg, const sfl_twell_t* out,
+                            sfl_stats_t* stats, sfl_stream_t stream);
+
+/* Workspace bytes needed by sfl_ffn_forward (backward = 0), sfl_ffn_backward
+ * (backward = 1, args must point to an sfl_ffn_bwd_args_t) or
+ * sfl_dense_ffn_baseline (backward = 2). */
+sfl_status_t sfl_workspace_size(const void* args, int backward, size_t* bytes);
+
+/* Sparse FFN forward: up (or gate) projection GEMM with the ReLU -> TwELL
+ * epilogue (Alg. 1), hybrid classification (Sec. 3.4), sparse down projection
+ * of the ELL rows (Alg. 3's sparse part; Alg. 2 fused up and down when gated)
+ * and the dense path for the dense-backup rows (Alg. 3's dense part).
+ * bf16: d % 64 == 0 and f % 64 == 0; fp32: any sizes. */
+sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* args, sfl_stream_t stream);
+
+/* The pre-activation Z = X W + b + s of the forward's up (or gate) projection,
+ * as float32 [T][f], computed by the same GEMM main loop as sfl_ffn_forward.
+ * Uses args->{dtype, gated, T, d, f, X, W_up or W_gate, bias_f, shift_t}. */
+sfl_status_t sfl_up_projection(const sfl_ffn_args_t* args, float* Z, sfl_stream_t stream);
+
+/* Sparse FFN backward (see sfl_ffn_bwd_args_t). BF16 only. */
+sfl_status_t sfl_ffn_backward(const sfl_ffn_bwd_args_t* args, sfl_stream_t stream);
+
+/* The library's dense FFN on the same arguments (comparator): GEMM with a ReLU
+ * epilogue writing dense H [T][f] into the workspace, then GEMM with W_down
+ * (three GEMMs when gated). Ignores args->twell and args->stats. */
+sfl_status_t sfl_dense_ffn_baseline(const sfl_ffn_args_t* args, sfl_stream_t stream);
+
+/* out[c][r] = in[r][c] for a rows x cols matrix of 2-byte (elem_bytes = 2) or
+ * 4-byte (elem_bytes = 4) elements; lets callers keep W_upT next to W_up. */
+sfl_status_t sfl_transpose(const void* in, void* out, int64_t rows, int64_t cols,
+                           int32_t elem_bytes, sfl_stream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SFL_H_ */

@@ -1,0 +1,411 @@
+// C ABI of libsfl: argument validation, workspace layout and the stage sequence of each
+// entry point. Every stage is a kernel launch on the caller's stream; nothing here
+// synchronises or allocates device memory.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+
+#include "backward.h"
+#include "common.h"
+#include "internal.h"
+
+using namespace sfl;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+size_t elem_size(sfl_dtype_t t) { return t == SFL_BF16 ? 2 : 4; }
+
+bool dtype_ok(sfl_dtype_t t) { return t == SFL_F32 || t == SFL_BF16; }
+
+int64_t capacity_of(const sfl_twell_cfg_t& c, int64_t T) {
+  return c.ovf_capacity > 0 ? std::min<int64_t>(c.ovf_capacity, T) : T;
+}
+
+sfl_status_t check_cfg(const sfl_twell_cfg_t* c, int64_t f) {
+  if (!c) return SFL_E_ARG;
+  if (c->tile_cols < 1 || c->tile_slots < 1 || c->tile_slots > c->tile_cols) return SFL_E_ARG;
+  if (c->ell_width < 0 || c->ovf_capacity < 0) return SFL_E_ARG;
+  if (c->tile_rows != 0 && (c->tile_rows < 0 || c->tile_rows > 256 || (c->tile_rows & (c->tile_rows - 1))))
+    return SFL_E_ARG;
+  if (f < 1 || f > 65535) return SFL_E_ARG;
+  return SFL_OK;
+}
+
+// Bump allocator over the caller's workspace.
+struct Carve {
+  char* base;
+  size_t used = 0;
+  explicit Carve(void* b) : base((char*)b) {}
+  void* take(size_t bytes) {
+    void* p = base ? base + used : nullptr;
+    used += align_up(bytes);
+    return p;
+  }
+};
+
+struct Events {
+  void* const* ev;
+  int n;
+  void record(int i, hipStream_t s) const {
+    if (ev && i < n && ev[i]) (void)hipEventRecord((hipEvent_t)ev[i], s);
+  }
+};
+
+#define SFL_HIP(x)                        \
+  do {                                    \
+    if ((x) != hipSuccess) return SFL_E_HIP; \
+  } while (0)
+
+bool fused_twell(const sfl_ffn_args_t& a) {
+  const int tn = a.cfg.tile_cols;
+  return a.dtype == SFL_BF16 && (tn == 64 || tn == 128 || tn == 256);
+}
+
+sfl_status_t check_forward(const sfl_ffn_args_t* a, bool need_output = true) {
+  if (!a) return SFL_E_ARG;
+  if (!dtype_ok(a->dtype)) return SFL_E_ARG;
+  if (a->T < 0 || a->d < 1) return SFL_E_ARG;
+  sfl_status_t st = check_cfg(&a->cfg, a->f);
+  if (st != SFL_OK) return st;
+  if (a->T > 0 && !a->X) return SFL_E_ARG;
+  if (need_output && a->T > 0 && (!a->Y || !a->W_down)) return SFL_E_ARG;
+  if (a->gated && !a->W_gate) return SFL_E_ARG;
+  if (!a->W_up && !(a->gated && a->W_upT)) return SFL_E_ARG;
+  if (a->T > INT32_MAX || a->d > INT32_MAX) return SFL_E_UNSUPPORTED;
+  if (a->dtype == SFL_BF16 && (a->d % 64 != 0 || a->f % 64 != 0)) return SFL_E_UNSUPPORTED;
+  if (a->gated && a->dtype != SFL_BF16) return SFL_E_UNSUPPORTED;
+  if (a->gated && !(a->d == 512 || a->d == 1024 || a->d == 2048 || a->d == 4096)) return SFL_E_UNSUPPORTED;
+  return SFL_OK;
+}
+
+sfl_status_t check_twell(const sfl_twell_t& t, bool need_ell) {
+  if (!t.val || !t.idx || !t.cnt || !t.row_nnz || !t.row_ovf || !t.ovf_rows || !t.n_ovf) return SFL_E_ARG;
+  if (need_ell && (!t.ell_val || !t.ell_idx)) return SFL_E_ARG;
+  return SFL_OK;
+}
+
+// Workspace plan of the forward.
+struct FwdPlan {
+  float* Z = nullptr;        // unfused path: fp32 pre-activations [T][f]
+  void* ovf_dense = nullptr; // dense-backup rows when the caller gave none [cap][f]
+  void* WupT = nullptr;      // gated: W_up transposed [f][d]
+  size_t bytes = 0;
+};
+
+FwdPlan plan_forward(const sfl_ffn_args_t& a, void* ws) {
+  Carve c(ws);
+  FwdPlan p;
+  const int64_t cap = capacity_of(a.cfg, a.T);
+  if (!fused_twell(a)) p.Z = (float*)c.take((size_t)a.T * a.f * 4);
+  if (!a.twell.ovf_dense) p.ovf_dense = c.take((size_t)cap * a.f * elem_size(a.dtype));
+  if (a.gated && !a.W_upT) p.WupT = c.take((size_t)a.f * a.d * elem_size(a.dtype));
+  p.bytes = c.used;
+  return p;
+}
+
+size_t dense_ws_bytes(const sfl_ffn_args_t& a) { return align_up((size_t)a.T * a.f * elem_size(a.dtype)); }
+
+GemmParams gp_zero() {
+  GemmParams g;
+  std::memset(&g, 0, sizeof(g));
+  return g;
+}
+
+// B operand of X W for W [d][f] (row-contiguous over f) or W^T [f][d] (K-contiguous).
+void set_weight_B(GemmParams& g, const void* W, const void* WT, int64_t d, int64_t f, int* blay) {
+  if (WT) {
+    g.B = WT;
+    g.ldb = d;
+    *blay = LAY_KC;
+  } else {
+    g.B = W;
+    g.ldb = f;
+    *blay = LAY_RC;
+  }
+}
+
+hipError_t run_gemm(sfl_dtype_t dt, int alay, int blay, int epi, const GemmParams& g, hipStream_t s) {
+  if (dt == SFL_BF16) return gemm_bf16(alay, blay, epi, g, s);
+  return gemm_f32(epi, g, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sfl_status_string(sfl_status_t s) {
+  switch (s) {
+    case SFL_OK: return "SFL_OK";
+    case SFL_E_ARG: return "SFL_E_ARG: invalid argument";
+    case SFL_E_UNSUPPORTED: return "SFL_E_UNSUPPORTED: no kernel for this request";
+    case SFL_E_WORKSPACE: return "SFL_E_WORKSPACE: workspace missing or too small";
+    case SFL_E_HIP: return "SFL_E_HIP: HIP runtime or launch failure";
+  }
+  return "unknown sfl_status_t";
+}
+
+const char* sfl_version(void) { return "sfl 0.1 gfx950"; }
+
+sfl_status_t sfl_twell_buffer_sizes(int64_t T, int64_t f, sfl_dtype_t val_dtype, const sfl_twell_cfg_t* cfg,
+                                    size_t* bytes) {
+  if (!bytes || !dtype_ok(val_dtype) || T < 0) return SFL_E_ARG;
+  sfl_status_t st = check_cfg(cfg, f);
+  if (st != SFL_OK) return st;
+  const int64_t NT = cdiv(f, cfg->tile_cols);
+  const int64_t S = cfg->tile_slots, K = cfg->ell_width;
+  const int64_t cap = capacity_of(*cfg, T);
+  const size_t es = elem_size(val_dtype);
+  bytes[SFL_BUF_VAL] = (size_t)(T * NT * S) * es;
+  bytes[SFL_BUF_IDX] = (size_t)(T * NT * S) * 2;
+  bytes[SFL_BUF_CNT] = (size_t)(T * NT) * 4;
+  bytes[SFL_BUF_ROW_NNZ] = (size_t)T * 4;
+  bytes[SFL_BUF_ROW_OVF] = (size_t)T;
+  bytes[SFL_BUF_OVF_ROWS] = (size_t)cap * 4;
+  bytes[SFL_BUF_N_OVF] = 4;
+  bytes[SFL_BUF_ELL_VAL] = (size_t)(T * K) * es;
+  bytes[SFL_BUF_ELL_IDX] = (size_t)(T * K) * 2;
+  bytes[SFL_BUF_OVF_DENSE] = (size_t)(cap * f) * es;
+  return SFL_OK;
+}
+
+sfl_status_t sfl_pack_twell(const float* Z, int64_t T, int64_t f, sfl_dtype_t val_dtype, const sfl_twell_cfg_t* cfg,
+                            const sfl_twell_t* out, sfl_stats_t* stats, sfl_stream_t stream) {
+  if (!out || !dtype_ok(val_dtype) || T < 0) return SFL_E_ARG;
+  sfl_status_t st = check_cfg(cfg, f);
+  if (st != SFL_OK) return st;
+  if (T > 0 && !Z) return SFL_E_ARG;
+  st = check_twell(*out, false);
+  if (st != SFL_OK) return st;
+  if ((out->ell_val == nullptr) != (out->ell_idx == nullptr)) return SFL_E_ARG;
+  hipStream_t s = (hipStream_t)stream;
+  const int vb = val_dtype == SFL_BF16;
+  const int64_t cap = capacity_of(*cfg, T);
+  SFL_HIP(launch_stats_init(stats, s));
+  SFL_HIP(launch_pack_twell(Z, T, f, vb, cfg->tile_cols, cfg->tile_slots, out->val, out->idx, out->cnt, s));
+  SFL_HIP(launch_classify(T, f, vb, cfg->tile_cols, cfg->tile_slots, cfg->ell_width, out->val, out->idx, out->cnt,
+                          out->row_nnz, out->row_ovf, out->ell_val, out->ell_idx, stats, s));
+  SFL_HIP(launch_ovf_list(T, (int32_t)cap, out->row_ovf, out->ovf_rows, out->n_ovf, stats, s));
+  return SFL_OK;
+}
+
+sfl_status_t sfl_workspace_size(const void* args, int backward, size_t* bytes) {
+  if (!args || !bytes) return SFL_E_ARG;
+  if (backward == 1) return sfl::backward_workspace((const sfl_ffn_bwd_args_t*)args, bytes);
+  const sfl_ffn_args_t* a = (const sfl_ffn_args_t*)args;
+  sfl_status_t st = check_forward(a);
+  if (st != SFL_OK) return st;
+  if (backward == 2) {
+    *bytes = dense_ws_bytes(*a);
+    return SFL_OK;
+  }
+  if (backward != 0) return SFL_E_ARG;
+  *bytes = plan_forward(*a, nullptr).bytes;
+  return SFL_OK;
+}
+
+sfl_status_t sfl_up_projection(const sfl_ffn_args_t* a, float* Z, sfl_stream_t stream) {
+  sfl_status_t st = check_forward(a, false);
+  if (st != SFL_OK) return st;
+  if (a->T > 0 && !Z) return SFL_E_ARG;
+  if (a->gated ? !a->W_gate : !a->W_up) return SFL_E_ARG;
+  if (a->T == 0) return SFL_OK;
+  hipStream_t s = (hipStream_t)stream;
+  GemmParams g = gp_zero();
+  g.M = (int)a->T;
+  g.N = (int)a->f;
+  g.K = (int)a->d;
+  g.A = a->X;
+  g.lda = a->d;
+  int blay = LAY_RC;
+  if (a->gated)
+    set_weight_B(g, a->W_gate, nullptr, a->d, a->f, &blay);
+  else
+    set_weight_B(g, a->W_up, nullptr, a->d, a->f, &blay);
+  g.bias = a->bias_f;
+  g.shift = a->shift_t;
+  g.C = Z;
+  g.ldc = a->f;
+  SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_F32, g, s));
+  return SFL_OK;
+}
+
+sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
+  sfl_status_t st = check_forward(a);
+  if (st != SFL_OK) return st;
+  st = check_twell(a->twell, true);
+  if (st != SFL_OK) return st;
+  FwdPlan plan = plan_forward(*a, nullptr);
+  if (plan.bytes > 0 && (!a->workspace || a->workspace_bytes < plan.bytes)) return SFL_E_WORKSPACE;
+  plan = plan_forward(*a, a->workspace);
+  hipStream_t s = (hipStream_t)stream;
+  const Events ev{a->events, a->n_events};
+  const int64_t T = a->T, d = a->d, f = a->f;
+  const int64_t cap = capacity_of(a->cfg, T);
+  const int vb = a->dtype == SFL_BF16;
+  const sfl_twell_t& tw = a->twell;
+  void* ovf_dense = tw.ovf_dense ? tw.ovf_dense : plan.ovf_dense;
+  ev.record(0, s);
+  SFL_HIP(launch_stats_init(a->stats, s));
+  if (T == 0) {
+    SFL_HIP(launch_ovf_list(0, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s));
+    for (int i = 1; i < 5; ++i) ev.record(i, s);
+    return SFL_OK;
+  }
+  const void* Wp = a->gated ? a->W_gate : a->W_up;  // pattern-deciding projection
+
+  // 1. up (or gate) projection with the ReLU -> TwELL epilogue (Alg. 1)
+  {
+    GemmParams g = gp_zero();
+    g.M = (int)T;
+    g.N = (int)f;
+    g.K = (int)d;
+    g.A = a->X;
+    g.lda = d;
+    int blay;
+    set_weight_B(g, Wp, nullptr, d, f, &blay);
+    g.bias = a->bias_f;
+    g.shift = a->shift_t;
+    if (fused_twell(*a)) {
+      g.tw_val = tw.val;
+      g.tw_idx = tw.idx;
+      g.tw_cnt = tw.cnt;
+      g.tile_cols = a->cfg.tile_cols;
+      g.tile_slots = a->cfg.tile_slots;
+      g.n_tiles = (int)cdiv(f, a->cfg.tile_cols);
+      SFL_HIP(gemm_bf16(LAY_KC, blay, EPI_TWELL, g, s));
+    } else {
+      g.C = plan.Z;
+      g.ldc = f;
+      SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_F32, g, s));
+      SFL_HIP(launch_pack_twell(plan.Z, T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, s));
+    }
+  }
+  ev.record(1, s);
+  // 2. hybrid classification (Sec. 3.4)
+  SFL_HIP(launch_classify(T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, a->cfg.ell_width, tw.val, tw.idx, tw.cnt,
+                          tw.row_nnz, tw.row_ovf, tw.ell_val, tw.ell_idx, a->stats, s));
+  SFL_HIP(launch_ovf_list(T, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s));
+  ev.record(2, s);
+  // 3. sparse down projection of the ELL rows
+  if (a->gated) {
+    const void* WupT = a->W_upT;
+    if (!WupT) {
+      SFL_HIP(launch_transpose(a->W_up, plan.WupT, d, f, 2, s));
+      WupT = plan.WupT;
+    }
+    SFL_HIP(launch_gated_gather(vb, T, d, a->cfg.ell_width, tw.ell_val, tw.ell_idx, tw.row_nnz, tw.row_ovf, a->X,
+                                WupT, a->W_down, a->Y, s));
+  } else {
+    SFL_HIP(launch_gather_down(vb, T, d, a->cfg.ell_width, tw.ell_val, tw.ell_idx, tw.row_nnz, tw.row_ovf,
+                               a->W_down, a->Y, s));
+  }
+  ev.record(3, s);
+  // 4. dense-backup rows (Alg. 3, dense part): rows gathered through ovf_rows, count on device
+  if (cap > 0) {
+    GemmParams g = gp_zero();
+    g.M = (int)cap;
+    g.N = (int)f;
+    g.K = (int)d;
+    g.A = a->X;
+    g.lda = d;
+    g.a_rows = tw.ovf_rows;
+    g.m_count = tw.n_ovf;
+    g.count_cap = (int32_t)cap;
+    int blay;
+    set_weight_B(g, Wp, nullptr, d, f, &blay);
+    g.bias = a->bias_f;
+    g.shift = a->shift_t;
+    g.s_rows = tw.ovf_rows;
+    g.C = ovf_dense;
+    g.ldc = f;
+    SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_ACT_RELU, g, s));
+    if (a->gated) {
+      GemmParams u = g;
+      u.bias = nullptr;
+      u.shift = nullptr;
+      set_weight_B(u, a->W_up, nullptr, d, f, &blay);
+      SFL_HIP(gemm_bf16(LAY_KC, blay, EPI_MUL_ACT, u, s));
+    }
+    GemmParams y = gp_zero();
+    y.M = (int)cap;
+    y.N = (int)d;
+    y.K = (int)f;
+    y.A = ovf_dense;
+    y.lda = f;
+    y.m_count = tw.n_ovf;
+    y.count_cap = (int32_t)cap;
+    y.B = a->W_down;
+    y.ldb = d;
+    y.c_rows = tw.ovf_rows;
+    y.C = a->Y;
+    y.ldc = d;
+    SFL_HIP(run_gemm(a->dtype, LAY_KC, LAY_RC, EPI_ACT, y, s));
+    SFL_HIP(launch_ovf_l1(f, vb, ovf_dense, tw.n_ovf, (int32_t)cap, a->stats, s));
+  }
+  ev.record(4, s);
+  return SFL_OK;
+}
+
+sfl_status_t sfl_dense_ffn_baseline(const sfl_ffn_args_t* a, sfl_stream_t stream) {
+  sfl_status_t st = check_forward(a);
+  if (st != SFL_OK) return st;
+  const size_t need = dense_ws_bytes(*a);
+  if (need > 0 && (!a->workspace || a->workspace_bytes < need)) return SFL_E_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  const Events ev{a->events, a->n_events};
+  ev.record(0, s);
+  if (a->T == 0) return SFL_OK;
+  const int64_t T = a->T, d = a->d, f = a->f;
+  GemmParams g = gp_zero();
+  g.M = (int)T;
+  g.N = (int)f;
+  g.K = (int)d;
+  g.A = a->X;
+  g.lda = d;
+  int blay;
+  set_weight_B(g, a->gated ? a->W_gate : a->W_up, nullptr, d, f, &blay);
+  g.bias = a->bias_f;
+  g.shift = a->shift_t;
+  g.C = a->workspace;
+  g.ldc = f;
+  SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_ACT_RELU, g, s));
+  if (a->gated) {
+    GemmParams u = g;
+    u.bias = nullptr;
+    u.shift = nullptr;
+    set_weight_B(u, a->W_up, nullptr, d, f, &blay);
+    SFL_HIP(gemm_bf16(LAY_KC, blay, EPI_MUL_ACT, u, s));
+  }
+  ev.record(1, s);
+  GemmParams y = gp_zero();
+  y.M = (int)T;
+  y.N = (int)d;
+  y.K = (int)f;
+  y.A = a->workspace;
+  y.lda = f;
+  y.B = a->W_down;
+  y.ldb = d;
+  y.C = a->Y;
+  y.ldc = d;
+  SFL_HIP(run_gemm(a->dtype, LAY_KC, LAY_RC, EPI_ACT, y, s));
+  ev.record(2, s);
+  return SFL_OK;
+}
+
+sfl_status_t sfl_transpose(const void* in, void* out, int64_t rows, int64_t cols, int32_t elem_bytes,
+                           sfl_stream_t stream) {
+  if (rows < 0 || cols < 0 || (elem_bytes != 2 && elem_bytes != 4)) return SFL_E_ARG;
+  if (rows * cols > 0 && (!in || !out)) return SFL_E_ARG;
+  SFL_HIP(launch_transpose(in, out, rows, cols, elem_bytes, (hipStream_t)stream));
+  return SFL_OK;
+}
+
+sfl_status_t sfl_ffn_backward(const sfl_ffn_bwd_args_t* a, sfl_stream_t stream) {
+  return sfl::backward_run(a, (hipStream_t)stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,449 @@
+// Dense GEMMs of the FFN layer: bf16 on MFMA (v_mfma_f32_32x32x16_bf16) and fp32 on FMA.
+//
+// The bf16 kernel computes a 256x256 output tile per workgroup of 8 waves (2 along M x
+// 4 along N, 128x64 per wave = 4x2 MFMA 32x32 tiles). K advances in steps of 64 through
+// a double-buffered LDS stage; the next K step is fetched from global memory into
+// registers while the current one feeds the MFMAs. Each operand tile is kept in LDS
+// K-contiguous ([rows][64 + 8 pad] bf16), the layout both MFMA operands read 16 bytes
+// per lane from. Operands stored row-contiguous ([K][rows], e.g. W_up [d][f] as the B of
+// X W_up) are transposed on the way in: a lane fetches one 4-byte pair of adjacent rows
+// from 8 consecutive k, and byte permutes turn them into two 8-element k vectors.
+//
+// Epilogues (the `Epilogue` enum) include the TwELL one of Alg. 1: z = acc (+ bias, shift)
+// is staged through LDS 64 rows at a time, then each wave compacts 8 rows: 64 columns per
+// step, ballot of z > 0 and mbcnt give each active column its slot (ascending order).
+#include "common.h"
+#include "internal.h"
+
+namespace sfl {
+
+namespace {
+
+constexpr int BM = 256, BN = 256, BK = 64, LDK = BK + 8;
+constexpr int NTHR = 512;
+constexpr int WAVES_M = 2, WAVES_N = 4;
+constexpr int WTM = BM / WAVES_M;  // 128 rows per wave
+constexpr int WTN = BN / WAVES_N;  // 64 cols per wave
+constexpr int TM = WTM / 32, TN = WTN / 32;
+constexpr int LDS_STAGE = (BM + BN) * LDK;  // bf16 elements per stage
+
+__device__ __forceinline__ bool active_bits(float z) {
+  const int32_t b = __float_as_int(z);
+  return b > 0 && b <= 0x7f800000;
+}
+
+// ---- loaders -----------------------------------------------------------------------
+// K-contiguous source rows ([R][K], stride ld): ROWS x 64 tile in 16-byte chunks.
+template <int ROWS>
+struct LoadKC {
+  static constexpr int PER = ROWS * (BK / 8) / NTHR;
+  u32x4_t reg[PER];
+  const bf16_t* src[PER];  // row base pointer (nullptr = out of range)
+  __device__ void init(const bf16_t* base, int64_t ld, const int32_t* rows, int r0, int rlimit, int tid) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int c = tid + p * NTHR;
+      const int r = r0 + c / (BK / 8);
+      const int kc = (c % (BK / 8)) * 8;
+      const bf16_t* q = nullptr;
+      if (r < rlimit) {
+        const int64_t sr = rows ? (int64_t)rows[r] : (int64_t)r;
+        q = base + sr * ld + kc;
+      }
+      src[p] = q;
+    }
+  }
+  __device__ void load(int k0, int klimit, int tid) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int c = tid + p * NTHR;
+      const int kc = (c % (BK / 8)) * 8;
+      if (src[p] && k0 + kc < klimit)
+        reg[p] = *(const u32x4_t*)(src[p] + k0);
+      else
+        reg[p] = u32x4_t{0, 0, 0, 0};
+    }
+  }
+  __device__ void store(bf16_t* lds, int tid) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int c = tid + p * NTHR;
+      const int row = c / (BK / 8);
+      const int kc = (c % (BK / 8)) * 8;
+      *(u32x4_t*)(lds + row * LDK + kc) = reg[p];
+    }
+  }
+};
+
+// Row-contiguous source ([K][R], stride ld, R contiguous): job = (pair of adjacent rows,
+// group of 8 k). Optional gather on K: source row of k is krows[k].
+template <int ROWS>
+struct LoadRC {
+  static constexpr int PAIRS = ROWS / 2;
+  static constexpr int PER = PAIRS * (BK / 8) / NTHR;
+  uint32_t reg[PER][8];
+  const bf16_t* base;
+  int64_t ld;
+  const int32_t* krows;
+  int r0, rlimit;
+  __device__ void init(const bf16_t* b, int64_t ld_, const int32_t* kr, int r0_, int rlimit_) {
+    base = b;
+    ld = ld_;
+    krows = kr;
+    r0 = r0_;
+    rlimit = rlimit_;
+  }
+  __device__ void load(int k0, int klimit, int tid) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int j = tid + p * NTHR;
+      const int pp = j % PAIRS;
+      const int g = j / PAIRS;
+      const int r = r0 + 2 * pp;
+      const bool rv = r < rlimit;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int k = k0 + g * 8 + e;
+        uint32_t v = 0;
+        if (rv && k < klimit) {
+          const int64_t sk = krows ? (int64_t)krows[k] : (int64_t)k;
+          v = *(const uint32_t*)(base + sk * ld + r);
+        }
+        reg[p][e] = v;
+      }
+    }
+  }
+  __device__ void store(bf16_t* lds, int tid) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int j = tid + p * NTHR;
+      const int pp = j % PAIRS;
+      const int g = j / PAIRS;
+      u32x4_t lo, hi;
+      lo[0] = __builtin_amdgcn_perm(reg[p][1], reg[p][0], 0x05040100u);
+      lo[1] = __builtin_amdgcn_perm(reg[p][3], reg[p][2], 0x05040100u);
+      lo[2] = __builtin_amdgcn_perm(reg[p][5], reg[p][4], 0x05040100u);
+      lo[3] = __builtin_amdgcn_perm(reg[p][7], reg[p][6], 0x05040100u);
+      hi[0] = __builtin_amdgcn_perm(reg[p][1], reg[p][0], 0x07060302u);
+      hi[1] = __builtin_amdgcn_perm(reg[p][3], reg[p][2], 0x07060302u);
+      hi[2] = __builtin_amdgcn_perm(reg[p][5], reg[p][4], 0x07060302u);
+      hi[3] = __builtin_amdgcn_perm(reg[p][7], reg[p][6], 0x07060302u);
+      *(u32x4_t*)(lds + (2 * pp) * LDK + g * 8) = lo;
+      *(u32x4_t*)(lds + (2 * pp + 1) * LDK + g * 8) = hi;
+    }
+  }
+};
+
+template <int LAY, int ROWS> struct LoaderSel;
+template <int ROWS> struct LoaderSel<LAY_KC, ROWS> { typedef LoadKC<ROWS> type; };
+template <int ROWS> struct LoaderSel<LAY_RC, ROWS> { typedef LoadRC<ROWS> type; };
+
+template <int LAY, int ROWS>
+__device__ __forceinline__ void loader_init(typename LoaderSel<LAY, ROWS>::type& L, const bf16_t* base, int64_t ld,
+                                            const int32_t* rows, int r0, int rlimit, int tid) {
+  if constexpr (LAY == LAY_KC)
+    L.init(base, ld, rows, r0, rlimit, tid);
+  else
+    L.init(base, ld, rows, r0, rlimit);
+}
+
+// Output-tile order: consecutive workgroup ids are dispatched round-robin over the 8 XCDs;
+// remap so that each XCD gets a contiguous range of logical tiles, then walk that range
+// in groups of 8 tile-rows so neighbouring workgroups share A rows and B columns in L2.
+__device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int nwg = tiles_m * tiles_n;
+  int g = blockIdx.x;
+  if ((nwg & 7) == 0) g = (g & 7) * (nwg >> 3) + (g >> 3);
+  constexpr int GM = 8;
+  const int group = g / (GM * tiles_n);
+  const int first_m = group * GM;
+  const int gm = min(tiles_m - first_m, GM);
+  const int in_group = g - group * GM * tiles_n;
+  tm = first_m + in_group % gm;
+  tn = in_group / gm;
+}
+
+template <int ALAY, int BLAY, int EPI>
+__global__ __launch_bounds__(NTHR) void k_gemm_bf16(GemmParams p) {
+  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * LDS_STAGE];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+
+  const int tiles_m = (int)cdiv(p.M, BM), tiles_n = (int)cdiv(p.N, BN);
+  int tm, tn;
+  tile_coords(tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
+  if (m0 >= m_eff) return;
+  const int k_eff = p.k_count ? min(*p.k_count, p.count_cap) : p.K;
+  if (EPI == EPI_ACCUM_F32 && k_eff <= 0) return;
+
+  typename LoaderSel<ALAY, BM>::type la;
+  typename LoaderSel<BLAY, BN>::type lb;
+  loader_init<ALAY, BM>(la, (const bf16_t*)p.A, p.lda, p.a_rows, m0, m_eff, tid);
+  loader_init<BLAY, BN>(lb, (const bf16_t*)p.B, p.ldb, p.b_rows, n0, p.N, tid);
+
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int nk = (int)cdiv(k_eff, BK);
+  if (nk > 0) {
+    la.load(0, k_eff, tid);
+    lb.load(0, k_eff, tid);
+    la.store(smem, tid);
+    lb.store(smem + BM * LDK, tid);
+  }
+  __syncthreads();
+
+  const int arow = wm * WTM + (lane & 31);
+  const int brow = wn * WTN + (lane & 31);
+  const int koff = (lane >> 5) * 8;
+  for (int kt = 0; kt < nk; ++kt) {
+    const bf16_t* As = smem + (kt & 1) * LDS_STAGE;
+    const bf16_t* Bs = As + BM * LDK;
+    const bool more = kt + 1 < nk;
+    if (more) {
+      la.load((kt + 1) * BK, k_eff, tid);
+      lb.load((kt + 1) * BK, k_eff, tid);
+    }
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      bf16x8_t a[TM], b[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) a[i] = *(const bf16x8_t*)(As + (arow + i * 32) * LDK + ks * 16 + koff);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) b[j] = *(const bf16x8_t*)(Bs + (brow + j * 32) * LDK + ks * 16 + koff);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    if (more) {
+      bf16_t* An = smem + ((kt + 1) & 1) * LDS_STAGE;
+      la.store(An, tid);
+      lb.store(An + BM * LDK, tid);
+    }
+    __syncthreads();
+  }
+
+  // ---- epilogue -------------------------------------------------------------------
+  // Accumulator element (i, j, r) of this lane sits at tile row
+  //   wm*128 + i*32 + 8*(r/4) + 4*(lane/32) + r%4   and tile column   wn*64 + j*32 + lane%32.
+  if constexpr (EPI == EPI_TWELL) {
+    float* stage = (float*)smem;  // 64 rows x 256 fp32 = 64 KB
+    const int Tn = p.tile_cols, S = p.tile_slots, NT = p.n_tiles;
+    bf16_t* tval = (bf16_t*)p.tw_val;
+#pragma unroll
+    for (int pass = 0; pass < 4; ++pass) {
+      if (wm == pass / 2) {
+#pragma unroll
+        for (int ii = 0; ii < 2; ++ii) {
+          const int i = (pass % 2) * 2 + ii;
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            const int col = wn * WTN + j * 32 + (lane & 31);
+            const int gcol = n0 + col;
+            const float b = (p.bias && gcol < p.N) ? p.bias[gcol] : 0.f;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int row = i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);  // within the wave's 128
+              const int lrow = (wm * WTM + row) - pass * 64;
+              const int grow = m0 + wm * WTM + row;
+              float sh = 0.f;
+              if (p.shift && grow < m_eff) sh = p.shift[p.s_rows ? p.s_rows[grow] : grow];
+              stage[lrow * BN + col] = (acc[i][j][r] + b) + sh;
+            }
+          }
+        }
+      }
+      __syncthreads();
+      // compaction: wave w handles rows 8w .. 8w+7 of this pass
+      for (int rr = 0; rr < 8; ++rr) {
+        const int lrow = wave * 8 + rr;
+        const int grow = m0 + pass * 64 + lrow;
+        if (grow >= m_eff) break;
+        int running = 0;
+        const int64_t rbase = (int64_t)grow * NT * S;
+#pragma unroll
+        for (int ch = 0; ch < BN / 64; ++ch) {
+          const int col = ch * 64 + lane;
+          const int gcol = n0 + col;
+          const float z = stage[lrow * BN + col];
+          const bool act = gcol < p.N && active_bits(z);
+          const uint64_t m = ballot(act);
+          if ((ch * 64) % Tn == 0) running = 0;
+          const int jt = gcol / Tn;  // same for all lanes of this chunk
+          const int slot = running + mbcnt(m);
+          if (act && slot < S) {
+            tval[rbase + (int64_t)jt * S + slot] = f32_to_bf16(z);
+            p.tw_idx[rbase + (int64_t)jt * S + slot] = (uint16_t)gcol;
+          }
+          running += __popcll(m);
+          const int tile_start = (n0 + ch * 64) / Tn * Tn;
+          const bool tile_end = ((ch * 64 + 64) % Tn == 0) || ch == BN / 64 - 1;
+          if (tile_end && lane == 0 && tile_start < p.N) p.tw_cnt[(int64_t)grow * NT + jt] = running;
+        }
+      }
+      __syncthreads();
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + wm * WTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (row >= m_eff) continue;
+        const int64_t crow = p.c_rows ? (int64_t)p.c_rows[row] : (int64_t)row;
+        float sh = 0.f;
+        if ((EPI == EPI_F32 || EPI == EPI_ACT_RELU) && p.shift) sh = p.shift[p.s_rows ? p.s_rows[row] : row];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int col = n0 + wn * WTN + j * 32 + (lane & 31);
+          if (col >= p.N) continue;
+          float v = acc[i][j][r];
+          if (EPI == EPI_F32 || EPI == EPI_ACT_RELU) {
+            if (p.bias) v += p.bias[col];
+            v += sh;
+          }
+          if (EPI == EPI_F32) {
+            ((float*)p.C)[crow * p.ldc + col] = v;
+          } else if (EPI == EPI_ACT_RELU) {
+            ((bf16_t*)p.C)[crow * p.ldc + col] = active_bits(v) ? f32_to_bf16(v) : (bf16_t)0;
+          } else if (EPI == EPI_ACT) {
+            ((bf16_t*)p.C)[crow * p.ldc + col] = f32_to_bf16(v);
+          } else if (EPI == EPI_MASKGRAD) {
+            const bf16_t h = ((const bf16_t*)p.mask)[(int64_t)row * p.ldm + col];
+            const bool on = (int16_t)h > 0;  // stored activation > 0 (bf16 bits, positive non-zero)
+            ((bf16_t*)p.C)[crow * p.ldc + col] = on ? f32_to_bf16(v + p.lam) : (bf16_t)0;
+          } else if (EPI == EPI_MUL_ACT) {
+            bf16_t* c = (bf16_t*)p.C + crow * p.ldc + col;
+            *c = f32_to_bf16(bf16_to_f32(*c) * v);
+          } else if (EPI == EPI_ACCUM_F32) {
+            float* c = (float*)p.C + crow * p.ldc + col;
+            *c = *c + v;
+          }
+        }
+      }
+    }
+  }
+}
+
+template <int ALAY, int BLAY, int EPI>
+hipError_t launch_bf16(const GemmParams& p, hipStream_t s) {
+  const int tiles = (int)(cdiv(p.M, BM) * cdiv(p.N, BN));
+  if (tiles == 0) return hipSuccess;
+  hipLaunchKernelGGL((k_gemm_bf16<ALAY, BLAY, EPI>), dim3(tiles), dim3(NTHR), 0, s, p);
+  return hipGetLastError();
+}
+
+// ---- fp32 FMA GEMM (A [M][K] row-major, B [K][N] row-major), 64x64 tiles ------------------
+template <int EPI>
+__global__ __launch_bounds__(256) void k_gemm_f32(GemmParams p) {
+  __shared__ float As[16][64 + 1];
+  __shared__ float Bs[16][64 + 1];
+  const int tid = threadIdx.x;
+  const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
+  const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
+  if (m0 >= m_eff) return;
+  const float* A = (const float*)p.A;
+  const float* B = (const float*)p.B;
+  const int tr = tid / 16, tc = tid % 16;  // 16x16 threads, 4x4 outputs each
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < p.K; k0 += 16) {
+    for (int e = tid; e < 64 * 16; e += 256) {
+      const int r = e / 16, k = e % 16;
+      const int gm = m0 + r, gk = k0 + k;
+      float v = 0.f;
+      if (gm < m_eff && gk < p.K) {
+        const int64_t sr = p.a_rows ? p.a_rows[gm] : gm;
+        v = A[sr * p.lda + gk];
+      }
+      As[k][r] = v;
+      const int kk = e / 64, n = e % 64;
+      const int gk2 = k0 + kk, gn = n0 + n;
+      Bs[kk][n] = (gk2 < p.K && gn < p.N) ? B[(int64_t)gk2 * p.ldb + gn] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = As[k][tr * 4 + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = Bs[k][tc * 4 + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = m0 + tr * 4 + i;
+    if (row >= m_eff) continue;
+    const int64_t crow = p.c_rows ? (int64_t)p.c_rows[row] : (int64_t)row;
+    float sh = 0.f;
+    if (p.shift) sh = p.shift[p.s_rows ? p.s_rows[row] : row];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int col = n0 + tc * 4 + j;
+      if (col >= p.N) continue;
+      float v = acc[i][j];
+      if (EPI == EPI_F32 || EPI == EPI_ACT_RELU) {
+        if (p.bias) v += p.bias[col];
+        v += sh;
+      }
+      float* C = (float*)p.C;
+      if (EPI == EPI_F32) C[crow * p.ldc + col] = v;
+      else if (EPI == EPI_ACT_RELU) C[crow * p.ldc + col] = active_bits(v) ? v : 0.f;
+      else if (EPI == EPI_ACT) C[crow * p.ldc + col] = v;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t gemm_bf16(int alay, int blay, int epi, const GemmParams& p, hipStream_t s) {
+#define SFL_CASE(A_, B_, E_) \
+  if (alay == A_ && blay == B_ && epi == E_) return launch_bf16<A_, B_, E_>(p, s);
+  // forward: X W_up (B row-contiguous [d][f]) with TwELL / f32 / ReLU epilogues
+  SFL_CASE(LAY_KC, LAY_RC, EPI_TWELL)
+  SFL_CASE(LAY_KC, LAY_RC, EPI_F32)
+  SFL_CASE(LAY_KC, LAY_RC, EPI_ACT_RELU)
+  SFL_CASE(LAY_KC, LAY_RC, EPI_ACT)
+  SFL_CASE(LAY_KC, LAY_RC, EPI_MUL_ACT)
+  // pre-transposed weights ([f][d]) variants
+  SFL_CASE(LAY_KC, LAY_KC, EPI_TWELL)
+  SFL_CASE(LAY_KC, LAY_KC, EPI_F32)
+  SFL_CASE(LAY_KC, LAY_KC, EPI_ACT_RELU)
+  SFL_CASE(LAY_KC, LAY_KC, EPI_ACT)
+  SFL_CASE(LAY_KC, LAY_KC, EPI_MUL_ACT)
+  // backward dense-backup rows
+  SFL_CASE(LAY_KC, LAY_KC, EPI_MASKGRAD)
+  SFL_CASE(LAY_RC, LAY_RC, EPI_ACCUM_F32)
+#undef SFL_CASE
+  return hipErrorInvalidValue;
+}
+
+hipError_t gemm_f32(int epi, const GemmParams& p, hipStream_t s) {
+  if (p.M == 0 || p.N == 0) return hipSuccess;
+  const dim3 grid((unsigned)cdiv(p.N, 64), (unsigned)cdiv(p.M, 64));
+  switch (epi) {
+    case EPI_F32: hipLaunchKernelGGL(k_gemm_f32<EPI_F32>, grid, dim3(256), 0, s, p); break;
+    case EPI_ACT_RELU: hipLaunchKernelGGL(k_gemm_f32<EPI_ACT_RELU>, grid, dim3(256), 0, s, p); break;
+    case EPI_ACT: hipLaunchKernelGGL(k_gemm_f32<EPI_ACT>, grid, dim3(256), 0, s, p); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace sfl

@@ -1,0 +1,94 @@
+// Internal launch interfaces between the C ABI layer (api.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/sfl.h"
+
+namespace sfl {
+
+// ---------------------------------------------------------------- GEMM ----
+// C = A * B with bf16 operands on MFMA (fp32 accumulate), or fp32 operands on FMA.
+// Layouts: A is MK ([M][K], row stride lda) or KM ([K][M]); B is NK ([N][K]) or KN ([K][N]).
+enum Layout { LAY_KC = 0, LAY_RC = 1 };  // K-contiguous rows / row-contiguous (K-major)
+
+enum Epilogue {
+  EPI_TWELL = 0,       // z = acc + bias[n] + shift[srow]; ReLU -> TwELL (val, idx, cnt)
+  EPI_F32 = 1,         // C_f32[crow][n] = acc + bias[n] + shift[srow]
+  EPI_ACT_RELU = 2,    // C_act[crow][n] = ReLU(acc + bias[n] + shift[srow])
+  EPI_ACT = 3,         // C_act[crow][n] = acc
+  EPI_MASKGRAD = 4,    // C_act[crow][n] = mask[row][n] > 0 ? acc + lam : 0
+  EPI_ACCUM_F32 = 5,   // C_f32[crow][n] += acc
+  EPI_MUL_ACT = 6,     // C_act[crow][n] = C_act[crow][n] * acc (gated h = ReLU(g) * u)
+};
+
+struct GemmParams {
+  int M, N, K;
+  const void* A;
+  int64_t lda;
+  const void* B;
+  int64_t ldb;
+  const int32_t* a_rows;   // gather: MK -> A row index per m; RC -> source row per k
+  const int32_t* b_rows;   // gather: KC -> B row per n (unused); RC -> source row per k
+  const int32_t* m_count;  // device bound on M (min(*m_count, count_cap)), optional
+  const int32_t* k_count;  // device bound on K (min(*k_count, count_cap)), optional
+  int32_t count_cap;
+  // epilogue
+  const float* bias;       // [N] optional
+  const float* shift;      // [rows of the source] optional, indexed by srow
+  const int32_t* s_rows;   // srow = s_rows ? s_rows[m] : m
+  const int32_t* c_rows;   // crow = c_rows ? c_rows[m] : m
+  void* C;
+  int64_t ldc;
+  const void* mask;        // EPI_MASKGRAD: activation-dtype [M][N] (row stride ldm)
+  int64_t ldm;
+  float lam;
+  // TwELL outputs (EPI_TWELL)
+  void* tw_val;
+  uint16_t* tw_idx;
+  int32_t* tw_cnt;
+  int tile_cols, tile_slots, n_tiles;
+};
+
+// bf16 MFMA GEMM. Requirements: K % 8 == 0; RC layouts need even M/N extents and
+// 4-byte aligned rows; EPI_TWELL needs tile_cols in {64,128,256}.
+hipError_t gemm_bf16(int alay, int blay, int epi, const GemmParams& p, hipStream_t s);
+// fp32 FMA GEMM for the F32 dtype (A MK, B KN only; any sizes).
+hipError_t gemm_f32(int epi, const GemmParams& p, hipStream_t s);
+
+// ----------------------------------------------------------- TwELL ----
+hipError_t launch_pack_twell(const float* Z, int64_t T, int64_t f, int val_bf16, int tile_cols,
+                             int tile_slots, void* val, uint16_t* idx, int32_t* cnt, hipStream_t s);
+// Hybrid classification: row_nnz, row_ovf, optional ELL rows and stats partials.
+hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int tile_cols, int tile_slots,
+                           int ell_width, const void* val, const uint16_t* idx, const int32_t* cnt,
+                           int32_t* row_nnz, uint8_t* row_ovf, void* ell_val, uint16_t* ell_idx,
+                           sfl_stats_t* stats, hipStream_t s);
+// Ascending dense-backup row list + n_ovf + capacity flag (one workgroup).
+hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32_t* ovf_rows,
+                           int32_t* n_ovf, sfl_stats_t* stats, hipStream_t s);
+hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s);
+// l1 of the computed dense-backup rows (adds into stats->l1_sum).
+hipError_t launch_ovf_l1(int64_t f, int val_bf16, const void* ovf_dense, const int32_t* n_ovf,
+                         int32_t cap, sfl_stats_t* stats, hipStream_t s);
+
+// ---------------------------------------------------------- gathers ----
+// Y[t, :] = sum_e ell_val[t][e] * W[ell_idx[t][e], :] for rows with row_ovf[t] == 0.
+hipError_t launch_gather_down(int val_bf16, int64_t T, int64_t d, int ell_width, const void* ell_val,
+                              const uint16_t* ell_idx, const int32_t* row_nnz,
+                              const uint8_t* row_ovf, const void* W, void* Y, hipStream_t s);
+// Gated fused up-dot + down (Alg. 2) from the ELL rows of the gate pattern.
+hipError_t launch_gated_gather(int val_bf16, int64_t T, int64_t d, int ell_width, const void* ell_val,
+                               const uint16_t* ell_idx, const int32_t* row_nnz,
+                               const uint8_t* row_ovf, const void* X, const void* W_upT,
+                               const void* W_down, void* Y, hipStream_t s);
+
+// --------------------------------------------------------- backward ----
+// (declared in backward.h)
+
+hipError_t launch_transpose(const void* in, void* out, int64_t rows, int64_t cols, int elem_bytes,
+                            hipStream_t s);
+
+}  // namespace sfl

@@ -1,0 +1,260 @@
+// TwELL packing from memory, hybrid row classification and the dense-backup row list.
+//
+// TwELL (Sec. 3.2, Alg. 1): per row t and column tile j of width T_n, the active
+// columns (z > 0) are stored left-aligned in S slots, in ascending column order,
+// with the true count in cnt[t][j]. The hybrid format (Sec. 3.4) sends a row to
+// the dense backup when its total count exceeds the ELL width K or one of its
+// tiles overflowed (cnt > S); the other rows get a compact ELL row.
+#include "common.h"
+#include "internal.h"
+
+namespace sfl {
+
+// Active iff z > 0 in IEEE order, decided on the bit pattern so that the result does
+// not depend on the denormal mode: positive finite values, positive subnormals and
+// +inf are active; +-0 and NaN are not.
+__device__ __forceinline__ bool is_active(float z) {
+  const int32_t b = __float_as_int(z);
+  return b > 0 && b <= 0x7f800000;
+}
+
+// One wave per (row, tile): 64 columns per step, ballot + mbcnt give each active lane its
+// slot (running count + active lanes below it), so slots follow ascending column order.
+template <typename V>
+__global__ __launch_bounds__(256) void k_pack_twell(const float* __restrict__ Z, int64_t T, int64_t f,
+                                                    int Tn, int S, int NT, V* __restrict__ val,
+                                                    uint16_t* __restrict__ idx, int32_t* __restrict__ cnt) {
+  const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (w >= T * NT) return;
+  const int l = threadIdx.x & 63;
+  const int64_t t = w / NT;
+  const int j = (int)(w - t * NT);
+  const int64_t c0 = (int64_t)j * Tn;
+  const int64_t c1 = c0 + Tn < f ? c0 + Tn : f;
+  const float* zr = Z + t * f;
+  const int64_t base = t * (int64_t)NT * S + (int64_t)j * S;
+  int running = 0;
+  for (int64_t c = c0; c < c1; c += 64) {
+    const int64_t col = c + l;
+    const float z = col < c1 ? zr[col] : 0.f;
+    const bool act = col < c1 && is_active(z);
+    const uint64_t m = ballot(act);
+    const int slot = running + mbcnt(m);
+    if (act && slot < S) {
+      val[base + slot] = VT<V>::cvt(z);
+      idx[base + slot] = (uint16_t)col;
+    }
+    running += __popcll(m);
+  }
+  if (l == 0) cnt[t * NT + j] = running;
+}
+
+hipError_t launch_pack_twell(const float* Z, int64_t T, int64_t f, int val_bf16, int Tn, int S,
+                             void* val, uint16_t* idx, int32_t* cnt, hipStream_t s) {
+  const int NT = (int)cdiv(f, Tn);
+  const int64_t waves = T * NT;
+  if (waves == 0) return hipSuccess;
+  const dim3 grid((unsigned)cdiv(waves, 4));
+  if (val_bf16)
+    hipLaunchKernelGGL(k_pack_twell<bf16_t>, grid, dim3(256), 0, s, Z, T, f, Tn, S, NT, (bf16_t*)val, idx, cnt);
+  else
+    hipLaunchKernelGGL(k_pack_twell<float>, grid, dim3(256), 0, s, Z, T, f, Tn, S, NT, (float*)val, idx, cnt);
+  return hipGetLastError();
+}
+
+// One wave per row. Pass 1: tile counts 64 at a time, prefix sums give each tile's
+// offset in the ELL row and the row total. Pass 2 (sparse rows with an ELL buffer):
+// copy each tile's slots to its offset. Stats use integer atomics (exact) and a
+// float64 atomic for the L1 sum of the stored values.
+template <typename V>
+__global__ __launch_bounds__(256) void k_classify(int64_t T, int NT, int S, int K, const V* __restrict__ val,
+                                                  const uint16_t* __restrict__ idx, const int32_t* __restrict__ cnt,
+                                                  int32_t* __restrict__ row_nnz, uint8_t* __restrict__ row_ovf,
+                                                  V* __restrict__ ell_val, uint16_t* __restrict__ ell_idx,
+                                                  sfl_stats_t* __restrict__ stats) {
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const int l = threadIdx.x & 63;
+  const int32_t* crow = cnt + t * NT;
+  int64_t total = 0;
+  int tile_over = 0;
+  for (int j0 = 0; j0 < NT; j0 += 64) {
+    const int c = (j0 + l < NT) ? crow[j0 + l] : 0;
+    total += wave_sum<int>(c);
+    tile_over += __popcll(ballot(c > S));
+  }
+  const bool ovf = total > K || tile_over > 0;
+  if (l == 0) {
+    row_nnz[t] = (int32_t)total;
+    row_ovf[t] = ovf ? 1 : 0;
+  }
+  float l1 = 0.f;
+  if (!ovf) {
+    const V* vrow = val + t * (int64_t)NT * S;
+    const uint16_t* irow = idx + t * (int64_t)NT * S;
+    int offset = 0;
+    for (int j0 = 0; j0 < NT; j0 += 64) {
+      const int c = (j0 + l < NT) ? crow[j0 + l] : 0;
+      const int incl = wave_incl_scan(c);
+      const int excl = incl - c;
+      const int nt_here = (NT - j0) < 64 ? (NT - j0) : 64;
+      for (int jj = 0; jj < nt_here; ++jj) {
+        const int cj = readlane_i(c, jj);
+        if (cj == 0) continue;
+        const int pos = offset + readlane_i(excl, jj);
+        const int64_t src = (int64_t)(j0 + jj) * S;
+        for (int s0 = 0; s0 < cj; s0 += 64) {
+          const int sidx = s0 + l;
+          if (sidx < cj) {
+            const V v = vrow[src + sidx];
+            l1 += VT<V>::load(&v, 0);
+            if (ell_val) {
+              ell_val[t * (int64_t)K + pos + sidx] = v;
+              ell_idx[t * (int64_t)K + pos + sidx] = irow[src + sidx];
+            }
+          }
+        }
+      }
+      offset += readlane_i(incl, 63);
+    }
+  }
+  if (stats) {
+    l1 = wave_sum<float>(l1);
+    if (l == 0) {
+      atomicAdd((unsigned long long*)&stats->total_nnz, (unsigned long long)total);
+      if (tile_over) atomicAdd((unsigned long long*)&stats->n_tile_ovf, (unsigned long long)tile_over);
+      if (l1 != 0.f) atomicAdd(&stats->l1_sum, (double)l1);
+    }
+  }
+}
+
+hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int Tn, int S, int K, const void* val,
+                           const uint16_t* idx, const int32_t* cnt, int32_t* row_nnz, uint8_t* row_ovf,
+                           void* ell_val, uint16_t* ell_idx, sfl_stats_t* stats, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  const int NT = (int)cdiv(f, Tn);
+  const dim3 grid((unsigned)cdiv(T, 4));
+  if (val_bf16)
+    hipLaunchKernelGGL(k_classify<bf16_t>, grid, dim3(256), 0, s, T, NT, S, K, (const bf16_t*)val, idx, cnt,
+                       row_nnz, row_ovf, (bf16_t*)ell_val, ell_idx, stats);
+  else
+    hipLaunchKernelGGL(k_classify<float>, grid, dim3(256), 0, s, T, NT, S, K, (const float*)val, idx, cnt,
+                       row_nnz, row_ovf, (float*)ell_val, ell_idx, stats);
+  return hipGetLastError();
+}
+
+__global__ void k_stats_init(sfl_stats_t* stats) {
+  if (threadIdx.x == 0) {
+    stats->total_nnz = 0;
+    stats->n_ovf_rows = 0;
+    stats->n_tile_ovf = 0;
+    stats->l1_sum = 0.0;
+    stats->capacity_exceeded = 0;
+    stats->reserved = 0;
+  }
+}
+
+hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s) {
+  if (!stats) return hipSuccess;
+  hipLaunchKernelGGL(k_stats_init, dim3(1), dim3(64), 0, s, stats);
+  return hipGetLastError();
+}
+
+// One workgroup of 1024 threads scans the row flags 1024 at a time (wave scans +
+// a scan of the 16 wave totals), so the list is in ascending row order.
+__global__ __launch_bounds__(1024) void k_ovf_list(int64_t T, int32_t cap, const uint8_t* __restrict__ row_ovf,
+                                                   int32_t* __restrict__ ovf_rows, int32_t* __restrict__ n_ovf,
+                                                   sfl_stats_t* __restrict__ stats) {
+  __shared__ int wsum[16];
+  const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
+  int64_t base = 0;
+  for (int64_t r0 = 0; r0 < T; r0 += 1024) {
+    const int64_t t = r0 + tid;
+    const int flag = (t < T && row_ovf[t]) ? 1 : 0;
+    const int incl = wave_incl_scan(flag);
+    if (l == 63) wsum[w] = incl;
+    __syncthreads();
+    int before = 0, all = 0;
+    for (int i = 0; i < 16; ++i) {
+      const int v = wsum[i];
+      before += (i < w) ? v : 0;
+      all += v;
+    }
+    const int64_t pos = base + before + incl - flag;
+    if (flag && pos < cap) ovf_rows[pos] = (int32_t)t;
+    base += all;
+    __syncthreads();
+  }
+  if (tid == 0) {
+    *n_ovf = (int32_t)base;
+    if (stats) {
+      stats->n_ovf_rows = base;
+      stats->capacity_exceeded = base > cap ? 1 : 0;
+    }
+  }
+}
+
+hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32_t* ovf_rows, int32_t* n_ovf,
+                           sfl_stats_t* stats, hipStream_t s) {
+  hipLaunchKernelGGL(k_ovf_list, dim3(1), dim3(1024), 0, s, T, cap, row_ovf, ovf_rows, n_ovf, stats);
+  return hipGetLastError();
+}
+
+// Sum of the dense-backup rows that were computed (min(n_ovf, cap) rows of ovf_dense).
+template <typename V>
+__global__ __launch_bounds__(256) void k_ovf_l1(int64_t f, const V* __restrict__ dense, const int32_t* n_ovf,
+                                                int32_t cap, sfl_stats_t* stats) {
+  const int n = min(*n_ovf, cap);
+  const int64_t row = blockIdx.x;
+  if (row >= n) return;
+  float s = 0.f;
+  for (int64_t c = threadIdx.x; c < f; c += 256) s += VT<V>::load(dense, row * f + c);
+  s = wave_sum<float>(s);
+  __shared__ float part[4];
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const float tot = part[0] + part[1] + part[2] + part[3];
+    if (tot != 0.f) atomicAdd(&stats->l1_sum, (double)tot);
+  }
+}
+
+hipError_t launch_ovf_l1(int64_t f, int val_bf16, const void* dense, const int32_t* n_ovf, int32_t cap,
+                         sfl_stats_t* stats, hipStream_t s) {
+  if (!stats || cap == 0) return hipSuccess;
+  if (val_bf16)
+    hipLaunchKernelGGL(k_ovf_l1<bf16_t>, dim3(cap), dim3(256), 0, s, f, (const bf16_t*)dense, n_ovf, cap, stats);
+  else
+    hipLaunchKernelGGL(k_ovf_l1<float>, dim3(cap), dim3(256), 0, s, f, (const float*)dense, n_ovf, cap, stats);
+  return hipGetLastError();
+}
+
+// Tiled transpose through LDS (64x64 tiles, 256 threads).
+template <typename E>
+__global__ __launch_bounds__(256) void k_transpose(const E* __restrict__ in, E* __restrict__ out, int64_t rows,
+                                                   int64_t cols) {
+  __shared__ E tile[64][65];
+  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += 4) {
+    const int64_t r = r0 + i, c = c0 + tx;
+    if (r < rows && c < cols) tile[i][tx] = in[r * cols + c];
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const int64_t c = c0 + i, r = r0 + tx;
+    if (r < rows && c < cols) out[c * rows + r] = tile[tx][i];
+  }
+}
+
+hipError_t launch_transpose(const void* in, void* out, int64_t rows, int64_t cols, int eb, hipStream_t s) {
+  if (rows == 0 || cols == 0) return hipSuccess;
+  const dim3 grid((unsigned)cdiv(cols, 64), (unsigned)cdiv(rows, 64));
+  if (eb == 2)
+    hipLaunchKernelGGL(k_transpose<uint16_t>, grid, dim3(256), 0, s, (const uint16_t*)in, (uint16_t*)out, rows, cols);
+  else
+    hipLaunchKernelGGL(k_transpose<uint32_t>, grid, dim3(256), 0, s, (const uint32_t*)in, (uint32_t*)out, rows, cols);
+  return hipGetLastError();
+}
+
+}  // namespace sfl

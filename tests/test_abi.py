@@ -1,0 +1,113 @@
+"""C ABI checks that need no GPU: the library loads, exports every entry point that
+include/sfl.h declares, sizes buffers by the documented formulas and rejects bad
+arguments synchronously (validation happens before any launch)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2603_23198_amd import binding as b
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    hdr = open(os.path.join(ROOT, "include", "sfl.h")).read()
+    hdr = re.sub(r"/\*.*?\*/", "", hdr, flags=re.S)
+    return sorted(set(re.findall(r"\b(sfl_[a-z0-9_]+)\s*\(", hdr)))
+
+
+def test_every_declared_symbol_is_exported():
+    lib = ctypes.CDLL(b.LIB_PATH)
+    names = declared_functions()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(b.EXPORTED)
+
+
+def test_version_and_status_strings():
+    assert "gfx950" in b.sfl_version()
+    for code in (0, -1, -2, -3, -4):
+        assert b.sfl_status_string(code).startswith("SFL_")
+
+
+def test_buffer_sizes_formula():
+    T, f = 300, 1000
+    cfg = b.make_cfg(tile_cols=256, tile_slots=32, ell_width=64, ovf_capacity=40)
+    s = dict(zip(b.BUF_NAMES, b.sfl_twell_buffer_sizes(T, f, "bf16", cfg)))
+    NT = 4
+    assert s["val"] == T * NT * 32 * 2 and s["idx"] == T * NT * 32 * 2
+    assert s["cnt"] == T * NT * 4 and s["row_nnz"] == T * 4 and s["row_ovf"] == T
+    assert s["ovf_rows"] == 40 * 4 and s["n_ovf"] == 4
+    assert s["ell_val"] == T * 64 * 2 and s["ell_idx"] == T * 64 * 2
+    assert s["ovf_dense"] == 40 * f * 2
+    s32 = dict(zip(b.BUF_NAMES, b.sfl_twell_buffer_sizes(T, f, "f32", b.make_cfg(3, 2, 5))))
+    assert s32["val"] == T * 334 * 2 * 4 and s32["ovf_rows"] == T * 4
+
+
+@pytest.mark.parametrize("cfg", [(0, 1, 1), (4, 5, 1), (4, 0, 1), (4, 2, -1)])
+def test_bad_cfg_rejected(cfg):
+    with pytest.raises(b.SflError) as e:
+        b.sfl_twell_buffer_sizes(10, 100, "f32", b.make_cfg(*cfg))
+    assert e.value.code == b.SFL_E_ARG
+
+
+def test_index_width_limit():
+    with pytest.raises(b.SflError):
+        b.sfl_twell_buffer_sizes(10, 65536, "bf16", b.make_cfg())
+
+
+def _fake_args(dtype, T, d, f, gated=False, **kw):
+    a = b.FfnArgs()
+    a.dtype = dtype
+    a.gated = 1 if gated else 0
+    a.T, a.d, a.f = T, d, f
+    a.X = a.Y = a.W_up = a.W_down = 0x1000
+    if gated:
+        a.W_gate = 0x1000
+    a.cfg = b.make_cfg(**kw)
+    return a
+
+
+def test_workspace_sizes():
+    a = _fake_args(b.SFL_BF16, 128, 256, 1024, ell_width=32)
+    ws = b.sfl_workspace_size(a, 0)
+    assert ws == 128 * 1024 * 2  # dense-backup rows live in the workspace when not given
+    a.twell.ovf_dense = 0x2000
+    assert b.sfl_workspace_size(a, 0) == 0  # fused TwELL epilogue: no scratch
+    a32 = _fake_args(b.SFL_F32, 64, 256, 1024, ell_width=32)
+    a32.twell.ovf_dense = 0x2000
+    assert b.sfl_workspace_size(a32, 0) == 64 * 1024 * 4  # fp32: pre-activations staged
+    assert b.sfl_workspace_size(a, 2) == 128 * 1024 * 2   # dense baseline: H
+
+
+def test_unsupported_shapes_and_missing_pointers():
+    a = _fake_args(b.SFL_BF16, 128, 200, 1024)
+    with pytest.raises(b.SflError) as e:
+        b.sfl_workspace_size(a, 0)
+    assert e.value.code == b.SFL_E_UNSUPPORTED
+    a = _fake_args(b.SFL_F32, 128, 256, 1024, gated=True)
+    with pytest.raises(b.SflError) as e:
+        b.sfl_workspace_size(a, 0)
+    assert e.value.code == b.SFL_E_UNSUPPORTED
+    a = _fake_args(b.SFL_BF16, 128, 256, 1024)
+    a.X = None
+    with pytest.raises(b.SflError) as e:
+        b.sfl_workspace_size(a, 0)
+    assert e.value.code == b.SFL_E_ARG
+
+
+def test_forward_validates_before_launch():
+    a = _fake_args(b.SFL_BF16, 128, 256, 1024)
+    # twell buffers missing -> argument error, no launch
+    with pytest.raises(b.SflError) as e:
+        b.sfl_ffn_forward(a, stream=0)
+    assert e.value.code == b.SFL_E_ARG
+    for n in b.BUF_NAMES:
+        setattr(a.twell, n, 0x3000)
+    a.twell.ovf_dense = None
+    with pytest.raises(b.SflError) as e:   # workspace needed for the dense-backup rows
+        b.sfl_ffn_forward(a, stream=0)
+    assert e.value.code == b.SFL_E_WORKSPACE

@@ -1,0 +1,224 @@
+"""sfl_ffn_forward / sfl_dense_ffn_baseline on the GPU against the fp64 oracle.
+
+Bars: relative L2 <= 2e-2 for bf16 and <= 1e-5 for fp32 (against the oracle's dense
+definition on the same stored inputs); the fused TwELL output is bit-identical to
+sfl_pack_twell applied to the float32 pre-activations of the same GEMM main loop; the
+pattern matches the oracle's except where |z| is within rounding of 0."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as wl
+from oracle import ffn, twell
+from tests.gpu_util import assert_twell_equal, dev, host_bits, rel_l2, to_f64, twell_views
+
+pytestmark = pytest.mark.gpu
+
+b = pytest.importorskip("paper_2603_23198_amd.binding")
+
+
+def run_forward(w, rows_check=None, use_wupt=False, dense=False):
+    X, Wu, Wd = dev(w.X), dev(w.W_up), dev(w.W_down)
+    Wg = dev(w.W_gate) if w.gated else None
+    cfg = b.make_cfg(**w.cfg)
+    dt = "bf16" if w.dtype == "bf16" else "f32"
+    bufs = b.alloc_twell(w.T, w.f, dt, cfg)
+    Y = torch.full((w.T, w.d), float("nan"), dtype=X.dtype, device="cuda")
+    stats = b.alloc_stats()
+    WupT = None
+    if use_wupt:
+        WupT = torch.empty((w.f, w.d), dtype=X.dtype, device="cuda")
+        b.sfl_transpose(Wu, WupT)
+    args = b.ffn_args(X, Wu, Wd, cfg, Y=Y, bufs=bufs, W_gate=Wg, W_upT=WupT, bias_f=dev(w.bias_f),
+                      shift_t=dev(w.shift_t), stats=stats)
+    ws_bytes = b.sfl_workspace_size(args, 2 if dense else 0)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device="cuda")
+    args = b.ffn_args(X, Wu, Wd, cfg, Y=Y, bufs=bufs, W_gate=Wg, W_upT=WupT, bias_f=dev(w.bias_f),
+                      shift_t=dev(w.shift_t), stats=stats, workspace=ws)
+    (b.sfl_dense_ffn_baseline if dense else b.sfl_ffn_forward)(args)
+    torch.cuda.synchronize()
+    return Y, bufs, stats, cfg
+
+
+def oracle_rows(w, rows):
+    X = w.as_f64(w.X)[rows]
+    sh = None if w.shift_t is None else w.shift_t[rows]
+    if w.gated:
+        Y, G, U, H = ffn.ffn_gated_dense(X, w.as_f64(w.W_gate), w.as_f64(w.W_up), w.as_f64(w.W_down), w.bias_f, sh)
+        return Y, G
+    Y, Z, H = ffn.ffn_dense(X, w.as_f64(w.W_up), w.as_f64(w.W_down), w.bias_f, sh)
+    return Y, Z
+
+
+def check_pattern(got, Zref, rows, f, Tn, S):
+    """GPU pattern vs the oracle's z > 0, allowing flips only where |z| <= 1e-4 * rms(z)."""
+    tol = 1e-4 * np.sqrt(np.mean(Zref ** 2))
+    NT = -(-f // Tn)
+    for i, t in enumerate(rows):
+        want = Zref[i] > 0
+        ambiguous = np.abs(Zref[i]) <= tol
+        cnt = got["cnt"][t]
+        gpu = np.zeros(f, dtype=bool)
+        for j in range(NT):
+            c = min(int(cnt[j]), S)
+            gpu[got["idx"][t, j * S:j * S + c].astype(np.int64)] = True
+        full = cnt <= S
+        for j in np.nonzero(full)[0]:
+            sl = slice(j * Tn, min((j + 1) * Tn, f))
+            bad = (gpu[sl] != want[sl]) & ~ambiguous[sl]
+            assert not bad.any(), (t, j, np.nonzero(bad)[0])
+
+
+def sample_rows(T, n, seed, extra=()):
+    r = np.random.default_rng(seed)
+    rows = r.choice(T, size=min(n, T), replace=False)
+    return np.unique(np.concatenate([rows, np.asarray(extra, dtype=np.int64)])).astype(np.int64)
+
+
+def test_c1_fp32_full():
+    w = wl.c1_small_fp32()
+    Y, bufs, stats, cfg = run_forward(w)
+    Yref, Z = oracle_rows(w, np.arange(w.T))
+    assert rel_l2(to_f64(Y), Yref) <= 1e-5
+    got = twell_views(bufs, w.T, w.f, cfg)
+    check_pattern(got, Z, np.arange(w.T), w.f, cfg.tile_cols, cfg.tile_slots)
+    # all rows computed exactly once: rows with no active unit are exactly zero
+    zero_rows = (Z > 0).sum(1) == 0
+    assert (to_f64(Y)[zero_rows] == 0).all()
+
+
+def test_c2_lognormal_overflow_full():
+    w = wl.c2_lognormal()
+    Y, bufs, stats, cfg = run_forward(w)
+    got = twell_views(bufs, w.T, w.f, cfg)
+    st = b.read_stats(stats)
+    n_ovf = got["n_ovf"]
+    assert 0.08 * w.T < n_ovf < 0.3 * w.T, n_ovf   # the dense-backup path is exercised
+    assert st["n_ovf_rows"] == n_ovf and st["capacity_exceeded"] == 0
+    rows = np.arange(w.T)
+    Yref, Z = oracle_rows(w, rows)
+    assert rel_l2(to_f64(Y), Yref) <= 2e-2
+    ovf = np.nonzero(got["row_ovf"])[0]
+    assert rel_l2(to_f64(Y)[ovf], Yref[ovf]) <= 2e-2
+    np.testing.assert_array_equal(got["ovf_rows"][:n_ovf], ovf)
+    prow = sample_rows(w.T, 64, 1)
+    check_pattern(got, Z[prow], prow, w.f, cfg.tile_cols, cfg.tile_slots)
+
+
+@pytest.mark.parametrize("sparsity", [0.9, 0.95, 0.99, 0.999])
+def test_c4_sweep_sampled(sparsity):
+    w = wl.c4_sweep(sparsity)
+    Y, bufs, stats, cfg = run_forward(w)
+    got = twell_views(bufs, w.T, w.f, cfg)
+    ovf = np.nonzero(got["row_ovf"])[0]
+    rows = sample_rows(w.T, 192, 2, extra=ovf[:64])
+    Yref, Z = oracle_rows(w, rows)
+    assert rel_l2(to_f64(Y)[rows], Yref) <= 2e-2
+    for i, t in enumerate(rows):
+        assert rel_l2(to_f64(Y)[t], Yref[i]) <= 2e-2
+    check_pattern(got, Z, rows[:48], w.f, cfg.tile_cols, cfg.tile_slots)
+    realised = 1 - got["row_nnz"].sum() / (w.T * w.f)
+    assert abs(realised - sparsity) < 0.1 * (1 - sparsity) + 1e-4
+
+
+def test_fused_twell_equals_pack_of_same_mainloop():
+    w = wl.make_ffn("fused-vs-pack", "bf16", 777, 512, 2048, seed=7, sparsity=0.97, ell_width=128)
+    Y, bufs, stats, cfg = run_forward(w)
+    X, Wu = dev(w.X), dev(w.W_up)
+    Z = torch.empty((w.T, w.f), dtype=torch.float32, device="cuda")
+    args = b.ffn_args(X, Wu, dev(w.W_down), cfg, shift_t=dev(w.shift_t))
+    b.sfl_up_projection(args, Z)
+    bufs2 = b.alloc_twell(w.T, w.f, "bf16", cfg)
+    b.sfl_pack_twell(Z, "bf16", cfg, bufs2)
+    torch.cuda.synchronize()
+    g1 = twell_views(bufs, w.T, w.f, cfg)
+    tw = twell.extract_twell(Z.cpu().numpy(), cfg.tile_cols, cfg.tile_slots, "bf16")
+    hy = twell.classify(tw, cfg.ell_width)
+    assert_twell_equal(g1, tw, hy)                       # fused epilogue == oracle on the same z
+    assert_twell_equal(twell_views(bufs2, w.T, w.f, cfg), tw, hy)
+    # the float32 pre-activations themselves match the fp64 oracle closely
+    Zref = ffn.preactivation(w.as_f64(w.X), w.as_f64(w.W_up), None, w.shift_t)
+    assert rel_l2(Z.cpu().numpy(), Zref) < 1e-5
+
+
+@pytest.mark.parametrize("T,d,f,Tn,S,K", [(300, 256, 320, 256, 32, 40), (65, 128, 1024, 64, 8, 24),
+                                            (1, 512, 2048, 128, 16, 64), (513, 64, 192, 64, 64, 192)])
+def test_ragged_shapes_bf16(T, d, f, Tn, S, K):
+    w = wl.make_ffn("ragged", "bf16", T, d, f, seed=T + f, sparsity=0.9, tile_cols=Tn, tile_slots=S, ell_width=K)
+    Y, bufs, stats, cfg = run_forward(w)
+    Yref, Z = oracle_rows(w, np.arange(T))
+    assert rel_l2(to_f64(Y), Yref) <= 2e-2
+    check_pattern(twell_views(bufs, T, f, cfg), Z, np.arange(min(T, 64)), f, Tn, S)
+
+
+def test_all_active_and_all_inactive_rows():
+    w = wl.make_ffn("extremes", "bf16", 96, 256, 512, seed=3, sparsity=0.95, ell_width=32)
+    w.shift_t[:8] = 100.0     # every unit active -> dense-backup rows
+    w.shift_t[8:16] = -100.0  # no unit active -> exact zeros
+    Y, bufs, stats, cfg = run_forward(w)
+    Yref, Z = oracle_rows(w, np.arange(w.T))
+    got = twell_views(bufs, w.T, w.f, cfg)
+    assert got["row_ovf"][:8].all() and (got["row_nnz"][:8] == w.f).all()
+    assert (to_f64(Y)[8:16] == 0).all()
+    assert rel_l2(to_f64(Y), Yref) <= 2e-2
+
+
+def test_capacity_exceeded_flag_then_enough_capacity():
+    w = wl.make_ffn("capacity", "bf16", 128, 256, 512, seed=4, sparsity=0.95, ell_width=16)
+    w.shift_t[::4] = 100.0    # 32 dense-backup rows
+    w.cfg["ovf_capacity"] = 10
+    Y, bufs, stats, cfg = run_forward(w)
+    st = b.read_stats(stats)
+    assert st["capacity_exceeded"] == 1 and st["n_ovf_rows"] >= 32
+    got = twell_views(bufs, w.T, w.f, cfg)
+    Yref, _ = oracle_rows(w, np.arange(w.T))
+    done = got["ovf_rows"][:10]
+    assert rel_l2(to_f64(Y)[done], Yref[done]) <= 2e-2
+    sparse = np.nonzero(got["row_ovf"] == 0)[0]
+    assert rel_l2(to_f64(Y)[sparse], Yref[sparse]) <= 2e-2
+    w.cfg["ovf_capacity"] = 0
+    Y2, _, stats2, _ = run_forward(w)
+    assert b.read_stats(stats2)["capacity_exceeded"] == 0
+    assert rel_l2(to_f64(Y2), Yref) <= 2e-2
+
+
+def test_dense_baseline_matches_oracle():
+    w = wl.make_ffn("dense", "bf16", 1000, 512, 2048, seed=9, sparsity=0.95)
+    Y, _, _, _ = run_forward(w, dense=True)
+    Yref, _ = oracle_rows(w, np.arange(w.T))
+    assert rel_l2(to_f64(Y), Yref) <= 2e-2
+    w32 = wl.c1_small_fp32()
+    Y32, _, _, _ = run_forward(w32, dense=True)
+    Yref32, _ = oracle_rows(w32, np.arange(w32.T))
+    assert rel_l2(to_f64(Y32), Yref32) <= 1e-5
+
+
+@pytest.mark.parametrize("T", [32, 700])
+def test_gated_forward(T):
+    w = wl.c3_gated(T=T, d=1024, f=4096)
+    Y, bufs, stats, cfg = run_forward(w)
+    Yref, G = oracle_rows(w, np.arange(T))
+    assert rel_l2(to_f64(Y), Yref) <= 2e-2
+    Yd, _, _, _ = run_forward(w, dense=True)
+    assert rel_l2(to_f64(Yd), Yref) <= 2e-2
+    # with a caller-provided W_up^T the result is identical
+    Y2, _, _, _ = run_forward(w, use_wupt=True)
+    assert torch.equal(Y.view(torch.int16), Y2.view(torch.int16))
+
+
+def test_gated_c3_sampled():
+    w = wl.c3_gated()
+    Y, bufs, stats, cfg = run_forward(w)
+    got = twell_views(bufs, w.T, w.f, cfg)
+    rows = sample_rows(w.T, 128, 3, extra=np.nonzero(got["row_ovf"])[0][:32])
+    Yref, _ = oracle_rows(w, rows)
+    assert rel_l2(to_f64(Y)[rows], Yref) <= 2e-2
+
+
+def test_forward_deterministic():
+    w = wl.make_ffn("det", "bf16", 1024, 1024, 4096, seed=11, sparsity=0.99, ell_width=128)
+    Y1, b1, _, _ = run_forward(w)
+    Y2, b2, _, _ = run_forward(w)
+    assert torch.equal(Y1.view(torch.int16), Y2.view(torch.int16))
+    for k in ("cnt", "row_nnz", "row_ovf"):
+        assert torch.equal(b1[k], b2[k])
