@@ -129,6 +129,11 @@ typedef struct {
  *  W_gate    [d][f], gated only
  *  W_upT     optional [f][d] copy of W_up transposed (read by the gated up-dot);
  *            when NULL the gated path transposes W_up into the workspace
+ *  W_down_packed  optional bf16 copy of W_down in the slice-major layout written by
+ *            sfl_pack_down_weights ([d/64][f][64]); the sparse down projection reads
+ *            64-column slices of W_down, and this layout makes each slice one
+ *            contiguous block. When NULL (bf16, d % 512 == 0) the forward builds it in
+ *            the workspace on every call.
  *  bias_f    optional float32 [f] added to every pre-activation of column n
  *  shift_t   optional float32 [T] added to every pre-activation of row t
  *            (both are extensions; NULL/NULL is the paper's bias-free FFN)
@@ -149,6 +154,7 @@ typedef struct {
   const void* W_up;
   const void* W_down;
   const void* W_upT;
+  const void* W_down_packed;
   const float* bias_f;
   const float* shift_t;
   sfl_twell_cfg_t cfg;
@@ -236,6 +242,11 @@ sfl_status_t sfl_ffn_backward(const sfl_ffn_bwd_args_t* args, sfl_stream_t strea
  * epilogue writing dense H [T][f] into the workspace, then GEMM with W_down
  * (three GEMMs when gated). Ignores args->twell and args->stats. */
 sfl_status_t sfl_dense_ffn_baseline(const sfl_ffn_args_t* args, sfl_stream_t stream);
+
+/* Slice-major copy of a bf16 W_down [f][d] for the sparse down projection:
+ * out[s][n][c] = W_down[n][64 s + c] for s < d/64, c < 64 (d % 64 == 0). Weights that
+ * stay fixed across calls are packed once and passed as W_down_packed. */
+sfl_status_t sfl_pack_down_weights(const void* W_down, void* out, int64_t f, int64_t d, sfl_stream_t stream);
 
 /* out[c][r] = in[r][c] for a rows x cols matrix of 2-byte (elem_bytes = 2) or
  * 4-byte (elem_bytes = 4) elements; lets callers keep W_upT next to W_up. */

@@ -27,7 +27,7 @@ BUF_NAMES = ["val", "idx", "cnt", "row_nnz", "row_ovf", "ovf_rows", "n_ovf", "el
 
 EXPORTED = ["sfl_status_string", "sfl_version", "sfl_twell_buffer_sizes", "sfl_pack_twell",
             "sfl_workspace_size", "sfl_ffn_forward", "sfl_up_projection", "sfl_ffn_backward",
-            "sfl_dense_ffn_baseline", "sfl_transpose"]
+            "sfl_dense_ffn_baseline", "sfl_transpose", "sfl_pack_down_weights"]
 
 
 class SflError(RuntimeError):
@@ -54,7 +54,8 @@ class Stats(Structure):
 class FfnArgs(Structure):
     _fields_ = [("dtype", c_int), ("gated", c_int32), ("T", c_int64), ("d", c_int64), ("f", c_int64),
                 ("X", c_void_p), ("W_gate", c_void_p), ("W_up", c_void_p), ("W_down", c_void_p),
-                ("W_upT", c_void_p), ("bias_f", c_void_p), ("shift_t", c_void_p), ("cfg", Cfg),
+                ("W_upT", c_void_p), ("W_down_packed", c_void_p), ("bias_f", c_void_p), ("shift_t", c_void_p),
+                ("cfg", Cfg),
                 ("Y", c_void_p), ("twell", Twell), ("stats", c_void_p), ("workspace", c_void_p),
                 ("workspace_bytes", c_size_t), ("events", c_void_p), ("n_events", c_int32)]
 
@@ -78,6 +79,7 @@ _lib.sfl_up_projection.argtypes = [POINTER(FfnArgs), c_void_p, c_void_p]
 _lib.sfl_ffn_backward.argtypes = [POINTER(BwdArgs), c_void_p]
 _lib.sfl_dense_ffn_baseline.argtypes = [POINTER(FfnArgs), c_void_p]
 _lib.sfl_transpose.argtypes = [c_void_p, c_void_p, c_int64, c_int64, c_int32, c_void_p]
+_lib.sfl_pack_down_weights.argtypes = [c_void_p, c_void_p, c_int64, c_int64, c_void_p]
 for _n in EXPORTED[2:]:
     getattr(_lib, _n).restype = c_int
 
@@ -168,8 +170,8 @@ def read_stats(stats_tensor):
     return {n: getattr(s, n) for n, _ in Stats._fields_ if n != "reserved"}
 
 
-def ffn_args(X, W_up, W_down, cfg, *, Y=None, bufs=None, W_gate=None, W_upT=None, bias_f=None, shift_t=None,
-             stats=None, workspace=None, events=None):
+def ffn_args(X, W_up, W_down, cfg, *, Y=None, bufs=None, W_gate=None, W_upT=None, W_down_packed=None,
+             bias_f=None, shift_t=None, stats=None, workspace=None, events=None):
     T, d = X.shape
     f = W_down.shape[0]
     a = FfnArgs()
@@ -177,6 +179,7 @@ def ffn_args(X, W_up, W_down, cfg, *, Y=None, bufs=None, W_gate=None, W_upT=None
     a.gated = 1 if W_gate is not None else 0
     a.T, a.d, a.f = T, d, f
     a.X, a.W_gate, a.W_up, a.W_down, a.W_upT = _ptr(X), _ptr(W_gate), _ptr(W_up), _ptr(W_down), _ptr(W_upT)
+    a.W_down_packed = _ptr(W_down_packed)
     a.bias_f, a.shift_t = _ptr(bias_f), _ptr(shift_t)
     a.cfg = cfg
     a.Y = _ptr(Y)
@@ -235,6 +238,11 @@ def bwd_args(X, W_up, W_down, dY, cfg, saved_bufs, lambda_l1, dX, dW_up, dW_down
 
 def sfl_ffn_backward(args, stream=None):
     _check("sfl_ffn_backward", _lib.sfl_ffn_backward(ctypes.byref(args), _stream(stream)))
+
+
+def sfl_pack_down_weights(W_down, out, stream=None):
+    f, d = W_down.shape
+    _check("sfl_pack_down_weights", _lib.sfl_pack_down_weights(_ptr(W_down), _ptr(out), f, d, _stream(stream)))
 
 
 def sfl_transpose(inp, out, stream=None):

@@ -35,8 +35,8 @@ def hipcc():
     raise RuntimeError("hipcc not found")
 
 
-def _compile(src, obj):
-    cmd = [hipcc(), *FLAGS, "-x", "hip", "-c", src, "-o", obj]
+def _compile(src, obj, extra=()):
+    cmd = [hipcc(), *FLAGS, *extra, "-x", "hip", "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     errs = "\n".join(l for l in (r.stderr or "").splitlines() if "packed-fp32-ops" not in l)
     if r.returncode != 0:
@@ -44,22 +44,24 @@ def _compile(src, obj):
     return errs
 
 
-def build(verbose=False, jobs=None) -> str:
+def build(verbose=False, jobs=None, extra_flags=(), out=None) -> str:
+    """Compile and link; `extra_flags` go to every hipcc line, `out` overrides the library path."""
+    lib = out or LIB
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
     jobs = jobs or min(len(srcs), max(1, (os.cpu_count() or 4)), 16)
     with tempfile.TemporaryDirectory(prefix="sfl_build_") as tmp:
         objs = [os.path.join(tmp, os.path.basename(s) + ".o") for s in srcs]
         with cf.ThreadPoolExecutor(jobs) as ex:
-            for src, msg in zip(srcs, ex.map(_compile, srcs, objs)):
+            for src, msg in zip(srcs, ex.map(lambda a, o: _compile(a, o, extra_flags), srcs, objs)):
                 if verbose and msg.strip():
                     print(f"[{os.path.basename(src)}]\n{msg}", file=sys.stderr)
-        tmp_lib = LIB + ".tmp"
+        tmp_lib = lib + ".tmp"
         cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp_lib]
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:
             raise RuntimeError(f"link failed:\n{r.stderr}")
-        os.replace(tmp_lib, LIB)
-    return LIB
+        os.replace(tmp_lib, lib)
+    return lib
 
 
 if __name__ == "__main__":

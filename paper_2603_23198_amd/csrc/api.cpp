@@ -79,6 +79,10 @@ sfl_status_t check_forward(const sfl_ffn_args_t* a, bool need_output = true) {
   if (a->dtype == SFL_BF16 && (a->d % 64 != 0 || a->f % 64 != 0)) return SFL_E_UNSUPPORTED;
   if (a->gated && a->dtype != SFL_BF16) return SFL_E_UNSUPPORTED;
   if (a->gated && !(a->d == 512 || a->d == 1024 || a->d == 2048 || a->d == 4096)) return SFL_E_UNSUPPORTED;
+  // the bf16 GEMMs address each operand with 32-bit byte offsets
+  const int64_t lim = (int64_t)1 << 31;
+  const int64_t es = a->dtype == SFL_BF16 ? 2 : 4;
+  if (a->T * a->d * es >= lim || a->d * a->f * es >= lim || a->T * a->f * es >= lim) return SFL_E_UNSUPPORTED;
   return SFL_OK;
 }
 
@@ -93,8 +97,11 @@ struct FwdPlan {
   float* Z = nullptr;        // unfused path: fp32 pre-activations [T][f]
   void* ovf_dense = nullptr; // dense-backup rows when the caller gave none [cap][f]
   void* WupT = nullptr;      // gated: W_up transposed [f][d]
+  void* WdP = nullptr;       // slice-major W_down when the caller gave none [d/64][f][64]
   size_t bytes = 0;
 };
+
+bool packed_gather(const sfl_ffn_args_t& a) { return a.dtype == SFL_BF16 && !a.gated && a.d % 512 == 0; }
 
 FwdPlan plan_forward(const sfl_ffn_args_t& a, void* ws) {
   Carve c(ws);
@@ -103,6 +110,7 @@ FwdPlan plan_forward(const sfl_ffn_args_t& a, void* ws) {
   if (!fused_twell(a)) p.Z = (float*)c.take((size_t)a.T * a.f * 4);
   if (!a.twell.ovf_dense) p.ovf_dense = c.take((size_t)cap * a.f * elem_size(a.dtype));
   if (a.gated && !a.W_upT) p.WupT = c.take((size_t)a.f * a.d * elem_size(a.dtype));
+  if (packed_gather(a) && !a.W_down_packed) p.WdP = c.take((size_t)a.f * a.d * 2);
   p.bytes = c.used;
   return p;
 }
@@ -117,6 +125,7 @@ GemmParams gp_zero() {
 
 // B operand of X W for W [d][f] (row-contiguous over f) or W^T [f][d] (K-contiguous).
 void set_weight_B(GemmParams& g, const void* W, const void* WT, int64_t d, int64_t f, int* blay) {
+  g.b_bytes = d * f * 2;
   if (WT) {
     g.B = WT;
     g.ldb = d;
@@ -220,6 +229,7 @@ sfl_status_t sfl_up_projection(const sfl_ffn_args_t* a, float* Z, sfl_stream_t s
   g.K = (int)a->d;
   g.A = a->X;
   g.lda = a->d;
+  g.a_bytes = a->T * a->d * 2;
   int blay = LAY_RC;
   if (a->gated)
     set_weight_B(g, a->W_gate, nullptr, a->d, a->f, &blay);
@@ -265,6 +275,7 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
     g.K = (int)d;
     g.A = a->X;
     g.lda = d;
+    g.a_bytes = T * d * 2;
     int blay;
     set_weight_B(g, Wp, nullptr, d, f, &blay);
     g.bias = a->bias_f;
@@ -299,6 +310,14 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
     }
     SFL_HIP(launch_gated_gather(vb, T, d, a->cfg.ell_width, tw.ell_val, tw.ell_idx, tw.row_nnz, tw.row_ovf, a->X,
                                 WupT, a->W_down, a->Y, s));
+  } else if (packed_gather(*a)) {
+    const void* WdP = a->W_down_packed;
+    if (!WdP) {
+      SFL_HIP(launch_pack_down(a->W_down, plan.WdP, f, d, s));
+      WdP = plan.WdP;
+    }
+    SFL_HIP(launch_gather_down_packed(T, d, f, a->cfg.ell_width, tw.ell_val, tw.ell_idx, tw.row_nnz, tw.row_ovf,
+                                      WdP, a->Y, s));
   } else {
     SFL_HIP(launch_gather_down(vb, T, d, a->cfg.ell_width, tw.ell_val, tw.ell_idx, tw.row_nnz, tw.row_ovf,
                                a->W_down, a->Y, s));
@@ -312,6 +331,7 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
     g.K = (int)d;
     g.A = a->X;
     g.lda = d;
+    g.a_bytes = T * d * 2;
     g.a_rows = tw.ovf_rows;
     g.m_count = tw.n_ovf;
     g.count_cap = (int32_t)cap;
@@ -336,10 +356,12 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
     y.K = (int)f;
     y.A = ovf_dense;
     y.lda = f;
+    y.a_bytes = cap * f * 2;
     y.m_count = tw.n_ovf;
     y.count_cap = (int32_t)cap;
     y.B = a->W_down;
     y.ldb = d;
+    y.b_bytes = f * d * 2;
     y.c_rows = tw.ovf_rows;
     y.C = a->Y;
     y.ldc = d;
@@ -366,6 +388,7 @@ sfl_status_t sfl_dense_ffn_baseline(const sfl_ffn_args_t* a, sfl_stream_t stream
   g.K = (int)d;
   g.A = a->X;
   g.lda = d;
+  g.a_bytes = T * d * 2;
   int blay;
   set_weight_B(g, a->gated ? a->W_gate : a->W_up, nullptr, d, f, &blay);
   g.bias = a->bias_f;
@@ -387,8 +410,10 @@ sfl_status_t sfl_dense_ffn_baseline(const sfl_ffn_args_t* a, sfl_stream_t stream
   y.K = (int)f;
   y.A = a->workspace;
   y.lda = f;
+  y.a_bytes = T * f * 2;
   y.B = a->W_down;
   y.ldb = d;
+  y.b_bytes = f * d * 2;
   y.C = a->Y;
   y.ldc = d;
   SFL_HIP(run_gemm(a->dtype, LAY_KC, LAY_RC, EPI_ACT, y, s));
@@ -401,6 +426,13 @@ sfl_status_t sfl_transpose(const void* in, void* out, int64_t rows, int64_t cols
   if (rows < 0 || cols < 0 || (elem_bytes != 2 && elem_bytes != 4)) return SFL_E_ARG;
   if (rows * cols > 0 && (!in || !out)) return SFL_E_ARG;
   SFL_HIP(launch_transpose(in, out, rows, cols, elem_bytes, (hipStream_t)stream));
+  return SFL_OK;
+}
+
+sfl_status_t sfl_pack_down_weights(const void* W_down, void* out, int64_t f, int64_t d, sfl_stream_t stream) {
+  if (f < 1 || d < 1 || d % 64 != 0 || !W_down || !out) return SFL_E_ARG;
+  if (f * d * 2 >= ((int64_t)1 << 31)) return SFL_E_UNSUPPORTED;
+  SFL_HIP(launch_pack_down(W_down, out, f, d, (hipStream_t)stream));
   return SFL_OK;
 }
 

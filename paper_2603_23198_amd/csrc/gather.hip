@@ -14,6 +14,8 @@
 #include "common.h"
 #include "internal.h"
 
+#include <algorithm>
+
 namespace sfl {
 
 namespace {
@@ -102,6 +104,115 @@ __global__ __launch_bounds__(256) void k_gather_down(int64_t T, int64_t d, int K
   }
 }
 
+// bf16 variant with 64-column slices, persistent over the slices of one XCD.
+// Workgroup g runs on XCD g % 8 (workgroups are dispatched round-robin over the XCDs);
+// it owns a block of tokens and walks that XCD's slices (x, x+8, x+16, ...) in order,
+// like every other workgroup of the XCD, so the XCD works on about one slice at a time.
+// W is the slice-major copy of W_down ([d/64][f][64]): a slice (f x 128 bytes, 2 MiB at
+// f = 16384) is one contiguous block that stays in the XCD's 4 MiB L2.
+// The block's ELL entries are copied once into LDS (index | bf16 value << 16) and
+// reused for every slice, so the per-token metadata latency is paid once, not per slice.
+// Lane = (group g = lane / 8, part i = lane % 8): the 8 groups each take a different ELL
+// entry and read its 128-byte row segment as 8 x 16 bytes, so one load instruction
+// fetches 8 rows; a token's partial sums are folded over the 8 groups at the end, in a
+// fixed order.
+constexpr int SLICE2 = 64;
+#ifndef SFL_GATHER_WAVES
+#define SFL_GATHER_WAVES 8
+#endif
+#ifndef SFL_GATHER_UNROLL
+#define SFL_GATHER_UNROLL 8
+#endif
+#ifndef SFL_GATHER_LDS
+#define SFL_GATHER_LDS 65536
+#endif
+constexpr int GATHER_WAVES = SFL_GATHER_WAVES;
+constexpr int GU = SFL_GATHER_UNROLL;  // row loads in flight per lane
+constexpr int GATHER_LDS = SFL_GATHER_LDS;  // bytes of cached ELL entries per workgroup
+
+__global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
+    int64_t T, int64_t d, int64_t f, int K, const bf16_t* __restrict__ ell_val, const uint16_t* __restrict__ ell_idx,
+    const int32_t* __restrict__ row_nnz, const uint8_t* __restrict__ row_ovf, const bf16_t* __restrict__ W,
+    bf16_t* __restrict__ Y, int n_slices, int tpw) {
+  extern __shared__ uint32_t ent[];  // [tpw][K] entries, then [tpw] counts (-1 = skip)
+  int* cnt_s = (int*)(ent + (size_t)tpw * K);
+  const int xcd = blockIdx.x & 7;
+  const int64_t t0 = (int64_t)(blockIdx.x >> 3) * tpw;
+  const int l = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int grp = l >> 3, sub = l & 7;
+  // stage the block's ELL rows in LDS
+  for (int i = threadIdx.x; i < tpw; i += blockDim.x) {
+    const int64_t t = t0 + i;
+    cnt_s[i] = (t < T && !row_ovf[t]) ? row_nnz[t] : -1;
+  }
+  __syncthreads();
+  for (int i = wave; i < tpw; i += GATHER_WAVES) {
+    const int c = cnt_s[i];
+    const int64_t t = t0 + i;
+    for (int e = l; e < c; e += 64)
+      ent[i * K + e] = (uint32_t)ell_idx[t * K + e] | ((uint32_t)ell_val[t * K + e] << 16);
+  }
+  __syncthreads();
+  const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc((void*)W, (short)0, 0x7fffffff, 0x00020000);
+  constexpr uint32_t row_b = SLICE2 * 2;
+  for (int slice = xcd; slice < n_slices; slice += 8) {
+    const int64_t col = (int64_t)slice * SLICE2 + sub * 8;
+    const uint32_t col_b = (uint32_t)(slice * f * SLICE2 * 2) + (uint32_t)sub * 16u;
+    for (int i = wave; i < tpw; i += GATHER_WAVES) {
+      const int nnz = __builtin_amdgcn_readfirstlane(cnt_s[i]);
+      if (nnz < 0) continue;
+      const uint32_t* er = ent + i * K;
+      float acc[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+      for (int q = 0; q < nnz; q += 8 * GU) {
+        u32x4_t w[GU];
+        float v[GU];
+#pragma unroll
+        for (int u = 0; u < GU; ++u) {
+          const int e = q + u * 8 + grp;  // entry of this group
+          const uint32_t x = e < nnz ? er[e] : 0u;
+          v[u] = bf16hi(x);
+          const uint32_t off = e < nnz ? (x & 0xffffu) * row_b + col_b : 0x80000000u;
+          w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0));
+        }
+#pragma unroll
+        for (int u = 0; u < GU; ++u)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            acc[2 * j] = fmaf(v[u], bf16lo(w[u][j]), acc[2 * j]);
+            acc[2 * j + 1] = fmaf(v[u], bf16hi(w[u][j]), acc[2 * j + 1]);
+          }
+      }
+      // fold the 8 groups: lanes l, l^8, l^16, l^32 hold partial sums of the same columns
+#pragma unroll
+      for (int o = 8; o < 64; o <<= 1)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], o, 64);
+      if (grp == 0) {
+        u32x4_t out;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          out[j] = (uint32_t)f32_to_bf16(acc[2 * j]) | ((uint32_t)f32_to_bf16(acc[2 * j + 1]) << 16);
+        *(u32x4_t*)(Y + (t0 + i) * d + col) = out;
+      }
+    }
+  }
+}
+
+// out[s][n][c] = W[n][64 s + c]: 16 bytes per thread, reads coalesced along rows.
+__global__ __launch_bounds__(256) void k_pack_down(const bf16_t* __restrict__ W, bf16_t* __restrict__ out, int64_t f,
+                                                   int64_t d) {
+  const int64_t chunks_per_row = d / 8;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= f * chunks_per_row) return;
+  const int64_t n = i / chunks_per_row;
+  const int64_t c = i - n * chunks_per_row;  // 8-column chunk within the row
+  const int64_t s = c / 8, c8 = c % 8;
+  *(u32x4_t*)(out + ((s * f + n) * SLICE2 + c8 * 8)) = *(const u32x4_t*)(W + n * d + c * 8);
+}
+
 // d = NQ * 512 (each lane holds 8 consecutive columns of every 512-column group).
 template <int NQ>
 __global__ __launch_bounds__(256) void k_gated_gather(int64_t T, int K, const bf16_t* __restrict__ ell_val,
@@ -187,6 +298,37 @@ hipError_t launch_gather_down(int val_bf16, int64_t T, int64_t d, int K, const v
   else
     hipLaunchKernelGGL(k_gather_down<float>, grid, dim3(256), 0, s, T, d, K, (const float*)ell_val, ell_idx,
                        row_nnz, row_ovf, (const float*)W, (float*)Y, n_slices, n_tb);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, const void* ell_val,
+                                     const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
+                                     const void* Wp, void* Y, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  if (d % (8 * SLICE2) != 0) return hipErrorInvalidValue;
+  const int n_slices = (int)(d / SLICE2);
+  // tokens per workgroup: what the LDS budget holds, at most 64; a token block goes to
+  // every XCD (each XCD covers its own slices), so the grid is 8 x the number of blocks
+  const int64_t per_tok = (int64_t)std::max(K, 1) * 4 + 4;
+  const int tpw = (int)std::max<int64_t>(1, std::min<int64_t>(GATHER_LDS / 1024, GATHER_LDS / per_tok));
+  const int64_t blocks = cdiv(T, tpw);
+  const size_t lds = (size_t)tpw * per_tok;
+  if (lds > 160 * 1024) return hipErrorInvalidValue;
+  if (lds > 65536) {
+    const hipError_t e = hipFuncSetAttribute((const void*)k_gather_down_b16,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k_gather_down_b16, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), lds, s, T, d, f, K,
+                     (const bf16_t*)ell_val, ell_idx, row_nnz, row_ovf, (const bf16_t*)Wp, (bf16_t*)Y, n_slices,
+                     tpw);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_down(const void* W, void* out, int64_t f, int64_t d, hipStream_t s) {
+  const int64_t n = f * (d / 8);
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_pack_down, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, s, (const bf16_t*)W, (bf16_t*)out, f, d);
   return hipGetLastError();
 }
 

@@ -21,6 +21,7 @@ namespace {
 
 constexpr int BM = 256, BN = 256, BK = 64, LDK = BK + 8;
 constexpr int NTHR = 512;
+constexpr int NWAVES = NTHR / 64;
 constexpr int WAVES_M = 2, WAVES_N = 4;
 constexpr int WTM = BM / WAVES_M;  // 128 rows per wave
 constexpr int WTN = BN / WAVES_N;  // 64 cols per wave
@@ -33,36 +34,45 @@ __device__ __forceinline__ bool active_bits(float z) {
 }
 
 // ---- loaders -----------------------------------------------------------------------
-// K-contiguous source rows ([R][K], stride ld): ROWS x 64 tile in 16-byte chunks.
+// All global reads go through raw buffer loads: an offset at or beyond the descriptor's
+// byte size reads as zero, so M/N/K tails and gathered rows need no branches. Offsets are
+// 32-bit, so every operand tensor must be smaller than 2 GiB (checked by the host).
+constexpr uint32_t kOOB = 0x80000000u;  // an offset that is always out of range
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  const int32_t n = bytes > 0x7fffffff ? 0x7fffffff : (int32_t)bytes;
+  return __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, n, 0x00020000);
+}
+
+// K-contiguous source rows ([R][K], row stride ld elements): ROWS x 64 tile in 16-byte
+// chunks; optional gather of the rows (rows[r]).
 template <int ROWS>
 struct LoadKC {
   static constexpr int PER = ROWS * (BK / 8) / NTHR;
   u32x4_t reg[PER];
-  const bf16_t* src[PER];  // row base pointer (nullptr = out of range)
-  __device__ void init(const bf16_t* base, int64_t ld, const int32_t* rows, int r0, int rlimit, int tid) {
+  uint32_t boff[PER];  // byte offset of the chunk at k = 0, or kOOB
+  __amdgpu_buffer_rsrc_t rs;
+  __device__ void init(const bf16_t* base, int64_t bytes, int64_t ld, const int32_t* rows, int r0, int rlimit,
+                       int tid) {
+    rs = make_rsrc(base, bytes);
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int c = tid + p * NTHR;
       const int r = r0 + c / (BK / 8);
       const int kc = (c % (BK / 8)) * 8;
-      const bf16_t* q = nullptr;
+      uint32_t o = kOOB;
       if (r < rlimit) {
         const int64_t sr = rows ? (int64_t)rows[r] : (int64_t)r;
-        q = base + sr * ld + kc;
+        o = (uint32_t)((sr * ld + kc) * 2);
       }
-      src[p] = q;
+      boff[p] = o;
     }
   }
-  __device__ void load(int k0, int klimit, int tid) {
+  // K must be a multiple of 64 here (no K tail); k0 goes in the scalar offset.
+  __device__ void load(int k0, int, int) {
 #pragma unroll
-    for (int p = 0; p < PER; ++p) {
-      const int c = tid + p * NTHR;
-      const int kc = (c % (BK / 8)) * 8;
-      if (src[p] && k0 + kc < klimit)
-        reg[p] = *(const u32x4_t*)(src[p] + k0);
-      else
-        reg[p] = u32x4_t{0, 0, 0, 0};
-    }
+    for (int p = 0; p < PER; ++p)
+      reg[p] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)boff[p], k0 * 2, 0));
   }
   __device__ void store(bf16_t* lds, int tid) {
 #pragma unroll
@@ -75,41 +85,51 @@ struct LoadKC {
   }
 };
 
-// Row-contiguous source ([K][R], stride ld, R contiguous): job = (pair of adjacent rows,
-// group of 8 k). Optional gather on K: source row of k is krows[k].
-template <int ROWS>
+// Row-contiguous source ([K][R], row stride ld elements, R contiguous): job = (pair of
+// adjacent rows, group of 8 k); with KG the source row of k is krows[k] (K gather).
+template <int ROWS, bool KG>
 struct LoadRC {
   static constexpr int PAIRS = ROWS / 2;
   static constexpr int PER = PAIRS * (BK / 8) / NTHR;
+  static_assert(NTHR % PAIRS == 0, "a thread keeps the same row pair for all its jobs");
+  static constexpr int GSTEP = NTHR / PAIRS;  // k-group step between a thread's jobs
   uint32_t reg[PER][8];
-  const bf16_t* base;
-  int64_t ld;
+  uint32_t coff[PER];     // gather path: byte offset of the row pair within a source row, or kOOB
+  uint32_t vbase;         // plain path: byte offset of (first k of the thread's first job, row pair)
+  __amdgpu_buffer_rsrc_t rs;
+  uint32_t ld2;           // source row stride in bytes
   const int32_t* krows;
-  int r0, rlimit;
-  __device__ void init(const bf16_t* b, int64_t ld_, const int32_t* kr, int r0_, int rlimit_) {
-    base = b;
-    ld = ld_;
+  __device__ void init(const bf16_t* base, int64_t bytes, int64_t ld, const int32_t* kr, int r0, int rlimit,
+                       int tid) {
+    rs = make_rsrc(base, bytes);
+    ld2 = (uint32_t)(ld * 2);
     krows = kr;
-    r0 = r0_;
-    rlimit = rlimit_;
+    const int r = r0 + 2 * (tid % PAIRS);
+#pragma unroll
+    for (int p = 0; p < PER; ++p) coff[p] = r < rlimit ? (uint32_t)r * 2u : kOOB;
+    // rows past the end read the last valid pair instead: they only feed output columns
+    // that are never stored
+    const int rc = r < rlimit ? r : rlimit - 2;
+    vbase = (uint32_t)((tid / PAIRS) * 8) * ld2 + (uint32_t)rc * 2u;
   }
   __device__ void load(int k0, int klimit, int tid) {
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
-      const int j = tid + p * NTHR;
-      const int pp = j % PAIRS;
-      const int g = j / PAIRS;
-      const int r = r0 + 2 * pp;
-      const bool rv = r < rlimit;
+      const int kl = (tid / PAIRS + p * GSTEP) * 8;  // first k of this job within the tile
+      if constexpr (KG) {
+        // K gather with a device-side K bound: per-k source rows, explicit tail check
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int k = k0 + g * 8 + e;
-        uint32_t v = 0;
-        if (rv && k < klimit) {
-          const int64_t sk = krows ? (int64_t)krows[k] : (int64_t)k;
-          v = *(const uint32_t*)(base + sk * ld + r);
+        for (int e = 0; e < 8; ++e) {
+          const int k = k0 + kl + e;
+          const uint32_t sr = (uint32_t)krows[min(k, klimit - 1)];
+          const bool ok = (k < klimit) & (coff[p] != kOOB);
+          reg[p][e] = __builtin_amdgcn_raw_buffer_load_b32(rs, (int)(ok ? sr * ld2 + coff[p] : kOOB), 0, 0);
         }
-        reg[p][e] = v;
+      } else {
+        // plain rows: K is a multiple of 64; the k part of the offset is uniform (scalar offset)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          reg[p][e] = __builtin_amdgcn_raw_buffer_load_b32(rs, (int)vbase, (k0 + p * GSTEP * 8 + e) * (int)ld2, 0);
       }
     }
   }
@@ -134,18 +154,12 @@ struct LoadRC {
   }
 };
 
+// LAY_KC, LAY_RC, or LAY_RCG (row-contiguous with a K gather)
+constexpr int LAY_RCG = LAY_RCG_;
 template <int LAY, int ROWS> struct LoaderSel;
 template <int ROWS> struct LoaderSel<LAY_KC, ROWS> { typedef LoadKC<ROWS> type; };
-template <int ROWS> struct LoaderSel<LAY_RC, ROWS> { typedef LoadRC<ROWS> type; };
-
-template <int LAY, int ROWS>
-__device__ __forceinline__ void loader_init(typename LoaderSel<LAY, ROWS>::type& L, const bf16_t* base, int64_t ld,
-                                            const int32_t* rows, int r0, int rlimit, int tid) {
-  if constexpr (LAY == LAY_KC)
-    L.init(base, ld, rows, r0, rlimit, tid);
-  else
-    L.init(base, ld, rows, r0, rlimit);
-}
+template <int ROWS> struct LoaderSel<LAY_RC, ROWS> { typedef LoadRC<ROWS, false> type; };
+template <int ROWS> struct LoaderSel<LAY_RCG, ROWS> { typedef LoadRC<ROWS, true> type; };
 
 // Output-tile order: consecutive workgroup ids are dispatched round-robin over the 8 XCDs;
 // remap so that each XCD gets a contiguous range of logical tiles, then walk that range
@@ -182,8 +196,8 @@ __global__ __launch_bounds__(NTHR) void k_gemm_bf16(GemmParams p) {
 
   typename LoaderSel<ALAY, BM>::type la;
   typename LoaderSel<BLAY, BN>::type lb;
-  loader_init<ALAY, BM>(la, (const bf16_t*)p.A, p.lda, p.a_rows, m0, m_eff, tid);
-  loader_init<BLAY, BN>(lb, (const bf16_t*)p.B, p.ldb, p.b_rows, n0, p.N, tid);
+  la.init((const bf16_t*)p.A, p.a_bytes, p.lda, p.a_rows, m0, m_eff, tid);
+  lb.init((const bf16_t*)p.B, p.b_bytes, p.ldb, p.b_rows, n0, p.N, tid);
 
   f32x16_t acc[TM][TN];
 #pragma unroll
@@ -265,9 +279,9 @@ __global__ __launch_bounds__(NTHR) void k_gemm_bf16(GemmParams p) {
         }
       }
       __syncthreads();
-      // compaction: wave w handles rows 8w .. 8w+7 of this pass
-      for (int rr = 0; rr < 8; ++rr) {
-        const int lrow = wave * 8 + rr;
+      // compaction: each wave handles 64 / NWAVES consecutive rows of this pass
+      for (int rr = 0; rr < 64 / NWAVES; ++rr) {
+        const int lrow = wave * (64 / NWAVES) + rr;
         const int grow = m0 + pass * 64 + lrow;
         if (grow >= m_eff) break;
         int running = 0;
@@ -429,7 +443,9 @@ hipError_t gemm_bf16(int alay, int blay, int epi, const GemmParams& p, hipStream
   SFL_CASE(LAY_KC, LAY_KC, EPI_MUL_ACT)
   // backward dense-backup rows
   SFL_CASE(LAY_KC, LAY_KC, EPI_MASKGRAD)
-  SFL_CASE(LAY_RC, LAY_RC, EPI_ACCUM_F32)
+  SFL_CASE(LAY_RCG, LAY_RCG, EPI_ACCUM_F32)
+  SFL_CASE(LAY_RC, LAY_RCG, EPI_ACCUM_F32)
+  SFL_CASE(LAY_RCG, LAY_RC, EPI_ACCUM_F32)
 #undef SFL_CASE
   return hipErrorInvalidValue;
 }

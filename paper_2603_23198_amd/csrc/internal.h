@@ -12,7 +12,8 @@ namespace sfl {
 // ---------------------------------------------------------------- GEMM ----
 // C = A * B with bf16 operands on MFMA (fp32 accumulate), or fp32 operands on FMA.
 // Layouts: A is MK ([M][K], row stride lda) or KM ([K][M]); B is NK ([N][K]) or KN ([K][N]).
-enum Layout { LAY_KC = 0, LAY_RC = 1 };  // K-contiguous rows / row-contiguous (K-major)
+// K-contiguous rows / row-contiguous (K-major) / row-contiguous with the K rows gathered
+enum Layout { LAY_KC = 0, LAY_RC = 1, LAY_RCG_ = 2 };
 
 enum Epilogue {
   EPI_TWELL = 0,       // z = acc + bias[n] + shift[srow]; ReLU -> TwELL (val, idx, cnt)
@@ -28,8 +29,10 @@ struct GemmParams {
   int M, N, K;
   const void* A;
   int64_t lda;
+  int64_t a_bytes;         // size of the A tensor in bytes (bounds of the buffer loads)
   const void* B;
   int64_t ldb;
+  int64_t b_bytes;
   const int32_t* a_rows;   // gather: MK -> A row index per m; RC -> source row per k
   const int32_t* b_rows;   // gather: KC -> B row per n (unused); RC -> source row per k
   const int32_t* m_count;  // device bound on M (min(*m_count, count_cap)), optional
@@ -79,6 +82,11 @@ hipError_t launch_ovf_l1(int64_t f, int val_bf16, const void* ovf_dense, const i
 hipError_t launch_gather_down(int val_bf16, int64_t T, int64_t d, int ell_width, const void* ell_val,
                               const uint16_t* ell_idx, const int32_t* row_nnz,
                               const uint8_t* row_ovf, const void* W, void* Y, hipStream_t s);
+// bf16, d % 512 == 0: same sum from the slice-major copy of W_down (persistent, XCD-aware).
+hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int ell_width, const void* ell_val,
+                                     const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
+                                     const void* W_packed, void* Y, hipStream_t s);
+hipError_t launch_pack_down(const void* W, void* out, int64_t f, int64_t d, hipStream_t s);
 // Gated fused up-dot + down (Alg. 2) from the ELL rows of the gate pattern.
 hipError_t launch_gated_gather(int val_bf16, int64_t T, int64_t d, int ell_width, const void* ell_val,
                                const uint16_t* ell_idx, const int32_t* row_nnz,

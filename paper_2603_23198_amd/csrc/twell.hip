@@ -62,70 +62,152 @@ hipError_t launch_pack_twell(const float* Z, int64_t T, int64_t f, int val_bf16,
   return hipGetLastError();
 }
 
-// One wave per row. Pass 1: tile counts 64 at a time, prefix sums give each tile's
-// offset in the ELL row and the row total. Pass 2 (sparse rows with an ELL buffer):
-// copy each tile's slots to its offset. Stats use integer atomics (exact) and a
-// float64 atomic for the L1 sum of the stored values.
+// One wave per row. Pass 1: the tile counts, 64 at a time, give the row total, the
+// number of overflowing tiles and (kept in LDS) the inclusive prefix of the counts.
+// Pass 2 (sparse rows): lane q of each 64-entry step finds the tile holding the row's
+// q-th active column by binary search over the prefix, then copies that slot to ELL
+// position q, so the ELL row lists the active columns in ascending order. Stats use
+// integer atomics (exact) and a float64 atomic for the sum of the stored values.
+constexpr int kClassifyMaxTiles = 512;
+constexpr int kClassifyRowsPerWave = 8;
+
+// Statistics of a block's rows, reduced in LDS and added to the device totals with one
+// atomic per field per block (per-row atomics on the same address serialise).
+__device__ __forceinline__ void block_stats_add(sfl_stats_t* stats, int64_t nnz, int tile_over, float l1) {
+  __shared__ long long s_nnz[4];
+  __shared__ int s_over[4];
+  __shared__ float s_l1[4];
+  const int w = threadIdx.x >> 6;
+  l1 = wave_sum<float>(l1);
+  if ((threadIdx.x & 63) == 0) {
+    s_nnz[w] = nnz;
+    s_over[w] = tile_over;
+    s_l1[w] = l1;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const long long a = s_nnz[0] + s_nnz[1] + s_nnz[2] + s_nnz[3];
+    const int b = s_over[0] + s_over[1] + s_over[2] + s_over[3];
+    const float c = (s_l1[0] + s_l1[1]) + (s_l1[2] + s_l1[3]);
+    if (a) atomicAdd((unsigned long long*)&stats->total_nnz, (unsigned long long)a);
+    if (b) atomicAdd((unsigned long long*)&stats->n_tile_ovf, (unsigned long long)b);
+    if (c != 0.f) atomicAdd(&stats->l1_sum, (double)c);
+  }
+}
+
 template <typename V>
 __global__ __launch_bounds__(256) void k_classify(int64_t T, int NT, int S, int K, const V* __restrict__ val,
                                                   const uint16_t* __restrict__ idx, const int32_t* __restrict__ cnt,
                                                   int32_t* __restrict__ row_nnz, uint8_t* __restrict__ row_ovf,
                                                   V* __restrict__ ell_val, uint16_t* __restrict__ ell_idx,
                                                   sfl_stats_t* __restrict__ stats) {
-  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T) return;
+  __shared__ int incl_lds[4][kClassifyMaxTiles];
+  const int l = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  int* incl_s = incl_lds[w];
+  int64_t nnz_sum = 0;
+  int over_sum = 0;
+  float l1 = 0.f;
+  for (int rr = 0; rr < kClassifyRowsPerWave; ++rr) {
+    const int64_t t = ((int64_t)blockIdx.x * 4 + w) * kClassifyRowsPerWave + rr;
+    if (t >= T) break;
+    const int32_t* crow = cnt + t * NT;
+    int total = 0;
+    int tile_over = 0;
+    for (int j0 = 0; j0 < NT; j0 += 64) {
+      const int c = (j0 + l < NT) ? crow[j0 + l] : 0;
+      const int incl = wave_incl_scan(c) + total;
+      if (j0 + l < NT) incl_s[j0 + l] = incl;
+      total = __shfl(incl, 63, 64);
+      tile_over += __popcll(ballot(c > S));
+    }
+    // the prefix just written to LDS is read by other lanes of this wave below
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const bool ovf = total > K || tile_over > 0;
+    if (l == 0) {
+      row_nnz[t] = total;
+      row_ovf[t] = ovf ? 1 : 0;
+    }
+    nnz_sum += total;
+    over_sum += tile_over;
+    if (!ovf) {
+      const V* vrow = val + t * (int64_t)NT * S;
+      const uint16_t* irow = idx + t * (int64_t)NT * S;
+      for (int q0 = 0; q0 < total; q0 += 64) {
+        const int q = q0 + l;
+        if (q < total) {
+          // first tile j with incl[j] > q
+          int lo = 0, hi = NT - 1;
+          while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (incl_s[mid] > q) hi = mid; else lo = mid + 1;
+          }
+          const int excl = lo > 0 ? incl_s[lo - 1] : 0;
+          const int64_t src = (int64_t)lo * S + (q - excl);
+          const V v = vrow[src];
+          l1 += VT<V>::load(&v, 0);
+          if (ell_val) {
+            ell_val[t * (int64_t)K + q] = v;
+            ell_idx[t * (int64_t)K + q] = irow[src];
+          }
+        }
+      }
+    }
+    // all lanes are done reading this row's prefix before the next row overwrites it
+    __builtin_amdgcn_wave_barrier();
+  }
+  if (stats) block_stats_add(stats, nnz_sum, over_sum, l1);
+}
+
+// Fallback for rows with more tiles than the LDS prefix holds: walks the tiles in order.
+template <typename V>
+__global__ __launch_bounds__(256) void k_classify_wide(int64_t T, int NT, int S, int K, const V* __restrict__ val,
+                                                       const uint16_t* __restrict__ idx,
+                                                       const int32_t* __restrict__ cnt,
+                                                       int32_t* __restrict__ row_nnz, uint8_t* __restrict__ row_ovf,
+                                                       V* __restrict__ ell_val, uint16_t* __restrict__ ell_idx,
+                                                       sfl_stats_t* __restrict__ stats) {
+  const int64_t t0 = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const bool row_ok = t0 < T;
+  const int64_t t = row_ok ? t0 : 0;
   const int l = threadIdx.x & 63;
   const int32_t* crow = cnt + t * NT;
   int64_t total = 0;
   int tile_over = 0;
   for (int j0 = 0; j0 < NT; j0 += 64) {
-    const int c = (j0 + l < NT) ? crow[j0 + l] : 0;
+    const int c = (row_ok && j0 + l < NT) ? crow[j0 + l] : 0;
     total += wave_sum<int>(c);
     tile_over += __popcll(ballot(c > S));
   }
   const bool ovf = total > K || tile_over > 0;
-  if (l == 0) {
+  if (row_ok && l == 0) {
     row_nnz[t] = (int32_t)total;
     row_ovf[t] = ovf ? 1 : 0;
   }
   float l1 = 0.f;
-  if (!ovf) {
+  if (row_ok && !ovf) {
     const V* vrow = val + t * (int64_t)NT * S;
     const uint16_t* irow = idx + t * (int64_t)NT * S;
     int offset = 0;
-    for (int j0 = 0; j0 < NT; j0 += 64) {
-      const int c = (j0 + l < NT) ? crow[j0 + l] : 0;
-      const int incl = wave_incl_scan(c);
-      const int excl = incl - c;
-      const int nt_here = (NT - j0) < 64 ? (NT - j0) : 64;
-      for (int jj = 0; jj < nt_here; ++jj) {
-        const int cj = readlane_i(c, jj);
-        if (cj == 0) continue;
-        const int pos = offset + readlane_i(excl, jj);
-        const int64_t src = (int64_t)(j0 + jj) * S;
-        for (int s0 = 0; s0 < cj; s0 += 64) {
-          const int sidx = s0 + l;
-          if (sidx < cj) {
-            const V v = vrow[src + sidx];
-            l1 += VT<V>::load(&v, 0);
-            if (ell_val) {
-              ell_val[t * (int64_t)K + pos + sidx] = v;
-              ell_idx[t * (int64_t)K + pos + sidx] = irow[src + sidx];
-            }
+    for (int j = 0; j < NT; ++j) {
+      const int cj = crow[j];
+      for (int s0 = 0; s0 < cj; s0 += 64) {
+        const int sidx = s0 + l;
+        if (sidx < cj) {
+          const V v = vrow[(int64_t)j * S + sidx];
+          l1 += VT<V>::load(&v, 0);
+          if (ell_val) {
+            ell_val[t * (int64_t)K + offset + sidx] = v;
+            ell_idx[t * (int64_t)K + offset + sidx] = irow[(int64_t)j * S + sidx];
           }
         }
       }
-      offset += readlane_i(incl, 63);
+      offset += cj;
     }
   }
-  if (stats) {
-    l1 = wave_sum<float>(l1);
-    if (l == 0) {
-      atomicAdd((unsigned long long*)&stats->total_nnz, (unsigned long long)total);
-      if (tile_over) atomicAdd((unsigned long long*)&stats->n_tile_ovf, (unsigned long long)tile_over);
-      if (l1 != 0.f) atomicAdd(&stats->l1_sum, (double)l1);
-    }
-  }
+  if (stats) block_stats_add(stats, total, tile_over, l1);
 }
 
 hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int Tn, int S, int K, const void* val,
@@ -133,13 +215,14 @@ hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int Tn, int S, in
                            void* ell_val, uint16_t* ell_idx, sfl_stats_t* stats, hipStream_t s) {
   if (T == 0) return hipSuccess;
   const int NT = (int)cdiv(f, Tn);
-  const dim3 grid((unsigned)cdiv(T, 4));
+  const bool wide = NT > kClassifyMaxTiles;
+  const dim3 grid((unsigned)(wide ? cdiv(T, 4) : cdiv(T, 4 * kClassifyRowsPerWave)));
   if (val_bf16)
-    hipLaunchKernelGGL(k_classify<bf16_t>, grid, dim3(256), 0, s, T, NT, S, K, (const bf16_t*)val, idx, cnt,
-                       row_nnz, row_ovf, (bf16_t*)ell_val, ell_idx, stats);
+    hipLaunchKernelGGL(wide ? k_classify_wide<bf16_t> : k_classify<bf16_t>, grid, dim3(256), 0, s, T, NT, S, K,
+                       (const bf16_t*)val, idx, cnt, row_nnz, row_ovf, (bf16_t*)ell_val, ell_idx, stats);
   else
-    hipLaunchKernelGGL(k_classify<float>, grid, dim3(256), 0, s, T, NT, S, K, (const float*)val, idx, cnt,
-                       row_nnz, row_ovf, (float*)ell_val, ell_idx, stats);
+    hipLaunchKernelGGL(wide ? k_classify_wide<float> : k_classify<float>, grid, dim3(256), 0, s, T, NT, S, K,
+                       (const float*)val, idx, cnt, row_nnz, row_ovf, (float*)ell_val, ell_idx, stats);
   return hipGetLastError();
 }
 

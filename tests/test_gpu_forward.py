@@ -17,7 +17,7 @@ pytestmark = pytest.mark.gpu
 b = pytest.importorskip("paper_2603_23198_amd.binding")
 
 
-def run_forward(w, rows_check=None, use_wupt=False, dense=False):
+def run_forward(w, rows_check=None, use_wupt=False, dense=False, packed_down=False):
     X, Wu, Wd = dev(w.X), dev(w.W_up), dev(w.W_down)
     Wg = dev(w.W_gate) if w.gated else None
     cfg = b.make_cfg(**w.cfg)
@@ -29,12 +29,16 @@ def run_forward(w, rows_check=None, use_wupt=False, dense=False):
     if use_wupt:
         WupT = torch.empty((w.f, w.d), dtype=X.dtype, device="cuda")
         b.sfl_transpose(Wu, WupT)
-    args = b.ffn_args(X, Wu, Wd, cfg, Y=Y, bufs=bufs, W_gate=Wg, W_upT=WupT, bias_f=dev(w.bias_f),
-                      shift_t=dev(w.shift_t), stats=stats)
+    WdP = None
+    if packed_down:
+        WdP = torch.empty_like(Wd)
+        b.sfl_pack_down_weights(Wd, WdP)
+    args = b.ffn_args(X, Wu, Wd, cfg, Y=Y, bufs=bufs, W_gate=Wg, W_upT=WupT, W_down_packed=WdP,
+                      bias_f=dev(w.bias_f), shift_t=dev(w.shift_t), stats=stats)
     ws_bytes = b.sfl_workspace_size(args, 2 if dense else 0)
     ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device="cuda")
-    args = b.ffn_args(X, Wu, Wd, cfg, Y=Y, bufs=bufs, W_gate=Wg, W_upT=WupT, bias_f=dev(w.bias_f),
-                      shift_t=dev(w.shift_t), stats=stats, workspace=ws)
+    args = b.ffn_args(X, Wu, Wd, cfg, Y=Y, bufs=bufs, W_gate=Wg, W_upT=WupT, W_down_packed=WdP,
+                      bias_f=dev(w.bias_f), shift_t=dev(w.shift_t), stats=stats, workspace=ws)
     (b.sfl_dense_ffn_baseline if dense else b.sfl_ffn_forward)(args)
     torch.cuda.synchronize()
     return Y, bufs, stats, cfg
@@ -222,3 +226,18 @@ def test_forward_deterministic():
     assert torch.equal(Y1.view(torch.int16), Y2.view(torch.int16))
     for k in ("cnt", "row_nnz", "row_ovf"):
         assert torch.equal(b1[k], b2[k])
+
+
+def test_packed_down_weights_layout_and_equivalence():
+    w = wl.make_ffn("packed", "bf16", 300, 1024, 2048, seed=12, sparsity=0.98, ell_width=96)
+    Wd = dev(w.W_down)
+    P = torch.empty_like(Wd)
+    b.sfl_pack_down_weights(Wd, P)
+    torch.cuda.synchronize()
+    want = w.W_down.reshape(w.f, w.d // 64, 64).transpose(1, 0, 2).reshape(-1)
+    np.testing.assert_array_equal(host_bits(P).reshape(-1), want)
+    Y1, _, _, _ = run_forward(w)
+    Y2, _, _, _ = run_forward(w, packed_down=True)
+    assert torch.equal(Y1.view(torch.int16), Y2.view(torch.int16))
+    Yref, _ = oracle_rows(w, np.arange(w.T))
+    assert rel_l2(to_f64(Y1), Yref) <= 2e-2
