@@ -176,7 +176,14 @@ typedef struct {
  *  dX        [T][d] activation dtype (overwritten)
  *  dW_up     float32 [d][f] (overwritten)
  *  dW_down   float32 [f][d] (overwritten)
- *  W_upT     optional [f][d]; transposed into the workspace when NULL. */
+ *  W_upT     optional [f][d]; transposed into the workspace when NULL.
+ *  saved     the sfl_twell_t the forward filled (row_nnz, row_ovf, ovf_rows, n_ovf,
+ *            ell_val, ell_idx and ovf_dense are read)
+ *  events / n_events  optional hipEvent_t array recorded at stage boundaries (0: start,
+ *            1: after dZ at the pattern, 2: after dX of the sparse rows, 3: after the
+ *            transposed pattern, 4: after the weight gradients of the sparse rows,
+ *            5: end, after the dense-backup rows).
+ * Supports d in {512, 1024, 2048, 4096}, f % 64 == 0 and f <= 40960. */
 typedef struct {
   sfl_dtype_t dtype;
   int64_t T, d, f;

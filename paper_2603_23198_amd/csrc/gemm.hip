@@ -86,7 +86,8 @@ struct LoadKC {
 };
 
 // Row-contiguous source ([K][R], row stride ld elements, R contiguous): job = (pair of
-// adjacent rows, group of 8 k); with KG the source row of k is krows[k] (K gather).
+// adjacent rows, group of 8 k). With KG, K is bounded on the device and the source row
+// of k is krows[k] (krows == nullptr: row k).
 template <int ROWS, bool KG>
 struct LoadRC {
   static constexpr int PAIRS = ROWS / 2;
@@ -121,7 +122,7 @@ struct LoadRC {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const int k = k0 + kl + e;
-          const uint32_t sr = (uint32_t)krows[min(k, klimit - 1)];
+          const uint32_t sr = krows ? (uint32_t)krows[min(k, klimit - 1)] : (uint32_t)k;
           const bool ok = (k < klimit) & (coff[p] != kOOB);
           reg[p][e] = __builtin_amdgcn_raw_buffer_load_b32(rs, (int)(ok ? sr * ld2 + coff[p] : kOOB), 0, 0);
         }

@@ -1,0 +1,133 @@
+"""sfl_ffn_backward on the GPU against the fp64 oracle (non-gated, with the L1 term).
+
+The oracle consumes the activity pattern the GPU forward saved (its fp32 pre-activation
+decides z > 0, which may differ from fp64 within rounding), then applies the chain rule of
+the loss sum(dY * Y) + lambda/(T f) sum|h|. Bar: relative L2 <= 2e-2 for dX, dW_up, dW_down."""
+import numpy as np
+import pytest
+import scipy.sparse as sp
+import torch
+
+import workloads as wl
+from oracle import ffn
+from tests.gpu_util import dev, host_bits, rel_l2, to_f64, twell_views
+
+pytestmark = pytest.mark.gpu
+
+b = pytest.importorskip("paper_2603_23198_amd.binding")
+
+
+def run_fwd_bwd(w, lam, with_wupt=False):
+    X, Wu, Wd, dY = dev(w.X), dev(w.W_up), dev(w.W_down), dev(w.dY)
+    cfg = b.make_cfg(**w.cfg)
+    bufs = b.alloc_twell(w.T, w.f, "bf16", cfg)
+    Y = torch.empty((w.T, w.d), dtype=torch.bfloat16, device="cuda")
+    args = b.ffn_args(X, Wu, Wd, cfg, Y=Y, bufs=bufs, shift_t=dev(w.shift_t))
+    ws = torch.empty(max(1, b.sfl_workspace_size(args)), dtype=torch.uint8, device="cuda")
+    args = b.ffn_args(X, Wu, Wd, cfg, Y=Y, bufs=bufs, shift_t=dev(w.shift_t), workspace=ws)
+    b.sfl_ffn_forward(args)
+    dX = torch.full((w.T, w.d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    dWu = torch.full((w.d, w.f), float("nan"), dtype=torch.float32, device="cuda")
+    dWd = torch.full((w.f, w.d), float("nan"), dtype=torch.float32, device="cuda")
+    WupT = None
+    if with_wupt:
+        WupT = torch.empty((w.f, w.d), dtype=torch.bfloat16, device="cuda")
+        b.sfl_transpose(Wu, WupT)
+    ba = b.bwd_args(X, Wu, Wd, dY, cfg, bufs, lam, dX, dWu, dWd, W_upT=WupT)
+    bws = torch.empty(max(1, b.sfl_workspace_size(ba, 1)), dtype=torch.uint8, device="cuda")
+    ba = b.bwd_args(X, Wu, Wd, dY, cfg, bufs, lam, dX, dWu, dWd, W_upT=WupT, workspace=bws)
+    b.sfl_ffn_backward(ba)
+    torch.cuda.synchronize()
+    return dX, dWu, dWd, bufs, cfg
+
+
+def gpu_pattern(bufs, w, cfg):
+    """Sparse [T, f] boolean activity saved by the GPU forward: ELL rows and dense-backup rows."""
+    got = twell_views(bufs, w.T, w.f, cfg)
+    rows, cols = [], []
+    for t in np.nonzero(got["row_ovf"] == 0)[0]:
+        c = int(got["row_nnz"][t])
+        rows.append(np.full(c, t))
+        cols.append(got["ell_idx"][t, :c].astype(np.int64))
+    n_ovf = got["n_ovf"]
+    dense = host_bits(bufs["ovf_dense"])[: n_ovf * w.f].reshape(n_ovf, w.f)
+    for i, t in enumerate(got["ovf_rows"][:n_ovf]):
+        c = np.nonzero(dense[i].view(np.int16) > 0)[0]
+        rows.append(np.full(len(c), t))
+        cols.append(c)
+    r = np.concatenate(rows) if rows else np.zeros(0, np.int64)
+    c = np.concatenate(cols) if cols else np.zeros(0, np.int64)
+    return sp.csr_matrix((np.ones(len(r), dtype=bool), (r, c)), shape=(w.T, w.f))
+
+
+def oracle_full(w, active, lam):
+    X, Wu, Wd, dY = w.as_f64(w.X), w.as_f64(w.W_up), w.as_f64(w.W_down), w.as_f64(w.dY)
+    Z = ffn.preactivation(X, Wu, None, w.shift_t)
+    act = active.toarray()
+    H = np.where(act, Z, 0.0)
+    dX, dWu, dWd, _ = ffn.ffn_backward(X, Wu, Wd, dY, H, act, lam)
+    return dX, dWu, dWd
+
+
+@pytest.mark.parametrize("T,d,f,K,S,lam_scale", [(300, 512, 2048, 96, 32, 0.0), (300, 512, 2048, 96, 32, 1e-3),
+                                                 (129, 1024, 1024, 24, 8, 1e-3), (64, 512, 512, 512, 64, 0.0)])
+def test_backward_small_full(T, d, f, K, S, lam_scale):
+    w = wl.make_ffn("bwd", "bf16", T, d, f, seed=T + d, sparsity=0.97, ell_width=K, tile_slots=S, with_dy=True)
+    w.shift_t[:3] = 10.0   # dense-backup rows
+    lam = lam_scale * T * f
+    dX, dWu, dWd, bufs, cfg = run_fwd_bwd(w, lam)
+    act = gpu_pattern(bufs, w, cfg)
+    rdX, rdWu, rdWd = oracle_full(w, act, lam)
+    assert rel_l2(to_f64(dX), rdX) <= 2e-2
+    assert rel_l2(to_f64(dWu), rdWu) <= 2e-2
+    assert rel_l2(to_f64(dWd), rdWd) <= 2e-2
+    ovf = np.nonzero(twell_views(bufs, w.T, w.f, cfg)["row_ovf"])[0]
+    assert len(ovf) >= 3
+    assert rel_l2(to_f64(dX)[ovf], rdX[ovf]) <= 2e-2
+
+
+def test_backward_lambda_term_is_injected():
+    """With dY = 0 the gradients come from the L1 term alone: dZ = lambda/(T f) on the pattern."""
+    w = wl.make_ffn("l1", "bf16", 200, 512, 1024, seed=5, sparsity=0.95, ell_width=128, with_dy=True)
+    w.dY[:] = 0
+    lam = 1e-3 * w.T * w.f
+    dX, dWu, dWd, bufs, cfg = run_fwd_bwd(w, lam)
+    act = gpu_pattern(bufs, w, cfg)
+    rdX, rdWu, rdWd = oracle_full(w, act, lam)
+    assert np.abs(to_f64(dWd)).max() == 0.0
+    assert rel_l2(to_f64(dWu), rdWu) <= 2e-2
+    assert rel_l2(to_f64(dX), rdX) <= 2e-2
+
+
+def test_backward_deterministic_and_wupt():
+    w = wl.make_ffn("bdet", "bf16", 512, 1024, 2048, seed=8, sparsity=0.98, ell_width=128, with_dy=True)
+    a = run_fwd_bwd(w, 2e-5)
+    c = run_fwd_bwd(w, 2e-5, with_wupt=True)
+    for x, y in zip(a[:3], c[:3]):
+        assert torch.equal(x.view(torch.int16) if x.dtype == torch.bfloat16 else x.view(torch.int32),
+                           y.view(torch.int16) if y.dtype == torch.bfloat16 else y.view(torch.int32))
+
+
+def test_backward_c5_sampled():
+    """Training shape: T=16384, d=4096, f=16384, ~99% sparse, K=256; sampled rows and units."""
+    w = wl.c5_training()
+    lam = 1e-3 * w.T * w.f   # per-element injection 1e-3, visible in bf16
+    dX, dWu, dWd, bufs, cfg = run_fwd_bwd(w, lam)
+    act = gpu_pattern(bufs, w, cfg).tocsc()
+    r = np.random.default_rng(0)
+    X, Wu, Wd, dY = w.as_f64(w.X), w.as_f64(w.W_up), w.as_f64(w.W_down), w.as_f64(w.dY)
+    lamp = lam / (w.T * w.f)
+    # dW for sampled units: needs column n of Z and dH over all tokens
+    units = r.choice(w.f, size=48, replace=False)
+    Zc = X @ Wu[:, units] + w.shift_t[:, None]
+    dHc = dY @ Wd[units].T + lamp
+    A = act[:, units].toarray()
+    dWd_ref = (np.where(A, Zc, 0.0)).T @ dY            # [units, d]
+    dWu_ref = X.T @ np.where(A, dHc, 0.0)              # [d, units]
+    assert rel_l2(to_f64(dWd)[units], dWd_ref) <= 2e-2
+    assert rel_l2(to_f64(dWu)[:, units], dWu_ref) <= 2e-2
+    # dX for sampled rows
+    rows = r.choice(w.T, size=64, replace=False)
+    Ar = act.tocsr()[rows].toarray()
+    dZr = np.where(Ar, dY[rows] @ Wd.T + lamp, 0.0)
+    assert rel_l2(to_f64(dX)[rows], dZr @ Wu.T) <= 2e-2
