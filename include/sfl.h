@@ -127,8 +127,9 @@ typedef struct {
  *  gated     0: y = ReLU(X W_up + b + s) W_down  (eq. secC:eq:non-gated-mlp)
  *            1: y = (ReLU(X W_gate + b + s) * (X W_up)) W_down (eq. sec2:eq:gated-mlp)
  *  W_gate    [d][f], gated only
- *  W_upT     optional [f][d] copy of W_up transposed (read by the gated up-dot);
- *            when NULL the gated path transposes W_up into the workspace
+ *  W_upT     optional [f][d] copy of W_up transposed. Non-gated: the up projection
+ *            reads it instead of W_up (K-contiguous B operand). Gated: read by the fused
+ *            up-dot; when NULL the gated path transposes W_up into the workspace.
  *  W_down_packed  optional bf16 copy of W_down in the slice-major layout written by
  *            sfl_pack_down_weights ([d/64][f][64]); the sparse down projection reads
  *            64-column slices of W_down, and this layout makes each slice one

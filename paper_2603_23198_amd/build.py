@@ -44,10 +44,12 @@ def _compile(src, obj, extra=()):
     return errs
 
 
-def build(verbose=False, jobs=None, extra_flags=(), out=None) -> str:
-    """Compile and link; `extra_flags` go to every hipcc line, `out` overrides the library path."""
+def build(verbose=False, jobs=None, extra_flags=(), out=None, csrc=None) -> str:
+    """Compile and link; `extra_flags` go to every hipcc line, `out` overrides the library
+    path and `csrc` the source directory."""
     lib = out or LIB
-    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
+    src_dir = csrc or CSRC
+    srcs = sorted(glob.glob(os.path.join(src_dir, "*.hip")) + glob.glob(os.path.join(src_dir, "*.cpp")))
     jobs = jobs or min(len(srcs), max(1, (os.cpu_count() or 4)), 16)
     with tempfile.TemporaryDirectory(prefix="sfl_build_") as tmp:
         objs = [os.path.join(tmp, os.path.basename(s) + ".o") for s in srcs]

@@ -265,7 +265,8 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
     for (int i = 1; i < 5; ++i) ev.record(i, s);
     return SFL_OK;
   }
-  const void* Wp = a->gated ? a->W_gate : a->W_up;  // pattern-deciding projection
+  const void* Wp = a->gated ? a->W_gate : a->W_up;        // pattern-deciding projection
+  const void* WpT = a->gated ? nullptr : a->W_upT;         // its transposed copy, if given
 
   // 1. up (or gate) projection with the ReLU -> TwELL epilogue (Alg. 1)
   {
@@ -277,7 +278,7 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
     g.lda = d;
     g.a_bytes = T * d * 2;
     int blay;
-    set_weight_B(g, Wp, nullptr, d, f, &blay);
+    set_weight_B(g, Wp, WpT, d, f, &blay);
     g.bias = a->bias_f;
     g.shift = a->shift_t;
     if (fused_twell(*a)) {
@@ -336,7 +337,7 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
     g.m_count = tw.n_ovf;
     g.count_cap = (int32_t)cap;
     int blay;
-    set_weight_B(g, Wp, nullptr, d, f, &blay);
+    set_weight_B(g, Wp, WpT, d, f, &blay);
     g.bias = a->bias_f;
     g.shift = a->shift_t;
     g.s_rows = tw.ovf_rows;

@@ -104,31 +104,74 @@ __global__ __launch_bounds__(256) void k_gather_down(int64_t T, int64_t d, int K
   }
 }
 
-// bf16 variant with 64-column slices, persistent over the slices of one XCD.
+// bf16 sparse down projection over a slice-major copy of W_down ([d/SLICE][f][SLICE]).
+// A slice (f x 2*SLICE bytes, 2 MiB at f = 16384 and SLICE = 64) is one contiguous block,
+// small enough to stay in one XCD's 4 MiB L2 while the XCD streams every token through it.
 // Workgroup g runs on XCD g % 8 (workgroups are dispatched round-robin over the XCDs);
 // it owns a block of tokens and walks that XCD's slices (x, x+8, x+16, ...) in order,
 // like every other workgroup of the XCD, so the XCD works on about one slice at a time.
-// W is the slice-major copy of W_down ([d/64][f][64]): a slice (f x 128 bytes, 2 MiB at
-// f = 16384) is one contiguous block that stays in the XCD's 4 MiB L2.
-// The block's ELL entries are copied once into LDS (index | bf16 value << 16) and
-// reused for every slice, so the per-token metadata latency is paid once, not per slice.
-// Lane = (group g = lane / 8, part i = lane % 8): the 8 groups each take a different ELL
-// entry and read its 128-byte row segment as 8 x 16 bytes, so one load instruction
-// fetches 8 rows; a token's partial sums are folded over the 8 groups at the end, in a
+// The block's ELL entries are copied once into LDS (index | bf16 value << 16) and reused
+// for every slice, so the per-token metadata latency is paid once, not per slice.
+// Lane = (group g = lane / LPR, part i = lane % LPR): the NGRP groups each take a
+// different ELL entry and read its row segment as LPR x 16 bytes, so one load instruction
+// fetches NGRP rows; a token's partial sums are folded over the groups at the end, in a
 // fixed order.
-constexpr int SLICE2 = 64;
+#ifndef SFL_SLICE
+#define SFL_SLICE 64
+#endif
+constexpr int SLICE2 = SFL_SLICE;      // columns per slice of W_down
+constexpr int LPR = SLICE2 * 2 / 16;   // lanes per row segment (16 bytes each)
+constexpr int NGRP = 64 / LPR;         // row segments per load instruction
 #ifndef SFL_GATHER_WAVES
-#define SFL_GATHER_WAVES 8
+#define SFL_GATHER_WAVES 12
 #endif
 #ifndef SFL_GATHER_UNROLL
 #define SFL_GATHER_UNROLL 8
 #endif
 #ifndef SFL_GATHER_LDS
-#define SFL_GATHER_LDS 65536
+#define SFL_GATHER_LDS 98304
 #endif
 constexpr int GATHER_WAVES = SFL_GATHER_WAVES;
-constexpr int GU = SFL_GATHER_UNROLL;  // row loads in flight per lane
+constexpr int GU = SFL_GATHER_UNROLL;       // row loads in flight per lane
 constexpr int GATHER_LDS = SFL_GATHER_LDS;  // bytes of cached ELL entries per workgroup
+
+// One token's slice: entries er[0..nnz) in LDS, W row segments read through the buffer
+// descriptor at byte offset idx * 2 * SLICE + col_b; on return the lanes of group 0 hold
+// the sums of their 8 columns.
+__device__ __forceinline__ void slice_token(const uint32_t* er, int nnz, __amdgpu_buffer_rsrc_t wr, uint32_t col_b,
+                                            int grp, float (&acc)[8]) {
+  static_assert(GU % 2 == 0, "entries are consumed in pairs");
+  constexpr uint32_t row_b = SLICE2 * 2;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+  for (int q = 0; q < nnz; q += NGRP * GU) {
+    u32x4_t w[GU];
+    uint32_t x[GU];
+#pragma unroll
+    for (int u = 0; u < GU; ++u) {
+      const int e = q + u * NGRP + grp;
+      x[u] = e < nnz ? er[e] : 0u;  // an absent entry has value 0 (and its load reads 0)
+      const uint32_t off = e < nnz ? (x[u] & 0xffffu) * row_b + col_b : 0x80000000u;
+      w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0));
+    }
+    // two entries at a time: (v_a, v_b) . (w_a[c], w_b[c]) with one bf16 dot2 per column
+#pragma unroll
+    for (int u = 0; u < GU; u += 2) {
+      const bf16x2_t vv = __builtin_bit_cast(bf16x2_t, __builtin_amdgcn_perm(x[u + 1], x[u], 0x07060302u));
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bf16x2_t lo = __builtin_bit_cast(bf16x2_t, __builtin_amdgcn_perm(w[u + 1][j], w[u][j], 0x05040100u));
+        const bf16x2_t hi = __builtin_bit_cast(bf16x2_t, __builtin_amdgcn_perm(w[u + 1][j], w[u][j], 0x07060302u));
+        acc[2 * j] = __builtin_amdgcn_fdot2_f32_bf16(vv, lo, acc[2 * j], false);
+        acc[2 * j + 1] = __builtin_amdgcn_fdot2_f32_bf16(vv, hi, acc[2 * j + 1], false);
+      }
+    }
+  }
+#pragma unroll
+  for (int o = LPR; o < 64; o <<= 1)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], o, 64);
+}
 
 __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
     int64_t T, int64_t d, int64_t f, int K, const bf16_t* __restrict__ ell_val, const uint16_t* __restrict__ ell_idx,
@@ -140,7 +183,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
   const int64_t t0 = (int64_t)(blockIdx.x >> 3) * tpw;
   const int l = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int grp = l >> 3, sub = l & 7;
+  const int grp = l / LPR, sub = l % LPR;
   // stage the block's ELL rows in LDS
   for (int i = threadIdx.x; i < tpw; i += blockDim.x) {
     const int64_t t = t0 + i;
@@ -155,41 +198,14 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
   }
   __syncthreads();
   const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc((void*)W, (short)0, 0x7fffffff, 0x00020000);
-  constexpr uint32_t row_b = SLICE2 * 2;
   for (int slice = xcd; slice < n_slices; slice += 8) {
     const int64_t col = (int64_t)slice * SLICE2 + sub * 8;
     const uint32_t col_b = (uint32_t)(slice * f * SLICE2 * 2) + (uint32_t)sub * 16u;
     for (int i = wave; i < tpw; i += GATHER_WAVES) {
       const int nnz = __builtin_amdgcn_readfirstlane(cnt_s[i]);
       if (nnz < 0) continue;
-      const uint32_t* er = ent + i * K;
       float acc[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) acc[j] = 0.f;
-      for (int q = 0; q < nnz; q += 8 * GU) {
-        u32x4_t w[GU];
-        float v[GU];
-#pragma unroll
-        for (int u = 0; u < GU; ++u) {
-          const int e = q + u * 8 + grp;  // entry of this group
-          const uint32_t x = e < nnz ? er[e] : 0u;
-          v[u] = bf16hi(x);
-          const uint32_t off = e < nnz ? (x & 0xffffu) * row_b + col_b : 0x80000000u;
-          w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0));
-        }
-#pragma unroll
-        for (int u = 0; u < GU; ++u)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            acc[2 * j] = fmaf(v[u], bf16lo(w[u][j]), acc[2 * j]);
-            acc[2 * j + 1] = fmaf(v[u], bf16hi(w[u][j]), acc[2 * j + 1]);
-          }
-      }
-      // fold the 8 groups: lanes l, l^8, l^16, l^32 hold partial sums of the same columns
-#pragma unroll
-      for (int o = 8; o < 64; o <<= 1)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], o, 64);
+      slice_token(ent + i * K, nnz, wr, col_b, grp, acc);
       if (grp == 0) {
         u32x4_t out;
 #pragma unroll
@@ -201,7 +217,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
   }
 }
 
-// out[s][n][c] = W[n][64 s + c]: 16 bytes per thread, reads coalesced along rows.
+// out[s][n][c] = W[n][SLICE s + c]: 16 bytes per thread, reads coalesced along rows.
 __global__ __launch_bounds__(256) void k_pack_down(const bf16_t* __restrict__ W, bf16_t* __restrict__ out, int64_t f,
                                                    int64_t d) {
   const int64_t chunks_per_row = d / 8;
@@ -209,7 +225,7 @@ __global__ __launch_bounds__(256) void k_pack_down(const bf16_t* __restrict__ W,
   if (i >= f * chunks_per_row) return;
   const int64_t n = i / chunks_per_row;
   const int64_t c = i - n * chunks_per_row;  // 8-column chunk within the row
-  const int64_t s = c / 8, c8 = c % 8;
+  const int64_t s = c / (SLICE2 / 8), c8 = c % (SLICE2 / 8);
   *(u32x4_t*)(out + ((s * f + n) * SLICE2 + c8 * 8)) = *(const u32x4_t*)(W + n * d + c * 8);
 }
 
@@ -307,6 +323,7 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
   if (T == 0) return hipSuccess;
   if (d % (8 * SLICE2) != 0) return hipErrorInvalidValue;
   const int n_slices = (int)(d / SLICE2);
+
   // tokens per workgroup: what the LDS budget holds, at most 64; a token block goes to
   // every XCD (each XCD covers its own slices), so the grid is 8 x the number of blocks
   const int64_t per_tok = (int64_t)std::max(K, 1) * 4 + 4;

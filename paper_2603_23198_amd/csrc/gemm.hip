@@ -52,7 +52,7 @@ struct LoadKC {
   u32x4_t reg[PER];
   uint32_t boff[PER];  // byte offset of the chunk at k = 0, or kOOB
   __amdgpu_buffer_rsrc_t rs;
-  __device__ void init(const bf16_t* base, int64_t bytes, int64_t ld, const int32_t* rows, int r0, int rlimit,
+  __device__ __forceinline__ void init(const bf16_t* base, int64_t bytes, int64_t ld, const int32_t* rows, int r0, int rlimit,
                        int tid) {
     rs = make_rsrc(base, bytes);
 #pragma unroll
@@ -69,12 +69,12 @@ struct LoadKC {
     }
   }
   // K must be a multiple of 64 here (no K tail); k0 goes in the scalar offset.
-  __device__ void load(int k0, int, int) {
+  __device__ __forceinline__ void load(int k0, int, int) {
 #pragma unroll
     for (int p = 0; p < PER; ++p)
       reg[p] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)boff[p], k0 * 2, 0));
   }
-  __device__ void store(bf16_t* lds, int tid) {
+  __device__ __forceinline__ void store(bf16_t* lds, int tid) {
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int c = tid + p * NTHR;
@@ -100,7 +100,7 @@ struct LoadRC {
   __amdgpu_buffer_rsrc_t rs;
   uint32_t ld2;           // source row stride in bytes
   const int32_t* krows;
-  __device__ void init(const bf16_t* base, int64_t bytes, int64_t ld, const int32_t* kr, int r0, int rlimit,
+  __device__ __forceinline__ void init(const bf16_t* base, int64_t bytes, int64_t ld, const int32_t* kr, int r0, int rlimit,
                        int tid) {
     rs = make_rsrc(base, bytes);
     ld2 = (uint32_t)(ld * 2);
@@ -113,7 +113,7 @@ struct LoadRC {
     const int rc = r < rlimit ? r : rlimit - 2;
     vbase = (uint32_t)((tid / PAIRS) * 8) * ld2 + (uint32_t)rc * 2u;
   }
-  __device__ void load(int k0, int klimit, int tid) {
+  __device__ __forceinline__ void load(int k0, int klimit, int tid) {
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int kl = (tid / PAIRS + p * GSTEP) * 8;  // first k of this job within the tile
@@ -134,7 +134,7 @@ struct LoadRC {
       }
     }
   }
-  __device__ void store(bf16_t* lds, int tid) {
+  __device__ __forceinline__ void store(bf16_t* lds, int tid) {
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int j = tid + p * NTHR;
@@ -178,80 +178,16 @@ __device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, i
   tn = in_group / gm;
 }
 
-template <int ALAY, int BLAY, int EPI>
-__global__ __launch_bounds__(NTHR) void k_gemm_bf16(GemmParams p) {
-  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * LDS_STAGE];
+// ---- epilogue -------------------------------------------------------------------------
+// Accumulator element (i, j, r) of this lane sits at tile row
+//   wm*128 + i*32 + 8*(r/4) + 4*(lane/32) + r%4   and tile column   wn*64 + j*32 + lane%32.
+template <int EPI>
+__device__ __forceinline__ void gemm_epilogue(const GemmParams& p, f32x16_t (&acc)[TM][TN], int m0, int n0,
+                                              int m_eff, bf16_t* smem) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-
-  const int tiles_m = (int)cdiv(p.M, BM), tiles_n = (int)cdiv(p.N, BN);
-  int tm, tn;
-  tile_coords(tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * BM, n0 = tn * BN;
-  const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
-  if (m0 >= m_eff) return;
-  const int k_eff = p.k_count ? min(*p.k_count, p.count_cap) : p.K;
-  if (EPI == EPI_ACCUM_F32 && k_eff <= 0) return;
-
-  typename LoaderSel<ALAY, BM>::type la;
-  typename LoaderSel<BLAY, BN>::type lb;
-  la.init((const bf16_t*)p.A, p.a_bytes, p.lda, p.a_rows, m0, m_eff, tid);
-  lb.init((const bf16_t*)p.B, p.b_bytes, p.ldb, p.b_rows, n0, p.N, tid);
-
-  f32x16_t acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-  const int nk = (int)cdiv(k_eff, BK);
-  if (nk > 0) {
-    la.load(0, k_eff, tid);
-    lb.load(0, k_eff, tid);
-    la.store(smem, tid);
-    lb.store(smem + BM * LDK, tid);
-  }
-  __syncthreads();
-
-  const int arow = wm * WTM + (lane & 31);
-  const int brow = wn * WTN + (lane & 31);
-  const int koff = (lane >> 5) * 8;
-  for (int kt = 0; kt < nk; ++kt) {
-    const bf16_t* As = smem + (kt & 1) * LDS_STAGE;
-    const bf16_t* Bs = As + BM * LDK;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      la.load((kt + 1) * BK, k_eff, tid);
-      lb.load((kt + 1) * BK, k_eff, tid);
-    }
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8_t a[TM], b[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) a[i] = *(const bf16x8_t*)(As + (arow + i * 32) * LDK + ks * 16 + koff);
-#pragma unroll
-      for (int j = 0; j < TN; ++j) b[j] = *(const bf16x8_t*)(Bs + (brow + j * 32) * LDK + ks * 16 + koff);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
-    if (more) {
-      bf16_t* An = smem + ((kt + 1) & 1) * LDS_STAGE;
-      la.store(An, tid);
-      lb.store(An + BM * LDK, tid);
-    }
-    __syncthreads();
-  }
-
-  // ---- epilogue -------------------------------------------------------------------
-  // Accumulator element (i, j, r) of this lane sits at tile row
-  //   wm*128 + i*32 + 8*(r/4) + 4*(lane/32) + r%4   and tile column   wn*64 + j*32 + lane%32.
   if constexpr (EPI == EPI_TWELL) {
     float* stage = (float*)smem;  // 64 rows x 256 fp32 = 64 KB
     const int Tn = p.tile_cols, S = p.tile_slots, NT = p.n_tiles;
@@ -352,6 +288,227 @@ __global__ __launch_bounds__(NTHR) void k_gemm_bf16(GemmParams p) {
 }
 
 template <int ALAY, int BLAY, int EPI>
+__global__ __launch_bounds__(NTHR) void k_gemm_bf16(GemmParams p) {
+  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * LDS_STAGE];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+
+  const int tiles_m = (int)cdiv(p.M, BM), tiles_n = (int)cdiv(p.N, BN);
+  int tm, tn;
+  tile_coords(tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
+  if (m0 >= m_eff) return;
+  const int k_eff = p.k_count ? min(*p.k_count, p.count_cap) : p.K;
+  if (EPI == EPI_ACCUM_F32 && k_eff <= 0) return;
+
+  typename LoaderSel<ALAY, BM>::type la;
+  typename LoaderSel<BLAY, BN>::type lb;
+  la.init((const bf16_t*)p.A, p.a_bytes, p.lda, p.a_rows, m0, m_eff, tid);
+  lb.init((const bf16_t*)p.B, p.b_bytes, p.ldb, p.b_rows, n0, p.N, tid);
+
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int nk = (int)cdiv(k_eff, BK);
+  if (nk > 0) {
+    la.load(0, k_eff, tid);
+    lb.load(0, k_eff, tid);
+    la.store(smem, tid);
+    lb.store(smem + BM * LDK, tid);
+  }
+  __syncthreads();
+
+  const int arow = wm * WTM + (lane & 31);
+  const int brow = wn * WTN + (lane & 31);
+  const int koff = (lane >> 5) * 8;
+  for (int kt = 0; kt < nk; ++kt) {
+    const bf16_t* As = smem + (kt & 1) * LDS_STAGE;
+    const bf16_t* Bs = As + BM * LDK;
+    const bool more = kt + 1 < nk;
+    if (more) {
+      la.load((kt + 1) * BK, k_eff, tid);
+      lb.load((kt + 1) * BK, k_eff, tid);
+    }
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      bf16x8_t a[TM], b[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) a[i] = *(const bf16x8_t*)(As + (arow + i * 32) * LDK + ks * 16 + koff);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) b[j] = *(const bf16x8_t*)(Bs + (brow + j * 32) * LDK + ks * 16 + koff);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    if (more) {
+      bf16_t* An = smem + ((kt + 1) & 1) * LDS_STAGE;
+      la.store(An, tid);
+      lb.store(An + BM * LDK, tid);
+    }
+    __syncthreads();
+  }
+
+  gemm_epilogue<EPI>(p, acc, m0, n0, m_eff, smem);
+}
+
+// ---- K-contiguous x K-contiguous GEMM with direct global -> LDS loads -------------------
+// Both operands K-contiguous (A [M][K], B [N][K]). Global reads go straight into LDS
+// (buffer loads with the LDS destination, 16 bytes per lane, no staging registers), which
+// lets the K loop keep V2_STAGES - 1 stages of 32 k in flight: the tiles the MFMAs read at
+// step kt were requested V2_STAGES - 1 steps earlier, enough to hide misses that go past
+// L2. A stage holds [256 rows][32 k] of each operand, 64 bytes per row; the 16-byte chunk
+// c of row r is stored at chunk position c ^ ((r >> 2) & 3), which makes the fragment
+// reads (32 rows, one chunk each) and the 1 KB per-instruction writes bank-conflict free.
+constexpr int V2_BK = 32;
+constexpr int V2_STAGES = 4;
+constexpr int V2_OPER = BM * V2_BK;                // bf16 elements per operand per stage
+constexpr int V2_STAGE = 2 * V2_OPER;              // A then B
+constexpr int V2_LDS = V2_STAGES * V2_STAGE * 2;   // bytes
+static_assert(V2_LDS >= 64 * BN * 4, "the TwELL epilogue stages 64 rows of fp32 in the same LDS");
+constexpr int V2_LOADS = V2_OPER * 2 / 1024 / NWAVES;  // 1 KB load instructions per operand per wave
+
+__device__ __forceinline__ int v2_swz(int row, int chunk) { return chunk ^ ((row >> 2) & 3); }
+
+// 16 bytes per lane from a buffer straight into LDS at lds_off + 16 * lane. Written as
+// inline assembly: the compiler does not count these loads and so does not make every
+// later LDS read wait for all of them (with several stages in flight it cannot tell which
+// stage a read touches); the K loop waits for them itself (s_waitcnt vmcnt) and orders
+// them with barriers. Counting stays safe for the compiler's own loads: loads complete
+// in order, so extra loads in flight only make its waits stricter.
+// The four descriptor words of make_rsrc, for inline assembly operands.
+__device__ __forceinline__ u32x4_t rsrc_words(const void* base, int64_t bytes) {
+  const uint64_t a = (uint64_t)(uintptr_t)base;
+  const uint32_t n = bytes > 0x7fffffff ? 0x7fffffffu : (uint32_t)bytes;
+  u32x4_t w;
+  w[0] = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  w[1] = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32) & 0xffffu);  // stride 0
+  w[2] = n;
+  w[3] = 0x00020000u;
+  return w;
+}
+
+__device__ __forceinline__ void load_lds16(u32x4_t rsrc, uint32_t lds_off, uint32_t voff, uint32_t soff) {
+  asm volatile("buffer_load_dwordx4 %0, %1, %2 offen lds"
+               :
+               : "v"(voff), "s"(rsrc), "s"(soff), "{m0}"(lds_off)
+               : "memory");
+}
+
+template <int EPI>
+__global__ __launch_bounds__(NTHR) void k_gemm_bf16_v2(GemmParams p) {
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[V2_STAGES * V2_STAGE];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+  const int tiles_m = (int)cdiv(p.M, BM), tiles_n = (int)cdiv(p.N, BN);
+  int tm, tn;
+  tile_coords(tiles_m, tiles_n, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
+  if (m0 >= m_eff) return;
+
+  // Per load instruction q of this wave: rows (wave*V2_LOADS + q)*16 + lane/4 of the
+  // operand tile, LDS chunk position lane%4, which holds logical chunk (lane%4) ^ swz.
+  const u32x4_t ra = rsrc_words(p.A, p.a_bytes);
+  const u32x4_t rb = rsrc_words(p.B, p.b_bytes);
+  uint32_t offa[V2_LOADS], offb[V2_LOADS];
+#pragma unroll
+  for (int q = 0; q < V2_LOADS; ++q) {
+    const int row = (wave * V2_LOADS + q) * 16 + (lane >> 2);
+    const int c = v2_swz(row, lane & 3);
+    const int ga = m0 + row, gb = n0 + row;
+    const int64_t sa = ga < m_eff ? (p.a_rows ? (int64_t)p.a_rows[ga] : (int64_t)ga) : -1;
+    offa[q] = sa >= 0 ? (uint32_t)((sa * p.lda + c * 8) * 2) : kOOB;
+    offb[q] = gb < p.N ? (uint32_t)(((int64_t)gb * p.ldb + c * 8) * 2) : kOOB;
+  }
+  // stage kt of the K loop into `st` (beyond the last stage every lane is out of range, so
+  // the loads only keep the number in flight uniform)
+  auto issue = [&](bf16_t* st, int kt) {
+    const int so = kt * V2_BK * 2;
+    const bool live = kt * V2_BK < p.K;
+#pragma unroll
+    for (int q = 0; q < V2_LOADS; ++q) {
+      bf16_t* da = st + (wave * V2_LOADS + q) * 16 * V2_BK;
+      const uint32_t la = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16_t*)da;
+      const uint32_t lb = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16_t*)(da + V2_OPER);
+      load_lds16(ra, __builtin_amdgcn_readfirstlane(la), live ? offa[q] : kOOB, (uint32_t)so);
+      load_lds16(rb, __builtin_amdgcn_readfirstlane(lb), live ? offb[q] : kOOB, (uint32_t)so);
+    }
+  };
+
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int arow = wm * WTM + (lane & 31);
+  const int brow = wn * WTN + (lane & 31);
+  auto compute = [&](const bf16_t* As) {
+    const bf16_t* Bs = As + V2_OPER;
+#pragma unroll
+    for (int ks = 0; ks < V2_BK / 16; ++ks) {
+      const int c = ks * 2 + (lane >> 5);
+      bf16x8_t a[TM], b[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int r = arow + i * 32;
+        a[i] = *(const bf16x8_t*)(As + r * V2_BK + v2_swz(r, c) * 8);
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int r = brow + j * 32;
+        b[j] = *(const bf16x8_t*)(Bs + r * V2_BK + v2_swz(r, c) * 8);
+      }
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  };
+  // Before each step: this wave's loads for the stage about to be read are the oldest in
+  // flight, the (V2_STAGES - 2) stages issued after them may stay outstanding; its LDS
+  // reads of the previous step have completed (lgkmcnt 0), so after the barrier the slot
+  // they read can be refilled.
+  constexpr int later = (V2_STAGES - 2) * 2 * V2_LOADS;
+  constexpr int wait_imm = (later & 15) | (7 << 4) | (0 << 8) | ((later >> 4) << 14);
+  const int nk = (int)cdiv(p.K, V2_BK);
+#pragma unroll
+  for (int st = 0; st < V2_STAGES - 1; ++st) issue(smem + st * V2_STAGE, st);
+  for (int kt = 0; kt < nk; ++kt) {
+    __builtin_amdgcn_s_waitcnt(wait_imm);
+    __syncthreads();
+    issue(smem + ((kt + V2_STAGES - 1) % V2_STAGES) * V2_STAGE, kt + V2_STAGES - 1);
+    compute(smem + (kt % V2_STAGES) * V2_STAGE);
+  }
+  __builtin_amdgcn_s_waitcnt(0);  // the trailing out-of-range loads also write LDS
+  __syncthreads();
+  gemm_epilogue<EPI>(p, acc, m0, n0, m_eff, smem);
+}
+
+template <int EPI>
+hipError_t launch_bf16_v2(const GemmParams& p, hipStream_t s) {
+  const int tiles = (int)(cdiv(p.M, BM) * cdiv(p.N, BN));
+  if (tiles == 0) return hipSuccess;
+  hipLaunchKernelGGL((k_gemm_bf16_v2<EPI>), dim3(tiles), dim3(NTHR), 0, s, p);
+  return hipGetLastError();
+}
+
+template <int ALAY, int BLAY, int EPI>
 hipError_t launch_bf16(const GemmParams& p, hipStream_t s) {
   const int tiles = (int)(cdiv(p.M, BM) * cdiv(p.N, BN));
   if (tiles == 0) return hipSuccess;
@@ -428,6 +585,17 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmParams p) {
 }  // namespace
 
 hipError_t gemm_bf16(int alay, int blay, int epi, const GemmParams& p, hipStream_t s) {
+  if (alay == LAY_KC && blay == LAY_KC && p.K % V2_BK == 0 && !p.k_count && !p.b_rows) {
+    switch (epi) {
+      case EPI_TWELL: return launch_bf16_v2<EPI_TWELL>(p, s);
+      case EPI_F32: return launch_bf16_v2<EPI_F32>(p, s);
+      case EPI_ACT_RELU: return launch_bf16_v2<EPI_ACT_RELU>(p, s);
+      case EPI_ACT: return launch_bf16_v2<EPI_ACT>(p, s);
+      case EPI_MASKGRAD: return launch_bf16_v2<EPI_MASKGRAD>(p, s);
+      case EPI_MUL_ACT: return launch_bf16_v2<EPI_MUL_ACT>(p, s);
+      default: break;
+    }
+  }
 #define SFL_CASE(A_, B_, E_) \
   if (alay == A_ && blay == B_ && epi == E_) return launch_bf16<A_, B_, E_>(p, s);
   // forward: X W_up (B row-contiguous [d][f]) with TwELL / f32 / ReLU epilogues

@@ -241,3 +241,28 @@ def test_packed_down_weights_layout_and_equivalence():
     assert torch.equal(Y1.view(torch.int16), Y2.view(torch.int16))
     Yref, _ = oracle_rows(w, np.arange(w.T))
     assert rel_l2(to_f64(Y1), Yref) <= 2e-2
+
+
+@pytest.mark.parametrize("T,d,f", [(777, 512, 2048), (8192, 4096, 16384)])
+def test_transposed_up_weights_give_identical_results(T, d, f):
+    """With W_up^T the up projection runs the direct-to-LDS GEMM; its MFMA sequence per
+    output element is the same, so Z, the TwELL and Y are bit-identical."""
+    w = wl.make_ffn("wupt", "bf16", T, d, f, seed=13, sparsity=0.99, ell_width=256)
+    Y1, b1, _, cfg = run_forward(w)
+    Y2, b2, _, _ = run_forward(w, use_wupt=True)
+    assert torch.equal(Y1.view(torch.int16), Y2.view(torch.int16))
+    for k in ("cnt", "row_nnz", "row_ovf"):
+        assert torch.equal(b1[k], b2[k]), k
+    g1, g2 = twell_views(b1, T, f, cfg), twell_views(b2, T, f, cfg)
+    S = cfg.tile_slots
+    for j in range(g1["cnt"].shape[1]):
+        nv = np.minimum(g1["cnt"][:, j], S)
+        for s_ in range(S):
+            sel = np.nonzero(nv > s_)[0]
+            if len(sel) == 0:
+                break
+            np.testing.assert_array_equal(g1["idx"][sel, j * S + s_], g2["idx"][sel, j * S + s_])
+            np.testing.assert_array_equal(g1["val"][sel, j * S + s_], g2["val"][sel, j * S + s_])
+    rows = sample_rows(T, 64, 5)
+    Yref, _ = oracle_rows(w, rows)
+    assert rel_l2(to_f64(Y2)[rows], Yref) <= 2e-2
