@@ -127,9 +127,11 @@ typedef struct {
  *  gated     0: y = ReLU(X W_up + b + s) W_down  (eq. secC:eq:non-gated-mlp)
  *            1: y = (ReLU(X W_gate + b + s) * (X W_up)) W_down (eq. sec2:eq:gated-mlp)
  *  W_gate    [d][f], gated only
- *  W_upT     optional [f][d] copy of W_up transposed. Non-gated: the up projection
- *            reads it instead of W_up (K-contiguous B operand). Gated: read by the fused
- *            up-dot; when NULL the gated path transposes W_up into the workspace.
+ *  W_upT     optional [f][d] copy of W_up transposed (bf16 only; ignored for F32).
+ *            Non-gated: the up projection reads it instead of W_up (K-contiguous B
+ *            operand). Gated: read by the fused up-dot; when NULL the gated path
+ *            transposes W_up into the workspace. sfl_dense_ffn_baseline reads it for
+ *            its X W_up GEMM the same way.
  *  W_down_packed  optional bf16 copy of W_down in the slice-major layout written by
  *            sfl_pack_down_weights ([d/64][f][64]); the sparse down projection reads
  *            64-column slices of W_down, and this layout makes each slice one
@@ -240,7 +242,7 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* args, sfl_stream_t stream);
 
 /* The pre-activation Z = X W + b + s of the forward's up (or gate) projection,
  * as float32 [T][f], computed by the same GEMM main loop as sfl_ffn_forward.
- * Uses args->{dtype, gated, T, d, f, X, W_up or W_gate, bias_f, shift_t}. */
+ * Uses args->{dtype, gated, T, d, f, X, W_up or W_gate, W_upT, bias_f, shift_t}. */
 sfl_status_t sfl_up_projection(const sfl_ffn_args_t* args, float* Z, sfl_stream_t stream);
 
 /* Sparse FFN backward (see sfl_ffn_bwd_args_t). BF16 only. */

@@ -24,6 +24,9 @@ FLAGS = [
     # keep the compiler from emitting packed fp32 arithmetic (v_pk_* f32)
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-munsafe-fp-atomics",
+    # the GEMM epilogues index their accumulator arrays from fully unrolled loops; let the
+    # unroller expand them however large, so the arrays stay in registers
+    "-mllvm", "-pragma-unroll-threshold=1000000",
     "-Wno-unused-result",
 ]
 

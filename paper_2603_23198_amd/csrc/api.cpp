@@ -234,7 +234,7 @@ sfl_status_t sfl_up_projection(const sfl_ffn_args_t* a, float* Z, sfl_stream_t s
   if (a->gated)
     set_weight_B(g, a->W_gate, nullptr, a->d, a->f, &blay);
   else
-    set_weight_B(g, a->W_up, nullptr, a->d, a->f, &blay);
+    set_weight_B(g, a->W_up, a->dtype == SFL_BF16 ? a->W_upT : nullptr, a->d, a->f, &blay);
   g.bias = a->bias_f;
   g.shift = a->shift_t;
   g.C = Z;
@@ -266,7 +266,7 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
     return SFL_OK;
   }
   const void* Wp = a->gated ? a->W_gate : a->W_up;        // pattern-deciding projection
-  const void* WpT = a->gated ? nullptr : a->W_upT;         // its transposed copy, if given
+  const void* WpT = a->gated || a->dtype != SFL_BF16 ? nullptr : a->W_upT;  // its transposed copy, if given
 
   // 1. up (or gate) projection with the ReLU -> TwELL epilogue (Alg. 1)
   {
@@ -391,7 +391,8 @@ sfl_status_t sfl_dense_ffn_baseline(const sfl_ffn_args_t* a, sfl_stream_t stream
   g.lda = d;
   g.a_bytes = T * d * 2;
   int blay;
-  set_weight_B(g, a->gated ? a->W_gate : a->W_up, nullptr, d, f, &blay);
+  const bool bf = a->dtype == SFL_BF16;
+  set_weight_B(g, a->gated ? a->W_gate : a->W_up, a->gated || !bf ? nullptr : a->W_upT, d, f, &blay);
   g.bias = a->bias_f;
   g.shift = a->shift_t;
   g.C = a->workspace;
@@ -401,7 +402,7 @@ sfl_status_t sfl_dense_ffn_baseline(const sfl_ffn_args_t* a, sfl_stream_t stream
     GemmParams u = g;
     u.bias = nullptr;
     u.shift = nullptr;
-    set_weight_B(u, a->W_up, nullptr, d, f, &blay);
+    set_weight_B(u, a->W_up, a->W_upT, d, f, &blay);
     SFL_HIP(gemm_bf16(LAY_KC, blay, EPI_MUL_ACT, u, s));
   }
   ev.record(1, s);

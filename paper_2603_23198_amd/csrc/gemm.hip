@@ -179,85 +179,147 @@ __device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, i
 }
 
 // ---- epilogue -------------------------------------------------------------------------
-// Accumulator element (i, j, r) of this lane sits at tile row
-//   wm*128 + i*32 + 8*(r/4) + 4*(lane/32) + r%4   and tile column   wn*64 + j*32 + lane%32.
-template <int EPI>
-__device__ __forceinline__ void gemm_epilogue(const GemmParams& p, f32x16_t (&acc)[TM][TN], int m0, int n0,
-                                              int m_eff, bf16_t* smem) {
+// Accumulator geometry of one MFMA output block (FM x FM) per lane: register r of lane l
+// holds row row(r, l) and column col(l). A row's columns of one register sit in one
+// group of GL consecutive lanes, so a ballot masked to the lane's group gives that row's
+// active columns among GL.
+template <int FM> struct AccGeo;
+template <> struct AccGeo<32> {  // v_mfma_f32_32x32x16_bf16
+  typedef f32x16_t acc_t;
+  static constexpr int R = 16, GL = 32;
+  static __device__ __forceinline__ int row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
+  static __device__ __forceinline__ int col(int lane) { return lane & 31; }
+  static __device__ __forceinline__ uint64_t group(int lane) { return (lane >> 5) ? 0xffffffff00000000ull : 0xffffffffull; }
+};
+template <> struct AccGeo<16> {  // v_mfma_f32_16x16x32_bf16
+  typedef f32x4_t acc_t;
+  static constexpr int R = 4, GL = 16;
+  static __device__ __forceinline__ int row(int r, int lane) { return 4 * (lane >> 4) + r; }
+  static __device__ __forceinline__ int col(int lane) { return lane & 15; }
+  static __device__ __forceinline__ uint64_t group(int lane) { return 0xffffull << (lane & 48); }
+};
+
+// With WM_ x WN_ waves, wave (wm, wn) holds the WTM_ x WTN_ block of the tile at
+// (wm*WTM_, wn*WTN_), as TM_ x TN_ MFMA blocks of FM x FM.
+template <int WM_, int WN_, int FM>
+struct WaveTile {
+  static constexpr int WTM_ = BM / WM_, WTN_ = BN / WN_, TM_ = WTM_ / FM, TN_ = WTN_ / FM;
+  typedef typename AccGeo<FM>::acc_t acc_t;
+  typedef acc_t Acc[TM_][TN_];
+};
+
+// TwELL epilogue (Alg. 1), straight from the accumulators: z = acc + bias + shift; per
+// register, a ballot of the active lanes masked to the lane's group gives one row's active
+// columns, and mbcnt of it the slot of each (ascending column order). A TwELL tile wider
+// than a wave's columns continues in the next wave(s) along N: each wave first publishes
+// its per-row active counts in LDS and starts from the sum of the counts of the waves left
+// of it in the same tile. Active means z > 0 and not NaN on the fp32 value.
+template <int WM_, int WN_, int FM>
+__device__ __forceinline__ void twell_epilogue(const GemmParams& p, const typename WaveTile<WM_, WN_, FM>::Acc& acc,
+                                               int m0, int n0, int m_eff, bf16_t* smem) {
+  typedef WaveTile<WM_, WN_, FM> W;
+  typedef AccGeo<FM> G;
+  constexpr int NT_ = WM_ * WN_ * 64;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-  if constexpr (EPI == EPI_TWELL) {
-    float* stage = (float*)smem;  // 64 rows x 256 fp32 = 64 KB
-    const int Tn = p.tile_cols, S = p.tile_slots, NT = p.n_tiles;
-    bf16_t* tval = (bf16_t*)p.tw_val;
+  const int wm = wave / WN_, wn = wave % WN_;
+  const uint64_t gmask = G::group(lane);
+  const bool leader = (lane % G::GL) == 0;
+  float* sh_lds = (float*)smem;              // [BM] row shifts of the tile
+  int* cnt_lds = (int*)smem + BM;            // [WN_][BM] per-wave row counts
+  for (int r = tid; r < BM; r += NT_) {
+    const int g = m0 + r;
+    float s = 0.f;
+    if (p.shift && g < m_eff) s = p.shift[p.s_rows ? p.s_rows[g] : g];
+    sh_lds[r] = s;
+  }
+  __syncthreads();
+  const int Tn = p.tile_cols, S = p.tile_slots, NT = p.n_tiles;
+  const int wcol0 = n0 + wn * W::WTN_;  // first column of this wave
+  float bj[W::TN_];
 #pragma unroll
-    for (int pass = 0; pass < 4; ++pass) {
-      if (wm == pass / 2) {
+  for (int j = 0; j < W::TN_; ++j) {
+    const int gc = wcol0 + j * FM + G::col(lane);
+    bj[j] = (p.bias && gc < p.N) ? p.bias[gc] : 0.f;
+  }
+  const bool spans = Tn > W::WTN_;  // uniform; tiles then start on wave boundaries
+  if (spans) {
 #pragma unroll
-        for (int ii = 0; ii < 2; ++ii) {
-          const int i = (pass % 2) * 2 + ii;
+    for (int i = 0; i < W::TM_; ++i)
 #pragma unroll
-          for (int j = 0; j < TN; ++j) {
-            const int col = wn * WTN + j * 32 + (lane & 31);
-            const int gcol = n0 + col;
-            const float b = (p.bias && gcol < p.N) ? p.bias[gcol] : 0.f;
+      for (int r = 0; r < G::R; ++r) {
+        const int lrow = wm * W::WTM_ + i * FM + G::row(r, lane);
+        const float sh = sh_lds[lrow];
+        int c = 0;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const int row = i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);  // within the wave's 128
-              const int lrow = (wm * WTM + row) - pass * 64;
-              const int grow = m0 + wm * WTM + row;
-              float sh = 0.f;
-              if (p.shift && grow < m_eff) sh = p.shift[p.s_rows ? p.s_rows[grow] : grow];
-              stage[lrow * BN + col] = (acc[i][j][r] + b) + sh;
-            }
-          }
+        for (int j = 0; j < W::TN_; ++j) {
+          const bool act = wcol0 + j * FM + G::col(lane) < p.N && active_bits((acc[i][j][r] + bj[j]) + sh);
+          c += __popcll(ballot(act) & gmask);
         }
+        if (leader) cnt_lds[wn * BM + lrow] = c;
       }
-      __syncthreads();
-      // compaction: each wave handles 64 / NWAVES consecutive rows of this pass
-      for (int rr = 0; rr < 64 / NWAVES; ++rr) {
-        const int lrow = wave * (64 / NWAVES) + rr;
-        const int grow = m0 + pass * 64 + lrow;
-        if (grow >= m_eff) break;
-        int running = 0;
-        const int64_t rbase = (int64_t)grow * NT * S;
+  }
+  __syncthreads();
+  const int wpt = spans ? Tn / W::WTN_ : 1;  // waves per TwELL tile
+  const int first_w = wn - wn % wpt;
+  const bool last_w = wn % wpt == wpt - 1;
+  bf16_t* tval = (bf16_t*)p.tw_val;
 #pragma unroll
-        for (int ch = 0; ch < BN / 64; ++ch) {
-          const int col = ch * 64 + lane;
-          const int gcol = n0 + col;
-          const float z = stage[lrow * BN + col];
-          const bool act = gcol < p.N && active_bits(z);
-          const uint64_t m = ballot(act);
-          if ((ch * 64) % Tn == 0) running = 0;
-          const int jt = gcol / Tn;  // same for all lanes of this chunk
-          const int slot = running + mbcnt(m);
-          if (act && slot < S) {
-            tval[rbase + (int64_t)jt * S + slot] = f32_to_bf16(z);
-            p.tw_idx[rbase + (int64_t)jt * S + slot] = (uint16_t)gcol;
-          }
-          running += __popcll(m);
-          const int tile_start = (n0 + ch * 64) / Tn * Tn;
-          const bool tile_end = ((ch * 64 + 64) % Tn == 0) || ch == BN / 64 - 1;
-          if (tile_end && lane == 0 && tile_start < p.N) p.tw_cnt[(int64_t)grow * NT + jt] = running;
+  for (int i = 0; i < W::TM_; ++i)
+#pragma unroll
+    for (int r = 0; r < G::R; ++r) {
+      const int lrow = wm * W::WTM_ + i * FM + G::row(r, lane);
+      const int grow = m0 + lrow;
+      const bool rok = grow < m_eff;
+      const float sh = sh_lds[lrow];
+      int run = 0;
+      for (int w = first_w; w < wn; ++w) run += cnt_lds[w * BM + lrow];
+      const int64_t rbase = (int64_t)grow * NT * S;
+#pragma unroll
+      for (int j = 0; j < W::TN_; ++j) {
+        const int cb = wcol0 + j * FM;  // first column of this block
+        if (!spans && cb % Tn == 0) run = 0;
+        const int gc = cb + G::col(lane);
+        const float z = (acc[i][j][r] + bj[j]) + sh;
+        const bool act = gc < p.N && active_bits(z);
+        const uint64_t m = ballot(act) & gmask;
+        const int slot = run + mbcnt(m);
+        const int jt = cb / Tn;
+        if (act && rok && slot < S) {
+          tval[rbase + (int64_t)jt * S + slot] = f32_to_bf16(z);
+          p.tw_idx[rbase + (int64_t)jt * S + slot] = (uint16_t)gc;
         }
+        run += __popcll(m);
+        const bool tend = spans ? (last_w && j == W::TN_ - 1) : ((cb + FM) % Tn == 0);
+        if (tend && leader && rok && jt * Tn < p.N) p.tw_cnt[(int64_t)grow * NT + jt] = run;
       }
-      __syncthreads();
     }
+}
+
+template <int EPI, int WM_, int WN_, int FM>
+__device__ __forceinline__ void gemm_epilogue(const GemmParams& p, const typename WaveTile<WM_, WN_, FM>::Acc& acc,
+                                              int m0, int n0, int m_eff, bf16_t* smem) {
+  typedef WaveTile<WM_, WN_, FM> W;
+  typedef AccGeo<FM> G;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave / WN_, wn = wave % WN_;
+  if constexpr (EPI == EPI_TWELL) {
+    twell_epilogue<WM_, WN_, FM>(p, acc, m0, n0, m_eff, smem);
   } else {
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
+    for (int i = 0; i < W::TM_; ++i) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * WTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      for (int r = 0; r < G::R; ++r) {
+        const int row = m0 + wm * W::WTM_ + i * FM + G::row(r, lane);
         if (row >= m_eff) continue;
         const int64_t crow = p.c_rows ? (int64_t)p.c_rows[row] : (int64_t)row;
         float sh = 0.f;
         if ((EPI == EPI_F32 || EPI == EPI_ACT_RELU) && p.shift) sh = p.shift[p.s_rows ? p.s_rows[row] : row];
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const int col = n0 + wn * WTN + j * 32 + (lane & 31);
+        for (int j = 0; j < W::TN_; ++j) {
+          const int col = n0 + wn * W::WTN_ + j * FM + G::col(lane);
           if (col >= p.N) continue;
           float v = acc[i][j][r];
           if (EPI == EPI_F32 || EPI == EPI_ACT_RELU) {
@@ -286,7 +348,6 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, f32x16_t (&ac
     }
   }
 }
-
 template <int ALAY, int BLAY, int EPI>
 __global__ __launch_bounds__(NTHR) void k_gemm_bf16(GemmParams p) {
   __shared__ __attribute__((aligned(16))) bf16_t smem[2 * LDS_STAGE];
@@ -358,34 +419,31 @@ __global__ __launch_bounds__(NTHR) void k_gemm_bf16(GemmParams p) {
     __syncthreads();
   }
 
-  gemm_epilogue<EPI>(p, acc, m0, n0, m_eff, smem);
+  gemm_epilogue<EPI, WAVES_M, WAVES_N, 32>(p, acc, m0, n0, m_eff, smem);
 }
 
-// ---- K-contiguous x K-contiguous GEMM with direct global -> LDS loads -------------------
-// Both operands K-contiguous (A [M][K], B [N][K]). Global reads go straight into LDS
-// (buffer loads with the LDS destination, 16 bytes per lane, no staging registers), which
-// lets the K loop keep V2_STAGES - 1 stages of 32 k in flight: the tiles the MFMAs read at
-// step kt were requested V2_STAGES - 1 steps earlier, enough to hide misses that go past
-// L2. A stage holds [256 rows][32 k] of each operand, 64 bytes per row; the 16-byte chunk
-// c of row r is stored at chunk position c ^ ((r >> 2) & 3), which makes the fragment
-// reads (32 rows, one chunk each) and the 1 KB per-instruction writes bank-conflict free.
-constexpr int V2_BK = 32;
-constexpr int V2_STAGES = 4;
-constexpr int V2_OPER = BM * V2_BK;                // bf16 elements per operand per stage
-constexpr int V2_STAGE = 2 * V2_OPER;              // A then B
-constexpr int V2_LDS = V2_STAGES * V2_STAGE * 2;   // bytes
-static_assert(V2_LDS >= 64 * BN * 4, "the TwELL epilogue stages 64 rows of fp32 in the same LDS");
-constexpr int V2_LOADS = V2_OPER * 2 / 1024 / NWAVES;  // 1 KB load instructions per operand per wave
+// ---- K-contiguous x K-contiguous GEMM: direct global -> LDS loads, 16x16x32 MFMAs -------
+// Both operands K-contiguous (A [M][K] with optional row gather, B [N][K]), K % 64 == 0.
+// 8 waves, 4 along M x 2 along N, 64 x 128 outputs each as 4 x 8 blocks of
+// v_mfma_f32_16x16x32_bf16 (this shape retires more flops per cycle on gfx950 than the
+// 32x32x16 one). Global reads go straight into LDS (buffer loads with the LDS
+// destination, 16 bytes per lane, no staging registers), two stages of 64 k: the loads of
+// stage kt+1 are in flight while the MFMAs consume stage kt. A stage holds [256 rows]
+// [64 k] per operand, 128 bytes per row; chunk c (8 k) of row r is stored at chunk
+// position c ^ (r & 7), so the fragment reads (16 rows, one chunk each, per lane group)
+// are bank-conflict free; each load instruction writes one contiguous 1 KB. The waves
+// raise their issue priority around MFMA bursts so that the waves still issuing loads or
+// LDS reads do not starve the matrix pipe.
+constexpr int KC_BK = 64;
+constexpr int KC_OPER = BM * KC_BK;              // bf16 elements per operand per stage
+constexpr int KC_STAGE = 2 * KC_OPER;            // A then B
+constexpr int KC_WM = 4, KC_WN = 2, KC_FM = 16;
+constexpr int KC_LOADS = KC_OPER * 2 / 1024 / NWAVES;  // 1 KB load instructions per operand per wave
+static_assert(2 * KC_STAGE * 2 >= (BM + KC_WN * BM) * 4, "TwELL epilogue scratch fits in the stage buffers");
 
-__device__ __forceinline__ int v2_swz(int row, int chunk) { return chunk ^ ((row >> 2) & 3); }
+__device__ __forceinline__ int kc_swz(int row, int chunk) { return chunk ^ (row & 7); }
 
-// 16 bytes per lane from a buffer straight into LDS at lds_off + 16 * lane. Written as
-// inline assembly: the compiler does not count these loads and so does not make every
-// later LDS read wait for all of them (with several stages in flight it cannot tell which
-// stage a read touches); the K loop waits for them itself (s_waitcnt vmcnt) and orders
-// them with barriers. Counting stays safe for the compiler's own loads: loads complete
-// in order, so extra loads in flight only make its waits stricter.
-// The four descriptor words of make_rsrc, for inline assembly operands.
+// The four descriptor words of a raw buffer resource, for inline assembly operands.
 __device__ __forceinline__ u32x4_t rsrc_words(const void* base, int64_t bytes) {
   const uint64_t a = (uint64_t)(uintptr_t)base;
   const uint32_t n = bytes > 0x7fffffff ? 0x7fffffffu : (uint32_t)bytes;
@@ -397,6 +455,11 @@ __device__ __forceinline__ u32x4_t rsrc_words(const void* base, int64_t bytes) {
   return w;
 }
 
+// 16 bytes per lane from a buffer straight into LDS at lds_off + 16 * lane. Written as
+// inline assembly: the compiler does not count these loads and so does not make every
+// later LDS read wait for all of them; the K loop waits for them itself (s_waitcnt vmcnt)
+// and orders them with barriers. Counting stays safe for the compiler's own loads: loads
+// complete in order, so extra loads in flight only make its waits stricter.
 __device__ __forceinline__ void load_lds16(u32x4_t rsrc, uint32_t lds_off, uint32_t voff, uint32_t soff) {
   asm volatile("buffer_load_dwordx4 %0, %1, %2 offen lds"
                :
@@ -405,12 +468,13 @@ __device__ __forceinline__ void load_lds16(u32x4_t rsrc, uint32_t lds_off, uint3
 }
 
 template <int EPI>
-__global__ __launch_bounds__(NTHR) void k_gemm_bf16_v2(GemmParams p) {
-  __shared__ __attribute__((aligned(1024))) bf16_t smem[V2_STAGES * V2_STAGE];
+__global__ __launch_bounds__(NTHR) void k_gemm_kc(GemmParams p) {
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * KC_STAGE];
+  typedef WaveTile<KC_WM, KC_WN, KC_FM> W;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+  const int wm = wave / KC_WN, wn = wave % KC_WN;
   const int tiles_m = (int)cdiv(p.M, BM), tiles_n = (int)cdiv(p.N, BN);
   int tm, tn;
   tile_coords(tiles_m, tiles_n, tm, tn);
@@ -418,96 +482,93 @@ __global__ __launch_bounds__(NTHR) void k_gemm_bf16_v2(GemmParams p) {
   const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
   if (m0 >= m_eff) return;
 
-  // Per load instruction q of this wave: rows (wave*V2_LOADS + q)*16 + lane/4 of the
-  // operand tile, LDS chunk position lane%4, which holds logical chunk (lane%4) ^ swz.
+  // Load instruction q of this wave fills rows (wave*KC_LOADS + q)*8 .. +7 of the operand
+  // tile; lane l writes row +l/8 at chunk position l%8, which holds logical chunk
+  // kc_swz(row, l%8).
   const u32x4_t ra = rsrc_words(p.A, p.a_bytes);
   const u32x4_t rb = rsrc_words(p.B, p.b_bytes);
-  uint32_t offa[V2_LOADS], offb[V2_LOADS];
+  uint32_t offa[KC_LOADS], offb[KC_LOADS];
 #pragma unroll
-  for (int q = 0; q < V2_LOADS; ++q) {
-    const int row = (wave * V2_LOADS + q) * 16 + (lane >> 2);
-    const int c = v2_swz(row, lane & 3);
+  for (int q = 0; q < KC_LOADS; ++q) {
+    const int row = (wave * KC_LOADS + q) * 8 + (lane >> 3);
+    const int c = kc_swz(row, lane & 7);
     const int ga = m0 + row, gb = n0 + row;
     const int64_t sa = ga < m_eff ? (p.a_rows ? (int64_t)p.a_rows[ga] : (int64_t)ga) : -1;
     offa[q] = sa >= 0 ? (uint32_t)((sa * p.lda + c * 8) * 2) : kOOB;
     offb[q] = gb < p.N ? (uint32_t)(((int64_t)gb * p.ldb + c * 8) * 2) : kOOB;
   }
-  // stage kt of the K loop into `st` (beyond the last stage every lane is out of range, so
-  // the loads only keep the number in flight uniform)
-  auto issue = [&](bf16_t* st, int kt) {
-    const int so = kt * V2_BK * 2;
-    const bool live = kt * V2_BK < p.K;
+  auto issue = [&](int kt) {
+    bf16_t* st = smem + (kt & 1) * KC_STAGE;
+    const int so = kt * KC_BK * 2;
 #pragma unroll
-    for (int q = 0; q < V2_LOADS; ++q) {
-      bf16_t* da = st + (wave * V2_LOADS + q) * 16 * V2_BK;
+    for (int q = 0; q < KC_LOADS; ++q) {
+      bf16_t* da = st + (wave * KC_LOADS + q) * 8 * KC_BK;
       const uint32_t la = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16_t*)da;
-      const uint32_t lb = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16_t*)(da + V2_OPER);
-      load_lds16(ra, __builtin_amdgcn_readfirstlane(la), live ? offa[q] : kOOB, (uint32_t)so);
-      load_lds16(rb, __builtin_amdgcn_readfirstlane(lb), live ? offb[q] : kOOB, (uint32_t)so);
+      const uint32_t lb = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16_t*)(da + KC_OPER);
+      load_lds16(ra, __builtin_amdgcn_readfirstlane(la), offa[q], (uint32_t)so);
+      load_lds16(rb, __builtin_amdgcn_readfirstlane(lb), offb[q], (uint32_t)so);
     }
   };
 
-  f32x16_t acc[TM][TN];
+  typename W::Acc acc;
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+  for (int i = 0; i < W::TM_; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+    for (int j = 0; j < W::TN_; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+      for (int r = 0; r < 4; ++r) acc[i][j][r] = 0.f;
 
-  const int arow = wm * WTM + (lane & 31);
-  const int brow = wn * WTN + (lane & 31);
-  auto compute = [&](const bf16_t* As) {
-    const bf16_t* Bs = As + V2_OPER;
+  // 16x16x32 operands: lane l supplies row (or column) l%16 at k 8*(l/16) .. +7
+  const int arow = wm * W::WTM_ + (lane & 15);
+  const int brow = wn * W::WTN_ + (lane & 15);
+  auto compute = [&](int kt) {
+    const bf16_t* As = smem + (kt & 1) * KC_STAGE;
+    const bf16_t* Bs = As + KC_OPER;
 #pragma unroll
-    for (int ks = 0; ks < V2_BK / 16; ++ks) {
-      const int c = ks * 2 + (lane >> 5);
-      bf16x8_t a[TM], b[TN];
+    for (int ks = 0; ks < KC_BK / 32; ++ks) {
+      const int c = ks * 4 + (lane >> 4);
+      bf16x8_t a[W::TM_], b[W::TN_];
 #pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int r = arow + i * 32;
-        a[i] = *(const bf16x8_t*)(As + r * V2_BK + v2_swz(r, c) * 8);
+      for (int i = 0; i < W::TM_; ++i) {
+        const int r = arow + i * 16;
+        a[i] = *(const bf16x8_t*)(As + r * KC_BK + kc_swz(r, c) * 8);
       }
 #pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int r = brow + j * 32;
-        b[j] = *(const bf16x8_t*)(Bs + r * V2_BK + v2_swz(r, c) * 8);
+      for (int j = 0; j < W::TN_; ++j) {
+        const int r = brow + j * 16;
+        b[j] = *(const bf16x8_t*)(Bs + r * KC_BK + kc_swz(r, c) * 8);
       }
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
+      for (int i = 0; i < W::TM_; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < W::TN_; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_s_setprio(0);
     }
   };
-  // Before each step: this wave's loads for the stage about to be read are the oldest in
-  // flight, the (V2_STAGES - 2) stages issued after them may stay outstanding; its LDS
-  // reads of the previous step have completed (lgkmcnt 0), so after the barrier the slot
-  // they read can be refilled.
-  constexpr int later = (V2_STAGES - 2) * 2 * V2_LOADS;
-  constexpr int wait_imm = (later & 15) | (7 << 4) | (0 << 8) | ((later >> 4) << 14);
-  const int nk = (int)cdiv(p.K, V2_BK);
-#pragma unroll
-  for (int st = 0; st < V2_STAGES - 1; ++st) issue(smem + st * V2_STAGE, st);
+  // Each step: this wave's loads of stage kt have landed and its LDS reads of step kt-1
+  // are complete (vmcnt 0, lgkmcnt 0); after the barrier the same holds for all waves, so
+  // stage kt may be read and the slot of stage kt-1 refilled with stage kt+1.
+  const int nk = (int)(p.K / KC_BK);
+  if (nk > 0) issue(0);
   for (int kt = 0; kt < nk; ++kt) {
-    __builtin_amdgcn_s_waitcnt(wait_imm);
+    __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt(0) expcnt(7) lgkmcnt(0)
     __syncthreads();
-    issue(smem + ((kt + V2_STAGES - 1) % V2_STAGES) * V2_STAGE, kt + V2_STAGES - 1);
-    compute(smem + (kt % V2_STAGES) * V2_STAGE);
+    if (kt + 1 < nk) issue(kt + 1);
+    compute(kt);
   }
-  __builtin_amdgcn_s_waitcnt(0);  // the trailing out-of-range loads also write LDS
-  __syncthreads();
-  gemm_epilogue<EPI>(p, acc, m0, n0, m_eff, smem);
+  __syncthreads();  // the epilogue reuses the stage buffers
+  gemm_epilogue<EPI, KC_WM, KC_WN, KC_FM>(p, acc, m0, n0, m_eff, smem);
 }
 
 template <int EPI>
-hipError_t launch_bf16_v2(const GemmParams& p, hipStream_t s) {
+hipError_t launch_kc(const GemmParams& p, hipStream_t s) {
   const int tiles = (int)(cdiv(p.M, BM) * cdiv(p.N, BN));
   if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL((k_gemm_bf16_v2<EPI>), dim3(tiles), dim3(NTHR), 0, s, p);
+  hipLaunchKernelGGL((k_gemm_kc<EPI>), dim3(tiles), dim3(NTHR), 0, s, p);
   return hipGetLastError();
 }
-
 template <int ALAY, int BLAY, int EPI>
 hipError_t launch_bf16(const GemmParams& p, hipStream_t s) {
   const int tiles = (int)(cdiv(p.M, BM) * cdiv(p.N, BN));
@@ -585,14 +646,14 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmParams p) {
 }  // namespace
 
 hipError_t gemm_bf16(int alay, int blay, int epi, const GemmParams& p, hipStream_t s) {
-  if (alay == LAY_KC && blay == LAY_KC && p.K % V2_BK == 0 && !p.k_count && !p.b_rows) {
+  if (alay == LAY_KC && blay == LAY_KC && p.K % KC_BK == 0 && !p.k_count && !p.b_rows) {
     switch (epi) {
-      case EPI_TWELL: return launch_bf16_v2<EPI_TWELL>(p, s);
-      case EPI_F32: return launch_bf16_v2<EPI_F32>(p, s);
-      case EPI_ACT_RELU: return launch_bf16_v2<EPI_ACT_RELU>(p, s);
-      case EPI_ACT: return launch_bf16_v2<EPI_ACT>(p, s);
-      case EPI_MASKGRAD: return launch_bf16_v2<EPI_MASKGRAD>(p, s);
-      case EPI_MUL_ACT: return launch_bf16_v2<EPI_MUL_ACT>(p, s);
+      case EPI_TWELL: return launch_kc<EPI_TWELL>(p, s);
+      case EPI_F32: return launch_kc<EPI_F32>(p, s);
+      case EPI_ACT_RELU: return launch_kc<EPI_ACT_RELU>(p, s);
+      case EPI_ACT: return launch_kc<EPI_ACT>(p, s);
+      case EPI_MASKGRAD: return launch_kc<EPI_MASKGRAD>(p, s);
+      case EPI_MUL_ACT: return launch_kc<EPI_MUL_ACT>(p, s);
       default: break;
     }
   }
