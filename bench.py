@@ -152,7 +152,9 @@ class Bench:
         if packed and not w.gated and w.d % 512 == 0:
             WdP = t.empty_like(Wd)
             b.sfl_pack_down_weights(Wd, WdP)
-        if w.gated:
+        if w.dtype == "bf16":
+            # W_up^T ([f][d]) is kept beside W_up, like W_down's slice-major copy: a one-time
+            # weight layout that lets the up projection read both operands K-contiguously
             WupT = t.empty((w.f, w.d), dtype=t.bfloat16, device="cuda")
             b.sfl_transpose(Wu, WupT)
         kw = dict(Y=Y, bufs=bufs, W_gate=Wg, W_upT=WupT, W_down_packed=WdP, bias_f=self.dev(w.bias_f),
@@ -160,11 +162,12 @@ class Bench:
         a0 = b.ffn_args(X, Wu, Wd, cfg, **kw)
         ws = t.empty(max(1, b.sfl_workspace_size(a0)), dtype=t.uint8, device="cuda")
         dws = t.empty(max(1, b.sfl_workspace_size(a0, 2)), dtype=t.uint8, device="cuda")
-        s = dict(X=X, Wu=Wu, Wd=Wd, cfg=cfg, bufs=bufs, stats=stats, kw=kw, ws=ws, dws=dws, Y=Y)
+        s = dict(X=X, Wu=Wu, Wd=Wd, WupT=WupT, cfg=cfg, bufs=bufs, stats=stats, kw=kw, ws=ws, dws=dws, Y=Y)
         s["args"] = b.ffn_args(X, Wu, Wd, cfg, **kw, workspace=ws)
         dkw = dict(kw)
         dkw["Y"] = t.empty_like(Y)
         s["dargs"] = b.ffn_args(X, Wu, Wd, cfg, **dkw, workspace=dws)
+        s["dkw"] = dkw
         s["mk"] = lambda ev: b.ffn_args(X, Wu, Wd, cfg, **kw, workspace=ws, events=ev)
         return s
 
@@ -182,6 +185,29 @@ class Bench:
             dms = self.time(lambda: b.sfl_dense_ffn_baseline(s["dargs"], self.stream))
             rec["dense_ms"] = round(dms, 4)
             rec["speedup_vs_dense"] = round(dms / ms, 4)
+            rec["dense_stages_ms"] = dict(zip(["up_gemm_relu", "down_gemm"],
+                                              self.stage_times(lambda ev: b.ffn_args(
+                                                  s["X"], s["Wu"], s["Wd"], s["cfg"], **s["dkw"],
+                                                  workspace=s["dws"], events=ev),
+                                                  b.sfl_dense_ffn_baseline, 3)))
+            if not w.gated:
+                # the same dense FFN through torch (hipBLASLt GEMMs), for context
+                t = self.torch
+                X, Wd, WupT = s["X"], s["Wd"], s["WupT"]
+                bias = None if w.bias_f is None else self.dev(w.bias_f).to(t.bfloat16)
+                sh = None if w.shift_t is None else self.dev(w.shift_t).to(t.bfloat16)[:, None]
+
+                def torch_dense():
+                    Z = X @ WupT.t()
+                    if bias is not None:
+                        Z += bias
+                    if sh is not None:
+                        Z += sh
+                    return t.relu_(Z) @ Wd
+
+                tms = self.time(torch_dense)
+                rec["dense_torch_ms"] = round(tms, 4)
+                rec["speedup_vs_dense_torch"] = round(tms / ms, 4)
         return rec, s, st
 
     def training_record(self, w, lam):
@@ -194,10 +220,10 @@ class Bench:
         dWu = t.empty((w.d, w.f), dtype=t.float32, device="cuda")
         dWd = t.empty((w.f, w.d), dtype=t.float32, device="cuda")
         bws = t.empty(max(1, b.sfl_workspace_size(
-            b.bwd_args(s["X"], s["Wu"], s["Wd"], dY, s["cfg"], s["bufs"], lam, dX, dWu, dWd), 1)),
+            b.bwd_args(s["X"], s["Wu"], s["Wd"], dY, s["cfg"], s["bufs"], lam, dX, dWu, dWd, W_upT=s["WupT"]), 1)),
             dtype=t.uint8, device="cuda")
         mkb = lambda ev=None: b.bwd_args(s["X"], s["Wu"], s["Wd"], dY, s["cfg"], s["bufs"], lam, dX, dWu, dWd,
-                                         workspace=bws, events=ev)
+                                         W_upT=s["WupT"], workspace=bws, events=ev)
         bargs = mkb()
 
         def step():
@@ -273,7 +299,7 @@ def main():
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_MFMA_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / BF16_MFMA_PEAK_TFLOPS, 4),
                 "traffic": measured_traffic("up_gemm_twell", gemm_hash),
-                "kernel": "k_gemm_bf16<KC,RC,TWELL>", "work": "2*T*d*f flops per launch"}
+                "kernel": "k_gemm_kc<EPI_TWELL, 256>", "work": "2*T*d*f flops per launch"}
     # the sparse down projection: algorithmic bytes = sum_t nnz_t*(2d + 4) + (2d + 5) per sparse row
     nnz = int(st["total_nnz"])
     n_sparse = T - int(st["n_ovf_rows"])
@@ -306,6 +332,9 @@ def main():
                    "parallelism": "single GPU"},
         "dense_ms_per_step": head["dense_ms"],
         "speedup_vs_dense": head["speedup_vs_dense"],
+        "dense_stages_ms": head["dense_stages_ms"],
+        "dense_torch_ms_per_step": head.get("dense_torch_ms"),
+        "speedup_vs_dense_torch": head.get("speedup_vs_dense_torch"),
         "stages_ms": stages,
         "ms_per_step_w_down_packed_per_call": round(ms_unpacked, 4),
         "n_ovf_rows": head["n_ovf_rows"],

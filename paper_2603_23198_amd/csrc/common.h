@@ -27,6 +27,11 @@ __device__ __forceinline__ bf16_t f32_to_bf16(float x) {
   uint32_t r = u + 0x7fffu + ((u >> 16) & 1u);
   return (bf16_t)(r >> 16);
 }
+// The same rounding for a value known not to be NaN (no NaN test).
+__device__ __forceinline__ bf16_t f32_to_bf16_finite(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return (bf16_t)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+}
 __device__ __forceinline__ float bf16_to_f32(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 __device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }

@@ -123,7 +123,7 @@ constexpr int SLICE2 = SFL_SLICE;      // columns per slice of W_down
 constexpr int LPR = SLICE2 * 2 / 16;   // lanes per row segment (16 bytes each)
 constexpr int NGRP = 64 / LPR;         // row segments per load instruction
 #ifndef SFL_GATHER_WAVES
-#define SFL_GATHER_WAVES 12
+#define SFL_GATHER_WAVES 16
 #endif
 #ifndef SFL_GATHER_UNROLL
 #define SFL_GATHER_UNROLL 8
@@ -324,10 +324,15 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
   if (d % (8 * SLICE2) != 0) return hipErrorInvalidValue;
   const int n_slices = (int)(d / SLICE2);
 
-  // tokens per workgroup: what the LDS budget holds, at most 64; a token block goes to
-  // every XCD (each XCD covers its own slices), so the grid is 8 x the number of blocks
+  // Tokens per workgroup: at most what the LDS budget holds (one workgroup per CU). A
+  // token block goes to every XCD (each XCD covers its own slices), so the grid is 8 x the
+  // number of blocks; the blocks are sized so that each XCD's 32 CUs get whole rounds.
   const int64_t per_tok = (int64_t)std::max(K, 1) * 4 + 4;
-  const int tpw = (int)std::max<int64_t>(1, std::min<int64_t>(GATHER_LDS / 1024, GATHER_LDS / per_tok));
+  const int64_t tpw_max = std::max<int64_t>(1, std::min<int64_t>(GATHER_LDS / 1024, GATHER_LDS / per_tok));
+  const int64_t wg_per_cu = std::max<int64_t>(1, (160 * 1024) / (tpw_max * per_tok));
+  const int64_t slots = 32 * std::min<int64_t>(wg_per_cu, 2048 / (GATHER_WAVES * 64));
+  const int64_t rounds = cdiv(T, tpw_max * slots);
+  const int tpw = (int)std::max<int64_t>(1, cdiv(T, rounds * slots));
   const int64_t blocks = cdiv(T, tpw);
   const size_t lds = (size_t)tpw * per_tok;
   if (lds > 160 * 1024) return hipErrorInvalidValue;

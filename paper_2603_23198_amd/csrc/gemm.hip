@@ -1,17 +1,22 @@
-// Dense GEMMs of the FFN layer: bf16 on MFMA (v_mfma_f32_32x32x16_bf16) and fp32 on FMA.
+// Dense GEMMs of the FFN layer: bf16 on MFMA and fp32 on FMA.
 //
-// The bf16 kernel computes a 256x256 output tile per workgroup of 8 waves (2 along M x
-// 4 along N, 128x64 per wave = 4x2 MFMA 32x32 tiles). K advances in steps of 64 through
-// a double-buffered LDS stage; the next K step is fetched from global memory into
-// registers while the current one feeds the MFMAs. Each operand tile is kept in LDS
-// K-contiguous ([rows][64 + 8 pad] bf16), the layout both MFMA operands read 16 bytes
-// per lane from. Operands stored row-contiguous ([K][rows], e.g. W_up [d][f] as the B of
-// X W_up) are transposed on the way in: a lane fetches one 4-byte pair of adjacent rows
-// from 8 consecutive k, and byte permutes turn them into two 8-element k vectors.
+// Two bf16 kernels, both 256x256 output tiles per workgroup of 8 waves:
+//  * k_gemm_kc (both operands K-contiguous, K % 64 == 0; the forward's X W_up^T, the
+//    dense baseline's first GEMM, the backward's dZ W_up^T): v_mfma_f32_16x16x32_bf16,
+//    waves 4 along M x 2 along N, operands loaded straight from global memory into LDS
+//    (no staging registers) through two 64-k stages.
+//  * k_gemm_bf16 (any layout pair, K gathers, device-side K bounds): v_mfma_f32_32x32x16,
+//    waves 2 along M x 4 along N (128x64 per wave = 4x2 MFMA 32x32 tiles). K advances in
+//    steps of 64 through a double-buffered LDS stage; the next K step is fetched from
+//    global memory into registers while the current one feeds the MFMAs. Each operand
+//    tile is kept in LDS K-contiguous ([rows][64 + 8 pad] bf16). Operands stored
+//    row-contiguous ([K][rows], e.g. W_up [d][f] as the B of X W_up) are transposed on
+//    the way in: a lane fetches one 4-byte pair of adjacent rows from 8 consecutive k,
+//    and byte permutes turn them into two 8-element k vectors.
 //
-// Epilogues (the `Epilogue` enum) include the TwELL one of Alg. 1: z = acc (+ bias, shift)
-// is staged through LDS 64 rows at a time, then each wave compacts 8 rows: 64 columns per
-// step, ballot of z > 0 and mbcnt give each active column its slot (ascending order).
+// Epilogues (the `Epilogue` enum) include the TwELL one of Alg. 1, which compacts the
+// active pre-activations straight from the accumulator registers (ballot + mbcnt per
+// row, see twell_epilogue).
 #include "common.h"
 #include "internal.h"
 
@@ -29,8 +34,8 @@ constexpr int TM = WTM / 32, TN = WTN / 32;
 constexpr int LDS_STAGE = (BM + BN) * LDK;  // bf16 elements per stage
 
 __device__ __forceinline__ bool active_bits(float z) {
-  const int32_t b = __float_as_int(z);
-  return b > 0 && b <= 0x7f800000;
+  // z > 0 and not NaN: the bits, minus one, as unsigned, are below those of +inf
+  return (uint32_t)__float_as_int(z) - 1u < 0x7f800000u;
 }
 
 // ---- loaders -----------------------------------------------------------------------
@@ -214,9 +219,10 @@ struct WaveTile {
 // than a wave's columns continues in the next wave(s) along N: each wave first publishes
 // its per-row active counts in LDS and starts from the sum of the counts of the waves left
 // of it in the same tile. Active means z > 0 and not NaN on the fp32 value.
-template <int WM_, int WN_, int FM>
+template <int WM_, int WN_, int FM, int Tn>
 __device__ __forceinline__ void twell_epilogue(const GemmParams& p, const typename WaveTile<WM_, WN_, FM>::Acc& acc,
                                                int m0, int n0, int m_eff, bf16_t* smem) {
+  static_assert(Tn == 64 || Tn == 128 || Tn == 256, "TwELL tile width");
   typedef WaveTile<WM_, WN_, FM> W;
   typedef AccGeo<FM> G;
   constexpr int NT_ = WM_ * WN_ * 64;
@@ -235,16 +241,18 @@ __device__ __forceinline__ void twell_epilogue(const GemmParams& p, const typena
     sh_lds[r] = s;
   }
   __syncthreads();
-  const int Tn = p.tile_cols, S = p.tile_slots, NT = p.n_tiles;
+  const int S = p.tile_slots, NT = p.n_tiles;
   const int wcol0 = n0 + wn * W::WTN_;  // first column of this wave
   float bj[W::TN_];
+  bool cok[W::TN_];
 #pragma unroll
   for (int j = 0; j < W::TN_; ++j) {
     const int gc = wcol0 + j * FM + G::col(lane);
-    bj[j] = (p.bias && gc < p.N) ? p.bias[gc] : 0.f;
+    cok[j] = gc < p.N;
+    bj[j] = (p.bias && cok[j]) ? p.bias[gc] : 0.f;
   }
-  const bool spans = Tn > W::WTN_;  // uniform; tiles then start on wave boundaries
-  if (spans) {
+  constexpr bool spans = Tn > W::WTN_;  // tiles then start on wave boundaries
+  if constexpr (spans) {
 #pragma unroll
     for (int i = 0; i < W::TM_; ++i)
 #pragma unroll
@@ -254,17 +262,17 @@ __device__ __forceinline__ void twell_epilogue(const GemmParams& p, const typena
         int c = 0;
 #pragma unroll
         for (int j = 0; j < W::TN_; ++j) {
-          const bool act = wcol0 + j * FM + G::col(lane) < p.N && active_bits((acc[i][j][r] + bj[j]) + sh);
+          const bool act = cok[j] & active_bits((acc[i][j][r] + bj[j]) + sh);
           c += __popcll(ballot(act) & gmask);
         }
         if (leader) cnt_lds[wn * BM + lrow] = c;
       }
   }
   __syncthreads();
-  const int wpt = spans ? Tn / W::WTN_ : 1;  // waves per TwELL tile
+  constexpr int wpt = spans ? Tn / W::WTN_ : 1;  // waves per TwELL tile
   const int first_w = wn - wn % wpt;
   const bool last_w = wn % wpt == wpt - 1;
-  bf16_t* tval = (bf16_t*)p.tw_val;
+  const int jt0 = wcol0 / Tn;  // TwELL tile of the wave's first column
 #pragma unroll
   for (int i = 0; i < W::TM_; ++i)
 #pragma unroll
@@ -275,29 +283,30 @@ __device__ __forceinline__ void twell_epilogue(const GemmParams& p, const typena
       const float sh = sh_lds[lrow];
       int run = 0;
       for (int w = first_w; w < wn; ++w) run += cnt_lds[w * BM + lrow];
-      const int64_t rbase = (int64_t)grow * NT * S;
+      bf16_t* vrow = (bf16_t*)p.tw_val + (int64_t)grow * NT * S;
+      uint16_t* irow = p.tw_idx + (int64_t)grow * NT * S;
+      int32_t* crow = p.tw_cnt + (int64_t)grow * NT;
 #pragma unroll
       for (int j = 0; j < W::TN_; ++j) {
-        const int cb = wcol0 + j * FM;  // first column of this block
-        if (!spans && cb % Tn == 0) run = 0;
-        const int gc = cb + G::col(lane);
+        if (!spans && (j * FM) % Tn == 0) run = 0;  // wave starts are tile-aligned
+        const int gc = wcol0 + j * FM + G::col(lane);
         const float z = (acc[i][j][r] + bj[j]) + sh;
-        const bool act = gc < p.N && active_bits(z);
+        const bool act = cok[j] & active_bits(z);
         const uint64_t m = ballot(act) & gmask;
         const int slot = run + mbcnt(m);
-        const int jt = cb / Tn;
+        const int jt = jt0 + (spans ? 0 : (j * FM) / Tn);
         if (act && rok && slot < S) {
-          tval[rbase + (int64_t)jt * S + slot] = f32_to_bf16(z);
-          p.tw_idx[rbase + (int64_t)jt * S + slot] = (uint16_t)gc;
+          vrow[jt * S + slot] = f32_to_bf16_finite(z);
+          irow[jt * S + slot] = (uint16_t)gc;
         }
         run += __popcll(m);
-        const bool tend = spans ? (last_w && j == W::TN_ - 1) : ((cb + FM) % Tn == 0);
-        if (tend && leader && rok && jt * Tn < p.N) p.tw_cnt[(int64_t)grow * NT + jt] = run;
+        const bool tend = spans ? (last_w && j == W::TN_ - 1) : ((j * FM + FM) % Tn == 0);
+        if (tend && leader && rok && jt * Tn < p.N) crow[jt] = run;
       }
     }
 }
 
-template <int EPI, int WM_, int WN_, int FM>
+template <int EPI, int WM_, int WN_, int FM, int Tn>
 __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, const typename WaveTile<WM_, WN_, FM>::Acc& acc,
                                               int m0, int n0, int m_eff, bf16_t* smem) {
   typedef WaveTile<WM_, WN_, FM> W;
@@ -306,7 +315,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, const typenam
   const int wave = threadIdx.x >> 6;
   const int wm = wave / WN_, wn = wave % WN_;
   if constexpr (EPI == EPI_TWELL) {
-    twell_epilogue<WM_, WN_, FM>(p, acc, m0, n0, m_eff, smem);
+    twell_epilogue<WM_, WN_, FM, Tn>(p, acc, m0, n0, m_eff, smem);
   } else {
 #pragma unroll
     for (int i = 0; i < W::TM_; ++i) {
@@ -348,7 +357,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, const typenam
     }
   }
 }
-template <int ALAY, int BLAY, int EPI>
+template <int ALAY, int BLAY, int EPI, int Tn>
 __global__ __launch_bounds__(NTHR) void k_gemm_bf16(GemmParams p) {
   __shared__ __attribute__((aligned(16))) bf16_t smem[2 * LDS_STAGE];
   const int tid = threadIdx.x;
@@ -419,7 +428,7 @@ __global__ __launch_bounds__(NTHR) void k_gemm_bf16(GemmParams p) {
     __syncthreads();
   }
 
-  gemm_epilogue<EPI, WAVES_M, WAVES_N, 32>(p, acc, m0, n0, m_eff, smem);
+  gemm_epilogue<EPI, WAVES_M, WAVES_N, 32, Tn>(p, acc, m0, n0, m_eff, smem);
 }
 
 // ---- K-contiguous x K-contiguous GEMM: direct global -> LDS loads, 16x16x32 MFMAs -------
@@ -467,7 +476,7 @@ __device__ __forceinline__ void load_lds16(u32x4_t rsrc, uint32_t lds_off, uint3
                : "memory");
 }
 
-template <int EPI>
+template <int EPI, int Tn>
 __global__ __launch_bounds__(NTHR) void k_gemm_kc(GemmParams p) {
   __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * KC_STAGE];
   typedef WaveTile<KC_WM, KC_WN, KC_FM> W;
@@ -559,22 +568,34 @@ __global__ __launch_bounds__(NTHR) void k_gemm_kc(GemmParams p) {
     compute(kt);
   }
   __syncthreads();  // the epilogue reuses the stage buffers
-  gemm_epilogue<EPI, KC_WM, KC_WN, KC_FM>(p, acc, m0, n0, m_eff, smem);
+  gemm_epilogue<EPI, KC_WM, KC_WN, KC_FM, Tn>(p, acc, m0, n0, m_eff, smem);
 }
 
-template <int EPI>
+template <int EPI, int Tn = 0>
 hipError_t launch_kc(const GemmParams& p, hipStream_t s) {
   const int tiles = (int)(cdiv(p.M, BM) * cdiv(p.N, BN));
   if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL((k_gemm_kc<EPI>), dim3(tiles), dim3(NTHR), 0, s, p);
+  hipLaunchKernelGGL((k_gemm_kc<EPI, Tn>), dim3(tiles), dim3(NTHR), 0, s, p);
   return hipGetLastError();
 }
-template <int ALAY, int BLAY, int EPI>
+template <int ALAY, int BLAY, int EPI, int Tn = 0>
 hipError_t launch_bf16(const GemmParams& p, hipStream_t s) {
   const int tiles = (int)(cdiv(p.M, BM) * cdiv(p.N, BN));
   if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL((k_gemm_bf16<ALAY, BLAY, EPI>), dim3(tiles), dim3(NTHR), 0, s, p);
+  hipLaunchKernelGGL((k_gemm_bf16<ALAY, BLAY, EPI, Tn>), dim3(tiles), dim3(NTHR), 0, s, p);
   return hipGetLastError();
+}
+
+// TwELL epilogue with the tile width as a compile-time constant
+template <int ALAY, int BLAY>
+hipError_t launch_twell(const GemmParams& p, hipStream_t s) {
+  const bool kc = ALAY == LAY_KC && BLAY == LAY_KC && p.K % KC_BK == 0 && !p.k_count && !p.b_rows;
+  switch (p.tile_cols) {
+    case 64: return kc ? launch_kc<EPI_TWELL, 64>(p, s) : launch_bf16<ALAY, BLAY, EPI_TWELL, 64>(p, s);
+    case 128: return kc ? launch_kc<EPI_TWELL, 128>(p, s) : launch_bf16<ALAY, BLAY, EPI_TWELL, 128>(p, s);
+    case 256: return kc ? launch_kc<EPI_TWELL, 256>(p, s) : launch_bf16<ALAY, BLAY, EPI_TWELL, 256>(p, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 // ---- fp32 FMA GEMM (A [M][K] row-major, B [K][N] row-major), 64x64 tiles ------------------
@@ -648,7 +669,6 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmParams p) {
 hipError_t gemm_bf16(int alay, int blay, int epi, const GemmParams& p, hipStream_t s) {
   if (alay == LAY_KC && blay == LAY_KC && p.K % KC_BK == 0 && !p.k_count && !p.b_rows) {
     switch (epi) {
-      case EPI_TWELL: return launch_kc<EPI_TWELL>(p, s);
       case EPI_F32: return launch_kc<EPI_F32>(p, s);
       case EPI_ACT_RELU: return launch_kc<EPI_ACT_RELU>(p, s);
       case EPI_ACT: return launch_kc<EPI_ACT>(p, s);
@@ -660,13 +680,13 @@ hipError_t gemm_bf16(int alay, int blay, int epi, const GemmParams& p, hipStream
 #define SFL_CASE(A_, B_, E_) \
   if (alay == A_ && blay == B_ && epi == E_) return launch_bf16<A_, B_, E_>(p, s);
   // forward: X W_up (B row-contiguous [d][f]) with TwELL / f32 / ReLU epilogues
-  SFL_CASE(LAY_KC, LAY_RC, EPI_TWELL)
+  if (epi == EPI_TWELL && alay == LAY_KC && blay == LAY_RC) return launch_twell<LAY_KC, LAY_RC>(p, s);
+  if (epi == EPI_TWELL && alay == LAY_KC && blay == LAY_KC) return launch_twell<LAY_KC, LAY_KC>(p, s);
   SFL_CASE(LAY_KC, LAY_RC, EPI_F32)
   SFL_CASE(LAY_KC, LAY_RC, EPI_ACT_RELU)
   SFL_CASE(LAY_KC, LAY_RC, EPI_ACT)
   SFL_CASE(LAY_KC, LAY_RC, EPI_MUL_ACT)
   // pre-transposed weights ([f][d]) variants
-  SFL_CASE(LAY_KC, LAY_KC, EPI_TWELL)
   SFL_CASE(LAY_KC, LAY_KC, EPI_F32)
   SFL_CASE(LAY_KC, LAY_KC, EPI_ACT_RELU)
   SFL_CASE(LAY_KC, LAY_KC, EPI_ACT)
