@@ -148,17 +148,25 @@ class Bench:
         bufs = b.alloc_twell(w.T, w.f, "bf16", cfg)
         Y = t.empty((w.T, w.d), dtype=t.bfloat16, device="cuda")
         stats = b.alloc_stats()
-        WdP = WupT = None
+        WdP = WupT = WgT = WdT = None
         if packed and not w.gated and w.d % 512 == 0:
             WdP = t.empty_like(Wd)
             b.sfl_pack_down_weights(Wd, WdP)
+
+        def transposed(W):
+            out = t.empty((W.shape[1], W.shape[0]), dtype=W.dtype, device="cuda")
+            b.sfl_transpose(W, out)
+            return out
+
         if w.dtype == "bf16":
-            # W_up^T ([f][d]) is kept beside W_up, like W_down's slice-major copy: a one-time
-            # weight layout that lets the up projection read both operands K-contiguously
-            WupT = t.empty((w.f, w.d), dtype=t.bfloat16, device="cuda")
-            b.sfl_transpose(Wu, WupT)
-        kw = dict(Y=Y, bufs=bufs, W_gate=Wg, W_upT=WupT, W_down_packed=WdP, bias_f=self.dev(w.bias_f),
-                  shift_t=self.dev(w.shift_t), stats=stats)
+            # Transposed weight copies are kept beside the weights, like W_down's slice-major
+            # copy: one-time layouts that let every dense GEMM (the up / gate projection, the
+            # dense-backup rows, the dense baseline) read both operands K-contiguously.
+            WupT, WdT = transposed(Wu), transposed(Wd)
+            if w.gated:
+                WgT = transposed(Wg)
+        kw = dict(Y=Y, bufs=bufs, W_gate=Wg, W_upT=WupT, W_gateT=WgT, W_downT=WdT, W_down_packed=WdP,
+                  bias_f=self.dev(w.bias_f), shift_t=self.dev(w.shift_t), stats=stats)
         a0 = b.ffn_args(X, Wu, Wd, cfg, **kw)
         ws = t.empty(max(1, b.sfl_workspace_size(a0)), dtype=t.uint8, device="cuda")
         dws = t.empty(max(1, b.sfl_workspace_size(a0, 2)), dtype=t.uint8, device="cuda")

@@ -132,6 +132,15 @@ typedef struct {
  *            operand). Gated: read by the fused up-dot; when NULL the gated path
  *            transposes W_up into the workspace. sfl_dense_ffn_baseline reads it for
  *            its X W_up GEMM the same way.
+ *  W_gateT   optional [f][d] copy of W_gate transposed (bf16, gated only): the gate
+ *            projection (forward, sfl_up_projection, dense baseline) reads it instead
+ *            of W_gate.
+ *  W_downT   optional [d][f] copy of W_down transposed (bf16): the dense-backup rows'
+ *            down GEMM and the dense baseline's down GEMM read it instead of W_down
+ *            (K-contiguous B operand). The sparse down projection never reads it.
+ *  Transposed copies are one-time weight layouts (sfl_transpose writes them); each
+ *  GEMM that has its operand K-contiguous runs the direct-to-LDS kernel, the others
+ *  transpose 8-k groups on the way into LDS.
  *  W_down_packed  optional bf16 copy of W_down in the slice-major layout written by
  *            sfl_pack_down_weights ([d/64][f][64]); the sparse down projection reads
  *            64-column slices of W_down, and this layout makes each slice one
@@ -157,6 +166,8 @@ typedef struct {
   const void* W_up;
   const void* W_down;
   const void* W_upT;
+  const void* W_gateT;
+  const void* W_downT;
   const void* W_down_packed;
   const float* bias_f;
   const float* shift_t;

@@ -98,10 +98,19 @@ struct FwdPlan {
   void* ovf_dense = nullptr; // dense-backup rows when the caller gave none [cap][f]
   void* WupT = nullptr;      // gated: W_up transposed [f][d]
   void* WdP = nullptr;       // slice-major W_down when the caller gave none [d/64][f][64]
+  float* part = nullptr;     // split-K partial sums of the dense-backup GEMMs [part_rows][max(f, d)]
+  int part_rows = 0;
   size_t bytes = 0;
 };
 
+// Dense-backup rows are few but their GEMMs are long in K (d, then f): split K over up to
+// this many blocks per output tile, with partial sums for up to kPartRows rows.
+constexpr int kMaxSplit = 8;
+constexpr int64_t kPartRows = 4096;
+
 bool packed_gather(const sfl_ffn_args_t& a) { return a.dtype == SFL_BF16 && !a.gated && a.d % 512 == 0; }
+
+int64_t align_rows(int64_t r) { return (r + 255) / 256 * 256; }
 
 FwdPlan plan_forward(const sfl_ffn_args_t& a, void* ws) {
   Carve c(ws);
@@ -111,6 +120,10 @@ FwdPlan plan_forward(const sfl_ffn_args_t& a, void* ws) {
   if (!a.twell.ovf_dense) p.ovf_dense = c.take((size_t)cap * a.f * elem_size(a.dtype));
   if (a.gated && !a.W_upT) p.WupT = c.take((size_t)a.f * a.d * elem_size(a.dtype));
   if (packed_gather(a) && !a.W_down_packed) p.WdP = c.take((size_t)a.f * a.d * 2);
+  if (a.dtype == SFL_BF16 && cap > 0) {
+    p.part_rows = (int)std::min<int64_t>(align_rows(cap), kPartRows);
+    p.part = (float*)c.take((size_t)p.part_rows * std::max(a.f, a.d) * 4);
+  }
   p.bytes = c.used;
   return p;
 }
@@ -133,6 +146,20 @@ void set_weight_B(GemmParams& g, const void* W, const void* WT, int64_t d, int64
   } else {
     g.B = W;
     g.ldb = f;
+    *blay = LAY_RC;
+  }
+}
+
+// B operand of H W_down for W_down [f][d] (row-contiguous over d) or W_down^T [d][f].
+void set_down_B(GemmParams& g, const void* Wd, const void* WdT, int64_t d, int64_t f, int* blay) {
+  g.b_bytes = d * f * 2;
+  if (WdT) {
+    g.B = WdT;
+    g.ldb = f;
+    *blay = LAY_KC;
+  } else {
+    g.B = Wd;
+    g.ldb = d;
     *blay = LAY_RC;
   }
 }
@@ -231,10 +258,11 @@ sfl_status_t sfl_up_projection(const sfl_ffn_args_t* a, float* Z, sfl_stream_t s
   g.lda = a->d;
   g.a_bytes = a->T * a->d * 2;
   int blay = LAY_RC;
+  const bool bf = a->dtype == SFL_BF16;
   if (a->gated)
-    set_weight_B(g, a->W_gate, nullptr, a->d, a->f, &blay);
+    set_weight_B(g, a->W_gate, bf ? a->W_gateT : nullptr, a->d, a->f, &blay);
   else
-    set_weight_B(g, a->W_up, a->dtype == SFL_BF16 ? a->W_upT : nullptr, a->d, a->f, &blay);
+    set_weight_B(g, a->W_up, bf ? a->W_upT : nullptr, a->d, a->f, &blay);
   g.bias = a->bias_f;
   g.shift = a->shift_t;
   g.C = Z;
@@ -265,8 +293,10 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
     for (int i = 1; i < 5; ++i) ev.record(i, s);
     return SFL_OK;
   }
-  const void* Wp = a->gated ? a->W_gate : a->W_up;        // pattern-deciding projection
-  const void* WpT = a->gated || a->dtype != SFL_BF16 ? nullptr : a->W_upT;  // its transposed copy, if given
+  const bool bf = a->dtype == SFL_BF16;
+  const void* Wp = a->gated ? a->W_gate : a->W_up;                        // pattern-deciding projection
+  const void* WpT = !bf ? nullptr : a->gated ? a->W_gateT : a->W_upT;     // its transposed copy, if given
+  const void* WdT = bf ? a->W_downT : nullptr;
 
   // 1. up (or gate) projection with the ReLU -> TwELL epilogue (Alg. 1)
   {
@@ -303,8 +333,8 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
   SFL_HIP(launch_ovf_list(T, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s));
   ev.record(2, s);
   // 3. sparse down projection of the ELL rows
+  const void* WupT = a->W_upT;  // gated: W_up^T, given or built in the workspace
   if (a->gated) {
-    const void* WupT = a->W_upT;
     if (!WupT) {
       SFL_HIP(launch_transpose(a->W_up, plan.WupT, d, f, 2, s));
       WupT = plan.WupT;
@@ -343,12 +373,15 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
     g.s_rows = tw.ovf_rows;
     g.C = ovf_dense;
     g.ldc = f;
+    g.ksplit = kMaxSplit;
+    g.part = plan.part;
+    g.part_rows = plan.part_rows;
     SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_ACT_RELU, g, s));
     if (a->gated) {
       GemmParams u = g;
       u.bias = nullptr;
       u.shift = nullptr;
-      set_weight_B(u, a->W_up, nullptr, d, f, &blay);
+      set_weight_B(u, a->W_up, WupT, d, f, &blay);
       SFL_HIP(gemm_bf16(LAY_KC, blay, EPI_MUL_ACT, u, s));
     }
     GemmParams y = gp_zero();
@@ -360,13 +393,14 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
     y.a_bytes = cap * f * 2;
     y.m_count = tw.n_ovf;
     y.count_cap = (int32_t)cap;
-    y.B = a->W_down;
-    y.ldb = d;
-    y.b_bytes = f * d * 2;
+    set_down_B(y, a->W_down, WdT, d, f, &blay);
     y.c_rows = tw.ovf_rows;
     y.C = a->Y;
     y.ldc = d;
-    SFL_HIP(run_gemm(a->dtype, LAY_KC, LAY_RC, EPI_ACT, y, s));
+    y.ksplit = kMaxSplit;
+    y.part = plan.part;
+    y.part_rows = plan.part_rows;
+    SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_ACT, y, s));
     SFL_HIP(launch_ovf_l1(f, vb, ovf_dense, tw.n_ovf, (int32_t)cap, a->stats, s));
   }
   ev.record(4, s);
@@ -392,7 +426,7 @@ sfl_status_t sfl_dense_ffn_baseline(const sfl_ffn_args_t* a, sfl_stream_t stream
   g.a_bytes = T * d * 2;
   int blay;
   const bool bf = a->dtype == SFL_BF16;
-  set_weight_B(g, a->gated ? a->W_gate : a->W_up, a->gated || !bf ? nullptr : a->W_upT, d, f, &blay);
+  set_weight_B(g, a->gated ? a->W_gate : a->W_up, !bf ? nullptr : a->gated ? a->W_gateT : a->W_upT, d, f, &blay);
   g.bias = a->bias_f;
   g.shift = a->shift_t;
   g.C = a->workspace;
@@ -413,12 +447,10 @@ sfl_status_t sfl_dense_ffn_baseline(const sfl_ffn_args_t* a, sfl_stream_t stream
   y.A = a->workspace;
   y.lda = f;
   y.a_bytes = T * f * 2;
-  y.B = a->W_down;
-  y.ldb = d;
-  y.b_bytes = f * d * 2;
+  set_down_B(y, a->W_down, bf ? a->W_downT : nullptr, d, f, &blay);
   y.C = a->Y;
   y.ldc = d;
-  SFL_HIP(run_gemm(a->dtype, LAY_KC, LAY_RC, EPI_ACT, y, s));
+  SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_ACT, y, s));
   ev.record(2, s);
   return SFL_OK;
 }

@@ -452,6 +452,17 @@ static_assert(2 * KC_STAGE * 2 >= (BM + KC_WN * BM) * 4, "TwELL epilogue scratch
 
 __device__ __forceinline__ int kc_swz(int row, int chunk) { return chunk ^ (row & 7); }
 
+// Split count for m_eff counted rows: enough blocks for about two per CU, at least four
+// 64-k steps per split, and partial sums that fit part_rows rows.
+__device__ __forceinline__ int splitk_count(int ksplit, int part_rows, int m_eff, int N, int nk) {
+  if (ksplit <= 1 || m_eff <= 0) return 1;
+  const int tiles = (int)(cdiv(m_eff, BM) * cdiv(N, BN));
+  int ks = min(ksplit, part_rows / m_eff);
+  ks = min(ks, nk / 4);
+  ks = min(ks, max(1, 512 / tiles));
+  return max(ks, 1);
+}
+
 // The four descriptor words of a raw buffer resource, for inline assembly operands.
 __device__ __forceinline__ u32x4_t rsrc_words(const void* base, int64_t bytes) {
   const uint64_t a = (uint64_t)(uintptr_t)base;
@@ -476,7 +487,7 @@ __device__ __forceinline__ void load_lds16(u32x4_t rsrc, uint32_t lds_off, uint3
                : "memory");
 }
 
-template <int EPI, int Tn>
+template <int EPI, int Tn, bool SPLIT>
 __global__ __launch_bounds__(NTHR) void k_gemm_kc(GemmParams p) {
   __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * KC_STAGE];
   typedef WaveTile<KC_WM, KC_WN, KC_FM> W;
@@ -485,11 +496,27 @@ __global__ __launch_bounds__(NTHR) void k_gemm_kc(GemmParams p) {
   const int wave = tid >> 6;
   const int wm = wave / KC_WN, wn = wave % KC_WN;
   const int tiles_m = (int)cdiv(p.M, BM), tiles_n = (int)cdiv(p.N, BN);
-  int tm, tn;
-  tile_coords(tiles_m, tiles_n, tm, tn);
+  int tm, tn, split = 0;
+  if constexpr (SPLIT) {
+    // block = (tile, split), tiles row-major: the tiles of the counted rows come first
+    split = (int)(blockIdx.x % (unsigned)p.ksplit);
+    const int t = (int)(blockIdx.x / (unsigned)p.ksplit);
+    tm = t / tiles_n;
+    tn = t % tiles_n;
+  } else {
+    tile_coords(tiles_m, tiles_n, tm, tn);
+  }
   const int m0 = tm * BM, n0 = tn * BN;
   const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
   if (m0 >= m_eff) return;
+  const int nk_all = (int)(p.K / KC_BK);
+  int kt0 = 0, kt1 = nk_all, ks = 1;
+  if constexpr (SPLIT) {
+    ks = splitk_count(p.ksplit, p.part_rows, m_eff, p.N, nk_all);
+    if (split >= ks) return;
+    kt0 = (int)((int64_t)nk_all * split / ks);
+    kt1 = (int)((int64_t)nk_all * (split + 1) / ks);
+  }
 
   // Load instruction q of this wave fills rows (wave*KC_LOADS + q)*8 .. +7 of the operand
   // tile; lane l writes row +l/8 at chunk position l%8, which holds logical chunk
@@ -559,23 +586,90 @@ __global__ __launch_bounds__(NTHR) void k_gemm_kc(GemmParams p) {
   // Each step: this wave's loads of stage kt have landed and its LDS reads of step kt-1
   // are complete (vmcnt 0, lgkmcnt 0); after the barrier the same holds for all waves, so
   // stage kt may be read and the slot of stage kt-1 refilled with stage kt+1.
-  const int nk = (int)(p.K / KC_BK);
-  if (nk > 0) issue(0);
-  for (int kt = 0; kt < nk; ++kt) {
+  if (kt0 < kt1) issue(kt0);
+  for (int kt = kt0; kt < kt1; ++kt) {
     __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt(0) expcnt(7) lgkmcnt(0)
     __syncthreads();
-    if (kt + 1 < nk) issue(kt + 1);
+    if (kt + 1 < kt1) issue(kt + 1);
     compute(kt);
   }
   __syncthreads();  // the epilogue reuses the stage buffers
+  if (SPLIT && ks > 1) {
+    // partial sums of this K range: part[split][row][col], rows in gathered order
+    typedef AccGeo<KC_FM> G;
+#pragma unroll
+    for (int i = 0; i < W::TM_; ++i)
+#pragma unroll
+      for (int r = 0; r < G::R; ++r) {
+        const int row = m0 + wm * W::WTM_ + i * KC_FM + G::row(r, lane);
+        if (row >= m_eff) continue;
+        float* prow = p.part + ((int64_t)split * m_eff + row) * p.N;
+#pragma unroll
+        for (int j = 0; j < W::TN_; ++j) {
+          const int col = n0 + wn * W::WTN_ + j * KC_FM + G::col(lane);
+          if (col < p.N) prow[col] = acc[i][j][r];
+        }
+      }
+    return;
+  }
   gemm_epilogue<EPI, KC_WM, KC_WN, KC_FM, Tn>(p, acc, m0, n0, m_eff, smem);
+}
+
+// Sum of the split-K partials in split order, then the epilogue of element (m, n); four
+// consecutive columns per thread, grid-stride over the counted rows.
+template <int EPI>
+__global__ __launch_bounds__(256) void k_splitk_reduce(GemmParams p) {
+  const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
+  const int ks = splitk_count(p.ksplit, p.part_rows, m_eff, p.N, (int)(p.K / KC_BK));
+  if (ks <= 1) return;
+  const int n4 = p.N / 4;
+  const int64_t total = (int64_t)m_eff * n4;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
+    const int m = (int)(e / n4);
+    const int n = (int)(e % n4) * 4;
+    f32x4_t v = *(const f32x4_t*)(p.part + (int64_t)m * p.N + n);
+    for (int sp = 1; sp < ks; ++sp) v += *(const f32x4_t*)(p.part + ((int64_t)sp * m_eff + m) * p.N + n);
+    const int64_t crow = p.c_rows ? (int64_t)p.c_rows[m] : (int64_t)m;
+    float sh = 0.f;
+    if ((EPI == EPI_F32 || EPI == EPI_ACT_RELU) && p.shift) sh = p.shift[p.s_rows ? p.s_rows[m] : m];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float x = v[q];
+      const int col = n + q;
+      if (EPI == EPI_F32 || EPI == EPI_ACT_RELU) {
+        if (p.bias) x += p.bias[col];
+        x += sh;
+      }
+      if (EPI == EPI_F32) {
+        ((float*)p.C)[crow * p.ldc + col] = x;
+      } else if (EPI == EPI_ACT_RELU) {
+        ((bf16_t*)p.C)[crow * p.ldc + col] = active_bits(x) ? f32_to_bf16(x) : (bf16_t)0;
+      } else if (EPI == EPI_ACT) {
+        ((bf16_t*)p.C)[crow * p.ldc + col] = f32_to_bf16(x);
+      } else if (EPI == EPI_MUL_ACT) {
+        bf16_t* c = (bf16_t*)p.C + crow * p.ldc + col;
+        *c = f32_to_bf16(bf16_to_f32(*c) * x);
+      }
+    }
+  }
 }
 
 template <int EPI, int Tn = 0>
 hipError_t launch_kc(const GemmParams& p, hipStream_t s) {
   const int tiles = (int)(cdiv(p.M, BM) * cdiv(p.N, BN));
   if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL((k_gemm_kc<EPI, Tn>), dim3(tiles), dim3(NTHR), 0, s, p);
+  hipLaunchKernelGGL((k_gemm_kc<EPI, Tn, false>), dim3(tiles), dim3(NTHR), 0, s, p);
+  return hipGetLastError();
+}
+
+// Split-K launch: the GEMM over (tile, split) blocks, then the partial-sum reduction. The
+// split count is decided on the device from the row count, identically in both kernels.
+template <int EPI>
+hipError_t launch_kc_split(const GemmParams& p, hipStream_t s) {
+  const int64_t tiles = cdiv(p.M, BM) * cdiv(p.N, BN);
+  if (tiles == 0) return hipSuccess;
+  hipLaunchKernelGGL((k_gemm_kc<EPI, 0, true>), dim3((unsigned)(tiles * p.ksplit)), dim3(NTHR), 0, s, p);
+  hipLaunchKernelGGL((k_splitk_reduce<EPI>), dim3(1024), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 template <int ALAY, int BLAY, int EPI, int Tn = 0>
@@ -667,6 +761,16 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmParams p) {
 }  // namespace
 
 hipError_t gemm_bf16(int alay, int blay, int epi, const GemmParams& p, hipStream_t s) {
+  if (alay == LAY_KC && blay == LAY_KC && p.K % KC_BK == 0 && !p.k_count && !p.b_rows && p.ksplit > 1 &&
+      p.part && p.N % 4 == 0) {
+    switch (epi) {
+      case EPI_F32: return launch_kc_split<EPI_F32>(p, s);
+      case EPI_ACT_RELU: return launch_kc_split<EPI_ACT_RELU>(p, s);
+      case EPI_ACT: return launch_kc_split<EPI_ACT>(p, s);
+      case EPI_MUL_ACT: return launch_kc_split<EPI_MUL_ACT>(p, s);
+      default: break;
+    }
+  }
   if (alay == LAY_KC && blay == LAY_KC && p.K % KC_BK == 0 && !p.k_count && !p.b_rows) {
     switch (epi) {
       case EPI_F32: return launch_kc<EPI_F32>(p, s);

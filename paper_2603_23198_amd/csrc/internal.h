@@ -53,6 +53,13 @@ struct GemmParams {
   uint16_t* tw_idx;
   int32_t* tw_cnt;
   int tile_cols, tile_slots, n_tiles;
+  // split-K (K-contiguous kernel only; for skinny GEMMs such as the dense-backup rows):
+  // up to `ksplit` K ranges per output tile, chosen on the device from the row count so
+  // that ks * rows <= part_rows; fp32 partial sums go to part [ks][rows][N] and a second
+  // kernel adds them in split order and applies the epilogue. ksplit <= 1: no split.
+  int ksplit;
+  float* part;
+  int part_rows;
 };
 
 // bf16 MFMA GEMM. Requirements: K % 8 == 0; RC layouts need even M/N extents and

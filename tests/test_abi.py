@@ -74,9 +74,10 @@ def _fake_args(dtype, T, d, f, gated=False, **kw):
 def test_workspace_sizes():
     a = _fake_args(b.SFL_BF16, 128, 256, 1024, ell_width=32)
     ws = b.sfl_workspace_size(a, 0)
-    assert ws == 128 * 1024 * 2  # dense-backup rows live in the workspace when not given
+    part = 256 * 1024 * 4  # split-K partial sums of the dense-backup GEMMs: 256-row multiple x max(f, d) fp32
+    assert ws == 128 * 1024 * 2 + part  # dense-backup rows live in the workspace when not given
     a.twell.ovf_dense = 0x2000
-    assert b.sfl_workspace_size(a, 0) == 0  # fused TwELL epilogue: no scratch
+    assert b.sfl_workspace_size(a, 0) == part  # fused TwELL epilogue: no other scratch
     a32 = _fake_args(b.SFL_F32, 64, 256, 1024, ell_width=32)
     a32.twell.ovf_dense = 0x2000
     assert b.sfl_workspace_size(a32, 0) == 64 * 1024 * 4  # fp32: pre-activations staged

@@ -17,7 +17,14 @@ pytestmark = pytest.mark.gpu
 b = pytest.importorskip("paper_2603_23198_amd.binding")
 
 
-def run_forward(w, rows_check=None, use_wupt=False, dense=False, packed_down=False):
+def transposed(W):
+    out = torch.empty((W.shape[1], W.shape[0]), dtype=W.dtype, device="cuda")
+    b.sfl_transpose(W, out)
+    return out
+
+
+def run_forward(w, rows_check=None, use_wupt=False, dense=False, packed_down=False, use_wgatet=False,
+                use_wdownt=False):
     X, Wu, Wd = dev(w.X), dev(w.W_up), dev(w.W_down)
     Wg = dev(w.W_gate) if w.gated else None
     cfg = b.make_cfg(**w.cfg)
@@ -25,20 +32,19 @@ def run_forward(w, rows_check=None, use_wupt=False, dense=False, packed_down=Fal
     bufs = b.alloc_twell(w.T, w.f, dt, cfg)
     Y = torch.full((w.T, w.d), float("nan"), dtype=X.dtype, device="cuda")
     stats = b.alloc_stats()
-    WupT = None
-    if use_wupt:
-        WupT = torch.empty((w.f, w.d), dtype=X.dtype, device="cuda")
-        b.sfl_transpose(Wu, WupT)
+    WupT = transposed(Wu) if use_wupt else None
+    WgT = transposed(Wg) if use_wgatet else None
+    WdT = transposed(Wd) if use_wdownt else None
     WdP = None
     if packed_down:
         WdP = torch.empty_like(Wd)
         b.sfl_pack_down_weights(Wd, WdP)
-    args = b.ffn_args(X, Wu, Wd, cfg, Y=Y, bufs=bufs, W_gate=Wg, W_upT=WupT, W_down_packed=WdP,
-                      bias_f=dev(w.bias_f), shift_t=dev(w.shift_t), stats=stats)
+    kw = dict(Y=Y, bufs=bufs, W_gate=Wg, W_upT=WupT, W_gateT=WgT, W_downT=WdT, W_down_packed=WdP,
+              bias_f=dev(w.bias_f), shift_t=dev(w.shift_t), stats=stats)
+    args = b.ffn_args(X, Wu, Wd, cfg, **kw)
     ws_bytes = b.sfl_workspace_size(args, 2 if dense else 0)
     ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device="cuda")
-    args = b.ffn_args(X, Wu, Wd, cfg, Y=Y, bufs=bufs, W_gate=Wg, W_upT=WupT, W_down_packed=WdP,
-                      bias_f=dev(w.bias_f), shift_t=dev(w.shift_t), stats=stats, workspace=ws)
+    args = b.ffn_args(X, Wu, Wd, cfg, **kw, workspace=ws)
     (b.sfl_dense_ffn_baseline if dense else b.sfl_ffn_forward)(args)
     torch.cuda.synchronize()
     return Y, bufs, stats, cfg
@@ -281,3 +287,24 @@ def test_transposed_up_weights_match_row_contiguous_ones(T, d, f):
     check_pattern(twell_views(b2, T, f, cfg), Zref, rows, f, cfg.tile_cols, cfg.tile_slots)
 
 
+@pytest.mark.parametrize("gated", [False, True])
+def test_transposed_gate_and_down_copies(gated):
+    """W_gate^T and W_down^T move the gate projection, the dense-backup down GEMM and the
+    dense baseline's GEMMs to the K-contiguous kernel; results still meet the oracle and the
+    activity pattern. Rows forced active exercise the dense-backup rows."""
+    if gated:
+        w = wl.make_ffn("wt-gated", "bf16", 700, 512, 2048, seed=21, sparsity=0.99, ell_width=64, gated=True)
+    else:
+        w = wl.make_ffn("wt", "bf16", 700, 512, 2048, seed=22, sparsity=0.99, ell_width=64)
+    w.shift_t[:40] = 100.0  # dense-backup rows
+    rows = sample_rows(w.T, 96, 9, extra=range(0, 40, 3))
+    Yref, Zref = oracle_rows(w, rows)
+    cfg = b.make_cfg(**w.cfg)
+    for dense in (False, True):
+        Y0, b0, _, _ = run_forward(w, dense=dense)
+        Y1, b1, st1, _ = run_forward(w, dense=dense, use_wupt=True, use_wgatet=gated, use_wdownt=True)
+        assert rel_l2(to_f64(Y1)[rows], Yref) <= 2e-2
+        assert rel_l2(to_f64(Y1), to_f64(Y0)) <= 1e-2
+        if not dense:
+            assert b.read_stats(st1)["n_ovf_rows"] >= 40
+            check_pattern(twell_views(b1, w.T, w.f, cfg), Zref, rows, w.f, cfg.tile_cols, cfg.tile_slots)
