@@ -148,8 +148,8 @@ class Bench:
         bufs = b.alloc_twell(w.T, w.f, "bf16", cfg)
         Y = t.empty((w.T, w.d), dtype=t.bfloat16, device="cuda")
         stats = b.alloc_stats()
-        WdP = WupT = WgT = WdT = None
-        if packed and not w.gated and w.d % 512 == 0:
+        WdP = WuP = WupT = WgT = WdT = None
+        if packed and w.dtype == "bf16" and w.d % 512 == 0:
             WdP = t.empty_like(Wd)
             b.sfl_pack_down_weights(Wd, WdP)
 
@@ -165,7 +165,10 @@ class Bench:
             WupT, WdT = transposed(Wu), transposed(Wd)
             if w.gated:
                 WgT = transposed(Wg)
-        kw = dict(Y=Y, bufs=bufs, W_gate=Wg, W_upT=WupT, W_gateT=WgT, W_downT=WdT, W_down_packed=WdP,
+                if packed and w.d % 512 == 0:
+                    WuP = t.empty_like(Wu)
+                    b.sfl_pack_down_weights(WupT, WuP)
+        kw = dict(Y=Y, bufs=bufs, W_gate=Wg, W_upT=WupT, W_gateT=WgT, W_downT=WdT, W_down_packed=WdP, W_up_packed=WuP,
                   bias_f=self.dev(w.bias_f), shift_t=self.dev(w.shift_t), stats=stats)
         a0 = b.ffn_args(X, Wu, Wd, cfg, **kw)
         ws = t.empty(max(1, b.sfl_workspace_size(a0)), dtype=t.uint8, device="cuda")

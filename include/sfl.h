@@ -129,9 +129,9 @@ typedef struct {
  *  W_gate    [d][f], gated only
  *  W_upT     optional [f][d] copy of W_up transposed (bf16 only; ignored for F32).
  *            Non-gated: the up projection reads it instead of W_up (K-contiguous B
- *            operand). Gated: read by the fused up-dot; when NULL the gated path
- *            transposes W_up into the workspace. sfl_dense_ffn_baseline reads it for
- *            its X W_up GEMM the same way.
+ *            operand). Gated: the dense-backup rows' X W_up GEMM reads it, and the
+ *            forward packs W_up_packed from it when that is NULL.
+ *            sfl_dense_ffn_baseline reads it for its X W_up GEMM the same way.
  *  W_gateT   optional [f][d] copy of W_gate transposed (bf16, gated only): the gate
  *            projection (forward, sfl_up_projection, dense baseline) reads it instead
  *            of W_gate.
@@ -144,8 +144,13 @@ typedef struct {
  *  W_down_packed  optional bf16 copy of W_down in the slice-major layout written by
  *            sfl_pack_down_weights ([d/64][f][64]); the sparse down projection reads
  *            64-column slices of W_down, and this layout makes each slice one
- *            contiguous block. When NULL (bf16, d % 512 == 0) the forward builds it in
- *            the workspace on every call.
+ *            contiguous block. When NULL (bf16, d % 512 == 0; gated or not) the forward
+ *            builds it in the workspace on every call.
+ *  W_up_packed  optional bf16 slice-major copy of W_up for the gated path:
+ *            [d/64][f][64] with element [s][n][c] = W_up[64 s + c][n], i.e.
+ *            sfl_pack_down_weights applied to W_up^T. The gated up-dots read 64-row
+ *            slices of W_up; when NULL the forward builds it in the workspace on every
+ *            call (from W_upT, itself transposed into the workspace when NULL).
  *  bias_f    optional float32 [f] added to every pre-activation of column n
  *  shift_t   optional float32 [T] added to every pre-activation of row t
  *            (both are extensions; NULL/NULL is the paper's bias-free FFN)
@@ -169,6 +174,7 @@ typedef struct {
   const void* W_gateT;
   const void* W_downT;
   const void* W_down_packed;
+  const void* W_up_packed;
   const float* bias_f;
   const float* shift_t;
   sfl_twell_cfg_t cfg;

@@ -55,6 +55,7 @@ class FfnArgs(Structure):
     _fields_ = [("dtype", c_int), ("gated", c_int32), ("T", c_int64), ("d", c_int64), ("f", c_int64),
                 ("X", c_void_p), ("W_gate", c_void_p), ("W_up", c_void_p), ("W_down", c_void_p),
                 ("W_upT", c_void_p), ("W_gateT", c_void_p), ("W_downT", c_void_p), ("W_down_packed", c_void_p),
+                ("W_up_packed", c_void_p),
                 ("bias_f", c_void_p), ("shift_t", c_void_p),
                 ("cfg", Cfg),
                 ("Y", c_void_p), ("twell", Twell), ("stats", c_void_p), ("workspace", c_void_p),
@@ -172,7 +173,8 @@ def read_stats(stats_tensor):
 
 
 def ffn_args(X, W_up, W_down, cfg, *, Y=None, bufs=None, W_gate=None, W_upT=None, W_gateT=None, W_downT=None,
-             W_down_packed=None, bias_f=None, shift_t=None, stats=None, workspace=None, events=None):
+             W_down_packed=None, W_up_packed=None, bias_f=None, shift_t=None, stats=None, workspace=None,
+             events=None):
     T, d = X.shape
     f = W_down.shape[0]
     a = FfnArgs()
@@ -181,7 +183,7 @@ def ffn_args(X, W_up, W_down, cfg, *, Y=None, bufs=None, W_gate=None, W_upT=None
     a.T, a.d, a.f = T, d, f
     a.X, a.W_gate, a.W_up, a.W_down, a.W_upT = _ptr(X), _ptr(W_gate), _ptr(W_up), _ptr(W_down), _ptr(W_upT)
     a.W_gateT, a.W_downT = _ptr(W_gateT), _ptr(W_downT)
-    a.W_down_packed = _ptr(W_down_packed)
+    a.W_down_packed, a.W_up_packed = _ptr(W_down_packed), _ptr(W_up_packed)
     a.bias_f, a.shift_t = _ptr(bias_f), _ptr(shift_t)
     a.cfg = cfg
     a.Y = _ptr(Y)

@@ -78,7 +78,7 @@ sfl_status_t check_forward(const sfl_ffn_args_t* a, bool need_output = true) {
   if (a->T > INT32_MAX || a->d > INT32_MAX) return SFL_E_UNSUPPORTED;
   if (a->dtype == SFL_BF16 && (a->d % 64 != 0 || a->f % 64 != 0)) return SFL_E_UNSUPPORTED;
   if (a->gated && a->dtype != SFL_BF16) return SFL_E_UNSUPPORTED;
-  if (a->gated && !(a->d == 512 || a->d == 1024 || a->d == 2048 || a->d == 4096)) return SFL_E_UNSUPPORTED;
+  if (a->gated && a->d % 512 != 0) return SFL_E_UNSUPPORTED;
   // the bf16 GEMMs address each operand with 32-bit byte offsets
   const int64_t lim = (int64_t)1 << 31;
   const int64_t es = a->dtype == SFL_BF16 ? 2 : 4;
@@ -98,6 +98,9 @@ struct FwdPlan {
   void* ovf_dense = nullptr; // dense-backup rows when the caller gave none [cap][f]
   void* WupT = nullptr;      // gated: W_up transposed [f][d]
   void* WdP = nullptr;       // slice-major W_down when the caller gave none [d/64][f][64]
+  void* WuP = nullptr;       // gated: slice-major W_up when the caller gave none [d/64][f][64]
+  float* part_u = nullptr;   // gated: per-XCD partial up-dots [8][T][K]
+  void* hval = nullptr;      // gated: h = g * u of the ELL entries [T][K] bf16
   float* part = nullptr;     // split-K partial sums of the dense-backup GEMMs [part_rows][max(f, d)]
   int part_rows = 0;
   size_t bytes = 0;
@@ -108,7 +111,7 @@ struct FwdPlan {
 constexpr int kMaxSplit = 8;
 constexpr int64_t kPartRows = 4096;
 
-bool packed_gather(const sfl_ffn_args_t& a) { return a.dtype == SFL_BF16 && !a.gated && a.d % 512 == 0; }
+bool packed_gather(const sfl_ffn_args_t& a) { return a.dtype == SFL_BF16 && a.d % 512 == 0; }
 
 int64_t align_rows(int64_t r) { return (r + 255) / 256 * 256; }
 
@@ -118,8 +121,14 @@ FwdPlan plan_forward(const sfl_ffn_args_t& a, void* ws) {
   const int64_t cap = capacity_of(a.cfg, a.T);
   if (!fused_twell(a)) p.Z = (float*)c.take((size_t)a.T * a.f * 4);
   if (!a.twell.ovf_dense) p.ovf_dense = c.take((size_t)cap * a.f * elem_size(a.dtype));
-  if (a.gated && !a.W_upT) p.WupT = c.take((size_t)a.f * a.d * elem_size(a.dtype));
+  if (a.gated && !a.W_up_packed && !a.W_upT) p.WupT = c.take((size_t)a.f * a.d * elem_size(a.dtype));
   if (packed_gather(a) && !a.W_down_packed) p.WdP = c.take((size_t)a.f * a.d * 2);
+  if (a.gated && !a.W_up_packed) p.WuP = c.take((size_t)a.f * a.d * 2);
+  if (a.gated) {
+    const int64_t K = std::max<int64_t>(a.cfg.ell_width, 1);
+    p.part_u = (float*)c.take((size_t)8 * a.T * K * 4);
+    p.hval = c.take((size_t)a.T * K * 2);
+  }
   if (a.dtype == SFL_BF16 && cap > 0) {
     p.part_rows = (int)std::min<int64_t>(align_rows(cap), kPartRows);
     p.part = (float*)c.take((size_t)p.part_rows * std::max(a.f, a.d) * 4);
@@ -333,22 +342,33 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
   SFL_HIP(launch_ovf_list(T, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s));
   ev.record(2, s);
   // 3. sparse down projection of the ELL rows
-  const void* WupT = a->W_upT;  // gated: W_up^T, given or built in the workspace
-  if (a->gated) {
-    if (!WupT) {
-      SFL_HIP(launch_transpose(a->W_up, plan.WupT, d, f, 2, s));
-      WupT = plan.WupT;
-    }
-    SFL_HIP(launch_gated_gather(vb, T, d, a->cfg.ell_width, tw.ell_val, tw.ell_idx, tw.row_nnz, tw.row_ovf, a->X,
-                                WupT, a->W_down, a->Y, s));
-  } else if (packed_gather(*a)) {
+  const void* WupT = a->W_upT;  // gated: W_up^T, given or built in the workspace when needed
+  if (packed_gather(*a)) {
     const void* WdP = a->W_down_packed;
     if (!WdP) {
       SFL_HIP(launch_pack_down(a->W_down, plan.WdP, f, d, s));
       WdP = plan.WdP;
     }
-    SFL_HIP(launch_gather_down_packed(T, d, f, a->cfg.ell_width, tw.ell_val, tw.ell_idx, tw.row_nnz, tw.row_ovf,
-                                      WdP, a->Y, s));
+    const void* hv = tw.ell_val;
+    if (a->gated) {
+      // Alg. 2 in two passes over slice-major weights: u = x . W_up[:, n] per entry, then
+      // the same down-projection gather as the non-gated layer with h = g * u
+      const void* WuP = a->W_up_packed;
+      if (!WuP) {
+        if (!WupT) {
+          SFL_HIP(launch_transpose(a->W_up, plan.WupT, d, f, 2, s));
+          WupT = plan.WupT;
+        }
+        SFL_HIP(launch_pack_down(WupT, plan.WuP, f, d, s));
+        WuP = plan.WuP;
+      }
+      SFL_HIP(launch_gated_updot(T, d, f, a->cfg.ell_width, tw.ell_idx, tw.row_nnz, tw.row_ovf, a->X, WuP,
+                                 plan.part_u, s));
+      SFL_HIP(launch_gated_h(T, a->cfg.ell_width, tw.ell_val, tw.row_nnz, tw.row_ovf, plan.part_u, plan.hval, s));
+      hv = plan.hval;
+    }
+    SFL_HIP(launch_gather_down_packed(T, d, f, a->cfg.ell_width, hv, tw.ell_idx, tw.row_nnz, tw.row_ovf, WdP, a->Y,
+                                      s));
   } else {
     SFL_HIP(launch_gather_down(vb, T, d, a->cfg.ell_width, tw.ell_val, tw.ell_idx, tw.row_nnz, tw.row_ovf,
                                a->W_down, a->Y, s));

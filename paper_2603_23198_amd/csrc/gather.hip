@@ -1,16 +1,18 @@
 // Sparse down projections from the compact ELL rows of the hybrid format.
 //
 // Non-gated (Alg. 3, sparse part): y[t, :] = sum_e v[t, e] * W_down[n[t, e], :].
-// The work is split into (d-slice of 128 columns) x (block of tokens). A wave owns one
-// token at a time and one 128-column slice: each lane accumulates two columns in fp32
-// while the wave walks the token's ELL entries in order (so the sum order is fixed),
-// reading one 256-byte W_down row segment per entry. Workgroups are laid out so that all
-// workgroups resident on one XCD work on the same slice: the slice of W_down
-// (f x 256 bytes) is then shared in that XCD's L2 by every token it processes.
+//  * k_gather_down (any dtype, any d): (d-slice of 128 columns) x (block of tokens); a
+//    wave owns one token at a time and walks its ELL entries in order, reading one
+//    256-byte W_down row segment per entry.
+//  * k_gather_down_b16 (bf16, d % 512 == 0): over a slice-major copy of W_down, each XCD
+//    walking its own 64-column slices so that one 2 MiB slice stays in its L2 while every
+//    token streams through it (see below).
 //
 // Gated (Alg. 2 / eq. sec3:eq:twell_to_dense_fused_matmul): per active gate value g at
-// column n, u = x[t] . W_up[:, n] (read as the contiguous row n of W_up^T), and
-// y[t] += (g * u) W_down[n]. One wave per token keeps x[t] and y[t] in registers.
+// column n, u = x[t] . W_up[:, n] and y[t] += (g * u) W_down[n]. Done in two passes with
+// the same slice walk: k_gated_updot forms u for every entry (per-XCD partial sums over
+// that XCD's slices of d, from a slice-major copy of W_up), k_gated_h combines them into
+// h = g * u, and k_gather_down_b16 does the down projection with h as the values.
 #include "common.h"
 #include "internal.h"
 
@@ -217,6 +219,104 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
   }
 }
 
+// ---- gated up-dot over slice-major W_up^T (Alg. 2's u, split over d) --------------------
+// u[t, e] = x[t] . W_up[:, n[t, e]] for every ELL entry, as 8 per-XCD partial sums: XCD x
+// covers the 64-column slices x, x+8, ... of d exactly like the down-projection gather
+// (same token blocks, same slice walk, same L2 residency of one 2 MiB slice of W_up^T),
+// and adds its slices' partial dot products per entry in LDS. Group g (8 lanes) of a wave
+// takes entry q + u * NGRP + g; each lane dots its 8 columns (bf16 dot2), the group sums
+// its 8 lanes, lane 0 of the group adds that to the entry's LDS sum. A token is always
+// handled by the same wave, so each entry's sum is updated in slice order.
+__global__ __launch_bounds__(GATHER_WAVES * 64) void k_gated_updot(
+    int64_t T, int64_t d, int64_t f, int K, const uint16_t* __restrict__ ell_idx, const int32_t* __restrict__ row_nnz,
+    const uint8_t* __restrict__ row_ovf, const bf16_t* __restrict__ X, const bf16_t* __restrict__ WuP,
+    float* __restrict__ part_u, int n_slices, int tpw) {
+  extern __shared__ uint32_t ent[];  // [tpw][K] indices, [tpw][K] partial sums, [tpw] counts
+  float* us = (float*)(ent + (size_t)tpw * K);
+  int* cnt_s = (int*)(us + (size_t)tpw * K);
+  const int xcd = blockIdx.x & 7;
+  const int64_t t0 = (int64_t)(blockIdx.x >> 3) * tpw;
+  const int l = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int grp = l / LPR, sub = l % LPR;
+  for (int i = threadIdx.x; i < tpw; i += blockDim.x) {
+    const int64_t t = t0 + i;
+    cnt_s[i] = (t < T && !row_ovf[t]) ? row_nnz[t] : -1;
+  }
+  __syncthreads();
+  for (int i = wave; i < tpw; i += GATHER_WAVES) {
+    const int c = cnt_s[i];
+    const int64_t t = t0 + i;
+    for (int e = l; e < c; e += 64) {
+      ent[i * K + e] = (uint32_t)ell_idx[t * K + e];
+      us[i * K + e] = 0.f;
+    }
+  }
+  __syncthreads();
+  const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc((void*)WuP, (short)0, 0x7fffffff, 0x00020000);
+  constexpr uint32_t row_b = SLICE2 * 2;
+  for (int slice = xcd; slice < n_slices; slice += 8) {
+    const uint32_t col_b = (uint32_t)(slice * f * SLICE2 * 2) + (uint32_t)sub * 16u;
+    for (int i = wave; i < tpw; i += GATHER_WAVES) {
+      const int nnz = __builtin_amdgcn_readfirstlane(cnt_s[i]);
+      if (nnz <= 0) continue;
+      // this lane's 8 columns of x[t] in the slice, as bf16 pairs
+      const u32x4_t xv = *(const u32x4_t*)(X + (t0 + i) * d + (int64_t)slice * SLICE2 + sub * 8);
+      const uint32_t* er = ent + i * K;
+      float* ur = us + i * K;
+      for (int q = 0; q < nnz; q += NGRP * GU) {
+        u32x4_t w[GU];
+#pragma unroll
+        for (int u = 0; u < GU; ++u) {
+          const int e = q + u * NGRP + grp;
+          const uint32_t off = e < nnz ? er[e] * row_b + col_b : 0x80000000u;
+          w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0));
+        }
+#pragma unroll
+        for (int u = 0; u < GU; ++u) {
+          float s = 0.f;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            // copy the words out first: a bit cast applied straight to a vector element
+            // is compiled as a cast of element 0
+            const uint32_t xw = xv[j], ww = w[u][j];
+            s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, xw), __builtin_bit_cast(bf16x2_t, ww), s,
+                                                false);
+          }
+#pragma unroll
+          for (int o = 1; o < LPR; o <<= 1) s += __shfl_xor(s, o, 64);
+          const int e = q + u * NGRP + grp;
+          if (sub == 0 && e < nnz) ur[e] += s;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  for (int i = wave; i < tpw; i += GATHER_WAVES) {
+    const int c = cnt_s[i];
+    const int64_t t = t0 + i;
+    for (int e = l; e < c; e += 64) part_u[((int64_t)xcd * T + t) * K + e] = us[i * K + e];
+  }
+}
+
+// h[t, e] = g[t, e] * sum over the 8 XCD partials of u[t, e] (in XCD order), rounded to
+// bf16 like every stored activation; entries past row_nnz and dense-backup rows untouched.
+__global__ __launch_bounds__(256) void k_gated_h(int64_t T, int K, const bf16_t* __restrict__ ell_val,
+                                                 const int32_t* __restrict__ row_nnz,
+                                                 const uint8_t* __restrict__ row_ovf,
+                                                 const float* __restrict__ part_u, bf16_t* __restrict__ h) {
+  const int64_t total = T * (int64_t)K;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int64_t t = i / K;
+    const int e = (int)(i % K);
+    if (row_ovf[t] || e >= row_nnz[t]) continue;
+    float u = 0.f;
+#pragma unroll
+    for (int x = 0; x < 8; ++x) u += part_u[(int64_t)x * total + i];
+    h[i] = f32_to_bf16(bf16_to_f32(ell_val[i]) * u);
+  }
+}
+
 // out[s][n][c] = W[n][SLICE s + c]: 16 bytes per thread, reads coalesced along rows.
 __global__ __launch_bounds__(256) void k_pack_down(const bf16_t* __restrict__ W, bf16_t* __restrict__ out, int64_t f,
                                                    int64_t d) {
@@ -229,77 +329,9 @@ __global__ __launch_bounds__(256) void k_pack_down(const bf16_t* __restrict__ W,
   *(u32x4_t*)(out + ((s * f + n) * SLICE2 + c8 * 8)) = *(const u32x4_t*)(W + n * d + c * 8);
 }
 
-// d = NQ * 512 (each lane holds 8 consecutive columns of every 512-column group).
-template <int NQ>
-__global__ __launch_bounds__(256) void k_gated_gather(int64_t T, int K, const bf16_t* __restrict__ ell_val,
-                                                      const uint16_t* __restrict__ ell_idx,
-                                                      const int32_t* __restrict__ row_nnz,
-                                                      const uint8_t* __restrict__ row_ovf,
-                                                      const bf16_t* __restrict__ X, const bf16_t* __restrict__ WupT,
-                                                      const bf16_t* __restrict__ Wd, bf16_t* __restrict__ Y) {
-  constexpr int64_t d = NQ * 512;
-  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T || __builtin_amdgcn_readfirstlane(row_ovf[t])) return;
-  const int l = threadIdx.x & 63;
-  float x[NQ][8], y[NQ][8];
-#pragma unroll
-  for (int q = 0; q < NQ; ++q) {
-    const u32x4_t w = *(const u32x4_t*)(X + t * d + q * 512 + l * 8);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      x[q][2 * i] = bf16lo(w[i]);
-      x[q][2 * i + 1] = bf16hi(w[i]);
-      y[q][2 * i] = 0.f;
-      y[q][2 * i + 1] = 0.f;
-    }
-  }
-  const int nnz = __builtin_amdgcn_readfirstlane(row_nnz[t]);
-  const bf16_t* ev = ell_val + t * (int64_t)K;
-  const uint16_t* ei = ell_idx + t * (int64_t)K;
-  for (int e0 = 0; e0 < nnz; e0 += 64) {
-    const int e = e0 + l;
-    const int n_l = e < nnz ? (int)ei[e] : 0;
-    const float g_l = e < nnz ? bf16_to_f32(ev[e]) : 0.f;
-    const int cnt = min(64, nnz - e0);
-    for (int q0 = 0; q0 < cnt; ++q0) {
-      const int64_t n = readlane_i(n_l, q0);
-      const float gv = readlane_f(g_l, q0);
-      u32x4_t wu[NQ], wd[NQ];
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        wu[q] = *(const u32x4_t*)(WupT + n * d + q * 512 + l * 8);
-        wd[q] = *(const u32x4_t*)(Wd + n * d + q * 512 + l * 8);
-      }
-      float part = 0.f;
-#pragma unroll
-      for (int q = 0; q < NQ; ++q)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          part = fmaf(x[q][2 * i], bf16lo(wu[q][i]), part);
-          part = fmaf(x[q][2 * i + 1], bf16hi(wu[q][i]), part);
-        }
-      const float u = wave_sum<float>(part);
-      const float h = gv * u;
-#pragma unroll
-      for (int q = 0; q < NQ; ++q)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          y[q][2 * i] = fmaf(h, bf16lo(wd[q][i]), y[q][2 * i]);
-          y[q][2 * i + 1] = fmaf(h, bf16hi(wd[q][i]), y[q][2 * i + 1]);
-        }
-    }
-  }
-#pragma unroll
-  for (int q = 0; q < NQ; ++q) {
-    u32x4_t o;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      o[i] = (uint32_t)f32_to_bf16(y[q][2 * i]) | ((uint32_t)f32_to_bf16(y[q][2 * i + 1]) << 16);
-    *(u32x4_t*)(Y + t * d + q * 512 + l * 8) = o;
-  }
-}
-
 }  // namespace
+
+static int slice_walk_tpw(int64_t T, int64_t per_tok);
 
 hipError_t launch_gather_down(int val_bf16, int64_t T, int64_t d, int K, const void* ell_val,
                               const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
@@ -324,15 +356,8 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
   if (d % (8 * SLICE2) != 0) return hipErrorInvalidValue;
   const int n_slices = (int)(d / SLICE2);
 
-  // Tokens per workgroup: at most what the LDS budget holds (one workgroup per CU). A
-  // token block goes to every XCD (each XCD covers its own slices), so the grid is 8 x the
-  // number of blocks; the blocks are sized so that each XCD's 32 CUs get whole rounds.
   const int64_t per_tok = (int64_t)std::max(K, 1) * 4 + 4;
-  const int64_t tpw_max = std::max<int64_t>(1, std::min<int64_t>(GATHER_LDS / 1024, GATHER_LDS / per_tok));
-  const int64_t wg_per_cu = std::max<int64_t>(1, (160 * 1024) / (tpw_max * per_tok));
-  const int64_t slots = 32 * std::min<int64_t>(wg_per_cu, 2048 / (GATHER_WAVES * 64));
-  const int64_t rounds = cdiv(T, tpw_max * slots);
-  const int tpw = (int)std::max<int64_t>(1, cdiv(T, rounds * slots));
+  const int tpw = slice_walk_tpw(T, per_tok);
   const int64_t blocks = cdiv(T, tpw);
   const size_t lds = (size_t)tpw * per_tok;
   if (lds > 160 * 1024) return hipErrorInvalidValue;
@@ -347,32 +372,51 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
   return hipGetLastError();
 }
 
+// Token blocks of the slice-walking kernels: at most what the LDS budget holds (one
+// workgroup per CU); each block goes to every XCD (each XCD covers its own slices), and the
+// blocks are sized so that each XCD's 32 CUs get whole rounds.
+static int slice_walk_tpw(int64_t T, int64_t per_tok) {
+  const int64_t tpw_max = std::max<int64_t>(1, std::min<int64_t>(GATHER_LDS / 1024, GATHER_LDS / per_tok));
+  const int64_t wg_per_cu = std::max<int64_t>(1, (160 * 1024) / (tpw_max * per_tok));
+  const int64_t slots = 32 * std::min<int64_t>(wg_per_cu, 2048 / (GATHER_WAVES * 64));
+  const int64_t rounds = cdiv(T, tpw_max * slots);
+  return (int)std::max<int64_t>(1, cdiv(T, rounds * slots));
+}
+
+hipError_t launch_gated_updot(int64_t T, int64_t d, int64_t f, int K, const uint16_t* ell_idx, const int32_t* row_nnz,
+                              const uint8_t* row_ovf, const void* X, const void* WuP, float* part_u, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  if (d % (8 * SLICE2) != 0) return hipErrorInvalidValue;
+  const int64_t per_tok = (int64_t)std::max(K, 1) * 8 + 4;
+  const int tpw = slice_walk_tpw(T, per_tok);
+  const int64_t blocks = cdiv(T, tpw);
+  const size_t lds = (size_t)tpw * per_tok;
+  if (lds > 160 * 1024) return hipErrorInvalidValue;
+  if (lds > 65536) {
+    const hipError_t e =
+        hipFuncSetAttribute((const void*)k_gated_updot, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k_gated_updot, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), lds, s, T, d, f, K, ell_idx,
+                     row_nnz, row_ovf, (const bf16_t*)X, (const bf16_t*)WuP, part_u, (int)(d / SLICE2), tpw);
+  return hipGetLastError();
+}
+
+hipError_t launch_gated_h(int64_t T, int K, const void* ell_val, const int32_t* row_nnz, const uint8_t* row_ovf,
+                          const float* part_u, void* h, hipStream_t s) {
+  if (T == 0 || K == 0) return hipSuccess;
+  const int64_t n = T * (int64_t)K;
+  const unsigned grid = (unsigned)std::min<int64_t>(cdiv(n, 256), 4096);
+  hipLaunchKernelGGL(k_gated_h, dim3(grid), dim3(256), 0, s, T, K, (const bf16_t*)ell_val, row_nnz, row_ovf, part_u,
+                     (bf16_t*)h);
+  return hipGetLastError();
+}
+
 hipError_t launch_pack_down(const void* W, void* out, int64_t f, int64_t d, hipStream_t s) {
   const int64_t n = f * (d / 8);
   if (n == 0) return hipSuccess;
   hipLaunchKernelGGL(k_pack_down, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, s, (const bf16_t*)W, (bf16_t*)out, f, d);
   return hipGetLastError();
-}
-
-hipError_t launch_gated_gather(int val_bf16, int64_t T, int64_t d, int K, const void* ell_val,
-                               const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
-                               const void* X, const void* WupT, const void* Wd, void* Y, hipStream_t s) {
-  if (!val_bf16) return hipErrorInvalidValue;
-  if (T == 0) return hipSuccess;
-  const dim3 grid((unsigned)cdiv(T, 4));
-#define SFL_GG(NQ)                                                                                          \
-  if (d == NQ * 512) {                                                                                      \
-    hipLaunchKernelGGL(k_gated_gather<NQ>, grid, dim3(256), 0, s, T, K, (const bf16_t*)ell_val, ell_idx,   \
-                       row_nnz, row_ovf, (const bf16_t*)X, (const bf16_t*)WupT, (const bf16_t*)Wd,         \
-                       (bf16_t*)Y);                                                                         \
-    return hipGetLastError();                                                                               \
-  }
-  SFL_GG(1)
-  SFL_GG(2)
-  SFL_GG(4)
-  SFL_GG(8)
-#undef SFL_GG
-  return hipErrorInvalidValue;
 }
 
 }  // namespace sfl

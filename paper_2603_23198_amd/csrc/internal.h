@@ -94,12 +94,13 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int ell_wi
                                      const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
                                      const void* W_packed, void* Y, hipStream_t s);
 hipError_t launch_pack_down(const void* W, void* out, int64_t f, int64_t d, hipStream_t s);
+// Gated, two passes over slice-major copies: per-XCD partial up-dots u of every ELL entry
+// (part_u [8][T][K] fp32), then h = g * u (bf16, [T][K]) for the down-projection gather.
+hipError_t launch_gated_updot(int64_t T, int64_t d, int64_t f, int K, const uint16_t* ell_idx, const int32_t* row_nnz,
+                              const uint8_t* row_ovf, const void* X, const void* WuP, float* part_u, hipStream_t s);
+hipError_t launch_gated_h(int64_t T, int K, const void* ell_val, const int32_t* row_nnz, const uint8_t* row_ovf,
+                          const float* part_u, void* h, hipStream_t s);
 // Gated fused up-dot + down (Alg. 2) from the ELL rows of the gate pattern.
-hipError_t launch_gated_gather(int val_bf16, int64_t T, int64_t d, int ell_width, const void* ell_val,
-                               const uint16_t* ell_idx, const int32_t* row_nnz,
-                               const uint8_t* row_ovf, const void* X, const void* W_upT,
-                               const void* W_down, void* Y, hipStream_t s);
-
 // --------------------------------------------------------- backward ----
 // (declared in backward.h)
 

@@ -24,7 +24,7 @@ def transposed(W):
 
 
 def run_forward(w, rows_check=None, use_wupt=False, dense=False, packed_down=False, use_wgatet=False,
-                use_wdownt=False):
+                use_wdownt=False, packed_up=False):
     X, Wu, Wd = dev(w.X), dev(w.W_up), dev(w.W_down)
     Wg = dev(w.W_gate) if w.gated else None
     cfg = b.make_cfg(**w.cfg)
@@ -39,7 +39,11 @@ def run_forward(w, rows_check=None, use_wupt=False, dense=False, packed_down=Fal
     if packed_down:
         WdP = torch.empty_like(Wd)
         b.sfl_pack_down_weights(Wd, WdP)
-    kw = dict(Y=Y, bufs=bufs, W_gate=Wg, W_upT=WupT, W_gateT=WgT, W_downT=WdT, W_down_packed=WdP,
+    WuP = None
+    if packed_up:
+        WuP = torch.empty_like(Wu)
+        b.sfl_pack_down_weights(transposed(Wu), WuP)
+    kw = dict(Y=Y, bufs=bufs, W_gate=Wg, W_upT=WupT, W_gateT=WgT, W_downT=WdT, W_down_packed=WdP, W_up_packed=WuP,
               bias_f=dev(w.bias_f), shift_t=dev(w.shift_t), stats=stats)
     args = b.ffn_args(X, Wu, Wd, cfg, **kw)
     ws_bytes = b.sfl_workspace_size(args, 2 if dense else 0)
@@ -225,9 +229,14 @@ def test_gated_forward(T):
     assert rel_l2(to_f64(Y), Yref) <= 2e-2
     Yd, _, _, _ = run_forward(w, dense=True)
     assert rel_l2(to_f64(Yd), Yref) <= 2e-2
-    # with a caller-provided W_up^T the result is identical
+    # with caller-provided W_up^T, or slice-major copies of W_up and W_down, the result is
+    # identical (the same kernels read copies made outside instead of inside the call)
     Y2, _, _, _ = run_forward(w, use_wupt=True)
     assert torch.equal(Y.view(torch.int16), Y2.view(torch.int16))
+    Y3, _, _, _ = run_forward(w, packed_up=True, packed_down=True)
+    assert torch.equal(Y.view(torch.int16), Y3.view(torch.int16))
+    Y4, _, _, _ = run_forward(w)
+    assert torch.equal(Y.view(torch.int16), Y4.view(torch.int16))  # deterministic
 
 
 def test_gated_c3_sampled():
