@@ -259,7 +259,10 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* args, sfl_stream_t stream);
 
 /* The pre-activation Z = X W + b + s of the forward's up (or gate) projection,
  * as float32 [T][f], computed by the same GEMM main loop as sfl_ffn_forward.
- * Uses args->{dtype, gated, T, d, f, X, W_up or W_gate, W_upT, bias_f, shift_t}. */
+ * Uses args->{dtype, gated, T, d, f, X, W_up or W_gate, W_upT or W_gateT, bias_f,
+ * shift_t}, and args->workspace (sfl_workspace_size(args, 0) bytes) for batches of at
+ * most 256 rows given W_upT / W_gateT, whose GEMM splits K across blocks (as the
+ * forward's does). */
 sfl_status_t sfl_up_projection(const sfl_ffn_args_t* args, float* Z, sfl_stream_t stream);
 
 /* Sparse FFN backward (see sfl_ffn_bwd_args_t). BF16 only. */

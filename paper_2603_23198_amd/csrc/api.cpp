@@ -60,9 +60,17 @@ struct Events {
     if ((x) != hipSuccess) return SFL_E_HIP; \
   } while (0)
 
+// A batch too small to fill the GPU with whole 256 x 256 output tiles (decode-like T):
+// its K-contiguous GEMMs split K across blocks. The up (gate) projection then writes the
+// fp32 pre-activations and the standalone pack builds the TwELL from them.
+bool small_batch(const sfl_ffn_args_t& a) {
+  const void* wt = a.gated ? a.W_gateT : a.W_upT;
+  return a.dtype == SFL_BF16 && a.T <= 256 && cdiv(a.f, 256) < 128 && wt != nullptr;
+}
+
 bool fused_twell(const sfl_ffn_args_t& a) {
   const int tn = a.cfg.tile_cols;
-  return a.dtype == SFL_BF16 && (tn == 64 || tn == 128 || tn == 256);
+  return a.dtype == SFL_BF16 && (tn == 64 || tn == 128 || tn == 256) && !small_batch(a);
 }
 
 sfl_status_t check_forward(const sfl_ffn_args_t* a, bool need_output = true) {
@@ -129,15 +137,21 @@ FwdPlan plan_forward(const sfl_ffn_args_t& a, void* ws) {
     p.part_u = (float*)c.take((size_t)8 * a.T * K * 4);
     p.hval = c.take((size_t)a.T * K * 2);
   }
-  if (a.dtype == SFL_BF16 && cap > 0) {
-    p.part_rows = (int)std::min<int64_t>(align_rows(cap), kPartRows);
+  if (a.dtype == SFL_BF16 && (cap > 0 || small_batch(a))) {
+    p.part_rows = (int)std::min<int64_t>(align_rows(std::max<int64_t>(cap, a.T)), kPartRows);
     p.part = (float*)c.take((size_t)p.part_rows * std::max(a.f, a.d) * 4);
   }
   p.bytes = c.used;
   return p;
 }
 
-size_t dense_ws_bytes(const sfl_ffn_args_t& a) { return align_up((size_t)a.T * a.f * elem_size(a.dtype)); }
+// The dense baseline's workspace: H [T][f], then (small batches) split-K partial sums.
+bool dense_split(const sfl_ffn_args_t& a) { return a.dtype == SFL_BF16 && a.T <= 256; }
+size_t dense_ws_bytes(const sfl_ffn_args_t& a) {
+  size_t n = align_up((size_t)a.T * a.f * elem_size(a.dtype));
+  if (dense_split(a)) n += align_up((size_t)256 * std::max(a.f, a.d) * 4);
+  return n;
+}
 
 GemmParams gp_zero() {
   GemmParams g;
@@ -241,7 +255,7 @@ sfl_status_t sfl_workspace_size(const void* args, int backward, size_t* bytes) {
   if (!args || !bytes) return SFL_E_ARG;
   if (backward == 1) return sfl::backward_workspace((const sfl_ffn_bwd_args_t*)args, bytes);
   const sfl_ffn_args_t* a = (const sfl_ffn_args_t*)args;
-  sfl_status_t st = check_forward(a);
+  sfl_status_t st = check_forward(a, false);  // sizes do not depend on the output pointers
   if (st != SFL_OK) return st;
   if (backward == 2) {
     *bytes = dense_ws_bytes(*a);
@@ -276,6 +290,13 @@ sfl_status_t sfl_up_projection(const sfl_ffn_args_t* a, float* Z, sfl_stream_t s
   g.shift = a->shift_t;
   g.C = Z;
   g.ldc = a->f;
+  if (small_batch(*a)) {  // the same split-K main loop as the forward's
+    const FwdPlan plan = plan_forward(*a, a->workspace);
+    if (plan.bytes > 0 && (!a->workspace || a->workspace_bytes < plan.bytes)) return SFL_E_WORKSPACE;
+    g.ksplit = kMaxSplit;
+    g.part = plan.part;
+    g.part_rows = plan.part_rows;
+  }
   SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_F32, g, s));
   return SFL_OK;
 }
@@ -331,6 +352,11 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
     } else {
       g.C = plan.Z;
       g.ldc = f;
+      if (small_batch(*a)) {
+        g.ksplit = kMaxSplit;
+        g.part = plan.part;
+        g.part_rows = plan.part_rows;
+      }
       SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_F32, g, s));
       SFL_HIP(launch_pack_twell(plan.Z, T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, s));
     }
@@ -451,6 +477,11 @@ sfl_status_t sfl_dense_ffn_baseline(const sfl_ffn_args_t* a, sfl_stream_t stream
   g.shift = a->shift_t;
   g.C = a->workspace;
   g.ldc = f;
+  if (dense_split(*a)) {
+    g.ksplit = kMaxSplit;
+    g.part = (float*)((char*)a->workspace + align_up((size_t)T * f * 2));
+    g.part_rows = 256;
+  }
   SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_ACT_RELU, g, s));
   if (a->gated) {
     GemmParams u = g;
@@ -470,6 +501,9 @@ sfl_status_t sfl_dense_ffn_baseline(const sfl_ffn_args_t* a, sfl_stream_t stream
   set_down_B(y, a->W_down, bf ? a->W_downT : nullptr, d, f, &blay);
   y.C = a->Y;
   y.ldc = d;
+  y.ksplit = g.ksplit;
+  y.part = g.part;
+  y.part_rows = g.part_rows;
   SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_ACT, y, s));
   ev.record(2, s);
   return SFL_OK;

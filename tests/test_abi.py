@@ -81,7 +81,7 @@ def test_workspace_sizes():
     a32 = _fake_args(b.SFL_F32, 64, 256, 1024, ell_width=32)
     a32.twell.ovf_dense = 0x2000
     assert b.sfl_workspace_size(a32, 0) == 64 * 1024 * 4  # fp32: pre-activations staged
-    assert b.sfl_workspace_size(a, 2) == 128 * 1024 * 2   # dense baseline: H
+    assert b.sfl_workspace_size(a, 2) == 128 * 1024 * 2 + part  # dense baseline: H, split-K partials (T <= 256)
 
 
 def test_unsupported_shapes_and_missing_pointers():

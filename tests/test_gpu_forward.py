@@ -136,12 +136,14 @@ def test_c4_sweep_sampled(sparsity):
 
 
 @pytest.mark.parametrize("use_wupt", [False, True])
-@pytest.mark.parametrize("T,f,Tn,S", [(777, 2048, 256, 32), (300, 1984, 128, 16), (129, 1088, 64, 16)])
+@pytest.mark.parametrize("T,f,Tn,S", [(777, 2048, 256, 32), (300, 1984, 128, 16), (129, 1088, 64, 16),
+                                       (32, 4096, 256, 32)])
 def test_fused_twell_equals_pack_of_same_mainloop(T, f, Tn, S, use_wupt):
     """The TwELL the GEMM epilogue writes equals the oracle's extraction from the float32
     pre-activations of the same GEMM main loop (sfl_up_projection), bit for bit; with W_up
     (row-contiguous B) and with W_up^T (K-contiguous B, the direct-to-LDS GEMM), for TwELL
-    tiles narrower than, equal to and wider than one wave's columns, and ragged T and f."""
+    tiles narrower than, equal to and wider than one wave's columns, and ragged T and f.
+    Small batches with W_up^T (T <= 256) take the split-K GEMM + standalone pack instead."""
     w = wl.make_ffn("fused-vs-pack", "bf16", T, 512, f, seed=7 + T, sparsity=0.97, tile_cols=Tn, tile_slots=S,
                     ell_width=128)
     Y, bufs, stats, cfg = run_forward(w, use_wupt=use_wupt)
@@ -152,6 +154,8 @@ def test_fused_twell_equals_pack_of_same_mainloop(T, f, Tn, S, use_wupt):
         b.sfl_transpose(Wu, WupT)
     Z = torch.empty((w.T, w.f), dtype=torch.float32, device="cuda")
     args = b.ffn_args(X, Wu, dev(w.W_down), cfg, shift_t=dev(w.shift_t), W_upT=WupT)
+    ws = torch.empty(max(1, b.sfl_workspace_size(args, 0)), dtype=torch.uint8, device="cuda")
+    args = b.ffn_args(X, Wu, dev(w.W_down), cfg, shift_t=dev(w.shift_t), W_upT=WupT, workspace=ws)
     b.sfl_up_projection(args, Z)
     bufs2 = b.alloc_twell(w.T, w.f, "bf16", cfg)
     b.sfl_pack_twell(Z, "bf16", cfg, bufs2)
