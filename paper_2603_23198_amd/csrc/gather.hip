@@ -200,10 +200,16 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
   }
   __syncthreads();
   const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc((void*)W, (short)0, 0x7fffffff, 0x00020000);
-  for (int slice = xcd; slice < n_slices; slice += 8) {
+  // work items (slice of this XCD, token) in slice-major order, dealt round-robin to the
+  // waves: the workgroup walks the slices in order, and a small block (decode) still
+  // keeps every wave busy
+  const int nsl = (n_slices - xcd + 7) / 8;
+  for (int it = wave; it < nsl * tpw; it += GATHER_WAVES) {
+    const int slice = xcd + 8 * (it / tpw);
+    const int i = it % tpw;
     const int64_t col = (int64_t)slice * SLICE2 + sub * 8;
     const uint32_t col_b = (uint32_t)(slice * f * SLICE2 * 2) + (uint32_t)sub * 16u;
-    for (int i = wave; i < tpw; i += GATHER_WAVES) {
+    {
       const int nnz = __builtin_amdgcn_readfirstlane(cnt_s[i]);
       if (nnz < 0) continue;
       float acc[8];
@@ -220,6 +226,10 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
 }
 
 // ---- gated up-dot over slice-major W_up^T (Alg. 2's u, split over d) --------------------
+// Copies of the per-entry sums: one per slice of the XCD when the token block is smaller
+// than the number of waves (decode), else one.
+__host__ __device__ inline int updot_copies(int tpw, int nsl) { return tpw < GATHER_WAVES ? nsl : 1; }
+
 // u[t, e] = x[t] . W_up[:, n[t, e]] for every ELL entry, as 8 per-XCD partial sums: XCD x
 // covers the 64-column slices x, x+8, ... of d exactly like the down-projection gather
 // (same token blocks, same slice walk, same L2 residency of one 2 MiB slice of W_up^T),
@@ -231,9 +241,14 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gated_updot(
     int64_t T, int64_t d, int64_t f, int K, const uint16_t* __restrict__ ell_idx, const int32_t* __restrict__ row_nnz,
     const uint8_t* __restrict__ row_ovf, const bf16_t* __restrict__ X, const bf16_t* __restrict__ WuP,
     float* __restrict__ part_u, int n_slices, int tpw) {
-  extern __shared__ uint32_t ent[];  // [tpw][K] indices, [tpw][K] partial sums, [tpw] counts
+  // [tpw][K] indices, [ncopy][tpw][K] partial sums, [tpw] counts. With ncopy = 1 a token's
+  // slices are handled by one wave in order; a small block (decode) deals (slice, token)
+  // items to all waves, each slice with its own copy of the sums, added in slice order.
+  extern __shared__ uint32_t ent[];
+  const int nsl = (n_slices - (int)(blockIdx.x & 7) + 7) / 8;
+  const int ncopy = updot_copies(tpw, nsl);
   float* us = (float*)(ent + (size_t)tpw * K);
-  int* cnt_s = (int*)(us + (size_t)tpw * K);
+  int* cnt_s = (int*)(us + (size_t)ncopy * tpw * K);
   const int xcd = blockIdx.x & 7;
   const int64_t t0 = (int64_t)(blockIdx.x >> 3) * tpw;
   const int l = threadIdx.x & 63;
@@ -249,53 +264,66 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gated_updot(
     const int64_t t = t0 + i;
     for (int e = l; e < c; e += 64) {
       ent[i * K + e] = (uint32_t)ell_idx[t * K + e];
-      us[i * K + e] = 0.f;
+      for (int cp = 0; cp < ncopy; ++cp) us[((size_t)cp * tpw + i) * K + e] = 0.f;
     }
   }
   __syncthreads();
   const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc((void*)WuP, (short)0, 0x7fffffff, 0x00020000);
   constexpr uint32_t row_b = SLICE2 * 2;
-  for (int slice = xcd; slice < n_slices; slice += 8) {
+  // partial dot products of token i's entries with slice xcd + 8 * sl, added into ur
+  auto item = [&](int sl, int i, float* ur) {
+    const int slice = xcd + 8 * sl;
     const uint32_t col_b = (uint32_t)(slice * f * SLICE2 * 2) + (uint32_t)sub * 16u;
-    for (int i = wave; i < tpw; i += GATHER_WAVES) {
-      const int nnz = __builtin_amdgcn_readfirstlane(cnt_s[i]);
-      if (nnz <= 0) continue;
-      // this lane's 8 columns of x[t] in the slice, as bf16 pairs
-      const u32x4_t xv = *(const u32x4_t*)(X + (t0 + i) * d + (int64_t)slice * SLICE2 + sub * 8);
-      const uint32_t* er = ent + i * K;
-      float* ur = us + i * K;
-      for (int q = 0; q < nnz; q += NGRP * GU) {
-        u32x4_t w[GU];
+    const int nnz = __builtin_amdgcn_readfirstlane(cnt_s[i]);
+    if (nnz <= 0) return;
+    // this lane's 8 columns of x[t] in the slice, as bf16 pairs
+    const u32x4_t xv = *(const u32x4_t*)(X + (t0 + i) * d + (int64_t)slice * SLICE2 + sub * 8);
+    const uint32_t* er = ent + i * K;
+    for (int q = 0; q < nnz; q += NGRP * GU) {
+      u32x4_t w[GU];
 #pragma unroll
-        for (int u = 0; u < GU; ++u) {
-          const int e = q + u * NGRP + grp;
-          const uint32_t off = e < nnz ? er[e] * row_b + col_b : 0x80000000u;
-          w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0));
+      for (int u = 0; u < GU; ++u) {
+        const int e = q + u * NGRP + grp;
+        const uint32_t off = e < nnz ? er[e] * row_b + col_b : 0x80000000u;
+        w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0));
+      }
+#pragma unroll
+      for (int u = 0; u < GU; ++u) {
+        float sacc = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          // copy the words out first: a bit cast applied straight to a vector element
+          // is compiled as a cast of element 0
+          const uint32_t xw = xv[j], ww = w[u][j];
+          sacc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, xw), __builtin_bit_cast(bf16x2_t, ww),
+                                                 sacc, false);
         }
 #pragma unroll
-        for (int u = 0; u < GU; ++u) {
-          float s = 0.f;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            // copy the words out first: a bit cast applied straight to a vector element
-            // is compiled as a cast of element 0
-            const uint32_t xw = xv[j], ww = w[u][j];
-            s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, xw), __builtin_bit_cast(bf16x2_t, ww), s,
-                                                false);
-          }
-#pragma unroll
-          for (int o = 1; o < LPR; o <<= 1) s += __shfl_xor(s, o, 64);
-          const int e = q + u * NGRP + grp;
-          if (sub == 0 && e < nnz) ur[e] += s;
-        }
+        for (int o = 1; o < LPR; o <<= 1) sacc += __shfl_xor(sacc, o, 64);
+        const int e = q + u * NGRP + grp;
+        if (sub == 0 && e < nnz) ur[e] += sacc;
       }
     }
+  };
+  if (ncopy > 1) {
+    for (int it = wave; it < nsl * tpw; it += GATHER_WAVES) {
+      const int sl = it / tpw, i = it % tpw;
+      item(sl, i, us + ((size_t)sl * tpw + i) * K);
+    }
+  } else {
+    // slice-outer, like the down-projection gather: the XCD works on one slice at a time
+    for (int sl = 0; sl < nsl; ++sl)
+      for (int i = wave; i < tpw; i += GATHER_WAVES) item(sl, i, us + (size_t)i * K);
   }
   __syncthreads();
   for (int i = wave; i < tpw; i += GATHER_WAVES) {
     const int c = cnt_s[i];
     const int64_t t = t0 + i;
-    for (int e = l; e < c; e += 64) part_u[((int64_t)xcd * T + t) * K + e] = us[i * K + e];
+    for (int e = l; e < c; e += 64) {
+      float u = us[(size_t)i * K + e];
+      for (int cp = 1; cp < ncopy; ++cp) u += us[((size_t)cp * tpw + i) * K + e];
+      part_u[((int64_t)xcd * T + t) * K + e] = u;
+    }
   }
 }
 
@@ -390,7 +418,8 @@ hipError_t launch_gated_updot(int64_t T, int64_t d, int64_t f, int K, const uint
   const int64_t per_tok = (int64_t)std::max(K, 1) * 8 + 4;
   const int tpw = slice_walk_tpw(T, per_tok);
   const int64_t blocks = cdiv(T, tpw);
-  const size_t lds = (size_t)tpw * per_tok;
+  const int nsl_max = (int)cdiv(d / SLICE2, 8);
+  const size_t lds = (size_t)tpw * per_tok + (size_t)(updot_copies(tpw, nsl_max) - 1) * tpw * std::max(K, 1) * 4;
   if (lds > 160 * 1024) return hipErrorInvalidValue;
   if (lds > 65536) {
     const hipError_t e =
