@@ -20,6 +20,8 @@
 #include "common.h"
 #include "internal.h"
 
+#include <algorithm>
+
 namespace sfl {
 
 namespace {
@@ -487,36 +489,20 @@ __device__ __forceinline__ void load_lds16(u32x4_t rsrc, uint32_t lds_off, uint3
                : "memory");
 }
 
+// One output tile (tm, tn) over K steps [kt0, kt1); SPLIT with ks > 1 stores the fp32
+// partial sums of split `split`, otherwise the epilogue runs. Called by every thread.
 template <int EPI, int Tn, bool SPLIT>
-__global__ __launch_bounds__(NTHR) void k_gemm_kc(GemmParams p) {
-  __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * KC_STAGE];
+__device__ __forceinline__ void kc_tile(const GemmParams& p, int tm, int tn, int split, int ks, int m_eff,
+                                        bf16_t* smem) {
   typedef WaveTile<KC_WM, KC_WN, KC_FM> W;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave / KC_WN, wn = wave % KC_WN;
-  const int tiles_m = (int)cdiv(p.M, BM), tiles_n = (int)cdiv(p.N, BN);
-  int tm, tn, split = 0;
-  if constexpr (SPLIT) {
-    // block = (tile, split), tiles row-major: the tiles of the counted rows come first
-    split = (int)(blockIdx.x % (unsigned)p.ksplit);
-    const int t = (int)(blockIdx.x / (unsigned)p.ksplit);
-    tm = t / tiles_n;
-    tn = t % tiles_n;
-  } else {
-    tile_coords(tiles_m, tiles_n, tm, tn);
-  }
   const int m0 = tm * BM, n0 = tn * BN;
-  const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
-  if (m0 >= m_eff) return;
   const int nk_all = (int)(p.K / KC_BK);
-  int kt0 = 0, kt1 = nk_all, ks = 1;
-  if constexpr (SPLIT) {
-    ks = splitk_count(p.ksplit, p.part_rows, m_eff, p.N, nk_all);
-    if (split >= ks) return;
-    kt0 = (int)((int64_t)nk_all * split / ks);
-    kt1 = (int)((int64_t)nk_all * (split + 1) / ks);
-  }
+  const int kt0 = (int)((int64_t)nk_all * split / ks);
+  const int kt1 = (int)((int64_t)nk_all * (split + 1) / ks);
 
   // Load instruction q of this wave fills rows (wave*KC_LOADS + q)*8 .. +7 of the operand
   // tile; lane l writes row +l/8 at chunk position l%8, which holds logical chunk
@@ -615,6 +601,33 @@ __global__ __launch_bounds__(NTHR) void k_gemm_kc(GemmParams p) {
   gemm_epilogue<EPI, KC_WM, KC_WN, KC_FM, Tn>(p, acc, m0, n0, m_eff, smem);
 }
 
+template <int EPI, int Tn>
+__global__ __launch_bounds__(NTHR) void k_gemm_kc(GemmParams p) {
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * KC_STAGE];
+  const int tiles_m = (int)cdiv(p.M, BM), tiles_n = (int)cdiv(p.N, BN);
+  int tm, tn;
+  tile_coords(tiles_m, tiles_n, tm, tn);
+  const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
+  if (tm * BM >= m_eff) return;
+  kc_tile<EPI, Tn, false>(p, tm, tn, 0, 1, m_eff, smem);
+}
+
+// Split-K GEMM: persistent blocks over the (tile, split) items of the counted rows, so
+// the grid does not scale with a row capacity that the count may leave mostly empty.
+template <int EPI>
+__global__ __launch_bounds__(NTHR) void k_gemm_kc_split(GemmParams p) {
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * KC_STAGE];
+  const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
+  const int tiles_n = (int)cdiv(p.N, BN);
+  const int ks = splitk_count(p.ksplit, p.part_rows, m_eff, p.N, (int)(p.K / KC_BK));
+  const int n_items = (int)cdiv(m_eff, BM) * tiles_n * ks;
+  for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
+    const int split = item % ks, t = item / ks;
+    kc_tile<EPI, 0, true>(p, t / tiles_n, t % tiles_n, split, ks, m_eff, smem);
+    __syncthreads();  // the next item refills the stage buffers
+  }
+}
+
 // Sum of the split-K partials in split order, then the epilogue of element (m, n); four
 // consecutive columns per thread, grid-stride over the counted rows.
 template <int EPI>
@@ -658,7 +671,7 @@ template <int EPI, int Tn = 0>
 hipError_t launch_kc(const GemmParams& p, hipStream_t s) {
   const int tiles = (int)(cdiv(p.M, BM) * cdiv(p.N, BN));
   if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL((k_gemm_kc<EPI, Tn, false>), dim3(tiles), dim3(NTHR), 0, s, p);
+  hipLaunchKernelGGL((k_gemm_kc<EPI, Tn>), dim3(tiles), dim3(NTHR), 0, s, p);
   return hipGetLastError();
 }
 
@@ -668,7 +681,8 @@ template <int EPI>
 hipError_t launch_kc_split(const GemmParams& p, hipStream_t s) {
   const int64_t tiles = cdiv(p.M, BM) * cdiv(p.N, BN);
   if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL((k_gemm_kc<EPI, 0, true>), dim3((unsigned)(tiles * p.ksplit)), dim3(NTHR), 0, s, p);
+  const unsigned grid = (unsigned)std::min<int64_t>(tiles * p.ksplit, 512);  // about two blocks per CU
+  hipLaunchKernelGGL((k_gemm_kc_split<EPI>), dim3(grid), dim3(NTHR), 0, s, p);
   hipLaunchKernelGGL((k_splitk_reduce<EPI>), dim3(1024), dim3(256), 0, s, p);
   return hipGetLastError();
 }

@@ -100,7 +100,7 @@ __global__ __launch_bounds__(256) void k_classify(int64_t T, int NT, int S, int 
                                                   const uint16_t* __restrict__ idx, const int32_t* __restrict__ cnt,
                                                   int32_t* __restrict__ row_nnz, uint8_t* __restrict__ row_ovf,
                                                   V* __restrict__ ell_val, uint16_t* __restrict__ ell_idx,
-                                                  sfl_stats_t* __restrict__ stats) {
+                                                  sfl_stats_t* __restrict__ stats, int rpw) {
   __shared__ int incl_lds[4][kClassifyMaxTiles];
   const int l = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
@@ -108,8 +108,8 @@ __global__ __launch_bounds__(256) void k_classify(int64_t T, int NT, int S, int 
   int64_t nnz_sum = 0;
   int over_sum = 0;
   float l1 = 0.f;
-  for (int rr = 0; rr < kClassifyRowsPerWave; ++rr) {
-    const int64_t t = ((int64_t)blockIdx.x * 4 + w) * kClassifyRowsPerWave + rr;
+  for (int rr = 0; rr < rpw; ++rr) {
+    const int64_t t = ((int64_t)blockIdx.x * 4 + w) * rpw + rr;
     if (t >= T) break;
     const int32_t* crow = cnt + t * NT;
     int total = 0;
@@ -216,13 +216,25 @@ hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int Tn, int S, in
   if (T == 0) return hipSuccess;
   const int NT = (int)cdiv(f, Tn);
   const bool wide = NT > kClassifyMaxTiles;
-  const dim3 grid((unsigned)(wide ? cdiv(T, 4) : cdiv(T, 4 * kClassifyRowsPerWave)));
-  if (val_bf16)
-    hipLaunchKernelGGL(wide ? k_classify_wide<bf16_t> : k_classify<bf16_t>, grid, dim3(256), 0, s, T, NT, S, K,
-                       (const bf16_t*)val, idx, cnt, row_nnz, row_ovf, (bf16_t*)ell_val, ell_idx, stats);
-  else
-    hipLaunchKernelGGL(wide ? k_classify_wide<float> : k_classify<float>, grid, dim3(256), 0, s, T, NT, S, K,
-                       (const float*)val, idx, cnt, row_nnz, row_ovf, (float*)ell_val, ell_idx, stats);
+  // several rows per wave amortise the per-block statistics; small batches take one row
+  // per wave so that the rows are spread over more CUs
+  const int rpw = T >= 2048 ? kClassifyRowsPerWave : 1;
+  const dim3 grid((unsigned)(wide ? cdiv(T, 4) : cdiv(T, 4 * rpw)));
+  if (wide) {
+    if (val_bf16)
+      hipLaunchKernelGGL(k_classify_wide<bf16_t>, grid, dim3(256), 0, s, T, NT, S, K, (const bf16_t*)val, idx, cnt,
+                         row_nnz, row_ovf, (bf16_t*)ell_val, ell_idx, stats);
+    else
+      hipLaunchKernelGGL(k_classify_wide<float>, grid, dim3(256), 0, s, T, NT, S, K, (const float*)val, idx, cnt,
+                         row_nnz, row_ovf, (float*)ell_val, ell_idx, stats);
+  } else {
+    if (val_bf16)
+      hipLaunchKernelGGL(k_classify<bf16_t>, grid, dim3(256), 0, s, T, NT, S, K, (const bf16_t*)val, idx, cnt,
+                         row_nnz, row_ovf, (bf16_t*)ell_val, ell_idx, stats, rpw);
+    else
+      hipLaunchKernelGGL(k_classify<float>, grid, dim3(256), 0, s, T, NT, S, K, (const float*)val, idx, cnt, row_nnz,
+                         row_ovf, (float*)ell_val, ell_idx, stats, rpw);
+  }
   return hipGetLastError();
 }
 
