@@ -165,15 +165,18 @@ class Bench:
             WupT, WdT = transposed(Wu), transposed(Wd)
             if w.gated:
                 WgT = transposed(Wg)
-                if packed and w.d % 512 == 0:
-                    WuP = t.empty_like(Wu)
-                    b.sfl_pack_down_weights(WupT, WuP)
-        kw = dict(Y=Y, bufs=bufs, W_gate=Wg, W_upT=WupT, W_gateT=WgT, W_downT=WdT, W_down_packed=WdP, W_up_packed=WuP,
+            if packed and w.d % 512 == 0:
+                # slice-major W_up^T: the gated forward's up-dots and the backward's dX read it
+                WuP = t.empty_like(Wu)
+                b.sfl_pack_down_weights(WupT, WuP)
+        kw = dict(Y=Y, bufs=bufs, W_gate=Wg, W_upT=WupT, W_gateT=WgT, W_downT=WdT, W_down_packed=WdP,
+                  W_up_packed=WuP if w.gated else None,
                   bias_f=self.dev(w.bias_f), shift_t=self.dev(w.shift_t), stats=stats)
         a0 = b.ffn_args(X, Wu, Wd, cfg, **kw)
         ws = t.empty(max(1, b.sfl_workspace_size(a0)), dtype=t.uint8, device="cuda")
         dws = t.empty(max(1, b.sfl_workspace_size(a0, 2)), dtype=t.uint8, device="cuda")
-        s = dict(X=X, Wu=Wu, Wd=Wd, WupT=WupT, cfg=cfg, bufs=bufs, stats=stats, kw=kw, ws=ws, dws=dws, Y=Y)
+        s = dict(X=X, Wu=Wu, Wd=Wd, WupT=WupT, WdP=WdP, WuP=WuP, cfg=cfg, bufs=bufs, stats=stats, kw=kw, ws=ws,
+                 dws=dws, Y=Y)
         s["args"] = b.ffn_args(X, Wu, Wd, cfg, **kw, workspace=ws)
         dkw = dict(kw)
         dkw["Y"] = t.empty_like(Y)
@@ -231,10 +234,12 @@ class Bench:
         dWu = t.empty((w.d, w.f), dtype=t.float32, device="cuda")
         dWd = t.empty((w.f, w.d), dtype=t.float32, device="cuda")
         bws = t.empty(max(1, b.sfl_workspace_size(
-            b.bwd_args(s["X"], s["Wu"], s["Wd"], dY, s["cfg"], s["bufs"], lam, dX, dWu, dWd, W_upT=s["WupT"]), 1)),
+            b.bwd_args(s["X"], s["Wu"], s["Wd"], dY, s["cfg"], s["bufs"], lam, dX, dWu, dWd, W_upT=s["WupT"],
+                       W_down_packed=s["WdP"], W_up_packed=s["WuP"]), 1)),
             dtype=t.uint8, device="cuda")
         mkb = lambda ev=None: b.bwd_args(s["X"], s["Wu"], s["Wd"], dY, s["cfg"], s["bufs"], lam, dX, dWu, dWd,
-                                         W_upT=s["WupT"], workspace=bws, events=ev)
+                                         W_upT=s["WupT"], W_down_packed=s["WdP"], W_up_packed=s["WuP"],
+                                         workspace=bws, events=ev)
         bargs = mkb()
 
         def step():

@@ -197,13 +197,17 @@ typedef struct {
  *  dW_up     float32 [d][f] (overwritten)
  *  dW_down   float32 [f][d] (overwritten)
  *  W_upT     optional [f][d]; transposed into the workspace when NULL.
+ *  W_down_packed, W_up_packed  optional slice-major copies ([d/64][f][64]) of W_down and
+ *            of W_up^T, as the forward takes them (sfl_pack_down_weights of W_down and
+ *            of W_up^T); built in the workspace on every call when NULL. The dZ and dX
+ *            gathers walk 64-column slices of them, one slice per XCD at a time.
  *  saved     the sfl_twell_t the forward filled (row_nnz, row_ovf, ovf_rows, n_ovf,
  *            ell_val, ell_idx and ovf_dense are read)
  *  events / n_events  optional hipEvent_t array recorded at stage boundaries (0: start,
  *            1: after dZ at the pattern, 2: after dX of the sparse rows, 3: after the
  *            transposed pattern, 4: after the weight gradients of the sparse rows,
  *            5: end, after the dense-backup rows).
- * Supports d in {512, 1024, 2048, 4096}, f % 64 == 0 and f <= 40960. */
+ * Supports d % 512 == 0, f % 64 == 0, f <= 40960 and T <= 2^31 / (2 d). */
 typedef struct {
   sfl_dtype_t dtype;
   int64_t T, d, f;
@@ -211,6 +215,8 @@ typedef struct {
   const void* W_up;
   const void* W_down;
   const void* W_upT;
+  const void* W_down_packed;
+  const void* W_up_packed;
   const void* dY;
   sfl_twell_cfg_t cfg;
   sfl_twell_t saved;

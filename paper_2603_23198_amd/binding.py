@@ -65,6 +65,7 @@ class FfnArgs(Structure):
 class BwdArgs(Structure):
     _fields_ = [("dtype", c_int), ("T", c_int64), ("d", c_int64), ("f", c_int64),
                 ("X", c_void_p), ("W_up", c_void_p), ("W_down", c_void_p), ("W_upT", c_void_p),
+                ("W_down_packed", c_void_p), ("W_up_packed", c_void_p),
                 ("dY", c_void_p), ("cfg", Cfg), ("saved", Twell), ("lambda_l1", c_double),
                 ("dX", c_void_p), ("dW_up", c_void_p), ("dW_down", c_void_p), ("workspace", c_void_p),
                 ("workspace_bytes", c_size_t), ("events", c_void_p), ("n_events", c_int32)]
@@ -218,14 +219,15 @@ def sfl_dense_ffn_baseline(args, stream=None):
     _check("sfl_dense_ffn_baseline", _lib.sfl_dense_ffn_baseline(ctypes.byref(args), _stream(stream)))
 
 
-def bwd_args(X, W_up, W_down, dY, cfg, saved_bufs, lambda_l1, dX, dW_up, dW_down, *, W_upT=None, workspace=None,
-             events=None):
+def bwd_args(X, W_up, W_down, dY, cfg, saved_bufs, lambda_l1, dX, dW_up, dW_down, *, W_upT=None, W_down_packed=None,
+             W_up_packed=None, workspace=None, events=None):
     T, d = X.shape
     f = W_down.shape[0]
     a = BwdArgs()
     a.dtype = dtype_code(X.dtype)
     a.T, a.d, a.f = T, d, f
     a.X, a.W_up, a.W_down, a.W_upT, a.dY = _ptr(X), _ptr(W_up), _ptr(W_down), _ptr(W_upT), _ptr(dY)
+    a.W_down_packed, a.W_up_packed = _ptr(W_down_packed), _ptr(W_up_packed)
     a.cfg = cfg
     a.saved = _twell_struct(saved_bufs)
     a.lambda_l1 = float(lambda_l1)

@@ -4,12 +4,15 @@
 //   dH = dY W_down^T + lambda/(T f) on active entries; dZ = dH on the pattern;
 //   dW_down = H^T dY; dW_up = X^T dZ; dX = dZ W_up^T   (eq. sec3:eq:all_other_gradients,
 //   non-gated case). Nothing dense is computed for the sparse (ELL) rows:
-//  1. dZ at the pattern (an SDDMM): dz[t][e] = dY[t] . W_down[n_e] + lambda/(T f);
-//  2. dX[t] = sum_e dz[t][e] W_up^T[n_e]                       (gather of W_up^T rows);
+//  1. dZ at the pattern (an SDDMM): dz[t][e] = dY[t] . W_down[n_e] + lambda/(T f), by the
+//     slice-walking up-dot of the gated forward (dY in place of x, slice-major W_down);
+//  2. dX[t] = sum_e dz[t][e] W_up^T[n_e], by the slice-walking down-projection gather
+//     over slice-major W_up^T with fp32 values;
 //  3. the pattern transposed (per hidden unit, the tokens that activate it, in token order,
-//     by a deterministic counting sort);
-//  4. per unit n: dW_down[n] = sum h[t][e] dY[t], dW_up^T[n] = sum dz[t][e] X[t]
-//     (gathers of dY and X rows), then dW_up^T -> dW_up.
+//     by a deterministic counting sort), with each entry's h and dz beside its token;
+//  4. per unit n: dW_down[n] = sum h[t][e] dY[t], dW_up^T[n] = sum dz[t][e] X[t], by the
+//     slice-walking per-unit gather over slice-major copies of dY and X; then
+//     dW_up^T -> dW_up.
 // The dense-backup rows go through the MFMA GEMM with a pattern mask (Alg. 3's dense part):
 //  dZ_ovf = [H_ovf > 0] (dY_ovf W_down^T + lambda/(T f)), dX_ovf = dZ_ovf W_up^T,
 //  dW_down += H_ovf^T dY_ovf, dW_up += X_ovf^T dZ_ovf.
@@ -26,98 +29,6 @@ namespace sfl {
 namespace {
 
 constexpr int kBlkTok = 64;  // tokens per block of the counting sort
-
-// ---- 1. dz at the pattern -------------------------------------------------------------
-// One wave per token; dY[t] lives in registers (lane l holds columns 512 q + 8 l .. +8).
-template <int NQ>
-__global__ __launch_bounds__(256) void k_sddmm_dz(int64_t T, int K, const uint16_t* __restrict__ ell_idx,
-                                                  const int32_t* __restrict__ row_nnz,
-                                                  const uint8_t* __restrict__ row_ovf, const bf16_t* __restrict__ dY,
-                                                  const bf16_t* __restrict__ Wd, float lam, float* __restrict__ dz) {
-  constexpr int64_t d = NQ * 512;
-  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T || __builtin_amdgcn_readfirstlane(row_ovf[t])) return;
-  const int l = threadIdx.x & 63;
-  float y[NQ][8];
-#pragma unroll
-  for (int q = 0; q < NQ; ++q) {
-    const u32x4_t w = *(const u32x4_t*)(dY + t * d + q * 512 + l * 8);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      y[q][2 * i] = bf16lo(w[i]);
-      y[q][2 * i + 1] = bf16hi(w[i]);
-    }
-  }
-  const int nnz = __builtin_amdgcn_readfirstlane(row_nnz[t]);
-  const uint16_t* ei = ell_idx + t * (int64_t)K;
-  for (int e0 = 0; e0 < nnz; e0 += 64) {
-    const int n_l = e0 + l < nnz ? (int)ei[e0 + l] : 0;
-    const int cnt = min(64, nnz - e0);
-    float mine = 0.f;
-    for (int q0 = 0; q0 < cnt; ++q0) {
-      const int64_t n = readlane_i(n_l, q0);
-      float part = 0.f;
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        const u32x4_t w = *(const u32x4_t*)(Wd + n * d + q * 512 + l * 8);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          part = fmaf(y[q][2 * i], bf16lo(w[i]), part);
-          part = fmaf(y[q][2 * i + 1], bf16hi(w[i]), part);
-        }
-      }
-      const float s = wave_sum<float>(part) + lam;
-      if (l == q0) mine = s;
-    }
-    if (l < cnt) dz[t * (int64_t)K + e0 + l] = mine;
-  }
-}
-
-// ---- 2. dX of the sparse rows ---------------------------------------------------------
-template <int NQ>
-__global__ __launch_bounds__(256) void k_dx_gather(int64_t T, int K, const uint16_t* __restrict__ ell_idx,
-                                                   const int32_t* __restrict__ row_nnz,
-                                                   const uint8_t* __restrict__ row_ovf, const float* __restrict__ dz,
-                                                   const bf16_t* __restrict__ WupT, bf16_t* __restrict__ dX) {
-  constexpr int64_t d = NQ * 512;
-  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T || __builtin_amdgcn_readfirstlane(row_ovf[t])) return;
-  const int l = threadIdx.x & 63;
-  float acc[NQ][8];
-#pragma unroll
-  for (int q = 0; q < NQ; ++q)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) acc[q][i] = 0.f;
-  const int nnz = __builtin_amdgcn_readfirstlane(row_nnz[t]);
-  const uint16_t* ei = ell_idx + t * (int64_t)K;
-  const float* vz = dz + t * (int64_t)K;
-  for (int e0 = 0; e0 < nnz; e0 += 64) {
-    const int n_l = e0 + l < nnz ? (int)ei[e0 + l] : 0;
-    const float v_l = e0 + l < nnz ? vz[e0 + l] : 0.f;
-    const int cnt = min(64, nnz - e0);
-    for (int q0 = 0; q0 < cnt; ++q0) {
-      const int64_t n = readlane_i(n_l, q0);
-      const float v = readlane_f(v_l, q0);
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        const u32x4_t w = *(const u32x4_t*)(WupT + n * d + q * 512 + l * 8);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          acc[q][2 * i] = fmaf(v, bf16lo(w[i]), acc[q][2 * i]);
-          acc[q][2 * i + 1] = fmaf(v, bf16hi(w[i]), acc[q][2 * i + 1]);
-        }
-      }
-    }
-  }
-#pragma unroll
-  for (int q = 0; q < NQ; ++q) {
-    u32x4_t o;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      o[i] = (uint32_t)f32_to_bf16(acc[q][2 * i]) | ((uint32_t)f32_to_bf16(acc[q][2 * i + 1]) << 16);
-    *(u32x4_t*)(dX + t * d + q * 512 + l * 8) = o;
-  }
-}
 
 // ---- 3. transposed pattern (counting sort in token order) -----------------------------
 // (a) per block of 64 tokens, per unit: how many of the block's sparse rows activate it.
@@ -178,12 +89,13 @@ __global__ __launch_bounds__(1024) void k_col_ptr(int64_t f, const int32_t* __re
 
 // (d) fill: one wave per block walks its tokens in order; a unit appears at most once per
 // token, so the lanes of one token never share a unit, and the per-unit cursor in LDS
-// gives each (token, entry) its place in token order.
+// gives each (token, entry) its place in token order. The entry's h and dz go beside it.
 __global__ __launch_bounds__(64) void k_blk_fill(int64_t T, int K, int64_t f, const uint16_t* __restrict__ ell_idx,
                                                  const int32_t* __restrict__ row_nnz,
                                                  const uint8_t* __restrict__ row_ovf, const int32_t* __restrict__ bc,
-                                                 const int32_t* __restrict__ col_ptr, int32_t* __restrict__ csc_tok,
-                                                 int32_t* __restrict__ csc_ent) {
+                                                 const int32_t* __restrict__ col_ptr, const bf16_t* __restrict__ ell_val,
+                                                 const float* __restrict__ dz, int32_t* __restrict__ csc_tok,
+                                                 float* __restrict__ csc_h, float* __restrict__ csc_z) {
   extern __shared__ int32_t cursor[];  // [f]
   const int64_t b = blockIdx.x;
   const int l = threadIdx.x;
@@ -199,73 +111,10 @@ __global__ __launch_bounds__(64) void k_blk_fill(int64_t T, int K, int64_t f, co
       const int pos = col_ptr[n] + bc[b * f + n] + cursor[n];
       cursor[n] += 1;
       csc_tok[pos] = (int32_t)t;
-      csc_ent[pos] = e;
+      csc_h[pos] = bf16_to_f32(ell_val[t * (int64_t)K + e]);
+      csc_z[pos] = dz[t * (int64_t)K + e];
     }
     __syncthreads();
-  }
-}
-
-// ---- 4. per-unit gathers for dW_down and dW_up^T ---------------------------------------
-// One wave per unit: dW_down[n] = sum h dY[t], dWupT[n] = sum dz X[t] over the unit's
-// (token, entry) list in token order.
-template <int NQ>
-__global__ __launch_bounds__(256) void k_dw_gather(int64_t f, int K, const int32_t* __restrict__ col_ptr,
-                                                   const int32_t* __restrict__ csc_tok,
-                                                   const int32_t* __restrict__ csc_ent,
-                                                   const bf16_t* __restrict__ ell_val, const float* __restrict__ dz,
-                                                   const bf16_t* __restrict__ dY, const bf16_t* __restrict__ X,
-                                                   float* __restrict__ dWd, float* __restrict__ dWuT) {
-  constexpr int64_t d = NQ * 512;
-  const int64_t n = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (n >= f) return;
-  const int l = threadIdx.x & 63;
-  float ad[NQ][8], au[NQ][8];
-#pragma unroll
-  for (int q = 0; q < NQ; ++q)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      ad[q][i] = 0.f;
-      au[q][i] = 0.f;
-    }
-  const int p0 = __builtin_amdgcn_readfirstlane(col_ptr[n]);
-  const int p1 = __builtin_amdgcn_readfirstlane(col_ptr[n + 1]);
-  for (int e0 = p0; e0 < p1; e0 += 64) {
-    const int e = e0 + l;
-    int t_l = 0;
-    float h_l = 0.f, z_l = 0.f;
-    if (e < p1) {
-      t_l = csc_tok[e];
-      const int64_t slot = (int64_t)t_l * K + csc_ent[e];
-      h_l = bf16_to_f32(ell_val[slot]);
-      z_l = dz[slot];
-    }
-    const int cnt = min(64, p1 - e0);
-    for (int q0 = 0; q0 < cnt; ++q0) {
-      const int64_t t = readlane_i(t_l, q0);
-      const float h = readlane_f(h_l, q0);
-      const float z = readlane_f(z_l, q0);
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        const u32x4_t gy = *(const u32x4_t*)(dY + t * d + q * 512 + l * 8);
-        const u32x4_t gx = *(const u32x4_t*)(X + t * d + q * 512 + l * 8);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          ad[q][2 * i] = fmaf(h, bf16lo(gy[i]), ad[q][2 * i]);
-          ad[q][2 * i + 1] = fmaf(h, bf16hi(gy[i]), ad[q][2 * i + 1]);
-          au[q][2 * i] = fmaf(z, bf16lo(gx[i]), au[q][2 * i]);
-          au[q][2 * i + 1] = fmaf(z, bf16hi(gx[i]), au[q][2 * i + 1]);
-        }
-      }
-    }
-  }
-#pragma unroll
-  for (int q = 0; q < NQ; ++q) {
-    float* od = dWd + n * d + q * 512 + l * 8;
-    float* ou = dWuT + n * d + q * 512 + l * 8;
-    *(float4*)od = make_float4(ad[q][0], ad[q][1], ad[q][2], ad[q][3]);
-    *(float4*)(od + 4) = make_float4(ad[q][4], ad[q][5], ad[q][6], ad[q][7]);
-    *(float4*)ou = make_float4(au[q][0], au[q][1], au[q][2], au[q][3]);
-    *(float4*)(ou + 4) = make_float4(au[q][4], au[q][5], au[q][6], au[q][7]);
   }
 }
 
@@ -273,27 +122,24 @@ __global__ __launch_bounds__(256) void k_zero_f32(float* p, int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) p[i] = 0.f;
 }
 
-#define SFL_NQ_DISPATCH(d, KERNEL, ...)                                       \
-  switch (d) {                                                                \
-    case 512: hipLaunchKernelGGL(KERNEL<1>, __VA_ARGS__); break;              \
-    case 1024: hipLaunchKernelGGL(KERNEL<2>, __VA_ARGS__); break;             \
-    case 2048: hipLaunchKernelGGL(KERNEL<4>, __VA_ARGS__); break;             \
-    case 4096: hipLaunchKernelGGL(KERNEL<8>, __VA_ARGS__); break;             \
-    default: return SFL_E_UNSUPPORTED;                                        \
-  }
-
 constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct BwdPlan {
   float* dz = nullptr;        // [T][K]
+  float* part = nullptr;      // [8][T][K] per-XCD partial dz
   int32_t* bc = nullptr;      // [nb][f]
   int32_t* col_cnt = nullptr; // [f]
   int32_t* col_ptr = nullptr; // [f + 1]
   int32_t* csc_tok = nullptr; // [T K]
-  int32_t* csc_ent = nullptr; // [T K]
+  float* csc_h = nullptr;     // [T K]
+  float* csc_z = nullptr;     // [T K]
   float* dWuT = nullptr;      // [f][d]
-  void* WupT = nullptr;       // [f][d] when not given
+  void* WupT = nullptr;       // [f][d] when neither W_upT nor W_up_packed is given
+  void* WdP = nullptr;        // slice-major W_down when not given
+  void* WuP = nullptr;        // slice-major W_up^T when not given
+  void* dYP = nullptr;        // slice-major dY [d/64][T][64]
+  void* XP = nullptr;         // slice-major X
   void* dz_ovf = nullptr;     // [cap][f] bf16
   size_t bytes = 0;
 };
@@ -311,13 +157,19 @@ BwdPlan plan_backward(const sfl_ffn_bwd_args_t& a, void* ws) {
   const int64_t cap = a.cfg.ovf_capacity > 0 ? std::min<int64_t>(a.cfg.ovf_capacity, T) : T;
   const int64_t nb = cdiv(T, kBlkTok);
   p.dz = (float*)take((size_t)T * K * 4);
+  p.part = (float*)take((size_t)8 * T * K * 4);
   p.bc = (int32_t*)take((size_t)nb * f * 4);
   p.col_cnt = (int32_t*)take((size_t)f * 4);
   p.col_ptr = (int32_t*)take((size_t)(f + 1) * 4);
   p.csc_tok = (int32_t*)take((size_t)T * K * 4);
-  p.csc_ent = (int32_t*)take((size_t)T * K * 4);
+  p.csc_h = (float*)take((size_t)T * K * 4);
+  p.csc_z = (float*)take((size_t)T * K * 4);
   p.dWuT = (float*)take((size_t)f * d * 4);
-  if (!a.W_upT) p.WupT = take((size_t)f * d * 2);
+  if (!a.W_upT && !a.W_up_packed) p.WupT = take((size_t)f * d * 2);
+  if (!a.W_down_packed) p.WdP = take((size_t)f * d * 2);
+  if (!a.W_up_packed) p.WuP = take((size_t)f * d * 2);
+  p.dYP = take((size_t)T * d * 2);
+  p.XP = take((size_t)T * d * 2);
   p.dz_ovf = take((size_t)cap * f * 2);
   p.bytes = used;
   return p;
@@ -329,7 +181,7 @@ sfl_status_t check_backward(const sfl_ffn_bwd_args_t* a) {
   if (a->T < 0 || a->d < 1 || a->f < 1 || a->f > 65535) return SFL_E_ARG;
   if (a->cfg.ell_width < 0 || a->cfg.ovf_capacity < 0) return SFL_E_ARG;
   if (a->dtype != SFL_BF16) return SFL_E_UNSUPPORTED;
-  if (!(a->d == 512 || a->d == 1024 || a->d == 2048 || a->d == 4096) || a->f % 64 != 0) return SFL_E_UNSUPPORTED;
+  if (a->d % 512 != 0 || a->f % 64 != 0) return SFL_E_UNSUPPORTED;
   if (a->f > 40960) return SFL_E_UNSUPPORTED;  // the transpose keeps one cursor per unit in LDS
   if (!a->dW_up || !a->dW_down) return SFL_E_ARG;
   if (a->T > 0) {
@@ -387,22 +239,30 @@ sfl_status_t backward_run(const sfl_ffn_bwd_args_t* a, hipStream_t s) {
   const bf16_t* ev = (const bf16_t*)sv.ell_val;
   const int64_t nb = cdiv(T, kBlkTok);
 
-  // 1. dz at the pattern of the sparse rows
-  SFL_NQ_DISPATCH(d, k_sddmm_dz, dim3((unsigned)cdiv(T, 4)), dim3(256), 0, s, T, K, sv.ell_idx, sv.row_nnz, sv.row_ovf,
-                  dY, (const bf16_t*)a->W_down, lam, p.dz);
-  SFL_HIPB(hipGetLastError());
+  // slice-major weight copies (given, or built here)
+  const void* WdP = a->W_down_packed;
+  if (!WdP) {
+    SFL_HIPB(launch_pack_down(a->W_down, p.WdP, f, d, s));
+    WdP = p.WdP;
+  }
+  const void* WuP = a->W_up_packed;
+  if (!WuP) {
+    const void* WupT = a->W_upT;
+    if (!WupT) {
+      SFL_HIPB(launch_transpose(a->W_up, p.WupT, d, f, 2, s));
+      WupT = p.WupT;
+    }
+    SFL_HIPB(launch_pack_down(WupT, p.WuP, f, d, s));
+    WuP = p.WuP;
+  }
+  // 1. dz at the pattern of the sparse rows: per-XCD partial dots, then their sum + lambda'
+  SFL_HIPB(launch_gated_updot(T, d, f, K, sv.ell_idx, sv.row_nnz, sv.row_ovf, dY, WdP, p.part, s));
+  SFL_HIPB(launch_sum_parts(T, K, sv.row_nnz, sv.row_ovf, p.part, lam, p.dz, s));
   rec(1);
   // 2. dX of the sparse rows
-  const void* WupT = a->W_upT;
-  if (!WupT) {
-    SFL_HIPB(launch_transpose(a->W_up, p.WupT, d, f, 2, s));
-    WupT = p.WupT;
-  }
-  SFL_NQ_DISPATCH(d, k_dx_gather, dim3((unsigned)cdiv(T, 4)), dim3(256), 0, s, T, K, sv.ell_idx, sv.row_nnz,
-                  sv.row_ovf, p.dz, (const bf16_t*)WupT, (bf16_t*)a->dX);
-  SFL_HIPB(hipGetLastError());
+  SFL_HIPB(launch_gather_down_packed(T, d, f, K, p.dz, sv.ell_idx, sv.row_nnz, sv.row_ovf, WuP, a->dX, s, 1));
   rec(2);
-  // 3. transposed pattern
+  // 3. transposed pattern, with each entry's h and dz
   hipLaunchKernelGGL(k_blk_count, dim3((unsigned)nb), dim3(256), 0, s, T, K, f, sv.ell_idx, sv.row_nnz, sv.row_ovf,
                      p.bc);
   SFL_HIPB(hipGetLastError());
@@ -414,13 +274,14 @@ sfl_status_t backward_run(const sfl_ffn_bwd_args_t* a, hipStream_t s) {
   if (fill_lds > 65536)
     SFL_HIPB(hipFuncSetAttribute((const void*)k_blk_fill, hipFuncAttributeMaxDynamicSharedMemorySize, (int)fill_lds));
   hipLaunchKernelGGL(k_blk_fill, dim3((unsigned)nb), dim3(64), fill_lds, s, T, K, f, sv.ell_idx, sv.row_nnz,
-                     sv.row_ovf, p.bc, p.col_ptr, p.csc_tok, p.csc_ent);
+                     sv.row_ovf, p.bc, p.col_ptr, ev, p.dz, p.csc_tok, p.csc_h, p.csc_z);
   SFL_HIPB(hipGetLastError());
   rec(3);
-  // 4. weight gradients of the sparse rows
-  SFL_NQ_DISPATCH(d, k_dw_gather, dim3((unsigned)cdiv(f, 4)), dim3(256), 0, s, f, K, p.col_ptr, p.csc_tok,
-                  p.csc_ent, ev, p.dz, dY, X, a->dW_down, p.dWuT);
-  SFL_HIPB(hipGetLastError());
+  // 4. weight gradients of the sparse rows: per-unit gathers over slice-major dY and X
+  SFL_HIPB(launch_pack_down(dY, p.dYP, T, d, s));
+  SFL_HIPB(launch_pack_down(X, p.XP, T, d, s));
+  SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, p.csc_tok, p.csc_h, p.dYP, a->dW_down, s));
+  SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, p.csc_tok, p.csc_z, p.XP, p.dWuT, s));
   SFL_HIPB(launch_transpose(p.dWuT, a->dW_up, f, d, 4, s));
   rec(4);
   // 5. dense-backup rows: masked GEMMs, accumulated into the weight gradients

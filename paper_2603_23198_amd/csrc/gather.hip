@@ -175,12 +175,49 @@ __device__ __forceinline__ void slice_token(const uint32_t* er, int nnz, __amdgp
     for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], o, 64);
 }
 
+// The same with fp32 values: entries are (index, fp32 value bits) word pairs, and each
+// entry's row segment is scaled and added column by column (fp32 FMA, entries in order
+// per group, groups folded in a fixed order).
+__device__ __forceinline__ void slice_token_f32(const uint32_t* er, int nnz, __amdgpu_buffer_rsrc_t wr, uint32_t col_b,
+                                                int grp, float (&acc)[8]) {
+  constexpr uint32_t row_b = SLICE2 * 2;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+  for (int q = 0; q < nnz; q += NGRP * GU) {
+    u32x4_t w[GU];
+    float v[GU];
+#pragma unroll
+    for (int u = 0; u < GU; ++u) {
+      const int e = q + u * NGRP + grp;
+      const bool ok = e < nnz;
+      v[u] = ok ? __uint_as_float(er[2 * e + 1]) : 0.f;
+      const uint32_t off = ok ? er[2 * e] * row_b + col_b : 0x80000000u;
+      w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0));
+    }
+#pragma unroll
+    for (int u = 0; u < GU; ++u)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t ww = w[u][j];
+        acc[2 * j] = fmaf(v[u], bf16lo(ww), acc[2 * j]);
+        acc[2 * j + 1] = fmaf(v[u], bf16hi(ww), acc[2 * j + 1]);
+      }
+  }
+#pragma unroll
+  for (int o = LPR; o < 64; o <<= 1)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], o, 64);
+}
+
+// VF32: the ELL values are fp32 (the backward's dz), staged as two words per entry.
+template <bool VF32>
 __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
-    int64_t T, int64_t d, int64_t f, int K, const bf16_t* __restrict__ ell_val, const uint16_t* __restrict__ ell_idx,
+    int64_t T, int64_t d, int64_t f, int K, const void* __restrict__ ell_val, const uint16_t* __restrict__ ell_idx,
     const int32_t* __restrict__ row_nnz, const uint8_t* __restrict__ row_ovf, const bf16_t* __restrict__ W,
     bf16_t* __restrict__ Y, int n_slices, int tpw) {
+  constexpr int EW = VF32 ? 2 : 1;   // words per staged entry
   extern __shared__ uint32_t ent[];  // [tpw][K] entries, then [tpw] counts (-1 = skip)
-  int* cnt_s = (int*)(ent + (size_t)tpw * K);
+  int* cnt_s = (int*)(ent + (size_t)tpw * K * EW);
   const int xcd = blockIdx.x & 7;
   const int64_t t0 = (int64_t)(blockIdx.x >> 3) * tpw;
   const int l = threadIdx.x & 63;
@@ -195,8 +232,14 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
   for (int i = wave; i < tpw; i += GATHER_WAVES) {
     const int c = cnt_s[i];
     const int64_t t = t0 + i;
-    for (int e = l; e < c; e += 64)
-      ent[i * K + e] = (uint32_t)ell_idx[t * K + e] | ((uint32_t)ell_val[t * K + e] << 16);
+    for (int e = l; e < c; e += 64) {
+      if constexpr (VF32) {
+        ent[2 * (i * K + e)] = (uint32_t)ell_idx[t * K + e];
+        ent[2 * (i * K + e) + 1] = __float_as_uint(((const float*)ell_val)[t * K + e]);
+      } else {
+        ent[i * K + e] = (uint32_t)ell_idx[t * K + e] | ((uint32_t)((const bf16_t*)ell_val)[t * K + e] << 16);
+      }
+    }
   }
   __syncthreads();
   const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc((void*)W, (short)0, 0x7fffffff, 0x00020000);
@@ -213,7 +256,10 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
       const int nnz = __builtin_amdgcn_readfirstlane(cnt_s[i]);
       if (nnz < 0) continue;
       float acc[8];
-      slice_token(ent + i * K, nnz, wr, col_b, grp, acc);
+      if constexpr (VF32)
+        slice_token_f32(ent + 2 * i * K, nnz, wr, col_b, grp, acc);
+      else
+        slice_token(ent + i * K, nnz, wr, col_b, grp, acc);
       if (grp == 0) {
         u32x4_t out;
 #pragma unroll
@@ -345,6 +391,86 @@ __global__ __launch_bounds__(256) void k_gated_h(int64_t T, int K, const bf16_t*
   }
 }
 
+// ---- per-unit gathers of the backward (dW_down, dW_up^T) ---------------------------------
+// out[n, :] = sum over unit n's list e in [ptr[n], ptr[n+1]) of val[e] * G[tok[e], :], fp32,
+// with G ([R][d] rows: dY or X) in the slice-major copy [d/SLICE][R][SLICE]. The same slice
+// walk as the down-projection gather (XCD x covers slices x, x+8, ...; a slice of G stays in
+// its L2 while the XCD's units stream through it); the lists are read straight from global
+// memory (their lengths vary), the sums run in list order per group and the groups fold
+// in a fixed order.
+__global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_units, int64_t d, int64_t R,
+                                                                  const int32_t* __restrict__ ptr,
+                                                                  const int32_t* __restrict__ tok,
+                                                                  const float* __restrict__ val,
+                                                                  const bf16_t* __restrict__ G, float* __restrict__ out,
+                                                                  int n_slices, int upw) {
+  const int xcd = blockIdx.x & 7;
+  const int64_t u0 = (int64_t)(blockIdx.x >> 3) * upw;
+  const int l = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int grp = l / LPR, sub = l % LPR;
+  constexpr uint32_t row_b = SLICE2 * 2;
+  const __amdgpu_buffer_rsrc_t gr = __builtin_amdgcn_make_buffer_rsrc((void*)G, (short)0, 0x7fffffff, 0x00020000);
+  const int nsl = (n_slices - xcd + 7) / 8;
+  const int nu = (int)std::min<int64_t>(upw, n_units - u0);
+  for (int it = wave; it < nsl * nu; it += GATHER_WAVES) {
+    const int slice = xcd + 8 * (it / nu);
+    const int64_t n = u0 + it % nu;
+    const uint32_t col_b = (uint32_t)(slice * R * SLICE2 * 2) + (uint32_t)sub * 16u;
+    const int p0 = __builtin_amdgcn_readfirstlane(ptr[n]);
+    const int cnt = __builtin_amdgcn_readfirstlane(ptr[n + 1]) - p0;
+    float acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+    for (int q = 0; q < cnt; q += NGRP * GU) {
+      u32x4_t w[GU];
+      float v[GU];
+#pragma unroll
+      for (int u = 0; u < GU; ++u) {
+        const int e = q + u * NGRP + grp;
+        const bool ok = e < cnt;
+        v[u] = ok ? val[p0 + e] : 0.f;
+        const uint32_t off = ok ? (uint32_t)tok[p0 + e] * row_b + col_b : 0x80000000u;
+        w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(gr, (int)off, 0, 0));
+      }
+#pragma unroll
+      for (int u = 0; u < GU; ++u)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t ww = w[u][j];
+          acc[2 * j] = fmaf(v[u], bf16lo(ww), acc[2 * j]);
+          acc[2 * j + 1] = fmaf(v[u], bf16hi(ww), acc[2 * j + 1]);
+        }
+    }
+#pragma unroll
+    for (int o = LPR; o < 64; o <<= 1)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], o, 64);
+    if (grp == 0) {
+      float* o = out + n * d + (int64_t)slice * SLICE2 + sub * 8;
+      *(f32x4_t*)o = f32x4_t{acc[0], acc[1], acc[2], acc[3]};
+      *(f32x4_t*)(o + 4) = f32x4_t{acc[4], acc[5], acc[6], acc[7]};
+    }
+  }
+}
+
+// out[t, e] = sum over the 8 XCD partials (in XCD order) + add, fp32, for the ELL entries
+// of the sparse rows (the backward's dz = dY . W_down[n] + lambda / (T f)).
+__global__ __launch_bounds__(256) void k_sum_parts(int64_t T, int K, const int32_t* __restrict__ row_nnz,
+                                                   const uint8_t* __restrict__ row_ovf, const float* __restrict__ part,
+                                                   float add, float* __restrict__ out) {
+  const int64_t total = T * (int64_t)K;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int64_t t = i / K;
+    const int e = (int)(i % K);
+    if (row_ovf[t] || e >= row_nnz[t]) continue;
+    float u = 0.f;
+#pragma unroll
+    for (int x = 0; x < 8; ++x) u += part[(int64_t)x * total + i];
+    out[i] = u + add;
+  }
+}
+
 // out[s][n][c] = W[n][SLICE s + c]: 16 bytes per thread, reads coalesced along rows.
 __global__ __launch_bounds__(256) void k_pack_down(const bf16_t* __restrict__ W, bf16_t* __restrict__ out, int64_t f,
                                                    int64_t d) {
@@ -379,24 +505,47 @@ hipError_t launch_gather_down(int val_bf16, int64_t T, int64_t d, int K, const v
 
 hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, const void* ell_val,
                                      const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
-                                     const void* Wp, void* Y, hipStream_t s) {
+                                     const void* Wp, void* Y, hipStream_t s, int val_f32) {
   if (T == 0) return hipSuccess;
   if (d % (8 * SLICE2) != 0) return hipErrorInvalidValue;
   const int n_slices = (int)(d / SLICE2);
 
-  const int64_t per_tok = (int64_t)std::max(K, 1) * 4 + 4;
+  const int64_t per_tok = (int64_t)std::max(K, 1) * (val_f32 ? 8 : 4) + 4;
   const int tpw = slice_walk_tpw(T, per_tok);
   const int64_t blocks = cdiv(T, tpw);
   const size_t lds = (size_t)tpw * per_tok;
   if (lds > 160 * 1024) return hipErrorInvalidValue;
+  const void* kern = val_f32 ? (const void*)k_gather_down_b16<true> : (const void*)k_gather_down_b16<false>;
   if (lds > 65536) {
-    const hipError_t e = hipFuncSetAttribute((const void*)k_gather_down_b16,
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(k_gather_down_b16, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), lds, s, T, d, f, K,
-                     (const bf16_t*)ell_val, ell_idx, row_nnz, row_ovf, (const bf16_t*)Wp, (bf16_t*)Y, n_slices,
-                     tpw);
+  if (val_f32)
+    hipLaunchKernelGGL(k_gather_down_b16<true>, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), lds, s, T, d, f,
+                       K, ell_val, ell_idx, row_nnz, row_ovf, (const bf16_t*)Wp, (bf16_t*)Y, n_slices, tpw);
+  else
+    hipLaunchKernelGGL(k_gather_down_b16<false>, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), lds, s, T, d,
+                       f, K, ell_val, ell_idx, row_nnz, row_ovf, (const bf16_t*)Wp, (bf16_t*)Y, n_slices, tpw);
+  return hipGetLastError();
+}
+
+hipError_t launch_csc_gather(int64_t n_units, int64_t d, int64_t R, const int32_t* ptr, const int32_t* tok,
+                             const float* val, const void* Gp, float* out, hipStream_t s) {
+  if (n_units == 0) return hipSuccess;
+  if (d % (8 * SLICE2) != 0) return hipErrorInvalidValue;
+  // two rounds of 32 blocks per XCD (no LDS: the lists are read from global memory)
+  const int upw = (int)std::max<int64_t>(1, cdiv(n_units, 64));
+  const int64_t blocks = cdiv(n_units, upw);
+  hipLaunchKernelGGL(k_csc_gather, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), 0, s, n_units, d, R, ptr,
+                     tok, val, (const bf16_t*)Gp, out, (int)(d / SLICE2), upw);
+  return hipGetLastError();
+}
+
+hipError_t launch_sum_parts(int64_t T, int K, const int32_t* row_nnz, const uint8_t* row_ovf, const float* part,
+                            float add, float* out, hipStream_t s) {
+  if (T == 0 || K == 0) return hipSuccess;
+  const unsigned grid = (unsigned)std::min<int64_t>(cdiv(T * (int64_t)K, 256), 4096);
+  hipLaunchKernelGGL(k_sum_parts, dim3(grid), dim3(256), 0, s, T, K, row_nnz, row_ovf, part, add, out);
   return hipGetLastError();
 }
 

@@ -92,12 +92,20 @@ hipError_t launch_gather_down(int val_bf16, int64_t T, int64_t d, int ell_width,
 // bf16, d % 512 == 0: same sum from the slice-major copy of W_down (persistent, XCD-aware).
 hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int ell_width, const void* ell_val,
                                      const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
-                                     const void* W_packed, void* Y, hipStream_t s);
+                                     const void* W_packed, void* Y, hipStream_t s,
+                                     int val_f32 = 0);
 hipError_t launch_pack_down(const void* W, void* out, int64_t f, int64_t d, hipStream_t s);
 // Gated, two passes over slice-major copies: per-XCD partial up-dots u of every ELL entry
 // (part_u [8][T][K] fp32), then h = g * u (bf16, [T][K]) for the down-projection gather.
 hipError_t launch_gated_updot(int64_t T, int64_t d, int64_t f, int K, const uint16_t* ell_idx, const int32_t* row_nnz,
                               const uint8_t* row_ovf, const void* X, const void* WuP, float* part_u, hipStream_t s);
+// Backward per-unit gathers: out[n][:] = sum_e val[e] G[tok[e]][:] over n's list
+// [ptr[n], ptr[n+1]), G slice-major [d/64][R][64] bf16, out fp32 [n_units][d].
+hipError_t launch_csc_gather(int64_t n_units, int64_t d, int64_t R, const int32_t* ptr, const int32_t* tok,
+                             const float* val, const void* Gp, float* out, hipStream_t s);
+// out[t][e] = sum of the 8 partials [8][T][K] + add on the sparse rows' entries (fp32).
+hipError_t launch_sum_parts(int64_t T, int K, const int32_t* row_nnz, const uint8_t* row_ovf, const float* part,
+                            float add, float* out, hipStream_t s);
 hipError_t launch_gated_h(int64_t T, int K, const void* ell_val, const int32_t* row_nnz, const uint8_t* row_ovf,
                           const float* part_u, void* h, hipStream_t s);
 // Gated fused up-dot + down (Alg. 2) from the ELL rows of the gate pattern.

@@ -17,7 +17,7 @@ pytestmark = pytest.mark.gpu
 b = pytest.importorskip("paper_2603_23198_amd.binding")
 
 
-def run_fwd_bwd(w, lam, with_wupt=False):
+def run_fwd_bwd(w, lam, with_wupt=False, with_packed=False):
     X, Wu, Wd, dY = dev(w.X), dev(w.W_up), dev(w.W_down), dev(w.dY)
     cfg = b.make_cfg(**w.cfg)
     bufs = b.alloc_twell(w.T, w.f, "bf16", cfg)
@@ -33,9 +33,17 @@ def run_fwd_bwd(w, lam, with_wupt=False):
     if with_wupt:
         WupT = torch.empty((w.f, w.d), dtype=torch.bfloat16, device="cuda")
         b.sfl_transpose(Wu, WupT)
-    ba = b.bwd_args(X, Wu, Wd, dY, cfg, bufs, lam, dX, dWu, dWd, W_upT=WupT)
+    pk = {}
+    if with_packed:
+        pk["W_down_packed"] = torch.empty_like(Wd)
+        b.sfl_pack_down_weights(Wd, pk["W_down_packed"])
+        WuT = torch.empty((w.f, w.d), dtype=torch.bfloat16, device="cuda")
+        b.sfl_transpose(Wu, WuT)
+        pk["W_up_packed"] = torch.empty_like(Wu)
+        b.sfl_pack_down_weights(WuT, pk["W_up_packed"])
+    ba = b.bwd_args(X, Wu, Wd, dY, cfg, bufs, lam, dX, dWu, dWd, W_upT=WupT, **pk)
     bws = torch.empty(max(1, b.sfl_workspace_size(ba, 1)), dtype=torch.uint8, device="cuda")
-    ba = b.bwd_args(X, Wu, Wd, dY, cfg, bufs, lam, dX, dWu, dWd, W_upT=WupT, workspace=bws)
+    ba = b.bwd_args(X, Wu, Wd, dY, cfg, bufs, lam, dX, dWu, dWd, W_upT=WupT, workspace=bws, **pk)
     b.sfl_ffn_backward(ba)
     torch.cuda.synchronize()
     return dX, dWu, dWd, bufs, cfg
@@ -99,13 +107,16 @@ def test_backward_lambda_term_is_injected():
     assert rel_l2(to_f64(dX), rdX) <= 2e-2
 
 
-def test_backward_deterministic_and_wupt():
+def test_backward_deterministic_and_weight_copies():
+    """Bitwise reproducible, and identical whether W_up^T / the slice-major weight copies
+    come from the caller or are built inside the call."""
     w = wl.make_ffn("bdet", "bf16", 512, 1024, 2048, seed=8, sparsity=0.98, ell_width=128, with_dy=True)
     a = run_fwd_bwd(w, 2e-5)
-    c = run_fwd_bwd(w, 2e-5, with_wupt=True)
-    for x, y in zip(a[:3], c[:3]):
-        assert torch.equal(x.view(torch.int16) if x.dtype == torch.bfloat16 else x.view(torch.int32),
-                           y.view(torch.int16) if y.dtype == torch.bfloat16 else y.view(torch.int32))
+    for other in (run_fwd_bwd(w, 2e-5, with_wupt=True), run_fwd_bwd(w, 2e-5, with_packed=True),
+                  run_fwd_bwd(w, 2e-5)):
+        for x, y in zip(a[:3], other[:3]):
+            assert torch.equal(x.view(torch.int16) if x.dtype == torch.bfloat16 else x.view(torch.int32),
+                               y.view(torch.int16) if y.dtype == torch.bfloat16 else y.view(torch.int32))
 
 
 def test_backward_c5_sampled():
