@@ -280,8 +280,9 @@ sfl_status_t backward_run(const sfl_ffn_bwd_args_t* a, hipStream_t s) {
   // 4. weight gradients of the sparse rows: per-unit gathers over slice-major dY and X
   SFL_HIPB(launch_pack_down(dY, p.dYP, T, d, s));
   SFL_HIPB(launch_pack_down(X, p.XP, T, d, s));
-  SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, p.csc_tok, p.csc_h, p.dYP, a->dW_down, s));
-  SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, p.csc_tok, p.csc_z, p.XP, p.dWuT, s));
+  const int64_t mean_bound = cdiv(T * (int64_t)K, f);  // the lists hold at most T K entries
+  SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, p.csc_tok, p.csc_h, mean_bound, p.dYP, a->dW_down, s));
+  SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, p.csc_tok, p.csc_z, mean_bound, p.XP, p.dWuT, s));
   SFL_HIPB(launch_transpose(p.dWuT, a->dW_up, f, d, 4, s));
   rec(4);
   // 5. dense-backup rows: masked GEMMs, accumulated into the weight gradients

@@ -397,13 +397,15 @@ __global__ __launch_bounds__(256) void k_gated_h(int64_t T, int K, const bf16_t*
 // walk as the down-projection gather (XCD x covers slices x, x+8, ...; a slice of G stays in
 // its L2 while the XCD's units stream through it); the lists are read straight from global
 // memory (their lengths vary), the sums run in list order per group and the groups fold
-// in a fixed order.
+// in a fixed order. The block's lists are staged in LDS as (token, value) word pairs when
+// they fit (their total length is known only on the device), else read from global memory.
 __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_units, int64_t d, int64_t R,
                                                                   const int32_t* __restrict__ ptr,
                                                                   const int32_t* __restrict__ tok,
                                                                   const float* __restrict__ val,
                                                                   const bf16_t* __restrict__ G, float* __restrict__ out,
-                                                                  int n_slices, int upw) {
+                                                                  int n_slices, int upw, int lds_pairs) {
+  extern __shared__ uint32_t ent[];  // [lds_pairs][2]
   const int xcd = blockIdx.x & 7;
   const int64_t u0 = (int64_t)(blockIdx.x >> 3) * upw;
   const int l = threadIdx.x & 63;
@@ -413,6 +415,16 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_unit
   const __amdgpu_buffer_rsrc_t gr = __builtin_amdgcn_make_buffer_rsrc((void*)G, (short)0, 0x7fffffff, 0x00020000);
   const int nsl = (n_slices - xcd + 7) / 8;
   const int nu = (int)std::min<int64_t>(upw, n_units - u0);
+  const int pb = ptr[u0];
+  const int n_ent = ptr[u0 + nu] - pb;
+  const bool staged = n_ent <= lds_pairs;  // uniform over the block
+  if (staged) {
+    for (int e = threadIdx.x; e < n_ent; e += blockDim.x) {
+      ent[2 * e] = (uint32_t)tok[pb + e];
+      ent[2 * e + 1] = __float_as_uint(val[pb + e]);
+    }
+    __syncthreads();
+  }
   for (int it = wave; it < nsl * nu; it += GATHER_WAVES) {
     const int slice = xcd + 8 * (it / nu);
     const int64_t n = u0 + it % nu;
@@ -420,32 +432,36 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_unit
     const int p0 = __builtin_amdgcn_readfirstlane(ptr[n]);
     const int cnt = __builtin_amdgcn_readfirstlane(ptr[n + 1]) - p0;
     float acc[8];
+    if (staged) {
+      slice_token_f32(ent + 2 * (p0 - pb), cnt, gr, col_b, grp, acc);
+    } else {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[j] = 0.f;
-    for (int q = 0; q < cnt; q += NGRP * GU) {
-      u32x4_t w[GU];
-      float v[GU];
+      for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+      for (int q = 0; q < cnt; q += NGRP * GU) {
+        u32x4_t w[GU];
+        float v[GU];
 #pragma unroll
-      for (int u = 0; u < GU; ++u) {
-        const int e = q + u * NGRP + grp;
-        const bool ok = e < cnt;
-        v[u] = ok ? val[p0 + e] : 0.f;
-        const uint32_t off = ok ? (uint32_t)tok[p0 + e] * row_b + col_b : 0x80000000u;
-        w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(gr, (int)off, 0, 0));
+        for (int u = 0; u < GU; ++u) {
+          const int e = q + u * NGRP + grp;
+          const bool ok = e < cnt;
+          v[u] = ok ? val[p0 + e] : 0.f;
+          const uint32_t off = ok ? (uint32_t)tok[p0 + e] * row_b + col_b : 0x80000000u;
+          w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(gr, (int)off, 0, 0));
+        }
+#pragma unroll
+        for (int u = 0; u < GU; ++u)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const uint32_t ww = w[u][j];
+            acc[2 * j] = fmaf(v[u], bf16lo(ww), acc[2 * j]);
+            acc[2 * j + 1] = fmaf(v[u], bf16hi(ww), acc[2 * j + 1]);
+          }
       }
 #pragma unroll
-      for (int u = 0; u < GU; ++u)
+      for (int o = LPR; o < 64; o <<= 1)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint32_t ww = w[u][j];
-          acc[2 * j] = fmaf(v[u], bf16lo(ww), acc[2 * j]);
-          acc[2 * j + 1] = fmaf(v[u], bf16hi(ww), acc[2 * j + 1]);
-        }
+        for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], o, 64);
     }
-#pragma unroll
-    for (int o = LPR; o < 64; o <<= 1)
-#pragma unroll
-      for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], o, 64);
     if (grp == 0) {
       float* o = out + n * d + (int64_t)slice * SLICE2 + sub * 8;
       *(f32x4_t*)o = f32x4_t{acc[0], acc[1], acc[2], acc[3]};
@@ -530,14 +546,22 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
 }
 
 hipError_t launch_csc_gather(int64_t n_units, int64_t d, int64_t R, const int32_t* ptr, const int32_t* tok,
-                             const float* val, const void* Gp, float* out, hipStream_t s) {
+                             const float* val, int64_t mean_bound, const void* Gp, float* out, hipStream_t s) {
   if (n_units == 0) return hipSuccess;
   if (d % (8 * SLICE2) != 0) return hipErrorInvalidValue;
-  // two rounds of 32 blocks per XCD (no LDS: the lists are read from global memory)
-  const int upw = (int)std::max<int64_t>(1, cdiv(n_units, 64));
+  // units per block: lists of mean_bound entries (an upper bound of the mean list length)
+  // fill 3/4 of the LDS budget; a block whose lists do not fit reads them from global memory
+  const int lds_pairs = GATHER_LDS / 8;
+  const int upw = (int)std::max<int64_t>(
+      1, std::min<int64_t>(cdiv(n_units, 64), (int64_t)lds_pairs * 3 / 4 / std::max<int64_t>(mean_bound, 1)));
   const int64_t blocks = cdiv(n_units, upw);
-  hipLaunchKernelGGL(k_csc_gather, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), 0, s, n_units, d, R, ptr,
-                     tok, val, (const bf16_t*)Gp, out, (int)(d / SLICE2), upw);
+  if (GATHER_LDS > 65536) {
+    const hipError_t e =
+        hipFuncSetAttribute((const void*)k_csc_gather, hipFuncAttributeMaxDynamicSharedMemorySize, GATHER_LDS);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k_csc_gather, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), (size_t)GATHER_LDS, s,
+                     n_units, d, R, ptr, tok, val, (const bf16_t*)Gp, out, (int)(d / SLICE2), upw, lds_pairs);
   return hipGetLastError();
 }
 

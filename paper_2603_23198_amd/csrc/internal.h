@@ -100,9 +100,10 @@ hipError_t launch_pack_down(const void* W, void* out, int64_t f, int64_t d, hipS
 hipError_t launch_gated_updot(int64_t T, int64_t d, int64_t f, int K, const uint16_t* ell_idx, const int32_t* row_nnz,
                               const uint8_t* row_ovf, const void* X, const void* WuP, float* part_u, hipStream_t s);
 // Backward per-unit gathers: out[n][:] = sum_e val[e] G[tok[e]][:] over n's list
-// [ptr[n], ptr[n+1]), G slice-major [d/64][R][64] bf16, out fp32 [n_units][d].
+// [ptr[n], ptr[n+1]), G slice-major [d/64][R][64] bf16, out fp32 [n_units][d]; mean_bound
+// bounds the mean list length (sizes the blocks).
 hipError_t launch_csc_gather(int64_t n_units, int64_t d, int64_t R, const int32_t* ptr, const int32_t* tok,
-                             const float* val, const void* Gp, float* out, hipStream_t s);
+                             const float* val, int64_t mean_bound, const void* Gp, float* out, hipStream_t s);
 // out[t][e] = sum of the 8 partials [8][T][K] + add on the sparse rows' entries (fp32).
 hipError_t launch_sum_parts(int64_t T, int K, const int32_t* row_nnz, const uint8_t* row_ovf, const float* part,
                             float add, float* out, hipStream_t s);

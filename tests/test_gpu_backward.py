@@ -94,6 +94,42 @@ def test_backward_small_full(T, d, f, K, S, lam_scale):
     assert rel_l2(to_f64(dX)[ovf], rdX[ovf]) <= 2e-2
 
 
+def test_backward_hot_units_exceed_staged_lists():
+    """Units active in every token have lists longer than one block's LDS stage, so their
+    per-unit gathers read the lists from global memory; results still meet the oracle."""
+    T, d, f = 12800, 512, 1024
+    w = wl.make_ffn("hot", "bf16", T, d, f, seed=17, sparsity=0.99, ell_width=64, with_dy=True)
+    w.bias_f = np.zeros(f, dtype=np.float32)
+    w.bias_f[[5, 6, 700]] = 100.0  # always active
+    X, Wu, Wd, dY = dev(w.X), dev(w.W_up), dev(w.W_down), dev(w.dY)
+    cfg = b.make_cfg(**w.cfg)
+    bufs = b.alloc_twell(T, f, "bf16", cfg)
+    Y = torch.empty((T, d), dtype=torch.bfloat16, device="cuda")
+    kw = dict(Y=Y, bufs=bufs, bias_f=dev(w.bias_f), shift_t=dev(w.shift_t))
+    ws = torch.empty(max(1, b.sfl_workspace_size(b.ffn_args(X, Wu, Wd, cfg, **kw))), dtype=torch.uint8, device="cuda")
+    b.sfl_ffn_forward(b.ffn_args(X, Wu, Wd, cfg, **kw, workspace=ws))
+    lam = 1e-3 * T * f
+    dX = torch.empty((T, d), dtype=torch.bfloat16, device="cuda")
+    dWu = torch.empty((d, f), dtype=torch.float32, device="cuda")
+    dWd = torch.empty((f, d), dtype=torch.float32, device="cuda")
+    ba = b.bwd_args(X, Wu, Wd, dY, cfg, bufs, lam, dX, dWu, dWd)
+    bws = torch.empty(max(1, b.sfl_workspace_size(ba, 1)), dtype=torch.uint8, device="cuda")
+    b.sfl_ffn_backward(b.bwd_args(X, Wu, Wd, dY, cfg, bufs, lam, dX, dWu, dWd, workspace=bws))
+    torch.cuda.synchronize()
+    act = gpu_pattern(bufs, w, cfg)
+    assert act[:, 5].sum() == T and act[:, 700].sum() == T
+    Xd, Wud, Wdd, dYd = w.as_f64(w.X), w.as_f64(w.W_up), w.as_f64(w.W_down), w.as_f64(w.dY)
+    Z = ffn.preactivation(Xd, Wud, w.bias_f, w.shift_t)
+    A = act.toarray()
+    rdX, rdWu, rdWd, _ = ffn.ffn_backward(Xd, Wud, Wdd, dYd, np.where(A, Z, 0.0), A, lam)
+    assert rel_l2(to_f64(dWd), rdWd) <= 2e-2
+    assert rel_l2(to_f64(dWu), rdWu) <= 2e-2
+    assert rel_l2(to_f64(dX), rdX) <= 2e-2
+    for n in (5, 700):  # the long lists themselves
+        assert rel_l2(to_f64(dWd)[n], rdWd[n]) <= 2e-2
+        assert rel_l2(to_f64(dWu)[:, n], rdWu[:, n]) <= 2e-2
+
+
 def test_backward_lambda_term_is_injected():
     """With dY = 0 the gradients come from the L1 term alone: dZ = lambda/(T f) on the pattern."""
     w = wl.make_ffn("l1", "bf16", 200, 512, 1024, seed=5, sparsity=0.95, ell_width=128, with_dy=True)
