@@ -129,6 +129,22 @@ class Bench:
         t.cuda.synchronize()
         return e0.elapsed_time(e1) / steps
 
+    def per_call(self, fn, n=20, flush=None):
+        """Per-call ms of n calls, each timed alone (events around it); with `flush`, that
+        callable runs before each call, outside the timed span (cold caches)."""
+        t = self.torch
+        out = []
+        for _ in range(n):
+            if flush is not None:
+                flush()
+            e0, e1 = t.cuda.Event(enable_timing=True), t.cuda.Event(enable_timing=True)
+            e0.record(self.stream)
+            fn()
+            e1.record(self.stream)
+            t.cuda.synchronize()
+            out.append(e0.elapsed_time(e1))
+        return np.array(out)
+
     def stage_times(self, make_args, call, n_ev, steps=None):
         b = self.b
         steps = steps or self.steps
@@ -328,6 +344,20 @@ def main():
               "note": "effective rate: each token re-reads its W_down rows; they are served from L2, "
                       "so this exceeds the HBM peak; the HBM bytes actually moved are `traffic`"}
 
+    # distribution of single calls, warm and cold: before each cold call a 1 GiB buffer is
+    # written, which evicts W_up, W_down and X from L2 and the 256 MiB infinity cache
+    scratch = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    flush = lambda: scratch.fill_(1)
+    warm = B.per_call(lambda: b.sfl_ffn_forward(s["args"], B.stream))
+    cold = B.per_call(lambda: b.sfl_ffn_forward(s["args"], B.stream), flush=flush)
+    cold_dense = B.per_call(lambda: b.sfl_dense_ffn_baseline(s["dargs"], B.stream), flush=flush)
+    del scratch
+    pct = lambda v: {"median": round(float(np.median(v)), 4), "p10": round(float(np.percentile(v, 10)), 4),
+                     "p90": round(float(np.percentile(v, 90)), 4)}
+    timing = {"calls": len(warm), "warm_ms": pct(warm), "cold_ms": pct(cold), "cold_dense_ms": pct(cold_dense),
+              "cold_tokens_per_s": round(T / float(np.median(cold)) * 1e3, 1),
+              "cold_speedup_vs_dense": round(float(np.median(cold_dense)) / float(np.median(cold)), 4)}
+
     out = {
         "metric": "sparse FFN tokens/sec at 99% sparsity; HBM GB/s % peak; speedup vs dense FFN",
         "value": head["tokens_per_s"],
@@ -352,6 +382,7 @@ def main():
         "dense_torch_ms_per_step": head.get("dense_torch_ms"),
         "speedup_vs_dense_torch": head.get("speedup_vs_dense_torch"),
         "stages_ms": stages,
+        "single_call_timing": timing,
         "ms_per_step_w_down_packed_per_call": round(ms_unpacked, 4),
         "n_ovf_rows": head["n_ovf_rows"],
         "roofline": roofline,
