@@ -187,41 +187,59 @@ typedef struct {
   int32_t n_events;
 } sfl_ffn_args_t;
 
-/* Arguments of the backward entry point (non-gated ReLU FFN, bf16).
- * Gradients of  sum(dY * Y) + lambda_l1 / (T f) * sum |H|  (eq. l1 with one layer)
- * through the activity pattern the forward saved in `saved`:
- *   dH = dY W_down^T + lambda_l1/(T f) on active entries, dZ = dH on the pattern,
- *   dW_down = H^T dY, dW_up = X^T dZ, dX = dZ W_up^T  (eq. sec3:eq:all_other_gradients,
- *   non-gated case).
+/* Arguments of the backward entry point (bf16).
+ * Gradients of  sum(dY * Y) + lambda_l1 / (T f) * sum |h|  (eq. l1 with one layer)
+ * through the activity pattern the forward saved in `saved`
+ * (eq. sec3:eq:all_other_gradients):
+ *  non-gated (h = ReLU(z), z = X W_up + b + s):
+ *    dh = dY W_down^T + lambda_l1/(T f) on active entries, dz = dh on the pattern,
+ *    dW_down = H^T dY, dW_up = X^T dz, dX = dz W_up^T;
+ *  gated (h = h_g * h_u, h_g = ReLU(X W_gate + b + s), h_u = X W_up):
+ *    dh = dY W_down^T + lambda_l1/(T f) sign(h) on the pattern, dh_u = dh * h_g,
+ *    dh_g = dh * h_u (on the pattern), dW_up = X^T dh_u, dW_gate = X^T dh_g,
+ *    dW_down = H^T dY, dX = dh_u W_up^T + dh_g W_gate^T. h_u is recomputed (one
+ *    up-dot pass over the pattern), as are the dense-backup rows' h_g and h_u.
+ *  gated     0 or 1, as in the forward
+ *  X, W_gate, W_up, W_down, dY  as in the forward; dY [T][d] activation dtype
+ *  W_upT, W_gateT  optional [f][d] transposed copies (transposed into the workspace
+ *            when NULL and needed)
+ *  W_down_packed, W_up_packed, W_gate_packed  optional slice-major copies ([d/64][f][64])
+ *            of W_down, of W_up^T and of W_gate^T (sfl_pack_down_weights of W_down, W_up^T,
+ *            W_gate^T); built in the workspace on every call when NULL. The sparse
+ *            products walk 64-column slices of them, one slice per XCD at a time.
+ *  bias_f, shift_t  gated: the forward's gate bias / row shift (optional, as there)
  *  dX        [T][d] activation dtype (overwritten)
+ *  dW_gate   gated: float32 [d][f] (overwritten)
  *  dW_up     float32 [d][f] (overwritten)
  *  dW_down   float32 [f][d] (overwritten)
- *  W_upT     optional [f][d]; transposed into the workspace when NULL.
- *  W_down_packed, W_up_packed  optional slice-major copies ([d/64][f][64]) of W_down and
- *            of W_up^T, as the forward takes them (sfl_pack_down_weights of W_down and
- *            of W_up^T); built in the workspace on every call when NULL. The dZ and dX
- *            gathers walk 64-column slices of them, one slice per XCD at a time.
  *  saved     the sfl_twell_t the forward filled (row_nnz, row_ovf, ovf_rows, n_ovf,
- *            ell_val, ell_idx and ovf_dense are read)
+ *            ell_val, ell_idx and ovf_dense are read; ovf_dense only when non-gated)
  *  events / n_events  optional hipEvent_t array recorded at stage boundaries (0: start,
- *            1: after dZ at the pattern, 2: after dX of the sparse rows, 3: after the
+ *            1: after dh at the pattern, 2: after dX of the sparse rows, 3: after the
  *            transposed pattern, 4: after the weight gradients of the sparse rows,
  *            5: end, after the dense-backup rows).
  * Supports d % 512 == 0, f % 64 == 0, f <= 40960 and T <= 2^31 / (2 d). */
 typedef struct {
   sfl_dtype_t dtype;
+  int32_t gated;
   int64_t T, d, f;
   const void* X;
+  const void* W_gate;
   const void* W_up;
   const void* W_down;
   const void* W_upT;
+  const void* W_gateT;
   const void* W_down_packed;
   const void* W_up_packed;
+  const void* W_gate_packed;
+  const float* bias_f;
+  const float* shift_t;
   const void* dY;
   sfl_twell_cfg_t cfg;
   sfl_twell_t saved;
   double lambda_l1;
   void* dX;
+  float* dW_gate;
   float* dW_up;
   float* dW_down;
   void* workspace;

@@ -63,12 +63,14 @@ class FfnArgs(Structure):
 
 
 class BwdArgs(Structure):
-    _fields_ = [("dtype", c_int), ("T", c_int64), ("d", c_int64), ("f", c_int64),
-                ("X", c_void_p), ("W_up", c_void_p), ("W_down", c_void_p), ("W_upT", c_void_p),
-                ("W_down_packed", c_void_p), ("W_up_packed", c_void_p),
+    _fields_ = [("dtype", c_int), ("gated", c_int32), ("T", c_int64), ("d", c_int64), ("f", c_int64),
+                ("X", c_void_p), ("W_gate", c_void_p), ("W_up", c_void_p), ("W_down", c_void_p),
+                ("W_upT", c_void_p), ("W_gateT", c_void_p),
+                ("W_down_packed", c_void_p), ("W_up_packed", c_void_p), ("W_gate_packed", c_void_p),
+                ("bias_f", c_void_p), ("shift_t", c_void_p),
                 ("dY", c_void_p), ("cfg", Cfg), ("saved", Twell), ("lambda_l1", c_double),
-                ("dX", c_void_p), ("dW_up", c_void_p), ("dW_down", c_void_p), ("workspace", c_void_p),
-                ("workspace_bytes", c_size_t), ("events", c_void_p), ("n_events", c_int32)]
+                ("dX", c_void_p), ("dW_gate", c_void_p), ("dW_up", c_void_p), ("dW_down", c_void_p),
+                ("workspace", c_void_p), ("workspace_bytes", c_size_t), ("events", c_void_p), ("n_events", c_int32)]
 
 
 _lib.sfl_status_string.restype = c_char_p
@@ -220,7 +222,8 @@ def sfl_dense_ffn_baseline(args, stream=None):
 
 
 def bwd_args(X, W_up, W_down, dY, cfg, saved_bufs, lambda_l1, dX, dW_up, dW_down, *, W_upT=None, W_down_packed=None,
-             W_up_packed=None, workspace=None, events=None):
+             W_up_packed=None, W_gate=None, W_gateT=None, W_gate_packed=None, dW_gate=None, bias_f=None,
+             shift_t=None, workspace=None, events=None):
     T, d = X.shape
     f = W_down.shape[0]
     a = BwdArgs()
@@ -228,6 +231,9 @@ def bwd_args(X, W_up, W_down, dY, cfg, saved_bufs, lambda_l1, dX, dW_up, dW_down
     a.T, a.d, a.f = T, d, f
     a.X, a.W_up, a.W_down, a.W_upT, a.dY = _ptr(X), _ptr(W_up), _ptr(W_down), _ptr(W_upT), _ptr(dY)
     a.W_down_packed, a.W_up_packed = _ptr(W_down_packed), _ptr(W_up_packed)
+    a.gated = 1 if W_gate is not None else 0
+    a.W_gate, a.W_gateT, a.W_gate_packed = _ptr(W_gate), _ptr(W_gateT), _ptr(W_gate_packed)
+    a.bias_f, a.shift_t, a.dW_gate = _ptr(bias_f), _ptr(shift_t), _ptr(dW_gate)
     a.cfg = cfg
     a.saved = _twell_struct(saved_bufs)
     a.lambda_l1 = float(lambda_l1)

@@ -89,13 +89,19 @@ __global__ __launch_bounds__(1024) void k_col_ptr(int64_t f, const int32_t* __re
 
 // (d) fill: one wave per block walks its tokens in order; a unit appears at most once per
 // token, so the lanes of one token never share a unit, and the per-unit cursor in LDS
-// gives each (token, entry) its place in token order. The entry's h and dz go beside it.
+// gives each (token, entry) its place in token order. Up to three per-entry values go
+// beside the token (fp32 sources [T][K]; value 0 may come from the bf16 ELL values).
+struct FillValues {
+  const bf16_t* hb;    // when non-null: value 0 from these bf16 entries
+  const float* v[3];   // fp32 sources (null: unused)
+  float* out[3];       // [T K] destinations in list order
+};
+
 __global__ __launch_bounds__(64) void k_blk_fill(int64_t T, int K, int64_t f, const uint16_t* __restrict__ ell_idx,
                                                  const int32_t* __restrict__ row_nnz,
                                                  const uint8_t* __restrict__ row_ovf, const int32_t* __restrict__ bc,
-                                                 const int32_t* __restrict__ col_ptr, const bf16_t* __restrict__ ell_val,
-                                                 const float* __restrict__ dz, int32_t* __restrict__ csc_tok,
-                                                 float* __restrict__ csc_h, float* __restrict__ csc_z) {
+                                                 const int32_t* __restrict__ col_ptr, int32_t* __restrict__ csc_tok,
+                                                 FillValues fv) {
   extern __shared__ int32_t cursor[];  // [f]
   const int64_t b = blockIdx.x;
   const int l = threadIdx.x;
@@ -107,14 +113,48 @@ __global__ __launch_bounds__(64) void k_blk_fill(int64_t T, int K, int64_t f, co
     if (row_ovf[t]) continue;
     const int nnz = row_nnz[t];
     for (int e = l; e < nnz; e += 64) {
-      const int n = ell_idx[t * (int64_t)K + e];
+      const int64_t src = t * (int64_t)K + e;
+      const int n = ell_idx[src];
       const int pos = col_ptr[n] + bc[b * f + n] + cursor[n];
       cursor[n] += 1;
       csc_tok[pos] = (int32_t)t;
-      csc_h[pos] = bf16_to_f32(ell_val[t * (int64_t)K + e]);
-      csc_z[pos] = dz[t * (int64_t)K + e];
+      if (fv.out[0]) fv.out[0][pos] = fv.hb ? bf16_to_f32(fv.hb[src]) : fv.v[0][src];
+      if (fv.out[1]) fv.out[1][pos] = fv.v[1][src];
+      if (fv.out[2]) fv.out[2][pos] = fv.v[2][src];
     }
     __syncthreads();
+  }
+}
+
+// Gated dense-backup rows (counted rows r < min(n_ovf, cap)): from the recomputed gate
+// pre-activation G, h_u = U and D = dY W_down^T (fp32 [cap][f]):
+// h_g = ReLU(G), h = h_g U, dh = D + lambda' sign(h), dh_u = dh h_g, dh_g = [G > 0] dh U.
+__global__ __launch_bounds__(256) void k_gated_ovf_grads(int64_t f, const int32_t* __restrict__ n_ovf, int32_t cap,
+                                                         const float* __restrict__ G, const float* __restrict__ U,
+                                                         const float* __restrict__ D, float lam,
+                                                         bf16_t* __restrict__ dhu, bf16_t* __restrict__ dhg,
+                                                         bf16_t* __restrict__ h) {
+  const int64_t total = (int64_t)min(*n_ovf, cap) * f;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const float g = G[i], u = U[i];
+    const bool on = g > 0.f;
+    const float hg = on ? g : 0.f;
+    const float hh = hg * u;
+    const float dh = D[i] + (hh > 0.f ? lam : hh < 0.f ? -lam : 0.f);
+    dhu[i] = f32_to_bf16(dh * hg);
+    dhg[i] = f32_to_bf16(on ? dh * u : 0.f);
+    h[i] = f32_to_bf16(hh);
+  }
+}
+
+// dX[ovf_rows[r]] = bf16(acc[r]) for the counted dense-backup rows.
+__global__ __launch_bounds__(256) void k_scatter_rows(int64_t d, const int32_t* __restrict__ n_ovf, int32_t cap,
+                                                      const int32_t* __restrict__ rows, const float* __restrict__ acc,
+                                                      bf16_t* __restrict__ out) {
+  const int64_t total = (int64_t)min(*n_ovf, cap) * d;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int64_t r = i / d, c = i % d;
+    out[(int64_t)rows[r] * d + c] = f32_to_bf16(acc[i]);
   }
 }
 
@@ -126,21 +166,34 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct BwdPlan {
-  float* dz = nullptr;        // [T][K]
-  float* part = nullptr;      // [8][T][K] per-XCD partial dz
+  float* dz = nullptr;        // [T][K] non-gated: dz; gated: dh_u
+  float* part = nullptr;      // [8][T][K] per-XCD partial dots
+  float* u = nullptr;         // gated: [T][K] h_u at the pattern
+  float* dhg = nullptr;       // gated: [T][K] dh_g
+  float* hf = nullptr;        // gated: [T][K] h = h_g h_u
   int32_t* bc = nullptr;      // [nb][f]
   int32_t* col_cnt = nullptr; // [f]
   int32_t* col_ptr = nullptr; // [f + 1]
   int32_t* csc_tok = nullptr; // [T K]
-  float* csc_h = nullptr;     // [T K]
-  float* csc_z = nullptr;     // [T K]
+  float* csc_h = nullptr;     // [T K] h
+  float* csc_z = nullptr;     // [T K] dz (gated: dh_u)
+  float* csc_g = nullptr;     // [T K] gated: dh_g
   float* dWuT = nullptr;      // [f][d]
+  float* dWgT = nullptr;      // gated: [f][d]
   void* WupT = nullptr;       // [f][d] when neither W_upT nor W_up_packed is given
+  void* WgT = nullptr;        // gated: [f][d] when neither W_gateT nor W_gate_packed is given
   void* WdP = nullptr;        // slice-major W_down when not given
   void* WuP = nullptr;        // slice-major W_up^T when not given
+  void* WgP = nullptr;        // gated: slice-major W_gate^T when not given
   void* dYP = nullptr;        // slice-major dY [d/64][T][64]
   void* XP = nullptr;         // slice-major X
-  void* dz_ovf = nullptr;     // [cap][f] bf16
+  void* dz_ovf = nullptr;     // [cap][f] bf16 (gated: dh_u of the dense-backup rows)
+  float* Gf = nullptr;        // gated: [cap][f] recomputed gate pre-activations
+  float* Uf = nullptr;        // gated: [cap][f] recomputed h_u
+  float* Df = nullptr;        // gated: [cap][f] dY W_down^T
+  void* dhg_ovf = nullptr;    // gated: [cap][f] bf16
+  void* h_ovf = nullptr;      // gated: [cap][f] bf16
+  float* dx_ovf = nullptr;    // gated: [cap][d] fp32
   size_t bytes = 0;
 };
 
@@ -156,21 +209,39 @@ BwdPlan plan_backward(const sfl_ffn_bwd_args_t& a, void* ws) {
   const int64_t T = a.T, d = a.d, f = a.f, K = a.cfg.ell_width;
   const int64_t cap = a.cfg.ovf_capacity > 0 ? std::min<int64_t>(a.cfg.ovf_capacity, T) : T;
   const int64_t nb = cdiv(T, kBlkTok);
+  const bool gated = a.gated != 0;
   p.dz = (float*)take((size_t)T * K * 4);
   p.part = (float*)take((size_t)8 * T * K * 4);
+  if (gated) {
+    p.u = (float*)take((size_t)T * K * 4);
+    p.dhg = (float*)take((size_t)T * K * 4);
+    p.hf = (float*)take((size_t)T * K * 4);
+  }
   p.bc = (int32_t*)take((size_t)nb * f * 4);
   p.col_cnt = (int32_t*)take((size_t)f * 4);
   p.col_ptr = (int32_t*)take((size_t)(f + 1) * 4);
   p.csc_tok = (int32_t*)take((size_t)T * K * 4);
   p.csc_h = (float*)take((size_t)T * K * 4);
   p.csc_z = (float*)take((size_t)T * K * 4);
+  if (gated) p.csc_g = (float*)take((size_t)T * K * 4);
   p.dWuT = (float*)take((size_t)f * d * 4);
+  if (gated) p.dWgT = (float*)take((size_t)f * d * 4);
   if (!a.W_upT && !a.W_up_packed) p.WupT = take((size_t)f * d * 2);
+  if (gated && !a.W_gateT && !a.W_gate_packed) p.WgT = take((size_t)f * d * 2);
   if (!a.W_down_packed) p.WdP = take((size_t)f * d * 2);
   if (!a.W_up_packed) p.WuP = take((size_t)f * d * 2);
+  if (gated && !a.W_gate_packed) p.WgP = take((size_t)f * d * 2);
   p.dYP = take((size_t)T * d * 2);
   p.XP = take((size_t)T * d * 2);
   p.dz_ovf = take((size_t)cap * f * 2);
+  if (gated) {
+    p.Gf = (float*)take((size_t)cap * f * 4);
+    p.Uf = (float*)take((size_t)cap * f * 4);
+    p.Df = (float*)take((size_t)cap * f * 4);
+    p.dhg_ovf = take((size_t)cap * f * 2);
+    p.h_ovf = take((size_t)cap * f * 2);
+    p.dx_ovf = (float*)take((size_t)cap * d * 4);
+  }
   p.bytes = used;
   return p;
 }
@@ -183,16 +254,24 @@ sfl_status_t check_backward(const sfl_ffn_bwd_args_t* a) {
   if (a->dtype != SFL_BF16) return SFL_E_UNSUPPORTED;
   if (a->d % 512 != 0 || a->f % 64 != 0) return SFL_E_UNSUPPORTED;
   if (a->f > 40960) return SFL_E_UNSUPPORTED;  // the transpose keeps one cursor per unit in LDS
-  if (!a->dW_up || !a->dW_down) return SFL_E_ARG;
+  if (!a->dW_up || !a->dW_down || (a->gated && !a->dW_gate)) return SFL_E_ARG;
   if (a->T > 0) {
     if (!a->X || !a->W_up || !a->W_down || !a->dY || !a->dX) return SFL_E_ARG;
+    if (a->gated && !a->W_gate) return SFL_E_ARG;
     const sfl_twell_t& s = a->saved;
-    if (!s.row_nnz || !s.row_ovf || !s.ovf_rows || !s.n_ovf || !s.ell_val || !s.ell_idx || !s.ovf_dense)
-      return SFL_E_ARG;
+    if (!s.row_nnz || !s.row_ovf || !s.ovf_rows || !s.n_ovf || !s.ell_val || !s.ell_idx) return SFL_E_ARG;
+    if (!a->gated && !s.ovf_dense) return SFL_E_ARG;
   }
   const int64_t lim = (int64_t)1 << 31;
-  if (a->T * a->d * 2 >= lim || a->d * a->f * 4 >= lim || a->T * a->f * 2 >= lim) return SFL_E_UNSUPPORTED;
+  if (a->T * a->d * 2 >= lim || a->d * a->f * 4 >= lim || a->T * a->f * 4 >= lim) return SFL_E_UNSUPPORTED;
   return SFL_OK;
+}
+
+// GEMM parameter block with everything zero.
+GemmParams gp0() {
+  GemmParams g;
+  std::memset(&g, 0, sizeof(g));
+  return g;
 }
 
 }  // namespace
@@ -223,12 +302,14 @@ sfl_status_t backward_run(const sfl_ffn_bwd_args_t* a, hipStream_t s) {
   const int64_t T = a->T, d = a->d, f = a->f;
   const int K = a->cfg.ell_width;
   const int64_t cap = a->cfg.ovf_capacity > 0 ? std::min<int64_t>(a->cfg.ovf_capacity, T) : T;
+  const bool gated = a->gated != 0;
   if (T == 0) {
     // no tokens: the weight gradients are zero
-    hipLaunchKernelGGL(k_zero_f32, dim3(1024), dim3(256), 0, s, a->dW_down, f * d);
-    SFL_HIPB(hipGetLastError());
-    hipLaunchKernelGGL(k_zero_f32, dim3(1024), dim3(256), 0, s, a->dW_up, f * d);
-    SFL_HIPB(hipGetLastError());
+    for (float* g : {a->dW_down, a->dW_up, gated ? a->dW_gate : nullptr}) {
+      if (!g) continue;
+      hipLaunchKernelGGL(k_zero_f32, dim3(1024), dim3(256), 0, s, g, f * d);
+      SFL_HIPB(hipGetLastError());
+    }
     for (int i = 1; i < 6; ++i) rec(i);
     return SFL_OK;
   }
@@ -239,30 +320,52 @@ sfl_status_t backward_run(const sfl_ffn_bwd_args_t* a, hipStream_t s) {
   const bf16_t* ev = (const bf16_t*)sv.ell_val;
   const int64_t nb = cdiv(T, kBlkTok);
 
-  // slice-major weight copies (given, or built here)
+  // slice-major weight copies (given, or built here): of W_down, W_up^T and W_gate^T
+  auto packed_T = [&](const void* given_packed, const void* given_T, const void* W, void* tmpT, void* out,
+                      const void** res) -> hipError_t {
+    if (given_packed) {
+      *res = given_packed;
+      return hipSuccess;
+    }
+    const void* WT = given_T;
+    if (!WT) {
+      const hipError_t e = launch_transpose(W, tmpT, d, f, 2, s);
+      if (e != hipSuccess) return e;
+      WT = tmpT;
+    }
+    *res = out;
+    return launch_pack_down(WT, out, f, d, s);
+  };
   const void* WdP = a->W_down_packed;
   if (!WdP) {
     SFL_HIPB(launch_pack_down(a->W_down, p.WdP, f, d, s));
     WdP = p.WdP;
   }
-  const void* WuP = a->W_up_packed;
-  if (!WuP) {
-    const void* WupT = a->W_upT;
-    if (!WupT) {
-      SFL_HIPB(launch_transpose(a->W_up, p.WupT, d, f, 2, s));
-      WupT = p.WupT;
-    }
-    SFL_HIPB(launch_pack_down(WupT, p.WuP, f, d, s));
-    WuP = p.WuP;
+  const void *WuP = nullptr, *WgP = nullptr;
+  SFL_HIPB(packed_T(a->W_up_packed, a->W_upT, a->W_up, p.WupT, p.WuP, &WuP));
+  if (gated) SFL_HIPB(packed_T(a->W_gate_packed, a->W_gateT, a->W_gate, p.WgT, p.WgP, &WgP));
+
+  // 1. dh at the pattern of the sparse rows: per-XCD partial dots dY . W_down[n], then
+  //    non-gated: dz = sum + lambda'; gated: h_u recomputed the same way from X and W_up,
+  //    then dh_u, dh_g and h per entry
+  if (!gated) {
+    SFL_HIPB(launch_gated_updot(T, d, f, K, sv.ell_idx, sv.row_nnz, sv.row_ovf, dY, WdP, p.part, s));
+    SFL_HIPB(launch_sum_parts(T, K, sv.row_nnz, sv.row_ovf, p.part, lam, p.dz, s));
+  } else {
+    SFL_HIPB(launch_gated_updot(T, d, f, K, sv.ell_idx, sv.row_nnz, sv.row_ovf, X, WuP, p.part, s));
+    SFL_HIPB(launch_sum_parts(T, K, sv.row_nnz, sv.row_ovf, p.part, 0.f, p.u, s));  // h_u
+    SFL_HIPB(launch_gated_updot(T, d, f, K, sv.ell_idx, sv.row_nnz, sv.row_ovf, dY, WdP, p.part, s));
+    SFL_HIPB(launch_gated_entry_grads(T, K, ev, sv.row_nnz, sv.row_ovf, p.part, p.u, lam, p.dz, p.dhg, p.hf, s));
   }
-  // 1. dz at the pattern of the sparse rows: per-XCD partial dots, then their sum + lambda'
-  SFL_HIPB(launch_gated_updot(T, d, f, K, sv.ell_idx, sv.row_nnz, sv.row_ovf, dY, WdP, p.part, s));
-  SFL_HIPB(launch_sum_parts(T, K, sv.row_nnz, sv.row_ovf, p.part, lam, p.dz, s));
   rec(1);
-  // 2. dX of the sparse rows
-  SFL_HIPB(launch_gather_down_packed(T, d, f, K, p.dz, sv.ell_idx, sv.row_nnz, sv.row_ovf, WuP, a->dX, s, 1));
+  // 2. dX of the sparse rows (gated: dh_u W_up^T + dh_g W_gate^T in one pass)
+  if (!gated)
+    SFL_HIPB(launch_gather_down_packed(T, d, f, K, p.dz, sv.ell_idx, sv.row_nnz, sv.row_ovf, WuP, a->dX, s, 1));
+  else
+    SFL_HIPB(launch_gather_down_packed(T, d, f, K, p.dz, sv.ell_idx, sv.row_nnz, sv.row_ovf, WuP, a->dX, s, 1, p.dhg,
+                                       WgP));
   rec(2);
-  // 3. transposed pattern, with each entry's h and dz
+  // 3. transposed pattern, with each entry's values
   hipLaunchKernelGGL(k_blk_count, dim3((unsigned)nb), dim3(256), 0, s, T, K, f, sv.ell_idx, sv.row_nnz, sv.row_ovf,
                      p.bc);
   SFL_HIPB(hipGetLastError());
@@ -273,8 +376,21 @@ sfl_status_t backward_run(const sfl_ffn_bwd_args_t* a, hipStream_t s) {
   const size_t fill_lds = (size_t)f * 4;
   if (fill_lds > 65536)
     SFL_HIPB(hipFuncSetAttribute((const void*)k_blk_fill, hipFuncAttributeMaxDynamicSharedMemorySize, (int)fill_lds));
+  FillValues fv;
+  std::memset(&fv, 0, sizeof(fv));
+  if (!gated) {
+    fv.hb = ev;  // h = the stored activation
+    fv.v[1] = p.dz;
+  } else {
+    fv.v[0] = p.hf;
+    fv.v[1] = p.dz;  // dh_u
+    fv.v[2] = p.dhg;
+    fv.out[2] = p.csc_g;
+  }
+  fv.out[0] = p.csc_h;
+  fv.out[1] = p.csc_z;
   hipLaunchKernelGGL(k_blk_fill, dim3((unsigned)nb), dim3(64), fill_lds, s, T, K, f, sv.ell_idx, sv.row_nnz,
-                     sv.row_ovf, p.bc, p.col_ptr, ev, p.dz, p.csc_tok, p.csc_h, p.csc_z);
+                     sv.row_ovf, p.bc, p.col_ptr, p.csc_tok, fv);
   SFL_HIPB(hipGetLastError());
   rec(3);
   // 4. weight gradients of the sparse rows: per-unit gathers over slice-major dY and X
@@ -284,21 +400,49 @@ sfl_status_t backward_run(const sfl_ffn_bwd_args_t* a, hipStream_t s) {
   SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, p.csc_tok, p.csc_h, mean_bound, p.dYP, a->dW_down, s));
   SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, p.csc_tok, p.csc_z, mean_bound, p.XP, p.dWuT, s));
   SFL_HIPB(launch_transpose(p.dWuT, a->dW_up, f, d, 4, s));
+  if (gated) {
+    SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, p.csc_tok, p.csc_g, mean_bound, p.XP, p.dWgT, s));
+    SFL_HIPB(launch_transpose(p.dWgT, a->dW_gate, f, d, 4, s));
+  }
   rec(4);
-  // 5. dense-backup rows: masked GEMMs, accumulated into the weight gradients
-  {
-    GemmParams g;
-    std::memset(&g, 0, sizeof(g));
-    // dZ_ovf = [H_ovf > 0] (dY_ovf W_down^T + lam)
+  // 5. dense-backup rows: GEMMs over the counted rows, accumulated into the weight gradients
+  auto rows_gemm = [&](GemmParams& g, const void* A, int64_t a_rows_total, int M_N, int K_) {
     g.M = (int)cap;
-    g.N = (int)f;
-    g.K = (int)d;
-    g.A = dY;
-    g.lda = d;
-    g.a_bytes = T * d * 2;
+    g.N = M_N;
+    g.K = K_;
+    g.A = A;
+    g.lda = K_;
+    g.a_bytes = a_rows_total * K_ * 2;
     g.a_rows = sv.ovf_rows;
     g.m_count = sv.n_ovf;
     g.count_cap = (int32_t)cap;
+  };
+  // A = H-like [cap][f] as [K = m][M = f] against dY / X rows as [K = m][N = d]:
+  // out [f][d] or [d][f] += over the counted rows
+  auto accum_wgrad = [&](const void* Arows, const int32_t* a_rows, int64_t a_total, int64_t a_ld, int M, const void* B,
+                         const int32_t* b_rows, int64_t b_total, int64_t b_ld, int N, float* out) -> hipError_t {
+    GemmParams w = gp0();
+    w.M = M;
+    w.N = N;
+    w.K = (int)cap;
+    w.A = Arows;
+    w.lda = a_ld;
+    w.a_bytes = a_total * a_ld * 2;
+    w.a_rows = a_rows;
+    w.B = B;
+    w.ldb = b_ld;
+    w.b_bytes = b_total * b_ld * 2;
+    w.b_rows = b_rows;
+    w.k_count = sv.n_ovf;
+    w.count_cap = (int32_t)cap;
+    w.C = out;
+    w.ldc = N;
+    return gemm_bf16(LAY_RCG_, LAY_RCG_, EPI_ACCUM_F32, w, s);
+  };
+  if (!gated) {
+    // dZ_ovf = [H_ovf > 0] (dY_ovf W_down^T + lam)
+    GemmParams g = gp0();
+    rows_gemm(g, dY, T, (int)f, (int)d);
     g.B = a->W_down;
     g.ldb = d;
     g.b_bytes = f * d * 2;
@@ -309,8 +453,7 @@ sfl_status_t backward_run(const sfl_ffn_bwd_args_t* a, hipStream_t s) {
     g.lam = lam;
     SFL_HIPB(gemm_bf16(LAY_KC, LAY_KC, EPI_MASKGRAD, g, s));
     // dX_ovf = dZ_ovf W_up^T  (B = W_up [d][f] read as [N = d][K = f])
-    GemmParams x;
-    std::memset(&x, 0, sizeof(x));
+    GemmParams x = gp0();
     x.M = (int)cap;
     x.N = (int)d;
     x.K = (int)f;
@@ -326,44 +469,75 @@ sfl_status_t backward_run(const sfl_ffn_bwd_args_t* a, hipStream_t s) {
     x.C = a->dX;
     x.ldc = d;
     SFL_HIPB(gemm_bf16(LAY_KC, LAY_KC, EPI_ACT, x, s));
-    // dW_down += H_ovf^T dY_ovf: A = H_ovf as [K = m][M = f], B = dY rows as [K = m][N = d]
-    GemmParams w;
-    std::memset(&w, 0, sizeof(w));
-    w.M = (int)f;
-    w.N = (int)d;
-    w.K = (int)cap;
-    w.A = sv.ovf_dense;
-    w.lda = f;
-    w.a_bytes = cap * f * 2;
-    w.a_rows = nullptr;
-    w.B = dY;
-    w.ldb = d;
-    w.b_bytes = T * d * 2;
-    w.b_rows = sv.ovf_rows;
-    w.k_count = sv.n_ovf;
-    w.count_cap = (int32_t)cap;
-    w.C = a->dW_down;
-    w.ldc = d;
-    SFL_HIPB(gemm_bf16(LAY_RCG_, LAY_RCG_, EPI_ACCUM_F32, w, s));
-    // dW_up += X_ovf^T dZ_ovf: A = X rows as [K = m][M = d], B = dZ_ovf as [K = m][N = f]
-    GemmParams u;
-    std::memset(&u, 0, sizeof(u));
-    u.M = (int)d;
-    u.N = (int)f;
-    u.K = (int)cap;
-    u.A = X;
-    u.lda = d;
-    u.a_bytes = T * d * 2;
-    u.a_rows = sv.ovf_rows;
-    u.B = p.dz_ovf;
-    u.ldb = f;
-    u.b_bytes = cap * f * 2;
-    u.b_rows = nullptr;
-    u.k_count = sv.n_ovf;
-    u.count_cap = (int32_t)cap;
-    u.C = a->dW_up;
-    u.ldc = f;
-    SFL_HIPB(gemm_bf16(LAY_RCG_, LAY_RCG_, EPI_ACCUM_F32, u, s));
+    // dW_down += H_ovf^T dY_ovf;  dW_up += X_ovf^T dZ_ovf
+    SFL_HIPB(accum_wgrad(sv.ovf_dense, nullptr, cap, f, (int)f, dY, sv.ovf_rows, T, d, (int)d, a->dW_down));
+    SFL_HIPB(accum_wgrad(X, sv.ovf_rows, T, d, (int)d, p.dz_ovf, nullptr, cap, f, (int)f, a->dW_up));
+  } else {
+    // recompute the rows' gate pre-activations and h_u, and dY W_down^T (fp32 [cap][f])
+    auto weight_B = [&](GemmParams& g, const void* W, const void* WT, int* blay) {
+      g.b_bytes = d * f * 2;
+      if (WT) {
+        g.B = WT;
+        g.ldb = d;
+        *blay = LAY_KC;
+      } else {
+        g.B = W;
+        g.ldb = f;
+        *blay = LAY_RC;
+      }
+    };
+    int blay;
+    GemmParams gg = gp0();
+    rows_gemm(gg, X, T, (int)f, (int)d);
+    weight_B(gg, a->W_gate, a->W_gateT, &blay);
+    gg.bias = a->bias_f;
+    gg.shift = a->shift_t;
+    gg.s_rows = sv.ovf_rows;
+    gg.C = p.Gf;
+    gg.ldc = f;
+    SFL_HIPB(gemm_bf16(LAY_KC, blay, EPI_F32, gg, s));
+    GemmParams gu = gp0();
+    rows_gemm(gu, X, T, (int)f, (int)d);
+    weight_B(gu, a->W_up, a->W_upT, &blay);
+    gu.C = p.Uf;
+    gu.ldc = f;
+    SFL_HIPB(gemm_bf16(LAY_KC, blay, EPI_F32, gu, s));
+    GemmParams gd = gp0();
+    rows_gemm(gd, dY, T, (int)f, (int)d);
+    gd.B = a->W_down;  // [f][d] = [N][K]
+    gd.ldb = d;
+    gd.b_bytes = f * d * 2;
+    gd.C = p.Df;
+    gd.ldc = f;
+    SFL_HIPB(gemm_bf16(LAY_KC, LAY_KC, EPI_F32, gd, s));
+    hipLaunchKernelGGL(k_gated_ovf_grads, dim3(1024), dim3(256), 0, s, f, sv.n_ovf, (int32_t)cap, p.Gf, p.Uf, p.Df,
+                       lam, (bf16_t*)p.dz_ovf, (bf16_t*)p.dhg_ovf, (bf16_t*)p.h_ovf);
+    SFL_HIPB(hipGetLastError());
+    // dX_ovf = dh_u W_up^T + dh_g W_gate^T (fp32 sum, then bf16 into the rows of dX)
+    for (int k = 0; k < 2; ++k) {
+      GemmParams x = gp0();
+      x.M = (int)cap;
+      x.N = (int)d;
+      x.K = (int)f;
+      x.A = k == 0 ? p.dz_ovf : p.dhg_ovf;
+      x.lda = f;
+      x.a_bytes = cap * f * 2;
+      x.m_count = sv.n_ovf;
+      x.count_cap = (int32_t)cap;
+      x.B = k == 0 ? a->W_up : a->W_gate;  // [d][f] = [N][K]
+      x.ldb = f;
+      x.b_bytes = d * f * 2;
+      x.C = p.dx_ovf;
+      x.ldc = d;
+      SFL_HIPB(gemm_bf16(LAY_KC, LAY_KC, k == 0 ? EPI_F32 : EPI_ACCUM_F32, x, s));
+    }
+    hipLaunchKernelGGL(k_scatter_rows, dim3(1024), dim3(256), 0, s, d, sv.n_ovf, (int32_t)cap, sv.ovf_rows, p.dx_ovf,
+                       (bf16_t*)a->dX);
+    SFL_HIPB(hipGetLastError());
+    // dW_down += h^T dY, dW_up += X^T dh_u, dW_gate += X^T dh_g over the rows
+    SFL_HIPB(accum_wgrad(p.h_ovf, nullptr, cap, f, (int)f, dY, sv.ovf_rows, T, d, (int)d, a->dW_down));
+    SFL_HIPB(accum_wgrad(X, sv.ovf_rows, T, d, (int)d, p.dz_ovf, nullptr, cap, f, (int)f, a->dW_up));
+    SFL_HIPB(accum_wgrad(X, sv.ovf_rows, T, d, (int)d, p.dhg_ovf, nullptr, cap, f, (int)f, a->dW_gate));
   }
   rec(5);
   return SFL_OK;

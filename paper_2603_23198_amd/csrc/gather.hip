@@ -209,13 +209,52 @@ __device__ __forceinline__ void slice_token_f32(const uint32_t* er, int nnz, __a
     for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], o, 64);
 }
 
-// VF32: the ELL values are fp32 (the backward's dz), staged as two words per entry.
-template <bool VF32>
+// Two fp32 values per entry against two slice-major matrices (the gated backward's
+// dX = dh_u W_up^T + dh_g W_gate^T): entries are (index, v1 bits, v2 bits) word triples.
+__device__ __forceinline__ void slice_token_dual(const uint32_t* er, int nnz, __amdgpu_buffer_rsrc_t wr,
+                                                 __amdgpu_buffer_rsrc_t wr2, uint32_t col_b, int grp, float (&acc)[8]) {
+  constexpr uint32_t row_b = SLICE2 * 2;
+  constexpr int GD = GU / 2;  // two loads per entry
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+  for (int q = 0; q < nnz; q += NGRP * GD) {
+    u32x4_t w[GD], w2[GD];
+    float v[GD], v2[GD];
+#pragma unroll
+    for (int u = 0; u < GD; ++u) {
+      const int e = q + u * NGRP + grp;
+      const bool ok = e < nnz;
+      v[u] = ok ? __uint_as_float(er[3 * e + 1]) : 0.f;
+      v2[u] = ok ? __uint_as_float(er[3 * e + 2]) : 0.f;
+      const uint32_t off = ok ? er[3 * e] * row_b + col_b : 0x80000000u;
+      w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0));
+      w2[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr2, (int)off, 0, 0));
+    }
+#pragma unroll
+    for (int u = 0; u < GD; ++u)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t ww = w[u][j], ww2 = w2[u][j];
+        acc[2 * j] = fmaf(v[u], bf16lo(ww), acc[2 * j]);
+        acc[2 * j + 1] = fmaf(v[u], bf16hi(ww), acc[2 * j + 1]);
+        acc[2 * j] = fmaf(v2[u], bf16lo(ww2), acc[2 * j]);
+        acc[2 * j + 1] = fmaf(v2[u], bf16hi(ww2), acc[2 * j + 1]);
+      }
+  }
+#pragma unroll
+  for (int o = LPR; o < 64; o <<= 1)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], o, 64);
+}
+
+// VK: kind of the ELL values. 0: bf16 (packed with the index in one word); 1: fp32 (the
+// backward's dz, two words per entry); 2: two fp32 values against W and W2 (three words).
+template <int VK>
 __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
-    int64_t T, int64_t d, int64_t f, int K, const void* __restrict__ ell_val, const uint16_t* __restrict__ ell_idx,
-    const int32_t* __restrict__ row_nnz, const uint8_t* __restrict__ row_ovf, const bf16_t* __restrict__ W,
-    bf16_t* __restrict__ Y, int n_slices, int tpw) {
-  constexpr int EW = VF32 ? 2 : 1;   // words per staged entry
+    int64_t T, int64_t d, int64_t f, int K, const void* __restrict__ ell_val, const float* __restrict__ ell_val2,
+    const uint16_t* __restrict__ ell_idx, const int32_t* __restrict__ row_nnz, const uint8_t* __restrict__ row_ovf,
+    const bf16_t* __restrict__ W, const bf16_t* __restrict__ W2, bf16_t* __restrict__ Y, int n_slices, int tpw) {
+  constexpr int EW = VK + 1;         // words per staged entry
   extern __shared__ uint32_t ent[];  // [tpw][K] entries, then [tpw] counts (-1 = skip)
   int* cnt_s = (int*)(ent + (size_t)tpw * K * EW);
   const int xcd = blockIdx.x & 7;
@@ -233,9 +272,10 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
     const int c = cnt_s[i];
     const int64_t t = t0 + i;
     for (int e = l; e < c; e += 64) {
-      if constexpr (VF32) {
-        ent[2 * (i * K + e)] = (uint32_t)ell_idx[t * K + e];
-        ent[2 * (i * K + e) + 1] = __float_as_uint(((const float*)ell_val)[t * K + e]);
+      if constexpr (VK >= 1) {
+        ent[EW * (i * K + e)] = (uint32_t)ell_idx[t * K + e];
+        ent[EW * (i * K + e) + 1] = __float_as_uint(((const float*)ell_val)[t * K + e]);
+        if constexpr (VK == 2) ent[EW * (i * K + e) + 2] = __float_as_uint(ell_val2[t * K + e]);
       } else {
         ent[i * K + e] = (uint32_t)ell_idx[t * K + e] | ((uint32_t)((const bf16_t*)ell_val)[t * K + e] << 16);
       }
@@ -243,6 +283,8 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
   }
   __syncthreads();
   const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc((void*)W, (short)0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t wr2 =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(VK == 2 ? W2 : W), (short)0, 0x7fffffff, 0x00020000);
   // work items (slice of this XCD, token) in slice-major order, dealt round-robin to the
   // waves: the workgroup walks the slices in order, and a small block (decode) still
   // keeps every wave busy
@@ -256,7 +298,9 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
       const int nnz = __builtin_amdgcn_readfirstlane(cnt_s[i]);
       if (nnz < 0) continue;
       float acc[8];
-      if constexpr (VF32)
+      if constexpr (VK == 2)
+        slice_token_dual(ent + 3 * i * K, nnz, wr, wr2, col_b, grp, acc);
+      else if constexpr (VK == 1)
         slice_token_f32(ent + 2 * i * K, nnz, wr, col_b, grp, acc);
       else
         slice_token(ent + i * K, nnz, wr, col_b, grp, acc);
@@ -487,6 +531,34 @@ __global__ __launch_bounds__(256) void k_sum_parts(int64_t T, int K, const int32
   }
 }
 
+// Gated backward at the ELL entries (eq. sec3:eq:all_other_gradients with eq. l1 on h):
+// dh = sum of the 8 XCD partials of dY . W_down[n] (XCD order) + lambda' sign(h), with
+// h = g u (g = ReLU(gate) > 0 on the pattern, u = x . W_up[:, n]); dh_u = dh g, dh_g = dh u
+// (the ReLU passes it: g > 0); h is kept too (fp32) for dW_down.
+__global__ __launch_bounds__(256) void k_gated_entry_grads(int64_t T, int K, const bf16_t* __restrict__ ell_val,
+                                                           const int32_t* __restrict__ row_nnz,
+                                                           const uint8_t* __restrict__ row_ovf,
+                                                           const float* __restrict__ part, const float* __restrict__ u,
+                                                           float lam, float* __restrict__ dhu, float* __restrict__ dhg,
+                                                           float* __restrict__ h) {
+  const int64_t total = T * (int64_t)K;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+    const int64_t t = i / K;
+    const int e = (int)(i % K);
+    if (row_ovf[t] || e >= row_nnz[t]) continue;
+    float s = 0.f;
+#pragma unroll
+    for (int x = 0; x < 8; ++x) s += part[(int64_t)x * total + i];
+    const float g = bf16_to_f32(ell_val[i]);
+    const float uu = u[i];
+    const float hh = g * uu;
+    const float dh = s + (hh > 0.f ? lam : hh < 0.f ? -lam : 0.f);
+    dhu[i] = dh * g;
+    dhg[i] = dh * uu;
+    h[i] = hh;
+  }
+}
+
 // out[s][n][c] = W[n][SLICE s + c]: 16 bytes per thread, reads coalesced along rows.
 __global__ __launch_bounds__(256) void k_pack_down(const bf16_t* __restrict__ W, bf16_t* __restrict__ out, int64_t f,
                                                    int64_t d) {
@@ -521,27 +593,36 @@ hipError_t launch_gather_down(int val_bf16, int64_t T, int64_t d, int K, const v
 
 hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, const void* ell_val,
                                      const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
-                                     const void* Wp, void* Y, hipStream_t s, int val_f32) {
+                                     const void* Wp, void* Y, hipStream_t s, int val_f32, const float* ell_val2,
+                                     const void* W2p) {
   if (T == 0) return hipSuccess;
   if (d % (8 * SLICE2) != 0) return hipErrorInvalidValue;
   const int n_slices = (int)(d / SLICE2);
+  const int vk = ell_val2 ? 2 : val_f32 ? 1 : 0;
+  if (vk == 2 && (!val_f32 || !W2p)) return hipErrorInvalidValue;
 
-  const int64_t per_tok = (int64_t)std::max(K, 1) * (val_f32 ? 8 : 4) + 4;
+  const int64_t per_tok = (int64_t)std::max(K, 1) * 4 * (vk + 1) + 4;
   const int tpw = slice_walk_tpw(T, per_tok);
   const int64_t blocks = cdiv(T, tpw);
   const size_t lds = (size_t)tpw * per_tok;
   if (lds > 160 * 1024) return hipErrorInvalidValue;
-  const void* kern = val_f32 ? (const void*)k_gather_down_b16<true> : (const void*)k_gather_down_b16<false>;
+  const void* kern = vk == 2   ? (const void*)k_gather_down_b16<2>
+                     : vk == 1 ? (const void*)k_gather_down_b16<1>
+                               : (const void*)k_gather_down_b16<0>;
   if (lds > 65536) {
     const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  if (val_f32)
-    hipLaunchKernelGGL(k_gather_down_b16<true>, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), lds, s, T, d, f,
-                       K, ell_val, ell_idx, row_nnz, row_ovf, (const bf16_t*)Wp, (bf16_t*)Y, n_slices, tpw);
+  const dim3 grid((unsigned)(8 * blocks)), block(GATHER_WAVES * 64);
+  if (vk == 2)
+    hipLaunchKernelGGL(k_gather_down_b16<2>, grid, block, lds, s, T, d, f, K, ell_val, ell_val2, ell_idx, row_nnz,
+                       row_ovf, (const bf16_t*)Wp, (const bf16_t*)W2p, (bf16_t*)Y, n_slices, tpw);
+  else if (vk == 1)
+    hipLaunchKernelGGL(k_gather_down_b16<1>, grid, block, lds, s, T, d, f, K, ell_val, nullptr, ell_idx, row_nnz,
+                       row_ovf, (const bf16_t*)Wp, nullptr, (bf16_t*)Y, n_slices, tpw);
   else
-    hipLaunchKernelGGL(k_gather_down_b16<false>, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), lds, s, T, d,
-                       f, K, ell_val, ell_idx, row_nnz, row_ovf, (const bf16_t*)Wp, (bf16_t*)Y, n_slices, tpw);
+    hipLaunchKernelGGL(k_gather_down_b16<0>, grid, block, lds, s, T, d, f, K, ell_val, nullptr, ell_idx, row_nnz,
+                       row_ovf, (const bf16_t*)Wp, nullptr, (bf16_t*)Y, n_slices, tpw);
   return hipGetLastError();
 }
 
@@ -562,6 +643,16 @@ hipError_t launch_csc_gather(int64_t n_units, int64_t d, int64_t R, const int32_
   }
   hipLaunchKernelGGL(k_csc_gather, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), (size_t)GATHER_LDS, s,
                      n_units, d, R, ptr, tok, val, (const bf16_t*)Gp, out, (int)(d / SLICE2), upw, lds_pairs);
+  return hipGetLastError();
+}
+
+hipError_t launch_gated_entry_grads(int64_t T, int K, const void* ell_val, const int32_t* row_nnz,
+                                    const uint8_t* row_ovf, const float* part, const float* u, float lam, float* dhu,
+                                    float* dhg, float* h, hipStream_t s) {
+  if (T == 0 || K == 0) return hipSuccess;
+  const unsigned grid = (unsigned)std::min<int64_t>(cdiv(T * (int64_t)K, 256), 4096);
+  hipLaunchKernelGGL(k_gated_entry_grads, dim3(grid), dim3(256), 0, s, T, K, (const bf16_t*)ell_val, row_nnz, row_ovf,
+                     part, u, lam, dhu, dhg, h);
   return hipGetLastError();
 }
 

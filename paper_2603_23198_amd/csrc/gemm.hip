@@ -792,6 +792,7 @@ hipError_t gemm_bf16(int alay, int blay, int epi, const GemmParams& p, hipStream
       case EPI_ACT: return launch_kc<EPI_ACT>(p, s);
       case EPI_MASKGRAD: return launch_kc<EPI_MASKGRAD>(p, s);
       case EPI_MUL_ACT: return launch_kc<EPI_MUL_ACT>(p, s);
+      case EPI_ACCUM_F32: return launch_kc<EPI_ACCUM_F32>(p, s);
       default: break;
     }
   }

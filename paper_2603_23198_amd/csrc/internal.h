@@ -93,7 +93,12 @@ hipError_t launch_gather_down(int val_bf16, int64_t T, int64_t d, int ell_width,
 hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int ell_width, const void* ell_val,
                                      const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
                                      const void* W_packed, void* Y, hipStream_t s,
-                                     int val_f32 = 0);
+                                     int val_f32 = 0, const float* ell_val2 = nullptr,
+                                     const void* W2_packed = nullptr);
+// Gated backward at the ELL entries: dh (8 partials + lambda' sign(g u)) -> dh_u, dh_g, h.
+hipError_t launch_gated_entry_grads(int64_t T, int K, const void* ell_val, const int32_t* row_nnz,
+                                    const uint8_t* row_ovf, const float* part, const float* u, float lam, float* dhu,
+                                    float* dhg, float* h, hipStream_t s);
 hipError_t launch_pack_down(const void* W, void* out, int64_t f, int64_t d, hipStream_t s);
 // Gated, two passes over slice-major copies: per-XCD partial up-dots u of every ELL entry
 // (part_u [8][T][K] fp32), then h = g * u (bf16, [T][K]) for the down-projection gather.

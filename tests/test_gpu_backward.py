@@ -178,3 +178,82 @@ def test_backward_c5_sampled():
     Ar = act.tocsr()[rows].toarray()
     dZr = np.where(Ar, dY[rows] @ Wd.T + lamp, 0.0)
     assert rel_l2(to_f64(dX)[rows], dZr @ Wu.T) <= 2e-2
+
+
+# ---- gated block (eq. sec3:eq:all_other_gradients with eq. l1 on h = ReLU(g) h_u) --------
+
+def run_gated_fwd_bwd(w, lam, copies=False):
+    X, Wg, Wu, Wd, dY = dev(w.X), dev(w.W_gate), dev(w.W_up), dev(w.W_down), dev(w.dY)
+    cfg = b.make_cfg(**w.cfg)
+    bufs = b.alloc_twell(w.T, w.f, "bf16", cfg)
+    Y = torch.empty((w.T, w.d), dtype=torch.bfloat16, device="cuda")
+    kw = dict(Y=Y, bufs=bufs, W_gate=Wg, bias_f=dev(w.bias_f), shift_t=dev(w.shift_t))
+    ws = torch.empty(max(1, b.sfl_workspace_size(b.ffn_args(X, Wu, Wd, cfg, **kw))), dtype=torch.uint8, device="cuda")
+    b.sfl_ffn_forward(b.ffn_args(X, Wu, Wd, cfg, **kw, workspace=ws))
+    dX = torch.full((w.T, w.d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    dWg = torch.full((w.d, w.f), float("nan"), dtype=torch.float32, device="cuda")
+    dWu = torch.full((w.d, w.f), float("nan"), dtype=torch.float32, device="cuda")
+    dWd = torch.full((w.f, w.d), float("nan"), dtype=torch.float32, device="cuda")
+    extra = {}
+    if copies:
+        def tr(W):
+            out = torch.empty((W.shape[1], W.shape[0]), dtype=W.dtype, device="cuda")
+            b.sfl_transpose(W, out)
+            return out
+
+        def pk(Wt):
+            out = torch.empty_like(Wt)
+            b.sfl_pack_down_weights(Wt, out)
+            return out
+        extra = dict(W_upT=tr(Wu), W_gateT=tr(Wg), W_down_packed=pk(Wd))
+        extra["W_up_packed"] = pk(extra["W_upT"])
+        extra["W_gate_packed"] = pk(extra["W_gateT"])
+    bkw = dict(W_gate=Wg, dW_gate=dWg, bias_f=dev(w.bias_f), shift_t=dev(w.shift_t), **extra)
+    ba = b.bwd_args(X, Wu, Wd, dY, cfg, bufs, lam, dX, dWu, dWd, **bkw)
+    bws = torch.empty(max(1, b.sfl_workspace_size(ba, 1)), dtype=torch.uint8, device="cuda")
+    b.sfl_ffn_backward(b.bwd_args(X, Wu, Wd, dY, cfg, bufs, lam, dX, dWu, dWd, workspace=bws, **bkw))
+    torch.cuda.synchronize()
+    return dX, dWg, dWu, dWd, bufs, cfg
+
+
+def gated_oracle(w, bufs, cfg, lam):
+    """The fp64 gated gradients on the gate pattern the GPU saved (ELL rows); dense-backup
+    rows keep the fp64 pattern G > 0 (the GPU recomputes them)."""
+    X, Wg, Wu, Wd, dY = (w.as_f64(a) for a in (w.X, w.W_gate, w.W_up, w.W_down, w.dY))
+    G = ffn.preactivation(X, Wg, w.bias_f, w.shift_t)
+    U = X @ Wu
+    got = twell_views(bufs, w.T, w.f, cfg)
+    act = G > 0
+    for t in np.nonzero(got["row_ovf"] == 0)[0]:
+        act[t] = False
+        act[t, got["ell_idx"][t, :int(got["row_nnz"][t])].astype(np.int64)] = True
+    Gm = np.where(act, np.maximum(G, 1e-30), np.minimum(G, 0.0))
+    return ffn.ffn_gated_backward(X, Wg, Wu, Wd, dY, Gm, U, lam), got
+
+
+@pytest.mark.parametrize("T,d,f,K,lam_scale", [(300, 512, 2048, 96, 0.0), (300, 512, 2048, 96, 1e-3),
+                                               (129, 1024, 1024, 48, 1e-3)])
+def test_gated_backward_small_full(T, d, f, K, lam_scale):
+    w = wl.make_ffn("gbwd", "bf16", T, d, f, seed=T + f, gated=True, sparsity=0.97, ell_width=K, with_dy=True)
+    w.shift_t[:3] = 10.0   # dense-backup rows (every gate unit active)
+    lam = lam_scale * T * f
+    dX, dWg, dWu, dWd, bufs, cfg = run_gated_fwd_bwd(w, lam)
+    (rdX, rdWg, rdWu, rdWd), got = gated_oracle(w, bufs, cfg, lam)
+    assert got["row_ovf"][:3].all()
+    for gpu, ref in ((dX, rdX), (dWg, rdWg), (dWu, rdWu), (dWd, rdWd)):
+        assert rel_l2(to_f64(gpu), ref) <= 2e-2
+    assert rel_l2(to_f64(dX)[:3], rdX[:3]) <= 2e-2          # the dense-backup rows
+    sparse = np.nonzero(got["row_ovf"] == 0)[0]
+    assert rel_l2(to_f64(dX)[sparse], rdX[sparse]) <= 2e-2
+
+
+def test_gated_backward_copies_and_determinism():
+    """Identical with caller-provided transposed / slice-major copies, and run to run."""
+    w = wl.make_ffn("gbdet", "bf16", 400, 1024, 2048, seed=31, gated=True, sparsity=0.98, ell_width=96,
+                    with_dy=True)
+    w.shift_t[:2] = 10.0
+    a = run_gated_fwd_bwd(w, 2e-5)
+    for other in (run_gated_fwd_bwd(w, 2e-5, copies=True), run_gated_fwd_bwd(w, 2e-5)):
+        for x, y in zip(a[:4], other[:4]):
+            assert torch.equal(x.view(torch.int16) if x.dtype == torch.bfloat16 else x.view(torch.int32),
+                               y.view(torch.int16) if y.dtype == torch.bfloat16 else y.view(torch.int32))
