@@ -241,21 +241,27 @@ class Bench:
         return rec, s, st
 
     def training_record(self, w, lam):
-        """Forward + backward (sfl_ffn_backward) of the non-gated layer; dense reference timed
-        with torch matmuls (hipBLASLt) of the same shapes for context."""
+        """Forward + backward (sfl_ffn_backward) of the layer, gated or not; the same dense
+        layer through torch matmuls (hipBLASLt) for context."""
         b, t = self.b, self.torch
         s = self.setup_forward(w)
         dY = self.dev(w.dY)
         dX = t.empty((w.T, w.d), dtype=t.bfloat16, device="cuda")
         dWu = t.empty((w.d, w.f), dtype=t.float32, device="cuda")
         dWd = t.empty((w.f, w.d), dtype=t.float32, device="cuda")
+        extra = dict(W_upT=s["WupT"], W_down_packed=s["WdP"], W_up_packed=s["WuP"])
+        if w.gated:
+            dWg = t.empty((w.d, w.f), dtype=t.float32, device="cuda")
+            WgT = s["kw"]["W_gateT"]
+            WgP = t.empty_like(WgT)
+            b.sfl_pack_down_weights(WgT, WgP)
+            extra.update(W_gate=s["kw"]["W_gate"], W_gateT=WgT, W_gate_packed=WgP, dW_gate=dWg,
+                         bias_f=s["kw"]["bias_f"], shift_t=s["kw"]["shift_t"])
         bws = t.empty(max(1, b.sfl_workspace_size(
-            b.bwd_args(s["X"], s["Wu"], s["Wd"], dY, s["cfg"], s["bufs"], lam, dX, dWu, dWd, W_upT=s["WupT"],
-                       W_down_packed=s["WdP"], W_up_packed=s["WuP"]), 1)),
+            b.bwd_args(s["X"], s["Wu"], s["Wd"], dY, s["cfg"], s["bufs"], lam, dX, dWu, dWd, **extra), 1)),
             dtype=t.uint8, device="cuda")
         mkb = lambda ev=None: b.bwd_args(s["X"], s["Wu"], s["Wd"], dY, s["cfg"], s["bufs"], lam, dX, dWu, dWd,
-                                         W_upT=s["WupT"], W_down_packed=s["WdP"], W_up_packed=s["WuP"],
-                                         workspace=bws, events=ev)
+                                         workspace=bws, events=ev, **extra)
         bargs = mkb()
 
         def step():
@@ -267,19 +273,35 @@ class Bench:
         bwd = self.stage_times(lambda ev: mkb(ev), b.sfl_ffn_backward, 6, steps=steps)
         rec = {"workload": w.name, "tokens": w.T, "ms_fwd_bwd": round(ms, 4),
                "tokens_per_s": round(w.T / ms * 1e3, 1), "lambda_l1": lam,
-               "backward_stages_ms": dict(zip(["dz_sddmm", "dx_gather", "pattern_transpose", "dw_gathers",
+               "backward_stages_ms": dict(zip(["dh_at_pattern", "dx_gather", "pattern_transpose", "dw_gathers",
                                                "dense_backup_rows"], bwd))}
-        # dense reference (torch / hipBLASLt): 2 forward GEMMs + 4 backward GEMMs
+        # dense reference (torch / hipBLASLt)
         X, Wu, Wd = s["X"], s["Wu"], s["Wd"]
-        WuT, WdT, XT, dYT = Wu.t().contiguous(), Wd.t().contiguous(), X.t().contiguous(), dY.t().contiguous()
+        WuT, WdT, XT = Wu.t().contiguous(), Wd.t().contiguous(), X.t().contiguous()
+        if w.gated:
+            Wg = s["kw"]["W_gate"]
+            WgTc = Wg.t().contiguous()
 
-        def dense_step():
-            H = t.relu(X @ Wu)
-            _ = H @ Wd
-            dZ = (dY @ WdT) * (H > 0)
-            _ = dZ @ WuT
-            _ = XT @ dZ
-            _ = H.t().contiguous() @ dY
+            def dense_step():
+                G = X @ Wg
+                U = X @ Wu
+                H = t.relu(G) * U
+                _ = H @ Wd
+                dH = dY @ WdT
+                dU = dH * t.relu(G)
+                dG = dH * U * (G > 0)
+                _ = dU @ WuT + dG @ WgTc
+                _ = XT @ dU
+                _ = XT @ dG
+                _ = H.t().contiguous() @ dY
+        else:
+            def dense_step():
+                H = t.relu(X @ Wu)
+                _ = H @ Wd
+                dZ = (dY @ WdT) * (H > 0)
+                _ = dZ @ WuT
+                _ = XT @ dZ
+                _ = H.t().contiguous() @ dY
 
         dms = self.time(dense_step, steps=steps, warmup=2)
         rec["dense_torch_ms_fwd_bwd"] = round(dms, 4)
@@ -406,6 +428,9 @@ def main():
         torch.cuda.empty_cache()
         w5 = wl.c5_training()
         out["training_step"] = B.training_record(w5, 2e-5)
+        del w5
+        torch.cuda.empty_cache()
+        out["gated_training_step"] = B.training_record(wl.gated_training(), 2e-5)
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, a.cpu_seconds)
     print(json.dumps(out), flush=True)

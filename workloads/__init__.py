@@ -143,6 +143,14 @@ def c2_lognormal(seed=0, T=4096, d=2048, f=8192):
                     sparsity_rows=lognormal_row_counts(T, f, seed), tile_rows=32, ell_width=128)
 
 
+def gated_training(seed=0, T=8192, d=4096, f=14336, sparsity=0.995):
+    """Training step of the gated block at the gated forward's shape: dY ~ N(0, 1), dense
+    backup sized to T/8 rows (the paper's choice for its training runs)."""
+    return make_ffn(f"gated train bf16 T={T} d={d} f={f} s={sparsity}", "bf16", T, d, f, seed=seed,
+                    gated=True, sparsity=sparsity, tile_rows=32, ell_width=128, ovf_capacity=T // 8,
+                    with_dy=True)
+
+
 def c3_gated(seed=0, T=8192, d=4096, f=14336, sparsity=0.995):
     return make_ffn(f"gated bf16 T={T} d={d} f={f} s={sparsity}", "bf16", T, d, f, seed=seed,
                     gated=True, sparsity=sparsity, tile_rows=32, ell_width=128)
