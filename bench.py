@@ -46,6 +46,8 @@ def parse():
     p.add_argument("--quick", action="store_true", help="headline workload only")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="first run one plain 256 MiB device copy (reference for HBM byte counters)")
+    p.add_argument("--only", choices=["lognormal", "gated", "decode", "train", "gated_train"],
+                   help="run one secondary workload and print its record (for profiling); no headline line")
     return p.parse_args()
 
 
@@ -329,6 +331,16 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     B = Bench(b, torch, a.steps, a.warmup)
+    if a.only:
+        if a.only in ("train", "gated_train"):
+            wt = wl.c5_training() if a.only == "train" else wl.gated_training()
+            rec = B.training_record(wt, 2e-5)
+        else:
+            wo = {"lognormal": wl.c2_lognormal, "gated": lambda: wl.c3_gated(T=8192),
+                  "decode": lambda: wl.c3_gated(T=32)}[a.only]()
+            rec = B.forward_record(wo)[0]
+        print(json.dumps({"only": a.only, "record": rec}), flush=True)
+        return
     w = wl.c4_sweep(a.sparsity, T=a.tokens)
     T, d, f = w.T, w.d, w.f
     head, s, st = B.forward_record(w)
