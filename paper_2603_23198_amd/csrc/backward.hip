@@ -171,6 +171,7 @@ struct BwdPlan {
   float* u = nullptr;         // gated: [T][K] h_u at the pattern
   float* dhg = nullptr;       // gated: [T][K] dh_g
   float* hf = nullptr;        // gated: [T][K] h = h_g h_u
+  float* dxf = nullptr;       // gated: [T][d] fp32 dX accumulator of the sparse rows
   int32_t* bc = nullptr;      // [nb][f]
   int32_t* col_cnt = nullptr; // [f]
   int32_t* col_ptr = nullptr; // [f + 1]
@@ -216,6 +217,7 @@ BwdPlan plan_backward(const sfl_ffn_bwd_args_t& a, void* ws) {
     p.u = (float*)take((size_t)T * K * 4);
     p.dhg = (float*)take((size_t)T * K * 4);
     p.hf = (float*)take((size_t)T * K * 4);
+    p.dxf = (float*)take((size_t)T * d * 4);
   }
   p.bc = (int32_t*)take((size_t)nb * f * 4);
   p.col_cnt = (int32_t*)take((size_t)f * 4);
@@ -358,12 +360,16 @@ sfl_status_t backward_run(const sfl_ffn_bwd_args_t* a, hipStream_t s) {
     SFL_HIPB(launch_gated_entry_grads(T, K, ev, sv.row_nnz, sv.row_ovf, p.part, p.u, lam, p.dz, p.dhg, p.hf, s));
   }
   rec(1);
-  // 2. dX of the sparse rows (gated: dh_u W_up^T + dh_g W_gate^T in one pass)
-  if (!gated)
+  // 2. dX of the sparse rows (gated: dh_u W_up^T into an fp32 accumulator, then
+  //    + dh_g W_gate^T; one slice-major matrix per pass keeps one slice per XCD in L2)
+  if (!gated) {
     SFL_HIPB(launch_gather_down_packed(T, d, f, K, p.dz, sv.ell_idx, sv.row_nnz, sv.row_ovf, WuP, a->dX, s, 1));
-  else
-    SFL_HIPB(launch_gather_down_packed(T, d, f, K, p.dz, sv.ell_idx, sv.row_nnz, sv.row_ovf, WuP, a->dX, s, 1, p.dhg,
-                                       WgP));
+  } else {
+    SFL_HIPB(launch_gather_down_packed(T, d, f, K, p.dz, sv.ell_idx, sv.row_nnz, sv.row_ovf, WuP, nullptr, s, 1, 1,
+                                       p.dxf));
+    SFL_HIPB(launch_gather_down_packed(T, d, f, K, p.dhg, sv.ell_idx, sv.row_nnz, sv.row_ovf, WgP, a->dX, s, 1, 2,
+                                       p.dxf));
+  }
   rec(2);
   // 3. transposed pattern, with each entry's values
   hipLaunchKernelGGL(k_blk_count, dim3((unsigned)nb), dim3(256), 0, s, T, K, f, sv.ell_idx, sv.row_nnz, sv.row_ovf,

@@ -209,51 +209,14 @@ __device__ __forceinline__ void slice_token_f32(const uint32_t* er, int nnz, __a
     for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], o, 64);
 }
 
-// Two fp32 values per entry against two slice-major matrices (the gated backward's
-// dX = dh_u W_up^T + dh_g W_gate^T): entries are (index, v1 bits, v2 bits) word triples.
-__device__ __forceinline__ void slice_token_dual(const uint32_t* er, int nnz, __amdgpu_buffer_rsrc_t wr,
-                                                 __amdgpu_buffer_rsrc_t wr2, uint32_t col_b, int grp, float (&acc)[8]) {
-  constexpr uint32_t row_b = SLICE2 * 2;
-  constexpr int GD = GU / 2;  // two loads per entry
-#pragma unroll
-  for (int j = 0; j < 8; ++j) acc[j] = 0.f;
-  for (int q = 0; q < nnz; q += NGRP * GD) {
-    u32x4_t w[GD], w2[GD];
-    float v[GD], v2[GD];
-#pragma unroll
-    for (int u = 0; u < GD; ++u) {
-      const int e = q + u * NGRP + grp;
-      const bool ok = e < nnz;
-      v[u] = ok ? __uint_as_float(er[3 * e + 1]) : 0.f;
-      v2[u] = ok ? __uint_as_float(er[3 * e + 2]) : 0.f;
-      const uint32_t off = ok ? er[3 * e] * row_b + col_b : 0x80000000u;
-      w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0));
-      w2[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr2, (int)off, 0, 0));
-    }
-#pragma unroll
-    for (int u = 0; u < GD; ++u)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint32_t ww = w[u][j], ww2 = w2[u][j];
-        acc[2 * j] = fmaf(v[u], bf16lo(ww), acc[2 * j]);
-        acc[2 * j + 1] = fmaf(v[u], bf16hi(ww), acc[2 * j + 1]);
-        acc[2 * j] = fmaf(v2[u], bf16lo(ww2), acc[2 * j]);
-        acc[2 * j + 1] = fmaf(v2[u], bf16hi(ww2), acc[2 * j + 1]);
-      }
-  }
-#pragma unroll
-  for (int o = LPR; o < 64; o <<= 1)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], o, 64);
-}
-
 // VK: kind of the ELL values. 0: bf16 (packed with the index in one word); 1: fp32 (the
-// backward's dz, two words per entry); 2: two fp32 values against W and W2 (three words).
-template <int VK>
+// backward's dz, two words per entry). OUT: 0: bf16 Y; 1: fp32 Yf; 2: bf16 Y of the sum
+// with the fp32 addend Yf (the second of two passes that share an accumulator).
+template <int VK, int OUT>
 __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
-    int64_t T, int64_t d, int64_t f, int K, const void* __restrict__ ell_val, const float* __restrict__ ell_val2,
-    const uint16_t* __restrict__ ell_idx, const int32_t* __restrict__ row_nnz, const uint8_t* __restrict__ row_ovf,
-    const bf16_t* __restrict__ W, const bf16_t* __restrict__ W2, bf16_t* __restrict__ Y, int n_slices, int tpw) {
+    int64_t T, int64_t d, int64_t f, int K, const void* __restrict__ ell_val, const uint16_t* __restrict__ ell_idx,
+    const int32_t* __restrict__ row_nnz, const uint8_t* __restrict__ row_ovf, const bf16_t* __restrict__ W,
+    bf16_t* __restrict__ Y, float* __restrict__ Yf, int n_slices, int tpw) {
   constexpr int EW = VK + 1;         // words per staged entry
   extern __shared__ uint32_t ent[];  // [tpw][K] entries, then [tpw] counts (-1 = skip)
   int* cnt_s = (int*)(ent + (size_t)tpw * K * EW);
@@ -275,7 +238,6 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
       if constexpr (VK >= 1) {
         ent[EW * (i * K + e)] = (uint32_t)ell_idx[t * K + e];
         ent[EW * (i * K + e) + 1] = __float_as_uint(((const float*)ell_val)[t * K + e]);
-        if constexpr (VK == 2) ent[EW * (i * K + e) + 2] = __float_as_uint(ell_val2[t * K + e]);
       } else {
         ent[i * K + e] = (uint32_t)ell_idx[t * K + e] | ((uint32_t)((const bf16_t*)ell_val)[t * K + e] << 16);
       }
@@ -283,8 +245,6 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
   }
   __syncthreads();
   const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc((void*)W, (short)0, 0x7fffffff, 0x00020000);
-  const __amdgpu_buffer_rsrc_t wr2 =
-      __builtin_amdgcn_make_buffer_rsrc((void*)(VK == 2 ? W2 : W), (short)0, 0x7fffffff, 0x00020000);
   // work items (slice of this XCD, token) in slice-major order, dealt round-robin to the
   // waves: the workgroup walks the slices in order, and a small block (decode) still
   // keeps every wave busy
@@ -298,18 +258,30 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
       const int nnz = __builtin_amdgcn_readfirstlane(cnt_s[i]);
       if (nnz < 0) continue;
       float acc[8];
-      if constexpr (VK == 2)
-        slice_token_dual(ent + 3 * i * K, nnz, wr, wr2, col_b, grp, acc);
-      else if constexpr (VK == 1)
+      if constexpr (VK == 1)
         slice_token_f32(ent + 2 * i * K, nnz, wr, col_b, grp, acc);
       else
         slice_token(ent + i * K, nnz, wr, col_b, grp, acc);
       if (grp == 0) {
-        u32x4_t out;
+        const int64_t o = (t0 + i) * d + col;
+        if constexpr (OUT == 1) {
+          *(f32x4_t*)(Yf + o) = f32x4_t{acc[0], acc[1], acc[2], acc[3]};
+          *(f32x4_t*)(Yf + o + 4) = f32x4_t{acc[4], acc[5], acc[6], acc[7]};
+        } else {
+          if constexpr (OUT == 2) {
+            const f32x4_t a0 = *(const f32x4_t*)(Yf + o), a1 = *(const f32x4_t*)(Yf + o + 4);
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          out[j] = (uint32_t)f32_to_bf16(acc[2 * j]) | ((uint32_t)f32_to_bf16(acc[2 * j + 1]) << 16);
-        *(u32x4_t*)(Y + (t0 + i) * d + col) = out;
+            for (int j = 0; j < 4; ++j) {
+              acc[j] = a0[j] + acc[j];
+              acc[4 + j] = a1[j] + acc[4 + j];
+            }
+          }
+          u32x4_t out;
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            out[j] = (uint32_t)f32_to_bf16(acc[2 * j]) | ((uint32_t)f32_to_bf16(acc[2 * j + 1]) << 16);
+          *(u32x4_t*)(Y + o) = out;
+        }
       }
     }
   }
@@ -593,36 +565,35 @@ hipError_t launch_gather_down(int val_bf16, int64_t T, int64_t d, int K, const v
 
 hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, const void* ell_val,
                                      const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
-                                     const void* Wp, void* Y, hipStream_t s, int val_f32, const float* ell_val2,
-                                     const void* W2p) {
+                                     const void* Wp, void* Y, hipStream_t s, int val_f32, int out_mode, float* Yf) {
   if (T == 0) return hipSuccess;
   if (d % (8 * SLICE2) != 0) return hipErrorInvalidValue;
+  if (out_mode < 0 || out_mode > 2 || (out_mode > 0 && !Yf) || (out_mode != 1 && !Y)) return hipErrorInvalidValue;
   const int n_slices = (int)(d / SLICE2);
-  const int vk = ell_val2 ? 2 : val_f32 ? 1 : 0;
-  if (vk == 2 && (!val_f32 || !W2p)) return hipErrorInvalidValue;
+  const int vk = val_f32 ? 1 : 0;
 
   const int64_t per_tok = (int64_t)std::max(K, 1) * 4 * (vk + 1) + 4;
   const int tpw = slice_walk_tpw(T, per_tok);
   const int64_t blocks = cdiv(T, tpw);
   const size_t lds = (size_t)tpw * per_tok;
   if (lds > 160 * 1024) return hipErrorInvalidValue;
-  const void* kern = vk == 2   ? (const void*)k_gather_down_b16<2>
-                     : vk == 1 ? (const void*)k_gather_down_b16<1>
-                               : (const void*)k_gather_down_b16<0>;
-  if (lds > 65536) {
-    const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-  }
   const dim3 grid((unsigned)(8 * blocks)), block(GATHER_WAVES * 64);
-  if (vk == 2)
-    hipLaunchKernelGGL(k_gather_down_b16<2>, grid, block, lds, s, T, d, f, K, ell_val, ell_val2, ell_idx, row_nnz,
-                       row_ovf, (const bf16_t*)Wp, (const bf16_t*)W2p, (bf16_t*)Y, n_slices, tpw);
-  else if (vk == 1)
-    hipLaunchKernelGGL(k_gather_down_b16<1>, grid, block, lds, s, T, d, f, K, ell_val, nullptr, ell_idx, row_nnz,
-                       row_ovf, (const bf16_t*)Wp, nullptr, (bf16_t*)Y, n_slices, tpw);
-  else
-    hipLaunchKernelGGL(k_gather_down_b16<0>, grid, block, lds, s, T, d, f, K, ell_val, nullptr, ell_idx, row_nnz,
-                       row_ovf, (const bf16_t*)Wp, nullptr, (bf16_t*)Y, n_slices, tpw);
+#define SFL_GATHER_LAUNCH(VK_, OUT_)                                                                               \
+  do {                                                                                                             \
+    if (lds > 65536) {                                                                                             \
+      const hipError_t e = hipFuncSetAttribute((const void*)k_gather_down_b16<VK_, OUT_>,                          \
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);              \
+      if (e != hipSuccess) return e;                                                                               \
+    }                                                                                                              \
+    hipLaunchKernelGGL((k_gather_down_b16<VK_, OUT_>), grid, block, lds, s, T, d, f, K, ell_val, ell_idx, row_nnz, \
+                       row_ovf, (const bf16_t*)Wp, (bf16_t*)Y, Yf, n_slices, tpw);                                 \
+  } while (0)
+  if (vk == 0 && out_mode == 0) SFL_GATHER_LAUNCH(0, 0);
+  else if (vk == 1 && out_mode == 0) SFL_GATHER_LAUNCH(1, 0);
+  else if (vk == 1 && out_mode == 1) SFL_GATHER_LAUNCH(1, 1);
+  else if (vk == 1 && out_mode == 2) SFL_GATHER_LAUNCH(1, 2);
+  else return hipErrorInvalidValue;
+#undef SFL_GATHER_LAUNCH
   return hipGetLastError();
 }
 

@@ -90,11 +90,11 @@ hipError_t launch_gather_down(int val_bf16, int64_t T, int64_t d, int ell_width,
                               const uint16_t* ell_idx, const int32_t* row_nnz,
                               const uint8_t* row_ovf, const void* W, void* Y, hipStream_t s);
 // bf16, d % 512 == 0: same sum from the slice-major copy of W_down (persistent, XCD-aware).
+// out_mode 0: bf16 Y; 1: fp32 Yf; 2: bf16 Y of (sum + Yf) (val_f32 only for 1 and 2).
 hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int ell_width, const void* ell_val,
                                      const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
                                      const void* W_packed, void* Y, hipStream_t s,
-                                     int val_f32 = 0, const float* ell_val2 = nullptr,
-                                     const void* W2_packed = nullptr);
+                                     int val_f32 = 0, int out_mode = 0, float* Yf = nullptr);
 // Gated backward at the ELL entries: dh (8 partials + lambda' sign(g u)) -> dh_u, dh_g, h.
 hipError_t launch_gated_entry_grads(int64_t T, int K, const void* ell_val, const int32_t* row_nnz,
                                     const uint8_t* row_ovf, const float* part, const float* u, float lam, float* dhu,

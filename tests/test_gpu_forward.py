@@ -321,3 +321,33 @@ def test_transposed_gate_and_down_copies(gated):
         if not dense:
             assert b.read_stats(st1)["n_ovf_rows"] >= 40
             check_pattern(twell_views(b1, w.T, w.f, cfg), Zref, rows, w.f, cfg.tile_cols, cfg.tile_slots)
+
+
+def test_decode_forward_replays_from_a_hip_graph():
+    """The decode-shaped gated forward captured in a HIP graph: every replay, with eager
+    work and synchronisations between replays, equals the eager call bit for bit."""
+    w = wl.c3_gated(T=32, d=1024, f=4096)
+    X, Wu, Wd, Wg = dev(w.X), dev(w.W_up), dev(w.W_down), dev(w.W_gate)
+    cfg = b.make_cfg(**w.cfg)
+    bufs = b.alloc_twell(w.T, w.f, "bf16", cfg)
+    Y = torch.zeros((w.T, w.d), dtype=torch.bfloat16, device="cuda")
+    kw = dict(Y=Y, bufs=bufs, W_gate=Wg, W_upT=transposed(Wu), W_gateT=transposed(Wg), W_downT=transposed(Wd),
+              shift_t=dev(w.shift_t))
+    ws = torch.empty(max(1, b.sfl_workspace_size(b.ffn_args(X, Wu, Wd, cfg, **kw))), dtype=torch.uint8, device="cuda")
+    args = b.ffn_args(X, Wu, Wd, cfg, **kw, workspace=ws)
+    b.sfl_ffn_forward(args)
+    torch.cuda.synchronize()
+    Yeager = Y.clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        b.sfl_ffn_forward(args, torch.cuda.current_stream())
+    for i in range(3):
+        Y.fill_(float("nan"))
+        bufs["row_nnz"].fill_(-1)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(Y.view(torch.int16), Yeager.view(torch.int16)), i
+        _ = (X.float() @ X.float().t()).sum().item()  # unrelated eager work between replays
+    Yref, _ = oracle_rows(w, np.arange(w.T))
+    assert rel_l2(to_f64(Y), Yref) <= 2e-2
