@@ -257,3 +257,66 @@ def test_gated_backward_copies_and_determinism():
         for x, y in zip(a[:4], other[:4]):
             assert torch.equal(x.view(torch.int16) if x.dtype == torch.bfloat16 else x.view(torch.int32),
                                y.view(torch.int16) if y.dtype == torch.bfloat16 else y.view(torch.int32))
+
+
+def test_backward_c5_bench_configuration_is_identical():
+    """bench.py passes W_up^T and slice-major W_down / W_up^T to the backward at the training
+    shape; the gradients equal those of the copy-free call (sampled-oracle checked above)."""
+    w = wl.c5_training()
+    a = run_fwd_bwd(w, 2e-5)
+    c = run_fwd_bwd(w, 2e-5, with_wupt=True, with_packed=True)
+    for x, y in zip(a[:3], c[:3]):
+        assert torch.equal(x.view(torch.int16) if x.dtype == torch.bfloat16 else x.view(torch.int32),
+                           y.view(torch.int16) if y.dtype == torch.bfloat16 else y.view(torch.int32))
+
+
+def test_gated_training_bench_configuration_sampled():
+    """The gated training step as bench.py runs it (T=8192, d=4096, f=14336, dense backup of
+    T/8 rows, all weight copies): sampled units of dW_gate, dW_up, dW_down and sampled rows
+    of dX against the fp64 oracle on the GPU's saved pattern."""
+    w = wl.gated_training()
+    w.shift_t[:4] = 10.0  # a few dense-backup rows
+    lam = 1e-3 * w.T * w.f
+    dX, dWg, dWu, dWd, bufs, cfg = run_gated_fwd_bwd(w, lam, copies=True)
+    got = twell_views(bufs, w.T, w.f, cfg)
+    assert got["row_ovf"][:4].all()
+    X, Wg, Wu, Wd, dY = (w.as_f64(a) for a in (w.X, w.W_gate, w.W_up, w.W_down, w.dY))
+    lamp = lam / (w.T * w.f)
+    sparse_rows = np.nonzero(got["row_ovf"] == 0)[0]
+
+    def pattern(rows_sel, cols, G):
+        """GPU pattern on ELL rows, fp64 G > 0 on dense-backup rows, for [rows_sel][cols]."""
+        act = G > 0
+        colpos = {int(c): j for j, c in enumerate(cols)}
+        for i, t in enumerate(rows_sel):
+            if got["row_ovf"][t]:
+                continue
+            act[i] = False
+            for n in got["ell_idx"][t, :int(got["row_nnz"][t])]:
+                j = colpos.get(int(n))
+                if j is not None:
+                    act[i, j] = True
+        return act
+
+    r = np.random.default_rng(5)
+    units = r.choice(w.f, size=32, replace=False)
+    allrows = np.arange(w.T)
+    G = X @ Wg[:, units] + w.shift_t[:, None]
+    U = X @ Wu[:, units]
+    A = pattern(allrows, units, G)
+    hg = np.where(A, np.maximum(G, 1e-30), 0.0)
+    h = hg * U
+    dh = dY @ Wd[units].T + lamp * np.sign(h)
+    dhu, dG = dh * hg, np.where(A, dh * U, 0.0)
+    assert rel_l2(to_f64(dWd)[units], h.T @ dY) <= 2e-2
+    assert rel_l2(to_f64(dWu)[:, units], X.T @ dhu) <= 2e-2
+    assert rel_l2(to_f64(dWg)[:, units], X.T @ dG) <= 2e-2
+    rows = np.concatenate([r.choice(sparse_rows, size=24, replace=False), np.arange(4)])
+    Gr = X[rows] @ Wg + w.shift_t[rows, None]
+    Ur = X[rows] @ Wu
+    Ar = pattern(rows, np.arange(w.f), Gr)
+    hgr = np.where(Ar, np.maximum(Gr, 1e-30), 0.0)
+    hr = hgr * Ur
+    dhr = dY[rows] @ Wd.T + lamp * np.sign(hr)
+    dXr = (dhr * hgr) @ Wu.T + np.where(Ar, dhr * Ur, 0.0) @ Wg.T
+    assert rel_l2(to_f64(dX)[rows], dXr) <= 2e-2

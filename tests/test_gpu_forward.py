@@ -351,3 +351,32 @@ def test_decode_forward_replays_from_a_hip_graph():
         _ = (X.float() @ X.float().t()).sum().item()  # unrelated eager work between replays
     Yref, _ = oracle_rows(w, np.arange(w.T))
     assert rel_l2(to_f64(Y), Yref) <= 2e-2
+
+
+def test_c4_headline_in_the_bench_configuration():
+    """The headline workload as bench.py launches it: W_up^T and W_down^T copies, slice-major
+    W_down; sampled rows and their patterns against the oracle, and the dense baseline."""
+    w = wl.c4_sweep(0.99)
+    Y, bufs, stats, cfg = run_forward(w, use_wupt=True, use_wdownt=True, packed_down=True)
+    got = twell_views(bufs, w.T, w.f, cfg)
+    rows = sample_rows(w.T, 128, 21, extra=np.nonzero(got["row_ovf"])[0][:16])
+    Yref, Z = oracle_rows(w, rows)
+    assert rel_l2(to_f64(Y)[rows], Yref) <= 2e-2
+    check_pattern(got, Z, rows[:48], w.f, cfg.tile_cols, cfg.tile_slots)
+    Yd, _, _, _ = run_forward(w, dense=True, use_wupt=True, use_wdownt=True)
+    assert rel_l2(to_f64(Yd)[rows], Yref) <= 2e-2
+
+
+def test_c3_gated_in_the_bench_configuration():
+    """The gated prefill workload as bench.py launches it (transposed and slice-major copies
+    of all weights); sampled rows against the oracle, and the dense baseline."""
+    w = wl.c3_gated()
+    Y, bufs, stats, cfg = run_forward(w, use_wupt=True, use_wgatet=True, use_wdownt=True, packed_down=True,
+                                      packed_up=True)
+    got = twell_views(bufs, w.T, w.f, cfg)
+    rows = sample_rows(w.T, 128, 22, extra=np.nonzero(got["row_ovf"])[0][:16])
+    Yref, G = oracle_rows(w, rows)
+    assert rel_l2(to_f64(Y)[rows], Yref) <= 2e-2
+    check_pattern(got, G, rows[:48], w.f, cfg.tile_cols, cfg.tile_slots)
+    Yd, _, _, _ = run_forward(w, dense=True, use_wupt=True, use_wgatet=True, use_wdownt=True)
+    assert rel_l2(to_f64(Yd)[rows], Yref) <= 2e-2
