@@ -112,3 +112,42 @@ def test_forward_validates_before_launch():
     with pytest.raises(b.SflError) as e:   # workspace needed for the dense-backup rows
         b.sfl_ffn_forward(a, stream=0)
     assert e.value.code == b.SFL_E_WORKSPACE
+
+
+def _fake_bwd(T, d, f, gated=False, **kw):
+    a = b.BwdArgs()
+    a.dtype = b.SFL_BF16
+    a.gated = 1 if gated else 0
+    a.T, a.d, a.f = T, d, f
+    a.X = a.W_up = a.W_down = a.dY = a.dX = a.dW_up = a.dW_down = 0x1000
+    if gated:
+        a.W_gate = a.dW_gate = 0x1000
+    a.cfg = b.make_cfg(**kw)
+    for n in b.BUF_NAMES:
+        setattr(a.saved, n, 0x3000)
+    return a
+
+
+def test_backward_workspace_and_validation():
+    a = _fake_bwd(256, 512, 1024, ell_width=64)
+    ws = b.sfl_workspace_size(a, 1)
+    g = _fake_bwd(256, 512, 1024, gated=True, ell_width=64)
+    wsg = b.sfl_workspace_size(g, 1)
+    assert wsg > ws > 0  # the gated pass keeps more per-entry and per-row state
+    # caller-provided slice-major copies shrink the workspace by one weight each, and the
+    # transposed W_up that the packed W_up^T would be built from
+    a.W_down_packed = a.W_up_packed = 0x4000
+    assert b.sfl_workspace_size(a, 1) == ws - 3 * 512 * 1024 * 2
+    g.dW_gate = None  # gated needs dW_gate
+    with pytest.raises(b.SflError) as e:
+        b.sfl_workspace_size(g, 1)
+    assert e.value.code == b.SFL_E_ARG
+    u = _fake_bwd(256, 640, 1024, ell_width=64)  # d % 512 != 0
+    with pytest.raises(b.SflError) as e:
+        b.sfl_workspace_size(u, 1)
+    assert e.value.code == b.SFL_E_UNSUPPORTED
+    ng = _fake_bwd(256, 512, 1024, ell_width=64)
+    ng.saved.ovf_dense = None  # the non-gated backward reads the saved dense-backup rows
+    with pytest.raises(b.SflError) as e:
+        b.sfl_workspace_size(ng, 1)
+    assert e.value.code == b.SFL_E_ARG
