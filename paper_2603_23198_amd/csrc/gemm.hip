@@ -491,9 +491,20 @@ __device__ __forceinline__ void load_lds16(u32x4_t rsrc, uint32_t lds_off, uint3
 
 // One output tile (tm, tn) over K steps [kt0, kt1); SPLIT with ks > 1 stores the fp32
 // partial sums of split `split`, otherwise the epilogue runs. Called by every thread.
-template <int EPI, int Tn, bool SPLIT>
+// Row-contiguous B ([K][N], e.g. W_up [d][f] as the B of X W_up): a stage holds
+// [64 k][256 n], 512 bytes per k row; the 32-byte segment s (16 n) of row r is stored at
+// segment position s ^ (r & 7). gfx950's transposing LDS read (ds_read_b64_tr_b16) then
+// hands each lane the 4 consecutive k of one n that the MFMA operand wants: in a group of
+// 16 lanes, lane q reads k row q/4 at n offset 4 (q%4), and lane i receives n offset i of
+// the 4 rows. The segment swizzle spreads those 4 rows over distinct banks.
+__device__ __forceinline__ int rc_seg(int row, int seg) { return seg ^ (row & 7); }
+typedef short short4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+
+template <int EPI, int Tn, bool SPLIT, int BL>
 __device__ __forceinline__ void kc_tile(const GemmParams& p, int tm, int tn, int split, int ks, int m_eff,
                                         bf16_t* smem) {
+  static_assert(BL == LAY_KC || BL == LAY_RC, "B layout");
   typedef WaveTile<KC_WM, KC_WN, KC_FM> W;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -514,21 +525,31 @@ __device__ __forceinline__ void kc_tile(const GemmParams& p, int tm, int tn, int
   for (int q = 0; q < KC_LOADS; ++q) {
     const int row = (wave * KC_LOADS + q) * 8 + (lane >> 3);
     const int c = kc_swz(row, lane & 7);
-    const int ga = m0 + row, gb = n0 + row;
+    const int ga = m0 + row;
     const int64_t sa = ga < m_eff ? (p.a_rows ? (int64_t)p.a_rows[ga] : (int64_t)ga) : -1;
     offa[q] = sa >= 0 ? (uint32_t)((sa * p.lda + c * 8) * 2) : kOOB;
-    offb[q] = gb < p.N ? (uint32_t)(((int64_t)gb * p.ldb + c * 8) * 2) : kOOB;
+    if constexpr (BL == LAY_KC) {
+      const int gb = n0 + row;
+      offb[q] = gb < p.N ? (uint32_t)(((int64_t)gb * p.ldb + c * 8) * 2) : kOOB;
+    } else {
+      // k row kr of the stage, 16-byte chunk position lane%32 holding logical chunk cb
+      const int kr = (wave * KC_LOADS + q) * 2 + (lane >> 5);
+      const int cb = 2 * rc_seg(kr, (lane & 31) >> 1) + (lane & 1);
+      const int gn = n0 + cb * 8;
+      offb[q] = gn < p.N ? (uint32_t)(((int64_t)kr * p.ldb + gn) * 2) : kOOB;
+    }
   }
   auto issue = [&](int kt) {
     bf16_t* st = smem + (kt & 1) * KC_STAGE;
-    const int so = kt * KC_BK * 2;
+    const uint32_t soa = (uint32_t)(kt * KC_BK * 2);
+    const uint32_t sob = BL == LAY_KC ? soa : (uint32_t)((int64_t)kt * KC_BK * p.ldb * 2);
 #pragma unroll
     for (int q = 0; q < KC_LOADS; ++q) {
-      bf16_t* da = st + (wave * KC_LOADS + q) * 8 * KC_BK;
+      bf16_t* da = st + (wave * KC_LOADS + q) * 8 * KC_BK;  // 1 KB per load instruction
       const uint32_t la = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16_t*)da;
       const uint32_t lb = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16_t*)(da + KC_OPER);
-      load_lds16(ra, __builtin_amdgcn_readfirstlane(la), offa[q], (uint32_t)so);
-      load_lds16(rb, __builtin_amdgcn_readfirstlane(lb), offb[q], (uint32_t)so);
+      load_lds16(ra, __builtin_amdgcn_readfirstlane(la), offa[q], soa);
+      load_lds16(rb, __builtin_amdgcn_readfirstlane(lb), offb[q], sob);
     }
   };
 
@@ -555,10 +576,28 @@ __device__ __forceinline__ void kc_tile(const GemmParams& p, int tm, int tn, int
         const int r = arow + i * 16;
         a[i] = *(const bf16x8_t*)(As + r * KC_BK + kc_swz(r, c) * 8);
       }
+      if constexpr (BL == LAY_KC) {
 #pragma unroll
-      for (int j = 0; j < W::TN_; ++j) {
-        const int r = brow + j * 16;
-        b[j] = *(const bf16x8_t*)(Bs + r * KC_BK + kc_swz(r, c) * 8);
+        for (int j = 0; j < W::TN_; ++j) {
+          const int r = brow + j * 16;
+          b[j] = *(const bf16x8_t*)(Bs + r * KC_BK + kc_swz(r, c) * 8);
+        }
+      } else {
+        const int q = lane & 15;
+#pragma unroll
+        for (int j = 0; j < W::TN_; ++j) {
+          const int nb = wn * W::WTN_ + j * 16;  // first n of the fragment (tile-local)
+          short4_t h[2];
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const int kr = ks * 32 + (lane >> 4) * 8 + hh * 4 + (q >> 2);
+            const int pos = kr * BN + rc_seg(kr, nb >> 4) * 16 + 4 * (q & 3);
+            h[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) short4_t*)(__attribute__((address_space(3))) bf16_t*)(Bs + pos));
+          }
+          const bf16x4_t lo = __builtin_bit_cast(bf16x4_t, h[0]), hi = __builtin_bit_cast(bf16x4_t, h[1]);
+          b[j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        }
       }
       __builtin_amdgcn_s_setprio(1);
 #pragma unroll
@@ -601,7 +640,7 @@ __device__ __forceinline__ void kc_tile(const GemmParams& p, int tm, int tn, int
   gemm_epilogue<EPI, KC_WM, KC_WN, KC_FM, Tn>(p, acc, m0, n0, m_eff, smem);
 }
 
-template <int EPI, int Tn>
+template <int EPI, int Tn, int BL>
 __global__ __launch_bounds__(NTHR) void k_gemm_kc(GemmParams p) {
   __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * KC_STAGE];
   const int tiles_m = (int)cdiv(p.M, BM), tiles_n = (int)cdiv(p.N, BN);
@@ -609,12 +648,12 @@ __global__ __launch_bounds__(NTHR) void k_gemm_kc(GemmParams p) {
   tile_coords(tiles_m, tiles_n, tm, tn);
   const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
   if (tm * BM >= m_eff) return;
-  kc_tile<EPI, Tn, false>(p, tm, tn, 0, 1, m_eff, smem);
+  kc_tile<EPI, Tn, false, BL>(p, tm, tn, 0, 1, m_eff, smem);
 }
 
 // Split-K GEMM: persistent blocks over the (tile, split) items of the counted rows, so
 // the grid does not scale with a row capacity that the count may leave mostly empty.
-template <int EPI>
+template <int EPI, int BL>
 __global__ __launch_bounds__(NTHR) void k_gemm_kc_split(GemmParams p) {
   __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * KC_STAGE];
   const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
@@ -623,7 +662,7 @@ __global__ __launch_bounds__(NTHR) void k_gemm_kc_split(GemmParams p) {
   const int n_items = (int)cdiv(m_eff, BM) * tiles_n * ks;
   for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
     const int split = item % ks, t = item / ks;
-    kc_tile<EPI, 0, true>(p, t / tiles_n, t % tiles_n, split, ks, m_eff, smem);
+    kc_tile<EPI, 0, true, BL>(p, t / tiles_n, t % tiles_n, split, ks, m_eff, smem);
     __syncthreads();  // the next item refills the stage buffers
   }
 }
@@ -667,22 +706,22 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(GemmParams p) {
   }
 }
 
-template <int EPI, int Tn = 0>
+template <int EPI, int Tn = 0, int BL = LAY_KC>
 hipError_t launch_kc(const GemmParams& p, hipStream_t s) {
   const int tiles = (int)(cdiv(p.M, BM) * cdiv(p.N, BN));
   if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL((k_gemm_kc<EPI, Tn>), dim3(tiles), dim3(NTHR), 0, s, p);
+  hipLaunchKernelGGL((k_gemm_kc<EPI, Tn, BL>), dim3(tiles), dim3(NTHR), 0, s, p);
   return hipGetLastError();
 }
 
 // Split-K launch: the GEMM over (tile, split) blocks, then the partial-sum reduction. The
 // split count is decided on the device from the row count, identically in both kernels.
-template <int EPI>
+template <int EPI, int BL = LAY_KC>
 hipError_t launch_kc_split(const GemmParams& p, hipStream_t s) {
   const int64_t tiles = cdiv(p.M, BM) * cdiv(p.N, BN);
   if (tiles == 0) return hipSuccess;
   const unsigned grid = (unsigned)std::min<int64_t>(tiles * p.ksplit, 512);  // about two blocks per CU
-  hipLaunchKernelGGL((k_gemm_kc_split<EPI>), dim3(grid), dim3(NTHR), 0, s, p);
+  hipLaunchKernelGGL((k_gemm_kc_split<EPI, BL>), dim3(grid), dim3(NTHR), 0, s, p);
   hipLaunchKernelGGL((k_splitk_reduce<EPI>), dim3(1024), dim3(256), 0, s, p);
   return hipGetLastError();
 }
@@ -694,14 +733,22 @@ hipError_t launch_bf16(const GemmParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
+// The direct-to-LDS kernel takes A K-contiguous (rows optionally gathered) and B either
+// K-contiguous or row-contiguous, with K a multiple of 64 and no device-side K bound;
+// row-contiguous B also needs N % 8 == 0 (16-byte chunks along N).
+bool kc_ok(const GemmParams& p, int blay) {
+  return p.K % KC_BK == 0 && !p.k_count && !p.b_rows && (blay == LAY_KC || (blay == LAY_RC && p.N % 8 == 0));
+}
+
 // TwELL epilogue with the tile width as a compile-time constant
 template <int ALAY, int BLAY>
 hipError_t launch_twell(const GemmParams& p, hipStream_t s) {
-  const bool kc = ALAY == LAY_KC && BLAY == LAY_KC && p.K % KC_BK == 0 && !p.k_count && !p.b_rows;
+  const bool kc = ALAY == LAY_KC && kc_ok(p, BLAY);
+  constexpr int BL = BLAY == LAY_RC ? LAY_RC : LAY_KC;
   switch (p.tile_cols) {
-    case 64: return kc ? launch_kc<EPI_TWELL, 64>(p, s) : launch_bf16<ALAY, BLAY, EPI_TWELL, 64>(p, s);
-    case 128: return kc ? launch_kc<EPI_TWELL, 128>(p, s) : launch_bf16<ALAY, BLAY, EPI_TWELL, 128>(p, s);
-    case 256: return kc ? launch_kc<EPI_TWELL, 256>(p, s) : launch_bf16<ALAY, BLAY, EPI_TWELL, 256>(p, s);
+    case 64: return kc ? launch_kc<EPI_TWELL, 64, BL>(p, s) : launch_bf16<ALAY, BLAY, EPI_TWELL, 64>(p, s);
+    case 128: return kc ? launch_kc<EPI_TWELL, 128, BL>(p, s) : launch_bf16<ALAY, BLAY, EPI_TWELL, 128>(p, s);
+    case 256: return kc ? launch_kc<EPI_TWELL, 256, BL>(p, s) : launch_bf16<ALAY, BLAY, EPI_TWELL, 256>(p, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -775,26 +822,32 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmParams p) {
 }  // namespace
 
 hipError_t gemm_bf16(int alay, int blay, int epi, const GemmParams& p, hipStream_t s) {
-  if (alay == LAY_KC && blay == LAY_KC && p.K % KC_BK == 0 && !p.k_count && !p.b_rows && p.ksplit > 1 &&
-      p.part && p.N % 4 == 0) {
+  const bool kcb = alay == LAY_KC && kc_ok(p, blay);
+  if (kcb && p.ksplit > 1 && p.part && p.N % 4 == 0) {
+#define SFL_SPLIT(E_) \
+  case E_: return blay == LAY_KC ? launch_kc_split<E_, LAY_KC>(p, s) : launch_kc_split<E_, LAY_RC>(p, s);
     switch (epi) {
-      case EPI_F32: return launch_kc_split<EPI_F32>(p, s);
-      case EPI_ACT_RELU: return launch_kc_split<EPI_ACT_RELU>(p, s);
-      case EPI_ACT: return launch_kc_split<EPI_ACT>(p, s);
-      case EPI_MUL_ACT: return launch_kc_split<EPI_MUL_ACT>(p, s);
+      SFL_SPLIT(EPI_F32)
+      SFL_SPLIT(EPI_ACT_RELU)
+      SFL_SPLIT(EPI_ACT)
+      SFL_SPLIT(EPI_MUL_ACT)
       default: break;
     }
+#undef SFL_SPLIT
   }
-  if (alay == LAY_KC && blay == LAY_KC && p.K % KC_BK == 0 && !p.k_count && !p.b_rows) {
+  if (kcb && epi != EPI_TWELL) {
+#define SFL_KC(E_) \
+  case E_: return blay == LAY_KC ? launch_kc<E_, 0, LAY_KC>(p, s) : launch_kc<E_, 0, LAY_RC>(p, s);
     switch (epi) {
-      case EPI_F32: return launch_kc<EPI_F32>(p, s);
-      case EPI_ACT_RELU: return launch_kc<EPI_ACT_RELU>(p, s);
-      case EPI_ACT: return launch_kc<EPI_ACT>(p, s);
-      case EPI_MASKGRAD: return launch_kc<EPI_MASKGRAD>(p, s);
-      case EPI_MUL_ACT: return launch_kc<EPI_MUL_ACT>(p, s);
-      case EPI_ACCUM_F32: return launch_kc<EPI_ACCUM_F32>(p, s);
+      SFL_KC(EPI_F32)
+      SFL_KC(EPI_ACT_RELU)
+      SFL_KC(EPI_ACT)
+      SFL_KC(EPI_MASKGRAD)
+      SFL_KC(EPI_MUL_ACT)
+      SFL_KC(EPI_ACCUM_F32)
       default: break;
     }
+#undef SFL_KC
   }
 #define SFL_CASE(A_, B_, E_) \
   if (alay == A_ && blay == B_ && epi == E_) return launch_bf16<A_, B_, E_>(p, s);
