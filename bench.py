@@ -385,7 +385,7 @@ def main():
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_MFMA_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / BF16_MFMA_PEAK_TFLOPS, 4),
                 "traffic": measured_traffic("up_gemm_twell", gemm_hash),
-                "kernel": "k_gemm_kc<EPI_TWELL, 256>", "work": "2*T*d*f flops per launch"}
+                "kernel": "k_gemm_kc<EPI_TWELL, 256, LAY_KC>", "work": "2*T*d*f flops per launch"}
     # the sparse down projection: algorithmic bytes = sum_t nnz_t*(2d + 4) + (2d + 5) per sparse row
     nnz = int(st["total_nnz"])
     n_sparse = T - int(st["n_ovf_rows"])

@@ -261,6 +261,25 @@ def test_forward_deterministic():
         assert torch.equal(b1[k], b2[k])
 
 
+@pytest.mark.parametrize("T,Tn,S,K,s", [(4000, 64, 16, 64, 0.99), (4100, 128, 32, 640, 0.9)])
+def test_large_ragged_batches_narrow_tiles(T, Tn, S, K, s):
+    """Thousands of tokens, not a multiple of any block size, with tiles narrower than 256
+    columns and (at 90%) long ELL rows: sampled rows (overflow rows included) against the
+    oracle, and run-to-run identical output."""
+    w = wl.make_ffn("ragged-large", "bf16", T, 2048, 4096, seed=21, sparsity=s, tile_cols=Tn, tile_slots=S,
+                    ell_width=K)
+    Y, bufs, stats, cfg = run_forward(w, packed_down=True)
+    got = twell_views(bufs, w.T, w.f, cfg)
+    ovf = np.nonzero(got["row_ovf"])[0]
+    assert len(ovf) < 0.01 * T
+    rows = sample_rows(w.T, 96, 5, extra=[0, 255, 256, T - 1, *ovf[:8]])
+    Yref, _ = oracle_rows(w, rows)
+    for i, t in enumerate(rows):
+        assert rel_l2(to_f64(Y)[t], Yref[i]) <= 2e-2, t
+    Y2, _, _, _ = run_forward(w, packed_down=True)
+    assert torch.equal(Y.view(torch.int16), Y2.view(torch.int16))
+
+
 def test_packed_down_weights_layout_and_equivalence():
     w = wl.make_ffn("packed", "bf16", 300, 1024, 2048, seed=12, sparsity=0.98, ell_width=96)
     Wd = dev(w.W_down)
