@@ -68,6 +68,10 @@ bool small_batch(const sfl_ffn_args_t& a) {
   return a.dtype == SFL_BF16 && a.T <= 256 && cdiv(a.f, 256) < 128 && wt != nullptr;
 }
 
+// Dense-backup rows rebuilt from the TwELL slabs (rather than all recomputed by the GEMM)
+// for batches above 256 tokens; below, the rebuild's two launches cost more than it saves.
+bool rebuild_ovf(const sfl_ffn_args_t& a) { return a.T > 256; }
+
 bool fused_twell(const sfl_ffn_args_t& a) {
   const int tn = a.cfg.tile_cols;
   return a.dtype == SFL_BF16 && (tn == 64 || tn == 128 || tn == 256) && !small_batch(a);
@@ -111,6 +115,10 @@ struct FwdPlan {
   void* hval = nullptr;      // gated: h = g * u of the ELL entries [T][K] bf16
   float* part = nullptr;     // split-K partial sums of the dense-backup GEMMs [part_rows][max(f, d)]
   int part_rows = 0;
+  uint8_t* need = nullptr;       // dense-backup slots whose rows the GEMM recomputes [cap]
+  int32_t* need_rows = nullptr;  // their token rows [cap]
+  int32_t* need_slots = nullptr; // their ovf_dense rows [cap]
+  int32_t* n_need = nullptr;     // [1]
   size_t bytes = 0;
 };
 
@@ -140,6 +148,12 @@ FwdPlan plan_forward(const sfl_ffn_args_t& a, void* ws) {
   if (a.dtype == SFL_BF16 && (cap > 0 || small_batch(a))) {
     p.part_rows = (int)std::min<int64_t>(align_rows(std::max<int64_t>(cap, a.T)), kPartRows);
     p.part = (float*)c.take((size_t)p.part_rows * std::max(a.f, a.d) * 4);
+  }
+  if (cap > 0 && rebuild_ovf(a)) {
+    p.need = (uint8_t*)c.take((size_t)cap);
+    p.need_rows = (int32_t*)c.take((size_t)cap * 4);
+    p.need_slots = (int32_t*)c.take((size_t)cap * 4);
+    p.n_need = (int32_t*)c.take(4);
   }
   p.bytes = c.used;
   return p;
@@ -400,8 +414,16 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
                                a->W_down, a->Y, s));
   }
   ev.record(3, s);
-  // 4. dense-backup rows (Alg. 3, dense part): rows gathered through ovf_rows, count on device
+  // 4. dense-backup rows (Alg. 3, dense part), count on device: the dense ReLU rows are
+  // rebuilt from the TwELL slabs where every tile kept its values, and recomputed by the
+  // GEMM (rows gathered through the need list) where a tile overflowed; the gated layer
+  // then multiplies every row by x W_up.
   if (cap > 0) {
+    const bool rebuild = rebuild_ovf(*a);
+    if (rebuild)
+      SFL_HIP(launch_ovf_fill(f, vb, a->cfg.tile_cols, a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, tw.ovf_rows,
+                              tw.n_ovf, (int32_t)cap, ovf_dense, plan.need, plan.need_rows, plan.need_slots,
+                              plan.n_need, s));
     GemmParams g = gp_zero();
     g.M = (int)cap;
     g.N = (int)f;
@@ -409,14 +431,15 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
     g.A = a->X;
     g.lda = d;
     g.a_bytes = T * d * 2;
-    g.a_rows = tw.ovf_rows;
-    g.m_count = tw.n_ovf;
+    g.a_rows = rebuild ? plan.need_rows : tw.ovf_rows;
+    g.m_count = rebuild ? plan.n_need : tw.n_ovf;
     g.count_cap = (int32_t)cap;
     int blay;
     set_weight_B(g, Wp, WpT, d, f, &blay);
     g.bias = a->bias_f;
     g.shift = a->shift_t;
-    g.s_rows = tw.ovf_rows;
+    g.s_rows = g.a_rows;
+    g.c_rows = rebuild ? plan.need_slots : nullptr;
     g.C = ovf_dense;
     g.ldc = f;
     g.ksplit = kMaxSplit;
@@ -425,6 +448,10 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
     SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_ACT_RELU, g, s));
     if (a->gated) {
       GemmParams u = g;
+      u.a_rows = tw.ovf_rows;
+      u.m_count = tw.n_ovf;
+      u.c_rows = nullptr;
+      u.s_rows = nullptr;
       u.bias = nullptr;
       u.shift = nullptr;
       set_weight_B(u, a->W_up, WupT, d, f, &blay);

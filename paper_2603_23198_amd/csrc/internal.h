@@ -81,6 +81,12 @@ hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32
                            int32_t* n_ovf, sfl_stats_t* stats, hipStream_t s);
 hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s);
 // l1 of the computed dense-backup rows (adds into stats->l1_sum).
+// Dense-backup rows whose tiles kept every value, rebuilt from the TwELL slabs; the others
+// are listed (need_rows: token rows, need_slots: their ovf_dense rows, n_need) for the GEMM.
+hipError_t launch_ovf_fill(int64_t f, int val_bf16, int Tn, int S, const void* val, const uint16_t* idx,
+                           const int32_t* cnt, const int32_t* ovf_rows, const int32_t* n_ovf, int32_t cap,
+                           void* dense, uint8_t* need, int32_t* need_rows, int32_t* need_slots, int32_t* n_need,
+                           hipStream_t s);
 hipError_t launch_ovf_l1(int64_t f, int val_bf16, const void* ovf_dense, const int32_t* n_ovf,
                          int32_t cap, sfl_stats_t* stats, hipStream_t s);
 

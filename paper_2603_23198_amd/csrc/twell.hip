@@ -8,6 +8,8 @@
 #include "common.h"
 #include "internal.h"
 
+#include <algorithm>
+
 namespace sfl {
 
 // Active iff z > 0 in IEEE order, decided on the bit pattern so that the result does
@@ -216,9 +218,9 @@ hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int Tn, int S, in
   if (T == 0) return hipSuccess;
   const int NT = (int)cdiv(f, Tn);
   const bool wide = NT > kClassifyMaxTiles;
-  // several rows per wave amortise the per-block statistics; small batches take one row
-  // per wave so that the rows are spread over more CUs
-  const int rpw = T >= 2048 ? kClassifyRowsPerWave : 1;
+  // several rows per wave amortise the per-block statistics, but the walk is latency
+  // bound: keep about 4096 waves (16 per CU) in flight before packing rows
+  const int rpw = (int)std::max<int64_t>(1, std::min<int64_t>(kClassifyRowsPerWave, T / 4096));
   const dim3 grid((unsigned)(wide ? cdiv(T, 4) : cdiv(T, 4 * rpw)));
   if (wide) {
     if (val_bf16)
@@ -296,14 +298,32 @@ hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32
 }
 
 // Sum of the dense-backup rows that were computed (min(n_ovf, cap) rows of ovf_dense).
+// Up to kL1Blocks blocks stride over the rows with 16-byte loads, each adding its total
+// with one float64 atomic (atomics on one address serialise, so one per row would cost
+// more than the sums).
+constexpr int kL1Blocks = 256;
 template <typename V>
 __global__ __launch_bounds__(256) void k_ovf_l1(int64_t f, const V* __restrict__ dense, const int32_t* n_ovf,
                                                 int32_t cap, sfl_stats_t* stats) {
+  constexpr int PER = 16 / (int)sizeof(V);
   const int n = min(*n_ovf, cap);
-  const int64_t row = blockIdx.x;
-  if (row >= n) return;
   float s = 0.f;
-  for (int64_t c = threadIdx.x; c < f; c += 256) s += VT<V>::load(dense, row * f + c);
+  const bool vec = f % PER == 0 && ((uintptr_t)dense & 15) == 0;
+  for (int64_t row = blockIdx.x; row < n; row += gridDim.x) {
+    const V* r = dense + row * f;
+    if (vec) {
+      for (int64_t c = (int64_t)threadIdx.x * PER; c < f; c += 256 * PER) {
+        const u32x4_t w = *(const u32x4_t*)(r + c);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if constexpr (sizeof(V) == 2) s += bf16lo(w[q]) + bf16hi(w[q]);
+          else s += __uint_as_float(w[q]);
+        }
+      }
+    } else {
+      for (int64_t c = threadIdx.x; c < f; c += 256) s += VT<V>::load(r, c);
+    }
+  }
   s = wave_sum<float>(s);
   __shared__ float part[4];
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = s;
@@ -317,10 +337,103 @@ __global__ __launch_bounds__(256) void k_ovf_l1(int64_t f, const V* __restrict__
 hipError_t launch_ovf_l1(int64_t f, int val_bf16, const void* dense, const int32_t* n_ovf, int32_t cap,
                          sfl_stats_t* stats, hipStream_t s) {
   if (!stats || cap == 0) return hipSuccess;
+  const dim3 grid((unsigned)std::min<int32_t>(cap, kL1Blocks));
   if (val_bf16)
-    hipLaunchKernelGGL(k_ovf_l1<bf16_t>, dim3(cap), dim3(256), 0, s, f, (const bf16_t*)dense, n_ovf, cap, stats);
+    hipLaunchKernelGGL(k_ovf_l1<bf16_t>, grid, dim3(256), 0, s, f, (const bf16_t*)dense, n_ovf, cap, stats);
   else
-    hipLaunchKernelGGL(k_ovf_l1<float>, dim3(cap), dim3(256), 0, s, f, (const float*)dense, n_ovf, cap, stats);
+    hipLaunchKernelGGL(k_ovf_l1<float>, grid, dim3(256), 0, s, f, (const float*)dense, n_ovf, cap, stats);
+  return hipGetLastError();
+}
+
+// Dense-backup rows straight from the TwELL slabs (Sec. 3.4): a row whose tiles all kept
+// every active value (cnt <= S) is rebuilt exactly, zeros and all, in LDS one window of
+// columns at a time and written out; a row with an overflowing tile lost values, so it
+// is flagged (need[i] = 1) for recomputation by the GEMM. Blocks stride over the slots
+// i < n_ovf.
+constexpr int kFillWindowBytes = 32768;
+constexpr int kFillBlocks = 1024;
+template <typename V>
+__global__ __launch_bounds__(256) void k_ovf_fill(int64_t f, int NT, int Tn, int S, const V* __restrict__ val,
+                                                  const uint16_t* __restrict__ idx, const int32_t* __restrict__ cnt,
+                                                  const int32_t* __restrict__ ovf_rows, const int32_t* __restrict__ n_ovf,
+                                                  int32_t cap, V* __restrict__ dense, uint8_t* __restrict__ need) {
+  constexpr int WIN = kFillWindowBytes / (int)sizeof(V);  // columns per window (a multiple of every tile width)
+  __shared__ V row_s[WIN];
+  const int n = min(*n_ovf, cap);
+  for (int i = blockIdx.x; i < n; i += gridDim.x) {
+    const int64_t t = ovf_rows[i];
+    const int32_t* crow = cnt + t * NT;
+    int over = 0;
+    for (int j = threadIdx.x; j < NT; j += 256) over |= crow[j] > S;
+    over = __syncthreads_or(over);
+    if (threadIdx.x == 0) need[i] = over ? 1 : 0;
+    if (over) continue;
+    const V* vrow = val + t * (int64_t)NT * S;
+    const uint16_t* irow = idx + t * (int64_t)NT * S;
+    V* out = dense + (int64_t)i * f;
+    for (int64_t c0 = 0; c0 < f; c0 += WIN) {
+      const int w = (int)std::min<int64_t>(WIN, f - c0);
+      for (int x = threadIdx.x; x < w; x += 256) row_s[x] = V(0);
+      __syncthreads();
+      const int j0 = (int)(c0 / Tn), nt = (w + Tn - 1) / Tn;
+      for (int q = threadIdx.x; q < nt * S; q += 256) {
+        const int j = j0 + q / S, sl = q % S;
+        if (sl < crow[j]) row_s[(int)(irow[(int64_t)j * S + sl] - c0)] = vrow[(int64_t)j * S + sl];
+      }
+      __syncthreads();
+      for (int x = threadIdx.x; x < w; x += 256) out[c0 + x] = row_s[x];
+      __syncthreads();
+    }
+  }
+}
+
+// Compaction of the flagged slots (ascending): rows[k] = ovf_rows[slot], slots[k] = slot.
+__global__ __launch_bounds__(1024) void k_need_list(int32_t cap, const int32_t* __restrict__ ovf_rows,
+                                                    const int32_t* __restrict__ n_ovf, const uint8_t* __restrict__ need,
+                                                    int32_t* __restrict__ rows, int32_t* __restrict__ slots,
+                                                    int32_t* __restrict__ n_need) {
+  __shared__ int wsum[16];
+  const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
+  const int n = min(*n_ovf, cap);
+  int base = 0;
+  for (int r0 = 0; r0 < n; r0 += 1024) {
+    const int i = r0 + tid;
+    const int flag = (i < n && need[i]) ? 1 : 0;
+    const int incl = wave_incl_scan(flag);
+    if (l == 63) wsum[w] = incl;
+    __syncthreads();
+    int before = 0, all = 0;
+    for (int q = 0; q < 16; ++q) {
+      const int v = wsum[q];
+      before += (q < w) ? v : 0;
+      all += v;
+    }
+    const int pos = base + before + incl - flag;
+    if (flag) {
+      rows[pos] = ovf_rows[i];
+      slots[pos] = i;
+    }
+    base += all;
+    __syncthreads();
+  }
+  if (tid == 0) *n_need = base;
+}
+
+hipError_t launch_ovf_fill(int64_t f, int val_bf16, int Tn, int S, const void* val, const uint16_t* idx,
+                           const int32_t* cnt, const int32_t* ovf_rows, const int32_t* n_ovf, int32_t cap,
+                           void* dense, uint8_t* need, int32_t* need_rows, int32_t* need_slots, int32_t* n_need,
+                           hipStream_t s) {
+  if (cap == 0) return hipSuccess;
+  const int NT = (int)cdiv(f, Tn);
+  const dim3 grid((unsigned)std::min<int32_t>(cap, kFillBlocks));
+  if (val_bf16)
+    hipLaunchKernelGGL(k_ovf_fill<bf16_t>, grid, dim3(256), 0, s, f, NT, Tn, S, (const bf16_t*)val, idx, cnt,
+                       ovf_rows, n_ovf, cap, (bf16_t*)dense, need);
+  else
+    hipLaunchKernelGGL(k_ovf_fill<float>, grid, dim3(256), 0, s, f, NT, Tn, S, (const float*)val, idx, cnt,
+                       ovf_rows, n_ovf, cap, (float*)dense, need);
+  hipLaunchKernelGGL(k_need_list, dim3(1), dim3(1024), 0, s, cap, ovf_rows, n_ovf, need, need_rows, need_slots,
+                     n_need);
   return hipGetLastError();
 }
 

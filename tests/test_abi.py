@@ -71,6 +71,15 @@ def _fake_args(dtype, T, d, f, gated=False, **kw):
     return a
 
 
+def _al(n):
+    return -(-n // 256) * 256  # workspace pieces are 256-byte aligned
+
+
+def _need_lists(cap):
+    # dense-backup slots recomputed by the GEMM: flags, token rows, ovf_dense rows, count
+    return _al(cap) + 2 * _al(4 * cap) + _al(4)
+
+
 def test_workspace_sizes():
     a = _fake_args(b.SFL_BF16, 128, 256, 1024, ell_width=32)
     ws = b.sfl_workspace_size(a, 0)
@@ -81,6 +90,11 @@ def test_workspace_sizes():
     a32 = _fake_args(b.SFL_F32, 64, 256, 1024, ell_width=32)
     a32.twell.ovf_dense = 0x2000
     assert b.sfl_workspace_size(a32, 0) == 64 * 1024 * 4  # fp32: pre-activations staged
+    # above 256 tokens the dense-backup rows are rebuilt from the TwELL slabs, and the rows
+    # the GEMM still recomputes are listed in the workspace
+    big = _fake_args(b.SFL_BF16, 512, 256, 1024, ell_width=32, ovf_capacity=64)
+    big.twell.ovf_dense = 0x2000
+    assert b.sfl_workspace_size(big, 0) == 512 * 1024 * 4 + _need_lists(64)  # partial sums: 512 rows (T)
     assert b.sfl_workspace_size(a, 2) == 128 * 1024 * 2 + part  # dense baseline: H, split-K partials (T <= 256)
 
 

@@ -109,6 +109,10 @@ def test_c2_lognormal_overflow_full():
     n_ovf = got["n_ovf"]
     assert 0.08 * w.T < n_ovf < 0.3 * w.T, n_ovf   # the dense-backup path is exercised
     assert st["n_ovf_rows"] == n_ovf and st["capacity_exceeded"] == 0
+    # both ways of forming dense-backup rows are exercised: rebuilt from the TwELL slabs
+    # (every tile kept its values) and recomputed (some tile overflowed)
+    tile_ovf_rows = (got["cnt"] > cfg.tile_slots).any(axis=1)
+    assert 0 < tile_ovf_rows.sum() < n_ovf, tile_ovf_rows.sum()
     rows = np.arange(w.T)
     Yref, Z = oracle_rows(w, rows)
     assert rel_l2(to_f64(Y), Yref) <= 2e-2
