@@ -76,10 +76,10 @@ constexpr int kClassifyRowsPerWave = 8;
 // Statistics of a block's rows, reduced in LDS and added to the device totals with one
 // atomic per field per block (per-row atomics on the same address serialise).
 __device__ __forceinline__ void block_stats_add(sfl_stats_t* stats, int64_t nnz, int tile_over, float l1) {
-  __shared__ long long s_nnz[4];
-  __shared__ int s_over[4];
-  __shared__ float s_l1[4];
-  const int w = threadIdx.x >> 6;
+  __shared__ long long s_nnz[16];
+  __shared__ int s_over[16];
+  __shared__ float s_l1[16];
+  const int w = threadIdx.x >> 6, nw = blockDim.x >> 6;
   l1 = wave_sum<float>(l1);
   if ((threadIdx.x & 63) == 0) {
     s_nnz[w] = nnz;
@@ -88,22 +88,28 @@ __device__ __forceinline__ void block_stats_add(sfl_stats_t* stats, int64_t nnz,
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    const long long a = s_nnz[0] + s_nnz[1] + s_nnz[2] + s_nnz[3];
-    const int b = s_over[0] + s_over[1] + s_over[2] + s_over[3];
-    const float c = (s_l1[0] + s_l1[1]) + (s_l1[2] + s_l1[3]);
+    long long a = 0;
+    int b = 0;
+    float c = 0.f;
+    for (int i = 0; i < nw; ++i) {
+      a += s_nnz[i];
+      b += s_over[i];
+      c += s_l1[i];
+    }
     if (a) atomicAdd((unsigned long long*)&stats->total_nnz, (unsigned long long)a);
     if (b) atomicAdd((unsigned long long*)&stats->n_tile_ovf, (unsigned long long)b);
     if (c != 0.f) atomicAdd(&stats->l1_sum, (double)c);
   }
 }
 
+constexpr int kClassifyWaves = 16;  // waves per block of k_classify
 template <typename V>
-__global__ __launch_bounds__(256) void k_classify(int64_t T, int NT, int S, int K, const V* __restrict__ val,
+__global__ __launch_bounds__(kClassifyWaves * 64) void k_classify(int64_t T, int NT, int S, int K, const V* __restrict__ val,
                                                   const uint16_t* __restrict__ idx, const int32_t* __restrict__ cnt,
                                                   int32_t* __restrict__ row_nnz, uint8_t* __restrict__ row_ovf,
                                                   V* __restrict__ ell_val, uint16_t* __restrict__ ell_idx,
                                                   sfl_stats_t* __restrict__ stats, int rpw) {
-  __shared__ int incl_lds[4][kClassifyMaxTiles];
+  __shared__ int incl_lds[kClassifyWaves][kClassifyMaxTiles];
   const int l = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   int* incl_s = incl_lds[w];
@@ -111,7 +117,7 @@ __global__ __launch_bounds__(256) void k_classify(int64_t T, int NT, int S, int 
   int over_sum = 0;
   float l1 = 0.f;
   for (int rr = 0; rr < rpw; ++rr) {
-    const int64_t t = ((int64_t)blockIdx.x * 4 + w) * rpw + rr;
+    const int64_t t = ((int64_t)blockIdx.x * kClassifyWaves + w) * rpw + rr;
     if (t >= T) break;
     const int32_t* crow = cnt + t * NT;
     int total = 0;
@@ -221,7 +227,7 @@ hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int Tn, int S, in
   // several rows per wave amortise the per-block statistics, but the walk is latency
   // bound: keep about 4096 waves (16 per CU) in flight before packing rows
   const int rpw = (int)std::max<int64_t>(1, std::min<int64_t>(kClassifyRowsPerWave, T / 4096));
-  const dim3 grid((unsigned)(wide ? cdiv(T, 4) : cdiv(T, 4 * rpw)));
+  const dim3 grid((unsigned)(wide ? cdiv(T, 4) : cdiv(T, kClassifyWaves * rpw)));
   if (wide) {
     if (val_bf16)
       hipLaunchKernelGGL(k_classify_wide<bf16_t>, grid, dim3(256), 0, s, T, NT, S, K, (const bf16_t*)val, idx, cnt,
@@ -231,11 +237,11 @@ hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int Tn, int S, in
                          row_nnz, row_ovf, (float*)ell_val, ell_idx, stats);
   } else {
     if (val_bf16)
-      hipLaunchKernelGGL(k_classify<bf16_t>, grid, dim3(256), 0, s, T, NT, S, K, (const bf16_t*)val, idx, cnt,
-                         row_nnz, row_ovf, (bf16_t*)ell_val, ell_idx, stats, rpw);
+      hipLaunchKernelGGL(k_classify<bf16_t>, grid, dim3(kClassifyWaves * 64), 0, s, T, NT, S, K, (const bf16_t*)val,
+                         idx, cnt, row_nnz, row_ovf, (bf16_t*)ell_val, ell_idx, stats, rpw);
     else
-      hipLaunchKernelGGL(k_classify<float>, grid, dim3(256), 0, s, T, NT, S, K, (const float*)val, idx, cnt, row_nnz,
-                         row_ovf, (float*)ell_val, ell_idx, stats, rpw);
+      hipLaunchKernelGGL(k_classify<float>, grid, dim3(kClassifyWaves * 64), 0, s, T, NT, S, K, (const float*)val,
+                         idx, cnt, row_nnz, row_ovf, (float*)ell_val, ell_idx, stats, rpw);
   }
   return hipGetLastError();
 }
