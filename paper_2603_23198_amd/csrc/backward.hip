@@ -31,34 +31,55 @@ namespace {
 constexpr int kBlkTok = 64;  // tokens per block of the counting sort
 
 // ---- 3. transposed pattern (counting sort in token order) -----------------------------
-// (a) per block of 64 tokens, per unit: how many of the block's sparse rows activate it.
-__global__ __launch_bounds__(256) void k_blk_count(int64_t T, int K, int64_t f, const uint16_t* __restrict__ ell_idx,
+// (a) per block of 64 tokens and per unit: which of the block's sparse rows activate it,
+// as a 64-bit mask (bit tt = token b*64 + tt), built with LDS atomics over a window of
+// kMaskUnits units per workgroup, and its population count.
+constexpr int kMaskUnits = 16384;  // 128 KiB of LDS masks per workgroup
+__global__ __launch_bounds__(1024) void k_blk_mask(int64_t T, int K, int64_t f, const uint16_t* __restrict__ ell_idx,
                                                    const int32_t* __restrict__ row_nnz,
-                                                   const uint8_t* __restrict__ row_ovf, int32_t* __restrict__ bc) {
+                                                   const uint8_t* __restrict__ row_ovf, uint64_t* __restrict__ bm,
+                                                   int32_t* __restrict__ bc) {
+  extern __shared__ unsigned long long mask_s[];  // [kMaskUnits]
   const int64_t b = blockIdx.x;
-  int32_t* out = bc + b * f;
-  for (int64_t i = threadIdx.x; i < f; i += 256) out[i] = 0;
+  const int64_t u0 = (int64_t)blockIdx.y * kMaskUnits;
+  const int nu = (int)std::min<int64_t>(kMaskUnits, f - u0);
+  for (int i = threadIdx.x; i < nu; i += 1024) mask_s[i] = 0ull;
   __syncthreads();
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
-  for (int tt = w; tt < kBlkTok; tt += 4) {
+  for (int tt = w; tt < kBlkTok; tt += 16) {
     const int64_t t = b * kBlkTok + tt;
     if (t >= T || row_ovf[t]) continue;
     const int nnz = row_nnz[t];
-    for (int e = l; e < nnz; e += 64) atomicAdd(&out[ell_idx[t * (int64_t)K + e]], 1);
+    for (int e = l; e < nnz; e += 64) {
+      const int64_t n = ell_idx[t * (int64_t)K + e] - u0;
+      if (n >= 0 && n < nu) atomicOr(&mask_s[n], 1ull << tt);
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < nu; i += 1024) {
+    const uint64_t m = mask_s[i];
+    bm[b * f + u0 + i] = m;
+    bc[b * f + u0 + i] = __popcll(m);
   }
 }
 
 // (b) per unit: exclusive scan over the blocks (in place: bc[b][n] becomes the offset of
-// block b within unit n's list) and the unit's total.
+// block b within unit n's list) and the unit's total; 16 blocks' counts are read at a
+// time so that their loads overlap.
 __global__ __launch_bounds__(256) void k_blk_scan(int64_t nb, int64_t f, int32_t* __restrict__ bc,
                                                   int32_t* __restrict__ col_cnt) {
   const int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (n >= f) return;
   int run = 0;
-  for (int64_t b = 0; b < nb; ++b) {
-    const int c = bc[b * f + n];
-    bc[b * f + n] = run;
-    run += c;
+  for (int64_t b0 = 0; b0 < nb; b0 += 16) {
+    int c[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) c[q] = b0 + q < nb ? bc[(b0 + q) * f + n] : 0;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      if (b0 + q < nb) bc[(b0 + q) * f + n] = run;
+      run += c[q];
+    }
   }
   col_cnt[n] = run;
 }
@@ -87,42 +108,38 @@ __global__ __launch_bounds__(1024) void k_col_ptr(int64_t f, const int32_t* __re
   if (tid == 0) col_ptr[f] = base;
 }
 
-// (d) fill: one wave per block walks its tokens in order; a unit appears at most once per
-// token, so the lanes of one token never share a unit, and the per-unit cursor in LDS
-// gives each (token, entry) its place in token order. Up to three per-entry values go
-// beside the token (fp32 sources [T][K]; value 0 may come from the bf16 ELL values).
+// (d) fill: entry (t, e) with unit n goes to position col_ptr[n] + (offset of t's block
+// in n's list) + (the block's earlier tokens that activate n: the mask's bits below t),
+// i.e. each unit's list in token order. Every entry is placed independently (one wave
+// per token). Up to three per-entry values go beside the token (fp32 sources [T][K];
+// value 0 may come from the bf16 ELL values).
 struct FillValues {
   const bf16_t* hb;    // when non-null: value 0 from these bf16 entries
   const float* v[3];   // fp32 sources (null: unused)
   float* out[3];       // [T K] destinations in list order
 };
 
-__global__ __launch_bounds__(64) void k_blk_fill(int64_t T, int K, int64_t f, const uint16_t* __restrict__ ell_idx,
-                                                 const int32_t* __restrict__ row_nnz,
-                                                 const uint8_t* __restrict__ row_ovf, const int32_t* __restrict__ bc,
-                                                 const int32_t* __restrict__ col_ptr, int32_t* __restrict__ csc_tok,
-                                                 FillValues fv) {
-  extern __shared__ int32_t cursor[];  // [f]
-  const int64_t b = blockIdx.x;
-  const int l = threadIdx.x;
-  for (int64_t i = l; i < f; i += 64) cursor[i] = 0;
-  __syncthreads();
-  for (int tt = 0; tt < kBlkTok; ++tt) {
-    const int64_t t = b * kBlkTok + tt;
-    if (t >= T) break;
-    if (row_ovf[t]) continue;
-    const int nnz = row_nnz[t];
-    for (int e = l; e < nnz; e += 64) {
-      const int64_t src = t * (int64_t)K + e;
-      const int n = ell_idx[src];
-      const int pos = col_ptr[n] + bc[b * f + n] + cursor[n];
-      cursor[n] += 1;
-      csc_tok[pos] = (int32_t)t;
-      if (fv.out[0]) fv.out[0][pos] = fv.hb ? bf16_to_f32(fv.hb[src]) : fv.v[0][src];
-      if (fv.out[1]) fv.out[1][pos] = fv.v[1][src];
-      if (fv.out[2]) fv.out[2][pos] = fv.v[2][src];
-    }
-    __syncthreads();
+__global__ __launch_bounds__(256) void k_blk_fill(int64_t T, int K, int64_t f, const uint16_t* __restrict__ ell_idx,
+                                                  const int32_t* __restrict__ row_nnz,
+                                                  const uint8_t* __restrict__ row_ovf,
+                                                  const uint64_t* __restrict__ bm, const int32_t* __restrict__ bc,
+                                                  const int32_t* __restrict__ col_ptr, int32_t* __restrict__ csc_tok,
+                                                  FillValues fv) {
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int l = threadIdx.x & 63;
+  if (t >= T || row_ovf[t]) return;
+  const int64_t b = t / kBlkTok;
+  const int tt = (int)(t % kBlkTok);
+  const uint64_t below = (1ull << tt) - 1ull;
+  const int nnz = row_nnz[t];
+  for (int e = l; e < nnz; e += 64) {
+    const int64_t src = t * (int64_t)K + e;
+    const int64_t n = ell_idx[src];
+    const int pos = col_ptr[n] + bc[b * f + n] + __popcll(bm[b * f + n] & below);
+    csc_tok[pos] = (int32_t)t;
+    if (fv.out[0]) fv.out[0][pos] = fv.hb ? bf16_to_f32(fv.hb[src]) : fv.v[0][src];
+    if (fv.out[1]) fv.out[1][pos] = fv.v[1][src];
+    if (fv.out[2]) fv.out[2][pos] = fv.v[2][src];
   }
 }
 
@@ -173,6 +190,7 @@ struct BwdPlan {
   float* hf = nullptr;        // gated: [T][K] h = h_g h_u
   float* dxf = nullptr;       // gated: [T][d] fp32 dX accumulator of the sparse rows
   int32_t* bc = nullptr;      // [nb][f]
+  uint64_t* bm = nullptr;     // [nb][f] per-block token masks
   int32_t* col_cnt = nullptr; // [f]
   int32_t* col_ptr = nullptr; // [f + 1]
   int32_t* csc_tok = nullptr; // [T K]
@@ -220,6 +238,7 @@ BwdPlan plan_backward(const sfl_ffn_bwd_args_t& a, void* ws) {
     p.dxf = (float*)take((size_t)T * d * 4);
   }
   p.bc = (int32_t*)take((size_t)nb * f * 4);
+  p.bm = (uint64_t*)take((size_t)nb * f * 8);
   p.col_cnt = (int32_t*)take((size_t)f * 4);
   p.col_ptr = (int32_t*)take((size_t)(f + 1) * 4);
   p.csc_tok = (int32_t*)take((size_t)T * K * 4);
@@ -372,16 +391,17 @@ sfl_status_t backward_run(const sfl_ffn_bwd_args_t* a, hipStream_t s) {
   }
   rec(2);
   // 3. transposed pattern, with each entry's values
-  hipLaunchKernelGGL(k_blk_count, dim3((unsigned)nb), dim3(256), 0, s, T, K, f, sv.ell_idx, sv.row_nnz, sv.row_ovf,
-                     p.bc);
-  SFL_HIPB(hipGetLastError());
+  {
+    const size_t mask_lds = (size_t)kMaskUnits * 8;
+    SFL_HIPB(hipFuncSetAttribute((const void*)k_blk_mask, hipFuncAttributeMaxDynamicSharedMemorySize, (int)mask_lds));
+    hipLaunchKernelGGL(k_blk_mask, dim3((unsigned)nb, (unsigned)cdiv(f, kMaskUnits)), dim3(1024), mask_lds, s, T, K, f,
+                       sv.ell_idx, sv.row_nnz, sv.row_ovf, p.bm, p.bc);
+    SFL_HIPB(hipGetLastError());
+  }
   hipLaunchKernelGGL(k_blk_scan, dim3((unsigned)cdiv(f, 256)), dim3(256), 0, s, nb, f, p.bc, p.col_cnt);
   SFL_HIPB(hipGetLastError());
   hipLaunchKernelGGL(k_col_ptr, dim3(1), dim3(1024), 0, s, f, p.col_cnt, p.col_ptr);
   SFL_HIPB(hipGetLastError());
-  const size_t fill_lds = (size_t)f * 4;
-  if (fill_lds > 65536)
-    SFL_HIPB(hipFuncSetAttribute((const void*)k_blk_fill, hipFuncAttributeMaxDynamicSharedMemorySize, (int)fill_lds));
   FillValues fv;
   std::memset(&fv, 0, sizeof(fv));
   if (!gated) {
@@ -395,8 +415,8 @@ sfl_status_t backward_run(const sfl_ffn_bwd_args_t* a, hipStream_t s) {
   }
   fv.out[0] = p.csc_h;
   fv.out[1] = p.csc_z;
-  hipLaunchKernelGGL(k_blk_fill, dim3((unsigned)nb), dim3(64), fill_lds, s, T, K, f, sv.ell_idx, sv.row_nnz,
-                     sv.row_ovf, p.bc, p.col_ptr, p.csc_tok, fv);
+  hipLaunchKernelGGL(k_blk_fill, dim3((unsigned)cdiv(T, 4)), dim3(256), 0, s, T, K, f, sv.ell_idx, sv.row_nnz,
+                     sv.row_ovf, p.bm, p.bc, p.col_ptr, p.csc_tok, fv);
   SFL_HIPB(hipGetLastError());
   rec(3);
   // 4. weight gradients of the sparse rows: per-unit gathers over slice-major dY and X
