@@ -441,6 +441,11 @@ def main():
         "n_ovf_rows": head["n_ovf_rows"],
         "roofline": roofline,
         "gather_roofline": gather,
+        # the fused ReLU -> TwELL epilogue measured as the difference to the same GEMM with a
+        # plain ReLU + bf16 store epilogue (the dense FFN's first GEMM)
+        "twell_epilogue_delta_ms": round(stages["up_gemm_twell"] - head["dense_stages_ms"]["up_gemm_relu"], 4),
+        # dense-equivalent work per second: the dense FFN's 4 T d f flops over the sparse time
+        "tflops_equivalent": round(4.0 * T * d * f / (ms * 1e-3) / 1e12, 1),
     }
     del s
     if not a.quick:
