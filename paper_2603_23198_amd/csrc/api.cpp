@@ -472,7 +472,8 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
     y.ldc = d;
     y.ksplit = kMaxSplit;
     y.part = plan.part;
-    y.part_rows = plan.part_rows;
+    // the partial-sum buffer holds part_rows rows of max(f, d) columns: more rows of d
+    y.part_rows = (int)std::min<int64_t>((int64_t)plan.part_rows * std::max(f, d) / d, INT32_MAX);
     SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_ACT, y, s));
     SFL_HIP(launch_ovf_l1(f, vb, ovf_dense, tw.n_ovf, (int32_t)cap, a->stats, s));
   }
