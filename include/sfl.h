@@ -81,7 +81,11 @@ typedef struct {
  *  ell_idx   [T][K]     uint16 columns of ell_val
  *  ovf_dense [cap][f]   activation dtype: dense ReLU rows of the dense-backup rows,
  *                       written by sfl_ffn_forward (training state), may be NULL
- *                       in sfl_pack_twell.
+ *                       in sfl_pack_twell. Above 256 tokens a row whose tiles all
+ *                       kept their values (every cnt <= S) is copied from the TwELL
+ *                       slabs (bit-identical to them); the others (and all rows of
+ *                       smaller batches) are recomputed from X by a GEMM whose fp32
+ *                       sums may round differently from the TwELL values.
  * Slots s >= min(cnt, S), ELL entries beyond a row's count and the ELL rows of
  * dense-backup rows are left unwritten (their contents are unspecified). */
 typedef struct {
