@@ -66,7 +66,8 @@ typedef struct {
 } sfl_twell_cfg_t;
 
 /* Packed activations: TwELL (Alg. 1 outputs) plus the hybrid format (Sec. 3.4).
- * With N_T = ceil(f / T_n), all row-major:
+ * With N_T = ceil(f / T_n), all row-major (with T = 0 every buffer but n_ovf has
+ * zero size and may be NULL):
  *  val       [T][N_T*S] activation dtype: val[t][j*S+s] = s-th active value of tile j
  *  idx       [T][N_T*S] uint16 global column of that value (f <= 65535)
  *  cnt       [T][N_T]   int32 true count of active columns in tile j (may exceed S)
@@ -222,7 +223,7 @@ typedef struct {
  *            1: after dh at the pattern, 2: after dX of the sparse rows, 3: after the
  *            transposed pattern, 4: after the weight gradients of the sparse rows,
  *            5: end, after the dense-backup rows).
- * Supports d % 512 == 0, f % 64 == 0, f <= 40960 and T <= 2^31 / (2 d). */
+ * Supports d % 512 == 0, f % 64 == 0, f <= 65535 and T <= 2^31 / (2 d). */
 typedef struct {
   sfl_dtype_t dtype;
   int32_t gated;

@@ -98,8 +98,11 @@ sfl_status_t check_forward(const sfl_ffn_args_t* a, bool need_output = true) {
   return SFL_OK;
 }
 
-sfl_status_t check_twell(const sfl_twell_t& t, bool need_ell) {
-  if (!t.val || !t.idx || !t.cnt || !t.row_nnz || !t.row_ovf || !t.ovf_rows || !t.n_ovf) return SFL_E_ARG;
+// With T == 0 every buffer but the count has zero size and may be NULL.
+sfl_status_t check_twell(const sfl_twell_t& t, bool need_ell, int64_t T) {
+  if (!t.n_ovf) return SFL_E_ARG;
+  if (T == 0) return SFL_OK;
+  if (!t.val || !t.idx || !t.cnt || !t.row_nnz || !t.row_ovf || !t.ovf_rows) return SFL_E_ARG;
   if (need_ell && (!t.ell_val || !t.ell_idx)) return SFL_E_ARG;
   return SFL_OK;
 }
@@ -251,7 +254,7 @@ sfl_status_t sfl_pack_twell(const float* Z, int64_t T, int64_t f, sfl_dtype_t va
   sfl_status_t st = check_cfg(cfg, f);
   if (st != SFL_OK) return st;
   if (T > 0 && !Z) return SFL_E_ARG;
-  st = check_twell(*out, false);
+  st = check_twell(*out, false, T);
   if (st != SFL_OK) return st;
   if ((out->ell_val == nullptr) != (out->ell_idx == nullptr)) return SFL_E_ARG;
   hipStream_t s = (hipStream_t)stream;
@@ -318,7 +321,7 @@ sfl_status_t sfl_up_projection(const sfl_ffn_args_t* a, float* Z, sfl_stream_t s
 sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
   sfl_status_t st = check_forward(a);
   if (st != SFL_OK) return st;
-  st = check_twell(a->twell, true);
+  st = check_twell(a->twell, true, a->T);
   if (st != SFL_OK) return st;
   FwdPlan plan = plan_forward(*a, nullptr);
   if (plan.bytes > 0 && (!a->workspace || a->workspace_bytes < plan.bytes)) return SFL_E_WORKSPACE;

@@ -274,7 +274,6 @@ sfl_status_t check_backward(const sfl_ffn_bwd_args_t* a) {
   if (a->cfg.ell_width < 0 || a->cfg.ovf_capacity < 0) return SFL_E_ARG;
   if (a->dtype != SFL_BF16) return SFL_E_UNSUPPORTED;
   if (a->d % 512 != 0 || a->f % 64 != 0) return SFL_E_UNSUPPORTED;
-  if (a->f > 40960) return SFL_E_UNSUPPORTED;  // the transpose keeps one cursor per unit in LDS
   if (!a->dW_up || !a->dW_down || (a->gated && !a->dW_gate)) return SFL_E_ARG;
   if (a->T > 0) {
     if (!a->X || !a->W_up || !a->W_down || !a->dY || !a->dX) return SFL_E_ARG;

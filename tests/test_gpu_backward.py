@@ -94,6 +94,29 @@ def test_backward_small_full(T, d, f, K, S, lam_scale):
     assert rel_l2(to_f64(dX)[ovf], rdX[ovf]) <= 2e-2
 
 
+def test_backward_empty_batch():
+    """T = 0: the weight gradients are zero (overwriting what the buffers held)."""
+    w = wl.make_ffn("empty", "bf16", 0, 512, 1024, seed=4, sparsity=0.99, ell_width=32, with_dy=True)
+    dX, dWu, dWd, bufs, cfg = run_fwd_bwd(w, 0.0)
+    assert dX.shape == (0, 512)
+    assert torch.count_nonzero(dWu).item() == 0 and torch.count_nonzero(dWd).item() == 0
+
+
+def test_backward_widest_f():
+    """f = 65472, the widest multiple of 64 the uint16 column index allows: the transposed
+    pattern spans four windows of per-unit token masks; two dense-backup rows."""
+    T, d, f = 96, 512, 65472
+    w = wl.make_ffn("wide", "bf16", T, d, f, seed=23, sparsity=0.99, ell_width=1024, with_dy=True)
+    w.shift_t[:2] = 10.0
+    lam = 1e-3 * T * f
+    dX, dWu, dWd, bufs, cfg = run_fwd_bwd(w, lam)
+    act = gpu_pattern(bufs, w, cfg)
+    rdX, rdWu, rdWd = oracle_full(w, act, lam)
+    assert rel_l2(to_f64(dX), rdX) <= 2e-2
+    assert rel_l2(to_f64(dWu), rdWu) <= 2e-2
+    assert rel_l2(to_f64(dWd), rdWd) <= 2e-2
+
+
 def test_backward_hot_units_exceed_staged_lists():
     """Units active in every token have lists longer than one block's LDS stage, so their
     per-unit gathers read the lists from global memory; results still meet the oracle."""

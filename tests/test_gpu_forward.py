@@ -284,6 +284,31 @@ def test_large_ragged_batches_narrow_tiles(T, Tn, S, K, s):
     assert torch.equal(Y.view(torch.int16), Y2.view(torch.int16))
 
 
+@pytest.mark.parametrize("dtype,gated", [("bf16", False), ("f32", False), ("bf16", True)])
+def test_empty_batch(dtype, gated):
+    """T = 0: the forward and the dense FFN succeed with every zero-size buffer NULL (an
+    empty tensor's pointer), write a dense-backup count of 0 and leave the statistics at 0."""
+    w = wl.make_ffn("empty", dtype, 0, 512, 1024, seed=3, gated=gated, sparsity=0.99, ell_width=32)
+    X, Wu, Wd = dev(w.X), dev(w.W_up), dev(w.W_down)
+    assert X.numel() == 0
+    Wg = dev(w.W_gate) if gated else None
+    cfg = b.make_cfg(**w.cfg)
+    bufs = {k: None for k in b.alloc_twell(1, w.f, dtype, cfg)}
+    bufs["n_ovf"] = torch.full((1,), -7, dtype=torch.int32, device="cuda")
+    stats = b.alloc_stats()
+    Y = torch.empty((0, w.d), dtype=X.dtype, device="cuda")
+    for dense in (False, True):
+        args = b.ffn_args(X, Wu, Wd, cfg, Y=Y, bufs=bufs, W_gate=Wg, stats=stats)
+        ws = torch.empty(max(1, b.sfl_workspace_size(args, 2 if dense else 0)), dtype=torch.uint8, device="cuda")
+        args = b.ffn_args(X, Wu, Wd, cfg, Y=Y, bufs=bufs, W_gate=Wg, stats=stats, workspace=ws)
+        (b.sfl_dense_ffn_baseline if dense else b.sfl_ffn_forward)(args)
+        torch.cuda.synchronize()
+    assert int(bufs["n_ovf"].item()) == 0
+    st = b.read_stats(stats)
+    assert st["total_nnz"] == 0 and st["n_ovf_rows"] == 0 and st["l1_sum"] == 0.0
+    assert st["capacity_exceeded"] == 0
+
+
 def test_packed_down_weights_layout_and_equivalence():
     w = wl.make_ffn("packed", "bf16", 300, 1024, 2048, seed=12, sparsity=0.98, ell_width=96)
     Wd = dev(w.W_down)
