@@ -137,6 +137,20 @@ constexpr int GATHER_WAVES = SFL_GATHER_WAVES;
 constexpr int GU = SFL_GATHER_UNROLL;       // row loads in flight per lane
 constexpr int GATHER_LDS = SFL_GATHER_LDS;  // bytes of cached ELL entries per workgroup
 
+// Sum of the 8 groups' partial sums (lanes l, l ^ 8, ..., l ^ 56) into every group: the
+// partner 8 lanes away is in the same 16-lane row (DPP row_ror:8), the other two steps
+// cross rows (lane shuffles). Same values as shuffles with xor 8, 16, 32.
+__device__ __forceinline__ void fold_groups(float (&acc)[8]) {
+  static_assert(LPR == 8, "groups of 8 lanes");
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+    acc[j] += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(acc[j]), 0x128, 0xf, 0xf, false));
+#pragma unroll
+  for (int o = 16; o < 64; o <<= 1)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], o, 64);
+}
+
 // One token's slice: entries er[0..nnz) in LDS, W row segments read through the buffer
 // descriptor at byte offset idx * 2 * SLICE + col_b; on return the lanes of group 0 hold
 // the sums of their 8 columns.
@@ -169,10 +183,7 @@ __device__ __forceinline__ void slice_token(const uint32_t* er, int nnz, __amdgp
       }
     }
   }
-#pragma unroll
-  for (int o = LPR; o < 64; o <<= 1)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], o, 64);
+  fold_groups(acc);
 }
 
 // The same with fp32 values: entries are (index, fp32 value bits) word pairs, and each
@@ -203,10 +214,7 @@ __device__ __forceinline__ void slice_token_f32(const uint32_t* er, int nnz, __a
         acc[2 * j + 1] = fmaf(v[u], bf16hi(ww), acc[2 * j + 1]);
       }
   }
-#pragma unroll
-  for (int o = LPR; o < 64; o <<= 1)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], o, 64);
+  fold_groups(acc);
 }
 
 // VK: kind of the ELL values. 0: bf16 (packed with the index in one word); 1: fp32 (the
@@ -287,6 +295,21 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
   }
 }
 
+// Sum over each group of 8 consecutive lanes, left in every lane of the group, with DPP
+// adds (no LDS traffic): partners lane ^ 1 and lane ^ 2 (quad permutes), then the other
+// quad of the group (row_half_mirror: lane 7 - i), whose lanes all hold that quad's sum.
+// Each lane gets the same value as from shuffles with xor 1, 2, 4 (additions commute).
+template <int CTRL> __device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float group8_sum(float v) {
+  static_assert(LPR == 8, "groups of 8 lanes");
+  v += dpp_f<0xB1>(v);   // quad_perm [1, 0, 3, 2]
+  v += dpp_f<0x4E>(v);   // quad_perm [2, 3, 0, 1]
+  v += dpp_f<0x141>(v);  // row_half_mirror
+  return v;
+}
+
 // ---- gated up-dot over slice-major W_up^T (Alg. 2's u, split over d) --------------------
 // Copies of the per-entry sums: one per slice of the XCD when the token block is smaller
 // than the number of waves (decode), else one.
@@ -360,8 +383,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gated_updot(
           sacc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, xw), __builtin_bit_cast(bf16x2_t, ww),
                                                  sacc, false);
         }
-#pragma unroll
-        for (int o = 1; o < LPR; o <<= 1) sacc += __shfl_xor(sacc, o, 64);
+        sacc = group8_sum(sacc);
         const int e = q + u * NGRP + grp;
         if (sub == 0 && e < nnz) ur[e] += sacc;
       }
