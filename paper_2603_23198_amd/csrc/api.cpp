@@ -95,6 +95,9 @@ sfl_status_t check_forward(const sfl_ffn_args_t* a, bool need_output = true) {
   const int64_t lim = (int64_t)1 << 31;
   const int64_t es = a->dtype == SFL_BF16 ? 2 : 4;
   if (a->T * a->d * es >= lim || a->d * a->f * es >= lim || a->T * a->f * es >= lim) return SFL_E_UNSUPPORTED;
+  // the fused TwELL epilogue stores its slabs with 32-bit byte offsets
+  if (a->dtype == SFL_BF16 && a->T * cdiv(a->f, a->cfg.tile_cols) * a->cfg.tile_slots * 2 >= lim)
+    return SFL_E_UNSUPPORTED;
   return SFL_OK;
 }
 

@@ -495,10 +495,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_unit
             acc[2 * j + 1] = fmaf(v[u], bf16hi(ww), acc[2 * j + 1]);
           }
       }
-#pragma unroll
-      for (int o = LPR; o < 64; o <<= 1)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], o, 64);
+      fold_groups(acc);
     }
     if (grp == 0) {
       float* o = out + n * d + (int64_t)slice * SLICE2 + sub * 8;

@@ -215,27 +215,27 @@ struct WaveTile {
   typedef acc_t Acc[TM_][TN_];
 };
 
-// TwELL epilogue (Alg. 1), straight from the accumulators: z = acc + bias + shift; per
-// register, a ballot of the active lanes masked to the lane's group gives one row's active
-// columns, and mbcnt of it the slot of each (ascending column order). A TwELL tile wider
-// than a wave's columns continues in the next wave(s) along N: each wave first publishes
-// its per-row active counts in LDS and starts from the sum of the counts of the waves left
-// of it in the same tile. Active means z > 0 and not NaN on the fp32 value.
+// TwELL epilogue (Alg. 1), straight from the accumulators: z = (acc + bias) + shift, and a
+// column is active when z > 0 (NaN never is). Per accumulator register, the ballot of the
+// test gives the active lanes; the lane's group (GL lanes) holds GL consecutive columns of
+// one row, so the group's ballot bits below the lane give the entry's slot after those
+// already written for the row (ascending column order). Columns past N take a bias of
+// -inf, which keeps them inactive. A TwELL tile wider than a wave's columns continues in
+// the next wave(s) along N: those waves take turns, left to right, between block
+// barriers, each handing the next its per-row running counts through LDS. Entries go out
+// through buffer stores whose offsets are 32-bit; rows past m_eff get an offset beyond
+// the buffer, which drops their stores.
 template <int WM_, int WN_, int FM, int Tn>
-__device__ __forceinline__ void twell_epilogue(const GemmParams& p, const typename WaveTile<WM_, WN_, FM>::Acc& acc,
-                                               int m0, int n0, int m_eff, bf16_t* smem) {
+__device__ __forceinline__ void twell_epilogue(const GemmParams& p, typename WaveTile<WM_, WN_, FM>::Acc& acc,
+                                               int wm, int wn, int m0, int n0, int m_eff, bf16_t* smem) {
   static_assert(Tn == 64 || Tn == 128 || Tn == 256, "TwELL tile width");
   typedef WaveTile<WM_, WN_, FM> W;
   typedef AccGeo<FM> G;
   constexpr int NT_ = WM_ * WN_ * 64;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave / WN_, wn = wave % WN_;
-  const uint64_t gmask = G::group(lane);
-  const bool leader = (lane % G::GL) == 0;
-  float* sh_lds = (float*)smem;              // [BM] row shifts of the tile
-  int* cnt_lds = (int*)smem + BM;            // [WN_][BM] per-wave row counts
+  float* sh_lds = (float*)smem;    // [BM] row shifts of the tile
+  int* cnt_lds = (int*)smem + BM;  // [WN_][BM] running row counts handed along N
   for (int r = tid; r < BM; r += NT_) {
     const int g = m0 + r;
     float s = 0.f;
@@ -245,36 +245,25 @@ __device__ __forceinline__ void twell_epilogue(const GemmParams& p, const typena
   __syncthreads();
   const int S = p.tile_slots, NT = p.n_tiles;
   const int wcol0 = n0 + wn * W::WTN_;  // first column of this wave
-  float bj[W::TN_];
-  bool cok[W::TN_];
 #pragma unroll
   for (int j = 0; j < W::TN_; ++j) {
     const int gc = wcol0 + j * FM + G::col(lane);
-    cok[j] = gc < p.N;
-    bj[j] = (p.bias && cok[j]) ? p.bias[gc] : 0.f;
-  }
-  constexpr bool spans = Tn > W::WTN_;  // tiles then start on wave boundaries
-  if constexpr (spans) {
+    const float bj = gc < p.N ? (p.bias ? p.bias[gc] : 0.f) : -__builtin_inff();
 #pragma unroll
     for (int i = 0; i < W::TM_; ++i)
 #pragma unroll
-      for (int r = 0; r < G::R; ++r) {
-        const int lrow = wm * W::WTM_ + i * FM + G::row(r, lane);
-        const float sh = sh_lds[lrow];
-        int c = 0;
-#pragma unroll
-        for (int j = 0; j < W::TN_; ++j) {
-          const bool act = cok[j] & active_bits((acc[i][j][r] + bj[j]) + sh);
-          c += __popcll(ballot(act) & gmask);
-        }
-        if (leader) cnt_lds[wn * BM + lrow] = c;
-      }
+      for (int r = 0; r < G::R; ++r)
+        acc[i][j][r] = (acc[i][j][r] + bj) + sh_lds[wm * W::WTM_ + i * FM + G::row(r, lane)];
   }
-  __syncthreads();
-  constexpr int wpt = spans ? Tn / W::WTN_ : 1;  // waves per TwELL tile
-  const int first_w = wn - wn % wpt;
-  const bool last_w = wn % wpt == wpt - 1;
-  const int jt0 = wcol0 / Tn;  // TwELL tile of the wave's first column
+  constexpr bool spans = Tn > W::WTN_;               // tiles then start on wave boundaries
+  constexpr int wpt = spans ? Tn / W::WTN_ : 1;      // waves per TwELL tile, taking turns
+  const int turn = wn % wpt;
+  const int jt0 = wcol0 / Tn;                        // TwELL tile of the wave's first column
+  const int gsh = lane & ~(G::GL - 1);               // the group's first lane
+  const uint32_t gbits = G::GL == 32 ? ~0u : (1u << G::GL) - 1u;
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(p.tw_val, (int64_t)m_eff * NT * S * 2);
+  const __amdgpu_buffer_rsrc_t ri = make_rsrc(p.tw_idx, (int64_t)m_eff * NT * S * 2);
+  for (int t = 0; t < turn; ++t) __syncthreads();  // the waves left of this one go first
 #pragma unroll
   for (int i = 0; i < W::TM_; ++i)
 #pragma unroll
@@ -282,42 +271,41 @@ __device__ __forceinline__ void twell_epilogue(const GemmParams& p, const typena
       const int lrow = wm * W::WTM_ + i * FM + G::row(r, lane);
       const int grow = m0 + lrow;
       const bool rok = grow < m_eff;
-      const float sh = sh_lds[lrow];
-      int run = 0;
-      for (int w = first_w; w < wn; ++w) run += cnt_lds[w * BM + lrow];
-      bf16_t* vrow = (bf16_t*)p.tw_val + (int64_t)grow * NT * S;
-      uint16_t* irow = p.tw_idx + (int64_t)grow * NT * S;
-      int32_t* crow = p.tw_cnt + (int64_t)grow * NT;
+      const uint32_t rowoff = rok ? (uint32_t)grow * (uint32_t)(NT * S * 2) : kOOB;
+      int run = turn ? cnt_lds[(wn - 1) * BM + lrow] : 0;
 #pragma unroll
       for (int j = 0; j < W::TN_; ++j) {
         if (!spans && (j * FM) % Tn == 0) run = 0;  // wave starts are tile-aligned
-        const int gc = wcol0 + j * FM + G::col(lane);
-        const float z = (acc[i][j][r] + bj[j]) + sh;
-        const bool act = cok[j] & active_bits(z);
-        const uint64_t m = ballot(act) & gmask;
-        const int slot = run + mbcnt(m);
         const int jt = jt0 + (spans ? 0 : (j * FM) / Tn);
-        if (act && rok && slot < S) {
-          vrow[jt * S + slot] = f32_to_bf16_finite(z);
-          irow[jt * S + slot] = (uint16_t)gc;
+        const float z = acc[i][j][r];
+        const bool act = __builtin_amdgcn_classf(z, 0x380);  // +subnormal, +normal, +inf
+        const uint64_t b = ballot(act);
+        if (b) {
+          const uint32_t x = (uint32_t)(b >> gsh) & gbits;
+          const int slot = run + __popc(x & ((1u << (lane & (G::GL - 1))) - 1u));
+          if (act && slot < S) {
+            const uint32_t off = rowoff + (uint32_t)(jt * S + slot) * 2u;
+            __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_finite(z), rv, off, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(wcol0 + j * FM + G::col(lane)), ri, off, 0, 0);
+          }
+          run += __popc(x);
         }
-        run += __popcll(m);
-        const bool tend = spans ? (last_w && j == W::TN_ - 1) : ((j * FM + FM) % Tn == 0);
-        if (tend && leader && rok && jt * Tn < p.N) crow[jt] = run;
+        const bool tend = spans ? (turn == wpt - 1 && j == W::TN_ - 1) : ((j * FM + FM) % Tn == 0);
+        if (tend && (lane % G::GL) == 0 && rok && jt * Tn < p.N) p.tw_cnt[(int64_t)grow * NT + jt] = run;
       }
+      if (spans && turn < wpt - 1) cnt_lds[wn * BM + lrow] = run;
     }
+  for (int t = turn + 1; t < wpt; ++t) __syncthreads();  // then those right of it
 }
 
 template <int EPI, int WM_, int WN_, int FM, int Tn>
-__device__ __forceinline__ void gemm_epilogue(const GemmParams& p, const typename WaveTile<WM_, WN_, FM>::Acc& acc,
-                                              int m0, int n0, int m_eff, bf16_t* smem) {
+__device__ __forceinline__ void gemm_epilogue(const GemmParams& p, typename WaveTile<WM_, WN_, FM>::Acc& acc,
+                                              int wm, int wn, int m0, int n0, int m_eff, bf16_t* smem) {
   typedef WaveTile<WM_, WN_, FM> W;
   typedef AccGeo<FM> G;
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int wm = wave / WN_, wn = wave % WN_;
   if constexpr (EPI == EPI_TWELL) {
-    twell_epilogue<WM_, WN_, FM, Tn>(p, acc, m0, n0, m_eff, smem);
+    twell_epilogue<WM_, WN_, FM, Tn>(p, acc, wm, wn, m0, n0, m_eff, smem);
   } else {
 #pragma unroll
     for (int i = 0; i < W::TM_; ++i) {
@@ -364,8 +352,10 @@ __global__ __launch_bounds__(NTHR) void k_gemm_bf16(GemmParams p) {
   __shared__ __attribute__((aligned(16))) bf16_t smem[2 * LDS_STAGE];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // wave (wm, wn) = (wave % WAVES_M, wave / WAVES_M): the waves of one column of the tile
+  // sit on different SIMDs (the TwELL epilogue runs one column of waves at a time)
+  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
 
   const int tiles_m = (int)cdiv(p.M, BM), tiles_n = (int)cdiv(p.N, BN);
   int tm, tn;
@@ -430,7 +420,7 @@ __global__ __launch_bounds__(NTHR) void k_gemm_bf16(GemmParams p) {
     __syncthreads();
   }
 
-  gemm_epilogue<EPI, WAVES_M, WAVES_N, 32, Tn>(p, acc, m0, n0, m_eff, smem);
+  gemm_epilogue<EPI, WAVES_M, WAVES_N, 32, Tn>(p, acc, wm, wn, m0, n0, m_eff, smem);
 }
 
 // ---- K-contiguous x K-contiguous GEMM: direct global -> LDS loads, 16x16x32 MFMAs -------
@@ -508,8 +498,10 @@ __device__ __forceinline__ void kc_tile(const GemmParams& p, int tm, int tn, int
   typedef WaveTile<KC_WM, KC_WN, KC_FM> W;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm = wave / KC_WN, wn = wave % KC_WN;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // wave (wm, wn) = (wave % KC_WM, wave / KC_WM): each SIMD holds one wave of each
+  // column of the tile (the TwELL epilogue runs one column of waves at a time)
+  const int wm = wave % KC_WM, wn = wave / KC_WM;
   const int m0 = tm * BM, n0 = tn * BN;
   const int nk_all = (int)(p.K / KC_BK);
   const int kt0 = (int)((int64_t)nk_all * split / ks);
@@ -637,7 +629,7 @@ __device__ __forceinline__ void kc_tile(const GemmParams& p, int tm, int tn, int
       }
     return;
   }
-  gemm_epilogue<EPI, KC_WM, KC_WN, KC_FM, Tn>(p, acc, m0, n0, m_eff, smem);
+  gemm_epilogue<EPI, KC_WM, KC_WN, KC_FM, Tn>(p, acc, wm, wn, m0, n0, m_eff, smem);
 }
 
 template <int EPI, int Tn, int BL>
