@@ -172,9 +172,9 @@ template <int ROWS> struct LoaderSel<LAY_RCG, ROWS> { typedef LoadRC<ROWS, true>
 // Output-tile order: consecutive workgroup ids are dispatched round-robin over the 8 XCDs;
 // remap so that each XCD gets a contiguous range of logical tiles, then walk that range
 // in groups of 8 tile-rows so neighbouring workgroups share A rows and B columns in L2.
-__device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
+__device__ __forceinline__ void tile_coords(int id, int tiles_m, int tiles_n, int& tm, int& tn) {
   const int nwg = tiles_m * tiles_n;
-  int g = blockIdx.x;
+  int g = id;
   if ((nwg & 7) == 0) g = (g & 7) * (nwg >> 3) + (g >> 3);
   constexpr int GM = 8;
   const int group = g / (GM * tiles_n);
@@ -215,27 +215,29 @@ struct WaveTile {
   typedef acc_t Acc[TM_][TN_];
 };
 
-// TwELL epilogue (Alg. 1), straight from the accumulators: z = (acc + bias) + shift, and a
-// column is active when z > 0 (NaN never is). Per accumulator register, the ballot of the
-// test gives the active lanes; the lane's group (GL lanes) holds GL consecutive columns of
-// one row, so the group's ballot bits below the lane give the entry's slot after those
-// already written for the row (ascending column order). Columns past N take a bias of
-// -inf, which keeps them inactive. A TwELL tile wider than a wave's columns continues in
-// the next wave(s) along N: those waves take turns, left to right, between block
-// barriers, each handing the next its per-row running counts through LDS. Entries go out
-// through buffer stores whose offsets are 32-bit; rows past m_eff get an offset beyond
-// the buffer, which drops their stores.
-template <int WM_, int WN_, int FM, int Tn>
-__device__ __forceinline__ void twell_epilogue(const GemmParams& p, typename WaveTile<WM_, WN_, FM>::Acc& acc,
-                                               int wm, int wn, int m0, int n0, int m_eff, bf16_t* smem) {
-  static_assert(Tn == 64 || Tn == 128 || Tn == 256, "TwELL tile width");
+// TwELL epilogue (Alg. 1), straight from the accumulators, in two parts. First the
+// pre-activations in place: z = (acc + bias) + shift, where columns past N take a bias of
+// -inf, which keeps them inactive. Then the compaction: a column is active when z > 0 (NaN
+// never is). Per accumulator register, the ballot of the test gives the active lanes; the
+// lane's group (GL lanes) holds GL consecutive columns of one row, so the group's ballot
+// bits below the lane give the entry's slot after those already written for the row
+// (ascending column order). A TwELL tile wider than a wave's columns continues in the next
+// wave(s) along N: every wave of such a tile but the last first counts its active columns
+// per row and publishes the counts in LDS; after one block barrier each wave starts its
+// rows from the counts of the waves left of it. Entries go out through buffer stores
+// whose offsets are 32-bit; an offset beyond the buffer (inactive lanes, rows past m_eff)
+// drops the store.
+
+// z in place, with the row shifts staged through LDS (smem[0 .. BM) floats).
+template <int WM_, int WN_, int FM>
+__device__ __forceinline__ void twell_z_lds(const GemmParams& p, typename WaveTile<WM_, WN_, FM>::Acc& acc, int wm,
+                                            int wn, int m0, int n0, int m_eff, bf16_t* smem) {
   typedef WaveTile<WM_, WN_, FM> W;
   typedef AccGeo<FM> G;
   constexpr int NT_ = WM_ * WN_ * 64;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  float* sh_lds = (float*)smem;    // [BM] row shifts of the tile
-  int* cnt_lds = (int*)smem + BM;  // [WN_][BM] running row counts handed along N
+  float* sh_lds = (float*)smem;
   for (int r = tid; r < BM; r += NT_) {
     const int g = m0 + r;
     float s = 0.f;
@@ -243,8 +245,7 @@ __device__ __forceinline__ void twell_epilogue(const GemmParams& p, typename Wav
     sh_lds[r] = s;
   }
   __syncthreads();
-  const int S = p.tile_slots, NT = p.n_tiles;
-  const int wcol0 = n0 + wn * W::WTN_;  // first column of this wave
+  const int wcol0 = n0 + wn * W::WTN_;
 #pragma unroll
   for (int j = 0; j < W::TN_; ++j) {
     const int gc = wcol0 + j * FM + G::col(lane);
@@ -255,15 +256,50 @@ __device__ __forceinline__ void twell_epilogue(const GemmParams& p, typename Wav
       for (int r = 0; r < G::R; ++r)
         acc[i][j][r] = (acc[i][j][r] + bj) + sh_lds[wm * W::WTM_ + i * FM + G::row(r, lane)];
   }
+}
+
+// The compaction pass over z; cnt_lds holds WN_ x BM ints of block scratch.
+template <int WM_, int WN_, int FM, int Tn>
+__device__ __forceinline__ void twell_compact(const GemmParams& p, typename WaveTile<WM_, WN_, FM>::Acc& acc,
+                                              int wm, int wn, int m0, int n0, int m_eff, int* cnt_lds) {
+  static_assert(Tn == 64 || Tn == 128 || Tn == 256, "TwELL tile width");
+  typedef WaveTile<WM_, WN_, FM> W;
+  typedef AccGeo<FM> G;
+  const int lane = threadIdx.x & 63;
+  const int S = p.tile_slots, NT = p.n_tiles;
+  const int wcol0 = n0 + wn * W::WTN_;               // first column of this wave
   constexpr bool spans = Tn > W::WTN_;               // tiles then start on wave boundaries
   constexpr int wpt = spans ? Tn / W::WTN_ : 1;      // waves per TwELL tile, taking turns
-  const int turn = wn % wpt;
+  const int turn = wn % wpt;                         // position of the wave in its TwELL tile
   const int jt0 = wcol0 / Tn;                        // TwELL tile of the wave's first column
   const int gsh = lane & ~(G::GL - 1);               // the group's first lane
   const uint32_t gbits = G::GL == 32 ? ~0u : (1u << G::GL) - 1u;
+  const uint32_t below = (1u << (lane & (G::GL - 1))) - 1u;
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(p.tw_val, (int64_t)m_eff * NT * S * 2);
   const __amdgpu_buffer_rsrc_t ri = make_rsrc(p.tw_idx, (int64_t)m_eff * NT * S * 2);
-  for (int t = 0; t < turn; ++t) __syncthreads();  // the waves left of this one go first
+  if constexpr (spans) {
+    if (turn < wpt - 1) {
+#pragma unroll
+      for (int i = 0; i < W::TM_; ++i)
+#pragma unroll
+        for (int r = 0; r < G::R; ++r) {
+          int c = 0;
+#pragma unroll
+          for (int j = 0; j < W::TN_; ++j) {
+            const uint64_t b = ballot(__builtin_amdgcn_classf(acc[i][j][r], 0x380));
+            c += __popc((uint32_t)(b >> gsh) & gbits);
+          }
+          cnt_lds[wn * BM + wm * W::WTM_ + i * FM + G::row(r, lane)] = c;
+        }
+      // The store pass tests z again: keep the compiler from carrying all the ballots of
+      // this pass over to it (they would not fit in scalar registers).
+#pragma unroll
+      for (int i = 0; i < W::TM_; ++i)
+#pragma unroll
+        for (int j = 0; j < W::TN_; ++j) asm volatile("" : "+v"(acc[i][j]));
+    }
+    __syncthreads();
+  }
 #pragma unroll
   for (int i = 0; i < W::TM_; ++i)
 #pragma unroll
@@ -272,7 +308,9 @@ __device__ __forceinline__ void twell_epilogue(const GemmParams& p, typename Wav
       const int grow = m0 + lrow;
       const bool rok = grow < m_eff;
       const uint32_t rowoff = rok ? (uint32_t)grow * (uint32_t)(NT * S * 2) : kOOB;
-      int run = turn ? cnt_lds[(wn - 1) * BM + lrow] : 0;
+      int run = 0;
+      if constexpr (spans)
+        for (int w = wn - turn; w < wn; ++w) run += cnt_lds[w * BM + lrow];
 #pragma unroll
       for (int j = 0; j < W::TN_; ++j) {
         if (!spans && (j * FM) % Tn == 0) run = 0;  // wave starts are tile-aligned
@@ -282,20 +320,16 @@ __device__ __forceinline__ void twell_epilogue(const GemmParams& p, typename Wav
         const uint64_t b = ballot(act);
         if (b) {
           const uint32_t x = (uint32_t)(b >> gsh) & gbits;
-          const int slot = run + __popc(x & ((1u << (lane & (G::GL - 1))) - 1u));
-          if (act && slot < S) {
-            const uint32_t off = rowoff + (uint32_t)(jt * S + slot) * 2u;
-            __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_finite(z), rv, off, 0, 0);
-            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(wcol0 + j * FM + G::col(lane)), ri, off, 0, 0);
-          }
+          const int slot = run + __popc(x & below);
+          const uint32_t off = (act && slot < S) ? rowoff + (uint32_t)(jt * S + slot) * 2u : kOOB;
+          __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_finite(z), rv, off, 0, 0);
+          __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(wcol0 + j * FM + G::col(lane)), ri, off, 0, 0);
           run += __popc(x);
         }
         const bool tend = spans ? (turn == wpt - 1 && j == W::TN_ - 1) : ((j * FM + FM) % Tn == 0);
         if (tend && (lane % G::GL) == 0 && rok && jt * Tn < p.N) p.tw_cnt[(int64_t)grow * NT + jt] = run;
       }
-      if (spans && turn < wpt - 1) cnt_lds[wn * BM + lrow] = run;
     }
-  for (int t = turn + 1; t < wpt; ++t) __syncthreads();  // then those right of it
 }
 
 template <int EPI, int WM_, int WN_, int FM, int Tn>
@@ -305,7 +339,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, typename Wave
   typedef AccGeo<FM> G;
   const int lane = threadIdx.x & 63;
   if constexpr (EPI == EPI_TWELL) {
-    twell_epilogue<WM_, WN_, FM, Tn>(p, acc, wm, wn, m0, n0, m_eff, smem);
+    twell_z_lds<WM_, WN_, FM>(p, acc, wm, wn, m0, n0, m_eff, smem);
+    twell_compact<WM_, WN_, FM, Tn>(p, acc, wm, wn, m0, n0, m_eff, (int*)smem + BM);
   } else {
 #pragma unroll
     for (int i = 0; i < W::TM_; ++i) {
@@ -359,7 +394,7 @@ __global__ __launch_bounds__(NTHR) void k_gemm_bf16(GemmParams p) {
 
   const int tiles_m = (int)cdiv(p.M, BM), tiles_n = (int)cdiv(p.N, BN);
   int tm, tn;
-  tile_coords(tiles_m, tiles_n, tm, tn);
+  tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
   if (m0 >= m_eff) return;
@@ -491,48 +526,54 @@ __device__ __forceinline__ int rc_seg(int row, int seg) { return seg ^ (row & 7)
 typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 
-template <int EPI, int Tn, bool SPLIT, int BL>
-__device__ __forceinline__ void kc_tile(const GemmParams& p, int tm, int tn, int split, int ks, int m_eff,
-                                        bf16_t* smem) {
+// Operand staging and MFMA steps of the direct-to-LDS GEMM for one wave: the per-lane
+// source offsets of a 256 x 256 output tile, the loads of one 64-k stage into a stage
+// buffer, and the MFMAs over a stage.
+template <int BL>
+struct KcOps {
   static_assert(BL == LAY_KC || BL == LAY_RC, "B layout");
   typedef WaveTile<KC_WM, KC_WN, KC_FM> W;
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  // wave (wm, wn) = (wave % KC_WM, wave / KC_WM): each SIMD holds one wave of each
-  // column of the tile (the TwELL epilogue runs one column of waves at a time)
-  const int wm = wave % KC_WM, wn = wave / KC_WM;
-  const int m0 = tm * BM, n0 = tn * BN;
-  const int nk_all = (int)(p.K / KC_BK);
-  const int kt0 = (int)((int64_t)nk_all * split / ks);
-  const int kt1 = (int)((int64_t)nk_all * (split + 1) / ks);
+  int lane, wave, wm, wn;
+  u32x4_t ra, rb;
+  uint32_t offa[KC_LOADS], offb[KC_LOADS];
+
+  __device__ __forceinline__ explicit KcOps(const GemmParams& p) {
+    lane = threadIdx.x & 63;
+    wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    // wave (wm, wn) = (wave % KC_WM, wave / KC_WM): each SIMD holds one wave of each
+    // column of the tile (the TwELL epilogue runs one column of waves at a time)
+    wm = wave % KC_WM;
+    wn = wave / KC_WM;
+    ra = rsrc_words(p.A, p.a_bytes);
+    rb = rsrc_words(p.B, p.b_bytes);
+  }
 
   // Load instruction q of this wave fills rows (wave*KC_LOADS + q)*8 .. +7 of the operand
   // tile; lane l writes row +l/8 at chunk position l%8, which holds logical chunk
   // kc_swz(row, l%8).
-  const u32x4_t ra = rsrc_words(p.A, p.a_bytes);
-  const u32x4_t rb = rsrc_words(p.B, p.b_bytes);
-  uint32_t offa[KC_LOADS], offb[KC_LOADS];
+  __device__ __forceinline__ void setup(const GemmParams& p, int m0, int n0, int m_eff) {
 #pragma unroll
-  for (int q = 0; q < KC_LOADS; ++q) {
-    const int row = (wave * KC_LOADS + q) * 8 + (lane >> 3);
-    const int c = kc_swz(row, lane & 7);
-    const int ga = m0 + row;
-    const int64_t sa = ga < m_eff ? (p.a_rows ? (int64_t)p.a_rows[ga] : (int64_t)ga) : -1;
-    offa[q] = sa >= 0 ? (uint32_t)((sa * p.lda + c * 8) * 2) : kOOB;
-    if constexpr (BL == LAY_KC) {
-      const int gb = n0 + row;
-      offb[q] = gb < p.N ? (uint32_t)(((int64_t)gb * p.ldb + c * 8) * 2) : kOOB;
-    } else {
-      // k row kr of the stage, 16-byte chunk position lane%32 holding logical chunk cb
-      const int kr = (wave * KC_LOADS + q) * 2 + (lane >> 5);
-      const int cb = 2 * rc_seg(kr, (lane & 31) >> 1) + (lane & 1);
-      const int gn = n0 + cb * 8;
-      offb[q] = gn < p.N ? (uint32_t)(((int64_t)kr * p.ldb + gn) * 2) : kOOB;
+    for (int q = 0; q < KC_LOADS; ++q) {
+      const int row = (wave * KC_LOADS + q) * 8 + (lane >> 3);
+      const int c = kc_swz(row, lane & 7);
+      const int ga = m0 + row;
+      const int64_t sa = ga < m_eff ? (p.a_rows ? (int64_t)p.a_rows[ga] : (int64_t)ga) : -1;
+      offa[q] = sa >= 0 ? (uint32_t)((sa * p.lda + c * 8) * 2) : kOOB;
+      if constexpr (BL == LAY_KC) {
+        const int gb = n0 + row;
+        offb[q] = gb < p.N ? (uint32_t)(((int64_t)gb * p.ldb + c * 8) * 2) : kOOB;
+      } else {
+        // k row kr of the stage, 16-byte chunk position lane%32 holding logical chunk cb
+        const int kr = (wave * KC_LOADS + q) * 2 + (lane >> 5);
+        const int cb = 2 * rc_seg(kr, (lane & 31) >> 1) + (lane & 1);
+        const int gn = n0 + cb * 8;
+        offb[q] = gn < p.N ? (uint32_t)(((int64_t)kr * p.ldb + gn) * 2) : kOOB;
+      }
     }
   }
-  auto issue = [&](int kt) {
-    bf16_t* st = smem + (kt & 1) * KC_STAGE;
+
+  // k step kt of the tile into stage buffer st
+  __device__ __forceinline__ void issue(const GemmParams& p, bf16_t* st, int kt) const {
     const uint32_t soa = (uint32_t)(kt * KC_BK * 2);
     const uint32_t sob = BL == LAY_KC ? soa : (uint32_t)((int64_t)kt * KC_BK * p.ldb * 2);
 #pragma unroll
@@ -543,22 +584,13 @@ __device__ __forceinline__ void kc_tile(const GemmParams& p, int tm, int tn, int
       load_lds16(ra, __builtin_amdgcn_readfirstlane(la), offa[q], soa);
       load_lds16(rb, __builtin_amdgcn_readfirstlane(lb), offb[q], sob);
     }
-  };
-
-  typename W::Acc acc;
-#pragma unroll
-  for (int i = 0; i < W::TM_; ++i)
-#pragma unroll
-    for (int j = 0; j < W::TN_; ++j)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) acc[i][j][r] = 0.f;
+  }
 
   // 16x16x32 operands: lane l supplies row (or column) l%16 at k 8*(l/16) .. +7
-  const int arow = wm * W::WTM_ + (lane & 15);
-  const int brow = wn * W::WTN_ + (lane & 15);
-  auto compute = [&](int kt) {
-    const bf16_t* As = smem + (kt & 1) * KC_STAGE;
+  __device__ __forceinline__ void compute(const bf16_t* As, typename W::Acc& acc) const {
     const bf16_t* Bs = As + KC_OPER;
+    const int arow = wm * W::WTM_ + (lane & 15);
+    const int brow = wn * W::WTN_ + (lane & 15);
 #pragma unroll
     for (int ks = 0; ks < KC_BK / 32; ++ks) {
       const int c = ks * 4 + (lane >> 4);
@@ -599,48 +631,169 @@ __device__ __forceinline__ void kc_tile(const GemmParams& p, int tm, int tn, int
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
       __builtin_amdgcn_s_setprio(0);
     }
-  };
-  // Each step: this wave's loads of stage kt have landed and its LDS reads of step kt-1
-  // are complete (vmcnt 0, lgkmcnt 0); after the barrier the same holds for all waves, so
-  // stage kt may be read and the slot of stage kt-1 refilled with stage kt+1.
-  if (kt0 < kt1) issue(kt0);
-  for (int kt = kt0; kt < kt1; ++kt) {
-    __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt(0) expcnt(7) lgkmcnt(0)
-    __syncthreads();
-    if (kt + 1 < kt1) issue(kt + 1);
-    compute(kt);
   }
+
+  // Stages kt_begin .. kt_end-1 of the tile; stage kt sits in buffer (b0 + kt - kt_begin) & 1
+  // and stage kt_begin has been issued. Each step: this wave's loads of stage kt have
+  // landed and its LDS reads of step kt-1 are complete (vmcnt 0, lgkmcnt 0); after the
+  // barrier the same holds for all waves, so stage kt may be read and the buffer of stage
+  // kt-1 refilled with stage kt+1.
+  __device__ __forceinline__ void run(const GemmParams& p, bf16_t* smem, int b0, int kt_begin, int kt_end,
+                                      typename W::Acc& acc) const {
+#pragma unroll
+    for (int i = 0; i < W::TM_; ++i)
+#pragma unroll
+      for (int j = 0; j < W::TN_; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[i][j][r] = 0.f;
+    for (int kt = kt_begin; kt < kt_end; ++kt) {
+      __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt(0) expcnt(7) lgkmcnt(0)
+      __syncthreads();
+      const int bi = (b0 + kt - kt_begin) & 1;
+      if (kt + 1 < kt_end) issue(p, smem + (bi ^ 1) * KC_STAGE, kt + 1);
+      compute(smem + bi * KC_STAGE, acc);
+    }
+  }
+};
+
+// One output tile (tm, tn) over the K steps of split `split` of ks; with ks > 1 it stores
+// the fp32 partial sums of its K range, otherwise the epilogue runs. Called by every thread.
+template <int EPI, int BL>
+__device__ __forceinline__ void kc_tile(const GemmParams& p, int tm, int tn, int split, int ks, int m_eff,
+                                        bf16_t* smem) {
+  typedef WaveTile<KC_WM, KC_WN, KC_FM> W;
+  typedef AccGeo<KC_FM> G;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int nk_all = (int)(p.K / KC_BK);
+  const int kt0 = (int)((int64_t)nk_all * split / ks);
+  const int kt1 = (int)((int64_t)nk_all * (split + 1) / ks);
+  KcOps<BL> op(p);
+  op.setup(p, m0, n0, m_eff);
+  if (kt0 < kt1) op.issue(p, smem, kt0);
+  typename W::Acc acc;
+  op.run(p, smem, 0, kt0, kt1, acc);
   __syncthreads();  // the epilogue reuses the stage buffers
-  if (SPLIT && ks > 1) {
+  if (ks > 1) {
     // partial sums of this K range: part[split][row][col], rows in gathered order
-    typedef AccGeo<KC_FM> G;
 #pragma unroll
     for (int i = 0; i < W::TM_; ++i)
 #pragma unroll
       for (int r = 0; r < G::R; ++r) {
-        const int row = m0 + wm * W::WTM_ + i * KC_FM + G::row(r, lane);
+        const int row = m0 + op.wm * W::WTM_ + i * KC_FM + G::row(r, op.lane);
         if (row >= m_eff) continue;
         float* prow = p.part + ((int64_t)split * m_eff + row) * p.N;
 #pragma unroll
         for (int j = 0; j < W::TN_; ++j) {
-          const int col = n0 + wn * W::WTN_ + j * KC_FM + G::col(lane);
+          const int col = n0 + op.wn * W::WTN_ + j * KC_FM + G::col(op.lane);
           if (col < p.N) prow[col] = acc[i][j][r];
         }
       }
     return;
   }
-  gemm_epilogue<EPI, KC_WM, KC_WN, KC_FM, Tn>(p, acc, wm, wn, m0, n0, m_eff, smem);
+  gemm_epilogue<EPI, KC_WM, KC_WN, KC_FM, 0>(p, acc, op.wm, op.wn, m0, n0, m_eff, smem);
 }
 
+// TwELL epilogue inputs of one tile held in registers: the shift of row wm*64 + lane and
+// the bias of columns wcol0 + lane and wcol0 + 64 + lane (-inf past N). Lanes fetch the
+// values of their accumulator rows and columns from these with lane permutes.
+struct KcTwPre {
+  float sh, b0, b1;
+  __device__ __forceinline__ void load(const GemmParams& p, int wm, int wn, int lane, int m0, int n0, int m_eff) {
+    typedef WaveTile<KC_WM, KC_WN, KC_FM> W;
+    const int g = m0 + wm * W::WTM_ + lane;
+    sh = (p.shift && g < m_eff) ? p.shift[p.s_rows ? p.s_rows[g] : g] : 0.f;
+    const int c0 = n0 + wn * W::WTN_ + lane, c1 = c0 + 64;
+    b0 = c0 < p.N ? (p.bias ? p.bias[c0] : 0.f) : -__builtin_inff();
+    b1 = c1 < p.N ? (p.bias ? p.bias[c1] : 0.f) : -__builtin_inff();
+  }
+  // z = (acc + bias) + shift in place
+  __device__ __forceinline__ void apply(WaveTile<KC_WM, KC_WN, KC_FM>::Acc& acc, int lane) const {
+    typedef WaveTile<KC_WM, KC_WN, KC_FM> W;
+    typedef AccGeo<KC_FM> G;
+    static_assert(W::WTM_ == 64 && W::WTN_ == 128, "one shift and two bias values per lane");
+    float shv[W::TM_][G::R];
+#pragma unroll
+    for (int i = 0; i < W::TM_; ++i)
+#pragma unroll
+      for (int r = 0; r < G::R; ++r) shv[i][r] = __shfl(sh, i * KC_FM + G::row(r, lane));
+#pragma unroll
+    for (int j = 0; j < W::TN_; ++j) {
+      const float bj = __shfl(j < 4 ? b0 : b1, (j & 3) * KC_FM + G::col(lane));
+#pragma unroll
+      for (int i = 0; i < W::TM_; ++i)
+#pragma unroll
+        for (int r = 0; r < G::R; ++r) acc[i][j][r] = (acc[i][j][r] + bj) + shv[i][r];
+    }
+  }
+  // Makes the loaded values available here: their loads then complete before any loads
+  // issued after this point (the compiler does not count the stage loads, so a wait for
+  // these placed after a stage issue would also wait for that stage).
+  __device__ __forceinline__ void settle() const { asm volatile("" ::"v"(sh), "v"(b0), "v"(b1)); }
+};
+
+// Persistent blocks (one per CU) walk the output tiles in the XCD-aware order; while a
+// tile's epilogue runs, the first stage of the block's next tile is already loading
+// (into the stage buffer the epilogue does not use), and for the TwELL epilogue so are
+// the next tile's bias and shift values.
 template <int EPI, int Tn, int BL>
 __global__ __launch_bounds__(NTHR) void k_gemm_kc(GemmParams p) {
   __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * KC_STAGE];
+  typedef WaveTile<KC_WM, KC_WN, KC_FM> W;
   const int tiles_m = (int)cdiv(p.M, BM), tiles_n = (int)cdiv(p.N, BN);
-  int tm, tn;
-  tile_coords(tiles_m, tiles_n, tm, tn);
+  const int nt = tiles_m * tiles_n;
   const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
-  if (tm * BM >= m_eff) return;
-  kc_tile<EPI, Tn, false, BL>(p, tm, tn, 0, 1, m_eff, smem);
+  const int nk = (int)(p.K / KC_BK);
+  // the next tile of this block at or after v whose rows are counted
+  auto next_live = [&](int v, int& tm, int& tn) {
+    for (; v < nt; v += gridDim.x) {
+      tile_coords(v, tiles_m, tiles_n, tm, tn);
+      if (tm * BM < m_eff) break;
+    }
+    return v;
+  };
+  int tm, tn;
+  int v = next_live(blockIdx.x, tm, tn);
+  if (v >= nt) return;
+  KcOps<BL> op(p);
+  op.setup(p, tm * BM, tn * BN, m_eff);
+  if (nk > 0) op.issue(p, smem, 0);
+  KcTwPre pre;
+  if constexpr (EPI == EPI_TWELL) pre.load(p, op.wm, op.wn, op.lane, tm * BM, tn * BN, m_eff);
+  int b0 = 0;  // stage buffer of the tile's first k step
+  for (;;) {
+    typename W::Acc acc;
+    op.run(p, smem, b0, 0, nk, acc);
+    const int bl = (b0 + nk - 1) & 1;  // buffer of the last k step: the epilogue's scratch
+    const int m0 = tm * BM, n0 = tn * BN;
+    int tm2 = 0, tn2 = 0;
+    const int v2 = next_live(v + gridDim.x, tm2, tn2);
+    KcTwPre pre2;
+    if constexpr (EPI == EPI_TWELL) pre.settle();
+    if (v2 < nt) {
+      // before the stage issue, so that no wait of the compiler's (a gathered shift row)
+      // waits for the stage; the other buffer was last read in step nk-2, which every wave
+      // finished before the barrier of step nk-1
+      if constexpr (EPI == EPI_TWELL) pre2.load(p, op.wm, op.wn, op.lane, tm2 * BM, tn2 * BN, m_eff);
+      op.setup(p, tm2 * BM, tn2 * BN, m_eff);
+      if (nk > 0) op.issue(p, smem + (bl ^ 1) * KC_STAGE, 0);
+    }
+    __syncthreads();  // every wave is done reading buffer bl
+    bf16_t* scratch = smem + bl * KC_STAGE;
+    if constexpr (EPI == EPI_TWELL) {
+      pre.apply(acc, op.lane);
+      twell_compact<KC_WM, KC_WN, KC_FM, Tn>(p, acc, op.wm, op.wn, m0, n0, m_eff, (int*)scratch);
+    } else {
+      gemm_epilogue<EPI, KC_WM, KC_WN, KC_FM, Tn>(p, acc, op.wm, op.wn, m0, n0, m_eff, scratch);
+    }
+    if (v2 >= nt) break;
+    // the first barrier of the next tile's K loop orders this epilogue's scratch use before
+    // the refill of buffer bl
+    v = v2;
+    tm = tm2;
+    tn = tn2;
+    b0 = bl ^ 1;
+    if constexpr (EPI == EPI_TWELL) pre = pre2;
+  }
 }
 
 // Split-K GEMM: persistent blocks over the (tile, split) items of the counted rows, so
@@ -654,7 +807,7 @@ __global__ __launch_bounds__(NTHR) void k_gemm_kc_split(GemmParams p) {
   const int n_items = (int)cdiv(m_eff, BM) * tiles_n * ks;
   for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
     const int split = item % ks, t = item / ks;
-    kc_tile<EPI, 0, true, BL>(p, t / tiles_n, t % tiles_n, split, ks, m_eff, smem);
+    kc_tile<EPI, BL>(p, t / tiles_n, t % tiles_n, split, ks, m_eff, smem);
     __syncthreads();  // the next item refills the stage buffers
   }
 }
@@ -698,11 +851,26 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(GemmParams p) {
   }
 }
 
+// Compute units of the current device (cached per device).
+int device_cus() {
+  static int cus[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] <= 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
+
 template <int EPI, int Tn = 0, int BL = LAY_KC>
 hipError_t launch_kc(const GemmParams& p, hipStream_t s) {
-  const int tiles = (int)(cdiv(p.M, BM) * cdiv(p.N, BN));
+  const int64_t tiles = cdiv(p.M, BM) * cdiv(p.N, BN);
   if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL((k_gemm_kc<EPI, Tn, BL>), dim3(tiles), dim3(NTHR), 0, s, p);
+  // one persistent block per CU (the stage buffers allow one per CU)
+  const unsigned grid = (unsigned)std::min<int64_t>(tiles, device_cus());
+  hipLaunchKernelGGL((k_gemm_kc<EPI, Tn, BL>), dim3(grid), dim3(NTHR), 0, s, p);
   return hipGetLastError();
 }
 
