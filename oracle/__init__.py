@@ -20,6 +20,9 @@ Language Models"):
              eq. sec3:eq:all_other_gradients.
 * `sizing` - the binomial tail behind the TwELL compression-factor choice
              (Appendix A, TwELL matmul discussion).
+* `training` - the dead-unit record (a unit is dead for a training step when it
+             was never active in it) and the targeted re-initialisation of dead
+             units' gate-projection columns (appendix on training modifications).
 
 Everything is computed in float64 on the *stored* inputs (bf16 bit patterns
 or float32 values widened exactly). Pins: every function is checked by the
