@@ -297,6 +297,22 @@ class Bench:
                "tokens_per_s": round(w.T / ms * 1e3, 1), "lambda_l1": lam,
                "backward_stages_ms": dict(zip(["dh_at_pattern", "dx_gather", "pattern_transpose", "dw_gathers",
                                                "dense_backup_rows"], bwd))}
+        if not w.gated:
+            # dead-unit record of this batch, and the targeted re-initialisation of the
+            # pattern-deciding projection (on a copy): with this batch's dead units, and
+            # with every unit dead (the bound: every weight read, blended, written)
+            last = t.zeros((w.f,), dtype=t.int64, device="cuda")
+            rec["track_active_units_ms"] = round(self.time(lambda: b.sfl_track_active_units(
+                s["bufs"], w.T, w.f, "bf16", s["cfg"], 1, last, self.stream), steps=steps, warmup=1), 4)
+            Wc = s["Wu"].clone()
+            noise = t.randn((w.d, w.f), dtype=t.float32, device="cuda")
+            rec["reinit_dead_units_ms"] = round(self.time(lambda: b.sfl_reinit_dead_units(
+                Wc, last, 1, 0.1, 0.02, noise, stream=self.stream), steps=steps, warmup=1), 4)
+            t.cuda.synchronize()
+            rec["dead_units_in_batch"] = int((last < 1).sum().item())
+            rec["reinit_all_dead_ms"] = round(self.time(lambda: b.sfl_reinit_dead_units(
+                Wc, last, 2, 0.1, 0.02, noise, stream=self.stream), steps=steps, warmup=1), 4)
+            del Wc, noise
         # dense reference (torch / hipBLASLt)
         X, Wu, Wd = s["X"], s["Wu"], s["Wd"]
         WuT, WdT, XT = Wu.t().contiguous(), Wd.t().contiguous(), X.t().contiguous()

@@ -307,6 +307,41 @@ sfl_status_t sfl_dense_ffn_baseline(const sfl_ffn_args_t* args, sfl_stream_t str
  * stay fixed across calls are packed once and passed as W_down_packed. */
 sfl_status_t sfl_pack_down_weights(const void* W_down, void* out, int64_t f, int64_t d, sfl_stream_t stream);
 
+/* Dead-unit record (training observability; the paper's extended results track, per
+ * hidden unit, the last training step in which it was active, and call a unit dead for a
+ * step when it was never active during it). Sets last_active[n] = step for every hidden
+ * unit n that the packed activations `tw` of a T x f batch show active:
+ *  - every column named by a stored TwELL slot: tw->idx of slots s < min(tw->cnt, S) of
+ *    every (row, tile) pair, i.e. all active columns of rows whose tiles kept their
+ *    values (the TwELL of sfl_pack_twell or sfl_ffn_forward);
+ *  - when tw->ovf_dense is not NULL, every column with a positive value in the first
+ *    min(*tw->n_ovf, capacity) stored dense-backup rows ([capacity][f], val_dtype), as
+ *    sfl_ffn_forward writes them; a unit active only in the truncated part of an
+ *    overflowing tile of a row without a stored dense-backup row is not seen.
+ * Other entries of last_active are left as they are. last_active: device int64 [f],
+ * caller-owned; a unit is dead for step s when last_active[n] < s after the step's last
+ * batch. Reads tw->cnt, tw->idx, tw->n_ovf, tw->ovf_dense; T = 0 does nothing.
+ * Errors: SFL_E_ARG for a NULL last_active, cnt or idx (T > 0), an ovf_dense without
+ * n_ovf, or an invalid cfg. */
+sfl_status_t sfl_track_active_units(const sfl_twell_t* tw, int64_t T, int64_t f, sfl_dtype_t val_dtype,
+                                    const sfl_twell_cfg_t* cfg, int64_t step, int64_t* last_active,
+                                    sfl_stream_t stream);
+
+/* Targeted re-initialisation of dead units (the paper's dead-neuron mitigation,
+ * appendix on training modifications): for every unit j with last_active[j] < step,
+ *   W[:, j] <- (1 - lam) W[:, j] + lam * sigma * noise[:, j]
+ * (a pull toward a fresh N(0, sigma^2) draw; the paper uses sigma = 0.02, the
+ * initialisation scale, and lam = 0.1 on the gate projection). W is a rows x cols
+ * row-major matrix of dtype (F32 or BF16), updated in place; units_on_rows = 0 when
+ * the units are its columns (W_gate or W_up [d][f]), 1 when they are its rows (a
+ * transposed copy [f][d]). noise: device float32 array of W's shape holding standard
+ * normal draws from the caller's generator. Computed in fp32 (one multiply, one fused
+ * multiply-add), bf16 results rounded to nearest even. Errors: SFL_E_ARG for NULL
+ * pointers (non-empty W), lam outside [0, 1], sigma < 0 or units_on_rows not 0/1. */
+sfl_status_t sfl_reinit_dead_units(void* W, sfl_dtype_t dtype, int64_t rows, int64_t cols, int32_t units_on_rows,
+                                   const int64_t* last_active, int64_t step, float lam, float sigma,
+                                   const float* noise, sfl_stream_t stream);
+
 /* out[c][r] = in[r][c] for a rows x cols matrix of 2-byte (elem_bytes = 2) or
  * 4-byte (elem_bytes = 4) elements; lets callers keep W_upT next to W_up. */
 sfl_status_t sfl_transpose(const void* in, void* out, int64_t rows, int64_t cols,

@@ -27,7 +27,8 @@ BUF_NAMES = ["val", "idx", "cnt", "row_nnz", "row_ovf", "ovf_rows", "n_ovf", "el
 
 EXPORTED = ["sfl_status_string", "sfl_version", "sfl_twell_buffer_sizes", "sfl_pack_twell",
             "sfl_workspace_size", "sfl_ffn_forward", "sfl_up_projection", "sfl_ffn_backward",
-            "sfl_dense_ffn_baseline", "sfl_transpose", "sfl_pack_down_weights"]
+            "sfl_dense_ffn_baseline", "sfl_transpose", "sfl_pack_down_weights", "sfl_track_active_units",
+            "sfl_reinit_dead_units"]
 
 
 class SflError(RuntimeError):
@@ -85,6 +86,10 @@ _lib.sfl_ffn_backward.argtypes = [POINTER(BwdArgs), c_void_p]
 _lib.sfl_dense_ffn_baseline.argtypes = [POINTER(FfnArgs), c_void_p]
 _lib.sfl_transpose.argtypes = [c_void_p, c_void_p, c_int64, c_int64, c_int32, c_void_p]
 _lib.sfl_pack_down_weights.argtypes = [c_void_p, c_void_p, c_int64, c_int64, c_void_p]
+_lib.sfl_track_active_units.argtypes = [POINTER(Twell), c_int64, c_int64, c_int, POINTER(Cfg), c_int64, c_void_p,
+                                        c_void_p]
+_lib.sfl_reinit_dead_units.argtypes = [c_void_p, c_int, c_int64, c_int64, c_int32, c_void_p, c_int64, ctypes.c_float,
+                                       ctypes.c_float, c_void_p, c_void_p]
 for _n in EXPORTED[2:]:
     getattr(_lib, _n).restype = c_int
 
@@ -255,6 +260,21 @@ def sfl_ffn_backward(args, stream=None):
 def sfl_pack_down_weights(W_down, out, stream=None):
     f, d = W_down.shape
     _check("sfl_pack_down_weights", _lib.sfl_pack_down_weights(_ptr(W_down), _ptr(out), f, d, _stream(stream)))
+
+
+def sfl_track_active_units(bufs, T, f, dtype, cfg, step, last_active, stream=None):
+    tw = _twell_struct(bufs)
+    _check("sfl_track_active_units", _lib.sfl_track_active_units(ctypes.byref(tw), T, f, dtype_code(dtype),
+                                                                 ctypes.byref(cfg), int(step), _ptr(last_active),
+                                                                 _stream(stream)))
+
+
+def sfl_reinit_dead_units(W, last_active, step, lam, sigma, noise, units_on_rows=False, stream=None):
+    rows, cols = W.shape
+    _check("sfl_reinit_dead_units", _lib.sfl_reinit_dead_units(_ptr(W), dtype_code(W.dtype), rows, cols,
+                                                               1 if units_on_rows else 0, _ptr(last_active),
+                                                               int(step), float(lam), float(sigma), _ptr(noise),
+                                                               _stream(stream)))
 
 
 def sfl_transpose(inp, out, stream=None):

@@ -558,6 +558,33 @@ sfl_status_t sfl_pack_down_weights(const void* W_down, void* out, int64_t f, int
   return SFL_OK;
 }
 
+sfl_status_t sfl_track_active_units(const sfl_twell_t* tw, int64_t T, int64_t f, sfl_dtype_t val_dtype,
+                                    const sfl_twell_cfg_t* cfg, int64_t step, int64_t* last_active,
+                                    sfl_stream_t stream) {
+  if (!tw || !dtype_ok(val_dtype) || T < 0) return SFL_E_ARG;
+  sfl_status_t st = check_cfg(cfg, f);
+  if (st != SFL_OK) return st;
+  if (!last_active) return SFL_E_ARG;
+  if (T == 0) return SFL_OK;
+  if (!tw->cnt || !tw->idx || (tw->ovf_dense && !tw->n_ovf)) return SFL_E_ARG;
+  const int64_t cap = capacity_of(*cfg, T);
+  SFL_HIP(launch_track_units(T, f, (int)cdiv(f, cfg->tile_cols), cfg->tile_slots, tw->cnt, tw->idx, tw->ovf_dense,
+                             val_dtype == SFL_BF16, tw->n_ovf, (int32_t)cap, step, last_active, (hipStream_t)stream));
+  return SFL_OK;
+}
+
+sfl_status_t sfl_reinit_dead_units(void* W, sfl_dtype_t dtype, int64_t rows, int64_t cols, int32_t units_on_rows,
+                                   const int64_t* last_active, int64_t step, float lam, float sigma,
+                                   const float* noise, sfl_stream_t stream) {
+  if (!dtype_ok(dtype) || rows < 0 || cols < 0 || (units_on_rows != 0 && units_on_rows != 1)) return SFL_E_ARG;
+  if (!(lam >= 0.f && lam <= 1.f) || !(sigma >= 0.f)) return SFL_E_ARG;
+  if (rows * cols == 0) return SFL_OK;
+  if (!W || !last_active || !noise) return SFL_E_ARG;
+  SFL_HIP(launch_reinit_units(W, dtype == SFL_BF16, rows, cols, units_on_rows, last_active, step, lam, sigma, noise,
+                              (hipStream_t)stream));
+  return SFL_OK;
+}
+
 sfl_status_t sfl_ffn_backward(const sfl_ffn_bwd_args_t* a, sfl_stream_t stream) {
   return sfl::backward_run(a, (hipStream_t)stream);
 }

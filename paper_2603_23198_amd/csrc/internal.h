@@ -127,4 +127,17 @@ hipError_t launch_gated_h(int64_t T, int K, const void* ell_val, const int32_t* 
 hipError_t launch_transpose(const void* in, void* out, int64_t rows, int64_t cols, int elem_bytes,
                             hipStream_t s);
 
+// ---------------------------------------------------------- hidden units ----
+// last[n] = step for every unit named by a stored slot (s < min(cnt, S)) of the T x n_tiles
+// (row, tile) pairs and, when ovf_dense is not null, by a positive entry of the first
+// min(*n_ovf, cap) dense-backup rows [cap][f].
+hipError_t launch_track_units(int64_t T, int64_t f, int n_tiles, int S, const int32_t* cnt, const uint16_t* idx,
+                              const void* ovf_dense, int val_bf16, const int32_t* n_ovf, int32_t cap, int64_t step,
+                              int64_t* last, hipStream_t s);
+// W [rows][cols] (bf16 or fp32): for unit u (row or column) with last[u] < step,
+// w <- (1 - lam) w + lam sigma noise, noise fp32 of W's shape.
+hipError_t launch_reinit_units(void* W, int val_bf16, int64_t rows, int64_t cols, int units_on_rows,
+                               const int64_t* last, int64_t step, float lam, float sigma, const float* noise,
+                               hipStream_t s);
+
 }  // namespace sfl

@@ -165,3 +165,29 @@ def test_backward_workspace_and_validation():
     with pytest.raises(b.SflError) as e:
         b.sfl_workspace_size(ng, 1)
     assert e.value.code == b.SFL_E_ARG
+
+
+def test_unit_tracking_and_reinit_validate_before_launch():
+    cfg = b.make_cfg(tile_cols=256, tile_slots=32, ell_width=64)
+    tw = b.Twell()
+    lib = b._lib
+    # NULL record, NULL slots for T > 0, ovf_dense without n_ovf, bad cfg
+    assert lib.sfl_track_active_units(ctypes.byref(tw), 4, 100, 1, ctypes.byref(cfg), 0, None, None) == b.SFL_E_ARG
+    assert lib.sfl_track_active_units(ctypes.byref(tw), 4, 100, 1, ctypes.byref(cfg), 0, 8, None) == b.SFL_E_ARG
+    tw2 = b.Twell(*[8] * 6 + [None, None, None, 8])
+    tw2.n_ovf = None
+    assert lib.sfl_track_active_units(ctypes.byref(tw2), 4, 100, 1, ctypes.byref(cfg), 0, 8, None) == b.SFL_E_ARG
+    bad = b.make_cfg(tile_cols=4, tile_slots=5)
+    assert lib.sfl_track_active_units(ctypes.byref(tw), 4, 100, 1, ctypes.byref(bad), 0, 8, None) == b.SFL_E_ARG
+    # an empty batch does nothing and needs no buffers but the record
+    assert lib.sfl_track_active_units(ctypes.byref(tw), 0, 100, 1, ctypes.byref(cfg), 0, 8, None) == b.SFL_OK
+    # re-initialisation: coefficient ranges, the unit axis flag, pointers; empty W is a no-op
+    rd = lib.sfl_reinit_dead_units
+    assert rd(8, 1, 4, 4, 0, 8, 1, -0.1, 0.02, 8, None) == b.SFL_E_ARG
+    assert rd(8, 1, 4, 4, 0, 8, 1, 1.5, 0.02, 8, None) == b.SFL_E_ARG
+    assert rd(8, 1, 4, 4, 0, 8, 1, 0.1, -1.0, 8, None) == b.SFL_E_ARG
+    assert rd(8, 1, 4, 4, 2, 8, 1, 0.1, 0.02, 8, None) == b.SFL_E_ARG
+    assert rd(8, 1, 4, 4, 0, None, 1, 0.1, 0.02, 8, None) == b.SFL_E_ARG
+    assert rd(8, 1, 4, 4, 0, 8, 1, 0.1, 0.02, None, None) == b.SFL_E_ARG
+    assert rd(None, 1, 0, 4, 0, None, 1, 0.1, 0.02, None, None) == b.SFL_OK
+    assert rd(8, 7, 4, 4, 0, 8, 1, 0.1, 0.02, 8, None) == b.SFL_E_ARG
