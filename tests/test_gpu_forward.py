@@ -177,6 +177,32 @@ def test_fused_twell_equals_pack_of_same_mainloop(T, f, Tn, S, use_wupt):
     assert rel_l2(to_f64(Y)[rows], Yref) <= 2e-2
 
 
+@pytest.mark.parametrize("T", [1, 17, 48, 64])
+def test_small_batch_split_gemm(T):
+    """Batches of at most 64 rows with K-contiguous weights take the split-K GEMMs (K
+    ranges over blocks, partial sums reduced in split order): Z against the fp64 oracle,
+    the forward's TwELL bit-identical to the oracle's extraction from that Z, Y of the
+    sparse forward and of the dense baseline against the oracle."""
+    w = wl.make_ffn("skinny", "bf16", T, 1024, 2048, seed=T, sparsity=0.97, ell_width=128)
+    X, Wu, Wd = dev(w.X), dev(w.W_up), dev(w.W_down)
+    WupT = transposed(Wu)
+    cfg = b.make_cfg(**w.cfg)
+    Z = torch.empty((T, w.f), dtype=torch.float32, device="cuda")
+    args = b.ffn_args(X, Wu, Wd, cfg, shift_t=dev(w.shift_t), W_upT=WupT)
+    ws = torch.empty(max(1, b.sfl_workspace_size(args, 0)), dtype=torch.uint8, device="cuda")
+    b.sfl_up_projection(b.ffn_args(X, Wu, Wd, cfg, shift_t=dev(w.shift_t), W_upT=WupT, workspace=ws), Z)
+    torch.cuda.synchronize()
+    Zref = ffn.preactivation(w.as_f64(w.X), w.as_f64(w.W_up), None, w.shift_t)
+    assert rel_l2(Z.cpu().numpy(), Zref) < 1e-5
+    Y, bufs, stats, cfg = run_forward(w, use_wupt=True, use_wdownt=True)
+    tw = twell.extract_twell(Z.cpu().numpy(), cfg.tile_cols, cfg.tile_slots, "bf16")
+    assert_twell_equal(twell_views(bufs, T, w.f, cfg), tw, twell.classify(tw, cfg.ell_width))
+    Yref, _ = oracle_rows(w, np.arange(T))
+    assert rel_l2(to_f64(Y), Yref) <= 2e-2
+    Yd, _, _, _ = run_forward(w, use_wupt=True, use_wdownt=True, dense=True)
+    assert rel_l2(to_f64(Yd), Yref) <= 2e-2
+
+
 @pytest.mark.parametrize("T,d,f,Tn,S,K", [(300, 256, 320, 256, 32, 40), (65, 128, 1024, 64, 8, 24),
                                             (1, 512, 2048, 128, 16, 64), (513, 64, 192, 64, 64, 192)])
 def test_ragged_shapes_bf16(T, d, f, Tn, S, K):
