@@ -481,7 +481,7 @@ __device__ __forceinline__ int kc_swz(int row, int chunk) { return chunk ^ (row 
 
 // Split count for m_eff counted rows: enough blocks for about two per CU, at least four
 // 64-k steps per split, and partial sums that fit part_rows rows.
-__device__ __forceinline__ int splitk_count(int ksplit, int part_rows, int m_eff, int N, int nk) {
+__host__ __device__ inline int splitk_count(int ksplit, int part_rows, int m_eff, int N, int nk) {
   if (ksplit <= 1 || m_eff <= 0) return 1;
   const int tiles = (int)(cdiv(m_eff, BM) * cdiv(N, BN));
   int ks = min(ksplit, part_rows / m_eff);
@@ -814,6 +814,103 @@ __global__ __launch_bounds__(NTHR) void k_gemm_kc_split(GemmParams p) {
 
 // Sum of the split-K partials in split order, then the epilogue of element (m, n); four
 // consecutive columns per thread, grid-stride over the counted rows.
+// Split-K GEMM for at most 64 rows of A (decode-sized batches), both operands
+// K-contiguous: at this size the GEMM is a stream of B, so each block keeps three 64-k
+// stages in flight (direct-to-LDS loads, two stages ahead of the MFMAs) instead of one.
+// A block computes up to 64 rows x 256 columns of one K range with 8 waves of 32 columns
+// (v_mfma_f32_32x32x16_bf16 on RB blocks of 32 rows); a stage holds 64 A rows and 256 B
+// rows of 128 bytes, chunk c of row r at position c ^ (r & 7) as in the 256 x 256 kernel.
+// Writes the fp32 partial sums of its split like k_gemm_kc_split; the reduction kernel
+// adds them in split order and applies the epilogue.
+constexpr int FR_NS = 3;                            // stages in the ring
+constexpr int FR_AROWS = 64;                        // A rows per stage
+constexpr int FR_STAGE = (FR_AROWS + BN) * KC_BK;   // bf16 elements per stage (40 KB)
+
+template <int RB>
+__global__ __launch_bounds__(NTHR) void k_gemm_few_rows(GemmParams p) {
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[FR_NS * FR_STAGE];
+  const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
+  if (m_eff <= 0) return;
+  const int nk_all = (int)(p.K / KC_BK);
+  const int ks = splitk_count(p.ksplit, p.part_rows, m_eff, p.N, nk_all);
+  const int tiles_n = (int)cdiv(p.N, BN);
+  if ((int)blockIdx.x >= tiles_n * ks) return;
+  const int split = blockIdx.x % ks, n0 = (blockIdx.x / ks) * BN;
+  const int kt0 = (int)((int64_t)nk_all * split / ks), kt1 = (int)((int64_t)nk_all * (split + 1) / ks);
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const u32x4_t ra = rsrc_words(p.A, p.a_bytes);
+  const u32x4_t rb = rsrc_words(p.B, p.b_bytes);
+  // one load instruction fills 8 rows: wave w loads A rows 8w .. 8w+7 and B rows
+  // 32w + 8q .. +7 (q < 4); lane l writes row +l/8 at chunk position l%8
+  uint32_t offa, offb[4];
+  {
+    const int row = wave * 8 + (lane >> 3);
+    const int c = kc_swz(row, lane & 7);
+    const int64_t sa = row < m_eff ? (p.a_rows ? (int64_t)p.a_rows[row] : (int64_t)row) : -1;
+    offa = sa >= 0 ? (uint32_t)((sa * p.lda + c * 8) * 2) : kOOB;
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int row = wave * 32 + q * 8 + (lane >> 3);
+    const int c = kc_swz(row, lane & 7);
+    const int gb = n0 + row;
+    offb[q] = gb < p.N ? (uint32_t)(((int64_t)gb * p.ldb + c * 8) * 2) : kOOB;
+  }
+  auto lds_addr = [](const bf16_t* ptr) {
+    return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(__attribute__((address_space(3))) const bf16_t*)ptr);
+  };
+  auto issue = [&](int kt) {  // 5 load instructions per wave
+    const bf16_t* st = smem + ((kt - kt0) % FR_NS) * FR_STAGE;
+    const uint32_t so = (uint32_t)(kt * KC_BK * 2);
+    load_lds16(ra, lds_addr(st + wave * 8 * KC_BK), offa, so);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) load_lds16(rb, lds_addr(st + (FR_AROWS + wave * 32 + q * 8) * KC_BK), offb[q], so);
+  };
+  f32x16_t acc[RB];
+#pragma unroll
+  for (int r = 0; r < RB; ++r)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[r][i] = 0.f;
+  // 32x32x16 operands: lane l supplies row (column) l%32 at k 8*(l/32) .. +7 of the step
+  const int brow = FR_AROWS + wave * 32 + (lane & 31);
+  if (kt0 < kt1) issue(kt0);
+  if (kt0 + 1 < kt1) issue(kt0 + 1);
+  for (int kt = kt0; kt < kt1; ++kt) {
+    // this wave's loads of stage kt have landed (only stage kt+1 may still be in flight)
+    // and its LDS reads of step kt-1 are done; after the barrier the same holds for all
+    // waves, so the buffer of step kt-1 takes stage kt+2
+    if (kt + 1 < kt1)
+      __builtin_amdgcn_s_waitcnt(0x0075);  // vmcnt(5) expcnt(7) lgkmcnt(0)
+    else
+      __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt(0) expcnt(7) lgkmcnt(0)
+    __syncthreads();
+    if (kt + 2 < kt1) issue(kt + 2);
+    const bf16_t* st = smem + ((kt - kt0) % FR_NS) * FR_STAGE;
+#pragma unroll
+    for (int s4 = 0; s4 < KC_BK / 16; ++s4) {
+      const int c = s4 * 2 + (lane >> 5);
+      const bf16x8_t b = *(const bf16x8_t*)(st + brow * KC_BK + kc_swz(brow, c) * 8);
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+        const int ar = r * 32 + (lane & 31);
+        const bf16x8_t a = *(const bf16x8_t*)(st + ar * KC_BK + kc_swz(ar, c) * 8);
+        acc[r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[r], 0, 0, 0);
+      }
+    }
+  }
+  typedef AccGeo<32> G;
+  const int col = n0 + wave * 32 + G::col(lane);
+  if (col >= p.N) return;
+#pragma unroll
+  for (int r = 0; r < RB; ++r)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int row = r * 32 + G::row(i, lane);
+      if (row < m_eff) p.part[((int64_t)split * m_eff + row) * p.N + col] = acc[r][i];
+    }
+}
+
 template <int EPI>
 __global__ __launch_bounds__(256) void k_splitk_reduce(GemmParams p) {
   const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
@@ -880,6 +977,21 @@ template <int EPI, int BL = LAY_KC>
 hipError_t launch_kc_split(const GemmParams& p, hipStream_t s) {
   const int64_t tiles = cdiv(p.M, BM) * cdiv(p.N, BN);
   if (tiles == 0) return hipSuccess;
+  if (BL == LAY_KC && !p.m_count && p.M <= FR_AROWS) {
+    // at most 64 rows: about one block per CU, each streaming its K range of B
+    const int tiles_n = (int)cdiv(p.N, BN);
+    GemmParams q = p;
+    q.ksplit = std::max(1, device_cus() / tiles_n);
+    const int ks = splitk_count(q.ksplit, q.part_rows, q.M, q.N, (int)(q.K / KC_BK));
+    if (ks > 1) {
+      if (q.M <= 32)
+        hipLaunchKernelGGL((k_gemm_few_rows<1>), dim3((unsigned)(tiles_n * ks)), dim3(NTHR), 0, s, q);
+      else
+        hipLaunchKernelGGL((k_gemm_few_rows<2>), dim3((unsigned)(tiles_n * ks)), dim3(NTHR), 0, s, q);
+      hipLaunchKernelGGL((k_splitk_reduce<EPI>), dim3(1024), dim3(256), 0, s, q);
+      return hipGetLastError();
+    }
+  }
   const unsigned grid = (unsigned)std::min<int64_t>(tiles * p.ksplit, 512);  // about two blocks per CU
   hipLaunchKernelGGL((k_gemm_kc_split<EPI, BL>), dim3(grid), dim3(NTHR), 0, s, p);
   hipLaunchKernelGGL((k_splitk_reduce<EPI>), dim3(1024), dim3(256), 0, s, p);
