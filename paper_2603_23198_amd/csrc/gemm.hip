@@ -4,7 +4,9 @@
 //  * k_gemm_kc (both operands K-contiguous, K % 64 == 0; the forward's X W_up^T, the
 //    dense baseline's first GEMM, the backward's dZ W_up^T): v_mfma_f32_16x16x32_bf16,
 //    waves 4 along M x 2 along N, operands loaded straight from global memory into LDS
-//    (no staging registers) through two 64-k stages.
+//    (no staging registers) through two 64-k stages; persistent blocks, one per CU. Its
+//    split-K forms (k_gemm_kc_split, and k_gemm_few_rows for at most 64 rows) serve
+//    small batches and the dense-backup rows.
 //  * k_gemm_bf16 (any layout pair, K gathers, device-side K bounds): v_mfma_f32_32x32x16,
 //    waves 2 along M x 4 along N (128x64 per wave = 4x2 MFMA 32x32 tiles). K advances in
 //    steps of 64 through a double-buffered LDS stage; the next K step is fetched from
@@ -15,8 +17,8 @@
 //    and byte permutes turn them into two 8-element k vectors.
 //
 // Epilogues (the `Epilogue` enum) include the TwELL one of Alg. 1, which compacts the
-// active pre-activations straight from the accumulator registers (ballot + mbcnt per
-// row, see twell_epilogue).
+// active pre-activations straight from the accumulator registers (a ballot per register
+// and popcounts of its row group's bits, see twell_compact).
 #include "common.h"
 #include "internal.h"
 
