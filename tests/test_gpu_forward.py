@@ -177,6 +177,34 @@ def test_fused_twell_equals_pack_of_same_mainloop(T, f, Tn, S, use_wupt):
     assert rel_l2(to_f64(Y)[rows], Yref) <= 2e-2
 
 
+@pytest.mark.parametrize("use_wupt", [False, True])
+@pytest.mark.parametrize("T,f,Tn,S", [(600, 1088, 256, 32), (300, 704, 128, 16), (40, 960, 256, 32)])
+def test_bias_and_shift_in_the_fused_epilogue(T, f, Tn, S, use_wupt):
+    """A per-column bias and a per-row shift, with f not a multiple of the GEMM tile: the
+    epilogue adds both to the accumulators (columns past f never active), bit-identical
+    TwELL to the oracle's extraction from the same main loop's Z, Z and Y against fp64."""
+    w = wl.make_ffn("bias", "bf16", T, 512, f, seed=T + f, sparsity=0.97, tile_cols=Tn, tile_slots=S,
+                    ell_width=128)
+    r = np.random.default_rng(T * 3 + f)
+    w.bias_f = (r.standard_normal(f) * 0.05).astype(np.float32)
+    X, Wu, Wd = dev(w.X), dev(w.W_up), dev(w.W_down)
+    WupT = transposed(Wu) if use_wupt else None
+    cfg = b.make_cfg(**w.cfg)
+    kw = dict(bias_f=dev(w.bias_f), shift_t=dev(w.shift_t), W_upT=WupT)
+    Z = torch.empty((T, f), dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(1, b.sfl_workspace_size(b.ffn_args(X, Wu, Wd, cfg, **kw), 0)), dtype=torch.uint8,
+                     device="cuda")
+    b.sfl_up_projection(b.ffn_args(X, Wu, Wd, cfg, **kw, workspace=ws), Z)
+    Y, bufs, stats, cfg = run_forward(w, use_wupt=use_wupt)
+    Zn = Z.cpu().numpy()
+    Zref = ffn.preactivation(w.as_f64(w.X), w.as_f64(w.W_up), w.bias_f, w.shift_t)
+    assert rel_l2(Zn, Zref) < 1e-5
+    tw = twell.extract_twell(Zn, Tn, S, "bf16")
+    assert_twell_equal(twell_views(bufs, T, f, cfg), tw, twell.classify(tw, cfg.ell_width))
+    Yref, _ = oracle_rows(w, np.arange(T))
+    assert rel_l2(to_f64(Y), Yref) <= 2e-2
+
+
 @pytest.mark.parametrize("T", [1, 17, 48, 64])
 def test_small_batch_split_gemm(T):
     """Batches of at most 64 rows with K-contiguous weights take the split-K GEMMs (K
