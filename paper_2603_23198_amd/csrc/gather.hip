@@ -135,6 +135,13 @@ constexpr int NGRP = 64 / LPR;         // row segments per load instruction
 #endif
 constexpr int GATHER_WAVES = SFL_GATHER_WAVES;
 constexpr int GU = SFL_GATHER_UNROLL;       // row loads in flight per lane
+// ELL rows of at most 128 entries (ELL width K <= 128) in kernels that run one workgroup
+// per CU anyway (the staged entries fill the LDS): 12 row loads per lane, so that a
+// token's slice mostly takes one round of loads (8 entries per load instruction) instead
+// of a second, nearly empty one. Elsewhere 8: wider rows slow down with more in flight,
+// and the 12-load kernels need more than the 64 VGPRs of two 16-wave workgroups per CU.
+constexpr int GU_SHORT = 12;
+inline bool use_short_unroll(int K, int64_t lds_per_wg) { return K <= 128 && 2 * lds_per_wg > 160 * 1024; }
 constexpr int GATHER_LDS = SFL_GATHER_LDS;  // bytes of cached ELL entries per workgroup
 
 // Sum of the 8 groups' partial sums (lanes l, l ^ 8, ..., l ^ 56) into every group: the
@@ -154,17 +161,18 @@ __device__ __forceinline__ void fold_groups(float (&acc)[8]) {
 // One token's slice: entries er[0..nnz) in LDS, W row segments read through the buffer
 // descriptor at byte offset idx * 2 * SLICE + col_b; on return the lanes of group 0 hold
 // the sums of their 8 columns.
+template <int U>
 __device__ __forceinline__ void slice_token(const uint32_t* er, int nnz, __amdgpu_buffer_rsrc_t wr, uint32_t col_b,
                                             int grp, float (&acc)[8]) {
-  static_assert(GU % 2 == 0, "entries are consumed in pairs");
+  static_assert(U % 2 == 0, "entries are consumed in pairs");
   constexpr uint32_t row_b = SLICE2 * 2;
 #pragma unroll
   for (int j = 0; j < 8; ++j) acc[j] = 0.f;
-  for (int q = 0; q < nnz; q += NGRP * GU) {
-    u32x4_t w[GU];
-    uint32_t x[GU];
+  for (int q = 0; q < nnz; q += NGRP * U) {
+    u32x4_t w[U];
+    uint32_t x[U];
 #pragma unroll
-    for (int u = 0; u < GU; ++u) {
+    for (int u = 0; u < U; ++u) {
       const int e = q + u * NGRP + grp;
       x[u] = e < nnz ? er[e] : 0u;  // an absent entry has value 0 (and its load reads 0)
       const uint32_t off = e < nnz ? (x[u] & 0xffffu) * row_b + col_b : 0x80000000u;
@@ -172,7 +180,7 @@ __device__ __forceinline__ void slice_token(const uint32_t* er, int nnz, __amdgp
     }
     // two entries at a time: (v_a, v_b) . (w_a[c], w_b[c]) with one bf16 dot2 per column
 #pragma unroll
-    for (int u = 0; u < GU; u += 2) {
+    for (int u = 0; u < U; u += 2) {
       const bf16x2_t vv = __builtin_bit_cast(bf16x2_t, __builtin_amdgcn_perm(x[u + 1], x[u], 0x07060302u));
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -189,16 +197,17 @@ __device__ __forceinline__ void slice_token(const uint32_t* er, int nnz, __amdgp
 // The same with fp32 values: entries are (index, fp32 value bits) word pairs, and each
 // entry's row segment is scaled and added column by column (fp32 FMA, entries in order
 // per group, groups folded in a fixed order).
+template <int U>
 __device__ __forceinline__ void slice_token_f32(const uint32_t* er, int nnz, __amdgpu_buffer_rsrc_t wr, uint32_t col_b,
                                                 int grp, float (&acc)[8]) {
   constexpr uint32_t row_b = SLICE2 * 2;
 #pragma unroll
   for (int j = 0; j < 8; ++j) acc[j] = 0.f;
-  for (int q = 0; q < nnz; q += NGRP * GU) {
-    u32x4_t w[GU];
-    float v[GU];
+  for (int q = 0; q < nnz; q += NGRP * U) {
+    u32x4_t w[U];
+    float v[U];
 #pragma unroll
-    for (int u = 0; u < GU; ++u) {
+    for (int u = 0; u < U; ++u) {
       const int e = q + u * NGRP + grp;
       const bool ok = e < nnz;
       v[u] = ok ? __uint_as_float(er[2 * e + 1]) : 0.f;
@@ -206,7 +215,7 @@ __device__ __forceinline__ void slice_token_f32(const uint32_t* er, int nnz, __a
       w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0));
     }
 #pragma unroll
-    for (int u = 0; u < GU; ++u)
+    for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const uint32_t ww = w[u][j];
@@ -220,7 +229,7 @@ __device__ __forceinline__ void slice_token_f32(const uint32_t* er, int nnz, __a
 // VK: kind of the ELL values. 0: bf16 (packed with the index in one word); 1: fp32 (the
 // backward's dz, two words per entry). OUT: 0: bf16 Y; 1: fp32 Yf; 2: bf16 Y of the sum
 // with the fp32 addend Yf (the second of two passes that share an accumulator).
-template <int VK, int OUT>
+template <int VK, int OUT, int U>
 __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
     int64_t T, int64_t d, int64_t f, int K, const void* __restrict__ ell_val, const uint16_t* __restrict__ ell_idx,
     const int32_t* __restrict__ row_nnz, const uint8_t* __restrict__ row_ovf, const bf16_t* __restrict__ W,
@@ -267,9 +276,9 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
       if (nnz < 0) continue;
       float acc[8];
       if constexpr (VK == 1)
-        slice_token_f32(ent + 2 * i * K, nnz, wr, col_b, grp, acc);
+        slice_token_f32<U>(ent + 2 * i * K, nnz, wr, col_b, grp, acc);
       else
-        slice_token(ent + i * K, nnz, wr, col_b, grp, acc);
+        slice_token<U>(ent + i * K, nnz, wr, col_b, grp, acc);
       if (grp == 0) {
         const int64_t o = (t0 + i) * d + col;
         if constexpr (OUT == 1) {
@@ -322,6 +331,7 @@ __host__ __device__ inline int updot_copies(int tpw, int nsl) { return tpw < GAT
 // takes entry q + u * NGRP + g; each lane dots its 8 columns (bf16 dot2), the group sums
 // its 8 lanes, lane 0 of the group adds that to the entry's LDS sum. A token is always
 // handled by the same wave, so each entry's sum is updated in slice order.
+template <int U>
 __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gated_updot(
     int64_t T, int64_t d, int64_t f, int K, const uint16_t* __restrict__ ell_idx, const int32_t* __restrict__ row_nnz,
     const uint8_t* __restrict__ row_ovf, const bf16_t* __restrict__ X, const bf16_t* __restrict__ WuP,
@@ -364,16 +374,16 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gated_updot(
     // this lane's 8 columns of x[t] in the slice, as bf16 pairs
     const u32x4_t xv = *(const u32x4_t*)(X + (t0 + i) * d + (int64_t)slice * SLICE2 + sub * 8);
     const uint32_t* er = ent + i * K;
-    for (int q = 0; q < nnz; q += NGRP * GU) {
-      u32x4_t w[GU];
+    for (int q = 0; q < nnz; q += NGRP * U) {
+      u32x4_t w[U];
 #pragma unroll
-      for (int u = 0; u < GU; ++u) {
+      for (int u = 0; u < U; ++u) {
         const int e = q + u * NGRP + grp;
         const uint32_t off = e < nnz ? er[e] * row_b + col_b : 0x80000000u;
         w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0));
       }
 #pragma unroll
-      for (int u = 0; u < GU; ++u) {
+      for (int u = 0; u < U; ++u) {
         float sacc = 0.f;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -471,7 +481,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_unit
     const int cnt = __builtin_amdgcn_readfirstlane(ptr[n + 1]) - p0;
     float acc[8];
     if (staged) {
-      slice_token_f32(ent + 2 * (p0 - pb), cnt, gr, col_b, grp, acc);
+      slice_token_f32<GU>(ent + 2 * (p0 - pb), cnt, gr, col_b, grp, acc);
     } else {
 #pragma unroll
       for (int j = 0; j < 8; ++j) acc[j] = 0.f;
@@ -597,15 +607,23 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
   const size_t lds = (size_t)tpw * per_tok;
   if (lds > 160 * 1024) return hipErrorInvalidValue;
   const dim3 grid((unsigned)(8 * blocks)), block(GATHER_WAVES * 64);
-#define SFL_GATHER_LAUNCH(VK_, OUT_)                                                                               \
+  const bool short_rows = use_short_unroll(K, (int64_t)lds);
+#define SFL_GATHER_LAUNCH_U(VK_, OUT_, U_)                                                                          \
   do {                                                                                                             \
     if (lds > 65536) {                                                                                             \
-      const hipError_t e = hipFuncSetAttribute((const void*)k_gather_down_b16<VK_, OUT_>,                          \
+      const hipError_t e = hipFuncSetAttribute((const void*)k_gather_down_b16<VK_, OUT_, U_>,                      \
                                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);              \
       if (e != hipSuccess) return e;                                                                               \
     }                                                                                                              \
-    hipLaunchKernelGGL((k_gather_down_b16<VK_, OUT_>), grid, block, lds, s, T, d, f, K, ell_val, ell_idx, row_nnz, \
-                       row_ovf, (const bf16_t*)Wp, (bf16_t*)Y, Yf, n_slices, tpw);                                 \
+    hipLaunchKernelGGL((k_gather_down_b16<VK_, OUT_, U_>), grid, block, lds, s, T, d, f, K, ell_val, ell_idx,      \
+                       row_nnz, row_ovf, (const bf16_t*)Wp, (bf16_t*)Y, Yf, n_slices, tpw);                        \
+  } while (0)
+#define SFL_GATHER_LAUNCH(VK_, OUT_)                  \
+  do {                                                \
+    if (short_rows)                                   \
+      SFL_GATHER_LAUNCH_U(VK_, OUT_, GU_SHORT);       \
+    else                                              \
+      SFL_GATHER_LAUNCH_U(VK_, OUT_, GU);             \
   } while (0)
   if (vk == 0 && out_mode == 0) SFL_GATHER_LAUNCH(0, 0);
   else if (vk == 1 && out_mode == 0) SFL_GATHER_LAUNCH(1, 0);
@@ -613,6 +631,7 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
   else if (vk == 1 && out_mode == 2) SFL_GATHER_LAUNCH(1, 2);
   else return hipErrorInvalidValue;
 #undef SFL_GATHER_LAUNCH
+#undef SFL_GATHER_LAUNCH_U
   return hipGetLastError();
 }
 
@@ -675,13 +694,19 @@ hipError_t launch_gated_updot(int64_t T, int64_t d, int64_t f, int K, const uint
   const int nsl_max = (int)cdiv(d / SLICE2, 8);
   const size_t lds = (size_t)tpw * per_tok + (size_t)(updot_copies(tpw, nsl_max) - 1) * tpw * std::max(K, 1) * 4;
   if (lds > 160 * 1024) return hipErrorInvalidValue;
+  const bool short_rows = use_short_unroll(K, (int64_t)lds);
+  const void* kern = short_rows ? (const void*)k_gated_updot<GU_SHORT> : (const void*)k_gated_updot<GU>;
   if (lds > 65536) {
-    const hipError_t e =
-        hipFuncSetAttribute((const void*)k_gated_updot, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(k_gated_updot, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), lds, s, T, d, f, K, ell_idx,
-                     row_nnz, row_ovf, (const bf16_t*)X, (const bf16_t*)WuP, part_u, (int)(d / SLICE2), tpw);
+  if (short_rows)
+    hipLaunchKernelGGL(k_gated_updot<GU_SHORT>, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), lds, s, T, d, f,
+                       K, ell_idx, row_nnz, row_ovf, (const bf16_t*)X, (const bf16_t*)WuP, part_u, (int)(d / SLICE2),
+                       tpw);
+  else
+    hipLaunchKernelGGL(k_gated_updot<GU>, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), lds, s, T, d, f, K,
+                       ell_idx, row_nnz, row_ovf, (const bf16_t*)X, (const bf16_t*)WuP, part_u, (int)(d / SLICE2), tpw);
   return hipGetLastError();
 }
 
