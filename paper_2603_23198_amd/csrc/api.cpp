@@ -372,13 +372,24 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
     } else {
       g.C = plan.Z;
       g.ldc = f;
+      int ks = 1;
       if (small_batch(*a)) {
         g.ksplit = kMaxSplit;
         g.part = plan.part;
         g.part_rows = plan.part_rows;
+        ks = gemm_split_count(LAY_KC, blay, g);
       }
-      SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_F32, g, s));
-      SFL_HIP(launch_pack_twell(plan.Z, T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, s));
+      if (ks > 1) {
+        // the pack sums the split-K partials itself (the reduction's arithmetic), so Z is
+        // never written
+        g.no_reduce = 1;
+        SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_F32, g, s));
+        SFL_HIP(launch_pack_twell_parts(plan.part, ks, a->bias_f, a->shift_t, T, f, vb, a->cfg.tile_cols,
+                                        a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, s));
+      } else {
+        SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_F32, g, s));
+        SFL_HIP(launch_pack_twell(plan.Z, T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, s));
+      }
     }
   }
   ev.record(1, s);

@@ -975,28 +975,34 @@ hipError_t launch_kc(const GemmParams& p, hipStream_t s) {
 
 // Split-K launch: the GEMM over (tile, split) blocks, then the partial-sum reduction. The
 // split count is decided on the device from the row count, identically in both kernels.
+// The few-rows split-K GEMM: its split cap (about one block per CU) and split count (it
+// runs only when that count exceeds 1).
+int few_rows_ksplit(const GemmParams& p) { return std::max(1, device_cus() / (int)cdiv(p.N, BN)); }
+int few_rows_split(const GemmParams& p, int blay) {
+  if (blay != LAY_KC || p.m_count || p.M > FR_AROWS) return 1;
+  return splitk_count(few_rows_ksplit(p), p.part_rows, p.M, p.N, (int)(p.K / KC_BK));
+}
+
 template <int EPI, int BL = LAY_KC>
 hipError_t launch_kc_split(const GemmParams& p, hipStream_t s) {
   const int64_t tiles = cdiv(p.M, BM) * cdiv(p.N, BN);
   if (tiles == 0) return hipSuccess;
-  if (BL == LAY_KC && !p.m_count && p.M <= FR_AROWS) {
+  if (few_rows_split(p, BL) > 1) {
     // at most 64 rows: about one block per CU, each streaming its K range of B
     const int tiles_n = (int)cdiv(p.N, BN);
     GemmParams q = p;
-    q.ksplit = std::max(1, device_cus() / tiles_n);
-    const int ks = splitk_count(q.ksplit, q.part_rows, q.M, q.N, (int)(q.K / KC_BK));
-    if (ks > 1) {
-      if (q.M <= 32)
-        hipLaunchKernelGGL((k_gemm_few_rows<1>), dim3((unsigned)(tiles_n * ks)), dim3(NTHR), 0, s, q);
-      else
-        hipLaunchKernelGGL((k_gemm_few_rows<2>), dim3((unsigned)(tiles_n * ks)), dim3(NTHR), 0, s, q);
-      hipLaunchKernelGGL((k_splitk_reduce<EPI>), dim3(1024), dim3(256), 0, s, q);
-      return hipGetLastError();
-    }
+    q.ksplit = few_rows_ksplit(p);
+    const int ks = few_rows_split(p, BL);
+    if (q.M <= 32)
+      hipLaunchKernelGGL((k_gemm_few_rows<1>), dim3((unsigned)(tiles_n * ks)), dim3(NTHR), 0, s, q);
+    else
+      hipLaunchKernelGGL((k_gemm_few_rows<2>), dim3((unsigned)(tiles_n * ks)), dim3(NTHR), 0, s, q);
+    if (!p.no_reduce) hipLaunchKernelGGL((k_splitk_reduce<EPI>), dim3(1024), dim3(256), 0, s, q);
+    return hipGetLastError();
   }
   const unsigned grid = (unsigned)std::min<int64_t>(tiles * p.ksplit, 512);  // about two blocks per CU
   hipLaunchKernelGGL((k_gemm_kc_split<EPI, BL>), dim3(grid), dim3(NTHR), 0, s, p);
-  hipLaunchKernelGGL((k_splitk_reduce<EPI>), dim3(1024), dim3(256), 0, s, p);
+  if (!p.no_reduce) hipLaunchKernelGGL((k_splitk_reduce<EPI>), dim3(1024), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 template <int ALAY, int BLAY, int EPI, int Tn = 0>
@@ -1144,6 +1150,14 @@ hipError_t gemm_bf16(int alay, int blay, int epi, const GemmParams& p, hipStream
   SFL_CASE(LAY_RCG, LAY_RC, EPI_ACCUM_F32)
 #undef SFL_CASE
   return hipErrorInvalidValue;
+}
+
+int gemm_split_count(int alay, int blay, const GemmParams& p) {
+  const bool kcb = alay == LAY_KC && kc_ok(p, blay);
+  if (!(kcb && p.ksplit > 1 && p.part && p.N % 4 == 0) || p.m_count) return 1;
+  const int fr = few_rows_split(p, blay);
+  if (fr > 1) return fr;
+  return splitk_count(p.ksplit, p.part_rows, p.M, p.N, (int)(p.K / KC_BK));
 }
 
 hipError_t gemm_f32(int epi, const GemmParams& p, hipStream_t s) {

@@ -60,17 +60,30 @@ struct GemmParams {
   int ksplit;
   float* part;
   int part_rows;
+  // split-K only: leave the partial sums in `part` (no reduction kernel); the caller
+  // reduces them itself, e.g. launch_pack_twell_parts
+  int no_reduce;
 };
 
 // bf16 MFMA GEMM. Requirements: K % 8 == 0; RC layouts need even M/N extents and
 // 4-byte aligned rows; EPI_TWELL needs tile_cols in {64,128,256}.
 hipError_t gemm_bf16(int alay, int blay, int epi, const GemmParams& p, hipStream_t s);
+// Number of K splits gemm_bf16 uses for p (bf16, no m_count): > 1 when it writes fp32
+// partial sums to part [ks][M][N] (and, with no_reduce, stops there), 1 when its
+// epilogue writes C directly.
+int gemm_split_count(int alay, int blay, const GemmParams& p);
 // fp32 FMA GEMM for the F32 dtype (A MK, B KN only; any sizes).
 hipError_t gemm_f32(int epi, const GemmParams& p, hipStream_t s);
 
 // ----------------------------------------------------------- TwELL ----
 hipError_t launch_pack_twell(const float* Z, int64_t T, int64_t f, int val_bf16, int tile_cols,
                              int tile_slots, void* val, uint16_t* idx, int32_t* cnt, hipStream_t s);
+// The same from split-K partial sums: z[t][n] = ((sum over s < ks of part[s][t][n], in
+// split order) + bias[n]) + shift[t], the arithmetic of the split-K reduction's fp32
+// epilogue (bias and shift optional).
+hipError_t launch_pack_twell_parts(const float* part, int ks, const float* bias, const float* shift, int64_t T,
+                                   int64_t f, int val_bf16, int tile_cols, int tile_slots, void* val, uint16_t* idx,
+                                   int32_t* cnt, hipStream_t s);
 // Hybrid classification: row_nnz, row_ovf, optional ELL rows and stats partials.
 hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int tile_cols, int tile_slots,
                            int ell_width, const void* val, const uint16_t* idx, const int32_t* cnt,

@@ -22,10 +22,13 @@ __device__ __forceinline__ bool is_active(float z) {
 
 // One wave per (row, tile): 64 columns per step, ballot + mbcnt give each active lane its
 // slot (running count + active lanes below it), so slots follow ascending column order.
+// With ks > 0, z comes from ks split-K partial sums part[s][t][n] (Z is then the partial
+// array, ks * T * f floats): their sum in split order, plus bias[n], plus shift[t].
 template <typename V>
 __global__ __launch_bounds__(256) void k_pack_twell(const float* __restrict__ Z, int64_t T, int64_t f,
                                                     int Tn, int S, int NT, V* __restrict__ val,
-                                                    uint16_t* __restrict__ idx, int32_t* __restrict__ cnt) {
+                                                    uint16_t* __restrict__ idx, int32_t* __restrict__ cnt, int ks,
+                                                    const float* __restrict__ bias, const float* __restrict__ shift) {
   const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (w >= T * NT) return;
   const int l = threadIdx.x & 63;
@@ -36,9 +39,18 @@ __global__ __launch_bounds__(256) void k_pack_twell(const float* __restrict__ Z,
   const float* zr = Z + t * f;
   const int64_t base = t * (int64_t)NT * S + (int64_t)j * S;
   int running = 0;
+  const float sh = (ks > 0 && shift) ? shift[t] : 0.f;
   for (int64_t c = c0; c < c1; c += 64) {
     const int64_t col = c + l;
-    const float z = col < c1 ? zr[col] : 0.f;
+    float z = 0.f;
+    if (col < c1) {
+      z = zr[col];
+      if (ks > 0) {
+        for (int sp = 1; sp < ks; ++sp) z += zr[(int64_t)sp * T * f + col];
+        if (bias) z += bias[col];
+        z += sh;
+      }
+    }
     const bool act = col < c1 && is_active(z);
     const uint64_t m = ballot(act);
     const int slot = running + mbcnt(m);
@@ -58,9 +70,28 @@ hipError_t launch_pack_twell(const float* Z, int64_t T, int64_t f, int val_bf16,
   if (waves == 0) return hipSuccess;
   const dim3 grid((unsigned)cdiv(waves, 4));
   if (val_bf16)
-    hipLaunchKernelGGL(k_pack_twell<bf16_t>, grid, dim3(256), 0, s, Z, T, f, Tn, S, NT, (bf16_t*)val, idx, cnt);
+    hipLaunchKernelGGL(k_pack_twell<bf16_t>, grid, dim3(256), 0, s, Z, T, f, Tn, S, NT, (bf16_t*)val, idx, cnt, 0,
+                       (const float*)nullptr, (const float*)nullptr);
   else
-    hipLaunchKernelGGL(k_pack_twell<float>, grid, dim3(256), 0, s, Z, T, f, Tn, S, NT, (float*)val, idx, cnt);
+    hipLaunchKernelGGL(k_pack_twell<float>, grid, dim3(256), 0, s, Z, T, f, Tn, S, NT, (float*)val, idx, cnt, 0,
+                       (const float*)nullptr, (const float*)nullptr);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_twell_parts(const float* part, int ks, const float* bias, const float* shift, int64_t T,
+                                   int64_t f, int val_bf16, int Tn, int S, void* val, uint16_t* idx, int32_t* cnt,
+                                   hipStream_t s) {
+  const int NT = (int)cdiv(f, Tn);
+  const int64_t waves = T * NT;
+  if (waves == 0) return hipSuccess;
+  if (ks < 1) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)cdiv(waves, 4));
+  if (val_bf16)
+    hipLaunchKernelGGL(k_pack_twell<bf16_t>, grid, dim3(256), 0, s, part, T, f, Tn, S, NT, (bf16_t*)val, idx, cnt, ks,
+                       bias, shift);
+  else
+    hipLaunchKernelGGL(k_pack_twell<float>, grid, dim3(256), 0, s, part, T, f, Tn, S, NT, (float*)val, idx, cnt, ks,
+                       bias, shift);
   return hipGetLastError();
 }
 
