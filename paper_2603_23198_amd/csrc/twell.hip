@@ -294,18 +294,25 @@ hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s) {
   return hipGetLastError();
 }
 
-// One workgroup of 1024 threads scans the row flags 1024 at a time (wave scans +
-// a scan of the 16 wave totals), so the list is in ascending row order.
+// One workgroup of 1024 threads; each pass covers 1024 x 16 rows, thread i taking 16
+// consecutive rows (their flags loaded together), so a pass costs one round of loads.
+// An exclusive scan of the threads' counts (wave scans + a scan of the 16 wave totals)
+// places each thread's rows, in ascending row order.
+constexpr int kOvfRowsPerThread = 16;
 __global__ __launch_bounds__(1024) void k_ovf_list(int64_t T, int32_t cap, const uint8_t* __restrict__ row_ovf,
                                                    int32_t* __restrict__ ovf_rows, int32_t* __restrict__ n_ovf,
                                                    sfl_stats_t* __restrict__ stats) {
   __shared__ int wsum[16];
   const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
   int64_t base = 0;
-  for (int64_t r0 = 0; r0 < T; r0 += 1024) {
-    const int64_t t = r0 + tid;
-    const int flag = (t < T && row_ovf[t]) ? 1 : 0;
-    const int incl = wave_incl_scan(flag);
+  for (int64_t r0 = 0; r0 < T; r0 += 1024 * kOvfRowsPerThread) {
+    const int64_t t0 = r0 + (int64_t)tid * kOvfRowsPerThread;
+    uint32_t bits = 0;
+#pragma unroll
+    for (int k = 0; k < kOvfRowsPerThread; ++k)
+      if (t0 + k < T && row_ovf[t0 + k]) bits |= 1u << k;
+    const int c = __popc(bits);
+    const int incl = wave_incl_scan(c);
     if (l == 63) wsum[w] = incl;
     __syncthreads();
     int before = 0, all = 0;
@@ -314,8 +321,9 @@ __global__ __launch_bounds__(1024) void k_ovf_list(int64_t T, int32_t cap, const
       before += (i < w) ? v : 0;
       all += v;
     }
-    const int64_t pos = base + before + incl - flag;
-    if (flag && pos < cap) ovf_rows[pos] = (int32_t)t;
+    int64_t pos = base + before + incl - c;
+    for (; bits; bits &= bits - 1, ++pos)
+      if (pos < cap) ovf_rows[pos] = (int32_t)(t0 + __builtin_ctz(bits));
     base += all;
     __syncthreads();
   }
