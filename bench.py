@@ -14,7 +14,7 @@ speedup. Per-stage times come from HIP events the library records on its stream.
 The same JSON line also reports the other workloads of the hot path (sparsity sweep,
 lognormal row counts with dense-backup rows, gated forward at prefill and decode sizes,
 and the training step: forward + backward with the L1 term). `--quick` skips them.
-`--gpus` above 1 is refused: this build runs on one GPU.
+`--gpus` above 1 is refused: the benchmark runs on one GPU.
 """
 from __future__ import annotations
 
@@ -351,7 +351,7 @@ class Bench:
 def main():
     a = parse()
     if a.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
+        print(json.dumps({"error": "the benchmark runs on one GPU; --gpus must be 1"}))
         sys.exit(2)
     import torch
 

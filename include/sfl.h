@@ -45,7 +45,7 @@ typedef enum { SFL_F32 = 0, SFL_BF16 = 1 } sfl_dtype_t;
 typedef enum {
   SFL_OK = 0,
   SFL_E_ARG = -1,          /* invalid argument (null pointer, bad size, inconsistent config) */
-  SFL_E_UNSUPPORTED = -2,  /* valid request that this build has no kernel for */
+  SFL_E_UNSUPPORTED = -2,  /* valid request that the library has no kernel for */
   SFL_E_WORKSPACE = -3,    /* workspace missing or smaller than the size query returned */
   SFL_E_HIP = -4           /* a HIP runtime call or kernel launch failed */
 } sfl_status_t;
