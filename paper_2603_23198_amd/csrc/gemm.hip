@@ -814,8 +814,56 @@ __global__ __launch_bounds__(NTHR) void k_gemm_kc_split(GemmParams p) {
   }
 }
 
+// Epilogue of the split-K sums v of row m (counted order), columns n .. n+3.
+template <int EPI>
+__device__ __forceinline__ void splitk_store(const GemmParams& p, int m, int n, const f32x4_t& v) {
+  const int64_t crow = p.c_rows ? (int64_t)p.c_rows[m] : (int64_t)m;
+  float sh = 0.f;
+  if ((EPI == EPI_F32 || EPI == EPI_ACT_RELU) && p.shift) sh = p.shift[p.s_rows ? p.s_rows[m] : m];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    float x = v[q];
+    const int col = n + q;
+    if (EPI == EPI_F32 || EPI == EPI_ACT_RELU) {
+      if (p.bias) x += p.bias[col];
+      x += sh;
+    }
+    if (EPI == EPI_F32) {
+      ((float*)p.C)[crow * p.ldc + col] = x;
+    } else if (EPI == EPI_ACT_RELU) {
+      ((bf16_t*)p.C)[crow * p.ldc + col] = active_bits(x) ? f32_to_bf16(x) : (bf16_t)0;
+    } else if (EPI == EPI_ACT) {
+      ((bf16_t*)p.C)[crow * p.ldc + col] = f32_to_bf16(x);
+    } else if (EPI == EPI_MUL_ACT) {
+      bf16_t* c = (bf16_t*)p.C + crow * p.ldc + col;
+      *c = f32_to_bf16(bf16_to_f32(*c) * x);
+    }
+  }
+}
+
+// Sum of the ks partials of row m, columns n .. n+3, in split order.
+__device__ __forceinline__ f32x4_t splitk_sum(const GemmParams& p, int ks, int m_eff, int m, int n) {
+  f32x4_t v = *(const f32x4_t*)(p.part + (int64_t)m * p.N + n);
+  for (int sp = 1; sp < ks; ++sp) v += *(const f32x4_t*)(p.part + ((int64_t)sp * m_eff + m) * p.N + n);
+  return v;
+}
+
 // Sum of the split-K partials in split order, then the epilogue of element (m, n); four
 // consecutive columns per thread, grid-stride over the counted rows.
+template <int EPI>
+__global__ __launch_bounds__(256) void k_splitk_reduce(GemmParams p) {
+  const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
+  const int ks = splitk_count(p.ksplit, p.part_rows, m_eff, p.N, (int)(p.K / KC_BK));
+  if (ks <= 1) return;
+  const int n4 = p.N / 4;
+  const int64_t total = (int64_t)m_eff * n4;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
+    const int m = (int)(e / n4);
+    const int n = (int)(e % n4) * 4;
+    splitk_store<EPI>(p, m, n, splitk_sum(p, ks, m_eff, m, n));
+  }
+}
+
 // Split-K GEMM for at most 64 rows of A (decode-sized batches), both operands
 // K-contiguous: at this size the GEMM is a stream of B, so each block keeps three 64-k
 // stages in flight (direct-to-LDS loads, two stages ahead of the MFMAs) instead of one.
@@ -823,12 +871,14 @@ __global__ __launch_bounds__(NTHR) void k_gemm_kc_split(GemmParams p) {
 // (v_mfma_f32_32x32x16_bf16 on RB blocks of 32 rows); a stage holds 64 A rows and 256 B
 // rows of 128 bytes, chunk c of row r at position c ^ (r & 7) as in the 256 x 256 kernel.
 // Writes the fp32 partial sums of its split like k_gemm_kc_split; the reduction kernel
-// adds them in split order and applies the epilogue.
+// adds them in split order and applies the epilogue, or, given tile counters, the last
+// block of each tile does (one launch instead of two, which is most of the cost of the
+// dense-backup GEMMs of a decode step when no row overflows).
 constexpr int FR_NS = 3;                            // stages in the ring
 constexpr int FR_AROWS = 64;                        // A rows per stage
 constexpr int FR_STAGE = (FR_AROWS + BN) * KC_BK;   // bf16 elements per stage (40 KB)
 
-template <int RB>
+template <int EPI, int RB>
 __global__ __launch_bounds__(NTHR) void k_gemm_few_rows(GemmParams p) {
   __shared__ __attribute__((aligned(1024))) bf16_t smem[FR_NS * FR_STAGE];
   const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
@@ -903,51 +953,32 @@ __global__ __launch_bounds__(NTHR) void k_gemm_few_rows(GemmParams p) {
   }
   typedef AccGeo<32> G;
   const int col = n0 + wave * 32 + G::col(lane);
-  if (col >= p.N) return;
+  if (col < p.N) {
 #pragma unroll
-  for (int r = 0; r < RB; ++r)
+    for (int r = 0; r < RB; ++r)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int row = r * 32 + G::row(i, lane);
-      if (row < m_eff) p.part[((int64_t)split * m_eff + row) * p.N + col] = acc[r][i];
-    }
-}
-
-template <int EPI>
-__global__ __launch_bounds__(256) void k_splitk_reduce(GemmParams p) {
-  const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
-  const int ks = splitk_count(p.ksplit, p.part_rows, m_eff, p.N, (int)(p.K / KC_BK));
-  if (ks <= 1) return;
-  const int n4 = p.N / 4;
-  const int64_t total = (int64_t)m_eff * n4;
-  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
-    const int m = (int)(e / n4);
-    const int n = (int)(e % n4) * 4;
-    f32x4_t v = *(const f32x4_t*)(p.part + (int64_t)m * p.N + n);
-    for (int sp = 1; sp < ks; ++sp) v += *(const f32x4_t*)(p.part + ((int64_t)sp * m_eff + m) * p.N + n);
-    const int64_t crow = p.c_rows ? (int64_t)p.c_rows[m] : (int64_t)m;
-    float sh = 0.f;
-    if ((EPI == EPI_F32 || EPI == EPI_ACT_RELU) && p.shift) sh = p.shift[p.s_rows ? p.s_rows[m] : m];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      float x = v[q];
-      const int col = n + q;
-      if (EPI == EPI_F32 || EPI == EPI_ACT_RELU) {
-        if (p.bias) x += p.bias[col];
-        x += sh;
+      for (int i = 0; i < 16; ++i) {
+        const int row = r * 32 + G::row(i, lane);
+        if (row < m_eff) p.part[((int64_t)split * m_eff + row) * p.N + col] = acc[r][i];
       }
-      if (EPI == EPI_F32) {
-        ((float*)p.C)[crow * p.ldc + col] = x;
-      } else if (EPI == EPI_ACT_RELU) {
-        ((bf16_t*)p.C)[crow * p.ldc + col] = active_bits(x) ? f32_to_bf16(x) : (bf16_t)0;
-      } else if (EPI == EPI_ACT) {
-        ((bf16_t*)p.C)[crow * p.ldc + col] = f32_to_bf16(x);
-      } else if (EPI == EPI_MUL_ACT) {
-        bf16_t* c = (bf16_t*)p.C + crow * p.ldc + col;
-        *c = f32_to_bf16(bf16_to_f32(*c) * x);
-      }
-    }
   }
+  if (!p.tile_sem) return;
+  // the last block of the tile to finish adds its ks partial sums (in split order) and
+  // applies the epilogue: every block's partial stores are visible device-wide before its
+  // counter increment, and the last block's loads come after it
+  __shared__ int last;
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) last = atomicAdd(&p.tile_sem[n0 / BN], 1) == ks - 1;
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  const int n4 = min(BN, p.N - n0) / 4;
+  for (int e = threadIdx.x; e < m_eff * n4; e += NTHR) {
+    const int m = e / n4, n = n0 + (e % n4) * 4;
+    splitk_store<EPI>(p, m, n, splitk_sum(p, ks, m_eff, m, n));
+  }
+  if (threadIdx.x == 0) p.tile_sem[n0 / BN] = 0;
 }
 
 // Compute units of the current device (cached per device).
@@ -978,9 +1009,15 @@ hipError_t launch_kc(const GemmParams& p, hipStream_t s) {
 // The few-rows split-K GEMM: its split cap (about one block per CU) and split count (it
 // runs only when that count exceeds 1).
 int few_rows_ksplit(const GemmParams& p) { return std::max(1, device_cus() / (int)cdiv(p.N, BN)); }
+// With counted rows (m_count) the device's split count, from m_eff <= M, is at least this
+// one; the grid then covers the largest count (m_eff = 1) and blocks past the device's
+// count return.
 int few_rows_split(const GemmParams& p, int blay) {
-  if (blay != LAY_KC || p.m_count || p.M > FR_AROWS) return 1;
+  if (blay != LAY_KC || p.M > FR_AROWS || (p.m_count && !p.tile_sem)) return 1;
   return splitk_count(few_rows_ksplit(p), p.part_rows, p.M, p.N, (int)(p.K / KC_BK));
+}
+int few_rows_grid_split(const GemmParams& p) {
+  return splitk_count(few_rows_ksplit(p), p.part_rows, p.m_count ? 1 : p.M, p.N, (int)(p.K / KC_BK));
 }
 
 template <int EPI, int BL = LAY_KC>
@@ -992,12 +1029,12 @@ hipError_t launch_kc_split(const GemmParams& p, hipStream_t s) {
     const int tiles_n = (int)cdiv(p.N, BN);
     GemmParams q = p;
     q.ksplit = few_rows_ksplit(p);
-    const int ks = few_rows_split(p, BL);
+    const unsigned grid = (unsigned)(tiles_n * few_rows_grid_split(p));
     if (q.M <= 32)
-      hipLaunchKernelGGL((k_gemm_few_rows<1>), dim3((unsigned)(tiles_n * ks)), dim3(NTHR), 0, s, q);
+      hipLaunchKernelGGL((k_gemm_few_rows<EPI, 1>), dim3(grid), dim3(NTHR), 0, s, q);
     else
-      hipLaunchKernelGGL((k_gemm_few_rows<2>), dim3((unsigned)(tiles_n * ks)), dim3(NTHR), 0, s, q);
-    if (!p.no_reduce) hipLaunchKernelGGL((k_splitk_reduce<EPI>), dim3(1024), dim3(256), 0, s, q);
+      hipLaunchKernelGGL((k_gemm_few_rows<EPI, 2>), dim3(grid), dim3(NTHR), 0, s, q);
+    if (!p.no_reduce && !p.tile_sem) hipLaunchKernelGGL((k_splitk_reduce<EPI>), dim3(1024), dim3(256), 0, s, q);
     return hipGetLastError();
   }
   const unsigned grid = (unsigned)std::min<int64_t>(tiles * p.ksplit, 512);  // about two blocks per CU

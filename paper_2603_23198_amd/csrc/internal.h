@@ -63,6 +63,10 @@ struct GemmParams {
   // split-K only: leave the partial sums in `part` (no reduction kernel); the caller
   // reduces them itself, e.g. launch_pack_twell_parts
   int no_reduce;
+  // split-K of at most 64 rows: zeroed counters, one per 256-column tile; the last block
+  // of each tile to finish adds the tile's partial sums and applies the epilogue (no
+  // reduction kernel), and sets its counter back to zero
+  int32_t* tile_sem;
 };
 
 // bf16 MFMA GEMM. Requirements: K % 8 == 0; RC layouts need even M/N extents and
@@ -91,7 +95,8 @@ hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int tile_cols, in
                            sfl_stats_t* stats, hipStream_t s);
 // Ascending dense-backup row list + n_ovf + capacity flag (one workgroup).
 hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32_t* ovf_rows,
-                           int32_t* n_ovf, sfl_stats_t* stats, hipStream_t s);
+                           int32_t* n_ovf, sfl_stats_t* stats, hipStream_t s,
+                           int32_t* zero = nullptr, int n_zero = 0);
 hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s);
 // l1 of the computed dense-backup rows (adds into stats->l1_sum).
 // Dense-backup rows whose tiles kept every value, rebuilt from the TwELL slabs; the others

@@ -299,11 +299,14 @@ hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s) {
 // An exclusive scan of the threads' counts (wave scans + a scan of the 16 wave totals)
 // places each thread's rows, in ascending row order.
 constexpr int kOvfRowsPerThread = 16;
+// It also zeroes n_zero ints at `zero` (counters the later stages start from).
 __global__ __launch_bounds__(1024) void k_ovf_list(int64_t T, int32_t cap, const uint8_t* __restrict__ row_ovf,
                                                    int32_t* __restrict__ ovf_rows, int32_t* __restrict__ n_ovf,
-                                                   sfl_stats_t* __restrict__ stats) {
+                                                   sfl_stats_t* __restrict__ stats, int32_t* __restrict__ zero,
+                                                   int n_zero) {
   __shared__ int wsum[16];
   const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
+  for (int i = tid; i < n_zero; i += 1024) zero[i] = 0;
   int64_t base = 0;
   for (int64_t r0 = 0; r0 < T; r0 += 1024 * kOvfRowsPerThread) {
     const int64_t t0 = r0 + (int64_t)tid * kOvfRowsPerThread;
@@ -337,8 +340,9 @@ __global__ __launch_bounds__(1024) void k_ovf_list(int64_t T, int32_t cap, const
 }
 
 hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32_t* ovf_rows, int32_t* n_ovf,
-                           sfl_stats_t* stats, hipStream_t s) {
-  hipLaunchKernelGGL(k_ovf_list, dim3(1), dim3(1024), 0, s, T, cap, row_ovf, ovf_rows, n_ovf, stats);
+                           sfl_stats_t* stats, hipStream_t s, int32_t* zero, int n_zero) {
+  hipLaunchKernelGGL(k_ovf_list, dim3(1), dim3(1024), 0, s, T, cap, row_ovf, ovf_rows, n_ovf, stats, zero,
+                     zero ? n_zero : 0);
   return hipGetLastError();
 }
 

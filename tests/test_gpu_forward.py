@@ -205,6 +205,27 @@ def test_bias_and_shift_in_the_fused_epilogue(T, f, Tn, S, use_wupt):
     assert rel_l2(to_f64(Y), Yref) <= 2e-2
 
 
+@pytest.mark.parametrize("copies", [False, True])
+@pytest.mark.parametrize("gated", [False, True])
+@pytest.mark.parametrize("T", [5, 48])
+def test_small_batch_dense_backup_rows(T, gated, copies):
+    """Batches of at most 64 rows with dense-backup rows (half the rows all active): with
+    K-contiguous weight copies their GEMMs split K without a reduction kernel (the last
+    block of each tile adds the partial sums, counted with per-tile counters). Two calls in
+    a row, so the second starts from the counters the first left behind."""
+    w = wl.make_ffn("small-ovf", "bf16", T, 1024, 2048, seed=T + 2 * gated, gated=gated, sparsity=0.97,
+                    ell_width=128)
+    w.shift_t[::2] = 100.0
+    Yref, _ = oracle_rows(w, np.arange(T))
+    for _ in range(2):
+        Y, bufs, stats, cfg = run_forward(w, use_wupt=copies, use_wgatet=copies and gated, use_wdownt=copies)
+        got = twell_views(bufs, T, w.f, cfg)
+        assert got["row_ovf"][::2].all() and not got["row_ovf"][1::2].any() and got["n_ovf"] == (T + 1) // 2
+        assert rel_l2(to_f64(Y), Yref) <= 2e-2
+        ovf = np.nonzero(got["row_ovf"])[0]
+        assert rel_l2(to_f64(Y)[ovf], Yref[ovf]) <= 2e-2
+
+
 @pytest.mark.parametrize("T", [1, 17, 48, 64])
 def test_small_batch_split_gemm(T):
     """Batches of at most 64 rows with K-contiguous weights take the split-K GEMMs (K
