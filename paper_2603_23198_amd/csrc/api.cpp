@@ -125,7 +125,8 @@ struct FwdPlan {
   int32_t* need_rows = nullptr;  // their token rows [cap]
   int32_t* need_slots = nullptr; // their ovf_dense rows [cap]
   int32_t* n_need = nullptr;     // [1]
-  int32_t* tile_sem = nullptr;   // dense-backup GEMMs of at most 64 rows: per-tile counters [256]
+  int32_t* tile_sem = nullptr;   // dense-backup GEMMs of at most 64 rows: one counter per 256-column tile
+  int n_sem = 0;                  // counters in tile_sem: 256-column tiles of the wider of f and d
   size_t bytes = 0;
 };
 
@@ -156,7 +157,10 @@ FwdPlan plan_forward(const sfl_ffn_args_t& a, void* ws) {
     p.part_rows = (int)std::min<int64_t>(align_rows(std::max<int64_t>(cap, a.T)), kPartRows);
     p.part = (float*)c.take((size_t)p.part_rows * std::max(a.f, a.d) * 4);
   }
-  if (a.dtype == SFL_BF16 && cap > 0 && cap <= 64) p.tile_sem = (int32_t*)c.take(256 * 4);
+  if (a.dtype == SFL_BF16 && cap > 0 && cap <= 64) {
+    p.n_sem = (int)cdiv(std::max(a.f, a.d), 256);
+    p.tile_sem = (int32_t*)c.take((size_t)p.n_sem * 4);
+  }
   if (cap > 0 && rebuild_ovf(a)) {
     p.need = (uint8_t*)c.take((size_t)cap);
     p.need_rows = (int32_t*)c.take((size_t)cap * 4);
@@ -398,7 +402,7 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
   // 2. hybrid classification (Sec. 3.4)
   SFL_HIP(launch_classify(T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, a->cfg.ell_width, tw.val, tw.idx, tw.cnt,
                           tw.row_nnz, tw.row_ovf, tw.ell_val, tw.ell_idx, a->stats, s));
-  SFL_HIP(launch_ovf_list(T, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s, plan.tile_sem, 256));
+  SFL_HIP(launch_ovf_list(T, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s, plan.tile_sem, plan.n_sem));
   ev.record(2, s);
   // 3. sparse down projection of the ELL rows
   const void* WupT = a->W_upT;  // gated: W_up^T, given or built in the workspace when needed

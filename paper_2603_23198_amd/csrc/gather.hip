@@ -143,6 +143,11 @@ constexpr int GU = SFL_GATHER_UNROLL;       // row loads in flight per lane
 constexpr int GU_SHORT = 12;
 inline bool use_short_unroll(int K, int64_t lds_per_wg) { return K <= 128 && 2 * lds_per_wg > 160 * 1024; }
 constexpr int GATHER_LDS = SFL_GATHER_LDS;  // bytes of cached ELL entries per workgroup
+// bf16-valued entries (the forward's down projection): two row loads per lane, 16 entries
+// per round. The workgroup's requests already exceed what a CU keeps in flight, so a
+// deeper round buys nothing, while the last round of a token's slice, mostly empty for
+// short rows, costs its full issue (99 % rows of 164 entries, 99.9 % rows of 16).
+constexpr int GU_BF16 = 2;
 
 // Sum of the 8 groups' partial sums (lanes l, l ^ 8, ..., l ^ 56) into every group: the
 // partner 8 lanes away is in the same 16-lane row (DPP row_ror:8), the other two steps
@@ -625,7 +630,7 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
     else                                              \
       SFL_GATHER_LAUNCH_U(VK_, OUT_, GU);             \
   } while (0)
-  if (vk == 0 && out_mode == 0) SFL_GATHER_LAUNCH(0, 0);
+  if (vk == 0 && out_mode == 0) SFL_GATHER_LAUNCH_U(0, 0, GU_BF16);
   else if (vk == 1 && out_mode == 0) SFL_GATHER_LAUNCH(1, 0);
   else if (vk == 1 && out_mode == 1) SFL_GATHER_LAUNCH(1, 1);
   else if (vk == 1 && out_mode == 2) SFL_GATHER_LAUNCH(1, 2);

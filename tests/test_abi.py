@@ -94,8 +94,12 @@ def test_workspace_sizes():
     # the GEMM still recomputes are listed in the workspace
     big = _fake_args(b.SFL_BF16, 512, 256, 1024, ell_width=32, ovf_capacity=64)
     big.twell.ovf_dense = 0x2000
-    # partial sums: 512 rows (T); a capacity of at most 64 rows adds 256 per-tile counters
-    assert b.sfl_workspace_size(big, 0) == 512 * 1024 * 4 + _need_lists(64) + _al(256 * 4)
+    # partial sums: 512 rows (T); a capacity of at most 64 rows adds one counter per
+    # 256-column tile of the wider of f and d
+    assert b.sfl_workspace_size(big, 0) == 512 * 1024 * 4 + _need_lists(64) + _al(4 * 4)
+    wide = _fake_args(b.SFL_BF16, 512, 70016, 1024, ell_width=32, ovf_capacity=64)
+    wide.twell.ovf_dense = 0x2000
+    assert b.sfl_workspace_size(wide, 0) == 512 * 70016 * 4 + _need_lists(64) + _al(4 * 274)
     assert b.sfl_workspace_size(a, 2) == 128 * 1024 * 2 + part  # dense baseline: H, split-K partials (T <= 256)
 
 
