@@ -503,3 +503,28 @@ def test_c3_gated_in_the_bench_configuration():
     check_pattern(got, G, rows[:48], w.f, cfg.tile_cols, cfg.tile_slots)
     Yd, _, _, _ = run_forward(w, dense=True, use_wupt=True, use_wgatet=True, use_wdownt=True)
     assert rel_l2(to_f64(Yd)[rows], Yref) <= 2e-2
+
+
+@pytest.mark.parametrize("force_ovf", [False, True])
+def test_c3_decode_in_the_bench_configuration(force_ovf):
+    """The gated decode workload (T=32, d=4096, f=14336) as bench.py launches it: every
+    row against the oracle, sparse and dense. With a quarter of the rows made all-active,
+    the dense-backup GEMMs of that width split K over the CUs and the last block of each
+    output tile adds the partial sums; two calls in a row reuse the tile counters."""
+    w = wl.c3_gated(T=32)
+    if force_ovf:
+        w.shift_t[::4] = 100.0
+    rows = np.arange(w.T)
+    Yref, G = oracle_rows(w, rows)
+    for _ in range(2 if force_ovf else 1):
+        Y, bufs, stats, cfg = run_forward(w, use_wupt=True, use_wgatet=True, use_wdownt=True, packed_down=True,
+                                          packed_up=True)
+        got = twell_views(bufs, w.T, w.f, cfg)
+        if force_ovf:
+            assert got["row_ovf"][::4].all() and got["n_ovf"] >= 8
+        assert rel_l2(to_f64(Y), Yref) <= 2e-2
+        sparse = np.nonzero(~got["row_ovf"].astype(bool))[0]
+        assert rel_l2(to_f64(Y)[sparse], Yref[sparse]) <= 2e-2
+        check_pattern(got, G[sparse[:8]], sparse[:8], w.f, cfg.tile_cols, cfg.tile_slots)
+    Yd, _, _, _ = run_forward(w, dense=True, use_wupt=True, use_wgatet=True, use_wdownt=True)
+    assert rel_l2(to_f64(Yd), Yref) <= 2e-2
