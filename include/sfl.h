@@ -21,8 +21,9 @@
  *    (how many rows overflowed, whether the dense-backup capacity was exceeded)
  *    are written to device memory (sfl_twell_t.n_ovf, sfl_stats_t) and can be
  *    read after the caller's own synchronisation.
- *  - Reentrancy: no global mutable state; concurrent calls on different streams
- *    with disjoint buffers are safe.
+ *  - Reentrancy: no global mutable state beyond a per-device cache of the CU
+ *    count; concurrent calls on different streams with disjoint buffers
+ *    (workspaces included) are safe.
  *  - Numerics: bf16 inputs are multiplied on MFMA with float32 accumulation;
  *    activations are stored in the activation dtype, bf16 by round-to-nearest-
  *    even. A hidden unit is active iff its pre-activation is > 0 (strict; +0,

@@ -17,7 +17,7 @@ import tempfile
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsfl.so")
-ARCH = os.environ.get("SFL_OFFLOAD_ARCH", "gfx950")
+ARCH = "gfx950"  # the kernels use CDNA4 instructions (MFMA 16x16x32 bf16, ds_read_b64_tr_b16)
 
 FLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

@@ -23,6 +23,7 @@
 #include "internal.h"
 
 #include <algorithm>
+#include <atomic>
 
 namespace sfl {
 
@@ -981,17 +982,18 @@ __global__ __launch_bounds__(NTHR) void k_gemm_few_rows(GemmParams p) {
   if (threadIdx.x == 0) p.tile_sem[n0 / BN] = 0;
 }
 
-// Compute units of the current device (cached per device).
+// Compute units of the current device (cached per device; threads that race on the first
+// query store the same value).
 int device_cus() {
-  static int cus[64];
+  static std::atomic<int> cus[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cus[dev] <= 0) {
-    int n = 0;
+  int n = cus[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    cus[dev] = n;
+    cus[dev].store(n, std::memory_order_relaxed);
   }
-  return cus[dev];
+  return n;
 }
 
 template <int EPI, int Tn = 0, int BL = LAY_KC>
