@@ -13,7 +13,8 @@ speedup. Per-stage times come from HIP events the library records on its stream.
 
 The same JSON line also reports the other workloads of the hot path (sparsity sweep,
 lognormal row counts with dense-backup rows, gated forward at prefill and decode sizes,
-and the training step: forward + backward with the L1 term). `--quick` skips them.
+the training step: forward + backward with the L1 term, and one GPU's share of the
+headline layer split eight ways over hidden units or over tokens). `--quick` skips them.
 `--gpus` above 1 is refused: the benchmark runs on one GPU.
 """
 from __future__ import annotations
@@ -46,7 +47,7 @@ def parse():
     p.add_argument("--quick", action="store_true", help="headline workload only")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="first run one plain 256 MiB device copy (reference for HBM byte counters)")
-    p.add_argument("--only", choices=["lognormal", "gated", "decode", "train", "gated_train"],
+    p.add_argument("--only", choices=["lognormal", "gated", "decode", "train", "gated_train", "tp8", "dp8"],
                    help="run one secondary workload and print its record (for profiling); no headline line")
     return p.parse_args()
 
@@ -373,7 +374,8 @@ def main():
             rec = B.training_record(wt, 2e-5)
         else:
             wo = {"lognormal": wl.c2_lognormal, "gated": lambda: wl.c3_gated(T=8192),
-                  "decode": lambda: wl.c3_gated(T=32)}[a.only]()
+                  "decode": lambda: wl.c3_gated(T=32), "tp8": lambda: wl.c4_shard("tp8"),
+                  "dp8": lambda: wl.c4_shard("dp8")}[a.only]()
             rec = B.forward_record(wo)[0]
         print(json.dumps({"only": a.only, "record": rec}), flush=True)
         return
@@ -478,6 +480,16 @@ def main():
             others.append(r)
             del s2
         out["other_workloads"] = others
+        # one GPU's share of the headline layer run on eight GPUs: hidden units split eight
+        # ways (tensor parallel, f = 2048) or tokens split eight ways (data parallel, T = 1024);
+        # the collectives around them are not part of this record
+        shards = []
+        for kind in ("tp8", "dp8"):
+            r, s2, _ = B.forward_record(wl.c4_shard(kind, T=a.tokens))
+            r["shard"] = kind
+            shards.append(r)
+            del s2
+        out["shard_shapes"] = shards
         torch.cuda.empty_cache()
         w5 = wl.c5_training()
         out["training_step"] = B.training_record(w5, 2e-5)

@@ -172,11 +172,23 @@ FwdPlan plan_forward(const sfl_ffn_args_t& a, void* ws) {
 }
 
 // The dense baseline's workspace: H [T][f], then (small batches) split-K partial sums.
-bool dense_split(const sfl_ffn_args_t& a) { return a.dtype == SFL_BF16 && a.T <= 256; }
+// K splits of a dense baseline GEMM C [M][N] = A [M][K] B: a bf16 GEMM whose 256 x 256
+// output tiles fill at most half of the 256 CUs splits K, into as many ranges as keep the
+// items within one block per CU (at most kMaxSplit, at least 256 of K per range), with
+// fp32 partial sums [split][M][N] of at most kDenseParts elements.
+constexpr int64_t kDenseParts = (int64_t)256 * 256 * 256;
+int dense_ks(const sfl_ffn_args_t& a, int64_t M, int64_t N, int64_t K) {
+  const int64_t tiles = cdiv(M, 256) * cdiv(N, 256);
+  if (a.dtype != SFL_BF16 || M * N == 0 || tiles > 128) return 1;
+  return (int)std::max<int64_t>(
+      1, std::min<int64_t>({(int64_t)kMaxSplit, K / 256, 256 / tiles, kDenseParts / (M * N)}));
+}
+int64_t dense_part_elems(const sfl_ffn_args_t& a) {
+  const int ku = dense_ks(a, a.T, a.f, a.d), kd = dense_ks(a, a.T, a.d, a.f);
+  return std::max<int64_t>(ku > 1 ? ku * a.T * a.f : 0, kd > 1 ? kd * a.T * a.d : 0);
+}
 size_t dense_ws_bytes(const sfl_ffn_args_t& a) {
-  size_t n = align_up((size_t)a.T * a.f * elem_size(a.dtype));
-  if (dense_split(a)) n += align_up((size_t)256 * std::max(a.f, a.d) * 4);
-  return n;
+  return align_up((size_t)a.T * a.f * elem_size(a.dtype)) + align_up((size_t)dense_part_elems(a) * 4);
 }
 
 GemmParams gp_zero() {
@@ -530,10 +542,12 @@ sfl_status_t sfl_dense_ffn_baseline(const sfl_ffn_args_t* a, sfl_stream_t stream
   g.shift = a->shift_t;
   g.C = a->workspace;
   g.ldc = f;
-  if (dense_split(*a)) {
-    g.ksplit = kMaxSplit;
-    g.part = (float*)((char*)a->workspace + align_up((size_t)T * f * 2));
-    g.part_rows = 256;
+  float* part = (float*)((char*)a->workspace + align_up((size_t)T * f * 2));
+  const int ks_up = dense_ks(*a, T, f, d), ks_down = dense_ks(*a, T, d, f);
+  if (ks_up > 1) {
+    g.ksplit = ks_up;
+    g.part = part;
+    g.part_rows = (int)(ks_up * T);
   }
   SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_ACT_RELU, g, s));
   if (a->gated) {
@@ -554,9 +568,11 @@ sfl_status_t sfl_dense_ffn_baseline(const sfl_ffn_args_t* a, sfl_stream_t stream
   set_down_B(y, a->W_down, bf ? a->W_downT : nullptr, d, f, &blay);
   y.C = a->Y;
   y.ldc = d;
-  y.ksplit = g.ksplit;
-  y.part = g.part;
-  y.part_rows = g.part_rows;
+  if (ks_down > 1) {
+    y.ksplit = ks_down;
+    y.part = part;
+    y.part_rows = (int)(ks_down * T);
+  }
   SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_ACT, y, s));
   ev.record(2, s);
   return SFL_OK;

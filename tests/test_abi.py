@@ -100,7 +100,15 @@ def test_workspace_sizes():
     wide = _fake_args(b.SFL_BF16, 512, 70016, 1024, ell_width=32, ovf_capacity=64)
     wide.twell.ovf_dense = 0x2000
     assert b.sfl_workspace_size(wide, 0) == 512 * 70016 * 4 + _need_lists(64) + _al(4 * 274)
-    assert b.sfl_workspace_size(a, 2) == 128 * 1024 * 2 + part  # dense baseline: H, split-K partials (T <= 256)
+    # dense baseline: H, then split-K partials for a GEMM whose 256 x 256 tiles fill at most
+    # half of the CUs (here the down GEMM, K = 1024: four ranges of 256) -- at most 8 splits,
+    # 256 of K each, items within one block per CU, 64 MiB of partial sums
+    assert b.sfl_workspace_size(a, 2) == 128 * 1024 * 2 + 4 * 128 * 256 * 4
+    for T, d, f, ks_up, ks_down in [(1024, 4096, 16384, 1, 4), (32, 4096, 14336, 4, 8), (8192, 4096, 16384, 1, 1),
+                                    (256, 4096, 16384, 4, 8)]:
+        g = _fake_args(b.SFL_BF16, T, d, f)
+        parts = max(ks_up * T * f if ks_up > 1 else 0, ks_down * T * d if ks_down > 1 else 0)
+        assert b.sfl_workspace_size(g, 2) == _al(T * f * 2) + _al(parts * 4), (T, d, f)
 
 
 def test_unsupported_shapes_and_missing_pointers():

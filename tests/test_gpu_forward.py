@@ -528,3 +528,19 @@ def test_c3_decode_in_the_bench_configuration(force_ovf):
         check_pattern(got, G[sparse[:8]], sparse[:8], w.f, cfg.tile_cols, cfg.tile_slots)
     Yd, _, _, _ = run_forward(w, dense=True, use_wupt=True, use_wgatet=True, use_wdownt=True)
     assert rel_l2(to_f64(Yd), Yref) <= 2e-2
+
+
+@pytest.mark.parametrize("kind", ["tp8", "dp8"])
+def test_shard_shapes_in_the_bench_configuration(kind):
+    """One GPU's share of the headline layer split eight ways, over hidden units (f = 2048,
+    K = 64; the up GEMM is a single round of 256 tiles) or over tokens (T = 1024): sampled
+    rows and their patterns against the oracle, and the dense baseline."""
+    w = wl.c4_shard(kind)
+    Y, bufs, stats, cfg = run_forward(w, use_wupt=True, use_wdownt=True, packed_down=True)
+    got = twell_views(bufs, w.T, w.f, cfg)
+    rows = sample_rows(w.T, 128, 23, extra=np.nonzero(got["row_ovf"])[0][:16])
+    Yref, Z = oracle_rows(w, rows)
+    assert rel_l2(to_f64(Y)[rows], Yref) <= 2e-2
+    check_pattern(got, Z, rows[:48], w.f, cfg.tile_cols, cfg.tile_slots)
+    Yd, _, _, _ = run_forward(w, dense=True, use_wupt=True, use_wdownt=True)
+    assert rel_l2(to_f64(Yd)[rows], Yref) <= 2e-2

@@ -168,6 +168,23 @@ def c4_sweep(sparsity=0.99, seed=0, T=8192, d=4096, f=16384, ell_width=None, til
                     ell_width=ell_width or K)
 
 
+def c4_shard(kind, T=8192, d=4096, f=16384, sparsity=0.99):
+    """One GPU's share of the 99 % layer when it runs on eight GPUs: hidden units split
+    eight ways (kind "tp8": f/8 units, K = ceil((mean + 6 sd)/64)*64 of Binomial(f/8, 1-s))
+    or tokens split eight ways (kind "dp8": T/8 tokens, the full layer's K)."""
+    if kind == "tp8":
+        fs = f // 8
+        mean, sd = fs * (1 - sparsity), math.sqrt(fs * sparsity * (1 - sparsity))
+        K = int(math.ceil((mean + 6 * sd) / 64) * 64)
+        w = c4_sweep(sparsity, T=T, d=d, f=fs, ell_width=K)
+    elif kind == "dp8":
+        w = c4_sweep(sparsity, T=T // 8, d=d, f=f)
+    else:
+        raise ValueError(kind)
+    w.name = f"{kind} shard of the {int(round(sparsity * 100))} % layer: " + w.name
+    return w
+
+
 def c5_training(seed=0, T=16384, d=4096, f=16384, sparsity=0.99):
     return make_ffn(f"train bf16 T={T} d={d} f={f} s={sparsity}", "bf16", T, d, f, seed=seed,
                     sparsity=sparsity, tile_rows=32, tile_slots=32, ell_width=256, with_dy=True)
