@@ -148,6 +148,13 @@ constexpr int GATHER_LDS = SFL_GATHER_LDS;  // bytes of cached ELL entries per w
 // deeper round buys nothing, while the last round of a token's slice, mostly empty for
 // short rows, costs its full issue (99 % rows of 164 entries, 99.9 % rows of 16).
 constexpr int GU_BF16 = 2;
+// Rows of at most kTokenGroupK entries (ELL width K <= 64: about 16-20 entries per row at
+// 99.9 % of 16384 units or 99 % of 2048) are walked by token groups instead: a work item
+// is (slice, 8 tokens), each lane group on its own token, 4 row loads per lane in flight.
+// With so few entries the per-(slice, token) fold of the 8 groups' partial sums, the
+// conversion and the store would otherwise cost more issue than the loads themselves.
+constexpr int kTokenGroupK = 64;
+constexpr int GU_GROUP = 4;
 
 // Sum of the 8 groups' partial sums (lanes l, l ^ 8, ..., l ^ 56) into every group: the
 // partner 8 lanes away is in the same 16-lane row (DPP row_ror:8), the other two steps
@@ -234,14 +241,16 @@ __device__ __forceinline__ void slice_token_f32(const uint32_t* er, int nnz, __a
 // VK: kind of the ELL values. 0: bf16 (packed with the index in one word); 1: fp32 (the
 // backward's dz, two words per entry). OUT: 0: bf16 Y; 1: fp32 Yf; 2: bf16 Y of the sum
 // with the fp32 addend Yf (the second of two passes that share an accumulator).
-template <int VK, int OUT, int U>
+template <int VK, int OUT, int U, bool TG = false>
 __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
     int64_t T, int64_t d, int64_t f, int K, const void* __restrict__ ell_val, const uint16_t* __restrict__ ell_idx,
     const int32_t* __restrict__ row_nnz, const uint8_t* __restrict__ row_ovf, const bf16_t* __restrict__ W,
     bf16_t* __restrict__ Y, float* __restrict__ Yf, int n_slices, int tpw) {
   constexpr int EW = VK + 1;         // words per staged entry
-  extern __shared__ uint32_t ent[];  // [tpw][K] entries, then [tpw] counts (-1 = skip)
-  int* cnt_s = (int*)(ent + (size_t)tpw * K * EW);
+  // token groups read 8 tokens' entries at once: an odd stride puts them in different banks
+  const int KS = TG ? K + 1 : K;
+  extern __shared__ uint32_t ent[];  // [tpw][KS] entries, then [tpw] counts (-1 = skip)
+  int* cnt_s = (int*)(ent + (size_t)tpw * KS * EW);
   const int xcd = blockIdx.x & 7;
   const int64_t t0 = (int64_t)(blockIdx.x >> 3) * tpw;
   const int l = threadIdx.x & 63;
@@ -258,10 +267,10 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
     const int64_t t = t0 + i;
     for (int e = l; e < c; e += 64) {
       if constexpr (VK >= 1) {
-        ent[EW * (i * K + e)] = (uint32_t)ell_idx[t * K + e];
-        ent[EW * (i * K + e) + 1] = __float_as_uint(((const float*)ell_val)[t * K + e]);
+        ent[EW * (i * KS + e)] = (uint32_t)ell_idx[t * K + e];
+        ent[EW * (i * KS + e) + 1] = __float_as_uint(((const float*)ell_val)[t * K + e]);
       } else {
-        ent[i * K + e] = (uint32_t)ell_idx[t * K + e] | ((uint32_t)((const bf16_t*)ell_val)[t * K + e] << 16);
+        ent[i * KS + e] = (uint32_t)ell_idx[t * K + e] | ((uint32_t)((const bf16_t*)ell_val)[t * K + e] << 16);
       }
     }
   }
@@ -271,6 +280,59 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
   // waves: the workgroup walks the slices in order, and a small block (decode) still
   // keeps every wave busy
   const int nsl = (n_slices - xcd + 7) / 8;
+  if constexpr (TG) {
+    static_assert(VK == 0 && OUT == 0 && U % 2 == 0, "token groups: bf16 values, bf16 Y");
+    // Short rows: a work item is (slice, NGRP tokens), lane group g walking token g's
+    // entries on its own, so that no partial sums are folded across groups; the wave runs
+    // to the longest of its tokens' rows (absent entries load nothing and add 0).
+    constexpr uint32_t row_b = SLICE2 * 2;
+    const int n_grp = (tpw + NGRP - 1) / NGRP;
+    for (int it = wave; it < nsl * n_grp; it += GATHER_WAVES) {
+      const int slice = xcd + 8 * (it / n_grp);
+      const int i = (it % n_grp) * NGRP + grp;
+      const int c = i < tpw ? cnt_s[i] : -1;
+      int cmax = c;
+#pragma unroll
+      for (int o = 8; o < 64; o <<= 1) cmax = max(cmax, __shfl_xor(cmax, o, 64));
+      cmax = __builtin_amdgcn_readfirstlane(cmax);
+      if (cmax < 0) continue;
+      const uint32_t col_b = (uint32_t)(slice * f * SLICE2 * 2) + (uint32_t)sub * 16u;
+      const uint32_t* er = ent + (size_t)(i < tpw ? i : 0) * KS;
+      float acc[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+      for (int e0 = 0; e0 < cmax; e0 += U) {
+        u32x4_t w[U];
+        uint32_t x[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const bool ok = e0 + u < c;
+          x[u] = ok ? er[e0 + u] : 0u;  // an absent entry has value 0 (and its load reads 0)
+          const uint32_t off = ok ? (x[u] & 0xffffu) * row_b + col_b : 0x80000000u;
+          w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0));
+        }
+#pragma unroll
+        for (int u = 0; u < U; u += 2) {
+          const bf16x2_t vv = __builtin_bit_cast(bf16x2_t, __builtin_amdgcn_perm(x[u + 1], x[u], 0x07060302u));
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const bf16x2_t lo = __builtin_bit_cast(bf16x2_t, __builtin_amdgcn_perm(w[u + 1][j], w[u][j], 0x05040100u));
+            const bf16x2_t hi = __builtin_bit_cast(bf16x2_t, __builtin_amdgcn_perm(w[u + 1][j], w[u][j], 0x07060302u));
+            acc[2 * j] = __builtin_amdgcn_fdot2_f32_bf16(vv, lo, acc[2 * j], false);
+            acc[2 * j + 1] = __builtin_amdgcn_fdot2_f32_bf16(vv, hi, acc[2 * j + 1], false);
+          }
+        }
+      }
+      if (c >= 0) {
+        u32x4_t out;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          out[j] = (uint32_t)f32_to_bf16(acc[2 * j]) | ((uint32_t)f32_to_bf16(acc[2 * j + 1]) << 16);
+        *(u32x4_t*)(Y + (t0 + i) * d + (int64_t)slice * SLICE2 + sub * 8) = out;
+      }
+    }
+    return;
+  }
   for (int it = wave; it < nsl * tpw; it += GATHER_WAVES) {
     const int slice = xcd + 8 * (it / tpw);
     const int i = it % tpw;
@@ -606,23 +668,26 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
   const int n_slices = (int)(d / SLICE2);
   const int vk = val_f32 ? 1 : 0;
 
-  const int64_t per_tok = (int64_t)std::max(K, 1) * 4 * (vk + 1) + 4;
+  // bf16 rows of at most kTokenGroupK entries take the token-group walk (padded rows)
+  const bool groups = vk == 0 && out_mode == 0 && K <= kTokenGroupK;
+  const int64_t per_tok = (int64_t)(std::max(K, 1) + (groups ? 1 : 0)) * 4 * (vk + 1) + 4;
   const int tpw = slice_walk_tpw(T, per_tok);
   const int64_t blocks = cdiv(T, tpw);
   const size_t lds = (size_t)tpw * per_tok;
   if (lds > 160 * 1024) return hipErrorInvalidValue;
   const dim3 grid((unsigned)(8 * blocks)), block(GATHER_WAVES * 64);
   const bool short_rows = use_short_unroll(K, (int64_t)lds);
-#define SFL_GATHER_LAUNCH_U(VK_, OUT_, U_)                                                                          \
+#define SFL_GATHER_LAUNCH_G(VK_, OUT_, U_, TG_)                                                                     \
   do {                                                                                                             \
     if (lds > 65536) {                                                                                             \
-      const hipError_t e = hipFuncSetAttribute((const void*)k_gather_down_b16<VK_, OUT_, U_>,                      \
+      const hipError_t e = hipFuncSetAttribute((const void*)k_gather_down_b16<VK_, OUT_, U_, TG_>,                 \
                                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);              \
       if (e != hipSuccess) return e;                                                                               \
     }                                                                                                              \
-    hipLaunchKernelGGL((k_gather_down_b16<VK_, OUT_, U_>), grid, block, lds, s, T, d, f, K, ell_val, ell_idx,      \
+    hipLaunchKernelGGL((k_gather_down_b16<VK_, OUT_, U_, TG_>), grid, block, lds, s, T, d, f, K, ell_val, ell_idx, \
                        row_nnz, row_ovf, (const bf16_t*)Wp, (bf16_t*)Y, Yf, n_slices, tpw);                        \
   } while (0)
+#define SFL_GATHER_LAUNCH_U(VK_, OUT_, U_) SFL_GATHER_LAUNCH_G(VK_, OUT_, U_, false)
 #define SFL_GATHER_LAUNCH(VK_, OUT_)                  \
   do {                                                \
     if (short_rows)                                   \
@@ -630,13 +695,15 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
     else                                              \
       SFL_GATHER_LAUNCH_U(VK_, OUT_, GU);             \
   } while (0)
-  if (vk == 0 && out_mode == 0) SFL_GATHER_LAUNCH_U(0, 0, GU_BF16);
+  if (groups) SFL_GATHER_LAUNCH_G(0, 0, GU_GROUP, true);
+  else if (vk == 0 && out_mode == 0) SFL_GATHER_LAUNCH_U(0, 0, GU_BF16);
   else if (vk == 1 && out_mode == 0) SFL_GATHER_LAUNCH(1, 0);
   else if (vk == 1 && out_mode == 1) SFL_GATHER_LAUNCH(1, 1);
   else if (vk == 1 && out_mode == 2) SFL_GATHER_LAUNCH(1, 2);
   else return hipErrorInvalidValue;
 #undef SFL_GATHER_LAUNCH
 #undef SFL_GATHER_LAUNCH_U
+#undef SFL_GATHER_LAUNCH_G
   return hipGetLastError();
 }
 

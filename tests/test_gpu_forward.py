@@ -544,3 +544,26 @@ def test_shard_shapes_in_the_bench_configuration(kind):
     check_pattern(got, Z, rows[:48], w.f, cfg.tile_cols, cfg.tile_slots)
     Yd, _, _, _ = run_forward(w, dense=True, use_wupt=True, use_wdownt=True)
     assert rel_l2(to_f64(Yd)[rows], Yref) <= 2e-2
+
+
+@pytest.mark.parametrize("T,K", [(1, 64), (9, 32), (777, 64), (2053, 48)])
+def test_token_group_walk_short_rows(T, K):
+    """ELL widths of at most 64 take the token-group walk of the down projection (8 tokens
+    per work item, each lane group on its own token): ragged batches whose last group is
+    partly empty, all-active rows (dense backup, skipped by the walk) and all-inactive rows
+    (Y exactly 0) among ordinary rows of about 20 entries."""
+    w = wl.make_ffn("short-rows", "bf16", T, 1024, 2048, seed=T + K, sparsity=0.99, ell_width=K)
+    zero = np.setdiff1d(np.arange(3, T, 5), np.arange(1, T, 7))
+    if T > 2:
+        w.shift_t[3::5] = -100.0
+        w.shift_t[1::7] = 100.0
+    Y, bufs, stats, cfg = run_forward(w, use_wupt=True, use_wdownt=True, packed_down=True)
+    got = twell_views(bufs, T, w.f, cfg)
+    Yref, Z = oracle_rows(w, np.arange(T))
+    assert rel_l2(to_f64(Y), Yref) <= 2e-2
+    ovf = got["row_ovf"].astype(bool)
+    if T > 2:
+        assert ovf[1::7].all() and int(got["row_nnz"][zero].max()) == 0
+        assert (host_bits(Y)[zero] == 0).all()
+    sparse = np.nonzero(~ovf)[0]
+    assert len(sparse) > 0 and rel_l2(to_f64(Y)[sparse], Yref[sparse]) <= 2e-2
