@@ -148,12 +148,15 @@ constexpr int GATHER_LDS = SFL_GATHER_LDS;  // bytes of cached ELL entries per w
 // deeper round buys nothing, while the last round of a token's slice, mostly empty for
 // short rows, costs its full issue (99 % rows of 164 entries, 99.9 % rows of 16).
 constexpr int GU_BF16 = 2;
-// Rows of at most kTokenGroupK entries (ELL width K <= 64: about 16-20 entries per row at
-// 99.9 % of 16384 units or 99 % of 2048) are walked by token groups instead: a work item
-// is (slice, 8 tokens), each lane group on its own token, 4 row loads per lane in flight.
-// With so few entries the per-(slice, token) fold of the 8 groups' partial sums, the
-// conversion and the store would otherwise cost more issue than the loads themselves.
-constexpr int kTokenGroupK = 64;
+// Batches of at least kTokenGroupT tokens with ELL rows of at most kTokenGroupK entries are
+// walked by token groups instead: a work item is (slice, 8 tokens), each lane group on its
+// own token, 4 row loads per lane in flight. The per-(slice, token) fold of the 8 groups'
+// partial sums, the conversion and the store are then shared by 8 tokens (at 16-164
+// entries per row they cost as much issue as the loads); the wave runs to the longest of
+// its 8 rows, which rows of about a thousand entries (95 %) or of widely varying length
+// (lognormal counts) pay for, and a small batch leaves most groups of a block empty.
+constexpr int kTokenGroupK = 256;
+constexpr int64_t kTokenGroupT = 1024;
 constexpr int GU_GROUP = 4;
 
 // Sum of the 8 groups' partial sums (lanes l, l ^ 8, ..., l ^ 56) into every group: the
@@ -668,8 +671,8 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
   const int n_slices = (int)(d / SLICE2);
   const int vk = val_f32 ? 1 : 0;
 
-  // bf16 rows of at most kTokenGroupK entries take the token-group walk (padded rows)
-  const bool groups = vk == 0 && out_mode == 0 && K <= kTokenGroupK;
+  // bf16 values, rows of at most kTokenGroupK entries, large batches: token-group walk
+  const bool groups = vk == 0 && out_mode == 0 && K <= kTokenGroupK && T >= kTokenGroupT;
   const int64_t per_tok = (int64_t)(std::max(K, 1) + (groups ? 1 : 0)) * 4 * (vk + 1) + 4;
   const int tpw = slice_walk_tpw(T, per_tok);
   const int64_t blocks = cdiv(T, tpw);

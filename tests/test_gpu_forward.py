@@ -546,12 +546,13 @@ def test_shard_shapes_in_the_bench_configuration(kind):
     assert rel_l2(to_f64(Yd)[rows], Yref) <= 2e-2
 
 
-@pytest.mark.parametrize("T,K", [(1, 64), (9, 32), (777, 64), (2053, 48)])
+@pytest.mark.parametrize("T,K", [(1, 64), (9, 32), (777, 64), (1024, 64), (1031, 256), (2053, 48), (4100, 128)])
 def test_token_group_walk_short_rows(T, K):
-    """ELL widths of at most 64 take the token-group walk of the down projection (8 tokens
-    per work item, each lane group on its own token): ragged batches whose last group is
-    partly empty, all-active rows (dense backup, skipped by the walk) and all-inactive rows
-    (Y exactly 0) among ordinary rows of about 20 entries."""
+    """Batches of at least 1024 tokens with ELL widths of at most 256 take the token-group
+    walk of the down projection (8 tokens per work item, each lane group on its own token;
+    smaller batches the per-token walk): ragged batches whose last group is partly empty,
+    all-active rows (dense backup, skipped by the walk) and all-inactive rows (Y exactly 0)
+    among ordinary rows of about 20 entries."""
     w = wl.make_ffn("short-rows", "bf16", T, 1024, 2048, seed=T + K, sparsity=0.99, ell_width=K)
     zero = np.setdiff1d(np.arange(3, T, 5), np.arange(1, T, 7))
     if T > 2:
