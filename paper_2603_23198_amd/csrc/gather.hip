@@ -158,6 +158,8 @@ constexpr int GU_BF16 = 2;
 constexpr int kTokenGroupK = 256;
 constexpr int64_t kTokenGroupT = 1024;
 constexpr int GU_GROUP = 4;
+// The backward's per-unit gathers group units the same way when their lists are short.
+constexpr int64_t kUnitGroupBound = 128;
 
 // Sum of the 8 groups' partial sums (lanes l, l ^ 8, ..., l ^ 56) into every group: the
 // partner 8 lanes away is in the same 16-lane row (DPP row_ror:8), the other two steps
@@ -244,6 +246,30 @@ __device__ __forceinline__ void slice_token_f32(const uint32_t* er, int nnz, __a
 // VK: kind of the ELL values. 0: bf16 (packed with the index in one word); 1: fp32 (the
 // backward's dz, two words per entry). OUT: 0: bf16 Y; 1: fp32 Yf; 2: bf16 Y of the sum
 // with the fp32 addend Yf (the second of two passes that share an accumulator).
+// One lane's 8 columns of a token's slice at element offset o. OUT 0: bf16 Y; 1: fp32 Yf;
+// 2: bf16 Y of the sum with the fp32 addend already in Yf.
+template <int OUT>
+__device__ __forceinline__ void store_slice(bf16_t* Y, float* Yf, int64_t o, float (&acc)[8]) {
+  if constexpr (OUT == 1) {
+    *(f32x4_t*)(Yf + o) = f32x4_t{acc[0], acc[1], acc[2], acc[3]};
+    *(f32x4_t*)(Yf + o + 4) = f32x4_t{acc[4], acc[5], acc[6], acc[7]};
+  } else {
+    if constexpr (OUT == 2) {
+      const f32x4_t a0 = *(const f32x4_t*)(Yf + o), a1 = *(const f32x4_t*)(Yf + o + 4);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        acc[j] = a0[j] + acc[j];
+        acc[4 + j] = a1[j] + acc[4 + j];
+      }
+    }
+    u32x4_t out;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      out[j] = (uint32_t)f32_to_bf16(acc[2 * j]) | ((uint32_t)f32_to_bf16(acc[2 * j + 1]) << 16);
+    *(u32x4_t*)(Y + o) = out;
+  }
+}
+
 template <int VK, int OUT, int U, bool TG = false>
 __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
     int64_t T, int64_t d, int64_t f, int K, const void* __restrict__ ell_val, const uint16_t* __restrict__ ell_idx,
@@ -284,7 +310,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
   // keeps every wave busy
   const int nsl = (n_slices - xcd + 7) / 8;
   if constexpr (TG) {
-    static_assert(VK == 0 && OUT == 0 && U % 2 == 0, "token groups: bf16 values, bf16 Y");
+    static_assert(VK == 1 || U % 2 == 0, "bf16 entries are consumed in pairs");
     // Short rows: a work item is (slice, NGRP tokens), lane group g walking token g's
     // entries on its own, so that no partial sums are folded across groups; the wave runs
     // to the longest of its tokens' rows (absent entries load nothing and add 0).
@@ -300,7 +326,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
       cmax = __builtin_amdgcn_readfirstlane(cmax);
       if (cmax < 0) continue;
       const uint32_t col_b = (uint32_t)(slice * f * SLICE2 * 2) + (uint32_t)sub * 16u;
-      const uint32_t* er = ent + (size_t)(i < tpw ? i : 0) * KS;
+      const uint32_t* er = ent + (size_t)(i < tpw ? i : 0) * KS * EW;
       float acc[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) acc[j] = 0.f;
@@ -310,29 +336,36 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
 #pragma unroll
         for (int u = 0; u < U; ++u) {
           const bool ok = e0 + u < c;
-          x[u] = ok ? er[e0 + u] : 0u;  // an absent entry has value 0 (and its load reads 0)
+          x[u] = ok ? er[EW * (e0 + u)] : 0u;  // an absent entry has value 0 (and its load reads 0)
           const uint32_t off = ok ? (x[u] & 0xffffu) * row_b + col_b : 0x80000000u;
           w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0));
         }
+        if constexpr (VK == 1) {
+          // fp32 values: each entry's row segment scaled and added in entry order
 #pragma unroll
-        for (int u = 0; u < U; u += 2) {
-          const bf16x2_t vv = __builtin_bit_cast(bf16x2_t, __builtin_amdgcn_perm(x[u + 1], x[u], 0x07060302u));
+          for (int u = 0; u < U; ++u) {
+            const float v = e0 + u < c ? __uint_as_float(er[EW * (e0 + u) + 1]) : 0.f;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const bf16x2_t lo = __builtin_bit_cast(bf16x2_t, __builtin_amdgcn_perm(w[u + 1][j], w[u][j], 0x05040100u));
-            const bf16x2_t hi = __builtin_bit_cast(bf16x2_t, __builtin_amdgcn_perm(w[u + 1][j], w[u][j], 0x07060302u));
-            acc[2 * j] = __builtin_amdgcn_fdot2_f32_bf16(vv, lo, acc[2 * j], false);
-            acc[2 * j + 1] = __builtin_amdgcn_fdot2_f32_bf16(vv, hi, acc[2 * j + 1], false);
+            for (int j = 0; j < 4; ++j) {
+              acc[2 * j] = fmaf(v, bf16lo(w[u][j]), acc[2 * j]);
+              acc[2 * j + 1] = fmaf(v, bf16hi(w[u][j]), acc[2 * j + 1]);
+            }
+          }
+        } else {
+#pragma unroll
+          for (int u = 0; u < U; u += 2) {
+            const bf16x2_t vv = __builtin_bit_cast(bf16x2_t, __builtin_amdgcn_perm(x[u + 1], x[u], 0x07060302u));
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const bf16x2_t lo = __builtin_bit_cast(bf16x2_t, __builtin_amdgcn_perm(w[u + 1][j], w[u][j], 0x05040100u));
+              const bf16x2_t hi = __builtin_bit_cast(bf16x2_t, __builtin_amdgcn_perm(w[u + 1][j], w[u][j], 0x07060302u));
+              acc[2 * j] = __builtin_amdgcn_fdot2_f32_bf16(vv, lo, acc[2 * j], false);
+              acc[2 * j + 1] = __builtin_amdgcn_fdot2_f32_bf16(vv, hi, acc[2 * j + 1], false);
+            }
           }
         }
       }
-      if (c >= 0) {
-        u32x4_t out;
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          out[j] = (uint32_t)f32_to_bf16(acc[2 * j]) | ((uint32_t)f32_to_bf16(acc[2 * j + 1]) << 16);
-        *(u32x4_t*)(Y + (t0 + i) * d + (int64_t)slice * SLICE2 + sub * 8) = out;
-      }
+      if (c >= 0) store_slice<OUT>(Y, Yf, (t0 + i) * d + (int64_t)slice * SLICE2 + sub * 8, acc);
     }
     return;
   }
@@ -349,27 +382,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
         slice_token_f32<U>(ent + 2 * i * K, nnz, wr, col_b, grp, acc);
       else
         slice_token<U>(ent + i * K, nnz, wr, col_b, grp, acc);
-      if (grp == 0) {
-        const int64_t o = (t0 + i) * d + col;
-        if constexpr (OUT == 1) {
-          *(f32x4_t*)(Yf + o) = f32x4_t{acc[0], acc[1], acc[2], acc[3]};
-          *(f32x4_t*)(Yf + o + 4) = f32x4_t{acc[4], acc[5], acc[6], acc[7]};
-        } else {
-          if constexpr (OUT == 2) {
-            const f32x4_t a0 = *(const f32x4_t*)(Yf + o), a1 = *(const f32x4_t*)(Yf + o + 4);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              acc[j] = a0[j] + acc[j];
-              acc[4 + j] = a1[j] + acc[4 + j];
-            }
-          }
-          u32x4_t out;
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            out[j] = (uint32_t)f32_to_bf16(acc[2 * j]) | ((uint32_t)f32_to_bf16(acc[2 * j + 1]) << 16);
-          *(u32x4_t*)(Y + o) = out;
-        }
-      }
+      if (grp == 0) store_slice<OUT>(Y, Yf, (t0 + i) * d + col, acc);
     }
   }
 }
@@ -517,6 +530,7 @@ __global__ __launch_bounds__(256) void k_gated_h(int64_t T, int K, const bf16_t*
 // memory (their lengths vary), the sums run in list order per group and the groups fold
 // in a fixed order. The block's lists are staged in LDS as (token, value) word pairs when
 // they fit (their total length is known only on the device), else read from global memory.
+template <bool TG>
 __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_units, int64_t d, int64_t R,
                                                                   const int32_t* __restrict__ ptr,
                                                                   const int32_t* __restrict__ tok,
@@ -542,6 +556,52 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_unit
       ent[2 * e + 1] = __float_as_uint(val[pb + e]);
     }
     __syncthreads();
+  }
+  if (TG && staged) {
+    // unit groups: a work item is (slice, NGRP units), lane group g summing unit g's list
+    // in list order on its own (no fold); the wave runs to the longest of the lists
+    const int n_grp = (nu + NGRP - 1) / NGRP;
+    for (int it = wave; it < nsl * n_grp; it += GATHER_WAVES) {
+      const int slice = xcd + 8 * (it / n_grp);
+      const int ui = (it % n_grp) * NGRP + grp;
+      const bool have = ui < nu;
+      const int64_t n = u0 + (have ? ui : 0);
+      const int p0 = ptr[n];
+      const int cnt = have ? ptr[n + 1] - p0 : 0;
+      int cmax = cnt;
+#pragma unroll
+      for (int o = 8; o < 64; o <<= 1) cmax = max(cmax, __shfl_xor(cmax, o, 64));
+      cmax = __builtin_amdgcn_readfirstlane(cmax);
+      const uint32_t col_b = (uint32_t)(slice * R * SLICE2 * 2) + (uint32_t)sub * 16u;
+      const uint32_t* er = ent + 2 * (p0 - pb);
+      float acc[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+      for (int e0 = 0; e0 < cmax; e0 += GU_GROUP) {
+        u32x4_t w[GU_GROUP];
+        float v[GU_GROUP];
+#pragma unroll
+        for (int u = 0; u < GU_GROUP; ++u) {
+          const bool ok = e0 + u < cnt;
+          v[u] = ok ? __uint_as_float(er[2 * (e0 + u) + 1]) : 0.f;
+          const uint32_t off = ok ? er[2 * (e0 + u)] * row_b + col_b : 0x80000000u;
+          w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(gr, (int)off, 0, 0));
+        }
+#pragma unroll
+        for (int u = 0; u < GU_GROUP; ++u)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            acc[2 * j] = fmaf(v[u], bf16lo(w[u][j]), acc[2 * j]);
+            acc[2 * j + 1] = fmaf(v[u], bf16hi(w[u][j]), acc[2 * j + 1]);
+          }
+      }
+      if (have) {
+        float* o = out + n * d + (int64_t)slice * SLICE2 + sub * 8;
+        *(f32x4_t*)o = f32x4_t{acc[0], acc[1], acc[2], acc[3]};
+        *(f32x4_t*)(o + 4) = f32x4_t{acc[4], acc[5], acc[6], acc[7]};
+      }
+    }
+    return;
   }
   for (int it = wave; it < nsl * nu; it += GATHER_WAVES) {
     const int slice = xcd + 8 * (it / nu);
@@ -671,8 +731,8 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
   const int n_slices = (int)(d / SLICE2);
   const int vk = val_f32 ? 1 : 0;
 
-  // bf16 values, rows of at most kTokenGroupK entries, large batches: token-group walk
-  const bool groups = vk == 0 && out_mode == 0 && K <= kTokenGroupK && T >= kTokenGroupT;
+  // rows of at most kTokenGroupK entries in large batches: token-group walk
+  const bool groups = K <= kTokenGroupK && T >= kTokenGroupT;
   const int64_t per_tok = (int64_t)(std::max(K, 1) + (groups ? 1 : 0)) * 4 * (vk + 1) + 4;
   const int tpw = slice_walk_tpw(T, per_tok);
   const int64_t blocks = cdiv(T, tpw);
@@ -698,7 +758,10 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
     else                                              \
       SFL_GATHER_LAUNCH_U(VK_, OUT_, GU);             \
   } while (0)
-  if (groups) SFL_GATHER_LAUNCH_G(0, 0, GU_GROUP, true);
+  if (groups && vk == 0 && out_mode == 0) SFL_GATHER_LAUNCH_G(0, 0, GU_GROUP, true);
+  else if (groups && vk == 1 && out_mode == 0) SFL_GATHER_LAUNCH_G(1, 0, GU_GROUP, true);
+  else if (groups && vk == 1 && out_mode == 1) SFL_GATHER_LAUNCH_G(1, 1, GU_GROUP, true);
+  else if (groups && vk == 1 && out_mode == 2) SFL_GATHER_LAUNCH_G(1, 2, GU_GROUP, true);
   else if (vk == 0 && out_mode == 0) SFL_GATHER_LAUNCH_U(0, 0, GU_BF16);
   else if (vk == 1 && out_mode == 0) SFL_GATHER_LAUNCH(1, 0);
   else if (vk == 1 && out_mode == 1) SFL_GATHER_LAUNCH(1, 1);
@@ -720,13 +783,23 @@ hipError_t launch_csc_gather(int64_t n_units, int64_t d, int64_t R, const int32_
   const int upw = (int)std::max<int64_t>(
       1, std::min<int64_t>(cdiv(n_units, 64), (int64_t)lds_pairs * 3 / 4 / std::max<int64_t>(mean_bound, 1)));
   const int64_t blocks = cdiv(n_units, upw);
+  // short lists: one unit per lane group (no fold). Measured against the per-unit walk:
+  // lists of about 41 entries (bound 74) 1.64 -> 1.26 ms for the gated step's three
+  // gathers, lists of about 164 entries (bound 256) 2.58 -> 2.75 ms for the two of the
+  // non-gated step, where the fold is already amortised and the groups' lists differ more
+  const bool groups = mean_bound <= kUnitGroupBound;
+  const void* kern = groups ? (const void*)k_csc_gather<true> : (const void*)k_csc_gather<false>;
   if (GATHER_LDS > 65536) {
-    const hipError_t e =
-        hipFuncSetAttribute((const void*)k_csc_gather, hipFuncAttributeMaxDynamicSharedMemorySize, GATHER_LDS);
+    const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, GATHER_LDS);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(k_csc_gather, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), (size_t)GATHER_LDS, s,
-                     n_units, d, R, ptr, tok, val, (const bf16_t*)Gp, out, (int)(d / SLICE2), upw, lds_pairs);
+  const dim3 grid((unsigned)(8 * blocks)), block(GATHER_WAVES * 64);
+  if (groups)
+    hipLaunchKernelGGL(k_csc_gather<true>, grid, block, (size_t)GATHER_LDS, s, n_units, d, R, ptr, tok, val,
+                       (const bf16_t*)Gp, out, (int)(d / SLICE2), upw, lds_pairs);
+  else
+    hipLaunchKernelGGL(k_csc_gather<false>, grid, block, (size_t)GATHER_LDS, s, n_units, d, R, ptr, tok, val,
+                       (const bf16_t*)Gp, out, (int)(d / SLICE2), upw, lds_pairs);
   return hipGetLastError();
 }
 
