@@ -6,7 +6,9 @@
 //    256-byte W_down row segment per entry.
 //  * k_gather_down_b16 (bf16, d % 512 == 0): over a slice-major copy of W_down, each XCD
 //    walking its own 64-column slices so that one 2 MiB slice stays in its L2 while every
-//    token streams through it (see below).
+//    token streams through it (see below). A work item is (slice, token), the 8 lane
+//    groups of the wave splitting the token's entries and folding their sums, or, for
+//    large batches of short rows, (slice, 8 tokens), one token per lane group.
 //
 // Gated (Alg. 2 / eq. sec3:eq:twell_to_dense_fused_matmul): per active gate value g at
 // column n, u = x[t] . W_up[:, n] and y[t] += (g * u) W_down[n]. Done in two passes with
