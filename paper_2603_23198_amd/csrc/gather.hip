@@ -19,6 +19,7 @@
 #include "internal.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace sfl {
 
@@ -322,22 +323,28 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
       const int slice = xcd + 8 * (it / n_grp);
       const int i = (it % n_grp) * NGRP + grp;
       const int c = i < tpw ? cnt_s[i] : -1;
-      int cmax = c;
+      int cmax = c, cmin = c;
 #pragma unroll
-      for (int o = 8; o < 64; o <<= 1) cmax = max(cmax, __shfl_xor(cmax, o, 64));
+      for (int o = 8; o < 64; o <<= 1) {
+        cmax = max(cmax, __shfl_xor(cmax, o, 64));
+        cmin = min(cmin, __shfl_xor(cmin, o, 64));
+      }
       cmax = __builtin_amdgcn_readfirstlane(cmax);
+      cmin = __builtin_amdgcn_readfirstlane(cmin);
       if (cmax < 0) continue;
       const uint32_t col_b = (uint32_t)(slice * f * SLICE2 * 2) + (uint32_t)sub * 16u;
       const uint32_t* er = ent + (size_t)(i < tpw ? i : 0) * KS * EW;
       float acc[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) acc[j] = 0.f;
-      for (int e0 = 0; e0 < cmax; e0 += U) {
+      // U entries from e0 for every group; `tail` marks rounds that pass the shortest row
+      // of the item, where a group's absent entries must read and add nothing
+      auto round = [&](int e0, auto tail) {
         u32x4_t w[U];
         uint32_t x[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-          const bool ok = e0 + u < c;
+          const bool ok = !decltype(tail)::value || e0 + u < c;
           x[u] = ok ? er[EW * (e0 + u)] : 0u;  // an absent entry has value 0 (and its load reads 0)
           const uint32_t off = ok ? (x[u] & 0xffffu) * row_b + col_b : 0x80000000u;
           w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0));
@@ -346,7 +353,8 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
           // fp32 values: each entry's row segment scaled and added in entry order
 #pragma unroll
           for (int u = 0; u < U; ++u) {
-            const float v = e0 + u < c ? __uint_as_float(er[EW * (e0 + u) + 1]) : 0.f;
+            const float v =
+                (!decltype(tail)::value || e0 + u < c) ? __uint_as_float(er[EW * (e0 + u) + 1]) : 0.f;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
               acc[2 * j] = fmaf(v, bf16lo(w[u][j]), acc[2 * j]);
@@ -366,7 +374,10 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
             }
           }
         }
-      }
+      };
+      int e0 = 0;
+      for (; e0 + U <= cmin; e0 += U) round(e0, std::false_type{});
+      for (; e0 < cmax; e0 += U) round(e0, std::true_type{});
       if (c >= 0) store_slice<OUT>(Y, Yf, (t0 + i) * d + (int64_t)slice * SLICE2 + sub * 8, acc);
     }
     return;
