@@ -160,7 +160,10 @@ constexpr int GU_BF16 = 2;
 // (lognormal counts) pay for, and a small batch leaves most groups of a block empty.
 constexpr int kTokenGroupK = 256;
 constexpr int64_t kTokenGroupT = 1024;
-constexpr int GU_GROUP = 4;
+#ifndef SFL_GROUP_UNROLL
+#define SFL_GROUP_UNROLL 4
+#endif
+constexpr int GU_GROUP = SFL_GROUP_UNROLL;  // row loads per lane in flight in the group walks
 // The backward's per-unit gathers group units the same way when their lists are short.
 constexpr int64_t kUnitGroupBound = 128;
 
@@ -581,21 +584,26 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_unit
       const int64_t n = u0 + (have ? ui : 0);
       const int p0 = ptr[n];
       const int cnt = have ? ptr[n + 1] - p0 : 0;
-      int cmax = cnt;
+      int cmax = cnt, cmin = have ? cnt : 0;
 #pragma unroll
-      for (int o = 8; o < 64; o <<= 1) cmax = max(cmax, __shfl_xor(cmax, o, 64));
+      for (int o = 8; o < 64; o <<= 1) {
+        cmax = max(cmax, __shfl_xor(cmax, o, 64));
+        cmin = min(cmin, __shfl_xor(cmin, o, 64));
+      }
       cmax = __builtin_amdgcn_readfirstlane(cmax);
+      cmin = __builtin_amdgcn_readfirstlane(cmin);
       const uint32_t col_b = (uint32_t)(slice * R * SLICE2 * 2) + (uint32_t)sub * 16u;
       const uint32_t* er = ent + 2 * (p0 - pb);
       float acc[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) acc[j] = 0.f;
-      for (int e0 = 0; e0 < cmax; e0 += GU_GROUP) {
+      // rounds below the shortest list of the item need no test for absent entries
+      auto round = [&](int e0, auto tail) {
         u32x4_t w[GU_GROUP];
         float v[GU_GROUP];
 #pragma unroll
         for (int u = 0; u < GU_GROUP; ++u) {
-          const bool ok = e0 + u < cnt;
+          const bool ok = !decltype(tail)::value || e0 + u < cnt;
           v[u] = ok ? __uint_as_float(er[2 * (e0 + u) + 1]) : 0.f;
           const uint32_t off = ok ? er[2 * (e0 + u)] * row_b + col_b : 0x80000000u;
           w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(gr, (int)off, 0, 0));
@@ -607,7 +615,10 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_unit
             acc[2 * j] = fmaf(v[u], bf16lo(w[u][j]), acc[2 * j]);
             acc[2 * j + 1] = fmaf(v[u], bf16hi(w[u][j]), acc[2 * j + 1]);
           }
-      }
+      };
+      int e0 = 0;
+      for (; e0 + GU_GROUP <= cmin; e0 += GU_GROUP) round(e0, std::false_type{});
+      for (; e0 < cmax; e0 += GU_GROUP) round(e0, std::true_type{});
       if (have) {
         float* o = out + n * d + (int64_t)slice * SLICE2 + sub * 8;
         *(f32x4_t*)o = f32x4_t{acc[0], acc[1], acc[2], acc[3]};
