@@ -293,11 +293,18 @@ def test_capacity_exceeded_flag_then_enough_capacity():
     assert rel_l2(to_f64(Y2), Yref) <= 2e-2
 
 
-def test_dense_baseline_matches_oracle():
-    w = wl.make_ffn("dense", "bf16", 1000, 512, 2048, seed=9, sparsity=0.95)
-    Y, _, _, _ = run_forward(w, dense=True)
+@pytest.mark.parametrize("T,copies,gated", [(1000, False, False), (200, True, False), (777, True, False),
+                                            (300, True, True)])
+def test_dense_baseline_matches_oracle(T, copies, gated):
+    """The library's dense FFN: GEMMs whose 256 x 256 tiles fill at most half of the CUs
+    split K (here every one: 2-8 ranges, ragged row counts), with row-contiguous weights
+    and with K-contiguous copies, non-gated and gated."""
+    w = wl.make_ffn("dense", "bf16", T, 512, 2048, seed=9 + T, sparsity=0.95, gated=gated)
+    Y, _, _, _ = run_forward(w, dense=True, use_wupt=copies, use_wdownt=copies, use_wgatet=copies and gated)
     Yref, _ = oracle_rows(w, np.arange(w.T))
     assert rel_l2(to_f64(Y), Yref) <= 2e-2
+    if T != 1000:
+        return
     w32 = wl.c1_small_fp32()
     Y32, _, _, _ = run_forward(w32, dense=True)
     Yref32, _ = oracle_rows(w32, np.arange(w32.T))
