@@ -114,9 +114,16 @@ enum {
  *  total_nnz          number of active (row, column) pairs
  *  n_ovf_rows         number of dense-backup rows
  *  n_tile_ovf         number of (row, tile) pairs with cnt > S
- *  l1_sum             sum of the stored activation values over sparse rows plus the
- *                     dense-backup rows that were computed (sfl_ffn_forward); times
- *                     lambda/(T f) this is the L1 term of eq. l1 for one layer
+ *  l1_sum             sum of |h| over the stored activations h of the sparse rows plus
+ *                     the dense-backup rows that were computed (sfl_ffn_forward); times
+ *                     lambda/(T f) this is the L1 term of eq. l1 for one layer. Non-gated,
+ *                     h = ReLU(z) are the stored TwELL values (bf16-rounded where bf16);
+ *                     gated, h = ReLU(g) * u, summed where the forward forms it (the
+ *                     bf16 h of the ELL entries, the dense-backup rows after the
+ *                     multiplication by u). With capacity_exceeded the rows beyond the
+ *                     capacity are not included. sfl_pack_twell sums the stored values
+ *                     (= ReLU(Z)) of its sparse rows. Accumulated with float64 atomics,
+ *                     so the last bits may vary from call to call.
  *  capacity_exceeded  1 iff n_ovf_rows > ovf capacity; the outputs of the rows
  *                     beyond the capacity are then unspecified. */
 typedef struct {

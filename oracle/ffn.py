@@ -164,3 +164,86 @@ def ffn_gated_backward(X, W_gate, W_up, W_down, dY, G, U, lam):
     dhu = dh * hg
     dG = np.where(G > 0, dh * U, 0.0)
     return dhu @ Wu.T + dG @ Wg.T, X.T @ dG, X.T @ dhu, h.T @ dY
+
+
+# ---- the same gradients for chosen hidden units or tokens ---------------------------------
+# Each hidden unit's weight gradients (column n of dW_up and dW_gate, row n of dW_down) need
+# only that unit's column of the pre-activations, and each token's dX row only that token's
+# row; the helpers below evaluate eq. sec3:eq:all_other_gradients on such a subset, so that
+# a layer too large for the full fp64 products can still be checked unit by unit and row by
+# row. `active` is the activity pattern of the subset (the unit passes exactly there);
+# lam/(T f) uses the layer's full T (rows of X) and f (columns of W_up).
+
+def ffn_backward_units(X, W_up, W_down, dY, units, active, lam, bias_f=None, shift_t=None):
+    """Non-gated: (dW_up[:, units], dW_down[units, :]) on the pattern `active` [T, len(units)].
+
+    z = X W_up[:, n] + b[n] + s, h = z on the pattern (0 elsewhere),
+    dh = dY W_down[n]^T + lam/(T f), dz = dh on the pattern; dW_up[:, n] = X^T dz,
+    dW_down[n] = h^T dY.
+    """
+    X = np.asarray(X, dtype=np.float64)
+    Wu = np.asarray(W_up, dtype=np.float64)
+    Wd = np.asarray(W_down, dtype=np.float64)
+    dY = np.asarray(dY, dtype=np.float64)
+    units = np.asarray(units, dtype=np.int64)
+    T, f = X.shape[0], Wu.shape[1]
+    Z = preactivation(X, Wu[:, units], None if bias_f is None else np.asarray(bias_f)[units], shift_t)
+    H = np.where(active, Z, 0.0)
+    dZ = np.where(active, dY @ Wd[units].T + lam / (T * f), 0.0)
+    return X.T @ dZ, H.T @ dY
+
+
+def ffn_backward_rows(X, W_up, W_down, dY, rows, active, lam):
+    """Non-gated: dX[rows] on the pattern `active` [len(rows), f]: dz = (dY W_down^T + lam/(T f))
+    on the pattern, dX = dz W_up^T."""
+    X = np.asarray(X, dtype=np.float64)
+    Wu = np.asarray(W_up, dtype=np.float64)
+    Wd = np.asarray(W_down, dtype=np.float64)
+    dY = np.asarray(dY, dtype=np.float64)
+    rows = np.asarray(rows, dtype=np.int64)
+    T, f = X.shape[0], Wu.shape[1]
+    dZ = np.where(active, dY[rows] @ Wd.T + lam / (T * f), 0.0)
+    return dZ @ Wu.T
+
+
+def ffn_gated_backward_units(X, W_gate, W_up, W_down, dY, units, active, lam, bias_f=None, shift_t=None):
+    """Gated: (dW_gate[:, units], dW_up[:, units], dW_down[units, :]) on the gate pattern
+    `active` [T, len(units)].
+
+    g = X W_gate[:, n] + b[n] + s, h_g = g on the pattern (0 elsewhere), h_u = X W_up[:, n],
+    h = h_g h_u; dh = dY W_down[n]^T + lam/(T f) sign(h); dh_u = dh h_g, dg = dh h_u on the
+    pattern; dW_gate[:, n] = X^T dg, dW_up[:, n] = X^T dh_u, dW_down[n] = h^T dY.
+    """
+    X = np.asarray(X, dtype=np.float64)
+    Wg = np.asarray(W_gate, dtype=np.float64)
+    Wu = np.asarray(W_up, dtype=np.float64)
+    Wd = np.asarray(W_down, dtype=np.float64)
+    dY = np.asarray(dY, dtype=np.float64)
+    units = np.asarray(units, dtype=np.int64)
+    T, f = X.shape[0], Wu.shape[1]
+    G = preactivation(X, Wg[:, units], None if bias_f is None else np.asarray(bias_f)[units], shift_t)
+    U = X @ Wu[:, units]
+    hg = np.where(active, G, 0.0)
+    h = hg * U
+    dh = dY @ Wd[units].T + lam / (T * f) * np.sign(h)
+    dG = np.where(active, dh * U, 0.0)
+    return X.T @ dG, X.T @ (dh * hg), h.T @ dY
+
+
+def ffn_gated_backward_rows(X, W_gate, W_up, W_down, dY, rows, active, lam, bias_f=None, shift_t=None):
+    """Gated: dX[rows] on the gate pattern `active` [len(rows), f]:
+    dX = dh_u W_up^T + dg W_gate^T with dh_u, dg as in ffn_gated_backward_units."""
+    X = np.asarray(X, dtype=np.float64)
+    Wg = np.asarray(W_gate, dtype=np.float64)
+    Wu = np.asarray(W_up, dtype=np.float64)
+    Wd = np.asarray(W_down, dtype=np.float64)
+    dY = np.asarray(dY, dtype=np.float64)
+    rows = np.asarray(rows, dtype=np.int64)
+    T, f = X.shape[0], Wu.shape[1]
+    G = preactivation(X[rows], Wg, bias_f, None if shift_t is None else np.asarray(shift_t)[rows])
+    U = X[rows] @ Wu
+    hg = np.where(active, G, 0.0)
+    h = hg * U
+    dh = dY[rows] @ Wd.T + lam / (T * f) * np.sign(h)
+    dG = np.where(active, dh * U, 0.0)
+    return (dh * hg) @ Wu.T + dG @ Wg.T

@@ -412,8 +412,10 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
   }
   ev.record(1, s);
   // 2. hybrid classification (Sec. 3.4)
+  // the stored values are h itself only in the non-gated layer (the gated layer's are the
+  // gate values; its sum of |h| is taken where h is formed)
   SFL_HIP(launch_classify(T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, a->cfg.ell_width, tw.val, tw.idx, tw.cnt,
-                          tw.row_nnz, tw.row_ovf, tw.ell_val, tw.ell_idx, a->stats, s));
+                          tw.row_nnz, tw.row_ovf, tw.ell_val, tw.ell_idx, a->stats, s, a->gated ? 0 : 1));
   SFL_HIP(launch_ovf_list(T, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s, plan.tile_sem, plan.n_sem));
   ev.record(2, s);
   // 3. sparse down projection of the ELL rows
@@ -439,7 +441,8 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
       }
       SFL_HIP(launch_gated_updot(T, d, f, a->cfg.ell_width, tw.ell_idx, tw.row_nnz, tw.row_ovf, a->X, WuP,
                                  plan.part_u, s));
-      SFL_HIP(launch_gated_h(T, a->cfg.ell_width, tw.ell_val, tw.row_nnz, tw.row_ovf, plan.part_u, plan.hval, s));
+      SFL_HIP(launch_gated_h(T, a->cfg.ell_width, tw.ell_val, tw.row_nnz, tw.row_ovf, plan.part_u, plan.hval, s,
+                             a->stats));
       hv = plan.hval;
     }
     SFL_HIP(launch_gather_down_packed(T, d, f, a->cfg.ell_width, hv, tw.ell_idx, tw.row_nnz, tw.row_ovf, WdP, a->Y,
@@ -512,7 +515,7 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
     // the partial-sum buffer holds part_rows rows of max(f, d) columns: more rows of d
     y.part_rows = (int)std::min<int64_t>((int64_t)plan.part_rows * std::max(f, d) / d, INT32_MAX);
     SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_ACT, y, s));
-    SFL_HIP(launch_ovf_l1(f, vb, ovf_dense, tw.n_ovf, (int32_t)cap, a->stats, s));
+    SFL_HIP(launch_ovf_l1(f, vb, ovf_dense, tw.n_ovf, (int32_t)cap, a->stats, s, a->gated ? 1 : 0));
   }
   ev.record(4, s);
   return SFL_OK;

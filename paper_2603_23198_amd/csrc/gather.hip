@@ -522,11 +522,15 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gated_updot(
 
 // h[t, e] = g[t, e] * sum over the 8 XCD partials of u[t, e] (in XCD order), rounded to
 // bf16 like every stored activation; entries past row_nnz and dense-backup rows untouched.
+// With stats, the block's sum of |h| (of the stored bf16 values) is added to l1_sum: the
+// L1 term of eq. l1 is on h, which in the gated block is signed.
 __global__ __launch_bounds__(256) void k_gated_h(int64_t T, int K, const bf16_t* __restrict__ ell_val,
                                                  const int32_t* __restrict__ row_nnz,
                                                  const uint8_t* __restrict__ row_ovf,
-                                                 const float* __restrict__ part_u, bf16_t* __restrict__ h) {
+                                                 const float* __restrict__ part_u, bf16_t* __restrict__ h,
+                                                 sfl_stats_t* __restrict__ stats) {
   const int64_t total = T * (int64_t)K;
+  float l1 = 0.f;
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
     const int64_t t = i / K;
     const int e = (int)(i % K);
@@ -534,7 +538,18 @@ __global__ __launch_bounds__(256) void k_gated_h(int64_t T, int K, const bf16_t*
     float u = 0.f;
 #pragma unroll
     for (int x = 0; x < 8; ++x) u += part_u[(int64_t)x * total + i];
-    h[i] = f32_to_bf16(bf16_to_f32(ell_val[i]) * u);
+    const bf16_t hb = f32_to_bf16(bf16_to_f32(ell_val[i]) * u);
+    h[i] = hb;
+    l1 += fabsf(bf16_to_f32(hb));
+  }
+  if (!stats) return;
+  l1 = wave_sum<float>(l1);
+  __shared__ float part[4];
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = l1;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const float tot = part[0] + part[1] + part[2] + part[3];
+    if (tot != 0.f) atomicAdd(&stats->l1_sum, (double)tot);
   }
 }
 
@@ -883,12 +898,13 @@ hipError_t launch_gated_updot(int64_t T, int64_t d, int64_t f, int K, const uint
 }
 
 hipError_t launch_gated_h(int64_t T, int K, const void* ell_val, const int32_t* row_nnz, const uint8_t* row_ovf,
-                          const float* part_u, void* h, hipStream_t s) {
+                          const float* part_u, void* h, hipStream_t s, sfl_stats_t* stats) {
   if (T == 0 || K == 0) return hipSuccess;
   const int64_t n = T * (int64_t)K;
-  const unsigned grid = (unsigned)std::min<int64_t>(cdiv(n, 256), 4096);
+  // with statistics each block adds one float64 atomic to the same address: fewer blocks
+  const unsigned grid = (unsigned)std::min<int64_t>(cdiv(n, 256), stats ? 1024 : 4096);
   hipLaunchKernelGGL(k_gated_h, dim3(grid), dim3(256), 0, s, T, K, (const bf16_t*)ell_val, row_nnz, row_ovf, part_u,
-                     (bf16_t*)h);
+                     (bf16_t*)h, stats);
   return hipGetLastError();
 }
 

@@ -88,25 +88,29 @@ hipError_t launch_pack_twell(const float* Z, int64_t T, int64_t f, int val_bf16,
 hipError_t launch_pack_twell_parts(const float* part, int ks, const float* bias, const float* shift, int64_t T,
                                    int64_t f, int val_bf16, int tile_cols, int tile_slots, void* val, uint16_t* idx,
                                    int32_t* cnt, hipStream_t s);
-// Hybrid classification: row_nnz, row_ovf, optional ELL rows and stats partials.
+// Hybrid classification: row_nnz, row_ovf, optional ELL rows and stats partials; with
+// l1_vals the stored values of the sparse rows are added to stats->l1_sum (they are the
+// activations h of the non-gated layer; the gated layer's are gate values, and its L1 sum
+// comes from launch_gated_h).
 hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int tile_cols, int tile_slots,
                            int ell_width, const void* val, const uint16_t* idx, const int32_t* cnt,
                            int32_t* row_nnz, uint8_t* row_ovf, void* ell_val, uint16_t* ell_idx,
-                           sfl_stats_t* stats, hipStream_t s);
+                           sfl_stats_t* stats, hipStream_t s, int l1_vals = 1);
 // Ascending dense-backup row list + n_ovf + capacity flag (one workgroup).
 hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32_t* ovf_rows,
                            int32_t* n_ovf, sfl_stats_t* stats, hipStream_t s,
                            int32_t* zero = nullptr, int n_zero = 0);
 hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s);
-// l1 of the computed dense-backup rows (adds into stats->l1_sum).
 // Dense-backup rows whose tiles kept every value, rebuilt from the TwELL slabs; the others
 // are listed (need_rows: token rows, need_slots: their ovf_dense rows, n_need) for the GEMM.
 hipError_t launch_ovf_fill(int64_t f, int val_bf16, int Tn, int S, const void* val, const uint16_t* idx,
                            const int32_t* cnt, const int32_t* ovf_rows, const int32_t* n_ovf, int32_t cap,
                            void* dense, uint8_t* need, int32_t* need_rows, int32_t* need_slots, int32_t* n_need,
                            hipStream_t s);
+// Sum (absval: of the absolute values) of the computed dense-backup rows, added into
+// stats->l1_sum.
 hipError_t launch_ovf_l1(int64_t f, int val_bf16, const void* ovf_dense, const int32_t* n_ovf,
-                         int32_t cap, sfl_stats_t* stats, hipStream_t s);
+                         int32_t cap, sfl_stats_t* stats, hipStream_t s, int absval);
 
 // ---------------------------------------------------------- gathers ----
 // Y[t, :] = sum_e ell_val[t][e] * W[ell_idx[t][e], :] for rows with row_ovf[t] == 0.
@@ -136,8 +140,9 @@ hipError_t launch_csc_gather(int64_t n_units, int64_t d, int64_t R, const int32_
 // out[t][e] = sum of the 8 partials [8][T][K] + add on the sparse rows' entries (fp32).
 hipError_t launch_sum_parts(int64_t T, int K, const int32_t* row_nnz, const uint8_t* row_ovf, const float* part,
                             float add, float* out, hipStream_t s);
+// With stats, sum |h| of the written entries into stats->l1_sum.
 hipError_t launch_gated_h(int64_t T, int K, const void* ell_val, const int32_t* row_nnz, const uint8_t* row_ovf,
-                          const float* part_u, void* h, hipStream_t s);
+                          const float* part_u, void* h, hipStream_t s, sfl_stats_t* stats = nullptr);
 // Gated fused up-dot + down (Alg. 2) from the ELL rows of the gate pattern.
 // --------------------------------------------------------- backward ----
 // (declared in backward.h)

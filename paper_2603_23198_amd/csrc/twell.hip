@@ -139,7 +139,7 @@ __global__ __launch_bounds__(kClassifyWaves * 64) void k_classify(int64_t T, int
                                                   const uint16_t* __restrict__ idx, const int32_t* __restrict__ cnt,
                                                   int32_t* __restrict__ row_nnz, uint8_t* __restrict__ row_ovf,
                                                   V* __restrict__ ell_val, uint16_t* __restrict__ ell_idx,
-                                                  sfl_stats_t* __restrict__ stats, int rpw) {
+                                                  sfl_stats_t* __restrict__ stats, int rpw, int l1_vals) {
   __shared__ int incl_lds[kClassifyWaves][kClassifyMaxTiles];
   const int l = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
@@ -186,7 +186,7 @@ __global__ __launch_bounds__(kClassifyWaves * 64) void k_classify(int64_t T, int
           const int excl = lo > 0 ? incl_s[lo - 1] : 0;
           const int64_t src = (int64_t)lo * S + (q - excl);
           const V v = vrow[src];
-          l1 += VT<V>::load(&v, 0);
+          if (l1_vals) l1 += VT<V>::load(&v, 0);
           if (ell_val) {
             ell_val[t * (int64_t)K + q] = v;
             ell_idx[t * (int64_t)K + q] = irow[src];
@@ -207,7 +207,7 @@ __global__ __launch_bounds__(256) void k_classify_wide(int64_t T, int NT, int S,
                                                        const int32_t* __restrict__ cnt,
                                                        int32_t* __restrict__ row_nnz, uint8_t* __restrict__ row_ovf,
                                                        V* __restrict__ ell_val, uint16_t* __restrict__ ell_idx,
-                                                       sfl_stats_t* __restrict__ stats) {
+                                                       sfl_stats_t* __restrict__ stats, int l1_vals) {
   const int64_t t0 = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const bool row_ok = t0 < T;
   const int64_t t = row_ok ? t0 : 0;
@@ -236,7 +236,7 @@ __global__ __launch_bounds__(256) void k_classify_wide(int64_t T, int NT, int S,
         const int sidx = s0 + l;
         if (sidx < cj) {
           const V v = vrow[(int64_t)j * S + sidx];
-          l1 += VT<V>::load(&v, 0);
+          if (l1_vals) l1 += VT<V>::load(&v, 0);
           if (ell_val) {
             ell_val[t * (int64_t)K + offset + sidx] = v;
             ell_idx[t * (int64_t)K + offset + sidx] = irow[(int64_t)j * S + sidx];
@@ -251,7 +251,7 @@ __global__ __launch_bounds__(256) void k_classify_wide(int64_t T, int NT, int S,
 
 hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int Tn, int S, int K, const void* val,
                            const uint16_t* idx, const int32_t* cnt, int32_t* row_nnz, uint8_t* row_ovf,
-                           void* ell_val, uint16_t* ell_idx, sfl_stats_t* stats, hipStream_t s) {
+                           void* ell_val, uint16_t* ell_idx, sfl_stats_t* stats, hipStream_t s, int l1_vals) {
   if (T == 0) return hipSuccess;
   const int NT = (int)cdiv(f, Tn);
   const bool wide = NT > kClassifyMaxTiles;
@@ -262,17 +262,17 @@ hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int Tn, int S, in
   if (wide) {
     if (val_bf16)
       hipLaunchKernelGGL(k_classify_wide<bf16_t>, grid, dim3(256), 0, s, T, NT, S, K, (const bf16_t*)val, idx, cnt,
-                         row_nnz, row_ovf, (bf16_t*)ell_val, ell_idx, stats);
+                         row_nnz, row_ovf, (bf16_t*)ell_val, ell_idx, stats, l1_vals);
     else
       hipLaunchKernelGGL(k_classify_wide<float>, grid, dim3(256), 0, s, T, NT, S, K, (const float*)val, idx, cnt,
-                         row_nnz, row_ovf, (float*)ell_val, ell_idx, stats);
+                         row_nnz, row_ovf, (float*)ell_val, ell_idx, stats, l1_vals);
   } else {
     if (val_bf16)
       hipLaunchKernelGGL(k_classify<bf16_t>, grid, dim3(kClassifyWaves * 64), 0, s, T, NT, S, K, (const bf16_t*)val,
-                         idx, cnt, row_nnz, row_ovf, (bf16_t*)ell_val, ell_idx, stats, rpw);
+                         idx, cnt, row_nnz, row_ovf, (bf16_t*)ell_val, ell_idx, stats, rpw, l1_vals);
     else
       hipLaunchKernelGGL(k_classify<float>, grid, dim3(kClassifyWaves * 64), 0, s, T, NT, S, K, (const float*)val,
-                         idx, cnt, row_nnz, row_ovf, (float*)ell_val, ell_idx, stats, rpw);
+                         idx, cnt, row_nnz, row_ovf, (float*)ell_val, ell_idx, stats, rpw, l1_vals);
   }
   return hipGetLastError();
 }
@@ -346,16 +346,19 @@ hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32
   return hipGetLastError();
 }
 
-// Sum of the dense-backup rows that were computed (min(n_ovf, cap) rows of ovf_dense).
-// Up to kL1Blocks blocks stride over the rows with 16-byte loads, each adding its total
-// with one float64 atomic (atomics on one address serialise, so one per row would cost
-// more than the sums).
+// Sum of the dense-backup rows that were computed (min(n_ovf, cap) rows of ovf_dense), of
+// their absolute values when absval is set (the gated rows hold h = ReLU(g) * u, which can
+// be negative; the non-gated ReLU rows are >= 0 either way). Up to kL1Blocks blocks stride
+// over the rows with 16-byte loads, each adding its total with one float64 atomic (atomics
+// on one address serialise, so one per row would cost more than the sums).
 constexpr int kL1Blocks = 256;
 template <typename V>
 __global__ __launch_bounds__(256) void k_ovf_l1(int64_t f, const V* __restrict__ dense, const int32_t* n_ovf,
-                                                int32_t cap, sfl_stats_t* stats) {
+                                                int32_t cap, sfl_stats_t* stats, int absval) {
   constexpr int PER = 16 / (int)sizeof(V);
   const int n = min(*n_ovf, cap);
+  // the magnitude keeps every bit but the sign
+  const uint32_t keep = absval ? 0x7fffffffu : 0xffffffffu;
   float s = 0.f;
   const bool vec = f % PER == 0 && ((uintptr_t)dense & 15) == 0;
   for (int64_t row = blockIdx.x; row < n; row += gridDim.x) {
@@ -365,12 +368,12 @@ __global__ __launch_bounds__(256) void k_ovf_l1(int64_t f, const V* __restrict__
         const u32x4_t w = *(const u32x4_t*)(r + c);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          if constexpr (sizeof(V) == 2) s += bf16lo(w[q]) + bf16hi(w[q]);
-          else s += __uint_as_float(w[q]);
+          if constexpr (sizeof(V) == 2) s += __uint_as_float((w[q] << 16) & keep) + __uint_as_float(w[q] & 0xffff0000u & keep);
+          else s += __uint_as_float(w[q] & keep);
         }
       }
     } else {
-      for (int64_t c = threadIdx.x; c < f; c += 256) s += VT<V>::load(r, c);
+      for (int64_t c = threadIdx.x; c < f; c += 256) s += __uint_as_float(__float_as_uint(VT<V>::load(r, c)) & keep);
     }
   }
   s = wave_sum<float>(s);
@@ -384,13 +387,13 @@ __global__ __launch_bounds__(256) void k_ovf_l1(int64_t f, const V* __restrict__
 }
 
 hipError_t launch_ovf_l1(int64_t f, int val_bf16, const void* dense, const int32_t* n_ovf, int32_t cap,
-                         sfl_stats_t* stats, hipStream_t s) {
+                         sfl_stats_t* stats, hipStream_t s, int absval) {
   if (!stats || cap == 0) return hipSuccess;
   const dim3 grid((unsigned)std::min<int32_t>(cap, kL1Blocks));
   if (val_bf16)
-    hipLaunchKernelGGL(k_ovf_l1<bf16_t>, grid, dim3(256), 0, s, f, (const bf16_t*)dense, n_ovf, cap, stats);
+    hipLaunchKernelGGL(k_ovf_l1<bf16_t>, grid, dim3(256), 0, s, f, (const bf16_t*)dense, n_ovf, cap, stats, absval);
   else
-    hipLaunchKernelGGL(k_ovf_l1<float>, grid, dim3(256), 0, s, f, (const float*)dense, n_ovf, cap, stats);
+    hipLaunchKernelGGL(k_ovf_l1<float>, grid, dim3(256), 0, s, f, (const float*)dense, n_ovf, cap, stats, absval);
   return hipGetLastError();
 }
 

@@ -179,28 +179,29 @@ def test_backward_deterministic_and_weight_copies():
 
 
 def test_backward_c5_sampled():
-    """Training shape: T=16384, d=4096, f=16384, ~99% sparse, K=256; sampled rows and units."""
+    """Training shape: T=16384, d=4096, f=16384, ~99% sparse, K=256; sampled units (dW_up
+    columns, dW_down rows) and sampled rows (dX) against the oracle's per-unit and per-row
+    gradients on the pattern the GPU saved, each unit and row on its own."""
     w = wl.c5_training()
     lam = 1e-3 * w.T * w.f   # per-element injection 1e-3, visible in bf16
     dX, dWu, dWd, bufs, cfg = run_fwd_bwd(w, lam)
     act = gpu_pattern(bufs, w, cfg).tocsc()
     r = np.random.default_rng(0)
     X, Wu, Wd, dY = w.as_f64(w.X), w.as_f64(w.W_up), w.as_f64(w.W_down), w.as_f64(w.dY)
-    lamp = lam / (w.T * w.f)
-    # dW for sampled units: needs column n of Z and dH over all tokens
     units = r.choice(w.f, size=48, replace=False)
-    Zc = X @ Wu[:, units] + w.shift_t[:, None]
-    dHc = dY @ Wd[units].T + lamp
-    A = act[:, units].toarray()
-    dWd_ref = (np.where(A, Zc, 0.0)).T @ dY            # [units, d]
-    dWu_ref = X.T @ np.where(A, dHc, 0.0)              # [d, units]
-    assert rel_l2(to_f64(dWd)[units], dWd_ref) <= 2e-2
-    assert rel_l2(to_f64(dWu)[:, units], dWu_ref) <= 2e-2
-    # dX for sampled rows
-    rows = r.choice(w.T, size=64, replace=False)
-    Ar = act.tocsr()[rows].toarray()
-    dZr = np.where(Ar, dY[rows] @ Wd.T + lamp, 0.0)
-    assert rel_l2(to_f64(dX)[rows], dZr @ Wu.T) <= 2e-2
+    dWu_ref, dWd_ref = ffn.ffn_backward_units(X, Wu, Wd, dY, units, act[:, units].toarray(), lam, None, w.shift_t)
+    gWu, gWd = to_f64(dWu)[:, units], to_f64(dWd)[units]
+    assert rel_l2(gWd, dWd_ref) <= 2e-2 and rel_l2(gWu, dWu_ref) <= 2e-2
+    for j in range(len(units)):
+        assert rel_l2(gWd[j], dWd_ref[j]) <= 2e-2, units[j]
+        assert rel_l2(gWu[:, j], dWu_ref[:, j]) <= 2e-2, units[j]
+    got = twell_views(bufs, w.T, w.f, cfg)
+    rows = np.unique(np.concatenate([r.choice(w.T, size=64, replace=False),
+                                     np.nonzero(got["row_ovf"])[0][:8]]))
+    dX_ref = ffn.ffn_backward_rows(X, Wu, Wd, dY, rows, act.tocsr()[rows].toarray(), lam)
+    gX = to_f64(dX)[rows]
+    for i, t in enumerate(rows):
+        assert rel_l2(gX[i], dX_ref[i]) <= 2e-2, t
 
 
 # ---- gated block (eq. sec3:eq:all_other_gradients with eq. l1 on h = ReLU(g) h_u) --------
@@ -296,7 +297,9 @@ def test_backward_c5_bench_configuration_is_identical():
 def test_gated_training_bench_configuration_sampled():
     """The gated training step as bench.py runs it (T=8192, d=4096, f=14336, dense backup of
     T/8 rows, all weight copies): sampled units of dW_gate, dW_up, dW_down and sampled rows
-    of dX against the fp64 oracle on the GPU's saved pattern."""
+    of dX, each on its own, against the oracle's per-unit and per-row gradients on the gate
+    pattern the GPU saved (ELL rows; fp64 G > 0 on the dense-backup rows, which the GPU
+    recomputes)."""
     w = wl.gated_training()
     w.shift_t[:4] = 10.0  # a few dense-backup rows
     lam = 1e-3 * w.T * w.f
@@ -304,12 +307,11 @@ def test_gated_training_bench_configuration_sampled():
     got = twell_views(bufs, w.T, w.f, cfg)
     assert got["row_ovf"][:4].all()
     X, Wg, Wu, Wd, dY = (w.as_f64(a) for a in (w.X, w.W_gate, w.W_up, w.W_down, w.dY))
-    lamp = lam / (w.T * w.f)
     sparse_rows = np.nonzero(got["row_ovf"] == 0)[0]
 
-    def pattern(rows_sel, cols, G):
+    def pattern(rows_sel, cols):
         """GPU pattern on ELL rows, fp64 G > 0 on dense-backup rows, for [rows_sel][cols]."""
-        act = G > 0
+        act = ffn.preactivation(X[rows_sel], Wg[:, cols], None, w.shift_t[rows_sel]) > 0
         colpos = {int(c): j for j, c in enumerate(cols)}
         for i, t in enumerate(rows_sel):
             if got["row_ovf"][t]:
@@ -323,23 +325,16 @@ def test_gated_training_bench_configuration_sampled():
 
     r = np.random.default_rng(5)
     units = r.choice(w.f, size=32, replace=False)
-    allrows = np.arange(w.T)
-    G = X @ Wg[:, units] + w.shift_t[:, None]
-    U = X @ Wu[:, units]
-    A = pattern(allrows, units, G)
-    hg = np.where(A, np.maximum(G, 1e-30), 0.0)
-    h = hg * U
-    dh = dY @ Wd[units].T + lamp * np.sign(h)
-    dhu, dG = dh * hg, np.where(A, dh * U, 0.0)
-    assert rel_l2(to_f64(dWd)[units], h.T @ dY) <= 2e-2
-    assert rel_l2(to_f64(dWu)[:, units], X.T @ dhu) <= 2e-2
-    assert rel_l2(to_f64(dWg)[:, units], X.T @ dG) <= 2e-2
+    A = pattern(np.arange(w.T), units)
+    rWg, rWu, rWd = ffn.ffn_gated_backward_units(X, Wg, Wu, Wd, dY, units, A, lam, None, w.shift_t)
+    gWg, gWu, gWd = to_f64(dWg)[:, units], to_f64(dWu)[:, units], to_f64(dWd)[units]
+    for j in range(len(units)):
+        assert rel_l2(gWd[j], rWd[j]) <= 2e-2, units[j]
+        assert rel_l2(gWu[:, j], rWu[:, j]) <= 2e-2, units[j]
+        assert rel_l2(gWg[:, j], rWg[:, j]) <= 2e-2, units[j]
     rows = np.concatenate([r.choice(sparse_rows, size=24, replace=False), np.arange(4)])
-    Gr = X[rows] @ Wg + w.shift_t[rows, None]
-    Ur = X[rows] @ Wu
-    Ar = pattern(rows, np.arange(w.f), Gr)
-    hgr = np.where(Ar, np.maximum(Gr, 1e-30), 0.0)
-    hr = hgr * Ur
-    dhr = dY[rows] @ Wd.T + lamp * np.sign(hr)
-    dXr = (dhr * hgr) @ Wu.T + np.where(Ar, dhr * Ur, 0.0) @ Wg.T
-    assert rel_l2(to_f64(dX)[rows], dXr) <= 2e-2
+    Ar = pattern(rows, np.arange(w.f))
+    rX = ffn.ffn_gated_backward_rows(X, Wg, Wu, Wd, dY, rows, Ar, lam, None, w.shift_t)
+    gX = to_f64(dX)[rows]
+    for i, t in enumerate(rows):
+        assert rel_l2(gX[i], rX[i]) <= 2e-2, t

@@ -194,3 +194,46 @@ def test_paper_tile_overflow_claim():
     order = claim["claimed_order_log10"]
     assert 10.0 ** (order - 2) < p_lo < 10.0 ** order < p_29 < 10.0 ** (order + 2)
     assert p_hi < 1e-28   # still negligible at the 39-nnz end
+
+
+@pytest.mark.parametrize("lam", [0.0, 5.0])
+def test_per_unit_and_per_row_gradients_equal_the_full_backward(lam):
+    """The subset helpers (chosen hidden units, chosen tokens) return exactly the columns /
+    rows of the full backward, which the finite-difference tests above pin; non-square
+    shapes, a bias and a row shift, on the fp64 pattern z > 0 and on a pattern with flipped
+    entries (the GPU's pattern may differ from fp64's within rounding of 0)."""
+    r = np.random.default_rng(3)
+    T, d, f = 13, 7, 19
+    X, Wu, Wd = r.standard_normal((T, d)), r.standard_normal((d, f)) * 0.5, r.standard_normal((f, d)) * 0.5
+    bias, shift, dY = r.standard_normal(f) * 0.3, r.standard_normal(T) * 0.3, r.standard_normal((T, d))
+    Z = ffn.preactivation(X, Wu, bias, shift)
+    units, rows = np.array([17, 0, 4, 11]), np.array([12, 3, 5])
+    flip = r.random((T, f)) < 0.1
+    for act in (Z > 0, (Z > 0) ^ flip):
+        dX, dWu, dWd, _ = ffn.ffn_backward(X, Wu, Wd, dY, np.where(act, Z, 0.0), act, lam)
+        gWu, gWd = ffn.ffn_backward_units(X, Wu, Wd, dY, units, act[:, units], lam, bias, shift)
+        np.testing.assert_allclose(gWu, dWu[:, units], rtol=1e-13, atol=1e-13)
+        np.testing.assert_allclose(gWd, dWd[units], rtol=1e-13, atol=1e-13)
+        np.testing.assert_allclose(ffn.ffn_backward_rows(X, Wu, Wd, dY, rows, act[rows], lam), dX[rows],
+                                   rtol=1e-13, atol=1e-13)
+
+
+@pytest.mark.parametrize("lam", [0.0, 5.0])
+def test_gated_per_unit_and_per_row_gradients_equal_the_full_backward(lam):
+    """The gated subset helpers on the pattern G > 0 return the columns / rows of
+    ffn_gated_backward (pinned by finite differences above), with a gate bias and shift."""
+    r = np.random.default_rng(4)
+    T, d, f = 11, 6, 17
+    X = r.standard_normal((T, d))
+    Wg, Wu, Wd = (r.standard_normal(s) * 0.5 for s in ((d, f), (d, f), (f, d)))
+    bias, shift, dY = r.standard_normal(f) * 0.3, r.standard_normal(T) * 0.3, r.standard_normal((T, d))
+    _, G, U, _ = ffn.ffn_gated_dense(X, Wg, Wu, Wd, bias, shift)
+    dX, dWg, dWu, dWd = ffn.ffn_gated_backward(X, Wg, Wu, Wd, dY, G, U, lam)
+    units, rows = np.array([16, 2, 9]), np.array([0, 10, 4, 7])
+    act = G > 0
+    gWg, gWu, gWd = ffn.ffn_gated_backward_units(X, Wg, Wu, Wd, dY, units, act[:, units], lam, bias, shift)
+    np.testing.assert_allclose(gWg, dWg[:, units], rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(gWu, dWu[:, units], rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(gWd, dWd[units], rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(ffn.ffn_gated_backward_rows(X, Wg, Wu, Wd, dY, rows, act[rows], lam, bias, shift),
+                               dX[rows], rtol=1e-13, atol=1e-13)
