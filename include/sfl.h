@@ -22,8 +22,10 @@
  *    are written to device memory (sfl_twell_t.n_ovf, sfl_stats_t) and can be
  *    read after the caller's own synchronisation.
  *  - Reentrancy: no global mutable state beyond a per-device cache of the CU
- *    count; concurrent calls on different streams with disjoint buffers
- *    (workspaces included) are safe.
+ *    count and of the address of sfl_ffn_forward_noalloc's scratch array;
+ *    concurrent calls on different streams with disjoint buffers (workspaces
+ *    included) are safe, except sfl_ffn_forward_noalloc calls that overlap on
+ *    one GPU (they share its scratch array).
  *  - Numerics: bf16 inputs are multiplied on MFMA with float32 accumulation;
  *    activations are stored in the activation dtype, bf16 by round-to-nearest-
  *    even. A hidden unit is active iff its pre-activation is > 0 (strict; +0,
@@ -293,6 +295,27 @@ sfl_status_t sfl_workspace_size(const void* args, int backward, size_t* bytes);
  * and the dense path for the dense-backup rows (Alg. 3's dense part).
  * bf16: d % 64 == 0 and f % 64 == 0; fp32: any sizes. */
 sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* args, sfl_stream_t stream);
+
+/* Bytes of the device scratch array that sfl_ffn_forward_noalloc uses as its workspace
+ * (one array per GPU, held from the first call on that GPU until the process ends). */
+#define SFL_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): sfl_ffn_forward with its workspace
+ * taken from a fixed device scratch array of SFL_NOALLOC_SCRATCH_BYTES bytes inside the
+ * library instead of from args->workspace (args->workspace and workspace_bytes are
+ * ignored). Same kernels, same results, bit for bit, as sfl_ffn_forward. It calls no
+ * allocating routine; the scratch's device address is looked up once per GPU, on the first
+ * call with that GPU current. Inputs, outputs and args->twell are still the caller's.
+ * Errors: those of sfl_ffn_forward, and SFL_E_WORKSPACE when the call needs more workspace
+ * than the scratch holds (sfl_workspace_size(args, 0) > SFL_NOALLOC_SCRATCH_BYTES); nothing
+ * is launched then. The workspace grows with T and, when the caller does not pass them,
+ * with the weight copies (W_down_packed, W_up_packed, W_upT) and the dense-backup rows
+ * (twell.ovf_dense): pass those to stay within the limit; decode-sized batches fit.
+ * Every call on a GPU shares that GPU's array and leaves its contents behind: calls that
+ * overlap on one GPU (different streams, or different host threads) race and must not be
+ * issued; calls in one stream are ordered and safe. */
+sfl_status_t sfl_ffn_forward_noalloc(const sfl_ffn_args_t* args, sfl_stream_t stream);
 
 /* The pre-activation Z = X W + b + s of the forward's up (or gate) projection,
  * as float32 [T][f], computed by the same GEMM main loop as sfl_ffn_forward.

@@ -28,7 +28,7 @@ BUF_NAMES = ["val", "idx", "cnt", "row_nnz", "row_ovf", "ovf_rows", "n_ovf", "el
 EXPORTED = ["sfl_status_string", "sfl_version", "sfl_twell_buffer_sizes", "sfl_pack_twell",
             "sfl_workspace_size", "sfl_ffn_forward", "sfl_up_projection", "sfl_ffn_backward",
             "sfl_dense_ffn_baseline", "sfl_transpose", "sfl_pack_down_weights", "sfl_track_active_units",
-            "sfl_reinit_dead_units"]
+            "sfl_reinit_dead_units", "sfl_ffn_forward_noalloc"]
 
 
 class SflError(RuntimeError):
@@ -81,6 +81,7 @@ _lib.sfl_twell_buffer_sizes.argtypes = [c_int64, c_int64, c_int, POINTER(Cfg), P
 _lib.sfl_pack_twell.argtypes = [c_void_p, c_int64, c_int64, c_int, POINTER(Cfg), POINTER(Twell), c_void_p, c_void_p]
 _lib.sfl_workspace_size.argtypes = [c_void_p, c_int, POINTER(c_size_t)]
 _lib.sfl_ffn_forward.argtypes = [POINTER(FfnArgs), c_void_p]
+_lib.sfl_ffn_forward_noalloc.argtypes = [POINTER(FfnArgs), c_void_p]
 _lib.sfl_up_projection.argtypes = [POINTER(FfnArgs), c_void_p, c_void_p]
 _lib.sfl_ffn_backward.argtypes = [POINTER(BwdArgs), c_void_p]
 _lib.sfl_dense_ffn_baseline.argtypes = [POINTER(FfnArgs), c_void_p]
@@ -216,6 +217,10 @@ def sfl_workspace_size(args, kind=0):
 
 def sfl_ffn_forward(args, stream=None):
     _check("sfl_ffn_forward", _lib.sfl_ffn_forward(ctypes.byref(args), _stream(stream)))
+
+
+def sfl_ffn_forward_noalloc(args, stream=None):
+    _check("sfl_ffn_forward_noalloc", _lib.sfl_ffn_forward_noalloc(ctypes.byref(args), _stream(stream)))
 
 
 def sfl_up_projection(args, Z, stream=None):

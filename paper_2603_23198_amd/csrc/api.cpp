@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <cstring>
+#include <mutex>
 
 #include "backward.h"
 #include "common.h"
@@ -230,6 +231,37 @@ hipError_t run_gemm(sfl_dtype_t dt, int alay, int blay, int epi, const GemmParam
   return gemm_f32(epi, g, s);
 }
 
+// Device scratch of sfl_ffn_forward_noalloc (for callers that cannot allocate): one array
+// per GPU the library runs on, held until the process ends. In host code `scratch` names a
+// host-side stand-in, not the device memory: the device address is taken once per device
+// (hipGetSymbolAddress with that device current) and only that address is passed on.
+static __device__ __align__(256) unsigned char scratch[SFL_NOALLOC_SCRATCH_BYTES];
+
+constexpr size_t kNoallocScratchBytes = SFL_NOALLOC_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices];  // device address of `scratch` per device, once known
+
+// Device address of the current device's scratch array.
+hipError_t scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_addr[dev] = p;
+  }
+  *out = g_scratch_addr[dev];
+  return hipSuccess;
+}
+
+sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hipStream_t s);
+
 }  // namespace
 
 extern "C" {
@@ -340,14 +372,34 @@ sfl_status_t sfl_up_projection(const sfl_ffn_args_t* a, float* Z, sfl_stream_t s
 }
 
 sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
+  if (!a) return SFL_E_ARG;
+  return forward_run(a, a->workspace, a->workspace_bytes, (hipStream_t)stream);
+}
+
+sfl_status_t sfl_ffn_forward_noalloc(const sfl_ffn_args_t* a, sfl_stream_t stream) {
+  sfl_status_t st = check_forward(a);
+  if (st != SFL_OK) return st;
+  st = check_twell(a->twell, true, a->T);
+  if (st != SFL_OK) return st;
+  if (plan_forward(*a, nullptr).bytes > kNoallocScratchBytes) return SFL_E_WORKSPACE;
+  void* ws = nullptr;
+  SFL_HIP(scratch_address(&ws));
+  return forward_run(a, ws, kNoallocScratchBytes, (hipStream_t)stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// The forward's stage sequence over the workspace ws (ws_bytes bytes).
+sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hipStream_t s) {
   sfl_status_t st = check_forward(a);
   if (st != SFL_OK) return st;
   st = check_twell(a->twell, true, a->T);
   if (st != SFL_OK) return st;
   FwdPlan plan = plan_forward(*a, nullptr);
-  if (plan.bytes > 0 && (!a->workspace || a->workspace_bytes < plan.bytes)) return SFL_E_WORKSPACE;
-  plan = plan_forward(*a, a->workspace);
-  hipStream_t s = (hipStream_t)stream;
+  if (plan.bytes > 0 && (!ws || ws_bytes < plan.bytes)) return SFL_E_WORKSPACE;
+  plan = plan_forward(*a, ws);
   const Events ev{a->events, a->n_events};
   const int64_t T = a->T, d = a->d, f = a->f;
   const int64_t cap = capacity_of(a->cfg, T);
@@ -520,6 +572,10 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
   ev.record(4, s);
   return SFL_OK;
 }
+
+}  // namespace
+
+extern "C" {
 
 sfl_status_t sfl_dense_ffn_baseline(const sfl_ffn_args_t* a, sfl_stream_t stream) {
   sfl_status_t st = check_forward(a);

@@ -141,6 +141,25 @@ def test_forward_validates_before_launch():
     assert e.value.code == b.SFL_E_WORKSPACE
 
 
+def test_noalloc_forward_validates_and_bounds_its_scratch_before_launch():
+    """The forward that takes its workspace from the library's fixed device scratch checks
+    its arguments and rejects any call whose workspace exceeds the scratch before touching
+    the GPU; args->workspace is ignored."""
+    lib = b._lib
+    assert b.sfl_workspace_size(_fake_args(b.SFL_BF16, 8192, 4096, 16384), 0) > (64 << 20)
+    a = _fake_args(b.SFL_BF16, 128, 256, 1024)
+    assert lib.sfl_ffn_forward_noalloc(ctypes.byref(a), None) == b.SFL_E_ARG  # no TwELL buffers
+    big = _fake_args(b.SFL_BF16, 8192, 4096, 16384)
+    for n in b.BUF_NAMES:
+        setattr(big.twell, n, 0x3000)
+    big.workspace, big.workspace_bytes = 0x5000, 1 << 40  # ignored
+    assert lib.sfl_ffn_forward_noalloc(ctypes.byref(big), None) == b.SFL_E_WORKSPACE
+    bad = _fake_args(b.SFL_BF16, 128, 200, 1024)
+    for n in b.BUF_NAMES:
+        setattr(bad.twell, n, 0x3000)
+    assert lib.sfl_ffn_forward_noalloc(ctypes.byref(bad), None) == b.SFL_E_UNSUPPORTED
+
+
 def _fake_bwd(T, d, f, gated=False, **kw):
     a = b.BwdArgs()
     a.dtype = b.SFL_BF16
