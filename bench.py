@@ -47,7 +47,7 @@ def parse():
     p.add_argument("--quick", action="store_true", help="headline workload only")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="first run one plain 256 MiB device copy (reference for HBM byte counters)")
-    p.add_argument("--only", choices=["lognormal", "gated", "decode", "train", "gated_train", "tp8", "dp8"],
+    p.add_argument("--only", choices=["lognormal", "gated", "decode", "train", "gated_train", "tp8", "dp8", "fp32"],
                    help="run one secondary workload and print its record (for profiling); no headline line")
     return p.parse_args()
 
@@ -63,6 +63,23 @@ def file_hash(*paths):
 def measured_traffic(kernel_key, src_hash):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if it was taken
     on the current kernel source; None otherwise."""
+    rec = profile_record(kernel_key, src_hash)
+    return None if rec is None else rec.get("hbm_bytes_per_launch")
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def profile_record(kernel_key, src_hash):
+    """The committed rocprofv3 figures (kernel-trace average duration, counter readings) of
+    one kernel, if they were taken on the current kernel source; None otherwise."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
@@ -72,7 +89,7 @@ def measured_traffic(kernel_key, src_hash):
         return None
     if not rec or rec.get("source_hash") != src_hash:
         return None
-    return rec.get("hbm_bytes_per_launch")
+    return rec
 
 
 def cpu_baseline(w, seconds):
@@ -100,6 +117,7 @@ def cpu_baseline(w, seconds):
         if dt < seconds / 8:
             n = min(w.T, n * 2)
     return {"value": round(done_rows / spent, 1), "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "cpu_model": cpu_model(),
             "sample": f"{done_rows} seeded random rows of the same workload (fp64 oracle: pre-activation, "
                       f"TwELL extraction, hybrid classification, ELL gather / dense rows), {spent:.1f} s"}
 
@@ -148,6 +166,38 @@ class Bench:
             out.append(e0.elapsed_time(e1))
         return np.array(out)
 
+    def ceilings(self):
+        """Bandwidth ceilings of this GPU (sfl_bandwidth_probe): HBM copy (1 GiB buffers),
+        HBM read (4 GiB, one pass), L2 read (16 MiB, i.e. 2 MiB per XCD, re-read 400 times)."""
+        b, t = self.b, self.torch
+        sink = t.zeros(1, dtype=t.int32, device="cuda")
+        out = {}
+
+        def rate(fn):
+            moved = fn()
+            t.cuda.synchronize()
+            e0, e1 = t.cuda.Event(enable_timing=True), t.cuda.Event(enable_timing=True)
+            e0.record(self.stream)
+            moved = fn()
+            e1.record(self.stream)
+            t.cuda.synchronize()
+            return round(moved / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
+
+        src = t.empty(1 << 30, dtype=t.uint8, device="cuda")
+        dst = t.empty_like(src)
+        out["hbm_copy_GBs"] = rate(lambda: b.sfl_bandwidth_probe(src, dst, reps=3, stream=self.stream))
+        del dst
+        big = t.empty(4 << 30, dtype=t.uint8, device="cuda")
+        out["hbm_read_GBs"] = rate(lambda: b.sfl_bandwidth_probe(big, None, reps=1, sink=sink, stream=self.stream))
+        del big
+        small = src[:16 << 20]
+        out["l2_read_GBs"] = rate(lambda: b.sfl_bandwidth_probe(small, None, reps=400, sink=sink,
+                                                                stream=self.stream))
+        del src, small
+        out["how"] = ("sfl_bandwidth_probe: copy of 1 GiB (bytes read + written), one read pass over 4 GiB, "
+                      "400 read passes over 16 MiB split so that each XCD re-reads its own 2 MiB")
+        return out
+
     def stage_times(self, make_args, call, n_ev, steps=None):
         b = self.b
         steps = steps or self.steps
@@ -164,8 +214,9 @@ class Bench:
         X, Wu, Wd = self.dev(w.X), self.dev(w.W_up), self.dev(w.W_down)
         Wg = self.dev(w.W_gate) if w.gated else None
         cfg = b.make_cfg(**w.cfg)
-        bufs = b.alloc_twell(w.T, w.f, "bf16", cfg)
-        Y = t.empty((w.T, w.d), dtype=t.bfloat16, device="cuda")
+        act = t.bfloat16 if w.dtype == "bf16" else t.float32
+        bufs = b.alloc_twell(w.T, w.f, "bf16" if w.dtype == "bf16" else "f32", cfg)
+        Y = t.empty((w.T, w.d), dtype=act, device="cuda")
         stats = b.alloc_stats()
         WdP = WuP = WupT = WgT = WdT = None
         if packed and w.dtype == "bf16" and w.d % 512 == 0:
@@ -209,7 +260,8 @@ class Bench:
         s = self.setup_forward(w)
         ms = self.time(lambda: b.sfl_ffn_forward(s["args"], self.stream))
         st = b.read_stats(s["stats"])
-        rec = {"workload": w.name, "tokens": w.T, "ms": round(ms, 4), "tokens_per_s": round(w.T / ms * 1e3, 1),
+        rec = {"workload": w.name, "dtype": w.dtype, "tokens": w.T, "ms": round(ms, 4),
+               "tokens_per_s": round(w.T / ms * 1e3, 1),
                "realised_sparsity": round(1 - st["total_nnz"] / (w.T * w.f), 5), "n_ovf_rows": st["n_ovf_rows"]}
         if stages:
             rec["stages_ms"] = dict(zip(["up_gemm_twell", "classify", "sparse_down", "dense_backup"],
@@ -243,7 +295,7 @@ class Bench:
                                                   s["X"], s["Wu"], s["Wd"], s["cfg"], **s["dkw"],
                                                   workspace=s["dws"], events=ev),
                                                   b.sfl_dense_ffn_baseline, 3)))
-            if not w.gated:
+            if not w.gated and w.dtype == "bf16":
                 # the same dense FFN through torch (hipBLASLt GEMMs), for context
                 t = self.torch
                 X, Wd, WupT = s["X"], s["Wd"], s["WupT"]
@@ -375,7 +427,7 @@ def main():
         else:
             wo = {"lognormal": wl.c2_lognormal, "gated": lambda: wl.c3_gated(T=8192),
                   "decode": lambda: wl.c3_gated(T=32), "tp8": lambda: wl.c4_shard("tp8"),
-                  "dp8": lambda: wl.c4_shard("dp8")}[a.only]()
+                  "dp8": lambda: wl.c4_shard("dp8"), "fp32": wl.c1_small_fp32}[a.only]()
             rec = B.forward_record(wo)[0]
         print(json.dumps({"only": a.only, "record": rec}), flush=True)
         return
@@ -394,27 +446,51 @@ def main():
     ms_unpacked = B.time(lambda: b.sfl_ffn_forward(ua, B.stream))
     del uws
 
-    # roofline of the dominant kernel (the up-projection GEMM with the TwELL epilogue)
+    # roofline of the dominant kernel (the up-projection GEMM with the TwELL epilogue).
+    # `achieved` divides the algorithmic flops by this run's HIP-event time of the up
+    # projection stage (one kernel launch on the library's stream); the committed rocprofv3
+    # kernel-trace average of the same kernel, and the MFMA busy share read from its counters,
+    # are reported beside it (when they were taken on the current kernel source).
     up_flops = 2.0 * T * d * f
     achieved = up_flops / (stages["up_gemm_twell"] * 1e-3) / 1e12
     csrc = os.path.join(ROOT, "paper_2603_23198_amd", "csrc")
     gemm_hash = file_hash(os.path.join(csrc, "gemm.hip"), os.path.join(csrc, "common.h"))
     gather_hash = file_hash(os.path.join(csrc, "gather.hip"), os.path.join(csrc, "common.h"))
+    gprof = profile_record("up_gemm_twell", gemm_hash) or {}
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": BF16_MFMA_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / BF16_MFMA_PEAK_TFLOPS, 4),
-                "traffic": measured_traffic("up_gemm_twell", gemm_hash),
-                "kernel": "k_gemm_kc<EPI_TWELL, 256, LAY_KC>", "work": "2*T*d*f flops per launch"}
-    # the sparse down projection: algorithmic bytes = sum_t nnz_t*(2d + 4) + (2d + 5) per sparse row
+                "traffic": gprof.get("hbm_bytes_per_launch"),
+                "kernel": "k_gemm_kc<EPI_TWELL, 256, LAY_KC>", "work": "2*T*d*f flops per launch",
+                "timing": "HIP events around the up-projection stage, this run"}
+    if gprof.get("avg_duration_us"):
+        pa = up_flops / (gprof["avg_duration_us"] * 1e-6) / 1e12
+        roofline["profile"] = {"avg_us": gprof["avg_duration_us"], "achieved": round(pa, 2),
+                               "frac": round(pa / BF16_MFMA_PEAK_TFLOPS, 4),
+                               "mfma_busy_frac": gprof.get("mfma_busy_frac"),
+                               "source": "profiles/traffic.json (rocprofv3 kernel trace and counters)"}
+    # the sparse down projection: algorithmic bytes = sum_t nnz_t*(2d + 4) + (2d + 5) per sparse
+    # row. Each token re-reads its W_down rows, which the XCDs' L2 caches serve (W_down is read
+    # slice by slice), so the effective rate is compared with the measured L2 read ceiling;
+    # the DRAM side is the counter bytes that came from beyond L2 over the kernel's duration.
     nnz = int(st["total_nnz"])
     n_sparse = T - int(st["n_ovf_rows"])
     gbytes = nnz * (2 * d + 4) + n_sparse * (2 * d + 5)
     g_rate = gbytes / (stages["sparse_down"] * 1e-3) / 1e9
-    gather = {"bound": "hbm", "achieved": round(g_rate, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-              "frac": round(g_rate / HBM_PEAK_GBS, 4), "algorithmic_bytes": gbytes,
-              "traffic": measured_traffic("gather_down", gather_hash),
+    ceil = B.ceilings()
+    dprof = profile_record("gather_down", gather_hash) or {}
+    gather = {"bound": "l2", "achieved": round(g_rate, 1), "peak": ceil["l2_read_GBs"], "unit": "GB/s",
+              "frac": round(g_rate / ceil["l2_read_GBs"], 4), "algorithmic_bytes": gbytes,
+              "effective_frac_of_hbm_spec": round(g_rate / HBM_PEAK_GBS, 4),
+              "traffic": dprof.get("hbm_bytes_per_launch"),
               "kernel": "k_gather_down_b16",
-              "note": "effective rate: each token re-reads its W_down rows; they are served from L2, "
-                      "so this exceeds the HBM peak; the HBM bytes actually moved are `traffic`"}
+              "timing": "HIP events around the sparse down projection stage, this run",
+              "peak_source": "measured L2 read ceiling (ceilings.l2_read_GBs)"}
+    if dprof.get("hbm_bytes_per_launch") and dprof.get("avg_duration_us"):
+        dram = dprof["hbm_bytes_per_launch"] / (dprof["avg_duration_us"] * 1e-6) / 1e9
+        gather["dram_side"] = {"GBs": round(dram, 1), "frac_of_hbm_spec": round(dram / HBM_PEAK_GBS, 4),
+                               "frac_of_measured_hbm_read": round(dram / ceil["hbm_read_GBs"], 4),
+                               "avg_us": dprof["avg_duration_us"],
+                               "source": "profiles/traffic.json (FETCH_SIZE + WRITE_SIZE, kernel trace)"}
 
     # distribution of single calls, warm and cold: before each cold call a 1 GiB buffer is
     # written, which evicts W_up, W_down and X from L2 and the 256 MiB infinity cache
@@ -459,6 +535,7 @@ def main():
         "n_ovf_rows": head["n_ovf_rows"],
         "roofline": roofline,
         "gather_roofline": gather,
+        "ceilings": ceil,
         # the fused ReLU -> TwELL epilogue measured as the difference to the same GEMM with a
         # plain ReLU + bf16 store epilogue (the dense FFN's first GEMM)
         "twell_epilogue_delta_ms": round(stages["up_gemm_twell"] - head["dense_stages_ms"]["up_gemm_relu"], 4),
@@ -473,6 +550,9 @@ def main():
             others.append(r)
             del s2
         r, s2, _ = B.forward_record(wl.c2_lognormal())
+        others.append(r)
+        del s2
+        r, s2, _ = B.forward_record(wl.c1_small_fp32())
         others.append(r)
         del s2
         for tt in (8192, 32):

@@ -378,6 +378,22 @@ sfl_status_t sfl_reinit_dead_units(void* W, sfl_dtype_t dtype, int64_t rows, int
 sfl_status_t sfl_transpose(const void* in, void* out, int64_t rows, int64_t cols,
                            int32_t elem_bytes, sfl_stream_t stream);
 
+/* Measurement utility (no step of the layer uses it): the bandwidth ceilings that the
+ * kernels' rates are compared against, on the machine at hand.
+ *  dst != NULL: copies bytes (rounded down to 16) from src to dst, reps times (the HBM copy
+ *               rate for buffers far larger than the 256 MiB infinity cache);
+ *  dst == NULL: 2048 blocks each read one contiguous 1/2048 of src (bytes rounded down to a
+ *               multiple of 2048 x 16) reps times. Block b runs on XCD b % 8, so each XCD
+ *               re-reads its own 1/8 of src: a src of at most 8 x 4 MiB is then served from
+ *               the XCDs' L2 caches after the first pass (the L2 read ceiling); a src beyond
+ *               the infinity cache with reps = 1 measures HBM reads.
+ * *moved (host) receives the bytes read plus written. sink: device uint32 [1] (read mode;
+ * written only on an unlikely value, so the reads cannot be optimised away). src and dst
+ * device memory, 16-byte aligned. Errors: SFL_E_ARG for NULL src or moved, reps < 1,
+ * misaligned pointers, or a read without sink. */
+sfl_status_t sfl_bandwidth_probe(const void* src, void* dst, size_t bytes, int32_t reps, uint32_t* sink,
+                                 size_t* moved, sfl_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -679,6 +679,14 @@ sfl_status_t sfl_reinit_dead_units(void* W, sfl_dtype_t dtype, int64_t rows, int
   return SFL_OK;
 }
 
+sfl_status_t sfl_bandwidth_probe(const void* src, void* dst, size_t bytes, int32_t reps, uint32_t* sink,
+                                 size_t* moved, sfl_stream_t stream) {
+  if (!src || !moved || reps < 1 || ((uintptr_t)src & 15) || ((uintptr_t)dst & 15)) return SFL_E_ARG;
+  if (!dst && !sink) return SFL_E_ARG;
+  SFL_HIP(launch_bandwidth_probe(src, dst, bytes, reps, sink, moved, (hipStream_t)stream));
+  return SFL_OK;
+}
+
 sfl_status_t sfl_ffn_backward(const sfl_ffn_bwd_args_t* a, sfl_stream_t stream) {
   return sfl::backward_run(a, (hipStream_t)stream);
 }

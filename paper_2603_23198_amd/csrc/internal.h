@@ -163,4 +163,10 @@ hipError_t launch_reinit_units(void* W, int val_bf16, int64_t rows, int64_t cols
                                const int64_t* last, int64_t step, float lam, float sigma, const float* noise,
                                hipStream_t s);
 
+// ---------------------------------------------------------- measurement ----
+// Copy (dst != null: dst = src, `reps` times) or read (dst == null: every block re-reads
+// its own chunk of src `reps` times) over `bytes`; *moved = bytes read plus written.
+hipError_t launch_bandwidth_probe(const void* src, void* dst, size_t bytes, int reps, uint32_t* sink, size_t* moved,
+                                  hipStream_t s);
+
 }  // namespace sfl
