@@ -47,7 +47,8 @@ def parse():
     p.add_argument("--quick", action="store_true", help="headline workload only")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="first run one plain 256 MiB device copy (reference for HBM byte counters)")
-    p.add_argument("--only", choices=["lognormal", "gated", "decode", "train", "gated_train", "tp8", "dp8", "fp32"],
+    p.add_argument("--only", choices=["lognormal", "gated", "decode", "train", "gated_train", "tp8", "dp8", "fp32",
+                                       "splitd"],
                    help="run one secondary workload and print its record (for profiling); no headline line")
     return p.parse_args()
 
@@ -255,10 +256,19 @@ class Bench:
         s["mk"] = lambda ev: b.ffn_args(X, Wu, Wd, cfg, **kw, workspace=ws, events=ev)
         return s
 
-    def forward_record(self, w, dense=True, stages=True):
+    def forward_record(self, w, dense=True, stages=True, order_ab=False):
         b = self.b
         s = self.setup_forward(w)
         ms = self.time(lambda: b.sfl_ffn_forward(s["args"], self.stream))
+        if order_ab:
+            # the sparse down projection's token order: descending row count / token order
+            # (the default picks one of them by batch size and ELL width)
+            ab = {}
+            for order in ("nnz", "token", "nnz", "token"):
+                os.environ["SFL_TOKEN_ORDER"] = order
+                ab.setdefault(order, []).append((self.time(lambda: b.sfl_ffn_forward(s["args"], self.stream)),
+                                                 self.stage_times(s["mk"], b.sfl_ffn_forward, 5)[2]))
+            os.environ.pop("SFL_TOKEN_ORDER", None)
         st = b.read_stats(s["stats"])
         rec = {"workload": w.name, "dtype": w.dtype, "tokens": w.T, "ms": round(ms, 4),
                "tokens_per_s": round(w.T / ms * 1e3, 1),
@@ -266,6 +276,12 @@ class Bench:
         if stages:
             rec["stages_ms"] = dict(zip(["up_gemm_twell", "classify", "sparse_down", "dense_backup"],
                                         self.stage_times(s["mk"], b.sfl_ffn_forward, 5)))
+        if order_ab:
+            rec["token_order_ab"] = {
+                o: {"ms": round(float(np.mean([x[0] for x in v])), 4),
+                    "sparse_down_ms": round(float(np.mean([x[1] for x in v])), 4)} for o, v in ab.items()}
+            rec["token_order_ab"]["note"] = ("SFL_TOKEN_ORDER=nnz (descending row count) / token; the order kernel "
+                                             "runs inside the sparse down projection stage")
         if w.T <= 256:
             # launch-bound shapes: the same call captured once in a HIP graph and replayed
             t = self.torch
@@ -314,6 +330,24 @@ class Bench:
                 rec["dense_torch_ms"] = round(tms, 4)
                 rec["speedup_vs_dense_torch"] = round(tms / ms, 4)
         return rec, s, st
+
+    def splitd_record(self, w, splits=(1, 2, 4, 8)):
+        """The forward's sparse down projection (slice-major walk, stage events) against the
+        paper-shaped row-wise kernel (sfl_down_projection_rowwise) on the same ELL rows, for
+        each split of d."""
+        b = self.b
+        s = self.setup_forward(w)
+        b.sfl_ffn_forward(s["args"], self.stream)
+        stages = dict(zip(["up_gemm_twell", "classify", "sparse_down", "dense_backup"],
+                          self.stage_times(s["mk"], b.sfl_ffn_forward, 5)))
+        Y2 = self.torch.empty_like(s["Y"])
+        a2 = b.ffn_args(s["X"], s["Wu"], s["Wd"], s["cfg"], Y=Y2, bufs=s["bufs"])
+        rw = {str(sp): round(self.time(lambda: b.sfl_down_projection_rowwise(a2, sp, self.stream)), 4)
+              for sp in splits}
+        best = min(rw, key=rw.get)
+        return {"workload": w.name, "ell_width": w.cfg["ell_width"], "slice_walk_ms": stages["sparse_down"],
+                "rowwise_ms_by_split": rw, "rowwise_best_split": int(best),
+                "slice_walk_speedup_vs_best_rowwise": round(rw[best] / stages["sparse_down"], 3)}
 
     def training_record(self, w, lam):
         """Forward + backward (sfl_ffn_backward) of the layer, gated or not; the same dense
@@ -421,6 +455,11 @@ def main():
         del src, dst
     B = Bench(b, torch, a.steps, a.warmup)
     if a.only:
+        if a.only == "splitd":
+            recs = [B.splitd_record(wl.c4_sweep(sp, ell_width=k)) for sp, k in
+                    ((0.99, 256), (0.995, 192), (0.998, 128), (0.999, 64))]
+            print(json.dumps({"only": a.only, "records": recs}), flush=True)
+            return
         if a.only in ("train", "gated_train"):
             wt = wl.c5_training() if a.only == "train" else wl.gated_training()
             rec = B.training_record(wt, 2e-5)
@@ -433,9 +472,18 @@ def main():
         return
     w = wl.c4_sweep(a.sparsity, T=a.tokens)
     T, d, f = w.T, w.d, w.f
-    head, s, st = B.forward_record(w)
+    head, s, st = B.forward_record(w, order_ab=True)
     ms = head["ms"]
     stages = head["stages_ms"]
+
+    # the up projection's persistent tile order: XCD-grouped (default) against a Hilbert curve
+    order_ab = {}
+    for order in ("grouped", "hilbert", "grouped", "hilbert", "grouped", "hilbert"):
+        os.environ["SFL_GEMM_TILE_ORDER"] = order
+        order_ab.setdefault(order + "_ms", []).append(
+            B.stage_times(s["mk"], b.sfl_ffn_forward, 5)[0])
+    os.environ.pop("SFL_GEMM_TILE_ORDER", None)
+    order_ab = {k: round(float(np.mean(v)), 4) for k, v in order_ab.items()}
 
     # the same step when W_down is re-laid out inside every call (no pre-packed copy)
     kw = dict(s["kw"])
@@ -530,8 +578,10 @@ def main():
         "dense_torch_ms_per_step": head.get("dense_torch_ms"),
         "speedup_vs_dense_torch": head.get("speedup_vs_dense_torch"),
         "stages_ms": stages,
+        "token_order_ab": head.get("token_order_ab"),
         "single_call_timing": timing,
         "ms_per_step_w_down_packed_per_call": round(ms_unpacked, 4),
+        "up_gemm_tile_order_ab": order_ab,
         "n_ovf_rows": head["n_ovf_rows"],
         "roofline": roofline,
         "gather_roofline": gather,
@@ -549,17 +599,19 @@ def main():
             r, s2, _ = B.forward_record(wl.c4_sweep(sp_, T=a.tokens), stages=True)
             others.append(r)
             del s2
-        r, s2, _ = B.forward_record(wl.c2_lognormal())
+        r, s2, _ = B.forward_record(wl.c2_lognormal(), order_ab=True)
         others.append(r)
         del s2
         r, s2, _ = B.forward_record(wl.c1_small_fp32())
         others.append(r)
         del s2
         for tt in (8192, 32):
-            r, s2, _ = B.forward_record(wl.c3_gated(T=tt))
+            r, s2, _ = B.forward_record(wl.c3_gated(T=tt), order_ab=True)
             others.append(r)
             del s2
         out["other_workloads"] = others
+        # the paper's row-wise down kernel against the slice walk at the headline workload
+        out["down_projection_ab"] = B.splitd_record(wl.c4_sweep(0.99, T=a.tokens))
         # one GPU's share of the headline layer run on eight GPUs: hidden units split eight
         # ways (tensor parallel, f = 2048) or tokens split eight ways (data parallel, T = 1024);
         # the collectives around them are not part of this record

@@ -26,6 +26,16 @@
  *    concurrent calls on different streams with disjoint buffers (workspaces
  *    included) are safe, except sfl_ffn_forward_noalloc calls that overlap on
  *    one GPU (they share its scratch array).
+ *  - Environment: SFL_GEMM_TILE_ORDER=hilbert makes the up (gate) projection of
+ *    sfl_ffn_forward and sfl_up_projection deal its 256 x 256 output tiles along a
+ *    Hilbert curve (the paper's persistent-GEMM schedule) instead of the default
+ *    XCD-grouped order; results are identical (each tile's sums do not depend on
+ *    the order). sfl_ffn_forward's sparse down projection (and the gated up-dots)
+ *    deals the tokens by descending row count (one more kernel, a counting sort) for
+ *    batches of at least 1024 tokens with ell_width <= 256, and in token order
+ *    otherwise; SFL_TOKEN_ORDER=nnz or SFL_TOKEN_ORDER=token forces one of the two.
+ *    Results are identical either way. Both variables are read on every call; they
+ *    are meant for schedule comparisons.
  *  - Numerics: bf16 inputs are multiplied on MFMA with float32 accumulation;
  *    activations are stored in the activation dtype, bf16 by round-to-nearest-
  *    even. A hidden unit is active iff its pre-activation is > 0 (strict; +0,
@@ -377,6 +387,19 @@ sfl_status_t sfl_reinit_dead_units(void* W, sfl_dtype_t dtype, int64_t rows, int
  * 4-byte (elem_bytes = 4) elements; lets callers keep W_upT next to W_up. */
 sfl_status_t sfl_transpose(const void* in, void* out, int64_t rows, int64_t cols,
                            int32_t elem_bytes, sfl_stream_t stream);
+
+/* The sparse down projection as the paper's non-gated down kernel lays it out (Alg. 3's
+ * sparse part, with d split into `split` segments): one wave per (token, segment of
+ * d / split columns) walks the token's ELL entries in order and streams each active unit's
+ * W_down row segment, fp32 accumulation, bf16 store. A comparison variant of the down
+ * projection inside sfl_ffn_forward (which walks slice-major copies of W_down per XCD
+ * instead); same inputs and the same arithmetic per entry, so the two agree to summation
+ * order. Reads args->{T, d, f, cfg.ell_width, W_down [f][d], twell.ell_val, ell_idx,
+ * row_nnz, row_ovf} as sfl_ffn_forward leaves them; writes Y [T][d] for the rows with
+ * row_ovf = 0 only (the dense-backup rows are left as they are). BF16 only.
+ * Errors: SFL_E_ARG for a non-bf16 dtype or NULL buffers (T > 0); SFL_E_UNSUPPORTED unless
+ * d / split is 512, 1024, 2048 or 4096. */
+sfl_status_t sfl_down_projection_rowwise(const sfl_ffn_args_t* args, int32_t split, sfl_stream_t stream);
 
 /* Measurement utility (no step of the layer uses it): the bandwidth ceilings that the
  * kernels' rates are compared against, on the machine at hand.

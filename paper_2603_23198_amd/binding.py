@@ -28,7 +28,8 @@ BUF_NAMES = ["val", "idx", "cnt", "row_nnz", "row_ovf", "ovf_rows", "n_ovf", "el
 EXPORTED = ["sfl_status_string", "sfl_version", "sfl_twell_buffer_sizes", "sfl_pack_twell",
             "sfl_workspace_size", "sfl_ffn_forward", "sfl_up_projection", "sfl_ffn_backward",
             "sfl_dense_ffn_baseline", "sfl_transpose", "sfl_pack_down_weights", "sfl_track_active_units",
-            "sfl_reinit_dead_units", "sfl_ffn_forward_noalloc", "sfl_bandwidth_probe"]
+            "sfl_reinit_dead_units", "sfl_ffn_forward_noalloc", "sfl_bandwidth_probe",
+            "sfl_down_projection_rowwise"]
 
 
 class SflError(RuntimeError):
@@ -82,6 +83,7 @@ _lib.sfl_pack_twell.argtypes = [c_void_p, c_int64, c_int64, c_int, POINTER(Cfg),
 _lib.sfl_workspace_size.argtypes = [c_void_p, c_int, POINTER(c_size_t)]
 _lib.sfl_ffn_forward.argtypes = [POINTER(FfnArgs), c_void_p]
 _lib.sfl_ffn_forward_noalloc.argtypes = [POINTER(FfnArgs), c_void_p]
+_lib.sfl_down_projection_rowwise.argtypes = [POINTER(FfnArgs), c_int32, c_void_p]
 _lib.sfl_bandwidth_probe.argtypes = [c_void_p, c_void_p, c_size_t, c_int32, c_void_p, POINTER(c_size_t), c_void_p]
 _lib.sfl_up_projection.argtypes = [POINTER(FfnArgs), c_void_p, c_void_p]
 _lib.sfl_ffn_backward.argtypes = [POINTER(BwdArgs), c_void_p]
@@ -281,6 +283,10 @@ def sfl_reinit_dead_units(W, last_active, step, lam, sigma, noise, units_on_rows
                                                                1 if units_on_rows else 0, _ptr(last_active),
                                                                int(step), float(lam), float(sigma), _ptr(noise),
                                                                _stream(stream)))
+
+
+def sfl_down_projection_rowwise(args, split, stream=None):
+    _check("sfl_down_projection_rowwise", _lib.sfl_down_projection_rowwise(ctypes.byref(args), split, _stream(stream)))
 
 
 def sfl_bandwidth_probe(src, dst=None, reps=1, sink=None, nbytes=None, stream=None):

@@ -280,7 +280,7 @@ template <int VK, int OUT, int U, bool TG = false>
 __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
     int64_t T, int64_t d, int64_t f, int K, const void* __restrict__ ell_val, const uint16_t* __restrict__ ell_idx,
     const int32_t* __restrict__ row_nnz, const uint8_t* __restrict__ row_ovf, const bf16_t* __restrict__ W,
-    bf16_t* __restrict__ Y, float* __restrict__ Yf, int n_slices, int tpw) {
+    bf16_t* __restrict__ Y, float* __restrict__ Yf, int n_slices, int tpw, const int32_t* __restrict__ order) {
   constexpr int EW = VK + 1;         // words per staged entry
   // token groups read 8 tokens' entries at once: an odd stride puts them in different banks
   const int KS = TG ? K + 1 : K;
@@ -291,15 +291,21 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
   const int l = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int grp = l / LPR, sub = l % LPR;
+  // the block's tokens: positions t0 .. t0+tpw-1 of the processing order (identity, or the
+  // tokens sorted by descending row count); token T marks a position past the batch
+  auto tok = [&](int i) -> int64_t {
+    const int64_t q = t0 + i;
+    return q < T ? (order ? (int64_t)order[q] : q) : T;
+  };
   // stage the block's ELL rows in LDS
   for (int i = threadIdx.x; i < tpw; i += blockDim.x) {
-    const int64_t t = t0 + i;
+    const int64_t t = tok(i);
     cnt_s[i] = (t < T && !row_ovf[t]) ? row_nnz[t] : -1;
   }
   __syncthreads();
   for (int i = wave; i < tpw; i += GATHER_WAVES) {
     const int c = cnt_s[i];
-    const int64_t t = t0 + i;
+    const int64_t t = tok(i);
     for (int e = l; e < c; e += 64) {
       if constexpr (VK >= 1) {
         ent[EW * (i * KS + e)] = (uint32_t)ell_idx[t * K + e];
@@ -381,7 +387,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
       int e0 = 0;
       for (; e0 + U <= cmin; e0 += U) round(e0, std::false_type{});
       for (; e0 < cmax; e0 += U) round(e0, std::true_type{});
-      if (c >= 0) store_slice<OUT>(Y, Yf, (t0 + i) * d + (int64_t)slice * SLICE2 + sub * 8, acc);
+      if (c >= 0) store_slice<OUT>(Y, Yf, tok(i) * d + (int64_t)slice * SLICE2 + sub * 8, acc);
     }
     return;
   }
@@ -398,7 +404,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
         slice_token_f32<U>(ent + 2 * i * K, nnz, wr, col_b, grp, acc);
       else
         slice_token<U>(ent + i * K, nnz, wr, col_b, grp, acc);
-      if (grp == 0) store_slice<OUT>(Y, Yf, (t0 + i) * d + col, acc);
+      if (grp == 0) store_slice<OUT>(Y, Yf, tok(i) * d + col, acc);
     }
   }
 }
@@ -434,7 +440,7 @@ template <int U>
 __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gated_updot(
     int64_t T, int64_t d, int64_t f, int K, const uint16_t* __restrict__ ell_idx, const int32_t* __restrict__ row_nnz,
     const uint8_t* __restrict__ row_ovf, const bf16_t* __restrict__ X, const bf16_t* __restrict__ WuP,
-    float* __restrict__ part_u, int n_slices, int tpw) {
+    float* __restrict__ part_u, int n_slices, int tpw, const int32_t* __restrict__ order) {
   // [tpw][K] indices, [ncopy][tpw][K] partial sums, [tpw] counts. With ncopy = 1 a token's
   // slices are handled by one wave in order; a small block (decode) deals (slice, token)
   // items to all waves, each slice with its own copy of the sums, added in slice order.
@@ -448,14 +454,18 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gated_updot(
   const int l = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int grp = l / LPR, sub = l % LPR;
+  auto tok = [&](int i) -> int64_t {  // as in k_gather_down_b16
+    const int64_t q = t0 + i;
+    return q < T ? (order ? (int64_t)order[q] : q) : T;
+  };
   for (int i = threadIdx.x; i < tpw; i += blockDim.x) {
-    const int64_t t = t0 + i;
+    const int64_t t = tok(i);
     cnt_s[i] = (t < T && !row_ovf[t]) ? row_nnz[t] : -1;
   }
   __syncthreads();
   for (int i = wave; i < tpw; i += GATHER_WAVES) {
     const int c = cnt_s[i];
-    const int64_t t = t0 + i;
+    const int64_t t = tok(i);
     for (int e = l; e < c; e += 64) {
       ent[i * K + e] = (uint32_t)ell_idx[t * K + e];
       for (int cp = 0; cp < ncopy; ++cp) us[((size_t)cp * tpw + i) * K + e] = 0.f;
@@ -471,7 +481,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gated_updot(
     const int nnz = __builtin_amdgcn_readfirstlane(cnt_s[i]);
     if (nnz <= 0) return;
     // this lane's 8 columns of x[t] in the slice, as bf16 pairs
-    const u32x4_t xv = *(const u32x4_t*)(X + (t0 + i) * d + (int64_t)slice * SLICE2 + sub * 8);
+    const u32x4_t xv = *(const u32x4_t*)(X + tok(i) * d + (int64_t)slice * SLICE2 + sub * 8);
     const uint32_t* er = ent + i * K;
     for (int q = 0; q < nnz; q += NGRP * U) {
       u32x4_t w[U];
@@ -511,7 +521,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gated_updot(
   __syncthreads();
   for (int i = wave; i < tpw; i += GATHER_WAVES) {
     const int c = cnt_s[i];
-    const int64_t t = t0 + i;
+    const int64_t t = tok(i);
     for (int e = l; e < c; e += 64) {
       float u = us[(size_t)i * K + e];
       for (int cp = 1; cp < ncopy; ++cp) u += us[((size_t)cp * tpw + i) * K + e];
@@ -763,7 +773,8 @@ hipError_t launch_gather_down(int val_bf16, int64_t T, int64_t d, int K, const v
 
 hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, const void* ell_val,
                                      const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
-                                     const void* Wp, void* Y, hipStream_t s, int val_f32, int out_mode, float* Yf) {
+                                     const void* Wp, void* Y, hipStream_t s, int val_f32, int out_mode, float* Yf,
+                                     const int32_t* order) {
   if (T == 0) return hipSuccess;
   if (d % (8 * SLICE2) != 0) return hipErrorInvalidValue;
   if (out_mode < 0 || out_mode > 2 || (out_mode > 0 && !Yf) || (out_mode != 1 && !Y)) return hipErrorInvalidValue;
@@ -787,7 +798,7 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
       if (e != hipSuccess) return e;                                                                               \
     }                                                                                                              \
     hipLaunchKernelGGL((k_gather_down_b16<VK_, OUT_, U_, TG_>), grid, block, lds, s, T, d, f, K, ell_val, ell_idx, \
-                       row_nnz, row_ovf, (const bf16_t*)Wp, (bf16_t*)Y, Yf, n_slices, tpw);                        \
+                       row_nnz, row_ovf, (const bf16_t*)Wp, (bf16_t*)Y, Yf, n_slices, tpw, order);                 \
   } while (0)
 #define SFL_GATHER_LAUNCH_U(VK_, OUT_, U_) SFL_GATHER_LAUNCH_G(VK_, OUT_, U_, false)
 #define SFL_GATHER_LAUNCH(VK_, OUT_)                  \
@@ -872,7 +883,8 @@ static int slice_walk_tpw(int64_t T, int64_t per_tok) {
 }
 
 hipError_t launch_gated_updot(int64_t T, int64_t d, int64_t f, int K, const uint16_t* ell_idx, const int32_t* row_nnz,
-                              const uint8_t* row_ovf, const void* X, const void* WuP, float* part_u, hipStream_t s) {
+                              const uint8_t* row_ovf, const void* X, const void* WuP, float* part_u, hipStream_t s,
+                              const int32_t* order) {
   if (T == 0) return hipSuccess;
   if (d % (8 * SLICE2) != 0) return hipErrorInvalidValue;
   const int64_t per_tok = (int64_t)std::max(K, 1) * 8 + 4;
@@ -890,10 +902,11 @@ hipError_t launch_gated_updot(int64_t T, int64_t d, int64_t f, int K, const uint
   if (short_rows)
     hipLaunchKernelGGL(k_gated_updot<GU_SHORT>, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), lds, s, T, d, f,
                        K, ell_idx, row_nnz, row_ovf, (const bf16_t*)X, (const bf16_t*)WuP, part_u, (int)(d / SLICE2),
-                       tpw);
+                       tpw, order);
   else
     hipLaunchKernelGGL(k_gated_updot<GU>, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), lds, s, T, d, f, K,
-                       ell_idx, row_nnz, row_ovf, (const bf16_t*)X, (const bf16_t*)WuP, part_u, (int)(d / SLICE2), tpw);
+                       ell_idx, row_nnz, row_ovf, (const bf16_t*)X, (const bf16_t*)WuP, part_u, (int)(d / SLICE2), tpw,
+                       order);
   return hipGetLastError();
 }
 

@@ -175,10 +175,56 @@ template <int ROWS> struct LoaderSel<LAY_RCG, ROWS> { typedef LoadRC<ROWS, true>
 // Output-tile order: consecutive workgroup ids are dispatched round-robin over the 8 XCDs;
 // remap so that each XCD gets a contiguous range of logical tiles, then walk that range
 // in groups of 8 tile-rows so neighbouring workgroups share A rows and B columns in L2.
-__device__ __forceinline__ void tile_coords(int id, int tiles_m, int tiles_n, int& tm, int& tn) {
+// With order = TILE_ORDER_HILBERT (and a grid of square power-of-two blocks of tiles, side
+// by side along N or stacked along M) the logical tiles follow a Hilbert curve over each
+// square instead (the paper's persistent-GEMM schedule); other grids keep the grouped order.
+// Position h on the Hilbert curve of a side x side square (side a power of two): four
+// quadrants visited in the order (0,0), (0,1), (1,1), (1,0) of (x, y), the first turned so
+// that the curve enters and leaves through adjacent corners, built up one level at a time.
+__device__ __forceinline__ void hilbert_cell(int side, int h, int& x, int& y) {
+  x = 0;
+  y = 0;
+  for (int s = 1; s < side; s <<= 1) {
+    const int qx = 1 & (h >> 1);
+    const int qy = 1 & (h ^ qx);
+    if (qy == 0) {  // lower quadrants: reflect (right one) and transpose the part done so far
+      if (qx == 1) {
+        x = s - 1 - x;
+        y = s - 1 - y;
+      }
+      const int tmp = x;
+      x = y;
+      y = tmp;
+    }
+    x += s * qx;
+    y += s * qy;
+    h >>= 2;
+  }
+}
+
+__device__ __forceinline__ void tile_coords(int id, int tiles_m, int tiles_n, int& tm, int& tn, int order = 0) {
   const int nwg = tiles_m * tiles_n;
   int g = id;
   if ((nwg & 7) == 0) g = (g & 7) * (nwg >> 3) + (g >> 3);
+  if (order == TILE_ORDER_HILBERT) {
+    const bool pow2_m = (tiles_m & (tiles_m - 1)) == 0, pow2_n = (tiles_n & (tiles_n - 1)) == 0;
+    if (pow2_m && tiles_n % tiles_m == 0) {  // squares of side tiles_m along N
+      const int sq = g / (tiles_m * tiles_m);
+      int x, y;
+      hilbert_cell(tiles_m, g % (tiles_m * tiles_m), x, y);
+      tm = y;
+      tn = sq * tiles_m + x;
+      return;
+    }
+    if (pow2_n && tiles_m % tiles_n == 0) {  // squares of side tiles_n along M
+      const int sq = g / (tiles_n * tiles_n);
+      int x, y;
+      hilbert_cell(tiles_n, g % (tiles_n * tiles_n), x, y);
+      tm = sq * tiles_n + y;
+      tn = x;
+      return;
+    }
+  }
   constexpr int GM = 8;
   const int group = g / (GM * tiles_n);
   const int first_m = group * GM;
@@ -397,7 +443,7 @@ __global__ __launch_bounds__(NTHR) void k_gemm_bf16(GemmParams p) {
 
   const int tiles_m = (int)cdiv(p.M, BM), tiles_n = (int)cdiv(p.N, BN);
   int tm, tn;
-  tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
+  tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn, p.tile_order);
   const int m0 = tm * BM, n0 = tn * BN;
   const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
   if (m0 >= m_eff) return;
@@ -749,7 +795,7 @@ __global__ __launch_bounds__(NTHR) void k_gemm_kc(GemmParams p) {
   // the next tile of this block at or after v whose rows are counted
   auto next_live = [&](int v, int& tm, int& tn) {
     for (; v < nt; v += gridDim.x) {
-      tile_coords(v, tiles_m, tiles_n, tm, tn);
+      tile_coords(v, tiles_m, tiles_n, tm, tn, p.tile_order);
       if (tm * BM < m_eff) break;
     }
     return v;

@@ -25,6 +25,9 @@ enum Epilogue {
   EPI_MUL_ACT = 6,     // C_act[crow][n] = C_act[crow][n] * acc (gated h = ReLU(g) * u)
 };
 
+// Persistent tile orders of the 256 x 256 GEMMs.
+enum TileOrder { TILE_ORDER_GROUPED = 0, TILE_ORDER_HILBERT = 1 };
+
 struct GemmParams {
   int M, N, K;
   const void* A;
@@ -67,6 +70,8 @@ struct GemmParams {
   // of each tile to finish adds the tile's partial sums and applies the epilogue (no
   // reduction kernel), and sets its counter back to zero
   int32_t* tile_sem;
+  // order in which output tiles are dealt (TileOrder)
+  int tile_order;
 };
 
 // bf16 MFMA GEMM. Requirements: K % 8 == 0; RC layouts need even M/N extents and
@@ -101,6 +106,12 @@ hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32
                            int32_t* n_ovf, sfl_stats_t* stats, hipStream_t s,
                            int32_t* zero = nullptr, int n_zero = 0);
 hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s);
+// order[0 .. T): the sparse rows by descending row_nnz, then the dense-backup rows (one
+// workgroup, counting sort over K + 2 buckets; order within a bucket unspecified). Fails
+// with hipErrorInvalidValue when K + 2 buckets do not fit the kernel's LDS histogram.
+bool nnz_order_supported(int K);
+hipError_t launch_nnz_order(int64_t T, int K, const int32_t* row_nnz, const uint8_t* row_ovf, int32_t* order,
+                            hipStream_t s);
 // Dense-backup rows whose tiles kept every value, rebuilt from the TwELL slabs; the others
 // are listed (need_rows: token rows, need_slots: their ovf_dense rows, n_need) for the GEMM.
 hipError_t launch_ovf_fill(int64_t f, int val_bf16, int Tn, int S, const void* val, const uint16_t* idx,
@@ -122,7 +133,8 @@ hipError_t launch_gather_down(int val_bf16, int64_t T, int64_t d, int ell_width,
 hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int ell_width, const void* ell_val,
                                      const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
                                      const void* W_packed, void* Y, hipStream_t s,
-                                     int val_f32 = 0, int out_mode = 0, float* Yf = nullptr);
+                                     int val_f32 = 0, int out_mode = 0, float* Yf = nullptr,
+                                     const int32_t* order = nullptr);
 // Gated backward at the ELL entries: dh (8 partials + lambda' sign(g u)) -> dh_u, dh_g, h.
 hipError_t launch_gated_entry_grads(int64_t T, int K, const void* ell_val, const int32_t* row_nnz,
                                     const uint8_t* row_ovf, const float* part, const float* u, float lam, float* dhu,
@@ -130,8 +142,11 @@ hipError_t launch_gated_entry_grads(int64_t T, int K, const void* ell_val, const
 hipError_t launch_pack_down(const void* W, void* out, int64_t f, int64_t d, hipStream_t s);
 // Gated, two passes over slice-major copies: per-XCD partial up-dots u of every ELL entry
 // (part_u [8][T][K] fp32), then h = g * u (bf16, [T][K]) for the down-projection gather.
+// order (optional, [T]): the tokens in the order their work items are dealt (see
+// launch_nnz_order); the results do not depend on it.
 hipError_t launch_gated_updot(int64_t T, int64_t d, int64_t f, int K, const uint16_t* ell_idx, const int32_t* row_nnz,
-                              const uint8_t* row_ovf, const void* X, const void* WuP, float* part_u, hipStream_t s);
+                              const uint8_t* row_ovf, const void* X, const void* WuP, float* part_u, hipStream_t s,
+                              const int32_t* order = nullptr);
 // Backward per-unit gathers: out[n][:] = sum_e val[e] G[tok[e]][:] over n's list
 // [ptr[n], ptr[n+1]), G slice-major [d/64][R][64] bf16, out fp32 [n_units][d]; mean_bound
 // bounds the mean list length (sizes the blocks).
@@ -161,6 +176,13 @@ hipError_t launch_track_units(int64_t T, int64_t f, int n_tiles, int S, const in
 // w <- (1 - lam) w + lam sigma noise, noise fp32 of W's shape.
 hipError_t launch_reinit_units(void* W, int val_bf16, int64_t rows, int64_t cols, int units_on_rows,
                                const int64_t* last, int64_t step, float lam, float sigma, const float* noise,
+                               hipStream_t s);
+
+// The paper's layout of the sparse down projection (one wave per token and segment of d),
+// for comparison with launch_gather_down_packed: Y rows of the sparse rows, bf16.
+bool rowwise_supported(int64_t d, int split);
+hipError_t launch_down_rowwise(int64_t T, int64_t d, int K, const void* ell_val, const uint16_t* ell_idx,
+                               const int32_t* row_nnz, const uint8_t* row_ovf, const void* W, void* Y, int split,
                                hipStream_t s);
 
 // ---------------------------------------------------------- measurement ----

@@ -294,6 +294,54 @@ hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Processing order of the tokens for the sparse down projection: the sparse rows by
+// descending row count, then the dense-backup rows (which the gathers skip). A counting
+// sort in one workgroup: bucket K - n for a sparse row of n entries (n <= K), bucket K + 1
+// for a dense-backup row; histogram in LDS, exclusive scan over the buckets, then each
+// token placed at its bucket's cursor (LDS atomics, so the order within a bucket varies;
+// the gathers' results do not depend on it).
+constexpr int kOrderMaxBuckets = 16384;
+bool nnz_order_supported(int K) { return K >= 0 && K + 2 <= kOrderMaxBuckets; }
+
+__global__ __launch_bounds__(1024) void k_nnz_order(int64_t T, int K, const int32_t* __restrict__ row_nnz,
+                                                    const uint8_t* __restrict__ row_ovf, int32_t* __restrict__ order) {
+  __shared__ int hist[kOrderMaxBuckets];
+  __shared__ int wsum[16];
+  const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
+  const int nb = K + 2;
+  auto bucket = [&](int64_t t) { return row_ovf[t] ? K + 1 : K - min(max(row_nnz[t], 0), K); };
+  for (int i = tid; i < nb; i += 1024) hist[i] = 0;
+  __syncthreads();
+  for (int64_t t = tid; t < T; t += 1024) atomicAdd(&hist[bucket(t)], 1);
+  __syncthreads();
+  // exclusive scan: thread j owns buckets [j per, (j + 1) per)
+  const int per = (nb + 1023) / 1024;
+  const int b0 = min(nb, tid * per), b1 = min(nb, b0 + per);
+  int local = 0;
+  for (int b = b0; b < b1; ++b) local += hist[b];
+  const int incl = wave_incl_scan(local);
+  if (l == 63) wsum[w] = incl;
+  __syncthreads();
+  int before = 0;
+  for (int i = 0; i < w; ++i) before += wsum[i];
+  int run = before + incl - local;
+  for (int b = b0; b < b1; ++b) {
+    const int c = hist[b];
+    hist[b] = run;
+    run += c;
+  }
+  __syncthreads();
+  for (int64_t t = tid; t < T; t += 1024) order[atomicAdd(&hist[bucket(t)], 1)] = (int32_t)t;
+}
+
+hipError_t launch_nnz_order(int64_t T, int K, const int32_t* row_nnz, const uint8_t* row_ovf, int32_t* order,
+                            hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  if (!nnz_order_supported(K) || T > INT32_MAX) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_nnz_order, dim3(1), dim3(1024), 0, s, T, K, row_nnz, row_ovf, order);
+  return hipGetLastError();
+}
+
 // One workgroup of 1024 threads; each pass covers 1024 x 16 rows, thread i taking 16
 // consecutive rows (their flags loaded together), so a pass costs one round of loads.
 // An exclusive scan of the threads' counts (wave scans + a scan of the 16 wave totals)

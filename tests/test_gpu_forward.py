@@ -177,16 +177,20 @@ def test_fused_twell_equals_pack_of_same_mainloop(T, f, Tn, S, use_wupt):
     assert rel_l2(to_f64(Y)[rows], Yref) <= 2e-2
 
 
+@pytest.mark.parametrize("order", ["grouped", "hilbert"])
 @pytest.mark.parametrize("use_wupt", [False, True])
 @pytest.mark.parametrize("T,f,Tn", [(2048, 16384, 256), (1800, 16320, 128)])
-def test_fused_twell_bit_exact_over_several_tiles_per_block(T, f, Tn, use_wupt):
+def test_fused_twell_bit_exact_over_several_tiles_per_block(T, f, Tn, use_wupt, order, monkeypatch):
     """The up projection's blocks are persistent (one per CU) and walk several 256 x 256
     output tiles each: 512 tiles at T = 2048, f = 16384 (two or more per block), 7 x 64
     ragged ones at T = 1800, f = 16320. While a tile's epilogue runs, the next tile's first
     stage, bias and shift are already loading into the other buffer. Every tile, second and
     later ones included, with a non-zero per-column bias and per-row shift: the fused TwELL
     is bit-identical to the oracle's extraction from the float32 pre-activations of the same
-    main loop (sfl_up_projection), for W_up and for W_up^T."""
+    main loop (sfl_up_projection), for W_up and for W_up^T, with the tiles dealt in the
+    XCD-grouped order and along a Hilbert curve (32 x 64 tiles: two 32 x 32 squares; the
+    ragged grid falls back to the grouped order)."""
+    monkeypatch.setenv("SFL_GEMM_TILE_ORDER", order)
     w = wl.make_ffn("multi-tile", "bf16", T, 512, f, seed=T + Tn, sparsity=0.99, tile_cols=Tn, tile_slots=32,
                     ell_width=256)
     r = np.random.default_rng(T)
@@ -613,3 +617,58 @@ def test_token_group_walk_short_rows(T, K):
         assert (host_bits(Y)[zero] == 0).all()
     sparse = np.nonzero(~ovf)[0]
     assert len(sparse) > 0 and rel_l2(to_f64(Y)[sparse], Yref[sparse]) <= 2e-2
+
+
+@pytest.mark.parametrize("T,d,f,splits", [(700, 1024, 4096, (1, 2)), (300, 4096, 2048, (1, 2, 4, 8))])
+def test_rowwise_down_projection_variant(T, d, f, splits):
+    """The paper-shaped down projection (one wave per token and segment of d) on the ELL rows
+    the forward saved: sparse rows equal the oracle, and the forward's own Y to summation order;
+    dense-backup rows are left untouched."""
+    w = wl.make_ffn("rowwise", "bf16", T, d, f, seed=T + d, sparsity=0.99, ell_width=64)
+    w.shift_t[::50] = 10.0  # dense-backup rows
+    Y, bufs, stats, cfg = run_forward(w)
+    got = twell_views(bufs, T, f, cfg)
+    ovf = got["row_ovf"].astype(bool)
+    assert ovf.sum() >= T // 50
+    sparse = np.nonzero(~ovf)[0]
+    Yref, _ = oracle_rows(w, sparse)
+    for split in splits:
+        Y2 = torch.full_like(Y, float("nan"))
+        args = b.ffn_args(dev(w.X), dev(w.W_up), dev(w.W_down), cfg, Y=Y2, bufs=bufs)
+        b.sfl_down_projection_rowwise(args, split)
+        torch.cuda.synchronize()
+        Yg = to_f64(Y2)
+        assert np.isnan(Yg[ovf]).all()
+        for i, t in enumerate(sparse):
+            assert rel_l2(Yg[t], Yref[i]) <= 2e-2, (split, t)
+        assert rel_l2(Yg[sparse], to_f64(Y)[sparse]) <= 1e-2
+    args = b.ffn_args(dev(w.X), dev(w.W_up), dev(w.W_down), cfg, Y=Y, bufs=bufs)
+    with pytest.raises(b.SflError) as e:
+        b.sfl_down_projection_rowwise(args, 3)
+    assert e.value.code == b.SFL_E_UNSUPPORTED
+
+
+@pytest.mark.parametrize("T,gated,K", [(1500, False, 64), (700, False, 96), (32, True, 128), (600, True, 96)])
+def test_descending_nnz_token_order_gives_identical_results(T, gated, K, monkeypatch):
+    """SFL_TOKEN_ORDER=nnz deals the sparse down projection's (and the gated up-dots') tokens
+    by descending row count (the default for batches of >= 1024 tokens with K <= 256),
+    SFL_TOKEN_ORDER=token in token order: the outputs are bit-identical (every token
+    is handled exactly once, by the same arithmetic), with dense-backup rows and rows of
+    widely varying length (token-group walk at 1500 tokens, per-token walk below 1024)."""
+    r = np.random.default_rng(T)
+    sp = np.where(r.random(T) < 0.5, 0.995, 0.98)
+    w = wl.make_ffn("order", "bf16", T, 512, 2048, seed=T + K, gated=gated, sparsity_rows=sp, ell_width=K)
+    w.shift_t[::37] = 10.0  # dense-backup rows
+    monkeypatch.setenv("SFL_TOKEN_ORDER", "token")
+    Y1, b1, _, cfg = run_forward(w, packed_down=True)
+    monkeypatch.setenv("SFL_TOKEN_ORDER", "nnz")
+    Y2, b2, _, _ = run_forward(w, packed_down=True)
+    assert torch.equal(Y1.view(torch.int16), Y2.view(torch.int16))
+    monkeypatch.delenv("SFL_TOKEN_ORDER")  # the default (by batch size and ELL width)
+    Y3, _, _, _ = run_forward(w, packed_down=True)
+    assert torch.equal(Y1.view(torch.int16), Y3.view(torch.int16))
+    got = twell_views(b2, T, w.f, cfg)
+    assert got["n_ovf"] >= T // 37
+    rows = sample_rows(T, 48, 4, extra=np.nonzero(got["row_ovf"])[0][:4])
+    Yref, _ = oracle_rows(w, rows)
+    assert rel_l2(to_f64(Y2)[rows], Yref) <= 2e-2
