@@ -180,3 +180,51 @@ def classify(tw: TwELL, ell_width) -> Hybrid:
             ell_val[t, pos:pos + c] = tw.val[t, j * S:j * S + c]
             pos += c
     return Hybrid(row_nnz, is_ovf, ovf_rows, int(tile_over.sum()), ell_cnt, ell_idx, ell_val)
+
+
+# ---- packed 32-bit TwELL (the paper's single-load inference format) ----------------------
+# Appendix A's inference kernels keep each (row, tile) as one run of 32-bit words: the count
+# in word 0, then one word per stored entry holding the column index and the value, so a
+# tile's slots are one contiguous 128-byte load and 31 slots are usable. Here: 32 words per
+# (row, tile); word 0 = the true count (may exceed 31); word 1 + s (s < min(count, 31)) =
+# global column index in the low 16 bits | bf16 value bits in the high 16 bits. Words past
+# the stored entries are unspecified (this oracle leaves them 0).
+PACK32_WORDS = 32
+PACK32_SLOTS = PACK32_WORDS - 1
+
+
+def pack32(tw: TwELL) -> np.ndarray:
+    """uint32 [T, N_T * 32] from a bf16 TwELL extracted with tile_slots = 31."""
+    if tw.tile_slots != PACK32_SLOTS or tw.val_dtype != "bf16":
+        raise ValueError("packed-32 TwELL holds 31 bf16 slots per tile")
+    T, NT = tw.cnt.shape
+    words = np.zeros((T, NT * PACK32_WORDS), dtype=np.uint32)
+    for j in range(NT):
+        base = j * PACK32_WORDS
+        words[:, base] = tw.cnt[:, j].astype(np.int64).astype(np.uint32)
+        n_valid = np.minimum(tw.cnt[:, j], PACK32_SLOTS)
+        for s in range(PACK32_SLOTS):
+            rows = np.nonzero(n_valid > s)[0]
+            col = tw.idx[rows, j * PACK32_SLOTS + s].astype(np.uint32)
+            val = tw.val[rows, j * PACK32_SLOTS + s].astype(np.uint32)
+            words[rows, base + 1 + s] = col | (val << np.uint32(16))
+    return words
+
+
+def unpack32(words, tile_cols) -> TwELL:
+    """The TwELL (31 bf16 slots per tile) that a packed-32 array encodes."""
+    words = np.asarray(words, dtype=np.uint32)
+    T = words.shape[0]
+    NT = words.shape[1] // PACK32_WORDS
+    S = PACK32_SLOTS
+    cnt = words[:, ::PACK32_WORDS].astype(np.int64).astype(np.int32)
+    idx = np.zeros((T, NT * S), dtype=np.uint16)
+    val = np.zeros((T, NT * S), dtype=np.uint16)
+    for j in range(NT):
+        n_valid = np.minimum(cnt[:, j], S)
+        for s in range(S):
+            rows = np.nonzero(n_valid > s)[0]
+            w = words[rows, j * PACK32_WORDS + 1 + s]
+            idx[rows, j * S + s] = (w & np.uint32(0xFFFF)).astype(np.uint16)
+            val[rows, j * S + s] = (w >> np.uint32(16)).astype(np.uint16)
+    return TwELL(val, idx, cnt, tile_cols, S, "bf16")

@@ -113,3 +113,38 @@ def test_row_ell_is_tiles_concatenated_in_order():
         cols = np.nonzero(Z[t] > 0)[0]
         np.testing.assert_array_equal(hy.ell_idx[t, :len(cols)], cols)
         assert hy.ell_cnt[t] == len(cols)
+
+
+def test_pack32_hand_worked_words():
+    """One tile of 40 columns: columns 1 (1.0 -> bf16 0x3F80) and 38 (-0.5 inactive) and
+    39 (0.5 -> 0x3F00) give count 2, then 0x3F80_0001 and 0x3F00_0027; a second row with
+    33 active columns keeps its true count 33 and only its first 31 entries."""
+    Z = np.zeros((2, 40), dtype=np.float32)
+    Z[0, 1], Z[0, 38], Z[0, 39] = 1.0, -0.5, 0.5
+    Z[1, :33] = 2.0  # bf16 0x4000
+    tw = twell.extract_twell_loops(Z, 40, 31, "bf16")
+    w = twell.pack32(tw)
+    assert w.shape == (2, 32)
+    assert w[0, 0] == 2 and w[0, 1] == 0x3F800001 and w[0, 2] == 0x3F000027
+    assert w[1, 0] == 33
+    np.testing.assert_array_equal(w[1, 1:32], [0x40000000 | c for c in range(31)])
+
+
+def test_pack32_round_trip_and_multi_tile():
+    """unpack32(pack32(tw)) gives back the counts and every stored slot, over ragged tiles
+    and rows whose tiles overflow."""
+    r = np.random.default_rng(12)
+    Z = r.standard_normal((9, 700)).astype(np.float32)
+    Z[2, :300] = 1.0  # tiles over 31 slots
+    tw = twell.extract_twell(Z, 256, 31, "bf16")
+    back = twell.unpack32(twell.pack32(tw), 256)
+    np.testing.assert_array_equal(back.cnt, tw.cnt)
+    S = 31
+    for j in range(tw.n_tiles):
+        nv = np.minimum(tw.cnt[:, j], S)
+        for s in range(S):
+            rows = np.nonzero(nv > s)[0]
+            np.testing.assert_array_equal(back.idx[rows, j * S + s], tw.idx[rows, j * S + s])
+            np.testing.assert_array_equal(back.val[rows, j * S + s], tw.val[rows, j * S + s])
+    with pytest.raises(ValueError):
+        twell.pack32(twell.extract_twell(Z, 256, 32, "bf16"))
