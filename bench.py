@@ -610,6 +610,16 @@ def main():
             others.append(r)
             del s2
         out["other_workloads"] = others
+        # TwELL storage: the packed 32-bit words (Appendix A's inference format) against the
+        # planes with the same 31 slots, at the headline workload
+        lay = {}
+        for name, layout in (("planes_s31", 0), ("packed32", 1)):
+            wp = wl.c4_sweep(0.99, T=a.tokens, tile_slots=31)
+            wp.cfg["layout"] = layout
+            r, s2, _ = B.forward_record(wp, dense=False)
+            lay[name] = {"ms": r["ms"], "stages_ms": r["stages_ms"]}
+            del s2
+        out["twell_layout_ab"] = lay
         # the paper's row-wise down kernel against the slice walk at the headline workload
         out["down_projection_ab"] = B.splitd_record(wl.c4_sweep(0.99, T=a.tokens))
         # one GPU's share of the headline layer run on eight GPUs: hidden units split eight

@@ -63,27 +63,43 @@ typedef enum {
   SFL_E_HIP = -4           /* a HIP runtime call or kernel launch failed */
 } sfl_status_t;
 
+/* Storage of the TwELL slabs (sfl_twell_cfg_t.layout). */
+typedef enum {
+  SFL_TWELL_PLANES = 0,   /* separate value, index and count planes (all S slots usable) */
+  SFL_TWELL_PACKED32 = 1  /* the paper's single-load inference format: per (row, tile) 32
+                             words of 32 bits, the count in word 0 and 31 slots of
+                             column | bf16 value << 16 (bf16 only, S = 31) */
+} sfl_twell_layout_t;
+
 /* TwELL / hybrid parameters (Sec. 3.2 and 3.4 of the paper).
  *  tile_rows    T_m: row tile of the producing GEMM. The TwELL layout does not
  *               depend on it (rows are independent); 0 or a power of two <= 256.
  *  tile_cols    T_n: width of the horizontal column tiles (>= 1).
- *  tile_slots   S = T_n / C: stored slots per (row, tile), 1 <= S <= T_n.
+ *  tile_slots   S = T_n / C: stored slots per (row, tile), 1 <= S <= T_n; 31 with
+ *               the packed layout.
  *  ell_width    K: hybrid ELL row width (the paper's N_nz-hat), >= 0.
- *  ovf_capacity rows of the dense backup (the paper's M^d); 0 means T. */
+ *  ovf_capacity rows of the dense backup (the paper's M^d); 0 means T.
+ *  layout       sfl_twell_layout_t (Appendix A's packed format is an option; the
+ *               planes are the default). */
 typedef struct {
   int32_t tile_rows;
   int32_t tile_cols;
   int32_t tile_slots;
   int32_t ell_width;
   int32_t ovf_capacity;
+  int32_t layout;
 } sfl_twell_cfg_t;
 
 /* Packed activations: TwELL (Alg. 1 outputs) plus the hybrid format (Sec. 3.4).
  * With N_T = ceil(f / T_n), all row-major (with T = 0 every buffer but n_ovf has
  * zero size and may be NULL):
  *  val       [T][N_T*S] activation dtype: val[t][j*S+s] = s-th active value of tile j
- *  idx       [T][N_T*S] uint16 global column of that value (f <= 65535)
- *  cnt       [T][N_T]   int32 true count of active columns in tile j (may exceed S)
+ *            (packed layout: [T][N_T][32] uint32 words: word 0 the true count of tile j,
+ *            word 1 + s = column | bf16 value << 16 of its s-th active entry)
+ *  idx       [T][N_T*S] uint16 global column of that value (f <= 65535); unused (size 0,
+ *            may be NULL) with the packed layout
+ *  cnt       [T][N_T]   int32 true count of active columns in tile j (may exceed S);
+ *            unused (size 0, may be NULL) with the packed layout
  *  row_nnz   [T]        int32 true count of active columns in row t
  *  row_ovf   [T]        uint8 1 iff row t is a dense-backup row (row_nnz > K or
  *                       some cnt > S), the paper's h_b
@@ -363,7 +379,7 @@ sfl_status_t sfl_pack_down_weights(const void* W_down, void* out, int64_t f, int
  * caller-owned; a unit is dead for step s when last_active[n] < s after the step's last
  * batch. Reads tw->cnt, tw->idx, tw->n_ovf, tw->ovf_dense; T = 0 does nothing.
  * Errors: SFL_E_ARG for a NULL last_active, cnt or idx (T > 0), an ovf_dense without
- * n_ovf, or an invalid cfg. */
+ * n_ovf, or an invalid cfg; SFL_E_UNSUPPORTED for the packed layout. */
 sfl_status_t sfl_track_active_units(const sfl_twell_t* tw, int64_t T, int64_t f, sfl_dtype_t val_dtype,
                                     const sfl_twell_cfg_t* cfg, int64_t step, int64_t* last_active,
                                     sfl_stream_t stream);

@@ -41,7 +41,10 @@ class SflError(RuntimeError):
 
 class Cfg(Structure):
     _fields_ = [("tile_rows", c_int32), ("tile_cols", c_int32), ("tile_slots", c_int32),
-                ("ell_width", c_int32), ("ovf_capacity", c_int32)]
+                ("ell_width", c_int32), ("ovf_capacity", c_int32), ("layout", c_int32)]
+
+
+SFL_TWELL_PLANES, SFL_TWELL_PACKED32 = 0, 1
 
 
 class Twell(Structure):
@@ -125,8 +128,8 @@ def dtype_code(dtype):
     raise ValueError(dtype)
 
 
-def make_cfg(tile_cols=256, tile_slots=32, ell_width=128, ovf_capacity=0, tile_rows=0, **_):
-    return Cfg(tile_rows, tile_cols, tile_slots, ell_width, ovf_capacity)
+def make_cfg(tile_cols=256, tile_slots=32, ell_width=128, ovf_capacity=0, tile_rows=0, layout=0, **_):
+    return Cfg(tile_rows, tile_cols, tile_slots, ell_width, ovf_capacity, layout)
 
 
 def sfl_version():
@@ -148,14 +151,16 @@ def alloc_twell(T, f, dtype, cfg, device="cuda", with_ell=True, with_dense=True)
     sizes = sfl_twell_buffer_sizes(T, f, dtype, cfg)
     act = torch.bfloat16 if dtype_code(dtype) == SFL_BF16 else torch.float32
     es = 2 if act == torch.bfloat16 else 4
-    kinds = {"val": act, "idx": torch.int16, "cnt": torch.int32, "row_nnz": torch.int32,
+    packed = cfg.layout == SFL_TWELL_PACKED32
+    kinds = {"val": torch.int32 if packed else act, "idx": torch.int16, "cnt": torch.int32, "row_nnz": torch.int32,
              "row_ovf": torch.uint8, "ovf_rows": torch.int32, "n_ovf": torch.int32,
              "ell_val": act, "ell_idx": torch.int16, "ovf_dense": act}
-    item = {"val": es, "idx": 2, "cnt": 4, "row_nnz": 4, "row_ovf": 1, "ovf_rows": 4, "n_ovf": 4,
+    item = {"val": 4 if packed else es, "idx": 2, "cnt": 4, "row_nnz": 4, "row_ovf": 1, "ovf_rows": 4, "n_ovf": 4,
             "ell_val": es, "ell_idx": 2, "ovf_dense": es}
     bufs = {}
     for name, nbytes in zip(BUF_NAMES, sizes):
-        if (name in ("ell_val", "ell_idx") and not with_ell) or (name == "ovf_dense" and not with_dense):
+        if (name in ("ell_val", "ell_idx") and not with_ell) or (name == "ovf_dense" and not with_dense) or \
+                (packed and name in ("idx", "cnt")):
             bufs[name] = None
             continue
         n = max(1, nbytes // item[name])

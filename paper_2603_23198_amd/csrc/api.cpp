@@ -27,9 +27,15 @@ int64_t capacity_of(const sfl_twell_cfg_t& c, int64_t T) {
   return c.ovf_capacity > 0 ? std::min<int64_t>(c.ovf_capacity, T) : T;
 }
 
+constexpr int kPack32Words = 32;  // words per (row, tile) of the packed layout: count + 31 slots
+
+bool packed_layout(const sfl_twell_cfg_t& c) { return c.layout == SFL_TWELL_PACKED32; }
+
 sfl_status_t check_cfg(const sfl_twell_cfg_t* c, int64_t f) {
   if (!c) return SFL_E_ARG;
   if (c->tile_cols < 1 || c->tile_slots < 1 || c->tile_slots > c->tile_cols) return SFL_E_ARG;
+  if (c->layout != SFL_TWELL_PLANES && c->layout != SFL_TWELL_PACKED32) return SFL_E_ARG;
+  if (packed_layout(*c) && c->tile_slots != kPack32Words - 1) return SFL_E_ARG;
   if (c->ell_width < 0 || c->ovf_capacity < 0) return SFL_E_ARG;
   if (c->tile_rows != 0 && (c->tile_rows < 0 || c->tile_rows > 256 || (c->tile_rows & (c->tile_rows - 1))))
     return SFL_E_ARG;
@@ -76,6 +82,7 @@ bool rebuild_ovf(const sfl_ffn_args_t& a) { return a.T > 256; }
 
 bool fused_twell(const sfl_ffn_args_t& a) {
   const int tn = a.cfg.tile_cols;
+  if (packed_layout(a.cfg)) return a.dtype == SFL_BF16 && tn == 256 && !small_batch(a);
   return a.dtype == SFL_BF16 && (tn == 64 || tn == 128 || tn == 256) && !small_batch(a);
 }
 
@@ -92,22 +99,24 @@ sfl_status_t check_forward(const sfl_ffn_args_t* a, bool need_output = true) {
   if (a->T > INT32_MAX || a->d > INT32_MAX) return SFL_E_UNSUPPORTED;
   if (a->dtype == SFL_BF16 && (a->d % 64 != 0 || a->f % 64 != 0)) return SFL_E_UNSUPPORTED;
   if (a->gated && a->dtype != SFL_BF16) return SFL_E_UNSUPPORTED;
+  if (packed_layout(a->cfg) && a->dtype != SFL_BF16) return SFL_E_ARG;
   if (a->gated && a->d % 512 != 0) return SFL_E_UNSUPPORTED;
   // the bf16 GEMMs address each operand with 32-bit byte offsets
   const int64_t lim = (int64_t)1 << 31;
   const int64_t es = a->dtype == SFL_BF16 ? 2 : 4;
   if (a->T * a->d * es >= lim || a->d * a->f * es >= lim || a->T * a->f * es >= lim) return SFL_E_UNSUPPORTED;
   // the fused TwELL epilogue stores its slabs with 32-bit byte offsets
-  if (a->dtype == SFL_BF16 && a->T * cdiv(a->f, a->cfg.tile_cols) * a->cfg.tile_slots * 2 >= lim)
-    return SFL_E_UNSUPPORTED;
+  const int64_t slab_bytes = packed_layout(a->cfg) ? kPack32Words * 4 : (int64_t)a->cfg.tile_slots * 2;
+  if (a->dtype == SFL_BF16 && a->T * cdiv(a->f, a->cfg.tile_cols) * slab_bytes >= lim) return SFL_E_UNSUPPORTED;
   return SFL_OK;
 }
 
 // With T == 0 every buffer but the count has zero size and may be NULL.
-sfl_status_t check_twell(const sfl_twell_t& t, bool need_ell, int64_t T) {
+sfl_status_t check_twell(const sfl_twell_t& t, bool need_ell, int64_t T, bool packed = false) {
   if (!t.n_ovf) return SFL_E_ARG;
   if (T == 0) return SFL_OK;
-  if (!t.val || !t.idx || !t.cnt || !t.row_nnz || !t.row_ovf || !t.ovf_rows) return SFL_E_ARG;
+  if (!t.val || !t.row_nnz || !t.row_ovf || !t.ovf_rows) return SFL_E_ARG;
+  if (!packed && (!t.idx || !t.cnt)) return SFL_E_ARG;
   if (need_ell && (!t.ell_val || !t.ell_idx)) return SFL_E_ARG;
   return SFL_OK;
 }
@@ -313,9 +322,16 @@ sfl_status_t sfl_twell_buffer_sizes(int64_t T, int64_t f, sfl_dtype_t val_dtype,
   const int64_t S = cfg->tile_slots, K = cfg->ell_width;
   const int64_t cap = capacity_of(*cfg, T);
   const size_t es = elem_size(val_dtype);
-  bytes[SFL_BUF_VAL] = (size_t)(T * NT * S) * es;
-  bytes[SFL_BUF_IDX] = (size_t)(T * NT * S) * 2;
-  bytes[SFL_BUF_CNT] = (size_t)(T * NT) * 4;
+  if (packed_layout(*cfg)) {
+    if (val_dtype != SFL_BF16) return SFL_E_ARG;
+    bytes[SFL_BUF_VAL] = (size_t)(T * NT * kPack32Words) * 4;
+    bytes[SFL_BUF_IDX] = 0;
+    bytes[SFL_BUF_CNT] = 0;
+  } else {
+    bytes[SFL_BUF_VAL] = (size_t)(T * NT * S) * es;
+    bytes[SFL_BUF_IDX] = (size_t)(T * NT * S) * 2;
+    bytes[SFL_BUF_CNT] = (size_t)(T * NT) * 4;
+  }
   bytes[SFL_BUF_ROW_NNZ] = (size_t)T * 4;
   bytes[SFL_BUF_ROW_OVF] = (size_t)T;
   bytes[SFL_BUF_OVF_ROWS] = (size_t)cap * 4;
@@ -332,16 +348,18 @@ sfl_status_t sfl_pack_twell(const float* Z, int64_t T, int64_t f, sfl_dtype_t va
   sfl_status_t st = check_cfg(cfg, f);
   if (st != SFL_OK) return st;
   if (T > 0 && !Z) return SFL_E_ARG;
-  st = check_twell(*out, false, T);
+  const bool pk = packed_layout(*cfg);
+  if (pk && val_dtype != SFL_BF16) return SFL_E_ARG;
+  st = check_twell(*out, false, T, pk);
   if (st != SFL_OK) return st;
   if ((out->ell_val == nullptr) != (out->ell_idx == nullptr)) return SFL_E_ARG;
   hipStream_t s = (hipStream_t)stream;
   const int vb = val_dtype == SFL_BF16;
   const int64_t cap = capacity_of(*cfg, T);
   SFL_HIP(launch_stats_init(stats, s));
-  SFL_HIP(launch_pack_twell(Z, T, f, vb, cfg->tile_cols, cfg->tile_slots, out->val, out->idx, out->cnt, s));
+  SFL_HIP(launch_pack_twell(Z, T, f, vb, cfg->tile_cols, cfg->tile_slots, out->val, out->idx, out->cnt, s, pk));
   SFL_HIP(launch_classify(T, f, vb, cfg->tile_cols, cfg->tile_slots, cfg->ell_width, out->val, out->idx, out->cnt,
-                          out->row_nnz, out->row_ovf, out->ell_val, out->ell_idx, stats, s));
+                          out->row_nnz, out->row_ovf, out->ell_val, out->ell_idx, stats, s, 1, pk));
   SFL_HIP(launch_ovf_list(T, (int32_t)cap, out->row_ovf, out->ovf_rows, out->n_ovf, stats, s));
   return SFL_OK;
 }
@@ -405,7 +423,7 @@ sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* a, sfl_stream_t stream) {
 sfl_status_t sfl_ffn_forward_noalloc(const sfl_ffn_args_t* a, sfl_stream_t stream) {
   sfl_status_t st = check_forward(a);
   if (st != SFL_OK) return st;
-  st = check_twell(a->twell, true, a->T);
+  st = check_twell(a->twell, true, a->T, packed_layout(a->cfg));
   if (st != SFL_OK) return st;
   if (plan_forward(*a, nullptr).bytes > kNoallocScratchBytes) return SFL_E_WORKSPACE;
   void* ws = nullptr;
@@ -421,7 +439,7 @@ namespace {
 sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hipStream_t s) {
   sfl_status_t st = check_forward(a);
   if (st != SFL_OK) return st;
-  st = check_twell(a->twell, true, a->T);
+  st = check_twell(a->twell, true, a->T, packed_layout(a->cfg));
   if (st != SFL_OK) return st;
   FwdPlan plan = plan_forward(*a, nullptr);
   if (plan.bytes > 0 && (!ws || ws_bytes < plan.bytes)) return SFL_E_WORKSPACE;
@@ -465,6 +483,7 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
       g.tile_cols = a->cfg.tile_cols;
       g.tile_slots = a->cfg.tile_slots;
       g.n_tiles = (int)cdiv(f, a->cfg.tile_cols);
+      g.tw_packed = packed_layout(a->cfg) ? 1 : 0;
       SFL_HIP(gemm_bf16(LAY_KC, blay, EPI_TWELL, g, s));
     } else {
       g.C = plan.Z;
@@ -482,10 +501,11 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
         g.no_reduce = 1;
         SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_F32, g, s));
         SFL_HIP(launch_pack_twell_parts(plan.part, ks, a->bias_f, a->shift_t, T, f, vb, a->cfg.tile_cols,
-                                        a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, s));
+                                        a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, s, packed_layout(a->cfg)));
       } else {
         SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_F32, g, s));
-        SFL_HIP(launch_pack_twell(plan.Z, T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, s));
+        SFL_HIP(launch_pack_twell(plan.Z, T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, s,
+                                  packed_layout(a->cfg)));
       }
     }
   }
@@ -494,7 +514,8 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
   // the stored values are h itself only in the non-gated layer (the gated layer's are the
   // gate values; its sum of |h| is taken where h is formed)
   SFL_HIP(launch_classify(T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, a->cfg.ell_width, tw.val, tw.idx, tw.cnt,
-                          tw.row_nnz, tw.row_ovf, tw.ell_val, tw.ell_idx, a->stats, s, a->gated ? 0 : 1));
+                          tw.row_nnz, tw.row_ovf, tw.ell_val, tw.ell_idx, a->stats, s, a->gated ? 0 : 1,
+                          packed_layout(a->cfg)));
   SFL_HIP(launch_ovf_list(T, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s, plan.tile_sem, plan.n_sem));
   ev.record(2, s);
   // 3. sparse down projection of the ELL rows
@@ -545,7 +566,7 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
     if (rebuild)
       SFL_HIP(launch_ovf_fill(f, vb, a->cfg.tile_cols, a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, tw.ovf_rows,
                               tw.n_ovf, (int32_t)cap, ovf_dense, plan.need, plan.need_rows, plan.need_slots,
-                              plan.n_need, s));
+                              plan.n_need, s, packed_layout(a->cfg)));
     GemmParams g = gp_zero();
     g.M = (int)cap;
     g.N = (int)f;
@@ -691,6 +712,7 @@ sfl_status_t sfl_track_active_units(const sfl_twell_t* tw, int64_t T, int64_t f,
   sfl_status_t st = check_cfg(cfg, f);
   if (st != SFL_OK) return st;
   if (!last_active) return SFL_E_ARG;
+  if (packed_layout(*cfg)) return SFL_E_UNSUPPORTED;
   if (T == 0) return SFL_OK;
   if (!tw->cnt || !tw->idx || (tw->ovf_dense && !tw->n_ovf)) return SFL_E_ARG;
   const int64_t cap = capacity_of(*cfg, T);

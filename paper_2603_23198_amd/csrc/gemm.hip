@@ -307,8 +307,9 @@ __device__ __forceinline__ void twell_z_lds(const GemmParams& p, typename WaveTi
   }
 }
 
-// The compaction pass over z; cnt_lds holds WN_ x BM ints of block scratch.
-template <int WM_, int WN_, int FM, int Tn>
+// The compaction pass over z; cnt_lds holds WN_ x BM ints of block scratch. PK: the packed
+// 32-bit layout (per (row, tile) 32 words: the count in word 0, then column | bf16 << 16).
+template <int WM_, int WN_, int FM, int Tn, bool PK = false>
 __device__ __forceinline__ void twell_compact(const GemmParams& p, typename WaveTile<WM_, WN_, FM>::Acc& acc,
                                               int wm, int wn, int m0, int n0, int m_eff, int* cnt_lds) {
   static_assert(Tn == 64 || Tn == 128 || Tn == 256, "TwELL tile width");
@@ -324,8 +325,10 @@ __device__ __forceinline__ void twell_compact(const GemmParams& p, typename Wave
   const int gsh = lane & ~(G::GL - 1);               // the group's first lane
   const uint32_t gbits = G::GL == 32 ? ~0u : (1u << G::GL) - 1u;
   const uint32_t below = (1u << (lane & (G::GL - 1))) - 1u;
-  const __amdgpu_buffer_rsrc_t rv = make_rsrc(p.tw_val, (int64_t)m_eff * NT * S * 2);
-  const __amdgpu_buffer_rsrc_t ri = make_rsrc(p.tw_idx, (int64_t)m_eff * NT * S * 2);
+  // planes: 2-byte value and index stores at (row NT + tile) S + slot; packed: one 4-byte
+  // store per entry at word (row NT + tile) 32 + 1 + slot
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(p.tw_val, (int64_t)m_eff * NT * (PK ? 128 : S * 2));
+  const __amdgpu_buffer_rsrc_t ri = make_rsrc(PK ? p.tw_val : p.tw_idx, (int64_t)m_eff * NT * (PK ? 128 : S * 2));
   if constexpr (spans) {
     if (turn < wpt - 1) {
 #pragma unroll
@@ -356,7 +359,7 @@ __device__ __forceinline__ void twell_compact(const GemmParams& p, typename Wave
       const int lrow = wm * W::WTM_ + i * FM + G::row(r, lane);
       const int grow = m0 + lrow;
       const bool rok = grow < m_eff;
-      const uint32_t rowoff = rok ? (uint32_t)grow * (uint32_t)(NT * S * 2) : kOOB;
+      const uint32_t rowoff = rok ? (uint32_t)grow * (uint32_t)(NT * (PK ? 128 : S * 2)) : kOOB;
       int run = 0;
       if constexpr (spans)
         for (int w = wn - turn; w < wn; ++w) run += cnt_lds[w * BM + lrow];
@@ -370,13 +373,23 @@ __device__ __forceinline__ void twell_compact(const GemmParams& p, typename Wave
         if (b) {
           const uint32_t x = (uint32_t)(b >> gsh) & gbits;
           const int slot = run + __popc(x & below);
-          const uint32_t off = (act && slot < S) ? rowoff + (uint32_t)(jt * S + slot) * 2u : kOOB;
-          __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_finite(z), rv, off, 0, 0);
-          __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(wcol0 + j * FM + G::col(lane)), ri, off, 0, 0);
+          const uint16_t col = (uint16_t)(wcol0 + j * FM + G::col(lane));
+          if constexpr (PK) {
+            const uint32_t off = (act && slot < S) ? rowoff + (uint32_t)(jt * 32 + 1 + slot) * 4u : kOOB;
+            __builtin_amdgcn_raw_buffer_store_b32((uint32_t)col | ((uint32_t)f32_to_bf16_finite(z) << 16), rv, off, 0,
+                                                  0);
+          } else {
+            const uint32_t off = (act && slot < S) ? rowoff + (uint32_t)(jt * S + slot) * 2u : kOOB;
+            __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_finite(z), rv, off, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b16(col, ri, off, 0, 0);
+          }
           run += __popc(x);
         }
         const bool tend = spans ? (turn == wpt - 1 && j == W::TN_ - 1) : ((j * FM + FM) % Tn == 0);
-        if (tend && (lane % G::GL) == 0 && rok && jt * Tn < p.N) p.tw_cnt[(int64_t)grow * NT + jt] = run;
+        if (tend && (lane % G::GL) == 0 && rok && jt * Tn < p.N) {
+          if constexpr (PK) ((uint32_t*)p.tw_val)[((int64_t)grow * NT + jt) * 32] = (uint32_t)run;
+          else p.tw_cnt[(int64_t)grow * NT + jt] = run;
+        }
       }
     }
 }
@@ -806,8 +819,9 @@ __global__ __launch_bounds__(NTHR) void k_gemm_kc(GemmParams p) {
   KcOps<BL> op(p);
   op.setup(p, tm * BM, tn * BN, m_eff);
   if (nk > 0) op.issue(p, smem, 0);
+  constexpr bool TW = EPI == EPI_TWELL || EPI == EPI_TWELL_P32;
   KcTwPre pre;
-  if constexpr (EPI == EPI_TWELL) pre.load(p, op.wm, op.wn, op.lane, tm * BM, tn * BN, m_eff);
+  if constexpr (TW) pre.load(p, op.wm, op.wn, op.lane, tm * BM, tn * BN, m_eff);
   int b0 = 0;  // stage buffer of the tile's first k step
   for (;;) {
     typename W::Acc acc;
@@ -817,20 +831,21 @@ __global__ __launch_bounds__(NTHR) void k_gemm_kc(GemmParams p) {
     int tm2 = 0, tn2 = 0;
     const int v2 = next_live(v + gridDim.x, tm2, tn2);
     KcTwPre pre2;
-    if constexpr (EPI == EPI_TWELL) pre.settle();
+    if constexpr (TW) pre.settle();
     if (v2 < nt) {
       // before the stage issue, so that no wait of the compiler's (a gathered shift row)
       // waits for the stage; the other buffer was last read in step nk-2, which every wave
       // finished before the barrier of step nk-1
-      if constexpr (EPI == EPI_TWELL) pre2.load(p, op.wm, op.wn, op.lane, tm2 * BM, tn2 * BN, m_eff);
+      if constexpr (TW) pre2.load(p, op.wm, op.wn, op.lane, tm2 * BM, tn2 * BN, m_eff);
       op.setup(p, tm2 * BM, tn2 * BN, m_eff);
       if (nk > 0) op.issue(p, smem + (bl ^ 1) * KC_STAGE, 0);
     }
     __syncthreads();  // every wave is done reading buffer bl
     bf16_t* scratch = smem + bl * KC_STAGE;
-    if constexpr (EPI == EPI_TWELL) {
+    if constexpr (EPI == EPI_TWELL || EPI == EPI_TWELL_P32) {
       pre.apply(acc, op.lane);
-      twell_compact<KC_WM, KC_WN, KC_FM, Tn>(p, acc, op.wm, op.wn, m0, n0, m_eff, (int*)scratch);
+      twell_compact<KC_WM, KC_WN, KC_FM, Tn, EPI == EPI_TWELL_P32>(p, acc, op.wm, op.wn, m0, n0, m_eff,
+                                                                    (int*)scratch);
     } else {
       gemm_epilogue<EPI, KC_WM, KC_WN, KC_FM, Tn>(p, acc, op.wm, op.wn, m0, n0, m_eff, scratch);
     }
@@ -841,7 +856,7 @@ __global__ __launch_bounds__(NTHR) void k_gemm_kc(GemmParams p) {
     tm = tm2;
     tn = tn2;
     b0 = bl ^ 1;
-    if constexpr (EPI == EPI_TWELL) pre = pre2;
+    if constexpr (TW) pre = pre2;
   }
 }
 
@@ -1110,6 +1125,10 @@ template <int ALAY, int BLAY>
 hipError_t launch_twell(const GemmParams& p, hipStream_t s) {
   const bool kc = ALAY == LAY_KC && kc_ok(p, BLAY);
   constexpr int BL = BLAY == LAY_RC ? LAY_RC : LAY_KC;
+  if (p.tw_packed) {  // the packed layout: 256-column tiles of 31 slots, direct-to-LDS kernel only
+    if (!kc || p.tile_cols != 256 || p.tile_slots != 31) return hipErrorInvalidValue;
+    return launch_kc<EPI_TWELL_P32, 256, BL>(p, s);
+  }
   switch (p.tile_cols) {
     case 64: return kc ? launch_kc<EPI_TWELL, 64, BL>(p, s) : launch_bf16<ALAY, BLAY, EPI_TWELL, 64>(p, s);
     case 128: return kc ? launch_kc<EPI_TWELL, 128, BL>(p, s) : launch_bf16<ALAY, BLAY, EPI_TWELL, 128>(p, s);

@@ -23,6 +23,7 @@ enum Epilogue {
   EPI_MASKGRAD = 4,    // C_act[crow][n] = mask[row][n] > 0 ? acc + lam : 0
   EPI_ACCUM_F32 = 5,   // C_f32[crow][n] += acc
   EPI_MUL_ACT = 6,     // C_act[crow][n] = C_act[crow][n] * acc (gated h = ReLU(g) * u)
+  EPI_TWELL_P32 = 7,   // EPI_TWELL into the packed 32-bit layout (tw_val words; S = 31)
 };
 
 // Persistent tile orders of the 256 x 256 GEMMs.
@@ -56,6 +57,7 @@ struct GemmParams {
   uint16_t* tw_idx;
   int32_t* tw_cnt;
   int tile_cols, tile_slots, n_tiles;
+  int tw_packed;           // packed 32-bit layout: tw_val holds [rows][n_tiles][32] words
   // split-K (K-contiguous kernel only; for skinny GEMMs such as the dense-backup rows):
   // up to `ksplit` K ranges per output tile, chosen on the device from the row count so
   // that ks * rows <= part_rows; fp32 partial sums go to part [ks][rows][N] and a second
@@ -85,14 +87,16 @@ int gemm_split_count(int alay, int blay, const GemmParams& p);
 hipError_t gemm_f32(int epi, const GemmParams& p, hipStream_t s);
 
 // ----------------------------------------------------------- TwELL ----
+// packed: the packed 32-bit layout (val holds the words; idx and cnt unused; bf16, S = 31).
 hipError_t launch_pack_twell(const float* Z, int64_t T, int64_t f, int val_bf16, int tile_cols,
-                             int tile_slots, void* val, uint16_t* idx, int32_t* cnt, hipStream_t s);
+                             int tile_slots, void* val, uint16_t* idx, int32_t* cnt, hipStream_t s,
+                             bool packed = false);
 // The same from split-K partial sums: z[t][n] = ((sum over s < ks of part[s][t][n], in
 // split order) + bias[n]) + shift[t], the arithmetic of the split-K reduction's fp32
 // epilogue (bias and shift optional).
 hipError_t launch_pack_twell_parts(const float* part, int ks, const float* bias, const float* shift, int64_t T,
                                    int64_t f, int val_bf16, int tile_cols, int tile_slots, void* val, uint16_t* idx,
-                                   int32_t* cnt, hipStream_t s);
+                                   int32_t* cnt, hipStream_t s, bool packed = false);
 // Hybrid classification: row_nnz, row_ovf, optional ELL rows and stats partials; with
 // l1_vals the stored values of the sparse rows are added to stats->l1_sum (they are the
 // activations h of the non-gated layer; the gated layer's are gate values, and its L1 sum
@@ -100,7 +104,7 @@ hipError_t launch_pack_twell_parts(const float* part, int ks, const float* bias,
 hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int tile_cols, int tile_slots,
                            int ell_width, const void* val, const uint16_t* idx, const int32_t* cnt,
                            int32_t* row_nnz, uint8_t* row_ovf, void* ell_val, uint16_t* ell_idx,
-                           sfl_stats_t* stats, hipStream_t s, int l1_vals = 1);
+                           sfl_stats_t* stats, hipStream_t s, int l1_vals = 1, bool packed = false);
 // Ascending dense-backup row list + n_ovf + capacity flag (one workgroup).
 hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32_t* ovf_rows,
                            int32_t* n_ovf, sfl_stats_t* stats, hipStream_t s,
@@ -117,7 +121,7 @@ hipError_t launch_nnz_order(int64_t T, int K, const int32_t* row_nnz, const uint
 hipError_t launch_ovf_fill(int64_t f, int val_bf16, int Tn, int S, const void* val, const uint16_t* idx,
                            const int32_t* cnt, const int32_t* ovf_rows, const int32_t* n_ovf, int32_t cap,
                            void* dense, uint8_t* need, int32_t* need_rows, int32_t* need_slots, int32_t* n_need,
-                           hipStream_t s);
+                           hipStream_t s, bool packed = false);
 // Sum (absval: of the absolute values) of the computed dense-backup rows, added into
 // stats->l1_sum.
 hipError_t launch_ovf_l1(int64_t f, int val_bf16, const void* ovf_dense, const int32_t* n_ovf,

@@ -24,7 +24,10 @@ __device__ __forceinline__ bool is_active(float z) {
 // slot (running count + active lanes below it), so slots follow ascending column order.
 // With ks > 0, z comes from ks split-K partial sums part[s][t][n] (Z is then the partial
 // array, ks * T * f floats): their sum in split order, plus bias[n], plus shift[t].
-template <typename V>
+// Packed 32-bit layout (PK): the (row, tile) pair's 32 words hold its true count in word 0
+// and, in word 1 + s, the s-th active entry as column | bf16 value << 16 (s < 31); V is
+// bf16 then, and `val` points to the words.
+template <typename V, bool PK = false>
 __global__ __launch_bounds__(256) void k_pack_twell(const float* __restrict__ Z, int64_t T, int64_t f,
                                                     int Tn, int S, int NT, V* __restrict__ val,
                                                     uint16_t* __restrict__ idx, int32_t* __restrict__ cnt, int ks,
@@ -38,6 +41,7 @@ __global__ __launch_bounds__(256) void k_pack_twell(const float* __restrict__ Z,
   const int64_t c1 = c0 + Tn < f ? c0 + Tn : f;
   const float* zr = Z + t * f;
   const int64_t base = t * (int64_t)NT * S + (int64_t)j * S;
+  uint32_t* words = PK ? (uint32_t*)val + w * 32 : nullptr;  // w = t NT + j
   int running = 0;
   const float sh = (ks > 0 && shift) ? shift[t] : 0.f;
   for (int64_t c = c0; c < c1; c += 64) {
@@ -55,45 +59,88 @@ __global__ __launch_bounds__(256) void k_pack_twell(const float* __restrict__ Z,
     const uint64_t m = ballot(act);
     const int slot = running + mbcnt(m);
     if (act && slot < S) {
-      val[base + slot] = VT<V>::cvt(z);
-      idx[base + slot] = (uint16_t)col;
+      if constexpr (PK) {
+        words[1 + slot] = (uint32_t)col | ((uint32_t)f32_to_bf16(z) << 16);
+      } else {
+        val[base + slot] = VT<V>::cvt(z);
+        idx[base + slot] = (uint16_t)col;
+      }
     }
     running += __popcll(m);
   }
-  if (l == 0) cnt[t * NT + j] = running;
+  if (l == 0) {
+    if constexpr (PK) words[0] = (uint32_t)running;
+    else cnt[t * NT + j] = running;
+  }
 }
 
 hipError_t launch_pack_twell(const float* Z, int64_t T, int64_t f, int val_bf16, int Tn, int S,
-                             void* val, uint16_t* idx, int32_t* cnt, hipStream_t s) {
+                             void* val, uint16_t* idx, int32_t* cnt, hipStream_t s, bool packed) {
   const int NT = (int)cdiv(f, Tn);
   const int64_t waves = T * NT;
   if (waves == 0) return hipSuccess;
   const dim3 grid((unsigned)cdiv(waves, 4));
-  if (val_bf16)
+  if (packed) {
+    if (!val_bf16 || S != 31) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_pack_twell<bf16_t, true>), grid, dim3(256), 0, s, Z, T, f, Tn, S, NT, (bf16_t*)val, idx, cnt,
+                       0, (const float*)nullptr, (const float*)nullptr);
+  } else if (val_bf16) {
     hipLaunchKernelGGL(k_pack_twell<bf16_t>, grid, dim3(256), 0, s, Z, T, f, Tn, S, NT, (bf16_t*)val, idx, cnt, 0,
                        (const float*)nullptr, (const float*)nullptr);
-  else
+  } else {
     hipLaunchKernelGGL(k_pack_twell<float>, grid, dim3(256), 0, s, Z, T, f, Tn, S, NT, (float*)val, idx, cnt, 0,
                        (const float*)nullptr, (const float*)nullptr);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_pack_twell_parts(const float* part, int ks, const float* bias, const float* shift, int64_t T,
                                    int64_t f, int val_bf16, int Tn, int S, void* val, uint16_t* idx, int32_t* cnt,
-                                   hipStream_t s) {
+                                   hipStream_t s, bool packed) {
   const int NT = (int)cdiv(f, Tn);
   const int64_t waves = T * NT;
   if (waves == 0) return hipSuccess;
   if (ks < 1) return hipErrorInvalidValue;
   const dim3 grid((unsigned)cdiv(waves, 4));
-  if (val_bf16)
+  if (packed) {
+    if (!val_bf16 || S != 31) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_pack_twell<bf16_t, true>), grid, dim3(256), 0, s, part, T, f, Tn, S, NT, (bf16_t*)val, idx,
+                       cnt, ks, bias, shift);
+  } else if (val_bf16) {
     hipLaunchKernelGGL(k_pack_twell<bf16_t>, grid, dim3(256), 0, s, part, T, f, Tn, S, NT, (bf16_t*)val, idx, cnt, ks,
                        bias, shift);
-  else
+  } else {
     hipLaunchKernelGGL(k_pack_twell<float>, grid, dim3(256), 0, s, part, T, f, Tn, S, NT, (float*)val, idx, cnt, ks,
                        bias, shift);
+  }
   return hipGetLastError();
 }
+
+// Access to the TwELL slabs of row t in either layout: the count of tile j, and slot s of
+// tile j (the stored value's bits and its column).
+template <typename V, bool PK>
+struct Slabs {
+  const V* val;
+  const uint16_t* idx;
+  const int32_t* cnt;
+  int64_t t;
+  int NT, S;
+  __device__ __forceinline__ int count(int j) const {
+    if constexpr (PK) return (int)((const uint32_t*)val)[(t * NT + j) * 32];
+    else return cnt[t * NT + j];
+  }
+  __device__ __forceinline__ void slot(int j, int s, V& v, uint16_t& col) const {
+    if constexpr (PK) {
+      const uint32_t w = ((const uint32_t*)val)[(t * NT + j) * 32 + 1 + s];
+      col = (uint16_t)(w & 0xffffu);
+      v = (V)(w >> 16);
+    } else {
+      const int64_t o = t * (int64_t)NT * S + (int64_t)j * S + s;
+      v = val[o];
+      col = idx[o];
+    }
+  }
+};
 
 // One wave per row. Pass 1: the tile counts, 64 at a time, give the row total, the
 // number of overflowing tiles and (kept in LDS) the inclusive prefix of the counts.
@@ -134,7 +181,7 @@ __device__ __forceinline__ void block_stats_add(sfl_stats_t* stats, int64_t nnz,
 }
 
 constexpr int kClassifyWaves = 16;  // waves per block of k_classify
-template <typename V>
+template <typename V, bool PK>
 __global__ __launch_bounds__(kClassifyWaves * 64) void k_classify(int64_t T, int NT, int S, int K, const V* __restrict__ val,
                                                   const uint16_t* __restrict__ idx, const int32_t* __restrict__ cnt,
                                                   int32_t* __restrict__ row_nnz, uint8_t* __restrict__ row_ovf,
@@ -150,11 +197,11 @@ __global__ __launch_bounds__(kClassifyWaves * 64) void k_classify(int64_t T, int
   for (int rr = 0; rr < rpw; ++rr) {
     const int64_t t = ((int64_t)blockIdx.x * kClassifyWaves + w) * rpw + rr;
     if (t >= T) break;
-    const int32_t* crow = cnt + t * NT;
+    const Slabs<V, PK> sl{val, idx, cnt, t, NT, S};
     int total = 0;
     int tile_over = 0;
     for (int j0 = 0; j0 < NT; j0 += 64) {
-      const int c = (j0 + l < NT) ? crow[j0 + l] : 0;
+      const int c = (j0 + l < NT) ? sl.count(j0 + l) : 0;
       const int incl = wave_incl_scan(c) + total;
       if (j0 + l < NT) incl_s[j0 + l] = incl;
       total = __shfl(incl, 63, 64);
@@ -172,8 +219,6 @@ __global__ __launch_bounds__(kClassifyWaves * 64) void k_classify(int64_t T, int
     nnz_sum += total;
     over_sum += tile_over;
     if (!ovf) {
-      const V* vrow = val + t * (int64_t)NT * S;
-      const uint16_t* irow = idx + t * (int64_t)NT * S;
       for (int q0 = 0; q0 < total; q0 += 64) {
         const int q = q0 + l;
         if (q < total) {
@@ -184,12 +229,13 @@ __global__ __launch_bounds__(kClassifyWaves * 64) void k_classify(int64_t T, int
             if (incl_s[mid] > q) hi = mid; else lo = mid + 1;
           }
           const int excl = lo > 0 ? incl_s[lo - 1] : 0;
-          const int64_t src = (int64_t)lo * S + (q - excl);
-          const V v = vrow[src];
+          V v;
+          uint16_t col;
+          sl.slot(lo, q - excl, v, col);
           if (l1_vals) l1 += VT<V>::load(&v, 0);
           if (ell_val) {
             ell_val[t * (int64_t)K + q] = v;
-            ell_idx[t * (int64_t)K + q] = irow[src];
+            ell_idx[t * (int64_t)K + q] = col;
           }
         }
       }
@@ -201,7 +247,7 @@ __global__ __launch_bounds__(kClassifyWaves * 64) void k_classify(int64_t T, int
 }
 
 // Fallback for rows with more tiles than the LDS prefix holds: walks the tiles in order.
-template <typename V>
+template <typename V, bool PK>
 __global__ __launch_bounds__(256) void k_classify_wide(int64_t T, int NT, int S, int K, const V* __restrict__ val,
                                                        const uint16_t* __restrict__ idx,
                                                        const int32_t* __restrict__ cnt,
@@ -212,11 +258,11 @@ __global__ __launch_bounds__(256) void k_classify_wide(int64_t T, int NT, int S,
   const bool row_ok = t0 < T;
   const int64_t t = row_ok ? t0 : 0;
   const int l = threadIdx.x & 63;
-  const int32_t* crow = cnt + t * NT;
+  const Slabs<V, PK> sl{val, idx, cnt, t, NT, S};
   int64_t total = 0;
   int tile_over = 0;
   for (int j0 = 0; j0 < NT; j0 += 64) {
-    const int c = (row_ok && j0 + l < NT) ? crow[j0 + l] : 0;
+    const int c = (row_ok && j0 + l < NT) ? sl.count(j0 + l) : 0;
     total += wave_sum<int>(c);
     tile_over += __popcll(ballot(c > S));
   }
@@ -227,19 +273,19 @@ __global__ __launch_bounds__(256) void k_classify_wide(int64_t T, int NT, int S,
   }
   float l1 = 0.f;
   if (row_ok && !ovf) {
-    const V* vrow = val + t * (int64_t)NT * S;
-    const uint16_t* irow = idx + t * (int64_t)NT * S;
     int offset = 0;
     for (int j = 0; j < NT; ++j) {
-      const int cj = crow[j];
+      const int cj = sl.count(j);
       for (int s0 = 0; s0 < cj; s0 += 64) {
         const int sidx = s0 + l;
         if (sidx < cj) {
-          const V v = vrow[(int64_t)j * S + sidx];
+          V v;
+          uint16_t col;
+          sl.slot(j, sidx, v, col);
           if (l1_vals) l1 += VT<V>::load(&v, 0);
           if (ell_val) {
             ell_val[t * (int64_t)K + offset + sidx] = v;
-            ell_idx[t * (int64_t)K + offset + sidx] = irow[(int64_t)j * S + sidx];
+            ell_idx[t * (int64_t)K + offset + sidx] = col;
           }
         }
       }
@@ -251,29 +297,32 @@ __global__ __launch_bounds__(256) void k_classify_wide(int64_t T, int NT, int S,
 
 hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int Tn, int S, int K, const void* val,
                            const uint16_t* idx, const int32_t* cnt, int32_t* row_nnz, uint8_t* row_ovf,
-                           void* ell_val, uint16_t* ell_idx, sfl_stats_t* stats, hipStream_t s, int l1_vals) {
+                           void* ell_val, uint16_t* ell_idx, sfl_stats_t* stats, hipStream_t s, int l1_vals,
+                           bool packed) {
   if (T == 0) return hipSuccess;
+  if (packed && !val_bf16) return hipErrorInvalidValue;
   const int NT = (int)cdiv(f, Tn);
   const bool wide = NT > kClassifyMaxTiles;
   // several rows per wave amortise the per-block statistics, but the walk is latency
   // bound: keep about 4096 waves (16 per CU) in flight before packing rows
   const int rpw = (int)std::max<int64_t>(1, std::min<int64_t>(kClassifyRowsPerWave, T / 4096));
   const dim3 grid((unsigned)(wide ? cdiv(T, 4) : cdiv(T, kClassifyWaves * rpw)));
-  if (wide) {
-    if (val_bf16)
-      hipLaunchKernelGGL(k_classify_wide<bf16_t>, grid, dim3(256), 0, s, T, NT, S, K, (const bf16_t*)val, idx, cnt,
-                         row_nnz, row_ovf, (bf16_t*)ell_val, ell_idx, stats, l1_vals);
-    else
-      hipLaunchKernelGGL(k_classify_wide<float>, grid, dim3(256), 0, s, T, NT, S, K, (const float*)val, idx, cnt,
-                         row_nnz, row_ovf, (float*)ell_val, ell_idx, stats, l1_vals);
-  } else {
-    if (val_bf16)
-      hipLaunchKernelGGL(k_classify<bf16_t>, grid, dim3(kClassifyWaves * 64), 0, s, T, NT, S, K, (const bf16_t*)val,
-                         idx, cnt, row_nnz, row_ovf, (bf16_t*)ell_val, ell_idx, stats, rpw, l1_vals);
-    else
-      hipLaunchKernelGGL(k_classify<float>, grid, dim3(kClassifyWaves * 64), 0, s, T, NT, S, K, (const float*)val,
-                         idx, cnt, row_nnz, row_ovf, (float*)ell_val, ell_idx, stats, rpw, l1_vals);
-  }
+#define SFL_CLASSIFY(V_, PK_)                                                                                         \
+  do {                                                                                                               \
+    if (wide)                                                                                                        \
+      hipLaunchKernelGGL((k_classify_wide<V_, PK_>), grid, dim3(256), 0, s, T, NT, S, K, (const V_*)val, idx, cnt,    \
+                         row_nnz, row_ovf, (V_*)ell_val, ell_idx, stats, l1_vals);                                   \
+    else                                                                                                             \
+      hipLaunchKernelGGL((k_classify<V_, PK_>), grid, dim3(kClassifyWaves * 64), 0, s, T, NT, S, K, (const V_*)val,  \
+                         idx, cnt, row_nnz, row_ovf, (V_*)ell_val, ell_idx, stats, rpw, l1_vals);                    \
+  } while (0)
+  if (packed)
+    SFL_CLASSIFY(bf16_t, true);
+  else if (val_bf16)
+    SFL_CLASSIFY(bf16_t, false);
+  else
+    SFL_CLASSIFY(float, false);
+#undef SFL_CLASSIFY
   return hipGetLastError();
 }
 
@@ -452,7 +501,7 @@ hipError_t launch_ovf_l1(int64_t f, int val_bf16, const void* dense, const int32
 // i < n_ovf.
 constexpr int kFillWindowBytes = 32768;
 constexpr int kFillBlocks = 1024;
-template <typename V>
+template <typename V, bool PK>
 __global__ __launch_bounds__(256) void k_ovf_fill(int64_t f, int NT, int Tn, int S, const V* __restrict__ val,
                                                   const uint16_t* __restrict__ idx, const int32_t* __restrict__ cnt,
                                                   const int32_t* __restrict__ ovf_rows, const int32_t* __restrict__ n_ovf,
@@ -462,14 +511,12 @@ __global__ __launch_bounds__(256) void k_ovf_fill(int64_t f, int NT, int Tn, int
   const int n = min(*n_ovf, cap);
   for (int i = blockIdx.x; i < n; i += gridDim.x) {
     const int64_t t = ovf_rows[i];
-    const int32_t* crow = cnt + t * NT;
+    const Slabs<V, PK> sl{val, idx, cnt, t, NT, S};
     int over = 0;
-    for (int j = threadIdx.x; j < NT; j += 256) over |= crow[j] > S;
+    for (int j = threadIdx.x; j < NT; j += 256) over |= sl.count(j) > S;
     over = __syncthreads_or(over);
     if (threadIdx.x == 0) need[i] = over ? 1 : 0;
     if (over) continue;
-    const V* vrow = val + t * (int64_t)NT * S;
-    const uint16_t* irow = idx + t * (int64_t)NT * S;
     V* out = dense + (int64_t)i * f;
     for (int64_t c0 = 0; c0 < f; c0 += WIN) {
       const int w = (int)std::min<int64_t>(WIN, f - c0);
@@ -477,8 +524,13 @@ __global__ __launch_bounds__(256) void k_ovf_fill(int64_t f, int NT, int Tn, int
       __syncthreads();
       const int j0 = (int)(c0 / Tn), nt = (w + Tn - 1) / Tn;
       for (int q = threadIdx.x; q < nt * S; q += 256) {
-        const int j = j0 + q / S, sl = q % S;
-        if (sl < crow[j]) row_s[(int)(irow[(int64_t)j * S + sl] - c0)] = vrow[(int64_t)j * S + sl];
+        const int j = j0 + q / S, slot = q % S;
+        if (slot < sl.count(j)) {
+          V v;
+          uint16_t col;
+          sl.slot(j, slot, v, col);
+          row_s[(int)(col - c0)] = v;
+        }
       }
       __syncthreads();
       for (int x = threadIdx.x; x < w; x += 256) out[c0 + x] = row_s[x];
@@ -522,15 +574,19 @@ __global__ __launch_bounds__(1024) void k_need_list(int32_t cap, const int32_t* 
 hipError_t launch_ovf_fill(int64_t f, int val_bf16, int Tn, int S, const void* val, const uint16_t* idx,
                            const int32_t* cnt, const int32_t* ovf_rows, const int32_t* n_ovf, int32_t cap,
                            void* dense, uint8_t* need, int32_t* need_rows, int32_t* need_slots, int32_t* n_need,
-                           hipStream_t s) {
+                           hipStream_t s, bool packed) {
   if (cap == 0) return hipSuccess;
+  if (packed && !val_bf16) return hipErrorInvalidValue;
   const int NT = (int)cdiv(f, Tn);
   const dim3 grid((unsigned)std::min<int32_t>(cap, kFillBlocks));
-  if (val_bf16)
-    hipLaunchKernelGGL(k_ovf_fill<bf16_t>, grid, dim3(256), 0, s, f, NT, Tn, S, (const bf16_t*)val, idx, cnt,
+  if (packed)
+    hipLaunchKernelGGL((k_ovf_fill<bf16_t, true>), grid, dim3(256), 0, s, f, NT, Tn, S, (const bf16_t*)val, idx, cnt,
+                       ovf_rows, n_ovf, cap, (bf16_t*)dense, need);
+  else if (val_bf16)
+    hipLaunchKernelGGL((k_ovf_fill<bf16_t, false>), grid, dim3(256), 0, s, f, NT, Tn, S, (const bf16_t*)val, idx, cnt,
                        ovf_rows, n_ovf, cap, (bf16_t*)dense, need);
   else
-    hipLaunchKernelGGL(k_ovf_fill<float>, grid, dim3(256), 0, s, f, NT, Tn, S, (const float*)val, idx, cnt,
+    hipLaunchKernelGGL((k_ovf_fill<float, false>), grid, dim3(256), 0, s, f, NT, Tn, S, (const float*)val, idx, cnt,
                        ovf_rows, n_ovf, cap, (float*)dense, need);
   hipLaunchKernelGGL(k_need_list, dim3(1), dim3(1024), 0, s, cap, ovf_rows, n_ovf, need, need_rows, need_slots,
                      n_need);

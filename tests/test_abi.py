@@ -223,3 +223,30 @@ def test_unit_tracking_and_reinit_validate_before_launch():
     assert rd(8, 1, 4, 4, 0, 8, 1, 0.1, 0.02, None, None) == b.SFL_E_ARG
     assert rd(None, 1, 0, 4, 0, None, 1, 0.1, 0.02, None, None) == b.SFL_OK
     assert rd(8, 7, 4, 4, 0, 8, 1, 0.1, 0.02, 8, None) == b.SFL_E_ARG
+
+
+def test_packed_layout_sizes_and_validation():
+    """The packed 32-bit TwELL: 32 words per (row, tile), no index or count planes; only with
+    31 slots and bf16 values; the dead-unit record needs the planes."""
+    T, f = 300, 1000
+    cfg = b.make_cfg(tile_cols=256, tile_slots=31, ell_width=64, layout=b.SFL_TWELL_PACKED32)
+    s = dict(zip(b.BUF_NAMES, b.sfl_twell_buffer_sizes(T, f, "bf16", cfg)))
+    assert s["val"] == T * 4 * 32 * 4 and s["idx"] == 0 and s["cnt"] == 0
+    assert s["ell_val"] == T * 64 * 2 and s["row_nnz"] == T * 4
+    for bad in (b.make_cfg(tile_cols=256, tile_slots=32, layout=1), b.make_cfg(tile_cols=256, tile_slots=31, layout=2)):
+        with pytest.raises(b.SflError) as e:
+            b.sfl_twell_buffer_sizes(T, f, "bf16", bad)
+        assert e.value.code == b.SFL_E_ARG
+    with pytest.raises(b.SflError) as e:
+        b.sfl_twell_buffer_sizes(T, f, "f32", cfg)
+    assert e.value.code == b.SFL_E_ARG
+    tw = b.Twell(*[8] * 10)
+    assert b._lib.sfl_track_active_units(ctypes.byref(tw), 4, 1000, 1, ctypes.byref(cfg), 0, 8, None) == \
+        b.SFL_E_UNSUPPORTED
+    a = _fake_args(b.SFL_BF16, 128, 512, 1024, tile_slots=31, layout=1)
+    a.twell.val, a.twell.row_nnz, a.twell.row_ovf, a.twell.ovf_rows, a.twell.n_ovf = (0x3000,) * 5
+    a.twell.ell_val = a.twell.ell_idx = 0x3000
+    a.twell.ovf_dense = None
+    with pytest.raises(b.SflError) as e:   # index and count planes may be NULL; only the workspace is missing
+        b.sfl_ffn_forward(a, stream=0)
+    assert e.value.code == b.SFL_E_WORKSPACE
