@@ -123,6 +123,16 @@ def cpu_baseline(w, seconds):
                       f"TwELL extraction, hybrid classification, ELL gather / dense rows), {spent:.1f} s"}
 
 
+def dense_fallback_taken(b, s, w):
+    """Whether sfl_ffn_forward took its dense fallback for this workload (the library's rule:
+    a candidate by ELL width, then the sparse rows' entries against T f / 64)."""
+    if w.gated or w.dtype != "bf16" or w.T <= 256 or w.cfg["ell_width"] * 32 < w.f:
+        return False
+    nnz = s["bufs"]["row_nnz"][:w.T].cpu().numpy()
+    ovf = s["bufs"]["row_ovf"][:w.T].cpu().numpy()
+    return bool(int(nnz[ovf == 0].sum()) * 64 > w.T * w.f)
+
+
 class Bench:
     def __init__(self, b, torch, steps, warmup):
         self.b, self.torch, self.steps, self.warmup = b, torch, steps, warmup
@@ -256,10 +266,15 @@ class Bench:
         s["mk"] = lambda ev: b.ffn_args(X, Wu, Wd, cfg, **kw, workspace=ws, events=ev)
         return s
 
-    def forward_record(self, w, dense=True, stages=True, order_ab=False):
+    def forward_record(self, w, dense=True, stages=True, order_ab=False, fallback_ab=False):
         b = self.b
         s = self.setup_forward(w)
         ms = self.time(lambda: b.sfl_ffn_forward(s["args"], self.stream))
+        if fallback_ab:
+            # the same call with the dense fallback disabled (ELL gather for every sparse row)
+            os.environ["SFL_DENSE_FALLBACK"] = "off"
+            ms_off = self.time(lambda: b.sfl_ffn_forward(s["args"], self.stream))
+            os.environ.pop("SFL_DENSE_FALLBACK", None)
         if order_ab:
             # the sparse down projection's token order: descending row count / token order
             # (the default picks one of them by batch size and ELL width)
@@ -272,10 +287,13 @@ class Bench:
         st = b.read_stats(s["stats"])
         rec = {"workload": w.name, "dtype": w.dtype, "tokens": w.T, "ms": round(ms, 4),
                "tokens_per_s": round(w.T / ms * 1e3, 1),
+               "dense_fallback_taken": dense_fallback_taken(b, s, w),
                "realised_sparsity": round(1 - st["total_nnz"] / (w.T * w.f), 5), "n_ovf_rows": st["n_ovf_rows"]}
         if stages:
             rec["stages_ms"] = dict(zip(["up_gemm_twell", "classify", "sparse_down", "dense_backup"],
                                         self.stage_times(s["mk"], b.sfl_ffn_forward, 5)))
+        if fallback_ab:
+            rec["ms_dense_fallback_off"] = round(ms_off, 4)
         if order_ab:
             rec["token_order_ab"] = {
                 o: {"ms": round(float(np.mean([x[0] for x in v])), 4),
@@ -596,7 +614,7 @@ def main():
     if not a.quick:
         others = []
         for sp_ in (0.9, 0.95, 0.999):
-            r, s2, _ = B.forward_record(wl.c4_sweep(sp_, T=a.tokens), stages=True)
+            r, s2, _ = B.forward_record(wl.c4_sweep(sp_, T=a.tokens), stages=True, fallback_ab=sp_ < 0.99)
             others.append(r)
             del s2
         r, s2, _ = B.forward_record(wl.c2_lognormal(), order_ab=True)

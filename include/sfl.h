@@ -36,6 +36,15 @@
  *    otherwise; SFL_TOKEN_ORDER=nnz or SFL_TOKEN_ORDER=token forces one of the two.
  *    Results are identical either way. Both variables are read on every call; they
  *    are meant for schedule comparisons.
+ *  - Dense fallback: a non-gated bf16 sfl_ffn_forward of more than 256 tokens whose
+ *    ell_width K is at least f / 32 also writes the dense ReLU rows H (T x f bf16, in
+ *    the workspace) from the up projection's epilogue; once the classification has
+ *    counted the rows, a batch whose sparse rows hold more than T f / 64 entries in all
+ *    computes Y = H W_down by one dense GEMM instead of the ELL gather (which costs more
+ *    at such densities).
+ *    The TwELL, classification, ELL rows, statistics and dense-backup rows are written as
+ *    in the sparse mode. SFL_DENSE_FALLBACK=off disables it; =on makes every such call
+ *    take the dense GEMM. Read on every call.
  *  - Numerics: bf16 inputs are multiplied on MFMA with float32 accumulation;
  *    activations are stored in the activation dtype, bf16 by round-to-nearest-
  *    even. A hidden unit is active iff its pre-activation is > 0 (strict; +0,

@@ -86,6 +86,33 @@ bool fused_twell(const sfl_ffn_args_t& a) {
   return a.dtype == SFL_BF16 && (tn == 64 || tn == 128 || tn == 256) && !small_batch(a);
 }
 
+// Dense fallback of the non-gated forward for weakly sparse inputs. A row's gather reads one
+// W_down row segment per active unit, re-read per token; a dense down GEMM costs the same
+// for every row. Measured on gfx950 (d = 4096, f = 16384): the gather moves ~21 TB/s of
+// effective bytes and the GEMM ~1.25 PFLOP/s, so the gather is the slower one once a row
+// has more than about f / 60 active units (95 % / 90 % sparsity: 2.3 / 4.3 ms against 0.8 ms
+// for the GEMM). The caller's ELL width K bounds the row counts it expects: with
+// K >= f / 32 a call is a candidate, and its up projection also stores the dense ReLU rows
+// H (T x f bf16 in the workspace). After the classification a one-workgroup kernel compares
+// the entries the gather would read (the sparse rows' counts) with T f / 64 and arms either
+// Y = H W_down (one dense GEMM over all rows) or the ELL gather; the other exits at once. The dense-backup rows go through
+// their usual stage either way (which rewrites their rows of Y with the same values). The
+// TwELL, classification, ELL rows and statistics are the sparse mode's. Non-gated bf16
+// batches above 256 tokens whose TwELL epilogue is fused. SFL_DENSE_FALLBACK=off disables
+// it, =on makes every such batch a candidate that always takes the dense GEMM.
+int dense_fallback_env() {  // 0 default, 1 on, -1 off (read per call)
+  const char* e = std::getenv("SFL_DENSE_FALLBACK");
+  if (e && std::strcmp(e, "on") == 0) return 1;
+  if (e && std::strcmp(e, "off") == 0) return -1;
+  return 0;
+}
+bool dense_candidate(const sfl_ffn_args_t& a) {
+  if (a.gated || a.dtype != SFL_BF16 || a.T <= 256 || !fused_twell(a)) return false;
+  const int e = dense_fallback_env();
+  if (e != 0) return e > 0;
+  return (int64_t)a.cfg.ell_width * 32 >= a.f;
+}
+
 sfl_status_t check_forward(const sfl_ffn_args_t* a, bool need_output = true) {
   if (!a) return SFL_E_ARG;
   if (!dtype_ok(a->dtype)) return SFL_E_ARG;
@@ -137,6 +164,8 @@ struct FwdPlan {
   int32_t* need_slots = nullptr; // their ovf_dense rows [cap]
   int32_t* n_need = nullptr;     // [1]
   int32_t* order = nullptr;      // tokens by descending row count [T] (slice-walking gathers)
+  void* H = nullptr;             // dense-fallback candidate: the dense ReLU rows [T][f] bf16
+  int32_t* dense_flags = nullptr; // [2]: rows of the dense down GEMM (T or 0), gather skipped (1 or 0)
   int32_t* tile_sem = nullptr;   // dense-backup GEMMs of at most 64 rows: one counter per 256-column tile
   int n_sem = 0;                  // counters in tile_sem: 256-column tiles of the wider of f and d
   size_t bytes = 0;
@@ -157,6 +186,10 @@ FwdPlan plan_forward(const sfl_ffn_args_t& a, void* ws) {
   const int64_t cap = capacity_of(a.cfg, a.T);
   if (!fused_twell(a)) p.Z = (float*)c.take((size_t)a.T * a.f * 4);
   if (!a.twell.ovf_dense) p.ovf_dense = c.take((size_t)cap * a.f * elem_size(a.dtype));
+  if (dense_candidate(a)) {
+    p.H = c.take((size_t)a.T * a.f * 2);
+    p.dense_flags = (int32_t*)c.take(8);
+  }
   if (a.gated && !a.W_up_packed && !a.W_upT) p.WupT = c.take((size_t)a.f * a.d * elem_size(a.dtype));
   if (packed_gather(a) && !a.W_down_packed) p.WdP = c.take((size_t)a.f * a.d * 2);
   if (packed_gather(a)) p.order = (int32_t*)c.take((size_t)a.T * 4);
@@ -477,6 +510,10 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
     g.shift = a->shift_t;
     g.tile_order = up_tile_order();
     if (fused_twell(*a)) {
+      if (plan.H) {
+        g.dense_h = plan.H;
+        g.ldh = f;
+      }
       g.tw_val = tw.val;
       g.tw_idx = tw.idx;
       g.tw_cnt = tw.cnt;
@@ -518,6 +555,25 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
                           packed_layout(a->cfg)));
   SFL_HIP(launch_ovf_list(T, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s, plan.tile_sem, plan.n_sem));
   ev.record(2, s);
+  if (plan.H) {
+    // dense-fallback candidate: decide on the batch's mean row count, then Y = H W_down over
+    // all rows when dense (the GEMM's row count is T or 0 on the device)
+    SFL_HIP(launch_dense_decision(T, f, dense_fallback_env() > 0, tw.row_nnz, tw.row_ovf, plan.dense_flags, s));
+    GemmParams y = gp_zero();
+    y.M = (int)T;
+    y.N = (int)d;
+    y.K = (int)f;
+    y.A = plan.H;
+    y.lda = f;
+    y.a_bytes = T * f * 2;
+    y.m_count = plan.dense_flags;
+    y.count_cap = (int32_t)T;
+    int blay;
+    set_down_B(y, a->W_down, WdT, d, f, &blay);
+    y.C = a->Y;
+    y.ldc = d;
+    SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_ACT, y, s));
+  }
   // 3. sparse down projection of the ELL rows
   const void* WupT = a->W_upT;  // gated: W_up^T, given or built in the workspace when needed
   if (packed_gather(*a)) {
@@ -551,7 +607,7 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
       hv = plan.hval;
     }
     SFL_HIP(launch_gather_down_packed(T, d, f, a->cfg.ell_width, hv, tw.ell_idx, tw.row_nnz, tw.row_ovf, WdP, a->Y,
-                                      s, 0, 0, nullptr, order));
+                                      s, 0, 0, nullptr, order, plan.dense_flags ? plan.dense_flags + 1 : nullptr));
   } else {
     SFL_HIP(launch_gather_down(vb, T, d, a->cfg.ell_width, tw.ell_val, tw.ell_idx, tw.row_nnz, tw.row_ovf,
                                a->W_down, a->Y, s));

@@ -280,7 +280,9 @@ template <int VK, int OUT, int U, bool TG = false>
 __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
     int64_t T, int64_t d, int64_t f, int K, const void* __restrict__ ell_val, const uint16_t* __restrict__ ell_idx,
     const int32_t* __restrict__ row_nnz, const uint8_t* __restrict__ row_ovf, const bf16_t* __restrict__ W,
-    bf16_t* __restrict__ Y, float* __restrict__ Yf, int n_slices, int tpw, const int32_t* __restrict__ order) {
+    bf16_t* __restrict__ Y, float* __restrict__ Yf, int n_slices, int tpw, const int32_t* __restrict__ order,
+    const int32_t* __restrict__ skip) {
+  if (skip && *skip) return;         // the dense fallback took this batch
   constexpr int EW = VK + 1;         // words per staged entry
   // token groups read 8 tokens' entries at once: an odd stride puts them in different banks
   const int KS = TG ? K + 1 : K;
@@ -774,7 +776,7 @@ hipError_t launch_gather_down(int val_bf16, int64_t T, int64_t d, int K, const v
 hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, const void* ell_val,
                                      const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
                                      const void* Wp, void* Y, hipStream_t s, int val_f32, int out_mode, float* Yf,
-                                     const int32_t* order) {
+                                     const int32_t* order, const int32_t* skip) {
   if (T == 0) return hipSuccess;
   if (d % (8 * SLICE2) != 0) return hipErrorInvalidValue;
   if (out_mode < 0 || out_mode > 2 || (out_mode > 0 && !Yf) || (out_mode != 1 && !Y)) return hipErrorInvalidValue;
@@ -798,7 +800,7 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
       if (e != hipSuccess) return e;                                                                               \
     }                                                                                                              \
     hipLaunchKernelGGL((k_gather_down_b16<VK_, OUT_, U_, TG_>), grid, block, lds, s, T, d, f, K, ell_val, ell_idx, \
-                       row_nnz, row_ovf, (const bf16_t*)Wp, (bf16_t*)Y, Yf, n_slices, tpw, order);                 \
+                       row_nnz, row_ovf, (const bf16_t*)Wp, (bf16_t*)Y, Yf, n_slices, tpw, order, skip);           \
   } while (0)
 #define SFL_GATHER_LAUNCH_U(VK_, OUT_, U_) SFL_GATHER_LAUNCH_G(VK_, OUT_, U_, false)
 #define SFL_GATHER_LAUNCH(VK_, OUT_)                  \

@@ -755,6 +755,30 @@ __device__ __forceinline__ void kc_tile(const GemmParams& p, int tm, int tn, int
   gemm_epilogue<EPI, KC_WM, KC_WN, KC_FM, 0>(p, acc, op.wm, op.wn, m0, n0, m_eff, smem);
 }
 
+// The TwELL epilogue's optional dense output: h = ReLU(z) in bf16 for every element of the
+// tile (z already in the accumulators; columns past N carry z = -inf and are not stored).
+template <int WM_, int WN_, int FM>
+__device__ __forceinline__ void store_dense_relu(const GemmParams& p, const typename WaveTile<WM_, WN_, FM>::Acc& acc,
+                                                 int wm, int wn, int m0, int n0, int m_eff) {
+  typedef WaveTile<WM_, WN_, FM> W;
+  typedef AccGeo<FM> G;
+  const int lane = threadIdx.x & 63;
+  bf16_t* H = (bf16_t*)p.dense_h;
+#pragma unroll
+  for (int i = 0; i < W::TM_; ++i)
+#pragma unroll
+    for (int r = 0; r < G::R; ++r) {
+      const int row = m0 + wm * W::WTM_ + i * FM + G::row(r, lane);
+      if (row >= m_eff) continue;
+#pragma unroll
+      for (int j = 0; j < W::TN_; ++j) {
+        const int col = n0 + wn * W::WTN_ + j * FM + G::col(lane);
+        const float z = acc[i][j][r];
+        if (col < p.N) H[(int64_t)row * p.ldh + col] = active_bits(z) ? f32_to_bf16_finite(z) : (bf16_t)0;
+      }
+    }
+}
+
 // TwELL epilogue inputs of one tile held in registers: the shift of row wm*64 + lane and
 // the bias of columns wcol0 + lane and wcol0 + 64 + lane (-inf past N). Lanes fetch the
 // values of their accumulator rows and columns from these with lane permutes.
@@ -844,6 +868,7 @@ __global__ __launch_bounds__(NTHR) void k_gemm_kc(GemmParams p) {
     bf16_t* scratch = smem + bl * KC_STAGE;
     if constexpr (EPI == EPI_TWELL || EPI == EPI_TWELL_P32) {
       pre.apply(acc, op.lane);
+      if (p.dense_h) store_dense_relu<KC_WM, KC_WN, KC_FM>(p, acc, op.wm, op.wn, m0, n0, m_eff);
       twell_compact<KC_WM, KC_WN, KC_FM, Tn, EPI == EPI_TWELL_P32>(p, acc, op.wm, op.wn, m0, n0, m_eff,
                                                                     (int*)scratch);
     } else {
@@ -1125,6 +1150,7 @@ template <int ALAY, int BLAY>
 hipError_t launch_twell(const GemmParams& p, hipStream_t s) {
   const bool kc = ALAY == LAY_KC && kc_ok(p, BLAY);
   constexpr int BL = BLAY == LAY_RC ? LAY_RC : LAY_KC;
+  if (p.dense_h && !kc) return hipErrorInvalidValue;  // the dense rows come from the direct-to-LDS kernel only
   if (p.tw_packed) {  // the packed layout: 256-column tiles of 31 slots, direct-to-LDS kernel only
     if (!kc || p.tile_cols != 256 || p.tile_slots != 31) return hipErrorInvalidValue;
     return launch_kc<EPI_TWELL_P32, 256, BL>(p, s);

@@ -58,6 +58,9 @@ struct GemmParams {
   int32_t* tw_cnt;
   int tile_cols, tile_slots, n_tiles;
   int tw_packed;           // packed 32-bit layout: tw_val holds [rows][n_tiles][32] words
+  // EPI_TWELL, optional: the dense ReLU rows as well, bf16 h[row][n] (row stride ldh)
+  void* dense_h;
+  int64_t ldh;
   // split-K (K-contiguous kernel only; for skinny GEMMs such as the dense-backup rows):
   // up to `ksplit` K ranges per output tile, chosen on the device from the row count so
   // that ks * rows <= part_rows; fp32 partial sums go to part [ks][rows][N] and a second
@@ -124,6 +127,10 @@ hipError_t launch_ovf_fill(int64_t f, int val_bf16, int Tn, int S, const void* v
                            hipStream_t s, bool packed = false);
 // Sum (absval: of the absolute values) of the computed dense-backup rows, added into
 // stats->l1_sum.
+// Dense fallback decision: flags[0] = T and flags[1] = 1 (dense down GEMM, gather skipped)
+// when force or the sparse rows' (row_ovf = 0) row_nnz sum to more than T f / 64, else 0, 0.
+hipError_t launch_dense_decision(int64_t T, int64_t f, bool force, const int32_t* row_nnz, const uint8_t* row_ovf,
+                                 int32_t* flags, hipStream_t s);
 hipError_t launch_ovf_l1(int64_t f, int val_bf16, const void* ovf_dense, const int32_t* n_ovf,
                          int32_t cap, sfl_stats_t* stats, hipStream_t s, int absval);
 
@@ -138,7 +145,7 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int ell_wi
                                      const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
                                      const void* W_packed, void* Y, hipStream_t s,
                                      int val_f32 = 0, int out_mode = 0, float* Yf = nullptr,
-                                     const int32_t* order = nullptr);
+                                     const int32_t* order = nullptr, const int32_t* skip = nullptr);
 // Gated backward at the ELL entries: dh (8 partials + lambda' sign(g u)) -> dh_u, dh_g, h.
 hipError_t launch_gated_entry_grads(int64_t T, int K, const void* ell_val, const int32_t* row_nnz,
                                     const uint8_t* row_ovf, const float* part, const float* u, float lam, float* dhu,

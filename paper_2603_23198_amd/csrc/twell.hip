@@ -494,6 +494,34 @@ hipError_t launch_ovf_l1(int64_t f, int val_bf16, const void* dense, const int32
   return hipGetLastError();
 }
 
+// The dense fallback's choice (one workgroup): the entries the gather would read (the sparse
+// rows' counts; the dense-backup rows take their own path either way) against T f / 64.
+__global__ __launch_bounds__(1024) void k_dense_decision(int64_t T, int64_t f, int force,
+                                                         const int32_t* __restrict__ row_nnz,
+                                                         const uint8_t* __restrict__ row_ovf,
+                                                         int32_t* __restrict__ flags) {
+  __shared__ long long part[16];
+  long long sum = 0;
+  for (int64_t t = threadIdx.x; t < T; t += 1024) sum += row_ovf[t] ? 0 : row_nnz[t];
+  sum = wave_sum<long long>(sum);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = sum;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    long long tot = 0;
+    for (int i = 0; i < 16; ++i) tot += part[i];
+    const bool dense = force || tot * 64 > T * f;
+    flags[0] = dense ? (int32_t)T : 0;
+    flags[1] = dense ? 1 : 0;
+  }
+}
+
+hipError_t launch_dense_decision(int64_t T, int64_t f, bool force, const int32_t* row_nnz, const uint8_t* row_ovf,
+                                 int32_t* flags, hipStream_t s) {
+  if (T > INT32_MAX) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_dense_decision, dim3(1), dim3(1024), 0, s, T, f, force ? 1 : 0, row_nnz, row_ovf, flags);
+  return hipGetLastError();
+}
+
 // Dense-backup rows straight from the TwELL slabs (Sec. 3.4): a row whose tiles all kept
 // every active value (cnt <= S) is rebuilt exactly, zeros and all, in LDS one window of
 // columns at a time and written out; a row with an overflowing tile lost values, so it

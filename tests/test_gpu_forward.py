@@ -123,8 +123,13 @@ def test_c2_lognormal_overflow_full():
     check_pattern(got, Z[prow], prow, w.f, cfg.tile_cols, cfg.tile_slots)
 
 
-@pytest.mark.parametrize("sparsity", [0.9, 0.95, 0.99, 0.999])
-def test_c4_sweep_sampled(sparsity):
+@pytest.mark.parametrize("sparsity,fallback", [(0.9, None), (0.95, None), (0.95, "off"), (0.99, None),
+                                               (0.999, None)])
+def test_c4_sweep_sampled(sparsity, fallback, monkeypatch):
+    """The sparsity sweep at full size (90 % and 95 % take the dense fallback by default; 95 %
+    is also run with it disabled, through the long-row gather)."""
+    if fallback:
+        monkeypatch.setenv("SFL_DENSE_FALLBACK", fallback)
     w = wl.c4_sweep(sparsity)
     Y, bufs, stats, cfg = run_forward(w)
     got = twell_views(bufs, w.T, w.f, cfg)
@@ -672,3 +677,47 @@ def test_descending_nnz_token_order_gives_identical_results(T, gated, K, monkeyp
     rows = sample_rows(T, 48, 4, extra=np.nonzero(got["row_ovf"])[0][:4])
     Yref, _ = oracle_rows(w, rows)
     assert rel_l2(to_f64(Y2)[rows], Yref) <= 2e-2
+
+
+@pytest.mark.parametrize("sparsity,K,dense_expected", [(0.9, 640, True), (0.99, 64, False)])
+def test_dense_fallback_choice_and_results(sparsity, K, dense_expected, monkeypatch):
+    """ELL width K >= f / 32 makes a call a dense-fallback candidate: the up projection also
+    writes H, and a batch whose mean row count exceeds f / 64 takes one dense down GEMM instead
+    of the gather (the sparse rows' entries against T f / 64). Both choices meet the oracle; the TwELL, classification and the
+    dense-backup rows' outputs are the same as with the fallback disabled; a candidate that
+    keeps the gather gives the disabled run's output bit for bit."""
+    T, d, f = 1000, 512, 2048
+    w = wl.make_ffn("fallback", "bf16", T, d, f, seed=int(sparsity * 1000), sparsity=sparsity, ell_width=K)
+    w.shift_t[::50] = 10.0  # dense-backup rows
+    monkeypatch.setenv("SFL_DENSE_FALLBACK", "off")
+    Y0, b0, st0, cfg = run_forward(w, use_wupt=True, use_wdownt=True, packed_down=True)
+    monkeypatch.delenv("SFL_DENSE_FALLBACK")
+    Y1, b1, st1, _ = run_forward(w, use_wupt=True, use_wdownt=True, packed_down=True)
+    for k in ("cnt", "row_nnz", "row_ovf"):
+        assert torch.equal(b0[k], b1[k]), k
+    got = twell_views(b1, T, f, cfg)
+    got0 = twell_views(b0, T, f, cfg)
+    for t in np.nonzero(got["row_ovf"] == 0)[0][::7]:  # ELL rows: the specified entries
+        c = int(got["row_nnz"][t])
+        np.testing.assert_array_equal(got["ell_idx"][t, :c], got0["ell_idx"][t, :c])
+        np.testing.assert_array_equal(got["ell_val"][t, :c], got0["ell_val"][t, :c])
+    gather_entries = got["row_nnz"][got["row_ovf"] == 0].sum()
+    assert (gather_entries * 64 > T * f) == dense_expected
+    ovf = np.nonzero(got["row_ovf"])[0]
+    assert len(ovf) >= T // 50
+    assert torch.equal(Y0.view(torch.int16)[ovf], Y1.view(torch.int16)[ovf])  # dense-backup rows
+    if dense_expected:
+        assert rel_l2(to_f64(Y1), to_f64(Y0)) <= 1e-2
+    else:
+        assert torch.equal(Y0.view(torch.int16), Y1.view(torch.int16))
+    s0, s1 = b.read_stats(st0), b.read_stats(st1)
+    assert s0["total_nnz"] == s1["total_nnz"] and abs(s0["l1_sum"] - s1["l1_sum"]) <= 1e-6 * s0["l1_sum"]
+    rows = sample_rows(T, 64, 8, extra=ovf[:4])
+    Yref, _ = oracle_rows(w, rows)
+    for i, t in enumerate(rows):
+        assert rel_l2(to_f64(Y1)[t], Yref[i]) <= 2e-2, t
+    monkeypatch.setenv("SFL_DENSE_FALLBACK", "on")  # every eligible call takes the dense GEMM
+    Y2, _, _, _ = run_forward(w, use_wupt=True, use_wdownt=True, packed_down=True)
+    assert rel_l2(to_f64(Y2)[rows], Yref) <= 2e-2
+    if dense_expected:
+        assert torch.equal(Y1.view(torch.int16), Y2.view(torch.int16))
