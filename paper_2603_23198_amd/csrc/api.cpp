@@ -159,10 +159,10 @@ struct FwdPlan {
   void* hval = nullptr;      // gated: h = g * u of the ELL entries [T][K] bf16
   float* part = nullptr;     // split-K partial sums of the dense-backup GEMMs [part_rows][max(f, d)]
   int part_rows = 0;
-  uint8_t* need = nullptr;       // dense-backup slots whose rows the GEMM recomputes [cap]
-  int32_t* need_rows = nullptr;  // their token rows [cap]
+  int32_t* need_rows = nullptr;  // token rows of the dense-backup rows the GEMM recomputes [cap]
   int32_t* need_slots = nullptr; // their ovf_dense rows [cap]
-  int32_t* n_need = nullptr;     // [1]
+  int32_t* n_need = nullptr;     // [1], zeroed with tile_sem by the overflow-list kernel
+  int n_zero = 0;                // counters from n_need (or tile_sem) on that the overflow list zeroes
   int32_t* order = nullptr;      // tokens by descending row count [T] (slice-walking gathers)
   void* H = nullptr;             // dense-fallback candidate: the dense ReLU rows [T][f] bf16
   int32_t* dense_flags = nullptr; // [2]: rows of the dense down GEMM (T or 0), gather skipped (1 or 0)
@@ -203,15 +203,17 @@ FwdPlan plan_forward(const sfl_ffn_args_t& a, void* ws) {
     p.part_rows = (int)std::min<int64_t>(align_rows(std::max<int64_t>(cap, a.T)), kPartRows);
     p.part = (float*)c.take((size_t)p.part_rows * std::max(a.f, a.d) * 4);
   }
-  if (a.dtype == SFL_BF16 && cap > 0 && cap <= 64) {
-    p.n_sem = (int)cdiv(std::max(a.f, a.d), 256);
-    p.tile_sem = (int32_t*)c.take((size_t)p.n_sem * 4);
-  }
-  if (cap > 0 && rebuild_ovf(a)) {
-    p.need = (uint8_t*)c.take((size_t)cap);
+  // counters the overflow-list kernel zeroes: the recompute list's length, then one per
+  // 256-column tile for dense-backup GEMMs of at most 64 rows
+  const bool need_list = cap > 0 && rebuild_ovf(a);
+  if (a.dtype == SFL_BF16 && cap > 0 && cap <= 64) p.n_sem = (int)cdiv(std::max(a.f, a.d), 256);
+  p.n_zero = (need_list ? 1 : 0) + p.n_sem;
+  int32_t* counters = p.n_zero > 0 ? (int32_t*)c.take((size_t)p.n_zero * 4) : nullptr;
+  if (need_list) p.n_need = counters;
+  if (p.n_sem > 0) p.tile_sem = counters + (need_list ? 1 : 0);
+  if (need_list) {
     p.need_rows = (int32_t*)c.take((size_t)cap * 4);
     p.need_slots = (int32_t*)c.take((size_t)cap * 4);
-    p.n_need = (int32_t*)c.take(4);
   }
   p.bytes = c.used;
   return p;
@@ -553,7 +555,8 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
   SFL_HIP(launch_classify(T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, a->cfg.ell_width, tw.val, tw.idx, tw.cnt,
                           tw.row_nnz, tw.row_ovf, tw.ell_val, tw.ell_idx, a->stats, s, a->gated ? 0 : 1,
                           packed_layout(a->cfg)));
-  SFL_HIP(launch_ovf_list(T, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s, plan.tile_sem, plan.n_sem));
+  SFL_HIP(launch_ovf_list(T, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s,
+                          plan.n_need ? plan.n_need : plan.tile_sem, plan.n_zero));
   ev.record(2, s);
   if (plan.H) {
     // dense-fallback candidate: decide on the batch's mean row count, then Y = H W_down over
@@ -621,8 +624,8 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
     const bool rebuild = rebuild_ovf(*a);
     if (rebuild)
       SFL_HIP(launch_ovf_fill(f, vb, a->cfg.tile_cols, a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, tw.ovf_rows,
-                              tw.n_ovf, (int32_t)cap, ovf_dense, plan.need, plan.need_rows, plan.need_slots,
-                              plan.n_need, s, packed_layout(a->cfg)));
+                              tw.n_ovf, (int32_t)cap, ovf_dense, plan.need_rows, plan.need_slots, plan.n_need, s,
+                              packed_layout(a->cfg)));
     GemmParams g = gp_zero();
     g.M = (int)cap;
     g.N = (int)f;

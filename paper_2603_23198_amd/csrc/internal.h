@@ -120,11 +120,12 @@ bool nnz_order_supported(int K);
 hipError_t launch_nnz_order(int64_t T, int K, const int32_t* row_nnz, const uint8_t* row_ovf, int32_t* order,
                             hipStream_t s);
 // Dense-backup rows whose tiles kept every value, rebuilt from the TwELL slabs; the others
-// are listed (need_rows: token rows, need_slots: their ovf_dense rows, n_need) for the GEMM.
+// are listed (need_rows: token rows, need_slots: their ovf_dense rows, *n_need: their number,
+// which must be zero before the call; list order unspecified) for the GEMM.
 hipError_t launch_ovf_fill(int64_t f, int val_bf16, int Tn, int S, const void* val, const uint16_t* idx,
                            const int32_t* cnt, const int32_t* ovf_rows, const int32_t* n_ovf, int32_t cap,
-                           void* dense, uint8_t* need, int32_t* need_rows, int32_t* need_slots, int32_t* n_need,
-                           hipStream_t s, bool packed = false);
+                           void* dense, int32_t* need_rows, int32_t* need_slots, int32_t* n_need, hipStream_t s,
+                           bool packed = false);
 // Sum (absval: of the absolute values) of the computed dense-backup rows, added into
 // stats->l1_sum.
 // Dense fallback decision: flags[0] = T and flags[1] = 1 (dense down GEMM, gather skipped)

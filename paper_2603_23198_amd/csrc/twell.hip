@@ -529,11 +529,16 @@ hipError_t launch_dense_decision(int64_t T, int64_t f, bool force, const int32_t
 // i < n_ovf.
 constexpr int kFillWindowBytes = 32768;
 constexpr int kFillBlocks = 1024;
+// A row with an overflowing tile is appended to the recompute list (need_rows: token row,
+// need_slots: its ovf_dense row) at a position taken from the zeroed counter n_need; the
+// list's order varies from call to call, which the recomputing GEMM does not see (each of
+// its rows is computed by the same arithmetic wherever it sits).
 template <typename V, bool PK>
 __global__ __launch_bounds__(256) void k_ovf_fill(int64_t f, int NT, int Tn, int S, const V* __restrict__ val,
                                                   const uint16_t* __restrict__ idx, const int32_t* __restrict__ cnt,
                                                   const int32_t* __restrict__ ovf_rows, const int32_t* __restrict__ n_ovf,
-                                                  int32_t cap, V* __restrict__ dense, uint8_t* __restrict__ need) {
+                                                  int32_t cap, V* __restrict__ dense, int32_t* __restrict__ need_rows,
+                                                  int32_t* __restrict__ need_slots, int32_t* __restrict__ n_need) {
   constexpr int WIN = kFillWindowBytes / (int)sizeof(V);  // columns per window (a multiple of every tile width)
   __shared__ V row_s[WIN];
   const int n = min(*n_ovf, cap);
@@ -543,8 +548,14 @@ __global__ __launch_bounds__(256) void k_ovf_fill(int64_t f, int NT, int Tn, int
     int over = 0;
     for (int j = threadIdx.x; j < NT; j += 256) over |= sl.count(j) > S;
     over = __syncthreads_or(over);
-    if (threadIdx.x == 0) need[i] = over ? 1 : 0;
-    if (over) continue;
+    if (over) {
+      if (threadIdx.x == 0) {
+        const int pos = atomicAdd(n_need, 1);
+        need_rows[pos] = (int32_t)t;
+        need_slots[pos] = i;
+      }
+      continue;
+    }
     V* out = dense + (int64_t)i * f;
     for (int64_t c0 = 0; c0 < f; c0 += WIN) {
       const int w = (int)std::min<int64_t>(WIN, f - c0);
@@ -567,57 +578,23 @@ __global__ __launch_bounds__(256) void k_ovf_fill(int64_t f, int NT, int Tn, int
   }
 }
 
-// Compaction of the flagged slots (ascending): rows[k] = ovf_rows[slot], slots[k] = slot.
-__global__ __launch_bounds__(1024) void k_need_list(int32_t cap, const int32_t* __restrict__ ovf_rows,
-                                                    const int32_t* __restrict__ n_ovf, const uint8_t* __restrict__ need,
-                                                    int32_t* __restrict__ rows, int32_t* __restrict__ slots,
-                                                    int32_t* __restrict__ n_need) {
-  __shared__ int wsum[16];
-  const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
-  const int n = min(*n_ovf, cap);
-  int base = 0;
-  for (int r0 = 0; r0 < n; r0 += 1024) {
-    const int i = r0 + tid;
-    const int flag = (i < n && need[i]) ? 1 : 0;
-    const int incl = wave_incl_scan(flag);
-    if (l == 63) wsum[w] = incl;
-    __syncthreads();
-    int before = 0, all = 0;
-    for (int q = 0; q < 16; ++q) {
-      const int v = wsum[q];
-      before += (q < w) ? v : 0;
-      all += v;
-    }
-    const int pos = base + before + incl - flag;
-    if (flag) {
-      rows[pos] = ovf_rows[i];
-      slots[pos] = i;
-    }
-    base += all;
-    __syncthreads();
-  }
-  if (tid == 0) *n_need = base;
-}
-
 hipError_t launch_ovf_fill(int64_t f, int val_bf16, int Tn, int S, const void* val, const uint16_t* idx,
                            const int32_t* cnt, const int32_t* ovf_rows, const int32_t* n_ovf, int32_t cap,
-                           void* dense, uint8_t* need, int32_t* need_rows, int32_t* need_slots, int32_t* n_need,
-                           hipStream_t s, bool packed) {
+                           void* dense, int32_t* need_rows, int32_t* need_slots, int32_t* n_need, hipStream_t s,
+                           bool packed) {
   if (cap == 0) return hipSuccess;
   if (packed && !val_bf16) return hipErrorInvalidValue;
   const int NT = (int)cdiv(f, Tn);
   const dim3 grid((unsigned)std::min<int32_t>(cap, kFillBlocks));
   if (packed)
     hipLaunchKernelGGL((k_ovf_fill<bf16_t, true>), grid, dim3(256), 0, s, f, NT, Tn, S, (const bf16_t*)val, idx, cnt,
-                       ovf_rows, n_ovf, cap, (bf16_t*)dense, need);
+                       ovf_rows, n_ovf, cap, (bf16_t*)dense, need_rows, need_slots, n_need);
   else if (val_bf16)
     hipLaunchKernelGGL((k_ovf_fill<bf16_t, false>), grid, dim3(256), 0, s, f, NT, Tn, S, (const bf16_t*)val, idx, cnt,
-                       ovf_rows, n_ovf, cap, (bf16_t*)dense, need);
+                       ovf_rows, n_ovf, cap, (bf16_t*)dense, need_rows, need_slots, n_need);
   else
     hipLaunchKernelGGL((k_ovf_fill<float, false>), grid, dim3(256), 0, s, f, NT, Tn, S, (const float*)val, idx, cnt,
-                       ovf_rows, n_ovf, cap, (float*)dense, need);
-  hipLaunchKernelGGL(k_need_list, dim3(1), dim3(1024), 0, s, cap, ovf_rows, n_ovf, need, need_rows, need_slots,
-                     n_need);
+                       ovf_rows, n_ovf, cap, (float*)dense, need_rows, need_slots, n_need);
   return hipGetLastError();
 }
 
