@@ -494,12 +494,17 @@ def main():
     ms = head["ms"]
     stages = head["stages_ms"]
 
-    # the up projection's persistent tile order: XCD-grouped (default) against a Hilbert curve
+    # the persistent GEMMs' tile order: a Hilbert curve over 32 x 32 blocks of tiles (default)
+    # against the XCD-grouped order, for the up projection of the sparse forward and for the
+    # dense FFN's two GEMMs (interleaved runs)
     order_ab = {}
+    dmk = lambda ev: b.ffn_args(s["X"], s["Wu"], s["Wd"], s["cfg"], **s["dkw"], workspace=s["dws"], events=ev)
     for order in ("grouped", "hilbert", "grouped", "hilbert", "grouped", "hilbert"):
         os.environ["SFL_GEMM_TILE_ORDER"] = order
         order_ab.setdefault(order + "_ms", []).append(
             B.stage_times(s["mk"], b.sfl_ffn_forward, 5)[0])
+        order_ab.setdefault("dense_" + order + "_ms", []).append(
+            float(sum(B.stage_times(dmk, b.sfl_dense_ffn_baseline, 3))))
     os.environ.pop("SFL_GEMM_TILE_ORDER", None)
     order_ab = {k: round(float(np.mean(v)), 4) for k, v in order_ab.items()}
 

@@ -26,11 +26,13 @@
  *    concurrent calls on different streams with disjoint buffers (workspaces
  *    included) are safe, except sfl_ffn_forward_noalloc calls that overlap on
  *    one GPU (they share its scratch array).
- *  - Environment: SFL_GEMM_TILE_ORDER=hilbert makes the up (gate) projection of
- *    sfl_ffn_forward and sfl_up_projection deal its 256 x 256 output tiles along a
- *    Hilbert curve (the paper's persistent-GEMM schedule) instead of the default
- *    XCD-grouped order; results are identical (each tile's sums do not depend on
- *    the order). sfl_ffn_forward's sparse down projection (and the gated up-dots)
+ *  - Environment: the persistent GEMMs (the up or gate projection of
+ *    sfl_ffn_forward and sfl_up_projection, the GEMMs of sfl_dense_ffn_baseline and
+ *    of the dense fallback) deal their 256 x 256 output tiles along a Hilbert curve
+ *    over square blocks of tiles (the paper's persistent-GEMM schedule) where the
+ *    tile grid is made of such squares, and in an XCD-grouped order otherwise;
+ *    SFL_GEMM_TILE_ORDER=grouped selects the grouped order everywhere. Results are
+ *    identical (each tile's sums do not depend on the order). sfl_ffn_forward's sparse down projection (and the gated up-dots)
  *    deals the tokens by descending row count (one more kernel, a counting sort) for
  *    batches of at least 1024 tokens with ell_width <= 256, and in token order
  *    otherwise; SFL_TOKEN_ORDER=nnz or SFL_TOKEN_ORDER=token forces one of the two.

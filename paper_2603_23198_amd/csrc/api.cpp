@@ -161,19 +161,24 @@ struct FwdPlan {
   int part_rows = 0;
   int32_t* need_rows = nullptr;  // token rows of the dense-backup rows the GEMM recomputes [cap]
   int32_t* need_slots = nullptr; // their ovf_dense rows [cap]
-  int32_t* n_need = nullptr;     // [1], zeroed with tile_sem by the overflow-list kernel
-  int n_zero = 0;                // counters from n_need (or tile_sem) on that the overflow list zeroes
+  int32_t* n_need = nullptr;     // [1], zeroed with tile_sem by the forward's first kernel
+  int n_zero = 0;                // counters from n_need (or tile_sem) on that the first kernel zeroes
   int32_t* order = nullptr;      // tokens by descending row count [T] (slice-walking gathers)
   void* H = nullptr;             // dense-fallback candidate: the dense ReLU rows [T][f] bf16
   int32_t* dense_flags = nullptr; // [2]: rows of the dense down GEMM (T or 0), gather skipped (1 or 0)
-  int32_t* tile_sem = nullptr;   // dense-backup GEMMs of at most 64 rows: one counter per 256-column tile
-  int n_sem = 0;                  // counters in tile_sem: 256-column tiles of the wider of f and d
+  int32_t* tile_sem = nullptr;   // split-K GEMMs of at most 64 rows: one counter per output tile
+                                 // (its last block resets it to zero)
+  int n_sem = 0;                  // counters in tile_sem: 128-column tiles of the wider of f and d
   size_t bytes = 0;
 };
 
 // Dense-backup rows are few but their GEMMs are long in K (d, then f): split K over up to
 // this many blocks per output tile, with partial sums for up to kPartRows rows.
 constexpr int kMaxSplit = 8;
+// Gated batches of at most this many tokens form h = g * u inside the down projection's
+// gather (the entries are staged once per XCD there, so the 8 partial sums of each entry
+// are read 8 times: cheap against a launch at decode sizes, not at prefill sizes).
+constexpr int64_t kGatherFormsH = 64;
 constexpr int64_t kPartRows = 4096;
 
 bool packed_gather(const sfl_ffn_args_t& a) { return a.dtype == SFL_BF16 && a.d % 512 == 0; }
@@ -203,10 +208,12 @@ FwdPlan plan_forward(const sfl_ffn_args_t& a, void* ws) {
     p.part_rows = (int)std::min<int64_t>(align_rows(std::max<int64_t>(cap, a.T)), kPartRows);
     p.part = (float*)c.take((size_t)p.part_rows * std::max(a.f, a.d) * 4);
   }
-  // counters the overflow-list kernel zeroes: the recompute list's length, then one per
-  // 256-column tile for dense-backup GEMMs of at most 64 rows
+  // counters the forward's first kernel zeroes: the recompute list's length, then one per
+  // output tile (256 columns, 128 for the gated pair) of the dense-backup GEMMs of at
+  // most 64 rows
   const bool need_list = cap > 0 && rebuild_ovf(a);
-  if (a.dtype == SFL_BF16 && cap > 0 && cap <= 64) p.n_sem = (int)cdiv(std::max(a.f, a.d), 256);
+  if (a.dtype == SFL_BF16 && cap > 0 && cap <= 64)
+    p.n_sem = (int)cdiv(std::max(a.f, a.d), 128);  // 128-column tiles of the gated pair
   p.n_zero = (need_list ? 1 : 0) + p.n_sem;
   int32_t* counters = p.n_zero > 0 ? (int32_t*)c.take((size_t)p.n_zero * 4) : nullptr;
   if (need_list) p.n_need = counters;
@@ -288,11 +295,12 @@ bool nnz_token_order(const sfl_ffn_args_t& a) {
   return a.T >= 1024 && a.cfg.ell_width <= 256;
 }
 
-// Tile order of the up (gate) projection's persistent GEMM: SFL_GEMM_TILE_ORDER=hilbert
-// selects the Hilbert-curve order, anything else the grouped XCD order (read per call).
-int up_tile_order() {
+// Tile order of the persistent GEMMs (the up or gate projection, the dense FFN's GEMMs):
+// along a Hilbert curve over square blocks of tiles where the grid allows it, and the
+// grouped XCD order with SFL_GEMM_TILE_ORDER=grouped (read per call).
+int gemm_tile_order() {
   const char* e = std::getenv("SFL_GEMM_TILE_ORDER");
-  return (e && std::strcmp(e, "hilbert") == 0) ? TILE_ORDER_HILBERT : TILE_ORDER_GROUPED;
+  return (e && std::strcmp(e, "grouped") == 0) ? TILE_ORDER_GROUPED : TILE_ORDER_HILBERT;
 }
 
 hipError_t run_gemm(sfl_dtype_t dt, int alay, int blay, int epi, const GemmParams& g, hipStream_t s) {
@@ -436,7 +444,7 @@ sfl_status_t sfl_up_projection(const sfl_ffn_args_t* a, float* Z, sfl_stream_t s
     set_weight_B(g, a->W_up, bf ? a->W_upT : nullptr, a->d, a->f, &blay);
   g.bias = a->bias_f;
   g.shift = a->shift_t;
-  g.tile_order = up_tile_order();
+  g.tile_order = gemm_tile_order();
   g.C = Z;
   g.ldc = a->f;
   if (small_batch(*a)) {  // the same split-K main loop as the forward's
@@ -486,7 +494,7 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
   const sfl_twell_t& tw = a->twell;
   void* ovf_dense = tw.ovf_dense ? tw.ovf_dense : plan.ovf_dense;
   ev.record(0, s);
-  SFL_HIP(launch_stats_init(a->stats, s));
+  SFL_HIP(launch_stats_init(a->stats, s, plan.n_need ? plan.n_need : plan.tile_sem, plan.n_zero));
   if (T == 0) {
     SFL_HIP(launch_ovf_list(0, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s));
     for (int i = 1; i < 5; ++i) ev.record(i, s);
@@ -510,7 +518,7 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
     set_weight_B(g, Wp, WpT, d, f, &blay);
     g.bias = a->bias_f;
     g.shift = a->shift_t;
-    g.tile_order = up_tile_order();
+    g.tile_order = gemm_tile_order();
     if (fused_twell(*a)) {
       if (plan.H) {
         g.dense_h = plan.H;
@@ -536,7 +544,8 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
       }
       if (ks > 1) {
         // the pack sums the split-K partials itself (the reduction's arithmetic), so Z is
-        // never written
+        // never written. (Packing in the GEMM's last block per tile was slower: the
+        // device-scope release each block then needs writes back its XCD's L2.)
         g.no_reduce = 1;
         SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_F32, g, s));
         SFL_HIP(launch_pack_twell_parts(plan.part, ks, a->bias_f, a->shift_t, T, f, vb, a->cfg.tile_cols,
@@ -555,8 +564,7 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
   SFL_HIP(launch_classify(T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, a->cfg.ell_width, tw.val, tw.idx, tw.cnt,
                           tw.row_nnz, tw.row_ovf, tw.ell_val, tw.ell_idx, a->stats, s, a->gated ? 0 : 1,
                           packed_layout(a->cfg)));
-  SFL_HIP(launch_ovf_list(T, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s,
-                          plan.n_need ? plan.n_need : plan.tile_sem, plan.n_zero));
+  SFL_HIP(launch_ovf_list(T, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s));
   ev.record(2, s);
   if (plan.H) {
     // dense-fallback candidate: decide on the batch's mean row count, then Y = H W_down over
@@ -571,6 +579,7 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
     y.a_bytes = T * f * 2;
     y.m_count = plan.dense_flags;
     y.count_cap = (int32_t)T;
+    y.tile_order = gemm_tile_order();
     int blay;
     set_down_B(y, a->W_down, WdT, d, f, &blay);
     y.C = a->Y;
@@ -605,12 +614,18 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
       }
       SFL_HIP(launch_gated_updot(T, d, f, a->cfg.ell_width, tw.ell_idx, tw.row_nnz, tw.row_ovf, a->X, WuP,
                                  plan.part_u, s, order));
-      SFL_HIP(launch_gated_h(T, a->cfg.ell_width, tw.ell_val, tw.row_nnz, tw.row_ovf, plan.part_u, plan.hval, s,
-                             a->stats));
-      hv = plan.hval;
+      if (T > kGatherFormsH) {
+        SFL_HIP(launch_gated_h(T, a->cfg.ell_width, tw.ell_val, tw.row_nnz, tw.row_ovf, plan.part_u, plan.hval, s,
+                               a->stats));
+        hv = plan.hval;
+      }
     }
+    // up to kGatherFormsH tokens the gated layer's gather forms h from the gate values and
+    // the up-dot partials itself
+    const bool form_h = a->gated && T <= kGatherFormsH;
     SFL_HIP(launch_gather_down_packed(T, d, f, a->cfg.ell_width, hv, tw.ell_idx, tw.row_nnz, tw.row_ovf, WdP, a->Y,
-                                      s, 0, 0, nullptr, order, plan.dense_flags ? plan.dense_flags + 1 : nullptr));
+                                      s, 0, 0, nullptr, order, plan.dense_flags ? plan.dense_flags + 1 : nullptr,
+                                      form_h ? plan.part_u : nullptr, form_h ? a->stats : nullptr));
   } else {
     SFL_HIP(launch_gather_down(vb, T, d, a->cfg.ell_width, tw.ell_val, tw.ell_idx, tw.row_nnz, tw.row_ovf,
                                a->W_down, a->Y, s));
@@ -647,18 +662,35 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
     g.ksplit = kMaxSplit;
     g.part = plan.part;
     g.part_rows = plan.part_rows;
-    g.tile_sem = plan.tile_sem;  // zeroed by the overflow-list kernel above
-    SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_ACT_RELU, g, s));
-    if (a->gated) {
-      GemmParams u = g;
-      u.a_rows = tw.ovf_rows;
-      u.m_count = tw.n_ovf;
-      u.c_rows = nullptr;
-      u.s_rows = nullptr;
-      u.bias = nullptr;
-      u.shift = nullptr;
-      set_weight_B(u, a->W_up, WupT, d, f, &blay);
-      SFL_HIP(gemm_bf16(LAY_KC, blay, EPI_MUL_ACT, u, s));
+    g.tile_sem = plan.tile_sem;  // zero: set by the first kernel, reset by the last blocks of each use
+    // where the GEMM's last blocks store the rows they also sum |h| (no separate launch)
+    bool l1_in_gemm = false;
+    GemmParams pair = g;
+    pair.B2 = WupT;
+    pair.l1_stats = a->stats;
+    if (a->gated && !rebuild && WupT && blay == LAY_KC && gated_pair_ok(pair)) {
+      // both products of at most 64 rows in one launch, h formed by the tiles' last blocks
+      // (every dense-backup row recomputed: none is rebuilt from the slabs)
+      SFL_HIP(launch_gated_pair(pair, s));
+      l1_in_gemm = true;
+    } else {
+      if (!a->gated && !rebuild) {
+        g.l1_stats = a->stats;
+        l1_in_gemm = few_rows_tile_epilogue(g, blay);
+        if (!l1_in_gemm) g.l1_stats = nullptr;
+      }
+      SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_ACT_RELU, g, s));
+      if (a->gated) {
+        GemmParams u = g;
+        u.a_rows = tw.ovf_rows;
+        u.m_count = tw.n_ovf;
+        u.c_rows = nullptr;
+        u.s_rows = nullptr;
+        u.bias = nullptr;
+        u.shift = nullptr;
+        set_weight_B(u, a->W_up, WupT, d, f, &blay);
+        SFL_HIP(gemm_bf16(LAY_KC, blay, EPI_MUL_ACT, u, s));
+      }
     }
     GemmParams y = gp_zero();
     y.M = (int)cap;
@@ -679,7 +711,7 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
     // the partial-sum buffer holds part_rows rows of max(f, d) columns: more rows of d
     y.part_rows = (int)std::min<int64_t>((int64_t)plan.part_rows * std::max(f, d) / d, INT32_MAX);
     SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_ACT, y, s));
-    SFL_HIP(launch_ovf_l1(f, vb, ovf_dense, tw.n_ovf, (int32_t)cap, a->stats, s, a->gated ? 1 : 0));
+    if (!l1_in_gemm) SFL_HIP(launch_ovf_l1(f, vb, ovf_dense, tw.n_ovf, (int32_t)cap, a->stats, s, a->gated ? 1 : 0));
   }
   ev.record(4, s);
   return SFL_OK;
@@ -713,6 +745,7 @@ sfl_status_t sfl_dense_ffn_baseline(const sfl_ffn_args_t* a, sfl_stream_t stream
   g.shift = a->shift_t;
   g.C = a->workspace;
   g.ldc = f;
+  g.tile_order = gemm_tile_order();
   float* part = (float*)((char*)a->workspace + align_up((size_t)T * f * 2));
   const int ks_up = dense_ks(*a, T, f, d), ks_down = dense_ks(*a, T, d, f);
   if (ks_up > 1) {
@@ -739,6 +772,7 @@ sfl_status_t sfl_dense_ffn_baseline(const sfl_ffn_args_t* a, sfl_stream_t stream
   set_down_B(y, a->W_down, bf ? a->W_downT : nullptr, d, f, &blay);
   y.C = a->Y;
   y.ldc = d;
+  y.tile_order = gemm_tile_order();
   if (ks_down > 1) {
     y.ksplit = ks_down;
     y.part = part;

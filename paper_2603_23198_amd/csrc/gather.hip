@@ -14,7 +14,9 @@
 // column n, u = x[t] . W_up[:, n] and y[t] += (g * u) W_down[n]. Done in two passes with
 // the same slice walk: k_gated_updot forms u for every entry (per-XCD partial sums over
 // that XCD's slices of d, from a slice-major copy of W_up), k_gated_h combines them into
-// h = g * u, and k_gather_down_b16 does the down projection with h as the values.
+// h = g * u, and k_gather_down_b16 does the down projection with h as the values (for
+// decode-sized batches the gather forms h itself while staging the entries, one launch
+// fewer).
 #include "common.h"
 #include "internal.h"
 
@@ -137,6 +139,21 @@ constexpr int NGRP = 64 / LPR;         // row segments per load instruction
 #define SFL_GATHER_LDS 98304
 #endif
 constexpr int GATHER_WAVES = SFL_GATHER_WAVES;
+
+// Adds the workgroup's sum of l1 (one value per thread) to stats->l1_sum with one float64
+// atomic (atomics on one address serialise, so one per thread would cost more than the
+// sum). Called by every thread of a GATHER_WAVES-wave workgroup.
+__device__ __forceinline__ void block_l1_add(sfl_stats_t* stats, float l1) {
+  __shared__ float wsum[GATHER_WAVES];
+  l1 = wave_sum<float>(l1);
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = l1;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float tot = 0.f;
+    for (int w = 0; w < GATHER_WAVES; ++w) tot += wsum[w];
+    if (tot != 0.f) atomicAdd(&stats->l1_sum, (double)tot);
+  }
+}
 constexpr int GU = SFL_GATHER_UNROLL;       // row loads in flight per lane
 // ELL rows of at most 128 entries (ELL width K <= 128) in kernels that run one workgroup
 // per CU anyway (the staged entries fill the LDS): 12 row loads per lane, so that a
@@ -281,7 +298,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
     int64_t T, int64_t d, int64_t f, int K, const void* __restrict__ ell_val, const uint16_t* __restrict__ ell_idx,
     const int32_t* __restrict__ row_nnz, const uint8_t* __restrict__ row_ovf, const bf16_t* __restrict__ W,
     bf16_t* __restrict__ Y, float* __restrict__ Yf, int n_slices, int tpw, const int32_t* __restrict__ order,
-    const int32_t* __restrict__ skip) {
+    const int32_t* __restrict__ skip, const float* __restrict__ part_u, sfl_stats_t* __restrict__ stats) {
   if (skip && *skip) return;         // the dense fallback took this batch
   constexpr int EW = VK + 1;         // words per staged entry
   // token groups read 8 tokens' entries at once: an odd stride puts them in different banks
@@ -305,6 +322,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
     cnt_s[i] = (t < T && !row_ovf[t]) ? row_nnz[t] : -1;
   }
   __syncthreads();
+  float l1 = 0.f;
   for (int i = wave; i < tpw; i += GATHER_WAVES) {
     const int c = cnt_s[i];
     const int64_t t = tok(i);
@@ -313,10 +331,23 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
         ent[EW * (i * KS + e)] = (uint32_t)ell_idx[t * K + e];
         ent[EW * (i * KS + e) + 1] = __float_as_uint(((const float*)ell_val)[t * K + e]);
       } else {
-        ent[i * KS + e] = (uint32_t)ell_idx[t * K + e] | ((uint32_t)((const bf16_t*)ell_val)[t * K + e] << 16);
+        uint32_t v = ((const bf16_t*)ell_val)[t * K + e];
+        if (part_u) {
+          // gated: h = g * u formed here, with the arithmetic of k_gated_h (u = the 8 XCD
+          // partial dot products in XCD order; one rounding of the product); the blocks of
+          // XCD 0 add |h| to the statistics
+          const int64_t total = T * (int64_t)K, ie = t * K + e;
+          float u = 0.f;
+#pragma unroll
+          for (int x = 0; x < 8; ++x) u += part_u[(int64_t)x * total + ie];
+          v = f32_to_bf16(bf16_to_f32((bf16_t)v) * u);
+          l1 += fabsf(bf16_to_f32((bf16_t)v));
+        }
+        ent[i * KS + e] = (uint32_t)ell_idx[t * K + e] | (v << 16);
       }
     }
   }
+  if (part_u && stats && xcd == 0) block_l1_add(stats, l1);
   __syncthreads();
   const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc((void*)W, (short)0, 0x7fffffff, 0x00020000);
   // work items (slice of this XCD, token) in slice-major order, dealt round-robin to the
@@ -776,8 +807,10 @@ hipError_t launch_gather_down(int val_bf16, int64_t T, int64_t d, int K, const v
 hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, const void* ell_val,
                                      const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
                                      const void* Wp, void* Y, hipStream_t s, int val_f32, int out_mode, float* Yf,
-                                     const int32_t* order, const int32_t* skip) {
+                                     const int32_t* order, const int32_t* skip, const float* part_u,
+                                     sfl_stats_t* stats) {
   if (T == 0) return hipSuccess;
+  if (part_u && (val_f32 || out_mode != 0)) return hipErrorInvalidValue;
   if (d % (8 * SLICE2) != 0) return hipErrorInvalidValue;
   if (out_mode < 0 || out_mode > 2 || (out_mode > 0 && !Yf) || (out_mode != 1 && !Y)) return hipErrorInvalidValue;
   const int n_slices = (int)(d / SLICE2);
@@ -800,7 +833,8 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
       if (e != hipSuccess) return e;                                                                               \
     }                                                                                                              \
     hipLaunchKernelGGL((k_gather_down_b16<VK_, OUT_, U_, TG_>), grid, block, lds, s, T, d, f, K, ell_val, ell_idx, \
-                       row_nnz, row_ovf, (const bf16_t*)Wp, (bf16_t*)Y, Yf, n_slices, tpw, order, skip);           \
+                       row_nnz, row_ovf, (const bf16_t*)Wp, (bf16_t*)Y, Yf, n_slices, tpw, order, skip, part_u,    \
+                       stats);                                                                                     \
   } while (0)
 #define SFL_GATHER_LAUNCH_U(VK_, OUT_, U_) SFL_GATHER_LAUNCH_G(VK_, OUT_, U_, false)
 #define SFL_GATHER_LAUNCH(VK_, OUT_)                  \

@@ -928,10 +928,13 @@ __device__ __forceinline__ void splitk_store(const GemmParams& p, int m, int n, 
   }
 }
 
-// Sum of the ks partials of row m, columns n .. n+3, in split order.
-__device__ __forceinline__ f32x4_t splitk_sum(const GemmParams& p, int ks, int m_eff, int m, int n) {
-  f32x4_t v = *(const f32x4_t*)(p.part + (int64_t)m * p.N + n);
-  for (int sp = 1; sp < ks; ++sp) v += *(const f32x4_t*)(p.part + ((int64_t)sp * m_eff + m) * p.N + n);
+// Sum of the ks partials of row m, columns n .. n+3, in split order (from p.part, or from
+// the partial sums at `part`).
+__device__ __forceinline__ f32x4_t splitk_sum(const GemmParams& p, int ks, int m_eff, int m, int n,
+                                              const float* part = nullptr) {
+  if (!part) part = p.part;
+  f32x4_t v = *(const f32x4_t*)(part + (int64_t)m * p.N + n);
+  for (int sp = 1; sp < ks; ++sp) v += *(const f32x4_t*)(part + ((int64_t)sp * m_eff + m) * p.N + n);
   return v;
 }
 
@@ -961,6 +964,9 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(GemmParams p) {
 // adds them in split order and applies the epilogue, or, given tile counters, the last
 // block of each tile does (one launch instead of two, which is most of the cost of the
 // dense-backup GEMMs of a decode step when no row overflows).
+// EPI_GATED_PAIR: a tile is 128 columns of two products, W_gate^T rows (B, waves 0-3) and
+// the same W_up^T rows (B2, waves 4-7), with their partial sums in two halves of `part`;
+// the last block forms h = ReLU(g) * u for the tile.
 constexpr int FR_NS = 3;                            // stages in the ring
 constexpr int FR_AROWS = 64;                        // A rows per stage
 constexpr int FR_STAGE = (FR_AROWS + BN) * KC_BK;   // bf16 elements per stage (40 KB)
@@ -968,18 +974,22 @@ constexpr int FR_STAGE = (FR_AROWS + BN) * KC_BK;   // bf16 elements per stage (
 template <int EPI, int RB>
 __global__ __launch_bounds__(NTHR) void k_gemm_few_rows(GemmParams p) {
   __shared__ __attribute__((aligned(1024))) bf16_t smem[FR_NS * FR_STAGE];
+  constexpr bool PAIR = EPI == EPI_GATED_PAIR;
+  constexpr int TN = PAIR ? BN / 2 : BN;  // output columns per tile (of each product)
   const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
   if (m_eff <= 0) return;
   const int nk_all = (int)(p.K / KC_BK);
   const int ks = splitk_count(p.ksplit, p.part_rows, m_eff, p.N, nk_all);
-  const int tiles_n = (int)cdiv(p.N, BN);
+  const int tiles_n = (int)cdiv(p.N, TN);
   if ((int)blockIdx.x >= tiles_n * ks) return;
-  const int split = blockIdx.x % ks, n0 = (blockIdx.x / ks) * BN;
+  const int split = blockIdx.x % ks, n0 = (blockIdx.x / ks) * TN;
   const int kt0 = (int)((int64_t)nk_all * split / ks), kt1 = (int)((int64_t)nk_all * (split + 1) / ks);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const u32x4_t ra = rsrc_words(p.A, p.a_bytes);
-  const u32x4_t rb = rsrc_words(p.B, p.b_bytes);
+  // the gated pair's waves 4-7 load (and multiply) W_up^T rows
+  const bool second = PAIR && wave >= 4;
+  const u32x4_t rb = rsrc_words(second ? p.B2 : p.B, p.b_bytes);
   // one load instruction fills 8 rows: wave w loads A rows 8w .. 8w+7 and B rows
   // 32w + 8q .. +7 (q < 4); lane l writes row +l/8 at chunk position l%8
   uint32_t offa, offb[4];
@@ -993,7 +1003,7 @@ __global__ __launch_bounds__(NTHR) void k_gemm_few_rows(GemmParams p) {
   for (int q = 0; q < 4; ++q) {
     const int row = wave * 32 + q * 8 + (lane >> 3);
     const int c = kc_swz(row, lane & 7);
-    const int gb = n0 + row;
+    const int gb = n0 + (PAIR ? row & (TN - 1) : row);
     offb[q] = gb < p.N ? (uint32_t)(((int64_t)gb * p.ldb + c * 8) * 2) : kOOB;
   }
   auto lds_addr = [](const bf16_t* ptr) {
@@ -1039,33 +1049,82 @@ __global__ __launch_bounds__(NTHR) void k_gemm_few_rows(GemmParams p) {
     }
   }
   typedef AccGeo<32> G;
-  const int col = n0 + wave * 32 + G::col(lane);
+  // the gated pair's second product (W_up^T) keeps its partial sums after the first's
+  const int64_t half = (int64_t)ks * m_eff * p.N;
+  const int col = n0 + (PAIR ? wave & 3 : wave) * 32 + G::col(lane);
+  float* part = p.part + (second ? half : 0);
   if (col < p.N) {
 #pragma unroll
     for (int r = 0; r < RB; ++r)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const int row = r * 32 + G::row(i, lane);
-        if (row < m_eff) p.part[((int64_t)split * m_eff + row) * p.N + col] = acc[r][i];
+        if (row < m_eff) part[((int64_t)split * m_eff + row) * p.N + col] = acc[r][i];
       }
   }
   if (!p.tile_sem) return;
   // the last block of the tile to finish adds its ks partial sums (in split order) and
-  // applies the epilogue: every block's partial stores are visible device-wide before its
-  // counter increment, and the last block's loads come after it
+  // applies the epilogue. Every wave waits until its partial stores have completed, then
+  // the barrier; thread 0's device-scope release fence and counter increment follow, so
+  // the block's stores are visible device-wide before its count. The last block's acquire
+  // fence orders its loads after the count. (One release per block: on this GPU a
+  // device-scope release writes back the XCD's L2 and an acquire invalidates it, which a
+  // fence in every thread, or a full fence in every block, would repeat many times over.)
   __shared__ int last;
-  __threadfence();
+  __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt(0) expcnt(7) lgkmcnt(0): this wave's stores done
   __syncthreads();
-  if (threadIdx.x == 0) last = atomicAdd(&p.tile_sem[n0 / BN], 1) == ks - 1;
+  if (threadIdx.x == 0) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    last = __hip_atomic_fetch_add(&p.tile_sem[n0 / TN], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == ks - 1;
+  }
   __syncthreads();
   if (!last) return;
-  __threadfence();
-  const int n4 = min(BN, p.N - n0) / 4;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  // the epilogue of the tile's elements; with l1_stats, the sum of the stored |h| (the
+  // dense-backup rows' share of the L1 statistic) is added with one atomic per tile
+  const int n4 = min(TN, p.N - n0) / 4;
+  float l1 = 0.f;
   for (int e = threadIdx.x; e < m_eff * n4; e += NTHR) {
     const int m = e / n4, n = n0 + (e % n4) * 4;
-    splitk_store<EPI>(p, m, n, splitk_sum(p, ks, m_eff, m, n));
+    if constexpr (PAIR) {
+      // h = bf16(bf16(ReLU(g + bias + shift)) * u): the values of EPI_ACT_RELU on g
+      // followed by EPI_MUL_ACT with u, formed at once
+      const f32x4_t g = splitk_sum(p, ks, m_eff, m, n);
+      const f32x4_t u = splitk_sum(p, ks, m_eff, m, n, p.part + half);
+      const int64_t crow = p.c_rows ? (int64_t)p.c_rows[m] : (int64_t)m;
+      const float sh = p.shift ? p.shift[p.s_rows ? p.s_rows[m] : m] : 0.f;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float x = g[q];
+        if (p.bias) x += p.bias[n + q];
+        x += sh;
+        const bf16_t r = active_bits(x) ? f32_to_bf16(x) : (bf16_t)0;
+        const bf16_t h = f32_to_bf16(bf16_to_f32(r) * u[q]);
+        ((bf16_t*)p.C)[crow * p.ldc + n + q] = h;
+        l1 += fabsf(bf16_to_f32(h));
+      }
+    } else {
+      const f32x4_t v = splitk_sum(p, ks, m_eff, m, n);
+      splitk_store<EPI>(p, m, n, v);
+      if (EPI == EPI_ACT_RELU && p.l1_stats) {
+        const int64_t crow = p.c_rows ? (int64_t)p.c_rows[m] : (int64_t)m;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) l1 += bf16_to_f32(((const bf16_t*)p.C)[crow * p.ldc + n + q]);
+      }
+    }
   }
-  if (threadIdx.x == 0) p.tile_sem[n0 / BN] = 0;
+  if ((PAIR || EPI == EPI_ACT_RELU) && p.l1_stats) {
+    __shared__ float wl1[NTHR / 64];
+    l1 = wave_sum<float>(l1);
+    if (lane == 0) wl1[wave] = l1;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      float tot = 0.f;
+      for (int w = 0; w < NTHR / 64; ++w) tot += wl1[w];
+      if (tot != 0.f) atomicAdd(&p.l1_stats->l1_sum, (double)tot);
+    }
+  }
+  if (threadIdx.x == 0) p.tile_sem[n0 / TN] = 0;
 }
 
 // Compute units of the current device (cached per device; threads that race on the first
@@ -1230,6 +1289,35 @@ __global__ __launch_bounds__(256) void k_gemm_f32(GemmParams p) {
 }
 
 }  // namespace
+
+// The gated pair of few-rows GEMMs (EPI_GATED_PAIR): both operands K-contiguous, at most
+// 64 rows, tile counters and partial sums for both products given.
+bool gated_pair_ok(const GemmParams& p) {
+  return kc_ok(p, LAY_KC) && p.B2 && p.tile_sem && p.part && p.C && p.M <= FR_AROWS && p.N % 4 == 0 &&
+         p.part_rows >= 2 * FR_AROWS;
+}
+
+hipError_t launch_gated_pair(const GemmParams& p, hipStream_t s) {
+  if (!gated_pair_ok(p)) return hipErrorInvalidValue;
+  if (p.M == 0 || p.N == 0) return hipSuccess;
+  constexpr int TN = BN / 2;
+  GemmParams q = p;
+  q.ksplit = std::max(1, device_cus() / (int)cdiv(p.N, TN));
+  q.part_rows = p.part_rows / 2;  // each product's partial sums take half of `part`
+  const int nk = (int)(p.K / KC_BK);
+  // the device's split count for m_eff <= M rows is at least the one for M; the grid covers
+  // the largest (m_eff = 1), and blocks past the device's count return
+  const unsigned grid = (unsigned)(cdiv(p.N, TN) * splitk_count(q.ksplit, q.part_rows, p.m_count ? 1 : p.M, p.N, nk));
+  if (q.M <= 32) hipLaunchKernelGGL((k_gemm_few_rows<EPI_GATED_PAIR, 1>), dim3(grid), dim3(NTHR), 0, s, q);
+  else hipLaunchKernelGGL((k_gemm_few_rows<EPI_GATED_PAIR, 2>), dim3(grid), dim3(NTHR), 0, s, q);
+  return hipGetLastError();
+}
+
+// Whether gemm_bf16 runs p (bf16, K-contiguous A, counted rows allowed) as the few-rows
+// split-K GEMM whose last blocks apply the epilogue (and then add l1_stats, if set).
+bool few_rows_tile_epilogue(const GemmParams& p, int blay) {
+  return kc_ok(p, blay) && p.ksplit > 1 && p.part && p.N % 4 == 0 && p.tile_sem && few_rows_split(p, blay) > 1;
+}
 
 hipError_t gemm_bf16(int alay, int blay, int epi, const GemmParams& p, hipStream_t s) {
   const bool kcb = alay == LAY_KC && kc_ok(p, blay);

@@ -24,6 +24,7 @@ enum Epilogue {
   EPI_ACCUM_F32 = 5,   // C_f32[crow][n] += acc
   EPI_MUL_ACT = 6,     // C_act[crow][n] = C_act[crow][n] * acc (gated h = ReLU(g) * u)
   EPI_TWELL_P32 = 7,   // EPI_TWELL into the packed 32-bit layout (tw_val words; S = 31)
+  EPI_GATED_PAIR = 8,  // few-rows split-K only: C_act[crow][n] = ReLU(A B^T + bias + shift) * (A B2^T)
 };
 
 // Persistent tile orders of the 256 x 256 GEMMs.
@@ -77,6 +78,11 @@ struct GemmParams {
   int32_t* tile_sem;
   // order in which output tiles are dealt (TileOrder)
   int tile_order;
+  // EPI_GATED_PAIR: the second B operand (W_up^T beside B = W_gate^T, same shape)
+  const void* B2;
+  // few-rows split-K with tile counters, EPI_ACT_RELU or EPI_GATED_PAIR: the sum of the
+  // stored |values| is added to l1_stats->l1_sum (one float64 atomic per tile)
+  sfl_stats_t* l1_stats;
 };
 
 // bf16 MFMA GEMM. Requirements: K % 8 == 0; RC layouts need even M/N extents and
@@ -86,6 +92,15 @@ hipError_t gemm_bf16(int alay, int blay, int epi, const GemmParams& p, hipStream
 // partial sums to part [ks][M][N] (and, with no_reduce, stops there), 1 when its
 // epilogue writes C directly.
 int gemm_split_count(int alay, int blay, const GemmParams& p);
+// The gated dense-backup rows of at most 64 rows in one launch (EPI_GATED_PAIR: B = W_gate^T,
+// B2 = W_up^T, K-contiguous; tile_sem zeroed beforehand; part holds part_rows rows of N
+// floats, half for each product); gated_pair_ok tells whether it applies.
+bool gated_pair_ok(const GemmParams& p);
+hipError_t launch_gated_pair(const GemmParams& p, hipStream_t s);
+// Whether gemm_bf16 runs p as the few-rows split-K GEMM whose last blocks apply the epilogue
+// (and add the stored |values| to l1_stats for EPI_ACT_RELU).
+bool few_rows_tile_epilogue(const GemmParams& p, int blay);
+
 // fp32 FMA GEMM for the F32 dtype (A MK, B KN only; any sizes).
 hipError_t gemm_f32(int epi, const GemmParams& p, hipStream_t s);
 
@@ -110,9 +125,9 @@ hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int tile_cols, in
                            sfl_stats_t* stats, hipStream_t s, int l1_vals = 1, bool packed = false);
 // Ascending dense-backup row list + n_ovf + capacity flag (one workgroup).
 hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32_t* ovf_rows,
-                           int32_t* n_ovf, sfl_stats_t* stats, hipStream_t s,
-                           int32_t* zero = nullptr, int n_zero = 0);
-hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s);
+                           int32_t* n_ovf, sfl_stats_t* stats, hipStream_t s);
+// Zeroes the statistics (if given) and n_zero counters from zero.
+hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s, int32_t* zero = nullptr, int n_zero = 0);
 // order[0 .. T): the sparse rows by descending row_nnz, then the dense-backup rows (one
 // workgroup, counting sort over K + 2 buckets; order within a bucket unspecified). Fails
 // with hipErrorInvalidValue when K + 2 buckets do not fit the kernel's LDS histogram.
@@ -142,11 +157,15 @@ hipError_t launch_gather_down(int val_bf16, int64_t T, int64_t d, int ell_width,
                               const uint8_t* row_ovf, const void* W, void* Y, hipStream_t s);
 // bf16, d % 512 == 0: same sum from the slice-major copy of W_down (persistent, XCD-aware).
 // out_mode 0: bf16 Y; 1: fp32 Yf; 2: bf16 Y of (sum + Yf) (val_f32 only for 1 and 2).
+// With part_u (bf16 values, out_mode 0; the gated layer): the values are
+// h = bf16(ell_val * sum_x part_u[x][t][e]), formed while staging the entries as
+// launch_gated_h forms them, and |h| is added to stats->l1_sum (if given).
 hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int ell_width, const void* ell_val,
                                      const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
                                      const void* W_packed, void* Y, hipStream_t s,
                                      int val_f32 = 0, int out_mode = 0, float* Yf = nullptr,
-                                     const int32_t* order = nullptr, const int32_t* skip = nullptr);
+                                     const int32_t* order = nullptr, const int32_t* skip = nullptr,
+                                     const float* part_u = nullptr, sfl_stats_t* stats = nullptr);
 // Gated backward at the ELL entries: dh (8 partials + lambda' sign(g u)) -> dh_u, dh_g, h.
 hipError_t launch_gated_entry_grads(int64_t T, int K, const void* ell_val, const int32_t* row_nnz,
                                     const uint8_t* row_ovf, const float* part, const float* u, float lam, float* dhu,

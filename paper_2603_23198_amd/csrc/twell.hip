@@ -20,44 +20,35 @@ __device__ __forceinline__ bool is_active(float z) {
   return b > 0 && b <= 0x7f800000;
 }
 
-// One wave per (row, tile): 64 columns per step, ballot + mbcnt give each active lane its
-// slot (running count + active lanes below it), so slots follow ascending column order.
-// With ks > 0, z comes from ks split-K partial sums part[s][t][n] (Z is then the partial
-// array, ks * T * f floats): their sum in split order, plus bias[n], plus shift[t].
-// Packed 32-bit layout (PK): the (row, tile) pair's 32 words hold its true count in word 0
-// and, in word 1 + s, the s-th active entry as column | bf16 value << 16 (s < 31); V is
-// bf16 then, and `val` points to the words.
-template <typename V, bool PK = false>
-__global__ __launch_bounds__(256) void k_pack_twell(const float* __restrict__ Z, int64_t T, int64_t f,
-                                                    int Tn, int S, int NT, V* __restrict__ val,
-                                                    uint16_t* __restrict__ idx, int32_t* __restrict__ cnt, int ks,
-                                                    const float* __restrict__ bias, const float* __restrict__ shift) {
-  const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (w >= T * NT) return;
-  const int l = threadIdx.x & 63;
-  const int64_t t = w / NT;
-  const int j = (int)(w - t * NT);
-  const int64_t c0 = (int64_t)j * Tn;
-  const int64_t c1 = c0 + Tn < f ? c0 + Tn : f;
-  const float* zr = Z + t * f;
-  const int64_t base = t * (int64_t)NT * S + (int64_t)j * S;
-  uint32_t* words = PK ? (uint32_t*)val + w * 32 : nullptr;  // w = t NT + j
+// One wave packs columns c0 .. c1-1 of one row into that row's TwELL entry for the tile
+// (Alg. 1): z is zr[col], or with ks > 0 the sum of ks split-K partial sums
+// zr[sp * sstride + col] in split order, plus bias[col] (if given), plus sh. 64 columns per
+// step; ballot + mbcnt give each active lane its slot (running count + active lanes below
+// it), so slots follow ascending column order; slots from S on are counted, not stored.
+// Planes: val[base + s], idx[base + s] and the count to *cnt. Packed 32-bit layout (PK):
+// words[1 + s] = column | bf16 value << 16 and the count in words[0]. Called by all 64
+// lanes of the wave.
+template <typename V, bool PK>
+__device__ __forceinline__ void pack_row_tile(const float* __restrict__ zr, int64_t sstride, int ks,
+                                              const float* __restrict__ bias, float sh, int64_t c0, int64_t c1,
+                                              int S, V* __restrict__ val, uint16_t* __restrict__ idx, int64_t base,
+                                              int32_t* __restrict__ cnt, uint32_t* __restrict__ words) {
+  const int l = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0));
   int running = 0;
-  const float sh = (ks > 0 && shift) ? shift[t] : 0.f;
   for (int64_t c = c0; c < c1; c += 64) {
     const int64_t col = c + l;
     float z = 0.f;
     if (col < c1) {
       z = zr[col];
       if (ks > 0) {
-        for (int sp = 1; sp < ks; ++sp) z += zr[(int64_t)sp * T * f + col];
+        for (int sp = 1; sp < ks; ++sp) z += zr[(int64_t)sp * sstride + col];
         if (bias) z += bias[col];
         z += sh;
       }
     }
     const bool act = col < c1 && is_active(z);
-    const uint64_t m = ballot(act);
-    const int slot = running + mbcnt(m);
+    const uint64_t m = __ballot(act);
+    const int slot = running + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
     if (act && slot < S) {
       if constexpr (PK) {
         words[1 + slot] = (uint32_t)col | ((uint32_t)f32_to_bf16(z) << 16);
@@ -70,8 +61,29 @@ __global__ __launch_bounds__(256) void k_pack_twell(const float* __restrict__ Z,
   }
   if (l == 0) {
     if constexpr (PK) words[0] = (uint32_t)running;
-    else cnt[t * NT + j] = running;
+    else *cnt = running;
   }
+}
+
+// One wave per (row, tile). With ks > 0, z comes from ks split-K partial sums
+// part[s][t][n] (Z is then the partial array, ks * T * f floats): their sum in split
+// order, plus bias[n], plus shift[t]. Packed 32-bit layout (PK): the (row, tile) pair's 32
+// words hold its true count in word 0 and, in word 1 + s, the s-th active entry as
+// column | bf16 value << 16 (s < 31); V is bf16 then, and `val` points to the words.
+template <typename V, bool PK = false>
+__global__ __launch_bounds__(256) void k_pack_twell(const float* __restrict__ Z, int64_t T, int64_t f,
+                                                    int Tn, int S, int NT, V* __restrict__ val,
+                                                    uint16_t* __restrict__ idx, int32_t* __restrict__ cnt, int ks,
+                                                    const float* __restrict__ bias, const float* __restrict__ shift) {
+  const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (w >= T * NT) return;
+  const int64_t t = w / NT;
+  const int j = (int)(w - t * NT);
+  const int64_t c0 = (int64_t)j * Tn;
+  const int64_t c1 = c0 + Tn < f ? c0 + Tn : f;
+  const float sh = (ks > 0 && shift) ? shift[t] : 0.f;
+  pack_row_tile<V, PK>(Z + t * f, T * f, ks, bias, sh, c0, c1, S, val, idx, t * (int64_t)NT * S + (int64_t)j * S,
+                       cnt + w, PK ? (uint32_t*)val + w * 32 : nullptr);  // w = t NT + j
 }
 
 hipError_t launch_pack_twell(const float* Z, int64_t T, int64_t f, int val_bf16, int Tn, int S,
@@ -326,8 +338,8 @@ hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int Tn, int S, in
   return hipGetLastError();
 }
 
-__global__ void k_stats_init(sfl_stats_t* stats) {
-  if (threadIdx.x == 0) {
+__global__ __launch_bounds__(256) void k_stats_init(sfl_stats_t* stats, int32_t* zero, int n_zero) {
+  if (stats && threadIdx.x == 0) {
     stats->total_nnz = 0;
     stats->n_ovf_rows = 0;
     stats->n_tile_ovf = 0;
@@ -335,11 +347,13 @@ __global__ void k_stats_init(sfl_stats_t* stats) {
     stats->capacity_exceeded = 0;
     stats->reserved = 0;
   }
+  for (int i = threadIdx.x; i < n_zero; i += 256) zero[i] = 0;
 }
 
-hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s) {
-  if (!stats) return hipSuccess;
-  hipLaunchKernelGGL(k_stats_init, dim3(1), dim3(64), 0, s, stats);
+hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s, int32_t* zero, int n_zero) {
+  if (!zero) n_zero = 0;
+  if (!stats && n_zero == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_stats_init, dim3(1), dim3(256), 0, s, stats, zero, n_zero);
   return hipGetLastError();
 }
 
@@ -396,14 +410,11 @@ hipError_t launch_nnz_order(int64_t T, int K, const int32_t* row_nnz, const uint
 // An exclusive scan of the threads' counts (wave scans + a scan of the 16 wave totals)
 // places each thread's rows, in ascending row order.
 constexpr int kOvfRowsPerThread = 16;
-// It also zeroes n_zero ints at `zero` (counters the later stages start from).
 __global__ __launch_bounds__(1024) void k_ovf_list(int64_t T, int32_t cap, const uint8_t* __restrict__ row_ovf,
                                                    int32_t* __restrict__ ovf_rows, int32_t* __restrict__ n_ovf,
-                                                   sfl_stats_t* __restrict__ stats, int32_t* __restrict__ zero,
-                                                   int n_zero) {
+                                                   sfl_stats_t* __restrict__ stats) {
   __shared__ int wsum[16];
   const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
-  for (int i = tid; i < n_zero; i += 1024) zero[i] = 0;
   int64_t base = 0;
   for (int64_t r0 = 0; r0 < T; r0 += 1024 * kOvfRowsPerThread) {
     const int64_t t0 = r0 + (int64_t)tid * kOvfRowsPerThread;
@@ -437,9 +448,8 @@ __global__ __launch_bounds__(1024) void k_ovf_list(int64_t T, int32_t cap, const
 }
 
 hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32_t* ovf_rows, int32_t* n_ovf,
-                           sfl_stats_t* stats, hipStream_t s, int32_t* zero, int n_zero) {
-  hipLaunchKernelGGL(k_ovf_list, dim3(1), dim3(1024), 0, s, T, cap, row_ovf, ovf_rows, n_ovf, stats, zero,
-                     zero ? n_zero : 0);
+                           sfl_stats_t* stats, hipStream_t s) {
+  hipLaunchKernelGGL(k_ovf_list, dim3(1), dim3(1024), 0, s, T, cap, row_ovf, ovf_rows, n_ovf, stats);
   return hipGetLastError();
 }
 

@@ -96,16 +96,16 @@ def test_workspace_sizes():
     big = _fake_args(b.SFL_BF16, 512, 256, 1024, ell_width=16, ovf_capacity=64)
     big.twell.ovf_dense = 0x2000
     # partial sums: 512 rows (T); a capacity of at most 64 rows adds one counter per
-    # 256-column tile of the wider of f and d
-    assert b.sfl_workspace_size(big, 0) == 512 * 1024 * 4 + _need_lists(64) + _al(4 * (1 + 4))
+    # 128-column tile of the wider of f and d
+    assert b.sfl_workspace_size(big, 0) == 512 * 1024 * 4 + _need_lists(64) + _al(4 * (1 + 8))
     wide = _fake_args(b.SFL_BF16, 512, 70016, 1024, ell_width=16, ovf_capacity=64)
     wide.twell.ovf_dense = 0x2000
-    assert b.sfl_workspace_size(wide, 0) == 512 * 70016 * 4 + _need_lists(64) + _al(4 * (1 + 274))
+    assert b.sfl_workspace_size(wide, 0) == 512 * 70016 * 4 + _need_lists(64) + _al(4 * (1 + 547))
     # an ELL width of at least f / 32 makes the call a dense-fallback candidate: the
     # workspace adds the dense ReLU rows H [T][f] bf16 and two flags
     dense = _fake_args(b.SFL_BF16, 512, 256, 1024, ell_width=32, ovf_capacity=64)
     dense.twell.ovf_dense = 0x2000
-    assert b.sfl_workspace_size(dense, 0) == 512 * 1024 * 4 + _need_lists(64) + _al(4 * (1 + 4)) + 512 * 1024 * 2 + _al(8)
+    assert b.sfl_workspace_size(dense, 0) == 512 * 1024 * 4 + _need_lists(64) + _al(4 * (1 + 8)) + 512 * 1024 * 2 + _al(8)
     # dense baseline: H, then split-K partials for a GEMM whose 256 x 256 tiles fill at most
     # half of the CUs (here the down GEMM, K = 1024: four ranges of 256) -- at most 8 splits,
     # 256 of K each, items within one block per CU, 64 MiB of partial sums

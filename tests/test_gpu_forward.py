@@ -253,11 +253,20 @@ def test_bias_and_shift_in_the_fused_epilogue(T, f, Tn, S, use_wupt):
 def test_small_batch_dense_backup_rows(T, gated, copies):
     """Batches of at most 64 rows with dense-backup rows (half the rows all active): with
     K-contiguous weight copies their GEMMs split K without a reduction kernel (the last
-    block of each tile adds the partial sums, counted with per-tile counters). Two calls in
-    a row, so the second starts from the counters the first left behind."""
+    block of each tile adds the partial sums, counted with per-tile counters); the gated
+    layer's two products then run as one launch whose last blocks form h = ReLU(g) * u.
+    Each dense-backup row of h against the oracle's (two bf16 roundings, fp32 sums: 1e-2
+    per row), and Y. Two calls in a row, so the second starts from the counters the first
+    left behind."""
     w = wl.make_ffn("small-ovf", "bf16", T, 1024, 2048, seed=T + 2 * gated, gated=gated, sparsity=0.97,
                     ell_width=128)
     w.shift_t[::2] = 100.0
+    X = w.as_f64(w.X)
+    if gated:
+        _, _, _, H = ffn.ffn_gated_dense(X, w.as_f64(w.W_gate), w.as_f64(w.W_up), w.as_f64(w.W_down), w.bias_f,
+                                         w.shift_t)
+    else:
+        _, _, H = ffn.ffn_dense(X, w.as_f64(w.W_up), w.as_f64(w.W_down), w.bias_f, w.shift_t)
     Yref, _ = oracle_rows(w, np.arange(T))
     for _ in range(2):
         Y, bufs, stats, cfg = run_forward(w, use_wupt=copies, use_wgatet=copies and gated, use_wdownt=copies)
@@ -266,15 +275,24 @@ def test_small_batch_dense_backup_rows(T, gated, copies):
         assert rel_l2(to_f64(Y), Yref) <= 2e-2
         ovf = np.nonzero(got["row_ovf"])[0]
         assert rel_l2(to_f64(Y)[ovf], Yref[ovf]) <= 2e-2
+        np.testing.assert_array_equal(got["ovf_rows"][:len(ovf)], ovf)
+        dense_rows = to_f64(bufs["ovf_dense"])[:len(ovf) * w.f].reshape(len(ovf), w.f)
+        for i, t in enumerate(ovf):
+            assert rel_l2(dense_rows[i], H[t]) <= 1e-2, (i, t)
 
 
-@pytest.mark.parametrize("T", [1, 17, 48, 64])
-def test_small_batch_split_gemm(T):
+@pytest.mark.parametrize("T,Tn,f", [(1, 256, 2048), (17, 256, 2048), (48, 256, 2048), (64, 256, 2048),
+                                    (17, 64, 2048), (64, 128, 2048), (40, 64, 2048), (33, 128, 1984)])
+def test_small_batch_split_gemm(T, Tn, f):
     """Batches of at most 64 rows with K-contiguous weights take the split-K GEMMs (K
-    ranges over blocks, partial sums reduced in split order): Z against the fp64 oracle,
-    the forward's TwELL bit-identical to the oracle's extraction from that Z, Y of the
-    sparse forward and of the dense baseline against the oracle."""
-    w = wl.make_ffn("skinny", "bf16", T, 1024, 2048, seed=T, sparsity=0.97, ell_width=128)
+    ranges over blocks, partial sums reduced in split order, by the TwELL pack in the
+    forward): Z against the fp64 oracle, the forward's TwELL bit-identical to the oracle's
+    extraction from that Z
+    (TwELL tiles of 64, 128 and 256 columns; f = 1984 ends in a partial 256-column GEMM tile
+    and a partial TwELL tile), Y of the sparse forward and of the dense baseline against
+    the oracle."""
+    w = wl.make_ffn("skinny", "bf16", T, 1024, f, seed=T + Tn, sparsity=0.97, tile_cols=Tn,
+                    tile_slots=min(32, Tn), ell_width=128)
     X, Wu, Wd = dev(w.X), dev(w.W_up), dev(w.W_down)
     WupT = transposed(Wu)
     cfg = b.make_cfg(**w.cfg)

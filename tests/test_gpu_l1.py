@@ -60,11 +60,12 @@ def check_l1(st, w, H, rows=None):
     assert abs(got - want) <= RTOL * want, (got, want, got / want)
 
 
-@pytest.mark.parametrize("T,copies", [(700, False), (700, True), (200, True), (200, False)])
+@pytest.mark.parametrize("T,copies", [(700, False), (700, True), (200, True), (200, False), (48, True), (48, False)])
 def test_l1_non_gated_with_both_kinds_of_dense_backup_rows(T, copies):
     """Non-gated: sparse rows (the TwELL values summed by the classification) and dense-backup
     rows; above 256 tokens some are rebuilt from the slabs and some recomputed by the GEMM,
-    at or below 256 tokens all are recomputed (with W_up^T, through the split-K GEMM)."""
+    at or below 256 tokens all are recomputed (with W_up^T, through the split-K GEMM; at
+    most 64 rows, whose last blocks sum the rows they store)."""
     w = wl.make_ffn("l1", "bf16", T, 512, 2048, seed=31 + T, sparsity_rows=mixed_rows(T, T), ell_width=64)
     Y, bufs, stats, cfg = run_forward(w, use_wupt=copies, use_wdownt=copies)
     st = b.read_stats(stats)
