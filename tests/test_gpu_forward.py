@@ -543,6 +543,54 @@ def test_decode_forward_replays_from_a_hip_graph():
     assert rel_l2(to_f64(Y), Yref) <= 2e-2
 
 
+@pytest.mark.parametrize("gated", [False, True])
+def test_prefill_forward_replays_from_a_hip_graph(gated):
+    """A forward above 256 tokens with dense-backup rows of both kinds (rebuilt from the
+    slabs and recomputed through the need list, whose counter the first kernel zeroes): the
+    eager call against the oracle, a second eager call equal to the first bit for bit, and
+    the forward captured in a HIP graph replaying to the same bits, with eager work between
+    replays."""
+    T = 600
+    sr = np.full(T, 0.99)
+    sr[::7] = 0.5    # half of the units active: overflowing tiles, recomputed by the GEMM
+    sr[3::7] = 0.95  # more than K = 64 active units but no tile over S: rebuilt from the slabs
+    w = wl.make_ffn("fork", "bf16", T, 512, 2048, seed=5 + gated, gated=gated, sparsity_rows=sr, ell_width=64)
+    X, Wu, Wd = dev(w.X), dev(w.W_up), dev(w.W_down)
+    Wg = dev(w.W_gate) if gated else None
+    cfg = b.make_cfg(**w.cfg)
+    bufs = b.alloc_twell(w.T, w.f, "bf16", cfg)
+    Y = torch.zeros((w.T, w.d), dtype=torch.bfloat16, device="cuda")
+    kw = dict(Y=Y, bufs=bufs, W_gate=Wg, W_upT=transposed(Wu), W_gateT=transposed(Wg) if gated else None,
+              W_downT=transposed(Wd), shift_t=dev(w.shift_t))
+    ws = torch.empty(max(1, b.sfl_workspace_size(b.ffn_args(X, Wu, Wd, cfg, **kw))), dtype=torch.uint8, device="cuda")
+    args = b.ffn_args(X, Wu, Wd, cfg, **kw, workspace=ws)
+    b.sfl_ffn_forward(args)
+    torch.cuda.synchronize()
+    Yeager = Y.clone()
+    got = twell_views(bufs, T, w.f, cfg)
+    tile_ovf = (got["cnt"] > cfg.tile_slots).any(axis=1)
+    assert got["n_ovf"] == 2 * len(range(0, T, 7)) and 0 < tile_ovf.sum() < got["n_ovf"]
+    Yref, _ = oracle_rows(w, np.arange(T))
+    assert rel_l2(to_f64(Y), Yref) <= 2e-2
+    ovf = np.nonzero(got["row_ovf"])[0]
+    assert rel_l2(to_f64(Y)[ovf], Yref[ovf]) <= 2e-2
+    Y.fill_(float("nan"))
+    b.sfl_ffn_forward(args)
+    torch.cuda.synchronize()
+    assert torch.equal(Y.view(torch.int16), Yeager.view(torch.int16))
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        b.sfl_ffn_forward(args, torch.cuda.current_stream())
+    for i in range(3):
+        Y.fill_(float("nan"))
+        bufs["row_nnz"].fill_(-1)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(Y.view(torch.int16), Yeager.view(torch.int16)), i
+        _ = (X.float() @ X.float().t()).sum().item()  # unrelated eager work between replays
+
+
 def test_c4_headline_in_the_bench_configuration():
     """The headline workload as bench.py launches it: W_up^T and W_down^T copies, slice-major
     W_down; sampled rows and their patterns against the oracle, and the dense baseline."""
