@@ -330,7 +330,13 @@ sfl_status_t sfl_workspace_size(const void* args, int backward, size_t* bytes);
  * epilogue (Alg. 1), hybrid classification (Sec. 3.4), sparse down projection
  * of the ELL rows (Alg. 3's sparse part; Alg. 2 fused up and down when gated)
  * and the dense path for the dense-backup rows (Alg. 3's dense part).
- * bf16: d % 64 == 0 and f % 64 == 0; fp32: any sizes. */
+ * bf16: d % 64 == 0 and f % 64 == 0; fp32: any sizes.
+ * Size limit: the kernels address each operand with 32-bit byte offsets, so X
+ * [T][d], the weights [d][f] and the activations [T][f] must each be below 2 GiB
+ * in the activation dtype, and so must the TwELL slabs (T x ceil(f / tile_cols) x
+ * tile_slots x 2 bytes, or x 128 bytes for the packed layout); larger requests
+ * return SFL_E_UNSUPPORTED (bf16 at f = 16384: T < 65536). Rows are independent,
+ * so a larger batch is run as row chunks of at most that size. */
 sfl_status_t sfl_ffn_forward(const sfl_ffn_args_t* args, sfl_stream_t stream);
 
 /* Bytes of the device scratch array that sfl_ffn_forward_noalloc uses as its workspace

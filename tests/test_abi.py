@@ -117,6 +117,17 @@ def test_workspace_sizes():
         assert b.sfl_workspace_size(g, 2) == _al(T * f * 2) + _al(parts * 4), (T, d, f)
 
 
+def test_size_limit_of_32_bit_offsets():
+    """The documented limit: each operand below 2 GiB (bf16 at f = 16384: T < 65536)."""
+    ok = _fake_args(b.SFL_BF16, 65535, 4096, 16384, ell_width=256)
+    assert b.sfl_workspace_size(ok, 0) > 0
+    for T, d, f in [(65536, 4096, 16384), (1024, 65536, 16384), (262144, 4096, 4096)]:
+        big = _fake_args(b.SFL_BF16, T, d, f, ell_width=256)
+        with pytest.raises(b.SflError) as e:
+            b.sfl_workspace_size(big, 0)
+        assert e.value.code == b.SFL_E_UNSUPPORTED, (T, d, f)
+
+
 def test_unsupported_shapes_and_missing_pointers():
     a = _fake_args(b.SFL_BF16, 128, 200, 1024)
     with pytest.raises(b.SflError) as e:
