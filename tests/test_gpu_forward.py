@@ -9,7 +9,7 @@ import pytest
 import torch
 
 import workloads as wl
-from oracle import ffn, twell
+from oracle import bf16, ffn, twell
 from tests.gpu_util import assert_twell_equal, dev, host_bits, rel_l2, to_f64, twell_views
 
 pytestmark = pytest.mark.gpu
@@ -180,6 +180,48 @@ def test_fused_twell_equals_pack_of_same_mainloop(T, f, Tn, S, use_wupt):
     rows = sample_rows(T, 64, 3)
     Yref, _ = oracle_rows(w, rows)
     assert rel_l2(to_f64(Y)[rows], Yref) <= 2e-2
+
+
+@pytest.mark.parametrize("Tn,S,packed", [(256, 32, False), (128, 16, False), (64, 8, False), (256, 31, True)])
+def test_rebuilt_dense_backup_rows_bit_exact(Tn, S, packed):
+    """Above 256 tokens the dense-backup rows whose tiles all kept their values are rebuilt
+    from the TwELL slabs: each equals the oracle's bf16 ReLU of the float32 pre-activations
+    of the same main loop (sfl_up_projection), bit for bit, for three TwELL tile widths and
+    the packed 32-bit layout. The rows with an overflowing tile are recomputed by the
+    split-K GEMM (another summation order): within 1e-2 per row of the same values."""
+    T, f = 600, 2048
+    sr = np.full(T, 0.99)
+    sr[::7] = 0.5    # overflowing tiles
+    sr[3::7] = 0.95  # more than K active units, no tile over S
+    w = wl.make_ffn("rebuild", "bf16", T, 512, f, seed=Tn + S, sparsity_rows=sr, tile_cols=Tn, tile_slots=S,
+                    ell_width=64)
+    if packed:
+        w.cfg["layout"] = b.SFL_TWELL_PACKED32
+    Y, bufs, stats, cfg = run_forward(w, use_wupt=True)
+    X, Wu = dev(w.X), dev(w.W_up)
+    Z = torch.empty((T, f), dtype=torch.float32, device="cuda")
+    kw = dict(shift_t=dev(w.shift_t), W_upT=transposed(Wu))
+    ws = torch.empty(max(1, b.sfl_workspace_size(b.ffn_args(X, Wu, dev(w.W_down), cfg, **kw), 0)), dtype=torch.uint8,
+                     device="cuda")
+    b.sfl_up_projection(b.ffn_args(X, Wu, dev(w.W_down), cfg, **kw, workspace=ws), Z)
+    torch.cuda.synchronize()
+    Zn = Z.cpu().numpy()
+    tw = twell.extract_twell(Zn, Tn, S, "bf16")
+    hy = twell.classify(tw, cfg.ell_width)
+    n = int(host_bits(bufs["n_ovf"])[0])
+    rows = host_bits(bufs["ovf_rows"])[:n]
+    np.testing.assert_array_equal(rows, hy.ovf_rows)
+    tile_over = (tw.cnt > S).any(axis=1)
+    assert 0 < tile_over[rows].sum() < n  # both kinds of dense-backup row
+    got = host_bits(bufs["ovf_dense"])[:n * f].reshape(n, f)
+    zr = Zn[rows].astype(np.float64)
+    want = np.where(zr > 0, bf16.to_bf16_bits(zr), np.uint16(0))
+    rebuilt = ~tile_over[rows]
+    np.testing.assert_array_equal(got[rebuilt], want[rebuilt])
+    for i in np.nonzero(~rebuilt)[0]:
+        assert rel_l2(bf16.from_bf16_bits(got[i]), bf16.from_bf16_bits(want[i])) <= 1e-2, rows[i]
+    Yref, _ = oracle_rows(w, np.arange(T))
+    assert rel_l2(to_f64(Y)[rows], Yref[rows]) <= 2e-2
 
 
 @pytest.mark.parametrize("order", ["grouped", "hilbert"])
