@@ -323,8 +323,17 @@ sfl_status_t sfl_pack_twell(const float* Z, int64_t T, int64_t f, sfl_dtype_t va
 
 /* Workspace bytes needed by sfl_ffn_forward (backward = 0), sfl_ffn_backward
  * (backward = 1, args must point to an sfl_ffn_bwd_args_t) or
- * sfl_dense_ffn_baseline (backward = 2). */
+ * sfl_dense_ffn_baseline (backward = 2). The untyped form of the two typed
+ * queries below, which return the same sizes. */
 sfl_status_t sfl_workspace_size(const void* args, int backward, size_t* bytes);
+
+/* Workspace bytes of sfl_ffn_forward (dense = 0) or sfl_dense_ffn_baseline
+ * (dense = 1) for these arguments (the output pointers are not needed). Errors as
+ * the call itself would report them for the sizes and configuration. */
+sfl_status_t sfl_forward_workspace_size(const sfl_ffn_args_t* args, int32_t dense, size_t* bytes);
+
+/* Workspace bytes of sfl_ffn_backward for these arguments. */
+sfl_status_t sfl_backward_workspace_size(const sfl_ffn_bwd_args_t* args, size_t* bytes);
 
 /* Sparse FFN forward: up (or gate) projection GEMM with the ReLU -> TwELL
  * epilogue (Alg. 1), hybrid classification (Sec. 3.4), sparse down projection
@@ -371,9 +380,13 @@ sfl_status_t sfl_up_projection(const sfl_ffn_args_t* args, float* Z, sfl_stream_
 /* Sparse FFN backward (see sfl_ffn_bwd_args_t). BF16 only. */
 sfl_status_t sfl_ffn_backward(const sfl_ffn_bwd_args_t* args, sfl_stream_t stream);
 
-/* The library's dense FFN on the same arguments (comparator): GEMM with a ReLU
- * epilogue writing dense H [T][f] into the workspace, then GEMM with W_down
- * (three GEMMs when gated). Ignores args->twell and args->stats. */
+/* The library's dense FFN on the same arguments (comparator), the layer as the
+ * paper defines it before any sparsity: y = ReLU(x W_up) W_down (eq.
+ * secC:eq:non-gated-mlp) or y = (ReLU(x W_gate) * (x W_up)) W_down (eq.
+ * sec2:eq:gated-mlp), with the same optional bias and shift as sfl_ffn_forward. A
+ * GEMM with a ReLU epilogue writes dense H [T][f] (bf16 or fp32) into the
+ * workspace, then a GEMM with W_down (three GEMMs when gated). Ignores args->twell
+ * and args->stats. */
 sfl_status_t sfl_dense_ffn_baseline(const sfl_ffn_args_t* args, sfl_stream_t stream);
 
 /* Slice-major copy of a bf16 W_down [f][d] for the sparse down projection:

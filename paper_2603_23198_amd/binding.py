@@ -29,7 +29,7 @@ EXPORTED = ["sfl_status_string", "sfl_version", "sfl_twell_buffer_sizes", "sfl_p
             "sfl_workspace_size", "sfl_ffn_forward", "sfl_up_projection", "sfl_ffn_backward",
             "sfl_dense_ffn_baseline", "sfl_transpose", "sfl_pack_down_weights", "sfl_track_active_units",
             "sfl_reinit_dead_units", "sfl_ffn_forward_noalloc", "sfl_bandwidth_probe",
-            "sfl_down_projection_rowwise"]
+            "sfl_down_projection_rowwise", "sfl_forward_workspace_size", "sfl_backward_workspace_size"]
 
 
 class SflError(RuntimeError):
@@ -84,6 +84,8 @@ _lib.sfl_version.restype = c_char_p
 _lib.sfl_twell_buffer_sizes.argtypes = [c_int64, c_int64, c_int, POINTER(Cfg), POINTER(c_size_t)]
 _lib.sfl_pack_twell.argtypes = [c_void_p, c_int64, c_int64, c_int, POINTER(Cfg), POINTER(Twell), c_void_p, c_void_p]
 _lib.sfl_workspace_size.argtypes = [c_void_p, c_int, POINTER(c_size_t)]
+_lib.sfl_forward_workspace_size.argtypes = [POINTER(FfnArgs), c_int32, POINTER(c_size_t)]
+_lib.sfl_backward_workspace_size.argtypes = [POINTER(BwdArgs), POINTER(c_size_t)]
 _lib.sfl_ffn_forward.argtypes = [POINTER(FfnArgs), c_void_p]
 _lib.sfl_ffn_forward_noalloc.argtypes = [POINTER(FfnArgs), c_void_p]
 _lib.sfl_down_projection_rowwise.argtypes = [POINTER(FfnArgs), c_int32, c_void_p]
@@ -220,6 +222,19 @@ def ffn_args(X, W_up, W_down, cfg, *, Y=None, bufs=None, W_gate=None, W_upT=None
 def sfl_workspace_size(args, kind=0):
     out = c_size_t(0)
     _check("sfl_workspace_size", _lib.sfl_workspace_size(ctypes.byref(args), kind, ctypes.byref(out)))
+    return out.value
+
+
+def sfl_forward_workspace_size(args, dense=False):
+    out = c_size_t(0)
+    _check("sfl_forward_workspace_size", _lib.sfl_forward_workspace_size(ctypes.byref(args), 1 if dense else 0,
+                                                                          ctypes.byref(out)))
+    return out.value
+
+
+def sfl_backward_workspace_size(args):
+    out = c_size_t(0)
+    _check("sfl_backward_workspace_size", _lib.sfl_backward_workspace_size(ctypes.byref(args), ctypes.byref(out)))
     return out.value
 
 

@@ -422,6 +422,15 @@ sfl_status_t sfl_workspace_size(const void* args, int backward, size_t* bytes) {
   return SFL_OK;
 }
 
+sfl_status_t sfl_forward_workspace_size(const sfl_ffn_args_t* args, int32_t dense, size_t* bytes) {
+  if (dense != 0 && dense != 1) return SFL_E_ARG;
+  return sfl_workspace_size(args, dense ? 2 : 0, bytes);
+}
+
+sfl_status_t sfl_backward_workspace_size(const sfl_ffn_bwd_args_t* args, size_t* bytes) {
+  return sfl_workspace_size(args, 1, bytes);
+}
+
 sfl_status_t sfl_up_projection(const sfl_ffn_args_t* a, float* Z, sfl_stream_t stream) {
   sfl_status_t st = check_forward(a, false);
   if (st != SFL_OK) return st;

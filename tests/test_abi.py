@@ -117,6 +117,27 @@ def test_workspace_sizes():
         assert b.sfl_workspace_size(g, 2) == _al(T * f * 2) + _al(parts * 4), (T, d, f)
 
 
+def test_typed_workspace_queries_match_the_untyped_one():
+    for a in (_fake_args(b.SFL_BF16, 128, 256, 1024, ell_width=32),
+              _fake_args(b.SFL_BF16, 512, 256, 1024, ell_width=16, ovf_capacity=64),
+              _fake_args(b.SFL_BF16, 32, 4096, 14336, gated=True, ell_width=128),
+              _fake_args(b.SFL_F32, 64, 256, 1024, ell_width=32)):
+        assert b.sfl_forward_workspace_size(a) == b.sfl_workspace_size(a, 0)
+        assert b.sfl_forward_workspace_size(a, dense=True) == b.sfl_workspace_size(a, 2)
+    for g in (_fake_bwd(256, 512, 1024, ell_width=64), _fake_bwd(256, 512, 1024, gated=True, ell_width=64)):
+        assert b.sfl_backward_workspace_size(g) == b.sfl_workspace_size(g, 1)
+    a = _fake_args(b.SFL_BF16, 128, 256, 1024, ell_width=32)
+    out = ctypes.c_size_t(0)
+    lib = b._lib
+    assert lib.sfl_forward_workspace_size(ctypes.byref(a), 2, ctypes.byref(out)) == b.SFL_E_ARG
+    assert lib.sfl_forward_workspace_size(None, 0, ctypes.byref(out)) == b.SFL_E_ARG
+    assert lib.sfl_backward_workspace_size(None, ctypes.byref(out)) == b.SFL_E_ARG
+    bad = _fake_args(b.SFL_BF16, 128, 200, 1024)
+    with pytest.raises(b.SflError) as e:
+        b.sfl_forward_workspace_size(bad)
+    assert e.value.code == b.SFL_E_UNSUPPORTED
+
+
 def test_size_limit_of_32_bit_offsets():
     """The documented limit: each operand below 2 GiB (bf16 at f = 16384: T < 65536)."""
     ok = _fake_args(b.SFL_BF16, 65535, 4096, 16384, ell_width=256)
