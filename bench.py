@@ -161,7 +161,7 @@ class Bench:
         t.cuda.synchronize()
         return e0.elapsed_time(e1) / steps
 
-    def per_call(self, fn, n=20, flush=None):
+    def per_call(self, fn, n=50, flush=None):
         """Per-call ms of n calls, each timed alone (events around it); with `flush`, that
         callable runs before each call, outside the timed span (cold caches)."""
         t = self.torch
