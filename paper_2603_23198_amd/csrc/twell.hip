@@ -455,9 +455,10 @@ hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32
 
 // Sum of the dense-backup rows that were computed (min(n_ovf, cap) rows of ovf_dense), of
 // their absolute values when absval is set (the gated rows hold h = ReLU(g) * u, which can
-// be negative; the non-gated ReLU rows are >= 0 either way). Up to kL1Blocks blocks stride
-// over the rows with 16-byte loads, each adding its total with one float64 atomic (atomics
-// on one address serialise, so one per row would cost more than the sums).
+// be negative; the non-gated ReLU rows are >= 0 either way). kL1Blocks blocks make one flat
+// pass over the rows (they are contiguous) with 16-byte loads, four in flight per lane,
+// each block adding its total with one float64 atomic (atomics on one address serialise, so
+// one per row would cost more than the sums).
 constexpr int kL1Blocks = 256;
 template <typename V>
 __global__ __launch_bounds__(256) void k_ovf_l1(int64_t f, const V* __restrict__ dense, const int32_t* n_ovf,
@@ -467,21 +468,32 @@ __global__ __launch_bounds__(256) void k_ovf_l1(int64_t f, const V* __restrict__
   // the magnitude keeps every bit but the sign
   const uint32_t keep = absval ? 0x7fffffffu : 0xffffffffu;
   float s = 0.f;
-  const bool vec = f % PER == 0 && ((uintptr_t)dense & 15) == 0;
-  for (int64_t row = blockIdx.x; row < n; row += gridDim.x) {
-    const V* r = dense + row * f;
-    if (vec) {
-      for (int64_t c = (int64_t)threadIdx.x * PER; c < f; c += 256 * PER) {
-        const u32x4_t w = *(const u32x4_t*)(r + c);
+  // the rows are contiguous: one flat pass over n f values, 16 bytes per lane and four
+  // loads in flight per lane
+  const int64_t total = (int64_t)n * f;
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  if (total % PER == 0 && ((uintptr_t)dense & 15) == 0) {
+    const u32x4_t* d4 = (const u32x4_t*)dense;
+    const int64_t n16 = total / PER;
+    auto add = [&](const u32x4_t& w) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          if constexpr (sizeof(V) == 2) s += __uint_as_float((w[q] << 16) & keep) + __uint_as_float(w[q] & 0xffff0000u & keep);
-          else s += __uint_as_float(w[q] & keep);
-        }
+      for (int q = 0; q < 4; ++q) {
+        if constexpr (sizeof(V) == 2) s += __uint_as_float((w[q] << 16) & keep) + __uint_as_float(w[q] & 0xffff0000u & keep);
+        else s += __uint_as_float(w[q] & keep);
       }
-    } else {
-      for (int64_t c = threadIdx.x; c < f; c += 256) s += __uint_as_float(__float_as_uint(VT<V>::load(r, c)) & keep);
+    };
+    int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    for (; i + 3 * stride < n16; i += 4 * stride) {
+      const u32x4_t a0 = d4[i], a1 = d4[i + stride], a2 = d4[i + 2 * stride], a3 = d4[i + 3 * stride];
+      add(a0);
+      add(a1);
+      add(a2);
+      add(a3);
     }
+    for (; i < n16; i += stride) add(d4[i]);
+  } else {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += stride)
+      s += __uint_as_float(__float_as_uint(VT<V>::load(dense, i)) & keep);
   }
   s = wave_sum<float>(s);
   __shared__ float part[4];
@@ -496,7 +508,7 @@ __global__ __launch_bounds__(256) void k_ovf_l1(int64_t f, const V* __restrict__
 hipError_t launch_ovf_l1(int64_t f, int val_bf16, const void* dense, const int32_t* n_ovf, int32_t cap,
                          sfl_stats_t* stats, hipStream_t s, int absval) {
   if (!stats || cap == 0) return hipSuccess;
-  const dim3 grid((unsigned)std::min<int32_t>(cap, kL1Blocks));
+  const dim3 grid((unsigned)kL1Blocks);
   if (val_bf16)
     hipLaunchKernelGGL(k_ovf_l1<bf16_t>, grid, dim3(256), 0, s, f, (const bf16_t*)dense, n_ovf, cap, stats, absval);
   else
@@ -550,8 +562,11 @@ __global__ __launch_bounds__(256) void k_ovf_fill(int64_t f, int NT, int Tn, int
                                                   int32_t cap, V* __restrict__ dense, int32_t* __restrict__ need_rows,
                                                   int32_t* __restrict__ need_slots, int32_t* __restrict__ n_need) {
   constexpr int WIN = kFillWindowBytes / (int)sizeof(V);  // columns per window (a multiple of every tile width)
-  __shared__ V row_s[WIN];
+  constexpr int PER = 16 / (int)sizeof(V);                 // values per 16-byte chunk
+  __shared__ __attribute__((aligned(16))) V row_s[WIN];
   const int n = min(*n_ovf, cap);
+  // rows of whole 16-byte chunks are zeroed and written out 16 bytes per lane
+  const bool vec = f % PER == 0 && ((uintptr_t)dense & 15) == 0;
   for (int i = blockIdx.x; i < n; i += gridDim.x) {
     const int64_t t = ovf_rows[i];
     const Slabs<V, PK> sl{val, idx, cnt, t, NT, S};
@@ -569,7 +584,10 @@ __global__ __launch_bounds__(256) void k_ovf_fill(int64_t f, int NT, int Tn, int
     V* out = dense + (int64_t)i * f;
     for (int64_t c0 = 0; c0 < f; c0 += WIN) {
       const int w = (int)std::min<int64_t>(WIN, f - c0);
-      for (int x = threadIdx.x; x < w; x += 256) row_s[x] = V(0);
+      if (vec)
+        for (int x = threadIdx.x; x < w / PER; x += 256) ((u32x4_t*)row_s)[x] = u32x4_t{0u, 0u, 0u, 0u};
+      else
+        for (int x = threadIdx.x; x < w; x += 256) row_s[x] = V(0);
       __syncthreads();
       const int j0 = (int)(c0 / Tn), nt = (w + Tn - 1) / Tn;
       for (int q = threadIdx.x; q < nt * S; q += 256) {
@@ -582,7 +600,10 @@ __global__ __launch_bounds__(256) void k_ovf_fill(int64_t f, int NT, int Tn, int
         }
       }
       __syncthreads();
-      for (int x = threadIdx.x; x < w; x += 256) out[c0 + x] = row_s[x];
+      if (vec)
+        for (int x = threadIdx.x; x < w / PER; x += 256) ((u32x4_t*)(out + c0))[x] = ((const u32x4_t*)row_s)[x];
+      else
+        for (int x = threadIdx.x; x < w; x += 256) out[c0 + x] = row_s[x];
       __syncthreads();
     }
   }
