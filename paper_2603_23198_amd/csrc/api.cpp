@@ -503,7 +503,16 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
   const sfl_twell_t& tw = a->twell;
   void* ovf_dense = tw.ovf_dense ? tw.ovf_dense : plan.ovf_dense;
   ev.record(0, s);
-  SFL_HIP(launch_stats_init(a->stats, s, plan.n_need ? plan.n_need : plan.tile_sem, plan.n_zero));
+  int32_t* const counters = plan.n_need ? plan.n_need : plan.tile_sem;
+  // the statistics and counters are cleared by the first kernel: the few-rows up projection
+  // of a small batch does it itself, other calls launch a clearing kernel
+  bool cleared = false;
+  auto clear_first = [&]() -> hipError_t {
+    if (cleared) return hipSuccess;
+    cleared = true;
+    return launch_stats_init(a->stats, s, counters, plan.n_zero);
+  };
+  if (T == 0) SFL_HIP(clear_first());
   if (T == 0) {
     SFL_HIP(launch_ovf_list(0, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s));
     for (int i = 1; i < 5; ++i) ev.record(i, s);
@@ -540,6 +549,7 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
       g.tile_slots = a->cfg.tile_slots;
       g.n_tiles = (int)cdiv(f, a->cfg.tile_cols);
       g.tw_packed = packed_layout(a->cfg) ? 1 : 0;
+      SFL_HIP(clear_first());
       SFL_HIP(gemm_bf16(LAY_KC, blay, EPI_TWELL, g, s));
     } else {
       g.C = plan.Z;
@@ -556,10 +566,18 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
         // never written. (Packing in the GEMM's last block per tile was slower: the
         // device-scope release each block then needs writes back its XCD's L2.)
         g.no_reduce = 1;
+        if (few_rows_path(g, blay)) {
+          g.zero_stats = a->stats;
+          g.zero = counters;
+          g.n_zero = counters ? plan.n_zero : 0;
+          cleared = true;
+        }
+        SFL_HIP(clear_first());
         SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_F32, g, s));
         SFL_HIP(launch_pack_twell_parts(plan.part, ks, a->bias_f, a->shift_t, T, f, vb, a->cfg.tile_cols,
                                         a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, s, packed_layout(a->cfg)));
       } else {
+        SFL_HIP(clear_first());
         SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_F32, g, s));
         SFL_HIP(launch_pack_twell(plan.Z, T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, s,
                                   packed_layout(a->cfg)));

@@ -928,6 +928,20 @@ __device__ __forceinline__ void splitk_store(const GemmParams& p, int m, int n, 
   }
 }
 
+// The statistics and counters a call's first kernel clears (zero_stats, zero[0 .. n_zero)),
+// by one block, before anything of the kernel can return.
+__device__ __forceinline__ void zero_first(const GemmParams& p) {
+  if (p.zero_stats && threadIdx.x == 0) {
+    p.zero_stats->total_nnz = 0;
+    p.zero_stats->n_ovf_rows = 0;
+    p.zero_stats->n_tile_ovf = 0;
+    p.zero_stats->l1_sum = 0.0;
+    p.zero_stats->capacity_exceeded = 0;
+    p.zero_stats->reserved = 0;
+  }
+  for (int i = threadIdx.x; i < p.n_zero; i += blockDim.x) p.zero[i] = 0;
+}
+
 // Sum of the ks partials of row m, columns n .. n+3, in split order (from p.part, or from
 // the partial sums at `part`).
 __device__ __forceinline__ f32x4_t splitk_sum(const GemmParams& p, int ks, int m_eff, int m, int n,
@@ -976,6 +990,7 @@ __global__ __launch_bounds__(NTHR) void k_gemm_few_rows(GemmParams p) {
   __shared__ __attribute__((aligned(1024))) bf16_t smem[FR_NS * FR_STAGE];
   constexpr bool PAIR = EPI == EPI_GATED_PAIR;
   constexpr int TN = PAIR ? BN / 2 : BN;  // output columns per tile (of each product)
+  if (blockIdx.x == 0) zero_first(p);
   const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
   if (m_eff <= 0) return;
   const int nk_all = (int)(p.K / KC_BK);
@@ -1311,6 +1326,12 @@ hipError_t launch_gated_pair(const GemmParams& p, hipStream_t s) {
   if (q.M <= 32) hipLaunchKernelGGL((k_gemm_few_rows<EPI_GATED_PAIR, 1>), dim3(grid), dim3(NTHR), 0, s, q);
   else hipLaunchKernelGGL((k_gemm_few_rows<EPI_GATED_PAIR, 2>), dim3(grid), dim3(NTHR), 0, s, q);
   return hipGetLastError();
+}
+
+// Whether gemm_bf16 runs p (bf16, K-contiguous A, no counted rows) as the few-rows split-K
+// GEMM, which clears zero_stats and zero[] first.
+bool few_rows_path(const GemmParams& p, int blay) {
+  return kc_ok(p, blay) && p.ksplit > 1 && p.part && p.N % 4 == 0 && !p.m_count && few_rows_split(p, blay) > 1;
 }
 
 // Whether gemm_bf16 runs p (bf16, K-contiguous A, counted rows allowed) as the few-rows

@@ -83,6 +83,11 @@ struct GemmParams {
   // few-rows split-K with tile counters, EPI_ACT_RELU or EPI_GATED_PAIR: the sum of the
   // stored |values| is added to l1_stats->l1_sum (one float64 atomic per tile)
   sfl_stats_t* l1_stats;
+  // few-rows split-K: statistics and n_zero int counters the kernel clears first (a call's
+  // first kernel does it in place of a separate clearing launch)
+  sfl_stats_t* zero_stats;
+  int32_t* zero;
+  int n_zero;
 };
 
 // bf16 MFMA GEMM. Requirements: K % 8 == 0; RC layouts need even M/N extents and
@@ -100,6 +105,9 @@ hipError_t launch_gated_pair(const GemmParams& p, hipStream_t s);
 // Whether gemm_bf16 runs p as the few-rows split-K GEMM whose last blocks apply the epilogue
 // (and add the stored |values| to l1_stats for EPI_ACT_RELU).
 bool few_rows_tile_epilogue(const GemmParams& p, int blay);
+// Whether gemm_bf16 runs p (no counted rows) as the few-rows split-K GEMM, which clears
+// zero_stats and zero[0 .. n_zero) before anything else.
+bool few_rows_path(const GemmParams& p, int blay);
 
 // fp32 FMA GEMM for the F32 dtype (A MK, B KN only; any sizes).
 hipError_t gemm_f32(int epi, const GemmParams& p, hipStream_t s);

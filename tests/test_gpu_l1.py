@@ -134,3 +134,39 @@ def test_l1_of_the_standalone_pack():
     sparse = np.nonzero(~hy.is_ovf)[0]
     assert len(sparse) < w.T  # some dense-backup rows, left out of the pack's sum
     check_l1(st, w, H, rows=sparse)
+
+
+@pytest.mark.parametrize("T,gated,copies", [(32, True, True), (48, False, True), (48, True, False), (700, False, True)])
+def test_statistics_and_counters_are_cleared_by_the_call(T, gated, copies):
+    """Every forward clears its statistics and workspace counters itself (a batch of at most
+    64 tokens with K-contiguous weights in its first GEMM, others in a clearing kernel): the
+    same call with the statistics and the workspace filled with 0xff bytes beforehand gives
+    the statistics of a clean start, and the same Y bit for bit. Rows with dense-backup rows,
+    so that the per-tile counters and the recompute list are in use."""
+    w = wl.make_ffn("clear", "bf16", T, 512, 2048, seed=3 + T, gated=gated,
+                    sparsity_rows=mixed_rows(T, T, 0.15, 0.15), ell_width=64)
+    X, Wu, Wd = dev(w.X), dev(w.W_up), dev(w.W_down)
+    Wg = dev(w.W_gate) if gated else None
+    tr = lambda W: None if (W is None or not copies) else W.t().contiguous()
+    cfg = b.make_cfg(**w.cfg)
+    out = []
+    for dirty in (False, True):
+        bufs = b.alloc_twell(T, w.f, "bf16", cfg)
+        Y = torch.empty((T, w.d), dtype=torch.bfloat16, device="cuda")
+        stats = b.alloc_stats()
+        kw = dict(Y=Y, bufs=bufs, W_gate=Wg, W_upT=tr(Wu), W_gateT=tr(Wg), W_downT=tr(Wd), shift_t=dev(w.shift_t),
+                  stats=stats)
+        ws = torch.empty(max(1, b.sfl_workspace_size(b.ffn_args(X, Wu, Wd, cfg, **kw))), dtype=torch.uint8,
+                         device="cuda")
+        if dirty:
+            stats.fill_(0xff)
+            ws.fill_(0xff)
+        b.sfl_ffn_forward(b.ffn_args(X, Wu, Wd, cfg, **kw, workspace=ws))
+        torch.cuda.synchronize()
+        out.append((Y, b.read_stats(stats), twell_views(bufs, T, w.f, cfg)["n_ovf"]))
+    (Y0, s0, n0), (Y1, s1, n1) = out
+    assert n0 == n1 > 0
+    assert torch.equal(Y0.view(torch.int16), Y1.view(torch.int16))
+    for k in ("total_nnz", "n_ovf_rows", "n_tile_ovf", "capacity_exceeded"):
+        assert s0[k] == s1[k], k
+    assert abs(s1["l1_sum"] - s0["l1_sum"]) <= 1e-6 * abs(s0["l1_sum"])
