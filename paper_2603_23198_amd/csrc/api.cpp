@@ -504,8 +504,9 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
   void* ovf_dense = tw.ovf_dense ? tw.ovf_dense : plan.ovf_dense;
   ev.record(0, s);
   int32_t* const counters = plan.n_need ? plan.n_need : plan.tile_sem;
-  // the statistics and counters are cleared by the first kernel: the few-rows up projection
-  // of a small batch does it itself, other calls launch a clearing kernel
+  // the statistics and counters are cleared by the first kernel: the fused TwELL GEMM and
+  // the few-rows up projection of a small batch do it themselves, other calls launch a
+  // clearing kernel
   bool cleared = false;
   auto clear_first = [&]() -> hipError_t {
     if (cleared) return hipSuccess;
@@ -549,7 +550,11 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
       g.tile_slots = a->cfg.tile_slots;
       g.n_tiles = (int)cdiv(f, a->cfg.tile_cols);
       g.tw_packed = packed_layout(a->cfg) ? 1 : 0;
-      SFL_HIP(clear_first());
+      // the TwELL GEMM (either kernel) clears the statistics and counters itself
+      g.zero_stats = a->stats;
+      g.zero = counters;
+      g.n_zero = counters ? plan.n_zero : 0;
+      cleared = true;
       SFL_HIP(gemm_bf16(LAY_KC, blay, EPI_TWELL, g, s));
     } else {
       g.C = plan.Z;

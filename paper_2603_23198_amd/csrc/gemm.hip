@@ -43,6 +43,21 @@ __device__ __forceinline__ bool active_bits(float z) {
   return (uint32_t)__float_as_int(z) - 1u < 0x7f800000u;
 }
 
+// The statistics and counters a call's first kernel clears (zero_stats, zero[0 .. n_zero)),
+// by one block, before anything of the kernel can return.
+__device__ __forceinline__ void zero_first(const GemmParams& p) {
+  if (p.zero_stats && threadIdx.x == 0) {
+    p.zero_stats->total_nnz = 0;
+    p.zero_stats->n_ovf_rows = 0;
+    p.zero_stats->n_tile_ovf = 0;
+    p.zero_stats->l1_sum = 0.0;
+    p.zero_stats->capacity_exceeded = 0;
+    p.zero_stats->reserved = 0;
+  }
+  for (int i = threadIdx.x; i < p.n_zero; i += blockDim.x) p.zero[i] = 0;
+}
+
+
 // ---- loaders -----------------------------------------------------------------------
 // All global reads go through raw buffer loads: an offset at or beyond the descriptor's
 // byte size reads as zero, so M/N/K tails and gathered rows need no branches. Offsets are
@@ -447,6 +462,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmParams& p, typename Wave
 template <int ALAY, int BLAY, int EPI, int Tn>
 __global__ __launch_bounds__(NTHR) void k_gemm_bf16(GemmParams p) {
   __shared__ __attribute__((aligned(16))) bf16_t smem[2 * LDS_STAGE];
+  if (blockIdx.x == 0) zero_first(p);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -824,6 +840,7 @@ struct KcTwPre {
 template <int EPI, int Tn, int BL>
 __global__ __launch_bounds__(NTHR) void k_gemm_kc(GemmParams p) {
   __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * KC_STAGE];
+  if (blockIdx.x == 0) zero_first(p);
   typedef WaveTile<KC_WM, KC_WN, KC_FM> W;
   const int tiles_m = (int)cdiv(p.M, BM), tiles_n = (int)cdiv(p.N, BN);
   const int nt = tiles_m * tiles_n;
@@ -926,20 +943,6 @@ __device__ __forceinline__ void splitk_store(const GemmParams& p, int m, int n, 
       *c = f32_to_bf16(bf16_to_f32(*c) * x);
     }
   }
-}
-
-// The statistics and counters a call's first kernel clears (zero_stats, zero[0 .. n_zero)),
-// by one block, before anything of the kernel can return.
-__device__ __forceinline__ void zero_first(const GemmParams& p) {
-  if (p.zero_stats && threadIdx.x == 0) {
-    p.zero_stats->total_nnz = 0;
-    p.zero_stats->n_ovf_rows = 0;
-    p.zero_stats->n_tile_ovf = 0;
-    p.zero_stats->l1_sum = 0.0;
-    p.zero_stats->capacity_exceeded = 0;
-    p.zero_stats->reserved = 0;
-  }
-  for (int i = threadIdx.x; i < p.n_zero; i += blockDim.x) p.zero[i] = 0;
 }
 
 // Sum of the ks partials of row m, columns n .. n+3, in split order (from p.part, or from

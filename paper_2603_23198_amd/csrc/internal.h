@@ -83,8 +83,9 @@ struct GemmParams {
   // few-rows split-K with tile counters, EPI_ACT_RELU or EPI_GATED_PAIR: the sum of the
   // stored |values| is added to l1_stats->l1_sum (one float64 atomic per tile)
   sfl_stats_t* l1_stats;
-  // few-rows split-K: statistics and n_zero int counters the kernel clears first (a call's
-  // first kernel does it in place of a separate clearing launch)
+  // statistics and n_zero int counters that block 0 clears first (the direct-to-LDS,
+  // register-staged and few-rows kernels; a call's first kernel does it in place of a
+  // separate clearing launch)
   sfl_stats_t* zero_stats;
   int32_t* zero;
   int n_zero;
