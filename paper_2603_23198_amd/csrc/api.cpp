@@ -596,7 +596,17 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
   SFL_HIP(launch_classify(T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, a->cfg.ell_width, tw.val, tw.idx, tw.cnt,
                           tw.row_nnz, tw.row_ovf, tw.ell_val, tw.ell_idx, a->stats, s, a->gated ? 0 : 1,
                           packed_layout(a->cfg)));
-  SFL_HIP(launch_ovf_list(T, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s));
+  // the dense-backup row list: up to 64 rows the gather's first block builds it (nothing
+  // before the dense-backup stage reads it), else its own kernel
+  OvfList late_list;
+  if (T <= 64 && packed_gather(*a) && !plan.H) {
+    late_list.rows = tw.ovf_rows;
+    late_list.n = tw.n_ovf;
+    late_list.cap = (int32_t)cap;
+    late_list.stats = a->stats;
+  } else {
+    SFL_HIP(launch_ovf_list(T, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s));
+  }
   ev.record(2, s);
   if (plan.H) {
     // dense-fallback candidate: decide on the batch's mean row count, then Y = H W_down over
@@ -657,7 +667,7 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
     const bool form_h = a->gated && T <= kGatherFormsH;
     SFL_HIP(launch_gather_down_packed(T, d, f, a->cfg.ell_width, hv, tw.ell_idx, tw.row_nnz, tw.row_ovf, WdP, a->Y,
                                       s, 0, 0, nullptr, order, plan.dense_flags ? plan.dense_flags + 1 : nullptr,
-                                      form_h ? plan.part_u : nullptr, form_h ? a->stats : nullptr));
+                                      form_h ? plan.part_u : nullptr, form_h ? a->stats : nullptr, late_list));
   } else {
     SFL_HIP(launch_gather_down(vb, T, d, a->cfg.ell_width, tw.ell_val, tw.ell_idx, tw.row_nnz, tw.row_ovf,
                                a->W_down, a->Y, s));

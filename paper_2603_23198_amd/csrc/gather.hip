@@ -293,12 +293,33 @@ __device__ __forceinline__ void store_slice(bf16_t* Y, float* Yf, int64_t o, flo
   }
 }
 
+// The ascending dense-backup row list of a batch of at most 64 rows (one wave; in place of
+// the list kernel): lane t takes row t, the ballot of the flags gives each flagged row its
+// position; the count, and the statistics' row count and capacity flag, from lane 0.
+__device__ __forceinline__ void ovf_list_small(int64_t T, const OvfList& ol, const uint8_t* __restrict__ row_ovf) {
+  const int l = threadIdx.x & 63;
+  const bool flag = l < T && row_ovf[l];
+  const uint64_t m = ballot(flag);
+  const int pos = mbcnt(m);
+  if (flag && pos < ol.cap) ol.rows[pos] = l;
+  if (l == 0) {
+    const int n = __popcll(m);
+    *ol.n = n;
+    if (ol.stats) {
+      ol.stats->n_ovf_rows = n;
+      ol.stats->capacity_exceeded = n > ol.cap ? 1 : 0;
+    }
+  }
+}
+
 template <int VK, int OUT, int U, bool TG = false>
 __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
     int64_t T, int64_t d, int64_t f, int K, const void* __restrict__ ell_val, const uint16_t* __restrict__ ell_idx,
     const int32_t* __restrict__ row_nnz, const uint8_t* __restrict__ row_ovf, const bf16_t* __restrict__ W,
     bf16_t* __restrict__ Y, float* __restrict__ Yf, int n_slices, int tpw, const int32_t* __restrict__ order,
-    const int32_t* __restrict__ skip, const float* __restrict__ part_u, sfl_stats_t* __restrict__ stats) {
+    const int32_t* __restrict__ skip, const float* __restrict__ part_u, sfl_stats_t* __restrict__ stats,
+    OvfList ol) {
+  if (ol.rows && blockIdx.x == 0 && threadIdx.x < 64) ovf_list_small(T, ol, row_ovf);
   if (skip && *skip) return;         // the dense fallback took this batch
   constexpr int EW = VK + 1;         // words per staged entry
   // token groups read 8 tokens' entries at once: an odd stride puts them in different banks
@@ -808,8 +829,9 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
                                      const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
                                      const void* Wp, void* Y, hipStream_t s, int val_f32, int out_mode, float* Yf,
                                      const int32_t* order, const int32_t* skip, const float* part_u,
-                                     sfl_stats_t* stats) {
+                                     sfl_stats_t* stats, OvfList ol) {
   if (T == 0) return hipSuccess;
+  if (ol.rows && (T > 64 || !ol.n)) return hipErrorInvalidValue;
   if (part_u && (val_f32 || out_mode != 0)) return hipErrorInvalidValue;
   if (d % (8 * SLICE2) != 0) return hipErrorInvalidValue;
   if (out_mode < 0 || out_mode > 2 || (out_mode > 0 && !Yf) || (out_mode != 1 && !Y)) return hipErrorInvalidValue;
@@ -834,7 +856,7 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
     }                                                                                                              \
     hipLaunchKernelGGL((k_gather_down_b16<VK_, OUT_, U_, TG_>), grid, block, lds, s, T, d, f, K, ell_val, ell_idx, \
                        row_nnz, row_ovf, (const bf16_t*)Wp, (bf16_t*)Y, Yf, n_slices, tpw, order, skip, part_u,    \
-                       stats);                                                                                     \
+                       stats, ol);                                                                                 \
   } while (0)
 #define SFL_GATHER_LAUNCH_U(VK_, OUT_, U_) SFL_GATHER_LAUNCH_G(VK_, OUT_, U_, false)
 #define SFL_GATHER_LAUNCH(VK_, OUT_)                  \

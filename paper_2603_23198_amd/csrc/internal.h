@@ -164,8 +164,18 @@ hipError_t launch_ovf_l1(int64_t f, int val_bf16, const void* ovf_dense, const i
 hipError_t launch_gather_down(int val_bf16, int64_t T, int64_t d, int ell_width, const void* ell_val,
                               const uint16_t* ell_idx, const int32_t* row_nnz,
                               const uint8_t* row_ovf, const void* W, void* Y, hipStream_t s);
+// The dense-backup row list (ascending rows, at most cap of them, the count in *n and, with
+// stats, its row count and capacity flag), built by another kernel in passing.
+struct OvfList {
+  int32_t* rows = nullptr;
+  int32_t* n = nullptr;
+  int32_t cap = 0;
+  sfl_stats_t* stats = nullptr;
+};
 // bf16, d % 512 == 0: same sum from the slice-major copy of W_down (persistent, XCD-aware).
 // out_mode 0: bf16 Y; 1: fp32 Yf; 2: bf16 Y of (sum + Yf) (val_f32 only for 1 and 2).
+// With ol.rows (at most 64 rows): block 0 also builds the dense-backup row list from row_ovf
+// (as launch_ovf_list would), before anything else.
 // With part_u (bf16 values, out_mode 0; the gated layer): the values are
 // h = bf16(ell_val * sum_x part_u[x][t][e]), formed while staging the entries as
 // launch_gated_h forms them, and |h| is added to stats->l1_sum (if given).
@@ -174,7 +184,8 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int ell_wi
                                      const void* W_packed, void* Y, hipStream_t s,
                                      int val_f32 = 0, int out_mode = 0, float* Yf = nullptr,
                                      const int32_t* order = nullptr, const int32_t* skip = nullptr,
-                                     const float* part_u = nullptr, sfl_stats_t* stats = nullptr);
+                                     const float* part_u = nullptr, sfl_stats_t* stats = nullptr,
+                                     OvfList ol = OvfList());
 // Gated backward at the ELL entries: dh (8 partials + lambda' sign(g u)) -> dh_u, dh_g, h.
 hipError_t launch_gated_entry_grads(int64_t T, int K, const void* ell_val, const int32_t* row_nnz,
                                     const uint8_t* row_ovf, const float* part, const float* u, float lam, float* dhu,

@@ -376,21 +376,28 @@ def test_all_active_and_all_inactive_rows():
     assert rel_l2(to_f64(Y), Yref) <= 2e-2
 
 
-def test_capacity_exceeded_flag_then_enough_capacity():
-    w = wl.make_ffn("capacity", "bf16", 128, 256, 512, seed=4, sparsity=0.95, ell_width=16)
-    w.shift_t[::4] = 100.0    # 32 dense-backup rows
+@pytest.mark.parametrize("T,d,copies", [(128, 256, False), (48, 512, True), (48, 512, False)])
+def test_capacity_exceeded_flag_then_enough_capacity(T, d, copies):
+    """More dense-backup rows than the capacity: the flag, the count and the first `capacity`
+    rows of the ascending list, which at most 64 rows with a slice-major gather are built by
+    the gather's first block instead of the list kernel."""
+    w = wl.make_ffn("capacity", "bf16", T, d, 512, seed=4, sparsity=0.95, ell_width=16)
+    w.shift_t[::4] = 100.0    # T / 4 dense-backup rows
     w.cfg["ovf_capacity"] = 10
-    Y, bufs, stats, cfg = run_forward(w)
+    Y, bufs, stats, cfg = run_forward(w, use_wupt=copies, use_wdownt=copies)
     st = b.read_stats(stats)
-    assert st["capacity_exceeded"] == 1 and st["n_ovf_rows"] >= 32
+    assert st["capacity_exceeded"] == 1 and st["n_ovf_rows"] >= T // 4
     got = twell_views(bufs, w.T, w.f, cfg)
+    flagged = np.nonzero(got["row_ovf"])[0]
+    assert got["n_ovf"] == st["n_ovf_rows"] == len(flagged)
+    np.testing.assert_array_equal(got["ovf_rows"][:10], flagged[:10])  # ascending, the first `capacity`
     Yref, _ = oracle_rows(w, np.arange(w.T))
     done = got["ovf_rows"][:10]
     assert rel_l2(to_f64(Y)[done], Yref[done]) <= 2e-2
     sparse = np.nonzero(got["row_ovf"] == 0)[0]
     assert rel_l2(to_f64(Y)[sparse], Yref[sparse]) <= 2e-2
     w.cfg["ovf_capacity"] = 0
-    Y2, _, stats2, _ = run_forward(w)
+    Y2, _, stats2, _ = run_forward(w, use_wupt=copies, use_wdownt=copies)
     assert b.read_stats(stats2)["capacity_exceeded"] == 0
     assert rel_l2(to_f64(Y2), Yref) <= 2e-2
 
