@@ -547,14 +547,12 @@ hipError_t launch_dense_decision(int64_t T, int64_t f, bool force, const int32_t
 // Dense-backup rows straight from the TwELL slabs (Sec. 3.4): a row whose tiles all kept
 // every active value (cnt <= S) is rebuilt exactly, zeros and all, in LDS one window of
 // columns at a time and written out; a row with an overflowing tile lost values, so it
-// is flagged (need[i] = 1) for recomputation by the GEMM. Blocks stride over the slots
-// i < n_ovf.
+// goes to the GEMM's recompute list (need_rows: token row, need_slots: its ovf_dense row)
+// at a position taken from the zeroed counter n_need. The list's order varies from call to
+// call, which the recomputing GEMM does not see (each of its rows is computed by the same
+// arithmetic wherever it sits). Blocks stride over the slots i < n_ovf.
 constexpr int kFillWindowBytes = 32768;
 constexpr int kFillBlocks = 1024;
-// A row with an overflowing tile is appended to the recompute list (need_rows: token row,
-// need_slots: its ovf_dense row) at a position taken from the zeroed counter n_need; the
-// list's order varies from call to call, which the recomputing GEMM does not see (each of
-// its rows is computed by the same arithmetic wherever it sits).
 template <typename V, bool PK>
 __global__ __launch_bounds__(256) void k_ovf_fill(int64_t f, int NT, int Tn, int S, const V* __restrict__ val,
                                                   const uint16_t* __restrict__ idx, const int32_t* __restrict__ cnt,
