@@ -323,6 +323,42 @@ def test_small_batch_dense_backup_rows(T, gated, copies):
             assert rel_l2(dense_rows[i], H[t]) <= 1e-2, (i, t)
 
 
+@pytest.mark.parametrize("copies", [False, True])
+@pytest.mark.parametrize("gated", [False, True])
+@pytest.mark.parametrize("T,every", [(100, 2), (100, 3), (600, 12), (600, 6)])
+def test_counted_dense_backup_rows_above_64_tokens(T, every, gated, copies):
+    """Batches above 64 tokens (dense-backup capacity T; the GEMMs' row count comes from
+    the device) with a few dozen to a hundred dense-backup rows: every `every`-th row is
+    all active, so 50, 34, 50 and 100 rows overflow (above 256 tokens the non-gated layer
+    recomputes them through the need list). Y, each dense-backup row of h against the
+    oracle's, and the L1 statistic; two calls in a row."""
+    w = wl.make_ffn("counted-ovf", "bf16", T, 1024, 2048, seed=T + every + 2 * gated, gated=gated, sparsity=0.97,
+                    ell_width=128)
+    w.shift_t[::every] = 100.0
+    X = w.as_f64(w.X)
+    if gated:
+        _, _, _, H = ffn.ffn_gated_dense(X, w.as_f64(w.W_gate), w.as_f64(w.W_up), w.as_f64(w.W_down), w.bias_f,
+                                         w.shift_t)
+    else:
+        _, _, H = ffn.ffn_dense(X, w.as_f64(w.W_up), w.as_f64(w.W_down), w.bias_f, w.shift_t)
+    Yref, _ = oracle_rows(w, np.arange(T))
+    n_ovf = -(-T // every)
+    for _ in range(2):
+        Y, bufs, stats, cfg = run_forward(w, use_wupt=copies, use_wgatet=copies and gated, use_wdownt=copies)
+        got = twell_views(bufs, T, w.f, cfg)
+        assert got["row_ovf"][::every].all() and got["n_ovf"] == n_ovf == int(got["row_ovf"].sum())
+        assert rel_l2(to_f64(Y), Yref) <= 2e-2
+        ovf = np.nonzero(got["row_ovf"])[0]
+        assert rel_l2(to_f64(Y)[ovf], Yref[ovf]) <= 2e-2
+        np.testing.assert_array_equal(got["ovf_rows"][:len(ovf)], ovf)
+        dense_rows = to_f64(bufs["ovf_dense"])[:len(ovf) * w.f].reshape(len(ovf), w.f)
+        for i, t in enumerate(ovf):
+            assert rel_l2(dense_rows[i], H[t]) <= 1e-2, (i, t)
+        # eq. l1 with lambda = 1, times T f: the sum of |h| (the bar of the L1 statistic tests)
+        want = ffn.l1_penalty(H, 1.0) * T * w.f
+        assert abs(b.read_stats(stats)["l1_sum"] - want) <= 5e-3 * want
+
+
 @pytest.mark.parametrize("T,Tn,f", [(1, 256, 2048), (17, 256, 2048), (48, 256, 2048), (64, 256, 2048),
                                     (17, 64, 2048), (64, 128, 2048), (40, 64, 2048), (33, 128, 1984)])
 def test_small_batch_split_gemm(T, Tn, f):
