@@ -183,6 +183,23 @@ constexpr int64_t kTokenGroupT = 1024;
 constexpr int GU_GROUP = SFL_GROUP_UNROLL;  // row loads per lane in flight in the group walks
 // The backward's per-unit gathers group units the same way when their lists are short.
 constexpr int64_t kUnitGroupBound = 128;
+// The forward's token-group walk stages each entry as its W_down row's byte offset
+// (uint32, rows of KS = K + 1 words) and its bf16 value (rows of KV values): the offset
+// then needs one add per load, and two consecutive values are read as the bf16 pair of a
+// dot2 as they stand. KV is even (pairs stay 4-byte aligned) with KV / 2 odd, so that the
+// 8 lane groups' value reads, one token each, fall in different banks.
+// KV also covers the last round of a row (values up to the row length rounded up to a
+// multiple of GU_GROUP are read, the ones past the row masked).
+static_assert(GU_GROUP % 2 == 0, "bf16 entries are consumed in pairs");
+__host__ __device__ inline int tg_value_stride(int K) {
+  const int h = (K + GU_GROUP - 1) / GU_GROUP * GU_GROUP / 2;
+  return 2 * (h | 1);
+}
+#ifndef SFL_TG_LDS
+#define SFL_TG_LDS 148608
+#endif
+constexpr int64_t kTgLds = SFL_TG_LDS;  // LDS budget of a token-group workgroup (bf16 values)
+__host__ __device__ inline int64_t tg_bytes_per_token(int K) { return (int64_t)(K + 1) * 4 + (int64_t)tg_value_stride(K) * 2 + 4; }
 
 // Sum of the 8 groups' partial sums (lanes l, l ^ 8, ..., l ^ 56) into every group: the
 // partner 8 lanes away is in the same 16-lane row (DPP row_ror:8), the other two steps
@@ -322,10 +339,15 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
   if (ol.rows && blockIdx.x == 0 && threadIdx.x < 64) ovf_list_small(T, ol, row_ovf);
   if (skip && *skip) return;         // the dense fallback took this batch
   constexpr int EW = VK + 1;         // words per staged entry
+  // bf16 entries of the token-group walk: offsets [tpw][KS] and values [tpw][KV] (above)
+  constexpr bool SPLIT = VK == 0 && TG;
+  constexpr uint32_t row_b = SLICE2 * 2;
   // token groups read 8 tokens' entries at once: an odd stride puts them in different banks
   const int KS = TG ? K + 1 : K;
-  extern __shared__ uint32_t ent[];  // [tpw][KS] entries, then [tpw] counts (-1 = skip)
-  int* cnt_s = (int*)(ent + (size_t)tpw * KS * EW);
+  const int KV = SPLIT ? tg_value_stride(K) : 0;
+  extern __shared__ uint32_t ent[];  // [tpw][KS] entries (offsets), [tpw][KV] bf16 values, [tpw] counts (-1 = skip)
+  bf16_t* val_s = (bf16_t*)(ent + (size_t)tpw * KS * EW);
+  int* cnt_s = (int*)(val_s + (size_t)tpw * KV);
   const int xcd = blockIdx.x & 7;
   const int64_t t0 = (int64_t)(blockIdx.x >> 3) * tpw;
   const int l = threadIdx.x & 63;
@@ -364,7 +386,12 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
           v = f32_to_bf16(bf16_to_f32((bf16_t)v) * u);
           l1 += fabsf(bf16_to_f32((bf16_t)v));
         }
-        ent[i * KS + e] = (uint32_t)ell_idx[t * K + e] | (v << 16);
+        if constexpr (SPLIT) {
+          ent[i * KS + e] = (uint32_t)ell_idx[t * K + e] * row_b;
+          val_s[i * KV + e] = (bf16_t)v;
+        } else {
+          ent[i * KS + e] = (uint32_t)ell_idx[t * K + e] | (v << 16);
+        }
       }
     }
   }
@@ -380,7 +407,6 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
     // Short rows: a work item is (slice, NGRP tokens), lane group g walking token g's
     // entries on its own, so that no partial sums are folded across groups; the wave runs
     // to the longest of its tokens' rows (absent entries load nothing and add 0).
-    constexpr uint32_t row_b = SLICE2 * 2;
     const int n_grp = (tpw + NGRP - 1) / NGRP;
     for (int it = wave; it < nsl * n_grp; it += GATHER_WAVES) {
       const int slice = xcd + 8 * (it / n_grp);
@@ -397,6 +423,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
       if (cmax < 0) continue;
       const uint32_t col_b = (uint32_t)(slice * f * SLICE2 * 2) + (uint32_t)sub * 16u;
       const uint32_t* er = ent + (size_t)(i < tpw ? i : 0) * KS * EW;
+      const bf16_t* ev = val_s + (size_t)(i < tpw ? i : 0) * KV;
       float acc[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) acc[j] = 0.f;
@@ -404,15 +431,29 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
       // of the item, where a group's absent entries must read and add nothing
       auto round = [&](int e0, auto tail) {
         u32x4_t w[U];
-        uint32_t x[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
           const bool ok = !decltype(tail)::value || e0 + u < c;
-          x[u] = ok ? er[EW * (e0 + u)] : 0u;  // an absent entry has value 0 (and its load reads 0)
-          const uint32_t off = ok ? (x[u] & 0xffffu) * row_b + col_b : 0x80000000u;
+          // an absent entry's load reads 0 (and its value is 0)
+          const uint32_t off = !ok ? 0x80000000u : SPLIT ? er[e0 + u] + col_b : er[EW * (e0 + u)] * row_b + col_b;
           w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0));
         }
-        if constexpr (VK == 1) {
+        if constexpr (SPLIT) {
+          // values e0 + u, e0 + u + 1 as one bf16 pair (e0 + u is even); absent ones are 0
+#pragma unroll
+          for (int u = 0; u < U; u += 2) {
+            uint32_t vp = *(const uint32_t*)(ev + e0 + u);
+            if constexpr (decltype(tail)::value) vp = e0 + u + 1 < c ? vp : (e0 + u < c ? vp & 0xffffu : 0u);
+            const bf16x2_t vv = __builtin_bit_cast(bf16x2_t, vp);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const bf16x2_t lo = __builtin_bit_cast(bf16x2_t, __builtin_amdgcn_perm(w[u + 1][j], w[u][j], 0x05040100u));
+              const bf16x2_t hi = __builtin_bit_cast(bf16x2_t, __builtin_amdgcn_perm(w[u + 1][j], w[u][j], 0x07060302u));
+              acc[2 * j] = __builtin_amdgcn_fdot2_f32_bf16(vv, lo, acc[2 * j], false);
+              acc[2 * j + 1] = __builtin_amdgcn_fdot2_f32_bf16(vv, hi, acc[2 * j + 1], false);
+            }
+          }
+        } else {
           // fp32 values: each entry's row segment scaled and added in entry order
 #pragma unroll
           for (int u = 0; u < U; ++u) {
@@ -424,21 +465,12 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
               acc[2 * j + 1] = fmaf(v, bf16hi(w[u][j]), acc[2 * j + 1]);
             }
           }
-        } else {
-#pragma unroll
-          for (int u = 0; u < U; u += 2) {
-            const bf16x2_t vv = __builtin_bit_cast(bf16x2_t, __builtin_amdgcn_perm(x[u + 1], x[u], 0x07060302u));
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const bf16x2_t lo = __builtin_bit_cast(bf16x2_t, __builtin_amdgcn_perm(w[u + 1][j], w[u][j], 0x05040100u));
-              const bf16x2_t hi = __builtin_bit_cast(bf16x2_t, __builtin_amdgcn_perm(w[u + 1][j], w[u][j], 0x07060302u));
-              acc[2 * j] = __builtin_amdgcn_fdot2_f32_bf16(vv, lo, acc[2 * j], false);
-              acc[2 * j + 1] = __builtin_amdgcn_fdot2_f32_bf16(vv, hi, acc[2 * j + 1], false);
-            }
-          }
         }
       };
       int e0 = 0;
+      // one round of U loads at a time (unrolled to two rounds, the wave waits on twice as
+      // many loads at once, which measured slower)
+#pragma unroll 1
       for (; e0 + U <= cmin; e0 += U) round(e0, std::false_type{});
       for (; e0 < cmax; e0 += U) round(e0, std::true_type{});
       if (c >= 0) store_slice<OUT>(Y, Yf, tok(i) * d + (int64_t)slice * SLICE2 + sub * 8, acc);
@@ -807,7 +839,7 @@ __global__ __launch_bounds__(256) void k_pack_down(const bf16_t* __restrict__ W,
 
 }  // namespace
 
-static int slice_walk_tpw(int64_t T, int64_t per_tok);
+static int slice_walk_tpw(int64_t T, int64_t per_tok, int64_t lds_budget = GATHER_LDS);
 
 hipError_t launch_gather_down(int val_bf16, int64_t T, int64_t d, int K, const void* ell_val,
                               const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
@@ -840,8 +872,9 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
 
   // rows of at most kTokenGroupK entries in large batches: token-group walk
   const bool groups = K <= kTokenGroupK && T >= kTokenGroupT;
-  const int64_t per_tok = (int64_t)(std::max(K, 1) + (groups ? 1 : 0)) * 4 * (vk + 1) + 4;
-  const int tpw = slice_walk_tpw(T, per_tok);
+  const int64_t per_tok = groups && vk == 0 ? tg_bytes_per_token(std::max(K, 1))
+                                            : (int64_t)(std::max(K, 1) + (groups ? 1 : 0)) * 4 * (vk + 1) + 4;
+  const int tpw = slice_walk_tpw(T, per_tok, groups && vk == 0 ? kTgLds : GATHER_LDS);
   const int64_t blocks = cdiv(T, tpw);
   const size_t lds = (size_t)tpw * per_tok;
   if (lds > 160 * 1024) return hipErrorInvalidValue;
@@ -932,8 +965,8 @@ hipError_t launch_sum_parts(int64_t T, int K, const int32_t* row_nnz, const uint
 // Token blocks of the slice-walking kernels: at most what the LDS budget holds (one
 // workgroup per CU); each block goes to every XCD (each XCD covers its own slices), and the
 // blocks are sized so that each XCD's 32 CUs get whole rounds.
-static int slice_walk_tpw(int64_t T, int64_t per_tok) {
-  const int64_t tpw_max = std::max<int64_t>(1, std::min<int64_t>(GATHER_LDS / 1024, GATHER_LDS / per_tok));
+static int slice_walk_tpw(int64_t T, int64_t per_tok, int64_t lds_budget) {
+  const int64_t tpw_max = std::max<int64_t>(1, std::min<int64_t>(GATHER_LDS / 1024, lds_budget / per_tok));
   const int64_t wg_per_cu = std::max<int64_t>(1, (160 * 1024) / (tpw_max * per_tok));
   const int64_t slots = 32 * std::min<int64_t>(wg_per_cu, 2048 / (GATHER_WAVES * 64));
   const int64_t rounds = cdiv(T, tpw_max * slots);
