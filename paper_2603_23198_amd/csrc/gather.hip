@@ -199,7 +199,7 @@ __host__ __device__ inline int tg_value_stride(int K) {
 #define SFL_TG_LDS 148608
 #endif
 constexpr int64_t kTgLds = SFL_TG_LDS;  // LDS budget of a token-group workgroup (bf16 values)
-__host__ __device__ inline int64_t tg_bytes_per_token(int K) { return (int64_t)(K + 1) * 4 + (int64_t)tg_value_stride(K) * 2 + 4; }
+__host__ __device__ inline int64_t tg_bytes_per_token(int K) { return (int64_t)(K + 1) * 4 + (int64_t)tg_value_stride(K) * 2 + 8; }
 
 // Sum of the 8 groups' partial sums (lanes l, l ^ 8, ..., l ^ 56) into every group: the
 // partner 8 lanes away is in the same 16-lane row (DPP row_ror:8), the other two steps
@@ -345,9 +345,12 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
   // token groups read 8 tokens' entries at once: an odd stride puts them in different banks
   const int KS = TG ? K + 1 : K;
   const int KV = SPLIT ? tg_value_stride(K) : 0;
-  extern __shared__ uint32_t ent[];  // [tpw][KS] entries (offsets), [tpw][KV] bf16 values, [tpw] counts (-1 = skip)
+  // [tpw][KS] entries (offsets), [tpw][KV] bf16 values, [tpw] counts (-1 = skip), then
+  // (SPLIT) [tpw] token rows
+  extern __shared__ uint32_t ent[];
   bf16_t* val_s = (bf16_t*)(ent + (size_t)tpw * KS * EW);
   int* cnt_s = (int*)(val_s + (size_t)tpw * KV);
+  int* tok_s = cnt_s + tpw;
   const int xcd = blockIdx.x & 7;
   const int64_t t0 = (int64_t)(blockIdx.x >> 3) * tpw;
   const int l = threadIdx.x & 63;
@@ -363,10 +366,51 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
   for (int i = threadIdx.x; i < tpw; i += blockDim.x) {
     const int64_t t = tok(i);
     cnt_s[i] = (t < T && !row_ovf[t]) ? row_nnz[t] : -1;
+    if constexpr (SPLIT) tok_s[i] = (int)t;
   }
   __syncthreads();
+  // SPLIT with 16-byte aligned rows of whole 8-entry chunks: the workgroup's chunks are
+  // dealt over all its threads, four loads of each kind in flight per thread (the copy is
+  // one round of load latency rather than one per 64 entries of each token a wave holds)
+  const bool flat = SPLIT && K % 8 == 0 && !part_u && ((((uintptr_t)ell_idx) | ((uintptr_t)ell_val)) & 15) == 0;
+  if constexpr (SPLIT) {
+    if (flat) {
+      constexpr int SU = 4;
+      const int cpt = K >> 3;  // chunks per token row
+      const int nch = tpw * cpt;
+      for (int q0 = threadIdx.x; q0 < nch; q0 += (int)blockDim.x * SU) {
+        u32x4_t vi[SU], vv[SU];
+        int qi[SU], qc[SU];
+        bool ok[SU];
+#pragma unroll
+        for (int u = 0; u < SU; ++u) {
+          const int q = q0 + u * (int)blockDim.x;
+          qi[u] = q / cpt;
+          qc[u] = q - qi[u] * cpt;
+          ok[u] = q < nch && qc[u] * 8 < cnt_s[qi[u]];  // a skipped token's count is -1
+          if (ok[u]) {
+            const int64_t o = (int64_t)tok_s[qi[u]] * K + qc[u] * 8;
+            vi[u] = *(const u32x4_t*)(ell_idx + o);
+            vv[u] = *(const u32x4_t*)((const bf16_t*)ell_val + o);
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < SU; ++u) {
+          if (!ok[u]) continue;
+          uint32_t* eo = ent + qi[u] * KS + qc[u] * 8;
+          uint32_t* vo = (uint32_t*)(val_s + qi[u] * KV + qc[u] * 8);  // KV and 8 qc even: 4-byte aligned
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            eo[2 * k] = (vi[u][k] & 0xffffu) * row_b;
+            eo[2 * k + 1] = (vi[u][k] >> 16) * row_b;
+            vo[k] = vv[u][k];
+          }
+        }
+      }
+    }
+  }
   float l1 = 0.f;
-  for (int i = wave; i < tpw; i += GATHER_WAVES) {
+  for (int i = flat ? tpw : wave; i < tpw; i += GATHER_WAVES) {
     const int c = cnt_s[i];
     const int64_t t = tok(i);
     for (int e = l; e < c; e += 64) {
