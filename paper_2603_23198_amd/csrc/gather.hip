@@ -571,7 +571,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gated_updot(
     int64_t T, int64_t d, int64_t f, int K, const uint16_t* __restrict__ ell_idx, const int32_t* __restrict__ row_nnz,
     const uint8_t* __restrict__ row_ovf, const bf16_t* __restrict__ X, const bf16_t* __restrict__ WuP,
     float* __restrict__ part_u, int n_slices, int tpw, const int32_t* __restrict__ order) {
-  // [tpw][K] indices, [ncopy][tpw][K] partial sums, [tpw] counts. With ncopy = 1 a token's
+  // [tpw][K] indices, [ncopy][tpw][K] partial sums, [tpw] counts, [tpw] token rows. With ncopy = 1 a token's
   // slices are handled by one wave in order; a small block (decode) deals (slice, token)
   // items to all waves, each slice with its own copy of the sums, added in slice order.
   extern __shared__ uint32_t ent[];
@@ -588,12 +588,50 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gated_updot(
     const int64_t q = t0 + i;
     return q < T ? (order ? (int64_t)order[q] : q) : T;
   };
+  int* tok_s = cnt_s + tpw;
   for (int i = threadIdx.x; i < tpw; i += blockDim.x) {
     const int64_t t = tok(i);
     cnt_s[i] = (t < T && !row_ovf[t]) ? row_nnz[t] : -1;
+    tok_s[i] = (int)t;
   }
   __syncthreads();
-  for (int i = wave; i < tpw; i += GATHER_WAVES) {
+  // rows of whole 8-entry chunks, 16-byte aligned: the chunks are dealt over all threads,
+  // four loads in flight per thread (one round of latency, as in the token-group gather)
+  const bool flat = K % 8 == 0 && (((uintptr_t)ell_idx) & 15) == 0;
+  if (flat) {
+    constexpr int SU = 4;
+    const int cpt = K >> 3;
+    const int nch = tpw * cpt;
+    for (int q0 = threadIdx.x; q0 < nch; q0 += (int)blockDim.x * SU) {
+      u32x4_t vi[SU];
+      int qi[SU], qc[SU];
+      bool ok[SU];
+#pragma unroll
+      for (int u = 0; u < SU; ++u) {
+        const int q = q0 + u * (int)blockDim.x;
+        qi[u] = q / cpt;
+        qc[u] = q - qi[u] * cpt;
+        ok[u] = q < nch && qc[u] * 8 < cnt_s[qi[u]];
+        if (ok[u]) vi[u] = *(const u32x4_t*)(ell_idx + (int64_t)tok_s[qi[u]] * K + qc[u] * 8);
+      }
+#pragma unroll
+      for (int u = 0; u < SU; ++u) {
+        if (!ok[u]) continue;
+        uint32_t* eo = ent + qi[u] * K + qc[u] * 8;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          eo[2 * k] = vi[u][k] & 0xffffu;
+          eo[2 * k + 1] = vi[u][k] >> 16;
+        }
+        for (int cp = 0; cp < ncopy; ++cp) {
+          f32x4_t* z = (f32x4_t*)(us + ((size_t)cp * tpw + qi[u]) * K + qc[u] * 8);
+          z[0] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+          z[1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        }
+      }
+    }
+  }
+  for (int i = flat ? tpw : wave; i < tpw; i += GATHER_WAVES) {
     const int c = cnt_s[i];
     const int64_t t = tok(i);
     for (int e = l; e < c; e += 64) {
@@ -1022,7 +1060,7 @@ hipError_t launch_gated_updot(int64_t T, int64_t d, int64_t f, int K, const uint
                               const int32_t* order) {
   if (T == 0) return hipSuccess;
   if (d % (8 * SLICE2) != 0) return hipErrorInvalidValue;
-  const int64_t per_tok = (int64_t)std::max(K, 1) * 8 + 4;
+  const int64_t per_tok = (int64_t)std::max(K, 1) * 8 + 8;
   const int tpw = slice_walk_tpw(T, per_tok);
   const int64_t blocks = cdiv(T, tpw);
   const int nsl_max = (int)cdiv(d / SLICE2, 8);
