@@ -517,7 +517,11 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
 #pragma unroll 1
       for (; e0 + U <= cmin; e0 += U) round(e0, std::false_type{});
       for (; e0 < cmax; e0 += U) round(e0, std::true_type{});
-      if (c >= 0) store_slice<OUT>(Y, Yf, tok(i) * d + (int64_t)slice * SLICE2 + sub * 8, acc);
+      if (c >= 0) {
+        // the token's row (SPLIT: from LDS, not the processing order in global memory)
+        const int64_t t = SPLIT ? (int64_t)tok_s[i] : tok(i);
+        store_slice<OUT>(Y, Yf, t * d + (int64_t)slice * SLICE2 + sub * 8, acc);
+      }
     }
     return;
   }
@@ -746,7 +750,8 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_unit
                                                                   const float* __restrict__ val,
                                                                   const bf16_t* __restrict__ G, float* __restrict__ out,
                                                                   int n_slices, int upw, int lds_pairs) {
-  extern __shared__ uint32_t ent[];  // [lds_pairs][2]
+  extern __shared__ uint32_t ent[];  // [lds_pairs][2], then the block's list offsets [upw + 1]
+  int* ptr_s = (int*)(ent + 2 * (size_t)lds_pairs);
   const int xcd = blockIdx.x & 7;
   const int64_t u0 = (int64_t)(blockIdx.x >> 3) * upw;
   const int l = threadIdx.x & 63;
@@ -759,13 +764,32 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_unit
   const int pb = ptr[u0];
   const int n_ent = ptr[u0 + nu] - pb;
   const bool staged = n_ent <= lds_pairs;  // uniform over the block
+  for (int k = threadIdx.x; k <= nu; k += blockDim.x) ptr_s[k] = ptr[u0 + k];
   if (staged) {
-    for (int e = threadIdx.x; e < n_ent; e += blockDim.x) {
-      ent[2 * e] = (uint32_t)tok[pb + e];
-      ent[2 * e + 1] = __float_as_uint(val[pb + e]);
+    // eight entries in flight per thread: the copy takes one or two rounds of load latency
+    constexpr int SU = 8;
+    for (int e0 = threadIdx.x; e0 < n_ent; e0 += (int)blockDim.x * SU) {
+      int tk[SU];
+      float vl[SU];
+#pragma unroll
+      for (int u = 0; u < SU; ++u) {
+        const int e = e0 + u * (int)blockDim.x;
+        if (e < n_ent) {
+          tk[u] = tok[pb + e];
+          vl[u] = val[pb + e];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < SU; ++u) {
+        const int e = e0 + u * (int)blockDim.x;
+        if (e < n_ent) {
+          ent[2 * e] = (uint32_t)tk[u];
+          ent[2 * e + 1] = __float_as_uint(vl[u]);
+        }
+      }
     }
-    __syncthreads();
   }
+  __syncthreads();
   if (TG && staged) {
     // unit groups: a work item is (slice, NGRP units), lane group g summing unit g's list
     // in list order on its own (no fold); the wave runs to the longest of the lists
@@ -775,8 +799,8 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_unit
       const int ui = (it % n_grp) * NGRP + grp;
       const bool have = ui < nu;
       const int64_t n = u0 + (have ? ui : 0);
-      const int p0 = ptr[n];
-      const int cnt = have ? ptr[n + 1] - p0 : 0;
+      const int p0 = ptr_s[have ? ui : 0];
+      const int cnt = have ? ptr_s[ui + 1] - p0 : 0;
       int cmax = cnt, cmin = have ? cnt : 0;
 #pragma unroll
       for (int o = 8; o < 64; o <<= 1) {
@@ -824,8 +848,8 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_unit
     const int slice = xcd + 8 * (it / nu);
     const int64_t n = u0 + it % nu;
     const uint32_t col_b = (uint32_t)(slice * R * SLICE2 * 2) + (uint32_t)sub * 16u;
-    const int p0 = __builtin_amdgcn_readfirstlane(ptr[n]);
-    const int cnt = __builtin_amdgcn_readfirstlane(ptr[n + 1]) - p0;
+    const int p0 = __builtin_amdgcn_readfirstlane(ptr_s[n - u0]);
+    const int cnt = __builtin_amdgcn_readfirstlane(ptr_s[n - u0 + 1]) - p0;
     float acc[8];
     if (staged) {
       slice_token_f32<GU>(ent + 2 * (p0 - pb), cnt, gr, col_b, grp, acc);
@@ -1012,16 +1036,18 @@ hipError_t launch_csc_gather(int64_t n_units, int64_t d, int64_t R, const int32_
   // non-gated step, where the fold is already amortised and the groups' lists differ more
   const bool groups = mean_bound <= kUnitGroupBound;
   const void* kern = groups ? (const void*)k_csc_gather<true> : (const void*)k_csc_gather<false>;
-  if (GATHER_LDS > 65536) {
-    const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, GATHER_LDS);
+  const size_t lds = (size_t)lds_pairs * 8 + (size_t)(upw + 1) * 4;  // the pairs, then the list offsets
+  if (lds > 160 * 1024) return hipErrorInvalidValue;
+  if (lds > 65536) {
+    const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
   const dim3 grid((unsigned)(8 * blocks)), block(GATHER_WAVES * 64);
   if (groups)
-    hipLaunchKernelGGL(k_csc_gather<true>, grid, block, (size_t)GATHER_LDS, s, n_units, d, R, ptr, tok, val,
+    hipLaunchKernelGGL(k_csc_gather<true>, grid, block, lds, s, n_units, d, R, ptr, tok, val,
                        (const bf16_t*)Gp, out, (int)(d / SLICE2), upw, lds_pairs);
   else
-    hipLaunchKernelGGL(k_csc_gather<false>, grid, block, (size_t)GATHER_LDS, s, n_units, d, R, ptr, tok, val,
+    hipLaunchKernelGGL(k_csc_gather<false>, grid, block, lds, s, n_units, d, R, ptr, tok, val,
                        (const bf16_t*)Gp, out, (int)(d / SLICE2), upw, lds_pairs);
   return hipGetLastError();
 }
