@@ -346,7 +346,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
   const int KS = TG ? K + 1 : K;
   const int KV = SPLIT ? tg_value_stride(K) : 0;
   // [tpw][KS] entries (offsets), [tpw][KV] bf16 values, [tpw] counts (-1 = skip), then
-  // (SPLIT) [tpw] token rows
+  // (token groups) [tpw] token rows
   extern __shared__ uint32_t ent[];
   bf16_t* val_s = (bf16_t*)(ent + (size_t)tpw * KS * EW);
   int* cnt_s = (int*)(val_s + (size_t)tpw * KV);
@@ -366,20 +366,20 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
   for (int i = threadIdx.x; i < tpw; i += blockDim.x) {
     const int64_t t = tok(i);
     cnt_s[i] = (t < T && !row_ovf[t]) ? row_nnz[t] : -1;
-    if constexpr (SPLIT) tok_s[i] = (int)t;
+    if constexpr (TG) tok_s[i] = (int)t;
   }
   __syncthreads();
-  // SPLIT with 16-byte aligned rows of whole 8-entry chunks: the workgroup's chunks are
-  // dealt over all its threads, four loads of each kind in flight per thread (the copy is
-  // one round of load latency rather than one per 64 entries of each token a wave holds)
-  const bool flat = SPLIT && K % 8 == 0 && !part_u && ((((uintptr_t)ell_idx) | ((uintptr_t)ell_val)) & 15) == 0;
-  if constexpr (SPLIT) {
+  // Token groups with 16-byte aligned rows of whole 8-entry chunks: the workgroup's chunks
+  // are dealt over all its threads, four chunks in flight per thread (the copy is one
+  // round of load latency rather than one per 64 entries of each token a wave holds)
+  const bool flat = TG && K % 8 == 0 && !part_u && ((((uintptr_t)ell_idx) | ((uintptr_t)ell_val)) & 15) == 0;
+  if constexpr (TG) {
     if (flat) {
       constexpr int SU = 4;
       const int cpt = K >> 3;  // chunks per token row
       const int nch = tpw * cpt;
       for (int q0 = threadIdx.x; q0 < nch; q0 += (int)blockDim.x * SU) {
-        u32x4_t vi[SU], vv[SU];
+        u32x4_t vi[SU], vv[SU][VK + 1];  // indices; values (bf16: one vector, fp32: two)
         int qi[SU], qc[SU];
         bool ok[SU];
 #pragma unroll
@@ -391,19 +391,32 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
           if (ok[u]) {
             const int64_t o = (int64_t)tok_s[qi[u]] * K + qc[u] * 8;
             vi[u] = *(const u32x4_t*)(ell_idx + o);
-            vv[u] = *(const u32x4_t*)((const bf16_t*)ell_val + o);
+            if constexpr (VK == 0) {
+              vv[u][0] = *(const u32x4_t*)((const bf16_t*)ell_val + o);
+            } else {
+              vv[u][0] = *(const u32x4_t*)((const float*)ell_val + o);
+              vv[u][1] = *(const u32x4_t*)((const float*)ell_val + o + 4);
+            }
           }
         }
 #pragma unroll
         for (int u = 0; u < SU; ++u) {
           if (!ok[u]) continue;
-          uint32_t* eo = ent + qi[u] * KS + qc[u] * 8;
-          uint32_t* vo = (uint32_t*)(val_s + qi[u] * KV + qc[u] * 8);  // KV and 8 qc even: 4-byte aligned
+          uint32_t* eo = ent + (size_t)EW * (qi[u] * KS + qc[u] * 8);
+          if constexpr (SPLIT) {
+            uint32_t* vo = (uint32_t*)(val_s + qi[u] * KV + qc[u] * 8);  // KV and 8 qc even: 4-byte aligned
 #pragma unroll
-          for (int k = 0; k < 4; ++k) {
-            eo[2 * k] = (vi[u][k] & 0xffffu) * row_b;
-            eo[2 * k + 1] = (vi[u][k] >> 16) * row_b;
-            vo[k] = vv[u][k];
+            for (int k = 0; k < 4; ++k) {
+              eo[2 * k] = (vi[u][k] & 0xffffu) * row_b;
+              eo[2 * k + 1] = (vi[u][k] >> 16) * row_b;
+              vo[k] = vv[u][0][k];
+            }
+          } else {
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+              eo[2 * k] = (k & 1) ? vi[u][k >> 1] >> 16 : vi[u][k >> 1] & 0xffffu;
+              eo[2 * k + 1] = vv[u][k >> 2][k & 3];
+            }
           }
         }
       }
@@ -518,8 +531,8 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gather_down_b16(
       for (; e0 + U <= cmin; e0 += U) round(e0, std::false_type{});
       for (; e0 < cmax; e0 += U) round(e0, std::true_type{});
       if (c >= 0) {
-        // the token's row (SPLIT: from LDS, not the processing order in global memory)
-        const int64_t t = SPLIT ? (int64_t)tok_s[i] : tok(i);
+        // the token's row, from LDS (not the processing order in global memory)
+        const int64_t t = tok_s[i];
         store_slice<OUT>(Y, Yf, t * d + (int64_t)slice * SLICE2 + sub * 8, acc);
       }
     }
@@ -978,8 +991,9 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
 
   // rows of at most kTokenGroupK entries in large batches: token-group walk
   const bool groups = K <= kTokenGroupK && T >= kTokenGroupT;
+  // token groups also keep each token's row in LDS
   const int64_t per_tok = groups && vk == 0 ? tg_bytes_per_token(std::max(K, 1))
-                                            : (int64_t)(std::max(K, 1) + (groups ? 1 : 0)) * 4 * (vk + 1) + 4;
+                                            : (int64_t)(std::max(K, 1) + (groups ? 1 : 0)) * 4 * (vk + 1) + (groups ? 8 : 4);
   const int tpw = slice_walk_tpw(T, per_tok, groups && vk == 0 ? kTgLds : GATHER_LDS);
   const int64_t blocks = cdiv(T, tpw);
   const size_t lds = (size_t)tpw * per_tok;
