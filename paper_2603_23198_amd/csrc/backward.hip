@@ -29,6 +29,7 @@ namespace sfl {
 namespace {
 
 constexpr int kBlkTok = 64;  // tokens per block of the counting sort
+constexpr int64_t kUnitOrderBuckets = 16382;  // at most this many list lengths told apart by the unit order
 
 // ---- 3. transposed pattern (counting sort in token order) -----------------------------
 // (a) per block of 64 tokens and per unit: which of the block's sparse rows activate it,
@@ -84,15 +85,20 @@ __global__ __launch_bounds__(256) void k_blk_scan(int64_t nb, int64_t f, int32_t
   col_cnt[n] = run;
 }
 
-// (c) exclusive scan of the unit totals -> col_ptr[f + 1] (one workgroup).
+// (c) the units' lists laid out in the processing order uorder (the units by descending
+// list length, so that the lists a per-unit gather walks side by side are of about equal
+// length): exclusive scan of the totals in that order -> col_ptr[f + 1] (list k of the
+// layout is unit uorder[k]), and each unit's start colstart[n] (one workgroup).
 __global__ __launch_bounds__(1024) void k_col_ptr(int64_t f, const int32_t* __restrict__ col_cnt,
-                                                  int32_t* __restrict__ col_ptr) {
+                                                  const int32_t* __restrict__ uorder, int32_t* __restrict__ col_ptr,
+                                                  int32_t* __restrict__ colstart) {
   __shared__ int wsum[16];
   const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
   int base = 0;
   for (int64_t r0 = 0; r0 < f; r0 += 1024) {
-    const int64_t n = r0 + tid;
-    const int c = n < f ? col_cnt[n] : 0;
+    const int64_t k = r0 + tid;
+    const int64_t n = k < f ? uorder[k] : 0;
+    const int c = k < f ? col_cnt[n] : 0;
     const int incl = wave_incl_scan(c);
     if (l == 63) wsum[w] = incl;
     __syncthreads();
@@ -101,14 +107,17 @@ __global__ __launch_bounds__(1024) void k_col_ptr(int64_t f, const int32_t* __re
       before += (i < w) ? wsum[i] : 0;
       all += wsum[i];
     }
-    if (n < f) col_ptr[n] = base + before + incl - c;
+    if (k < f) {
+      col_ptr[k] = base + before + incl - c;
+      colstart[n] = base + before + incl - c;
+    }
     base += all;
     __syncthreads();
   }
   if (tid == 0) col_ptr[f] = base;
 }
 
-// (d) fill: entry (t, e) with unit n goes to position col_ptr[n] + (offset of t's block
+// (d) fill: entry (t, e) with unit n goes to position colstart[n] + (offset of t's block
 // in n's list) + (the block's earlier tokens that activate n: the mask's bits below t),
 // i.e. each unit's list in token order. Every entry is placed independently (one wave
 // per token). Up to three per-entry values go beside the token (fp32 sources [T][K];
@@ -123,7 +132,7 @@ __global__ __launch_bounds__(256) void k_blk_fill(int64_t T, int K, int64_t f, c
                                                   const int32_t* __restrict__ row_nnz,
                                                   const uint8_t* __restrict__ row_ovf,
                                                   const uint64_t* __restrict__ bm, const int32_t* __restrict__ bc,
-                                                  const int32_t* __restrict__ col_ptr, int32_t* __restrict__ csc_tok,
+                                                  const int32_t* __restrict__ colstart, int32_t* __restrict__ csc_tok,
                                                   FillValues fv) {
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int l = threadIdx.x & 63;
@@ -135,7 +144,7 @@ __global__ __launch_bounds__(256) void k_blk_fill(int64_t T, int K, int64_t f, c
   for (int e = l; e < nnz; e += 64) {
     const int64_t src = t * (int64_t)K + e;
     const int64_t n = ell_idx[src];
-    const int pos = col_ptr[n] + bc[b * f + n] + __popcll(bm[b * f + n] & below);
+    const int pos = colstart[n] + bc[b * f + n] + __popcll(bm[b * f + n] & below);
     csc_tok[pos] = (int32_t)t;
     if (fv.out[0]) fv.out[0][pos] = fv.hb ? bf16_to_f32(fv.hb[src]) : fv.v[0][src];
     if (fv.out[1]) fv.out[1][pos] = fv.v[1][src];
@@ -192,7 +201,9 @@ struct BwdPlan {
   int32_t* bc = nullptr;      // [nb][f]
   uint64_t* bm = nullptr;     // [nb][f] per-block token masks
   int32_t* col_cnt = nullptr; // [f]
-  int32_t* col_ptr = nullptr; // [f + 1]
+  int32_t* col_ptr = nullptr; // [f + 1] list starts in the processing order
+  int32_t* uorder = nullptr;  // [f] the units by descending list length
+  int32_t* colstart = nullptr; // [f] list start of each unit
   int32_t* csc_tok = nullptr; // [T K]
   float* csc_h = nullptr;     // [T K] h
   float* csc_z = nullptr;     // [T K] dz (gated: dh_u)
@@ -241,6 +252,8 @@ BwdPlan plan_backward(const sfl_ffn_bwd_args_t& a, void* ws) {
   p.bm = (uint64_t*)take((size_t)nb * f * 8);
   p.col_cnt = (int32_t*)take((size_t)f * 4);
   p.col_ptr = (int32_t*)take((size_t)(f + 1) * 4);
+  p.uorder = (int32_t*)take((size_t)f * 4);
+  p.colstart = (int32_t*)take((size_t)f * 4);
   p.csc_tok = (int32_t*)take((size_t)T * K * 4);
   p.csc_h = (float*)take((size_t)T * K * 4);
   p.csc_z = (float*)take((size_t)T * K * 4);
@@ -399,7 +412,11 @@ sfl_status_t backward_run(const sfl_ffn_bwd_args_t* a, hipStream_t s) {
   }
   hipLaunchKernelGGL(k_blk_scan, dim3((unsigned)cdiv(f, 256)), dim3(256), 0, s, nb, f, p.bc, p.col_cnt);
   SFL_HIPB(hipGetLastError());
-  hipLaunchKernelGGL(k_col_ptr, dim3(1), dim3(1024), 0, s, f, p.col_cnt, p.col_ptr);
+  // units by descending list length; lists of more than four times the bound on the mean
+  // length (T K / f) share the first bucket (fewer buckets: a shorter scan in the sort)
+  const int64_t order_buckets = std::min<int64_t>({T, 4 * cdiv(T * (int64_t)K, f), kUnitOrderBuckets});
+  SFL_HIPB(launch_nnz_order(f, (int)order_buckets, p.col_cnt, nullptr, p.uorder, s));
+  hipLaunchKernelGGL(k_col_ptr, dim3(1), dim3(1024), 0, s, f, p.col_cnt, p.uorder, p.col_ptr, p.colstart);
   SFL_HIPB(hipGetLastError());
   FillValues fv;
   std::memset(&fv, 0, sizeof(fv));
@@ -415,18 +432,18 @@ sfl_status_t backward_run(const sfl_ffn_bwd_args_t* a, hipStream_t s) {
   fv.out[0] = p.csc_h;
   fv.out[1] = p.csc_z;
   hipLaunchKernelGGL(k_blk_fill, dim3((unsigned)cdiv(T, 4)), dim3(256), 0, s, T, K, f, sv.ell_idx, sv.row_nnz,
-                     sv.row_ovf, p.bm, p.bc, p.col_ptr, p.csc_tok, fv);
+                     sv.row_ovf, p.bm, p.bc, p.colstart, p.csc_tok, fv);
   SFL_HIPB(hipGetLastError());
   rec(3);
   // 4. weight gradients of the sparse rows: per-unit gathers over slice-major dY and X
   SFL_HIPB(launch_pack_down(dY, p.dYP, T, d, s));
   SFL_HIPB(launch_pack_down(X, p.XP, T, d, s));
   const int64_t mean_bound = cdiv(T * (int64_t)K, f);  // the lists hold at most T K entries
-  SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, p.csc_tok, p.csc_h, mean_bound, p.dYP, a->dW_down, s));
-  SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, p.csc_tok, p.csc_z, mean_bound, p.XP, p.dWuT, s));
+  SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, p.csc_tok, p.csc_h, mean_bound, p.dYP, a->dW_down, s, p.uorder));
+  SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, p.csc_tok, p.csc_z, mean_bound, p.XP, p.dWuT, s, p.uorder));
   SFL_HIPB(launch_transpose(p.dWuT, a->dW_up, f, d, 4, s));
   if (gated) {
-    SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, p.csc_tok, p.csc_g, mean_bound, p.XP, p.dWgT, s));
+    SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, p.csc_tok, p.csc_g, mean_bound, p.XP, p.dWgT, s, p.uorder));
     SFL_HIPB(launch_transpose(p.dWgT, a->dW_gate, f, d, 4, s));
   }
   rec(4);

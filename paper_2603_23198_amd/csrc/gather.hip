@@ -181,8 +181,10 @@ constexpr int64_t kTokenGroupT = 1024;
 #define SFL_GROUP_UNROLL 4
 #endif
 constexpr int GU_GROUP = SFL_GROUP_UNROLL;  // row loads per lane in flight in the group walks
-// The backward's per-unit gathers group units the same way when their lists are short.
-constexpr int64_t kUnitGroupBound = 128;
+// The backward's per-unit gathers group units the same way when their lists are short
+// (bounded by 256 entries on average; the lists come in descending length order, so the
+// 8 lists of a work item are of about equal length).
+constexpr int64_t kUnitGroupBound = 256;
 // The forward's token-group walk stages each entry as its W_down row's byte offset
 // (uint32, rows of KS = K + 1 words) and its bf16 value (rows of KV values): the offset
 // then needs one add per load, and two consecutive values are read as the bf16 pair of a
@@ -762,7 +764,8 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_unit
                                                                   const int32_t* __restrict__ tok,
                                                                   const float* __restrict__ val,
                                                                   const bf16_t* __restrict__ G, float* __restrict__ out,
-                                                                  int n_slices, int upw, int lds_pairs) {
+                                                                  int n_slices, int upw, int lds_pairs,
+                                                                  const int32_t* __restrict__ out_rows) {
   extern __shared__ uint32_t ent[];  // [lds_pairs][2], then the block's list offsets [upw + 1]
   int* ptr_s = (int*)(ent + 2 * (size_t)lds_pairs);
   const int xcd = blockIdx.x & 7;
@@ -850,7 +853,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_unit
       for (; e0 + GU_GROUP <= cmin; e0 += GU_GROUP) round(e0, std::false_type{});
       for (; e0 < cmax; e0 += GU_GROUP) round(e0, std::true_type{});
       if (have) {
-        float* o = out + n * d + (int64_t)slice * SLICE2 + sub * 8;
+        float* o = out + (out_rows ? (int64_t)out_rows[n] : n) * d + (int64_t)slice * SLICE2 + sub * 8;
         *(f32x4_t*)o = f32x4_t{acc[0], acc[1], acc[2], acc[3]};
         *(f32x4_t*)(o + 4) = f32x4_t{acc[4], acc[5], acc[6], acc[7]};
       }
@@ -892,7 +895,7 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_unit
       fold_groups(acc);
     }
     if (grp == 0) {
-      float* o = out + n * d + (int64_t)slice * SLICE2 + sub * 8;
+      float* o = out + (out_rows ? (int64_t)out_rows[n] : n) * d + (int64_t)slice * SLICE2 + sub * 8;
       *(f32x4_t*)o = f32x4_t{acc[0], acc[1], acc[2], acc[3]};
       *(f32x4_t*)(o + 4) = f32x4_t{acc[4], acc[5], acc[6], acc[7]};
     }
@@ -1035,7 +1038,8 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
 }
 
 hipError_t launch_csc_gather(int64_t n_units, int64_t d, int64_t R, const int32_t* ptr, const int32_t* tok,
-                             const float* val, int64_t mean_bound, const void* Gp, float* out, hipStream_t s) {
+                             const float* val, int64_t mean_bound, const void* Gp, float* out, hipStream_t s,
+                             const int32_t* out_rows) {
   if (n_units == 0) return hipSuccess;
   if (d % (8 * SLICE2) != 0) return hipErrorInvalidValue;
   // units per block: lists of mean_bound entries (an upper bound of the mean list length)
@@ -1046,8 +1050,8 @@ hipError_t launch_csc_gather(int64_t n_units, int64_t d, int64_t R, const int32_
   const int64_t blocks = cdiv(n_units, upw);
   // short lists: one unit per lane group (no fold). Measured against the per-unit walk:
   // lists of about 41 entries (bound 74) 1.64 -> 1.26 ms for the gated step's three
-  // gathers, lists of about 164 entries (bound 256) 2.58 -> 2.75 ms for the two of the
-  // non-gated step, where the fold is already amortised and the groups' lists differ more
+  // gathers; lists of about 164 entries (bound 256), the two of the non-gated step, 2.58
+  // -> 2.75 ms in unit order, 2.53 -> 2.41 ms once the lists come by descending length
   const bool groups = mean_bound <= kUnitGroupBound;
   const void* kern = groups ? (const void*)k_csc_gather<true> : (const void*)k_csc_gather<false>;
   const size_t lds = (size_t)lds_pairs * 8 + (size_t)(upw + 1) * 4;  // the pairs, then the list offsets
@@ -1059,10 +1063,10 @@ hipError_t launch_csc_gather(int64_t n_units, int64_t d, int64_t R, const int32_
   const dim3 grid((unsigned)(8 * blocks)), block(GATHER_WAVES * 64);
   if (groups)
     hipLaunchKernelGGL(k_csc_gather<true>, grid, block, lds, s, n_units, d, R, ptr, tok, val,
-                       (const bf16_t*)Gp, out, (int)(d / SLICE2), upw, lds_pairs);
+                       (const bf16_t*)Gp, out, (int)(d / SLICE2), upw, lds_pairs, out_rows);
   else
     hipLaunchKernelGGL(k_csc_gather<false>, grid, block, lds, s, n_units, d, R, ptr, tok, val,
-                       (const bf16_t*)Gp, out, (int)(d / SLICE2), upw, lds_pairs);
+                       (const bf16_t*)Gp, out, (int)(d / SLICE2), upw, lds_pairs, out_rows);
   return hipGetLastError();
 }
 

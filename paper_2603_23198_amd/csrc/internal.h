@@ -138,8 +138,9 @@ hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32
 // Zeroes the statistics (if given) and n_zero counters from zero.
 hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s, int32_t* zero = nullptr, int n_zero = 0);
 // order[0 .. T): the sparse rows by descending row_nnz, then the dense-backup rows (one
-// workgroup, counting sort over K + 2 buckets; order within a bucket unspecified). Fails
-// with hipErrorInvalidValue when K + 2 buckets do not fit the kernel's LDS histogram.
+// workgroup, counting sort over K + 2 buckets; order within a bucket unspecified; with
+// row_ovf null every row counts as sparse and counts above K share the first bucket).
+// Fails with hipErrorInvalidValue when K + 2 buckets do not fit the kernel's LDS histogram.
 bool nnz_order_supported(int K);
 hipError_t launch_nnz_order(int64_t T, int K, const int32_t* row_nnz, const uint8_t* row_ovf, int32_t* order,
                             hipStream_t s);
@@ -198,11 +199,12 @@ hipError_t launch_pack_down(const void* W, void* out, int64_t f, int64_t d, hipS
 hipError_t launch_gated_updot(int64_t T, int64_t d, int64_t f, int K, const uint16_t* ell_idx, const int32_t* row_nnz,
                               const uint8_t* row_ovf, const void* X, const void* WuP, float* part_u, hipStream_t s,
                               const int32_t* order = nullptr);
-// Backward per-unit gathers: out[n][:] = sum_e val[e] G[tok[e]][:] over n's list
-// [ptr[n], ptr[n+1]), G slice-major [d/64][R][64] bf16, out fp32 [n_units][d]; mean_bound
-// bounds the mean list length (sizes the blocks).
+// Backward per-unit gathers: out[r][:] = sum_e val[e] G[tok[e]][:] over list k's entries
+// [ptr[k], ptr[k+1]), r = out_rows[k] (or k when null), G slice-major [d/64][R][64] bf16,
+// out fp32 [n_units][d]; mean_bound bounds the mean list length (sizes the blocks).
 hipError_t launch_csc_gather(int64_t n_units, int64_t d, int64_t R, const int32_t* ptr, const int32_t* tok,
-                             const float* val, int64_t mean_bound, const void* Gp, float* out, hipStream_t s);
+                             const float* val, int64_t mean_bound, const void* Gp, float* out, hipStream_t s,
+                             const int32_t* out_rows = nullptr);
 // out[t][e] = sum of the 8 partials [8][T][K] + add on the sparse rows' entries (fp32).
 hipError_t launch_sum_parts(int64_t T, int K, const int32_t* row_nnz, const uint8_t* row_ovf, const float* part,
                             float add, float* out, hipStream_t s);

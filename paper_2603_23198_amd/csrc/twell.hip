@@ -358,7 +358,8 @@ hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s, int32_t* zero, i
 }
 
 // Processing order of the tokens for the sparse down projection: the sparse rows by
-// descending row count, then the dense-backup rows (which the gathers skip). A counting
+// descending row count, then the dense-backup rows (which the gathers skip; row_ovf may
+// be null: no such rows, and counts above K share the first bucket). A counting
 // sort in one workgroup: bucket K - n for a sparse row of n entries (n <= K), bucket K + 1
 // for a dense-backup row; histogram in LDS, exclusive scan over the buckets, then each
 // token placed at its bucket's cursor (LDS atomics, so the order within a bucket varies;
@@ -372,7 +373,7 @@ __global__ __launch_bounds__(1024) void k_nnz_order(int64_t T, int K, const int3
   __shared__ int wsum[16];
   const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
   const int nb = K + 2;
-  auto bucket = [&](int64_t t) { return row_ovf[t] ? K + 1 : K - min(max(row_nnz[t], 0), K); };
+  auto bucket = [&](int64_t t) { return row_ovf && row_ovf[t] ? K + 1 : K - min(max(row_nnz[t], 0), K); };
   for (int i = tid; i < nb; i += 1024) hist[i] = 0;
   __syncthreads();
   for (int64_t t = tid; t < T; t += 1024) atomicAdd(&hist[bucket(t)], 1);
