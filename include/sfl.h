@@ -32,10 +32,12 @@
  *    over square blocks of tiles (the paper's persistent-GEMM schedule) where the
  *    tile grid is made of such squares, and in an XCD-grouped order otherwise;
  *    SFL_GEMM_TILE_ORDER=grouped selects the grouped order everywhere. Results are
- *    identical (each tile's sums do not depend on the order). sfl_ffn_forward's sparse down projection (and the gated up-dots)
- *    deals the tokens by descending row count (one more kernel, a counting sort) for
- *    batches of at least 1024 tokens with ell_width <= 256, and in token order
- *    otherwise; SFL_TOKEN_ORDER=nnz or SFL_TOKEN_ORDER=token forces one of the two.
+ *    identical (each tile's sums do not depend on the order). The gathers over the
+ *    sparse rows (sfl_ffn_forward's down projection and gated up-dots, and
+ *    sfl_ffn_backward's dz up-dots and dX gathers) deal the tokens by descending row
+ *    count (one more kernel, a counting sort) for batches of at least 1024 tokens with
+ *    ell_width <= 256, and in token order otherwise; SFL_TOKEN_ORDER=nnz or
+ *    SFL_TOKEN_ORDER=token forces one of the two.
  *    Results are identical either way. Both variables are read on every call; they
  *    are meant for schedule comparisons.
  *  - Dense fallback: a non-gated bf16 sfl_ffn_forward of more than 256 tokens whose

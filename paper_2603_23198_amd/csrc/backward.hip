@@ -22,6 +22,7 @@
 #include "internal.h"
 
 #include <algorithm>
+#include <cstdlib>
 #include <cstring>
 
 namespace sfl {
@@ -30,6 +31,15 @@ namespace {
 
 constexpr int kBlkTok = 64;  // tokens per block of the counting sort
 constexpr int64_t kUnitOrderBuckets = 16382;  // at most this many list lengths told apart by the unit order
+
+// The forward's rule for the descending row-count token order (read per call).
+bool token_order(int64_t T, int K) {
+  if (!nnz_order_supported(K)) return false;
+  const char* e = std::getenv("SFL_TOKEN_ORDER");
+  if (e && std::strcmp(e, "nnz") == 0) return true;
+  if (e && std::strcmp(e, "token") == 0) return false;
+  return T >= 1024 && K <= 256;
+}
 
 // ---- 3. transposed pattern (counting sort in token order) -----------------------------
 // (a) per block of 64 tokens and per unit: which of the block's sparse rows activate it,
@@ -203,6 +213,7 @@ struct BwdPlan {
   int32_t* col_cnt = nullptr; // [f]
   int32_t* col_ptr = nullptr; // [f + 1] list starts in the processing order
   int32_t* uorder = nullptr;  // [f] the units by descending list length
+  int32_t* order = nullptr;   // [T] the tokens by descending row count (token-group walks)
   int32_t* colstart = nullptr; // [f] list start of each unit
   int32_t* csc_tok = nullptr; // [T K]
   float* csc_h = nullptr;     // [T K] h
@@ -253,6 +264,7 @@ BwdPlan plan_backward(const sfl_ffn_bwd_args_t& a, void* ws) {
   p.col_cnt = (int32_t*)take((size_t)f * 4);
   p.col_ptr = (int32_t*)take((size_t)(f + 1) * 4);
   p.uorder = (int32_t*)take((size_t)f * 4);
+  p.order = (int32_t*)take((size_t)T * 4);
   p.colstart = (int32_t*)take((size_t)f * 4);
   p.csc_tok = (int32_t*)take((size_t)T * K * 4);
   p.csc_h = (float*)take((size_t)T * K * 4);
@@ -378,28 +390,37 @@ sfl_status_t backward_run(const sfl_ffn_bwd_args_t* a, hipStream_t s) {
   SFL_HIPB(packed_T(a->W_up_packed, a->W_upT, a->W_up, p.WupT, p.WuP, &WuP));
   if (gated) SFL_HIPB(packed_T(a->W_gate_packed, a->W_gateT, a->W_gate, p.WgT, p.WgP, &WgP));
 
+  // tokens by descending row count for the gathers over the sparse rows, under the
+  // forward's rule (batches of at least 1024 tokens with ELL rows of at most 256 entries,
+  // where the walks take 8 tokens side by side; SFL_TOKEN_ORDER=nnz/token forces it)
+  const int32_t* order = nullptr;
+  if (token_order(T, (int)K)) {
+    SFL_HIPB(launch_nnz_order(T, (int)K, sv.row_nnz, sv.row_ovf, p.order, s));
+    order = p.order;
+  }
   // 1. dh at the pattern of the sparse rows: per-XCD partial dots dY . W_down[n], then
   //    non-gated: dz = sum + lambda'; gated: h_u recomputed the same way from X and W_up,
   //    then dh_u, dh_g and h per entry
   if (!gated) {
-    SFL_HIPB(launch_gated_updot(T, d, f, K, sv.ell_idx, sv.row_nnz, sv.row_ovf, dY, WdP, p.part, s));
+    SFL_HIPB(launch_gated_updot(T, d, f, K, sv.ell_idx, sv.row_nnz, sv.row_ovf, dY, WdP, p.part, s, order));
     SFL_HIPB(launch_sum_parts(T, K, sv.row_nnz, sv.row_ovf, p.part, lam, p.dz, s));
   } else {
-    SFL_HIPB(launch_gated_updot(T, d, f, K, sv.ell_idx, sv.row_nnz, sv.row_ovf, X, WuP, p.part, s));
+    SFL_HIPB(launch_gated_updot(T, d, f, K, sv.ell_idx, sv.row_nnz, sv.row_ovf, X, WuP, p.part, s, order));
     SFL_HIPB(launch_sum_parts(T, K, sv.row_nnz, sv.row_ovf, p.part, 0.f, p.u, s));  // h_u
-    SFL_HIPB(launch_gated_updot(T, d, f, K, sv.ell_idx, sv.row_nnz, sv.row_ovf, dY, WdP, p.part, s));
+    SFL_HIPB(launch_gated_updot(T, d, f, K, sv.ell_idx, sv.row_nnz, sv.row_ovf, dY, WdP, p.part, s, order));
     SFL_HIPB(launch_gated_entry_grads(T, K, ev, sv.row_nnz, sv.row_ovf, p.part, p.u, lam, p.dz, p.dhg, p.hf, s));
   }
   rec(1);
   // 2. dX of the sparse rows (gated: dh_u W_up^T into an fp32 accumulator, then
   //    + dh_g W_gate^T; one slice-major matrix per pass keeps one slice per XCD in L2)
   if (!gated) {
-    SFL_HIPB(launch_gather_down_packed(T, d, f, K, p.dz, sv.ell_idx, sv.row_nnz, sv.row_ovf, WuP, a->dX, s, 1));
+    SFL_HIPB(launch_gather_down_packed(T, d, f, K, p.dz, sv.ell_idx, sv.row_nnz, sv.row_ovf, WuP, a->dX, s, 1, 0,
+                                       nullptr, order));
   } else {
     SFL_HIPB(launch_gather_down_packed(T, d, f, K, p.dz, sv.ell_idx, sv.row_nnz, sv.row_ovf, WuP, nullptr, s, 1, 1,
-                                       p.dxf));
+                                       p.dxf, order));
     SFL_HIPB(launch_gather_down_packed(T, d, f, K, p.dhg, sv.ell_idx, sv.row_nnz, sv.row_ovf, WgP, a->dX, s, 1, 2,
-                                       p.dxf));
+                                       p.dxf, order));
   }
   rec(2);
   // 3. transposed pattern, with each entry's values
