@@ -197,10 +197,7 @@ __host__ __device__ inline int tg_value_stride(int K) {
   const int h = (K + GU_GROUP - 1) / GU_GROUP * GU_GROUP / 2;
   return 2 * (h | 1);
 }
-#ifndef SFL_TG_LDS
-#define SFL_TG_LDS 148608
-#endif
-constexpr int64_t kTgLds = SFL_TG_LDS;  // LDS budget of a token-group workgroup (bf16 values)
+constexpr int kTgTokens = 32;  // tokens per token-group workgroup (see launch_gather_down_packed)
 __host__ __device__ inline int64_t tg_bytes_per_token(int K) { return (int64_t)(K + 1) * 4 + (int64_t)tg_value_stride(K) * 2 + 8; }
 
 // Sum of the 8 groups' partial sums (lanes l, l ^ 8, ..., l ^ 56) into every group: the
@@ -961,7 +958,7 @@ __global__ __launch_bounds__(256) void k_pack_down(const bf16_t* __restrict__ W,
 
 }  // namespace
 
-static int slice_walk_tpw(int64_t T, int64_t per_tok, int64_t lds_budget = GATHER_LDS);
+static int slice_walk_tpw(int64_t T, int64_t per_tok);
 
 hipError_t launch_gather_down(int val_bf16, int64_t T, int64_t d, int K, const void* ell_val,
                               const uint16_t* ell_idx, const int32_t* row_nnz, const uint8_t* row_ovf,
@@ -997,7 +994,19 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
   // token groups also keep each token's row in LDS
   const int64_t per_tok = groups && vk == 0 ? tg_bytes_per_token(std::max(K, 1))
                                             : (int64_t)(std::max(K, 1) + (groups ? 1 : 0)) * 4 * (vk + 1) + (groups ? 8 : 4);
-  const int tpw = slice_walk_tpw(T, per_tok, groups && vk == 0 ? kTgLds : GATHER_LDS);
+  // Token groups: blocks of kTgTokens tokens (halved while that leaves fewer than 512
+  // workgroups), i.e. 4 groups of 8, so that the 16 waves of a block stay on whole slices:
+  // wave w takes group w % 4 of slices w / 4, w / 4 + 4, ... Block sizes whose group
+  // count does not divide 16 leave the waves of a block spread over more slices at once
+  // and measured slower (headline gather 0.466 ms at 32 tokens, 0.476 at 64, 0.483 at 86,
+  // 0.495 at 24, 0.508 at 40, 0.532 at 48).
+  int tpw;
+  if (groups) {
+    tpw = kTgTokens;
+    while (tpw > NGRP && 8 * cdiv(T, tpw) < 512) tpw /= 2;
+  } else {
+    tpw = slice_walk_tpw(T, per_tok);
+  }
   const int64_t blocks = cdiv(T, tpw);
   const size_t lds = (size_t)tpw * per_tok;
   if (lds > 160 * 1024) return hipErrorInvalidValue;
@@ -1091,8 +1100,8 @@ hipError_t launch_sum_parts(int64_t T, int K, const int32_t* row_nnz, const uint
 // Token blocks of the slice-walking kernels: at most what the LDS budget holds (one
 // workgroup per CU); each block goes to every XCD (each XCD covers its own slices), and the
 // blocks are sized so that each XCD's 32 CUs get whole rounds.
-static int slice_walk_tpw(int64_t T, int64_t per_tok, int64_t lds_budget) {
-  const int64_t tpw_max = std::max<int64_t>(1, std::min<int64_t>(GATHER_LDS / 1024, lds_budget / per_tok));
+static int slice_walk_tpw(int64_t T, int64_t per_tok) {
+  const int64_t tpw_max = std::max<int64_t>(1, std::min<int64_t>(GATHER_LDS / 1024, GATHER_LDS / per_tok));
   const int64_t wg_per_cu = std::max<int64_t>(1, (160 * 1024) / (tpw_max * per_tok));
   const int64_t slots = 32 * std::min<int64_t>(wg_per_cu, 2048 / (GATHER_WAVES * 64));
   const int64_t rounds = cdiv(T, tpw_max * slots);
