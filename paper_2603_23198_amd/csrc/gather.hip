@@ -994,16 +994,16 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
   // token groups also keep each token's row in LDS
   const int64_t per_tok = groups && vk == 0 ? tg_bytes_per_token(std::max(K, 1))
                                             : (int64_t)(std::max(K, 1) + (groups ? 1 : 0)) * 4 * (vk + 1) + (groups ? 8 : 4);
-  // Token groups: blocks of kTgTokens tokens (halved while that leaves fewer than 512
-  // workgroups), i.e. 4 groups of 8, so that the 16 waves of a block stay on whole slices:
-  // wave w takes group w % 4 of slices w / 4, w / 4 + 4, ... Block sizes whose group
-  // count does not divide 16 leave the waves of a block spread over more slices at once
-  // and measured slower (headline gather 0.466 ms at 32 tokens, 0.476 at 64, 0.483 at 86,
-  // 0.495 at 24, 0.508 at 40, 0.532 at 48).
+  // Token groups: blocks of at most kTgTokens tokens (4 groups of 8: wave w takes group
+  // w % 4 of slices w / 4, w / 4 + 4, ...), two workgroups per CU, and as many blocks per
+  // XCD as fill whole rounds of its 64 workgroup slots (32 tokens per block at 2048 tokens
+  // and above in powers of two, 16 at 1024). Measured at the headline: 0.466 ms at 32
+  // tokens, 0.476 at 64 and 0.483 at 86, but 0.495 at 24, 0.508 at 40, 0.532 at 48, whose
+  // last round is partly empty; the token shard (T = 1024) 0.093 -> 0.075 ms at 16.
   int tpw;
   if (groups) {
-    tpw = kTgTokens;
-    while (tpw > NGRP && 8 * cdiv(T, tpw) < 512) tpw /= 2;
+    constexpr int64_t kSlots = 64;  // per XCD: 32 CUs x 2 workgroups
+    tpw = (int)cdiv(T, cdiv(T, kTgTokens * kSlots) * kSlots);
   } else {
     tpw = slice_walk_tpw(T, per_tok);
   }
