@@ -646,9 +646,45 @@ __global__ __launch_bounds__(256) void k_transpose(const E* __restrict__ in, E* 
   }
 }
 
+// 4-byte elements, rows and columns multiples of 4, 16-byte aligned: a 64 x 64 tile moves
+// as 16-byte chunks both ways (four per thread in, four out), through a padded LDS tile.
+__global__ __launch_bounds__(256) void k_transpose_v4(const uint32_t* __restrict__ in, uint32_t* __restrict__ out,
+                                                      int64_t rows, int64_t cols) {
+  __shared__ uint32_t tile[64][65];
+  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int q = threadIdx.x + 256 * k;
+    const int i = q >> 4, j = (q & 15) * 4;  // tile row, first column of the chunk
+    const int64_t r = r0 + i, c = c0 + j;
+    if (r < rows && c < cols) {
+      const u32x4_t v = *(const u32x4_t*)(in + r * cols + c);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) tile[i][j + e] = v[e];
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int q = threadIdx.x + 256 * k;
+    const int i = q >> 4, j = (q & 15) * 4;  // output row (tile column), first element
+    const int64_t c = c0 + i, r = r0 + j;
+    if (c < cols && r < rows) {
+      u32x4_t v;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = tile[j + e][i];
+      *(u32x4_t*)(out + c * rows + r) = v;
+    }
+  }
+}
+
 hipError_t launch_transpose(const void* in, void* out, int64_t rows, int64_t cols, int eb, hipStream_t s) {
   if (rows == 0 || cols == 0) return hipSuccess;
   const dim3 grid((unsigned)cdiv(cols, 64), (unsigned)cdiv(rows, 64));
+  if (eb == 4 && rows % 4 == 0 && cols % 4 == 0 && ((((uintptr_t)in) | ((uintptr_t)out)) & 15) == 0) {
+    hipLaunchKernelGGL(k_transpose_v4, grid, dim3(256), 0, s, (const uint32_t*)in, (uint32_t*)out, rows, cols);
+    return hipGetLastError();
+  }
   if (eb == 2)
     hipLaunchKernelGGL(k_transpose<uint16_t>, grid, dim3(256), 0, s, (const uint16_t*)in, (uint16_t*)out, rows, cols);
   else

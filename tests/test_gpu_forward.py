@@ -536,6 +536,21 @@ def test_empty_batch(dtype, gated):
     assert st["capacity_exceeded"] == 0
 
 
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("rows,cols", [(64, 64), (100, 132), (4096, 1024), (99, 130), (1, 7), (130, 4)])
+def test_transpose_copies_bit_exact(rows, cols, dtype):
+    """sfl_transpose against torch's transpose, bit for bit: 2- and 4-byte elements, shapes
+    whose sides are multiples of 4 (the 16-byte path for 4-byte elements), of the 64 x 64
+    tile, and neither."""
+    g = torch.Generator().manual_seed(rows * 1000 + cols)
+    x = torch.randn(rows, cols, generator=g).to(dtype).cuda()
+    out = torch.full((cols, rows), float("nan"), dtype=dtype, device="cuda")
+    b.sfl_transpose(x, out)
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16 if dtype == torch.bfloat16 else torch.int32),
+                       x.t().contiguous().view(torch.int16 if dtype == torch.bfloat16 else torch.int32))
+
+
 def test_packed_down_weights_layout_and_equivalence():
     w = wl.make_ffn("packed", "bf16", 300, 1024, 2048, seed=12, sparsity=0.98, ell_width=96)
     Wd = dev(w.W_down)
