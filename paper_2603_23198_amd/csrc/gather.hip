@@ -700,10 +700,10 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gated_updot(
         w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, (int)off, 0, 0));
       }
       // the lane's partial dot products of the round's entries, then their sums over the
-      // group: with rounds of a multiple of 8 entries, eight at a time (lane sub of the
-      // group adds entry b + sub's sum: dz 1.298 -> 1.282 ms at the training shape), else
-      // one at a time (the rounds of 12 of short rows measured faster that way than
-      // rounds of 8 or 16 with the batched sums)
+      // group, eight entries at a time (lane sub of the group adds entry b + sub's sum) and
+      // the rest of a round of 12 one at a time: dz 1.298 -> 1.282 ms at the training
+      // shape, gated prefill sparse stage 0.585 -> 0.558 ms (rounds of 8 or 16 for the
+      // short rows were slower than 12)
       auto partial = [&](int u) {
         float sacc = 0.f;
 #pragma unroll
@@ -716,23 +716,20 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gated_updot(
         }
         return sacc;
       };
-      if constexpr (U % 8 == 0) {
 #pragma unroll
-        for (int b = 0; b < U; b += 8) {
-          float pk[8];
+      for (int b = 0; b + 8 <= U; b += 8) {
+        float pk[8];
 #pragma unroll
-          for (int u = 0; u < 8; ++u) pk[u] = partial(b + u);
-          const float tot = group8_reduce_scatter(pk, sub);
-          const int e = q + (b + sub) * NGRP + grp;
-          if (e < nnz) ur[e] += tot;
-        }
-      } else {
+        for (int u = 0; u < 8; ++u) pk[u] = partial(b + u);
+        const float tot = group8_reduce_scatter(pk, sub);
+        const int e = q + (b + sub) * NGRP + grp;
+        if (e < nnz) ur[e] += tot;
+      }
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const float sacc = group8_sum(partial(u));
-          const int e = q + u * NGRP + grp;
-          if (sub == 0 && e < nnz) ur[e] += sacc;
-        }
+      for (int u = U / 8 * 8; u < U; ++u) {
+        const float sacc = group8_sum(partial(u));
+        const int e = q + u * NGRP + grp;
+        if (sub == 0 && e < nnz) ur[e] += sacc;
       }
     }
   };
