@@ -117,7 +117,8 @@ __global__ __launch_bounds__(256) void k_gather_down(int64_t T, int64_t d, int K
 // Workgroup g runs on XCD g % 8 (workgroups are dispatched round-robin over the XCDs);
 // it owns a block of tokens and walks that XCD's slices (x, x+8, x+16, ...) in order,
 // like every other workgroup of the XCD, so the XCD works on about one slice at a time.
-// The block's ELL entries are copied once into LDS (index | bf16 value << 16) and reused
+// The block's ELL entries are copied once into LDS (index | bf16 value << 16; the
+// token-group walk keeps row offsets and values apart, see tg_value_stride) and reused
 // for every slice, so the per-token metadata latency is paid once, not per slice.
 // Lane = (group g = lane / LPR, part i = lane % LPR): the NGRP groups each take a
 // different ELL entry and read its row segment as LPR x 16 bytes, so one load instruction
