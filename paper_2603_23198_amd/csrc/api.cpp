@@ -400,9 +400,15 @@ sfl_status_t sfl_pack_twell(const float* Z, int64_t T, int64_t f, sfl_dtype_t va
   const int vb = val_dtype == SFL_BF16;
   const int64_t cap = capacity_of(*cfg, T);
   SFL_HIP(launch_stats_init(stats, s));
-  SFL_HIP(launch_pack_twell(Z, T, f, vb, cfg->tile_cols, cfg->tile_slots, out->val, out->idx, out->cnt, s, pk));
-  SFL_HIP(launch_classify(T, f, vb, cfg->tile_cols, cfg->tile_slots, cfg->ell_width, out->val, out->idx, out->cnt,
-                          out->row_nnz, out->row_ovf, out->ell_val, out->ell_idx, stats, s, 1, pk));
+  if (pack_classify_rows_ok(T, f, cfg->tile_cols, cfg->tile_slots, vb) && ((uintptr_t)Z & 15) == 0) {
+    SFL_HIP(launch_pack_classify_rows(Z, 0, nullptr, nullptr, T, f, vb, cfg->tile_cols, cfg->tile_slots,
+                                      cfg->ell_width, out->val, out->idx, out->cnt, out->row_nnz, out->row_ovf,
+                                      out->ell_val, out->ell_idx, stats, s, 1, pk));
+  } else {
+    SFL_HIP(launch_pack_twell(Z, T, f, vb, cfg->tile_cols, cfg->tile_slots, out->val, out->idx, out->cnt, s, pk));
+    SFL_HIP(launch_classify(T, f, vb, cfg->tile_cols, cfg->tile_slots, cfg->ell_width, out->val, out->idx, out->cnt,
+                            out->row_nnz, out->row_ovf, out->ell_val, out->ell_idx, stats, s, 1, pk));
+  }
   SFL_HIP(launch_ovf_list(T, (int32_t)cap, out->row_ovf, out->ovf_rows, out->n_ovf, stats, s));
   return SFL_OK;
 }
@@ -519,6 +525,12 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
     for (int i = 1; i < 5; ++i) ev.record(i, s);
     return SFL_OK;
   }
+  // the stored values are h itself only in the non-gated layer (the gated layer's are the
+  // gate values; its sum of |h| is taken where h is formed)
+  const int l1_vals = a->gated ? 0 : 1;
+  // small batches whose up projection leaves fp32 sums pack and classify in one launch
+  const bool row_classify = pack_classify_rows_ok(T, f, a->cfg.tile_cols, a->cfg.tile_slots, vb);
+  bool classified = false;
   const bool bf = a->dtype == SFL_BF16;
   const void* Wp = a->gated ? a->W_gate : a->W_up;                        // pattern-deciding projection
   const void* WpT = !bf ? nullptr : a->gated ? a->W_gateT : a->W_upT;     // its transposed copy, if given
@@ -579,23 +591,38 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
         }
         SFL_HIP(clear_first());
         SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_F32, g, s));
-        SFL_HIP(launch_pack_twell_parts(plan.part, ks, a->bias_f, a->shift_t, T, f, vb, a->cfg.tile_cols,
-                                        a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, s, packed_layout(a->cfg)));
+        if (row_classify && ((uintptr_t)plan.part & 15) == 0) {
+          SFL_HIP(launch_pack_classify_rows(plan.part, ks, a->bias_f, a->shift_t, T, f, vb, a->cfg.tile_cols,
+                                            a->cfg.tile_slots, a->cfg.ell_width, tw.val, tw.idx, tw.cnt, tw.row_nnz,
+                                            tw.row_ovf, tw.ell_val, tw.ell_idx, a->stats, s, l1_vals,
+                                            packed_layout(a->cfg)));
+          classified = true;
+        } else {
+          SFL_HIP(launch_pack_twell_parts(plan.part, ks, a->bias_f, a->shift_t, T, f, vb, a->cfg.tile_cols,
+                                          a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, s, packed_layout(a->cfg)));
+        }
       } else {
         SFL_HIP(clear_first());
         SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_F32, g, s));
-        SFL_HIP(launch_pack_twell(plan.Z, T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, s,
-                                  packed_layout(a->cfg)));
+        if (row_classify && ((uintptr_t)plan.Z & 15) == 0) {
+          SFL_HIP(launch_pack_classify_rows(plan.Z, 0, nullptr, nullptr, T, f, vb, a->cfg.tile_cols,
+                                            a->cfg.tile_slots, a->cfg.ell_width, tw.val, tw.idx, tw.cnt, tw.row_nnz,
+                                            tw.row_ovf, tw.ell_val, tw.ell_idx, a->stats, s, l1_vals,
+                                            packed_layout(a->cfg)));
+          classified = true;
+        } else {
+          SFL_HIP(launch_pack_twell(plan.Z, T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, tw.val, tw.idx, tw.cnt,
+                                    s, packed_layout(a->cfg)));
+        }
       }
     }
   }
   ev.record(1, s);
-  // 2. hybrid classification (Sec. 3.4)
-  // the stored values are h itself only in the non-gated layer (the gated layer's are the
-  // gate values; its sum of |h| is taken where h is formed)
-  SFL_HIP(launch_classify(T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, a->cfg.ell_width, tw.val, tw.idx, tw.cnt,
-                          tw.row_nnz, tw.row_ovf, tw.ell_val, tw.ell_idx, a->stats, s, a->gated ? 0 : 1,
-                          packed_layout(a->cfg)));
+  // 2. hybrid classification (Sec. 3.4), unless done with the pack
+  if (!classified)
+    SFL_HIP(launch_classify(T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, a->cfg.ell_width, tw.val, tw.idx,
+                            tw.cnt, tw.row_nnz, tw.row_ovf, tw.ell_val, tw.ell_idx, a->stats, s, l1_vals,
+                            packed_layout(a->cfg)));
   // the dense-backup row list: up to 64 rows the gather's first block builds it (nothing
   // before the dense-backup stage reads it), else its own kernel
   OvfList late_list;

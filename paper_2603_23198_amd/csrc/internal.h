@@ -132,6 +132,17 @@ hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int tile_cols, in
                            int ell_width, const void* val, const uint16_t* idx, const int32_t* cnt,
                            int32_t* row_nnz, uint8_t* row_ovf, void* ell_val, uint16_t* ell_idx,
                            sfl_stats_t* stats, hipStream_t s, int l1_vals = 1, bool packed = false);
+// Small batches (1 <= T <= 256 rows, f a multiple of 64, T_n of 64, 128 or 256, the row
+// and its tile entries within the kernel's LDS): the pack (from Z with ks = 0, else from
+// ks <= 8 split-K partial sums as launch_pack_twell_parts; fp32 values only with ks <= 1)
+// and the classification in one launch, one workgroup per row. Z (or the partials) must
+// be 16-byte aligned. The outputs and statistics are those of the two launches.
+bool pack_classify_rows_ok(int64_t T, int64_t f, int tile_cols, int tile_slots, int val_bf16);
+hipError_t launch_pack_classify_rows(const float* Z, int ks, const float* bias, const float* shift, int64_t T,
+                                     int64_t f, int val_bf16, int tile_cols, int tile_slots, int ell_width, void* val,
+                                     uint16_t* idx, int32_t* cnt, int32_t* row_nnz, uint8_t* row_ovf, void* ell_val,
+                                     uint16_t* ell_idx, sfl_stats_t* stats, hipStream_t s, int l1_vals = 1,
+                                     bool packed = false);
 // Ascending dense-backup row list + n_ovf + capacity flag (one workgroup).
 hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32_t* ovf_rows,
                            int32_t* n_ovf, sfl_stats_t* stats, hipStream_t s);

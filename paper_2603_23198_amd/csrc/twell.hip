@@ -338,6 +338,243 @@ hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int Tn, int S, in
   return hipGetLastError();
 }
 
+// Small batches: the TwELL pack (Alg. 1) and the hybrid classification (Sec. 3.4) of one
+// row in one workgroup, so that the two steps take one launch where launches, not bytes,
+// set the time. The row's pre-activations are first summed into LDS by all threads with
+// 16-byte loads: from ks split-K partial sums part[s][t][n] (in split order, then bias[n],
+// then shift[t]: the arithmetic of k_pack_twell) or, with ks = 0, from Z itself. Each wave
+// then compacts 256 columns at a time, four consecutive columns per lane, so a TwELL tile
+// of T_n columns is T_n / 4 lanes: four ballots give each active column its slot (the
+// tile's active columns in lower lanes, then those below it in its own lane), entries
+// with slots below S go to the slabs and to an LDS copy of the tile, the true count to
+// cnt. One wave then scans the tile counts (row total, overflowing tiles, each tile's
+// first ELL position); for a sparse row all threads copy the kept entries to the ELL
+// row. Outputs and statistics are those of k_pack_twell followed by k_classify.
+constexpr int kRowPackThreads = 1024;
+constexpr int kRowPackChunks = 4;  // 16-byte chunks per thread and pass of the load phase
+constexpr size_t kRowPackMaxLds = 128 * 1024;
+constexpr int64_t kRowPackMaxRows = 256;
+
+size_t row_pack_lds(int64_t f, int NT, int S, int vbytes) {
+  const size_t ent = ((size_t)NT * S + 1) / 2 * 2;  // columns (u16), padded to 4 bytes
+  return (size_t)f * 4 + (size_t)NT * 8 + ent * 2 + (size_t)NT * S * vbytes;
+}
+
+template <typename V, bool PK, int KS>  // KS = max(ks, 1): the number of partial sums read
+__global__ __launch_bounds__(kRowPackThreads) void k_pack_classify_rows(
+    const float* __restrict__ Z, int ks, const float* __restrict__ bias, const float* __restrict__ shift, int64_t T,
+    int64_t f, int Tn, int S, int NT, int K, V* __restrict__ val, uint16_t* __restrict__ idx,
+    int32_t* __restrict__ cnt, int32_t* __restrict__ row_nnz, uint8_t* __restrict__ row_ovf, V* __restrict__ ell_val,
+    uint16_t* __restrict__ ell_idx, sfl_stats_t* __restrict__ stats, int l1_vals) {
+  extern __shared__ __align__(16) unsigned char rp_lds[];
+  float* zrow = (float*)rp_lds;                 // [f]
+  int* tcnt = (int*)(zrow + f);                 // [NT] tile counts
+  int* tpre = tcnt + NT;                        // [NT] first ELL position of each tile
+  uint16_t* ecol = (uint16_t*)(tpre + NT);      // [NT][S] kept columns
+  V* evals = (V*)(ecol + ((int64_t)NT * S + 1) / 2 * 2);  // [NT][S] kept values
+  __shared__ int row_flag;
+  __shared__ float l1_w[kRowPackThreads / 64];
+  const int64_t t = blockIdx.x;
+  const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
+  // 1. z of the row into LDS; every load address is clamped into the row, so all of a
+  // pass's loads can be in flight together
+  const int64_t nch = f / 4;
+  const float* zr = Z + t * f;
+  const int64_t sstride = T * f;
+  const float sh = (ks > 0 && shift) ? shift[t] : 0.f;
+  constexpr int CH = KS > 4 ? 2 : kRowPackChunks;  // chunks per pass, as registers allow
+  const bool add = ks > 0;
+  for (int64_t c0 = tid; c0 < nch; c0 += (int64_t)kRowPackThreads * CH) {
+    float4 z[CH], bb[CH];
+#pragma unroll
+    for (int u = 0; u < CH; ++u) {
+      const int64_t c = min(c0 + (int64_t)u * kRowPackThreads, nch - 1);
+      bb[u] = (add && bias) ? ((const float4*)bias)[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+      z[u] = ((const float4*)zr)[c];
+    }
+#pragma unroll
+    for (int sp = 1; sp < KS; ++sp) {
+      const float* src = zr + (int64_t)sp * sstride;
+#pragma unroll
+      for (int u = 0; u < CH; ++u) {
+        const int64_t c = min(c0 + (int64_t)u * kRowPackThreads, nch - 1);
+        const float4 q = ((const float4*)src)[c];
+        z[u].x += q.x;
+        z[u].y += q.y;
+        z[u].z += q.z;
+        z[u].w += q.w;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < CH; ++u) {
+      const int64_t c = c0 + (int64_t)u * kRowPackThreads;
+      if (c >= nch) break;
+      if (add) {
+        if (bias) {
+          z[u].x += bb[u].x;
+          z[u].y += bb[u].y;
+          z[u].z += bb[u].z;
+          z[u].w += bb[u].w;
+        }
+        z[u].x += sh;
+        z[u].y += sh;
+        z[u].z += sh;
+        z[u].w += sh;
+      }
+      ((float4*)zrow)[c] = z[u];
+    }
+  }
+  __syncthreads();
+  // 2. compaction, 256 columns per wave and step
+  const int GL = Tn >> 2;                              // lanes per TwELL tile
+  const int gsh = l & ~(GL - 1);
+  const uint64_t gmask = (GL == 64 ? ~0ull : ((1ull << GL) - 1ull)) << gsh;
+  const uint64_t below = (1ull << l) - 1ull;
+  const int64_t row_words = (int64_t)NT * (PK ? 32 : S);
+  for (int64_t st = w; st * 256 < f; st += kRowPackThreads / 64) {
+    const int64_t col = st * 256 + 4 * l;
+    const bool in = col < f;
+    const float4 z = in ? ((const float4*)zrow)[col >> 2] : make_float4(0.f, 0.f, 0.f, 0.f);
+    const float zz[4] = {z.x, z.y, z.z, z.w};
+    bool act[4];
+    int cnt_below = 0, cnt_tile = 0;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      act[r] = in && is_active(zz[r]);
+      const uint64_t m = ballot(act[r]) & gmask;
+      cnt_below += __popcll(m & below);
+      cnt_tile += __popcll(m);
+    }
+    const int j = (int)(col / Tn);
+    int slot = cnt_below;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      if (act[r]) {
+        if (slot < S) {
+          const uint16_t c16 = (uint16_t)(col + r);
+          const V v = VT<V>::cvt(zz[r]);
+          if constexpr (PK) {
+            ((uint32_t*)val)[t * row_words + (int64_t)j * 32 + 1 + slot] =
+                (uint32_t)c16 | ((uint32_t)f32_to_bf16(zz[r]) << 16);
+          } else {
+            val[t * row_words + (int64_t)j * S + slot] = v;
+            idx[t * row_words + (int64_t)j * S + slot] = c16;
+          }
+          ecol[j * S + slot] = c16;
+          evals[j * S + slot] = v;
+        }
+        ++slot;
+      }
+    }
+    if (in && l == gsh) {
+      if constexpr (PK) ((uint32_t*)val)[t * row_words + (int64_t)j * 32] = (uint32_t)cnt_tile;
+      else cnt[t * NT + j] = cnt_tile;
+      tcnt[j] = cnt_tile;
+    }
+  }
+  __syncthreads();
+  // 3. row summary: total, overflowing tiles, exclusive prefix of the counts
+  if (w == 0) {
+    int total = 0, over = 0;
+    for (int j0 = 0; j0 < NT; j0 += 64) {
+      const int c = j0 + l < NT ? tcnt[j0 + l] : 0;
+      const int incl = wave_incl_scan(c) + total;
+      if (j0 + l < NT) tpre[j0 + l] = incl - c;
+      total = __shfl(incl, 63, 64);
+      over += __popcll(ballot(c > S));
+    }
+    const bool ovf = total > K || over > 0;
+    if (l == 0) {
+      row_nnz[t] = total;
+      row_ovf[t] = ovf ? 1 : 0;
+      row_flag = ovf ? 1 : 0;
+      if (stats) {
+        if (total) atomicAdd((unsigned long long*)&stats->total_nnz, (unsigned long long)total);
+        if (over) atomicAdd((unsigned long long*)&stats->n_tile_ovf, (unsigned long long)over);
+      }
+    }
+  }
+  __syncthreads();
+  // 4. a sparse row's ELL entries (every count is at most S then, so all were kept)
+  if (row_flag) return;  // uniform over the block
+  float l1 = 0.f;
+  for (int e = tid; e < NT * S; e += kRowPackThreads) {
+    const int j = e / S, sl = e - j * S;
+    if (sl < tcnt[j]) {
+      const int64_t q = t * K + tpre[j] + sl;
+      const V v = evals[e];
+      if (ell_val) {
+        ell_val[q] = v;
+        ell_idx[q] = ecol[e];
+      }
+      if (l1_vals) l1 += VT<V>::load(&v, 0);
+    }
+  }
+  if (stats && l1_vals) {
+    l1 = wave_sum<float>(l1);
+    if (l == 0) l1_w[w] = l1;
+    __syncthreads();
+    if (tid == 0) {
+      float c = 0.f;
+      for (int i = 0; i < kRowPackThreads / 64; ++i) c += l1_w[i];
+      if (c != 0.f) atomicAdd(&stats->l1_sum, (double)c);
+    }
+  }
+}
+
+bool pack_classify_rows_ok(int64_t T, int64_t f, int Tn, int S, int val_bf16) {
+  if (T < 1 || T > kRowPackMaxRows || f % 64 != 0) return false;
+  if (Tn != 64 && Tn != 128 && Tn != 256) return false;
+  const int NT = (int)cdiv(f, Tn);
+  return row_pack_lds(f, NT, S, val_bf16 ? 2 : 4) <= kRowPackMaxLds;
+}
+
+hipError_t launch_pack_classify_rows(const float* Z, int ks, const float* bias, const float* shift, int64_t T,
+                                     int64_t f, int val_bf16, int Tn, int S, int K, void* val, uint16_t* idx,
+                                     int32_t* cnt, int32_t* row_nnz, uint8_t* row_ovf, void* ell_val,
+                                     uint16_t* ell_idx, sfl_stats_t* stats, hipStream_t s, int l1_vals, bool packed) {
+  if (!pack_classify_rows_ok(T, f, Tn, S, val_bf16) || ks < 0 || ks > 8) return hipErrorInvalidValue;
+  if (packed && (!val_bf16 || S != 31)) return hipErrorInvalidValue;
+  if (!val_bf16 && ks > 1) return hipErrorInvalidValue;
+  const int NT = (int)cdiv(f, Tn);
+  const size_t lds = row_pack_lds(f, NT, S, val_bf16 ? 2 : 4);
+  const dim3 grid((unsigned)T), block(kRowPackThreads);
+#define SFL_ROWPACK(V_, PK_, KS_)                                                                                   \
+  do {                                                                                                             \
+    auto kern = k_pack_classify_rows<V_, PK_, KS_>;                                                                \
+    if (lds > 65536) {                                                                                             \
+      const hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,      \
+                                               (int)lds);                                                          \
+      if (e != hipSuccess) return e;                                                                               \
+    }                                                                                                              \
+    hipLaunchKernelGGL(kern, grid, block, lds, s, Z, ks, bias, shift, T, f, Tn, S, NT, K, (V_*)val, idx, cnt,     \
+                       row_nnz, row_ovf, (V_*)ell_val, ell_idx, stats, l1_vals);                                   \
+  } while (0)
+#define SFL_ROWPACK_KS(V_, PK_)                 \
+  do {                                          \
+    switch (ks) {                               \
+      case 0:                                   \
+      case 1: SFL_ROWPACK(V_, PK_, 1); break;   \
+      case 2: SFL_ROWPACK(V_, PK_, 2); break;   \
+      case 3: SFL_ROWPACK(V_, PK_, 3); break;   \
+      case 4: SFL_ROWPACK(V_, PK_, 4); break;   \
+      case 5: SFL_ROWPACK(V_, PK_, 5); break;   \
+      case 6: SFL_ROWPACK(V_, PK_, 6); break;   \
+      case 7: SFL_ROWPACK(V_, PK_, 7); break;   \
+      default: SFL_ROWPACK(V_, PK_, 8); break;  \
+    }                                           \
+  } while (0)
+  if (packed)
+    SFL_ROWPACK_KS(bf16_t, true);
+  else if (val_bf16)
+    SFL_ROWPACK_KS(bf16_t, false);
+  else
+    SFL_ROWPACK(float, false, 1);
+#undef SFL_ROWPACK_KS
+#undef SFL_ROWPACK
+  return hipGetLastError();
+}
+
 __global__ __launch_bounds__(256) void k_stats_init(sfl_stats_t* stats, int32_t* zero, int n_zero) {
   if (stats && threadIdx.x == 0) {
     stats->total_nnz = 0;

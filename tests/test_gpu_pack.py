@@ -36,6 +36,12 @@ CASES = [
     (300, 4096, 128, 8, 100, 7, "bf16"),     # capacity below the number of overflow rows
     (1, 65535, 256, 32, 2000, 0, "bf16"),    # largest index
     (0, 256, 256, 32, 8, 0, "bf16"),         # empty
+    # up to 256 rows with f a multiple of 64: one workgroup per row packs and classifies
+    (200, 2048, 64, 16, 40, 0, "bf16"),
+    (256, 4096, 128, 8, 100, 7, "bf16"),     # capacity below the number of overflow rows
+    (3, 1984, 256, 32, 64, 0, "bf16"),       # partial last tile
+    (17, 320, 128, 128, 500, 0, "f32"),      # every column of a tile kept
+    (2, 24576, 256, 32, 400, 0, "bf16"),     # a row of 96 KB of fp32 in LDS
 ]
 
 
