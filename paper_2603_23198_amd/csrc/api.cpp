@@ -164,6 +164,7 @@ struct FwdPlan {
   int32_t* n_need = nullptr;     // [1], zeroed with tile_sem by the forward's first kernel
   int n_zero = 0;                // counters from n_need (or tile_sem) on that the first kernel zeroes
   int32_t* order = nullptr;      // tokens by descending row count [T] (slice-walking gathers)
+  float* fill_l1 = nullptr;      // per-block sums of the rebuilt dense-backup rows [ovf_fill_grid(cap)]
   void* H = nullptr;             // dense-fallback candidate: the dense ReLU rows [T][f] bf16
   int32_t* dense_flags = nullptr; // [2]: rows of the dense down GEMM (T or 0), gather skipped (1 or 0)
   int32_t* tile_sem = nullptr;   // split-K GEMMs of at most 64 rows: one counter per output tile
@@ -221,6 +222,7 @@ FwdPlan plan_forward(const sfl_ffn_args_t& a, void* ws) {
   if (need_list) {
     p.need_rows = (int32_t*)c.take((size_t)cap * 4);
     p.need_slots = (int32_t*)c.take((size_t)cap * 4);
+    p.fill_l1 = (float*)c.take((size_t)ovf_fill_grid((int32_t)cap) * 4);
   }
   p.bytes = c.used;
   return p;
@@ -706,10 +708,6 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
   // then multiplies every row by x W_up.
   if (cap > 0) {
     const bool rebuild = rebuild_ovf(*a);
-    if (rebuild)
-      SFL_HIP(launch_ovf_fill(f, vb, a->cfg.tile_cols, a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, tw.ovf_rows,
-                              tw.n_ovf, (int32_t)cap, ovf_dense, plan.need_rows, plan.need_slots, plan.n_need, s,
-                              packed_layout(a->cfg)));
     GemmParams g = gp_zero();
     g.M = (int)cap;
     g.N = (int)f;
@@ -732,11 +730,27 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
     g.part = plan.part;
     g.part_rows = plan.part_rows;
     g.tile_sem = plan.tile_sem;  // zero: set by the first kernel, reset by the last blocks of each use
-    // where the GEMM's last blocks store the rows they also sum |h| (no separate launch)
+    // where the GEMM's last blocks or its reduction store the rows they also sum |h| (no
+    // separate launch); the non-gated rebuilt rows' share is summed by the rebuild
     bool l1_in_gemm = false;
+    if (rebuild) {
+      // the rebuild's blocks leave their sums to the reduction launch of the GEMM
+      const bool l1_split = !a->gated && a->stats && bf && split_gemm_l1(g, blay);
+      if (l1_split) {
+        g.l1_stats = a->stats;
+        g.l1_more = plan.fill_l1;
+        g.n_l1_more = ovf_fill_grid((int32_t)cap);
+      }
+      l1_in_gemm = l1_split;
+      SFL_HIP(launch_ovf_fill(f, vb, a->cfg.tile_cols, a->cfg.tile_slots, tw.val, tw.idx, tw.cnt, tw.ovf_rows,
+                              tw.n_ovf, (int32_t)cap, ovf_dense, plan.need_rows, plan.need_slots, plan.n_need, s,
+                              packed_layout(a->cfg), l1_split ? plan.fill_l1 : nullptr));
+    }
     GemmParams pair = g;
     pair.B2 = WupT;
     pair.l1_stats = a->stats;
+    pair.l1_more = nullptr;
+    pair.n_l1_more = 0;
     if (a->gated && !rebuild && WupT && blay == LAY_KC && gated_pair_ok(pair)) {
       // both products of at most 64 rows in one launch, h formed by the tiles' last blocks
       // (every dense-backup row recomputed: none is rebuilt from the slabs)

@@ -945,29 +945,74 @@ __device__ __forceinline__ void splitk_store(const GemmParams& p, int m, int n, 
   }
 }
 
+// Partials 1 .. N of a row segment added to v in split order, their loads all in flight.
+template <int N>
+__device__ __forceinline__ void add_partials(f32x4_t& v, const float* base, int64_t stride) {
+  f32x4_t q[N];
+#pragma unroll
+  for (int u = 0; u < N; ++u) q[u] = *(const f32x4_t*)(base + (int64_t)(u + 1) * stride);
+#pragma unroll
+  for (int u = 0; u < N; ++u) v += q[u];
+}
+
 // Sum of the ks partials of row m, columns n .. n+3, in split order (from p.part, or from
-// the partial sums at `part`).
+// the partial sums at `part`); up to 8 partials are loaded at once.
 __device__ __forceinline__ f32x4_t splitk_sum(const GemmParams& p, int ks, int m_eff, int m, int n,
                                               const float* part = nullptr) {
   if (!part) part = p.part;
-  f32x4_t v = *(const f32x4_t*)(part + (int64_t)m * p.N + n);
-  for (int sp = 1; sp < ks; ++sp) v += *(const f32x4_t*)(part + ((int64_t)sp * m_eff + m) * p.N + n);
+  const float* base = part + (int64_t)m * p.N + n;
+  const int64_t stride = (int64_t)m_eff * p.N;
+  f32x4_t v = *(const f32x4_t*)base;
+  switch (ks) {
+    case 1: break;
+    case 2: add_partials<1>(v, base, stride); break;
+    case 3: add_partials<2>(v, base, stride); break;
+    case 4: add_partials<3>(v, base, stride); break;
+    case 5: add_partials<4>(v, base, stride); break;
+    case 6: add_partials<5>(v, base, stride); break;
+    case 7: add_partials<6>(v, base, stride); break;
+    case 8: add_partials<7>(v, base, stride); break;
+    default:
+      for (int sp = 1; sp < ks; ++sp) v += *(const f32x4_t*)(base + (int64_t)sp * stride);
+  }
   return v;
 }
 
 // Sum of the split-K partials in split order, then the epilogue of element (m, n); four
-// consecutive columns per thread, grid-stride over the counted rows.
+// consecutive columns per thread, grid-stride over the counted rows. EPI_ACT_RELU with
+// l1_stats also adds the sum of the stored values to the L1 statistic (the dense-backup
+// rows' share of it), reading them back when the GEMM stored them itself (one split),
+// and block 0 adds the n_l1_more sums at l1_more.
 template <int EPI>
 __global__ __launch_bounds__(256) void k_splitk_reduce(GemmParams p) {
   const int m_eff = p.m_count ? min(*p.m_count, p.count_cap) : p.M;
   const int ks = splitk_count(p.ksplit, p.part_rows, m_eff, p.N, (int)(p.K / KC_BK));
-  if (ks <= 1) return;
+  const bool l1 = EPI == EPI_ACT_RELU && p.l1_stats;
+  if (ks <= 1 && !l1) return;
   const int n4 = p.N / 4;
   const int64_t total = (int64_t)m_eff * n4;
+  float s = 0.f;
+  if (l1 && blockIdx.x == 0)
+    for (int i = threadIdx.x; i < p.n_l1_more; i += 256) s += p.l1_more[i];
   for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
     const int m = (int)(e / n4);
     const int n = (int)(e % n4) * 4;
-    splitk_store<EPI>(p, m, n, splitk_sum(p, ks, m_eff, m, n));
+    if (ks > 1) splitk_store<EPI>(p, m, n, splitk_sum(p, ks, m_eff, m, n));
+    if (l1) {
+      const int64_t crow = p.c_rows ? (int64_t)p.c_rows[m] : (int64_t)m;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) s += bf16_to_f32(((const bf16_t*)p.C)[crow * p.ldc + n + q]);
+    }
+  }
+  if (l1) {
+    __shared__ float wl1[4];
+    s = wave_sum<float>(s);
+    if ((threadIdx.x & 63) == 0) wl1[threadIdx.x >> 6] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      const float tot = (wl1[0] + wl1[1]) + (wl1[2] + wl1[3]);
+      if (tot != 0.f) atomicAdd(&p.l1_stats->l1_sum, (double)tot);
+    }
   }
 }
 
@@ -1341,6 +1386,11 @@ bool few_rows_path(const GemmParams& p, int blay) {
 // split-K GEMM whose last blocks apply the epilogue (and then add l1_stats, if set).
 bool few_rows_tile_epilogue(const GemmParams& p, int blay) {
   return kc_ok(p, blay) && p.ksplit > 1 && p.part && p.N % 4 == 0 && p.tile_sem && few_rows_split(p, blay) > 1;
+}
+
+bool split_gemm_l1(const GemmParams& p, int blay) {
+  return kc_ok(p, blay) && p.ksplit > 1 && p.part && p.N % 4 == 0 && !p.no_reduce &&
+         !few_rows_tile_epilogue(p, blay);
 }
 
 hipError_t gemm_bf16(int alay, int blay, int epi, const GemmParams& p, hipStream_t s) {

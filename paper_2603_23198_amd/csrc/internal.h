@@ -80,9 +80,13 @@ struct GemmParams {
   int tile_order;
   // EPI_GATED_PAIR: the second B operand (W_up^T beside B = W_gate^T, same shape)
   const void* B2;
-  // few-rows split-K with tile counters, EPI_ACT_RELU or EPI_GATED_PAIR: the sum of the
-  // stored |values| is added to l1_stats->l1_sum (one float64 atomic per tile)
+  // split-K GEMMs of EPI_ACT_RELU (the few-rows kernel's last blocks, else the reduction
+  // launch) and EPI_GATED_PAIR: the sum of the stored |values| is added to
+  // l1_stats->l1_sum (one float64 atomic per tile or per reduction block); the reduction
+  // launch adds the n_l1_more sums at l1_more as well (another kernel's share)
   sfl_stats_t* l1_stats;
+  const float* l1_more;
+  int n_l1_more;
   // statistics and n_zero int counters that block 0 clears first (the direct-to-LDS,
   // register-staged and few-rows kernels; a call's first kernel does it in place of a
   // separate clearing launch)
@@ -106,6 +110,11 @@ hipError_t launch_gated_pair(const GemmParams& p, hipStream_t s);
 // Whether gemm_bf16 runs p as the few-rows split-K GEMM whose last blocks apply the epilogue
 // (and add the stored |values| to l1_stats for EPI_ACT_RELU).
 bool few_rows_tile_epilogue(const GemmParams& p, int blay);
+// Whether gemm_bf16 runs p (A K-contiguous, EPI_ACT_RELU) as a split-K GEMM with a
+// reduction launch, so that with l1_stats the sum of the stored values of the counted rows
+// (and l1_more) reaches the L1 statistic whatever number of splits the device's row count
+// gives.
+bool split_gemm_l1(const GemmParams& p, int blay);
 // Whether gemm_bf16 runs p (no counted rows) as the few-rows split-K GEMM, which clears
 // zero_stats and zero[0 .. n_zero) before anything else.
 bool few_rows_path(const GemmParams& p, int blay);
@@ -157,11 +166,14 @@ hipError_t launch_nnz_order(int64_t T, int K, const int32_t* row_nnz, const uint
                             hipStream_t s);
 // Dense-backup rows whose tiles kept every value, rebuilt from the TwELL slabs; the others
 // are listed (need_rows: token rows, need_slots: their ovf_dense rows, *n_need: their number,
-// which must be zero before the call; list order unspecified) for the GEMM.
+// which must be zero before the call; list order unspecified) for the GEMM. With l1_part
+// (ovf_fill_grid(cap) floats), each block stores there the sum of the values it rebuilt
+// (the non-gated layer's rows are h itself, all >= 0).
+int ovf_fill_grid(int32_t cap);
 hipError_t launch_ovf_fill(int64_t f, int val_bf16, int Tn, int S, const void* val, const uint16_t* idx,
                            const int32_t* cnt, const int32_t* ovf_rows, const int32_t* n_ovf, int32_t cap,
                            void* dense, int32_t* need_rows, int32_t* need_slots, int32_t* n_need, hipStream_t s,
-                           bool packed = false);
+                           bool packed = false, float* l1_part = nullptr);
 // Sum (absval: of the absolute values) of the computed dense-backup rows, added into
 // stats->l1_sum.
 // Dense fallback decision: flags[0] = T and flags[1] = 1 (dense down GEMM, gather skipped)

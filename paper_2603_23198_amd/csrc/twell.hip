@@ -796,13 +796,15 @@ __global__ __launch_bounds__(256) void k_ovf_fill(int64_t f, int NT, int Tn, int
                                                   const uint16_t* __restrict__ idx, const int32_t* __restrict__ cnt,
                                                   const int32_t* __restrict__ ovf_rows, const int32_t* __restrict__ n_ovf,
                                                   int32_t cap, V* __restrict__ dense, int32_t* __restrict__ need_rows,
-                                                  int32_t* __restrict__ need_slots, int32_t* __restrict__ n_need) {
+                                                  int32_t* __restrict__ need_slots, int32_t* __restrict__ n_need,
+                                                  float* __restrict__ l1_part) {
   constexpr int WIN = kFillWindowBytes / (int)sizeof(V);  // columns per window (a multiple of every tile width)
   constexpr int PER = 16 / (int)sizeof(V);                 // values per 16-byte chunk
   __shared__ __attribute__((aligned(16))) V row_s[WIN];
   const int n = min(*n_ovf, cap);
   // rows of whole 16-byte chunks are zeroed and written out 16 bytes per lane
   const bool vec = f % PER == 0 && ((uintptr_t)dense & 15) == 0;
+  float l1 = 0.f;
   for (int i = blockIdx.x; i < n; i += gridDim.x) {
     const int64_t t = ovf_rows[i];
     const Slabs<V, PK> sl{val, idx, cnt, t, NT, S};
@@ -833,6 +835,7 @@ __global__ __launch_bounds__(256) void k_ovf_fill(int64_t f, int NT, int Tn, int
           uint16_t col;
           sl.slot(j, slot, v, col);
           row_s[(int)(col - c0)] = v;
+          if (l1_part) l1 += VT<V>::load(&v, 0);
         }
       }
       __syncthreads();
@@ -843,25 +846,35 @@ __global__ __launch_bounds__(256) void k_ovf_fill(int64_t f, int NT, int Tn, int
       __syncthreads();
     }
   }
+  if (l1_part) {
+    // one plain store per block (same-address atomics from every block would serialise)
+    __shared__ float wl1[4];
+    l1 = wave_sum<float>(l1);
+    if ((threadIdx.x & 63) == 0) wl1[threadIdx.x >> 6] = l1;
+    __syncthreads();
+    if (threadIdx.x == 0) l1_part[blockIdx.x] = (wl1[0] + wl1[1]) + (wl1[2] + wl1[3]);
+  }
 }
+
+int ovf_fill_grid(int32_t cap) { return std::min<int32_t>(cap, kFillBlocks); }
 
 hipError_t launch_ovf_fill(int64_t f, int val_bf16, int Tn, int S, const void* val, const uint16_t* idx,
                            const int32_t* cnt, const int32_t* ovf_rows, const int32_t* n_ovf, int32_t cap,
                            void* dense, int32_t* need_rows, int32_t* need_slots, int32_t* n_need, hipStream_t s,
-                           bool packed) {
+                           bool packed, float* l1_part) {
   if (cap == 0) return hipSuccess;
   if (packed && !val_bf16) return hipErrorInvalidValue;
   const int NT = (int)cdiv(f, Tn);
-  const dim3 grid((unsigned)std::min<int32_t>(cap, kFillBlocks));
+  const dim3 grid((unsigned)ovf_fill_grid(cap));
   if (packed)
     hipLaunchKernelGGL((k_ovf_fill<bf16_t, true>), grid, dim3(256), 0, s, f, NT, Tn, S, (const bf16_t*)val, idx, cnt,
-                       ovf_rows, n_ovf, cap, (bf16_t*)dense, need_rows, need_slots, n_need);
+                       ovf_rows, n_ovf, cap, (bf16_t*)dense, need_rows, need_slots, n_need, l1_part);
   else if (val_bf16)
     hipLaunchKernelGGL((k_ovf_fill<bf16_t, false>), grid, dim3(256), 0, s, f, NT, Tn, S, (const bf16_t*)val, idx, cnt,
-                       ovf_rows, n_ovf, cap, (bf16_t*)dense, need_rows, need_slots, n_need);
+                       ovf_rows, n_ovf, cap, (bf16_t*)dense, need_rows, need_slots, n_need, l1_part);
   else
     hipLaunchKernelGGL((k_ovf_fill<float, false>), grid, dim3(256), 0, s, f, NT, Tn, S, (const float*)val, idx, cnt,
-                       ovf_rows, n_ovf, cap, (float*)dense, need_rows, need_slots, n_need);
+                       ovf_rows, n_ovf, cap, (float*)dense, need_rows, need_slots, n_need, l1_part);
   return hipGetLastError();
 }
 

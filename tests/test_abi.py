@@ -77,8 +77,8 @@ def _al(n):
 
 def _need_lists(cap):
     # dense-backup slots recomputed by the GEMM: token rows and ovf_dense rows (the count sits
-    # with the other zeroed counters)
-    return 2 * _al(4 * cap)
+    # with the other zeroed counters), then one float per block of the rebuild (at most 1024)
+    return 2 * _al(4 * cap) + _al(4 * min(cap, 1024))
 
 
 def test_workspace_sizes():
