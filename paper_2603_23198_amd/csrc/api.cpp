@@ -165,6 +165,8 @@ struct FwdPlan {
   int n_zero = 0;                // counters from n_need (or tile_sem) on that the first kernel zeroes
   int32_t* order = nullptr;      // tokens by descending row count [T] (slice-walking gathers)
   float* fill_l1 = nullptr;      // per-block sums of the rebuilt dense-backup rows [ovf_fill_grid(cap)]
+  ClassifyPart* cls_part = nullptr;  // per-block statistics of the classification (summed by the list kernel)
+  float* gh_l1 = nullptr;        // gated: per-block sums of |h| of the ELL entries (summed by the L1 pass)
   void* H = nullptr;             // dense-fallback candidate: the dense ReLU rows [T][f] bf16
   int32_t* dense_flags = nullptr; // [2]: rows of the dense down GEMM (T or 0), gather skipped (1 or 0)
   int32_t* tile_sem = nullptr;   // split-K GEMMs of at most 64 rows: one counter per output tile
@@ -186,6 +188,10 @@ bool packed_gather(const sfl_ffn_args_t& a) { return a.dtype == SFL_BF16 && a.d 
 
 int64_t align_rows(int64_t r) { return (r + 255) / 256 * 256; }
 
+// Up to 64 tokens the gather's first block builds the dense-backup row list, else the list
+// kernel (which then also adds the classification blocks' statistics).
+bool list_by_gather(const sfl_ffn_args_t& a) { return a.T <= 64 && packed_gather(a) && !dense_candidate(a); }
+
 FwdPlan plan_forward(const sfl_ffn_args_t& a, void* ws) {
   Carve c(ws);
   FwdPlan p;
@@ -204,6 +210,7 @@ FwdPlan plan_forward(const sfl_ffn_args_t& a, void* ws) {
     const int64_t K = std::max<int64_t>(a.cfg.ell_width, 1);
     p.part_u = (float*)c.take((size_t)8 * a.T * K * 4);
     p.hval = c.take((size_t)a.T * K * 2);
+    if (rebuild_ovf(a)) p.gh_l1 = (float*)c.take((size_t)kGatedHMaxBlocks * 4);
   }
   if (a.dtype == SFL_BF16 && (cap > 0 || small_batch(a))) {
     p.part_rows = (int)std::min<int64_t>(align_rows(std::max<int64_t>(cap, a.T)), kPartRows);
@@ -224,6 +231,8 @@ FwdPlan plan_forward(const sfl_ffn_args_t& a, void* ws) {
     p.need_slots = (int32_t*)c.take((size_t)cap * 4);
     p.fill_l1 = (float*)c.take((size_t)ovf_fill_grid((int32_t)cap) * 4);
   }
+  if (a.T > 0 && !list_by_gather(a))
+    p.cls_part = (ClassifyPart*)c.take((size_t)classify_grid(a.T, a.f, a.cfg.tile_cols) * sizeof(ClassifyPart));
   p.bytes = c.used;
   return p;
 }
@@ -533,6 +542,7 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
   // small batches whose up projection leaves fp32 sums pack and classify in one launch
   const bool row_classify = pack_classify_rows_ok(T, f, a->cfg.tile_cols, a->cfg.tile_slots, vb);
   bool classified = false;
+  int gh_l1_n = 0;  // gated: per-block |h| sums waiting for the dense-backup stage's L1 pass
   const bool bf = a->dtype == SFL_BF16;
   const void* Wp = a->gated ? a->W_gate : a->W_up;                        // pattern-deciding projection
   const void* WpT = !bf ? nullptr : a->gated ? a->W_gateT : a->W_upT;     // its transposed copy, if given
@@ -621,20 +631,23 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
   }
   ev.record(1, s);
   // 2. hybrid classification (Sec. 3.4), unless done with the pack
+  // (the statistics of its blocks summed by the list kernel when that runs)
+  ClassifyPart* cls_part = classified || !a->stats ? nullptr : plan.cls_part;
   if (!classified)
     SFL_HIP(launch_classify(T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, a->cfg.ell_width, tw.val, tw.idx,
                             tw.cnt, tw.row_nnz, tw.row_ovf, tw.ell_val, tw.ell_idx, a->stats, s, l1_vals,
-                            packed_layout(a->cfg)));
+                            packed_layout(a->cfg), cls_part));
   // the dense-backup row list: up to 64 rows the gather's first block builds it (nothing
   // before the dense-backup stage reads it), else its own kernel
   OvfList late_list;
-  if (T <= 64 && packed_gather(*a) && !plan.H) {
+  if (list_by_gather(*a)) {
     late_list.rows = tw.ovf_rows;
     late_list.n = tw.n_ovf;
     late_list.cap = (int32_t)cap;
     late_list.stats = a->stats;
   } else {
-    SFL_HIP(launch_ovf_list(T, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s));
+    SFL_HIP(launch_ovf_list(T, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s, cls_part,
+                            cls_part ? (int)classify_grid(T, f, a->cfg.tile_cols) : 0));
   }
   ev.record(2, s);
   if (plan.H) {
@@ -686,8 +699,12 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
       SFL_HIP(launch_gated_updot(T, d, f, a->cfg.ell_width, tw.ell_idx, tw.row_nnz, tw.row_ovf, a->X, WuP,
                                  plan.part_u, s, order));
       if (T > kGatherFormsH) {
+        // above 256 tokens the blocks' sums of |h| are added by the dense-backup stage's L1
+        // pass, which then always runs for this layer when it has dense-backup capacity
+        const bool later = a->stats && cap > 0 && rebuild_ovf(*a);
         SFL_HIP(launch_gated_h(T, a->cfg.ell_width, tw.ell_val, tw.row_nnz, tw.row_ovf, plan.part_u, plan.hval, s,
-                               a->stats));
+                               a->stats, later ? plan.gh_l1 : nullptr));
+        gh_l1_n = later ? launch_gated_h_blocks(T, a->cfg.ell_width) : 0;
         hv = plan.hval;
       }
     }
@@ -794,7 +811,9 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
     // the partial-sum buffer holds part_rows rows of max(f, d) columns: more rows of d
     y.part_rows = (int)std::min<int64_t>((int64_t)plan.part_rows * std::max(f, d) / d, INT32_MAX);
     SFL_HIP(run_gemm(a->dtype, LAY_KC, blay, EPI_ACT, y, s));
-    if (!l1_in_gemm) SFL_HIP(launch_ovf_l1(f, vb, ovf_dense, tw.n_ovf, (int32_t)cap, a->stats, s, a->gated ? 1 : 0));
+    if (!l1_in_gemm)
+      SFL_HIP(launch_ovf_l1(f, vb, ovf_dense, tw.n_ovf, (int32_t)cap, a->stats, s, a->gated ? 1 : 0,
+                            gh_l1_n ? plan.gh_l1 : nullptr, gh_l1_n));
   }
   ev.record(4, s);
   return SFL_OK;

@@ -67,6 +67,20 @@ template <typename T> __device__ __forceinline__ T wave_sum(T v) {
   return v;
 }
 
+// Sum of a[i] for i = first, first + step, ... below n, in that order, eight loads in
+// flight at a time (a load past the end re-reads a[n - 1] and zero is added in its place).
+__device__ __forceinline__ float strided_sum(const float* __restrict__ a, int n, int first, int step) {
+  float s = 0.f;
+  for (int i0 = first; i0 < n; i0 += 8 * step) {
+    float q[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) q[u] = a[min(i0 + u * step, n - 1)];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s += i0 + u * step < n ? q[u] : 0.f;
+  }
+  return s;
+}
+
 // Inclusive prefix sum over the 64 lanes.
 __device__ __forceinline__ int wave_incl_scan(int v) {
   const int l = lane_id();

@@ -764,7 +764,7 @@ __global__ __launch_bounds__(256) void k_gated_h(int64_t T, int K, const bf16_t*
                                                  const int32_t* __restrict__ row_nnz,
                                                  const uint8_t* __restrict__ row_ovf,
                                                  const float* __restrict__ part_u, bf16_t* __restrict__ h,
-                                                 sfl_stats_t* __restrict__ stats) {
+                                                 sfl_stats_t* __restrict__ stats, float* __restrict__ l1_part) {
   const int64_t total = T * (int64_t)K;
   float l1 = 0.f;
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
@@ -778,14 +778,15 @@ __global__ __launch_bounds__(256) void k_gated_h(int64_t T, int K, const bf16_t*
     h[i] = hb;
     l1 += fabsf(bf16_to_f32(hb));
   }
-  if (!stats) return;
+  if (!stats && !l1_part) return;
   l1 = wave_sum<float>(l1);
   __shared__ float part[4];
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = l1;
   __syncthreads();
   if (threadIdx.x == 0) {
     const float tot = part[0] + part[1] + part[2] + part[3];
-    if (tot != 0.f) atomicAdd(&stats->l1_sum, (double)tot);
+    if (l1_part) l1_part[blockIdx.x] = tot;  // a plain store: the blocks end together
+    else if (tot != 0.f) atomicAdd(&stats->l1_sum, (double)tot);
   }
 }
 
@@ -1186,14 +1187,20 @@ hipError_t launch_gated_updot(int64_t T, int64_t d, int64_t f, int K, const uint
   return hipGetLastError();
 }
 
+int launch_gated_h_blocks(int64_t T, int K) {
+  return (int)std::min<int64_t>(cdiv(T * (int64_t)K, 256), kGatedHMaxBlocks);
+}
+
 hipError_t launch_gated_h(int64_t T, int K, const void* ell_val, const int32_t* row_nnz, const uint8_t* row_ovf,
-                          const float* part_u, void* h, hipStream_t s, sfl_stats_t* stats) {
+                          const float* part_u, void* h, hipStream_t s, sfl_stats_t* stats, float* l1_part) {
   if (T == 0 || K == 0) return hipSuccess;
+  // with statistics added by atomics each block adds one float64 atomic to the same
+  // address, which serialise: fewer blocks then
   const int64_t n = T * (int64_t)K;
-  // with statistics each block adds one float64 atomic to the same address: fewer blocks
-  const unsigned grid = (unsigned)std::min<int64_t>(cdiv(n, 256), stats ? 1024 : 4096);
+  const unsigned grid = (unsigned)(stats && !l1_part ? std::min<int64_t>(cdiv(n, 256), 1024)
+                                                     : launch_gated_h_blocks(T, K));
   hipLaunchKernelGGL(k_gated_h, dim3(grid), dim3(256), 0, s, T, K, (const bf16_t*)ell_val, row_nnz, row_ovf, part_u,
-                     (bf16_t*)h, stats);
+                     (bf16_t*)h, l1_part ? nullptr : stats, l1_part);
   return hipGetLastError();
 }
 

@@ -992,8 +992,7 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(GemmParams p) {
   const int n4 = p.N / 4;
   const int64_t total = (int64_t)m_eff * n4;
   float s = 0.f;
-  if (l1 && blockIdx.x == 0)
-    for (int i = threadIdx.x; i < p.n_l1_more; i += 256) s += p.l1_more[i];
+  if (l1 && blockIdx.x == 0) s = strided_sum(p.l1_more, p.n_l1_more, threadIdx.x, 256);
   for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
     const int m = (int)(e / n4);
     const int n = (int)(e % n4) * 4;

@@ -133,14 +133,24 @@ hipError_t launch_pack_twell(const float* Z, int64_t T, int64_t f, int val_bf16,
 hipError_t launch_pack_twell_parts(const float* part, int ks, const float* bias, const float* shift, int64_t T,
                                    int64_t f, int val_bf16, int tile_cols, int tile_slots, void* val, uint16_t* idx,
                                    int32_t* cnt, hipStream_t s, bool packed = false);
-// Hybrid classification: row_nnz, row_ovf, optional ELL rows and stats partials; with
-// l1_vals the stored values of the sparse rows are added to stats->l1_sum (they are the
-// activations h of the non-gated layer; the gated layer's are gate values, and its L1 sum
-// comes from launch_gated_h).
+// Statistics of one classification block: entries, overflowing tiles, sum of the stored
+// values (l1_vals).
+struct ClassifyPart {
+  long long nnz;
+  int over;
+  float l1;
+};
+// Hybrid classification: row_nnz, row_ovf, optional ELL rows and stats; with l1_vals the
+// stored values of the sparse rows are added to stats->l1_sum (they are the activations h
+// of the non-gated layer; the gated layer's are gate values, and its L1 sum comes from
+// launch_gated_h). With part (classify_grid(T, f, tile_cols) entries) each block stores
+// its statistics there instead of adding them; launch_ovf_list then adds them.
+int64_t classify_grid(int64_t T, int64_t f, int tile_cols);
 hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int tile_cols, int tile_slots,
                            int ell_width, const void* val, const uint16_t* idx, const int32_t* cnt,
                            int32_t* row_nnz, uint8_t* row_ovf, void* ell_val, uint16_t* ell_idx,
-                           sfl_stats_t* stats, hipStream_t s, int l1_vals = 1, bool packed = false);
+                           sfl_stats_t* stats, hipStream_t s, int l1_vals = 1, bool packed = false,
+                           ClassifyPart* part = nullptr);
 // Small batches (1 <= T <= 256 rows, f a multiple of 64, T_n of 64, 128 or 256, the row
 // and its tile entries within the kernel's LDS): the pack (from Z with ks = 0, else from
 // ks <= 8 split-K partial sums as launch_pack_twell_parts; fp32 values only with ks <= 1)
@@ -152,9 +162,11 @@ hipError_t launch_pack_classify_rows(const float* Z, int ks, const float* bias, 
                                      uint16_t* idx, int32_t* cnt, int32_t* row_nnz, uint8_t* row_ovf, void* ell_val,
                                      uint16_t* ell_idx, sfl_stats_t* stats, hipStream_t s, int l1_vals = 1,
                                      bool packed = false);
-// Ascending dense-backup row list + n_ovf + capacity flag (one workgroup).
+// Ascending dense-backup row list + n_ovf + capacity flag (one workgroup); with parts and
+// stats, also adds the n_parts classification blocks' statistics to stats.
 hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32_t* ovf_rows,
-                           int32_t* n_ovf, sfl_stats_t* stats, hipStream_t s);
+                           int32_t* n_ovf, sfl_stats_t* stats, hipStream_t s, const ClassifyPart* parts = nullptr,
+                           int n_parts = 0);
 // Zeroes the statistics (if given) and n_zero counters from zero.
 hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s, int32_t* zero = nullptr, int n_zero = 0);
 // order[0 .. T): the sparse rows by descending row_nnz, then the dense-backup rows (one
@@ -180,8 +192,10 @@ hipError_t launch_ovf_fill(int64_t f, int val_bf16, int Tn, int S, const void* v
 // when force or the sparse rows' (row_ovf = 0) row_nnz sum to more than T f / 64, else 0, 0.
 hipError_t launch_dense_decision(int64_t T, int64_t f, bool force, const int32_t* row_nnz, const uint8_t* row_ovf,
                                  int32_t* flags, hipStream_t s);
+// Block 0 also adds the n_extra sums at extra (another kernel's per-block share).
 hipError_t launch_ovf_l1(int64_t f, int val_bf16, const void* ovf_dense, const int32_t* n_ovf,
-                         int32_t cap, sfl_stats_t* stats, hipStream_t s, int absval);
+                         int32_t cap, sfl_stats_t* stats, hipStream_t s, int absval, const float* extra = nullptr,
+                         int n_extra = 0);
 
 // ---------------------------------------------------------- gathers ----
 // Y[t, :] = sum_e ell_val[t][e] * W[ell_idx[t][e], :] for rows with row_ovf[t] == 0.
@@ -231,9 +245,14 @@ hipError_t launch_csc_gather(int64_t n_units, int64_t d, int64_t R, const int32_
 // out[t][e] = sum of the 8 partials [8][T][K] + add on the sparse rows' entries (fp32).
 hipError_t launch_sum_parts(int64_t T, int K, const int32_t* row_nnz, const uint8_t* row_ovf, const float* part,
                             float add, float* out, hipStream_t s);
-// With stats, sum |h| of the written entries into stats->l1_sum.
+// With stats, sum |h| of the written entries into stats->l1_sum; with l1_part instead
+// (kGatedHMaxBlocks floats), each block stores its sum there (launch_gated_h_blocks(T, K)
+// of them) for a later launch_ovf_l1 to add.
+constexpr int kGatedHMaxBlocks = 4096;
+int launch_gated_h_blocks(int64_t T, int K);
 hipError_t launch_gated_h(int64_t T, int K, const void* ell_val, const int32_t* row_nnz, const uint8_t* row_ovf,
-                          const float* part_u, void* h, hipStream_t s, sfl_stats_t* stats = nullptr);
+                          const float* part_u, void* h, hipStream_t s, sfl_stats_t* stats = nullptr,
+                          float* l1_part = nullptr);
 // Gated fused up-dot + down (Alg. 2) from the ELL rows of the gate pattern.
 // --------------------------------------------------------- backward ----
 // (declared in backward.h)

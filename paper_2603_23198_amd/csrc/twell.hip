@@ -164,8 +164,10 @@ constexpr int kClassifyMaxTiles = 512;
 constexpr int kClassifyRowsPerWave = 8;
 
 // Statistics of a block's rows, reduced in LDS and added to the device totals with one
-// atomic per field per block (per-row atomics on the same address serialise).
-__device__ __forceinline__ void block_stats_add(sfl_stats_t* stats, int64_t nnz, int tile_over, float l1) {
+// atomic per field per block (per-row atomics on the same address serialise), or, given
+// part, stored there for the dense-backup list kernel to add (no atomics at all).
+__device__ __forceinline__ void block_stats_add(sfl_stats_t* stats, int64_t nnz, int tile_over, float l1,
+                                                ClassifyPart* part = nullptr) {
   __shared__ long long s_nnz[16];
   __shared__ int s_over[16];
   __shared__ float s_l1[16];
@@ -186,9 +188,13 @@ __device__ __forceinline__ void block_stats_add(sfl_stats_t* stats, int64_t nnz,
       b += s_over[i];
       c += s_l1[i];
     }
-    if (a) atomicAdd((unsigned long long*)&stats->total_nnz, (unsigned long long)a);
-    if (b) atomicAdd((unsigned long long*)&stats->n_tile_ovf, (unsigned long long)b);
-    if (c != 0.f) atomicAdd(&stats->l1_sum, (double)c);
+    if (part) {
+      part[blockIdx.x] = ClassifyPart{a, b, c};
+    } else {
+      if (a) atomicAdd((unsigned long long*)&stats->total_nnz, (unsigned long long)a);
+      if (b) atomicAdd((unsigned long long*)&stats->n_tile_ovf, (unsigned long long)b);
+      if (c != 0.f) atomicAdd(&stats->l1_sum, (double)c);
+    }
   }
 }
 
@@ -198,7 +204,8 @@ __global__ __launch_bounds__(kClassifyWaves * 64) void k_classify(int64_t T, int
                                                   const uint16_t* __restrict__ idx, const int32_t* __restrict__ cnt,
                                                   int32_t* __restrict__ row_nnz, uint8_t* __restrict__ row_ovf,
                                                   V* __restrict__ ell_val, uint16_t* __restrict__ ell_idx,
-                                                  sfl_stats_t* __restrict__ stats, int rpw, int l1_vals) {
+                                                  sfl_stats_t* __restrict__ stats, int rpw, int l1_vals,
+                                                  ClassifyPart* __restrict__ part) {
   __shared__ int incl_lds[kClassifyWaves][kClassifyMaxTiles];
   const int l = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
@@ -231,9 +238,14 @@ __global__ __launch_bounds__(kClassifyWaves * 64) void k_classify(int64_t T, int
     nnz_sum += total;
     over_sum += tile_over;
     if (!ovf) {
-      for (int q0 = 0; q0 < total; q0 += 64) {
-        const int q = q0 + l;
-        if (q < total) {
+      // 4 x 64 entries per pass: the slots are located first, then all their loads issued
+      // (a lane past the row's total reads slot 0 of tile 0 and stores nothing), so a pass
+      // waits on memory once
+      for (int q0 = 0; q0 < total; q0 += 4 * 64) {
+        int jq[4], sq[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int q = q0 + u * 64 + l;
           // first tile j with incl[j] > q
           int lo = 0, hi = NT - 1;
           while (lo < hi) {
@@ -241,13 +253,23 @@ __global__ __launch_bounds__(kClassifyWaves * 64) void k_classify(int64_t T, int
             if (incl_s[mid] > q) hi = mid; else lo = mid + 1;
           }
           const int excl = lo > 0 ? incl_s[lo - 1] : 0;
-          V v;
-          uint16_t col;
-          sl.slot(lo, q - excl, v, col);
-          if (l1_vals) l1 += VT<V>::load(&v, 0);
-          if (ell_val) {
-            ell_val[t * (int64_t)K + q] = v;
-            ell_idx[t * (int64_t)K + q] = col;
+          const bool ok = q < total;
+          jq[u] = ok ? lo : 0;
+          sq[u] = ok ? q - excl : 0;
+        }
+        V v[4];
+        uint16_t col[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) sl.slot(jq[u], sq[u], v[u], col[u]);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int q = q0 + u * 64 + l;
+          if (q < total) {
+            if (l1_vals) l1 += VT<V>::load(&v[u], 0);
+            if (ell_val) {
+              ell_val[t * (int64_t)K + q] = v[u];
+              ell_idx[t * (int64_t)K + q] = col[u];
+            }
           }
         }
       }
@@ -255,7 +277,7 @@ __global__ __launch_bounds__(kClassifyWaves * 64) void k_classify(int64_t T, int
     // all lanes are done reading this row's prefix before the next row overwrites it
     __builtin_amdgcn_wave_barrier();
   }
-  if (stats) block_stats_add(stats, nnz_sum, over_sum, l1);
+  if (stats) block_stats_add(stats, nnz_sum, over_sum, l1, part);
 }
 
 // Fallback for rows with more tiles than the LDS prefix holds: walks the tiles in order.
@@ -265,7 +287,8 @@ __global__ __launch_bounds__(256) void k_classify_wide(int64_t T, int NT, int S,
                                                        const int32_t* __restrict__ cnt,
                                                        int32_t* __restrict__ row_nnz, uint8_t* __restrict__ row_ovf,
                                                        V* __restrict__ ell_val, uint16_t* __restrict__ ell_idx,
-                                                       sfl_stats_t* __restrict__ stats, int l1_vals) {
+                                                       sfl_stats_t* __restrict__ stats, int l1_vals,
+                                                       ClassifyPart* __restrict__ part) {
   const int64_t t0 = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const bool row_ok = t0 < T;
   const int64_t t = row_ok ? t0 : 0;
@@ -304,29 +327,37 @@ __global__ __launch_bounds__(256) void k_classify_wide(int64_t T, int NT, int S,
       offset += cj;
     }
   }
-  if (stats) block_stats_add(stats, total, tile_over, l1);
+  if (stats) block_stats_add(stats, total, tile_over, l1, part);
+}
+
+// several rows per wave amortise the per-block statistics, but the walk is latency bound:
+// keep about 4096 waves (16 per CU) in flight before packing rows
+int classify_rows_per_wave(int64_t T) {
+  return (int)std::max<int64_t>(1, std::min<int64_t>(kClassifyRowsPerWave, T / 4096));
+}
+int64_t classify_grid(int64_t T, int64_t f, int Tn) {
+  const int NT = (int)cdiv(f, Tn);
+  return NT > kClassifyMaxTiles ? cdiv(T, 4) : cdiv(T, kClassifyWaves * classify_rows_per_wave(T));
 }
 
 hipError_t launch_classify(int64_t T, int64_t f, int val_bf16, int Tn, int S, int K, const void* val,
                            const uint16_t* idx, const int32_t* cnt, int32_t* row_nnz, uint8_t* row_ovf,
                            void* ell_val, uint16_t* ell_idx, sfl_stats_t* stats, hipStream_t s, int l1_vals,
-                           bool packed) {
+                           bool packed, ClassifyPart* part) {
   if (T == 0) return hipSuccess;
   if (packed && !val_bf16) return hipErrorInvalidValue;
   const int NT = (int)cdiv(f, Tn);
   const bool wide = NT > kClassifyMaxTiles;
-  // several rows per wave amortise the per-block statistics, but the walk is latency
-  // bound: keep about 4096 waves (16 per CU) in flight before packing rows
-  const int rpw = (int)std::max<int64_t>(1, std::min<int64_t>(kClassifyRowsPerWave, T / 4096));
-  const dim3 grid((unsigned)(wide ? cdiv(T, 4) : cdiv(T, kClassifyWaves * rpw)));
+  const int rpw = classify_rows_per_wave(T);
+  const dim3 grid((unsigned)classify_grid(T, f, Tn));
 #define SFL_CLASSIFY(V_, PK_)                                                                                         \
   do {                                                                                                               \
     if (wide)                                                                                                        \
       hipLaunchKernelGGL((k_classify_wide<V_, PK_>), grid, dim3(256), 0, s, T, NT, S, K, (const V_*)val, idx, cnt,    \
-                         row_nnz, row_ovf, (V_*)ell_val, ell_idx, stats, l1_vals);                                   \
+                         row_nnz, row_ovf, (V_*)ell_val, ell_idx, stats, l1_vals, part);                             \
     else                                                                                                             \
       hipLaunchKernelGGL((k_classify<V_, PK_>), grid, dim3(kClassifyWaves * 64), 0, s, T, NT, S, K, (const V_*)val,  \
-                         idx, cnt, row_nnz, row_ovf, (V_*)ell_val, ell_idx, stats, rpw, l1_vals);                    \
+                         idx, cnt, row_nnz, row_ovf, (V_*)ell_val, ell_idx, stats, rpw, l1_vals, part);              \
   } while (0)
   if (packed)
     SFL_CLASSIFY(bf16_t, true);
@@ -650,9 +681,46 @@ hipError_t launch_nnz_order(int64_t T, int K, const int32_t* row_nnz, const uint
 constexpr int kOvfRowsPerThread = 16;
 __global__ __launch_bounds__(1024) void k_ovf_list(int64_t T, int32_t cap, const uint8_t* __restrict__ row_ovf,
                                                    int32_t* __restrict__ ovf_rows, int32_t* __restrict__ n_ovf,
-                                                   sfl_stats_t* __restrict__ stats) {
+                                                   sfl_stats_t* __restrict__ stats,
+                                                   const ClassifyPart* __restrict__ parts, int n_parts) {
   __shared__ int wsum[16];
   const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
+  if (parts && stats) {
+    // the classification blocks' statistics, added with one atomic per field
+    __shared__ long long pn[16];
+    __shared__ int po[16];
+    __shared__ float pl[16];
+    long long a = 0;
+    int b = 0;
+    float c = 0.f;
+    for (int i = tid; i < n_parts; i += 1024) {
+      a += parts[i].nnz;
+      b += parts[i].over;
+      c += parts[i].l1;
+    }
+    a = wave_sum<long long>(a);
+    b = wave_sum<int>(b);
+    c = wave_sum<float>(c);
+    if (l == 0) {
+      pn[w] = a;
+      po[w] = b;
+      pl[w] = c;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      a = 0;
+      b = 0;
+      c = 0.f;
+      for (int i = 0; i < 16; ++i) {
+        a += pn[i];
+        b += po[i];
+        c += pl[i];
+      }
+      if (a) atomicAdd((unsigned long long*)&stats->total_nnz, (unsigned long long)a);
+      if (b) atomicAdd((unsigned long long*)&stats->n_tile_ovf, (unsigned long long)b);
+      if (c != 0.f) atomicAdd(&stats->l1_sum, (double)c);
+    }
+  }
   int64_t base = 0;
   for (int64_t r0 = 0; r0 < T; r0 += 1024 * kOvfRowsPerThread) {
     const int64_t t0 = r0 + (int64_t)tid * kOvfRowsPerThread;
@@ -686,8 +754,9 @@ __global__ __launch_bounds__(1024) void k_ovf_list(int64_t T, int32_t cap, const
 }
 
 hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32_t* ovf_rows, int32_t* n_ovf,
-                           sfl_stats_t* stats, hipStream_t s) {
-  hipLaunchKernelGGL(k_ovf_list, dim3(1), dim3(1024), 0, s, T, cap, row_ovf, ovf_rows, n_ovf, stats);
+                           sfl_stats_t* stats, hipStream_t s, const ClassifyPart* parts, int n_parts) {
+  hipLaunchKernelGGL(k_ovf_list, dim3(1), dim3(1024), 0, s, T, cap, row_ovf, ovf_rows, n_ovf, stats, parts,
+                     n_parts);
   return hipGetLastError();
 }
 
@@ -700,12 +769,14 @@ hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32
 constexpr int kL1Blocks = 256;
 template <typename V>
 __global__ __launch_bounds__(256) void k_ovf_l1(int64_t f, const V* __restrict__ dense, const int32_t* n_ovf,
-                                                int32_t cap, sfl_stats_t* stats, int absval) {
+                                                int32_t cap, sfl_stats_t* stats, int absval,
+                                                const float* __restrict__ extra, int n_extra) {
   constexpr int PER = 16 / (int)sizeof(V);
   const int n = min(*n_ovf, cap);
   // the magnitude keeps every bit but the sign
   const uint32_t keep = absval ? 0x7fffffffu : 0xffffffffu;
   float s = 0.f;
+  if (blockIdx.x == 0) s = strided_sum(extra, n_extra, threadIdx.x, 256);
   // the rows are contiguous: one flat pass over n f values, 16 bytes per lane and four
   // loads in flight per lane
   const int64_t total = (int64_t)n * f;
@@ -744,13 +815,16 @@ __global__ __launch_bounds__(256) void k_ovf_l1(int64_t f, const V* __restrict__
 }
 
 hipError_t launch_ovf_l1(int64_t f, int val_bf16, const void* dense, const int32_t* n_ovf, int32_t cap,
-                         sfl_stats_t* stats, hipStream_t s, int absval) {
+                         sfl_stats_t* stats, hipStream_t s, int absval, const float* extra, int n_extra) {
   if (!stats || cap == 0) return hipSuccess;
+  if (!extra) n_extra = 0;
   const dim3 grid((unsigned)kL1Blocks);
   if (val_bf16)
-    hipLaunchKernelGGL(k_ovf_l1<bf16_t>, grid, dim3(256), 0, s, f, (const bf16_t*)dense, n_ovf, cap, stats, absval);
+    hipLaunchKernelGGL(k_ovf_l1<bf16_t>, grid, dim3(256), 0, s, f, (const bf16_t*)dense, n_ovf, cap, stats, absval,
+                       extra, n_extra);
   else
-    hipLaunchKernelGGL(k_ovf_l1<float>, grid, dim3(256), 0, s, f, (const float*)dense, n_ovf, cap, stats, absval);
+    hipLaunchKernelGGL(k_ovf_l1<float>, grid, dim3(256), 0, s, f, (const float*)dense, n_ovf, cap, stats, absval,
+                       extra, n_extra);
   return hipGetLastError();
 }
 

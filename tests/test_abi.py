@@ -81,31 +81,40 @@ def _need_lists(cap):
     return 2 * _al(4 * cap) + _al(4 * min(cap, 1024))
 
 
+def _cls_parts(T, f, Tn=256):
+    # the classification's per-block statistics, 16 bytes a block, summed by the list kernel
+    rpw = max(1, min(8, T // 4096))
+    grid = -(-T // 4) if -(-f // Tn) > 512 else -(-T // (16 * rpw))
+    return _al(16 * grid)
+
+
 def test_workspace_sizes():
     a = _fake_args(b.SFL_BF16, 128, 256, 1024, ell_width=32)
     ws = b.sfl_workspace_size(a, 0)
     part = 256 * 1024 * 4  # split-K partial sums of the dense-backup GEMMs: 256-row multiple x max(f, d) fp32
-    assert ws == 128 * 1024 * 2 + part  # dense-backup rows live in the workspace when not given
+    assert ws == 128 * 1024 * 2 + part + _cls_parts(128, 1024)  # dense-backup rows live in the workspace when not given
     a.twell.ovf_dense = 0x2000
-    assert b.sfl_workspace_size(a, 0) == part  # fused TwELL epilogue: no other scratch
+    assert b.sfl_workspace_size(a, 0) == part + _cls_parts(128, 1024)  # fused TwELL epilogue: no other scratch
     a32 = _fake_args(b.SFL_F32, 64, 256, 1024, ell_width=32)
     a32.twell.ovf_dense = 0x2000
-    assert b.sfl_workspace_size(a32, 0) == 64 * 1024 * 4  # fp32: pre-activations staged
+    assert b.sfl_workspace_size(a32, 0) == 64 * 1024 * 4 + _cls_parts(64, 1024)  # fp32: pre-activations staged
     # above 256 tokens the dense-backup rows are rebuilt from the TwELL slabs, and the rows
     # the GEMM still recomputes are listed in the workspace
     big = _fake_args(b.SFL_BF16, 512, 256, 1024, ell_width=16, ovf_capacity=64)
     big.twell.ovf_dense = 0x2000
     # partial sums: 512 rows (T); a capacity of at most 64 rows adds one counter per
     # 128-column tile of the wider of f and d
-    assert b.sfl_workspace_size(big, 0) == 512 * 1024 * 4 + _need_lists(64) + _al(4 * (1 + 8))
+    assert b.sfl_workspace_size(big, 0) == 512 * 1024 * 4 + _need_lists(64) + _al(4 * (1 + 8)) + _cls_parts(512, 1024)
     wide = _fake_args(b.SFL_BF16, 512, 70016, 1024, ell_width=16, ovf_capacity=64)
     wide.twell.ovf_dense = 0x2000
-    assert b.sfl_workspace_size(wide, 0) == 512 * 70016 * 4 + _need_lists(64) + _al(4 * (1 + 547))
+    assert b.sfl_workspace_size(wide, 0) == (512 * 70016 * 4 + _need_lists(64) + _al(4 * (1 + 547))
+                                             + _cls_parts(512, 1024))
     # an ELL width of at least f / 32 makes the call a dense-fallback candidate: the
     # workspace adds the dense ReLU rows H [T][f] bf16 and two flags
     dense = _fake_args(b.SFL_BF16, 512, 256, 1024, ell_width=32, ovf_capacity=64)
     dense.twell.ovf_dense = 0x2000
-    assert b.sfl_workspace_size(dense, 0) == 512 * 1024 * 4 + _need_lists(64) + _al(4 * (1 + 8)) + 512 * 1024 * 2 + _al(8)
+    assert b.sfl_workspace_size(dense, 0) == (512 * 1024 * 4 + _need_lists(64) + _al(4 * (1 + 8)) + 512 * 1024 * 2
+                                              + _al(8) + _cls_parts(512, 1024))
     # dense baseline: H, then split-K partials for a GEMM whose 256 x 256 tiles fill at most
     # half of the CUs (here the down GEMM, K = 1024: four ranges of 256) -- at most 8 splits,
     # 256 of K each, items within one block per CU, 64 MiB of partial sums
