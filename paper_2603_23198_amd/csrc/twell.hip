@@ -633,6 +633,7 @@ hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s, int32_t* zero, i
 // token placed at its bucket's cursor (LDS atomics, so the order within a bucket varies;
 // the gathers' results do not depend on it).
 constexpr int kOrderMaxBuckets = 16384;
+constexpr int kOrderPer = 8;  // tokens per thread and pass of k_nnz_order
 bool nnz_order_supported(int K) { return K >= 0 && K + 2 <= kOrderMaxBuckets; }
 
 __global__ __launch_bounds__(1024) void k_nnz_order(int64_t T, int K, const int32_t* __restrict__ row_nnz,
@@ -641,10 +642,37 @@ __global__ __launch_bounds__(1024) void k_nnz_order(int64_t T, int K, const int3
   __shared__ int wsum[16];
   const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
   const int nb = K + 2;
-  auto bucket = [&](int64_t t) { return row_ovf && row_ovf[t] ? K + 1 : K - min(max(row_nnz[t], 0), K); };
   for (int i = tid; i < nb; i += 1024) hist[i] = 0;
   __syncthreads();
-  for (int64_t t = tid; t < T; t += 1024) atomicAdd(&hist[bucket(t)], 1);
+  // passes of kOrderPer tokens per thread, their counts (and flags) loaded together, with
+  // no load under a condition (a token past the batch reads token T - 1 and counts
+  // nothing); a single pass keeps the buckets for the placement below
+  int bk[kOrderPer];
+  auto buckets = [&](int64_t t0) {
+    int nz[kOrderPer];
+    if (row_ovf) {
+      uint8_t ov[kOrderPer];
+#pragma unroll
+      for (int u = 0; u < kOrderPer; ++u) {
+        const int64_t t = min(t0 + 1024 * u, T - 1);
+        nz[u] = row_nnz[t];
+        ov[u] = row_ovf[t];
+      }
+#pragma unroll
+      for (int u = 0; u < kOrderPer; ++u) bk[u] = ov[u] ? K + 1 : K - min(max(nz[u], 0), K);
+    } else {
+#pragma unroll
+      for (int u = 0; u < kOrderPer; ++u) nz[u] = row_nnz[min(t0 + 1024 * u, T - 1)];
+#pragma unroll
+      for (int u = 0; u < kOrderPer; ++u) bk[u] = K - min(max(nz[u], 0), K);
+    }
+  };
+  for (int64_t t0 = tid; t0 < T; t0 += 1024 * kOrderPer) {
+    buckets(t0);
+#pragma unroll
+    for (int u = 0; u < kOrderPer; ++u)
+      if (t0 + 1024 * u < T) atomicAdd(&hist[bk[u]], 1);
+  }
   __syncthreads();
   // exclusive scan: thread j owns buckets [j per, (j + 1) per)
   const int per = (nb + 1023) / 1024;
@@ -663,7 +691,13 @@ __global__ __launch_bounds__(1024) void k_nnz_order(int64_t T, int K, const int3
     run += c;
   }
   __syncthreads();
-  for (int64_t t = tid; t < T; t += 1024) order[atomicAdd(&hist[bucket(t)], 1)] = (int32_t)t;
+  const bool one_pass = T <= 1024 * kOrderPer;
+  for (int64_t t0 = tid; t0 < T; t0 += 1024 * kOrderPer) {
+    if (!one_pass) buckets(t0);
+#pragma unroll
+    for (int u = 0; u < kOrderPer; ++u)
+      if (t0 + 1024 * u < T) order[atomicAdd(&hist[bk[u]], 1)] = (int32_t)(t0 + 1024 * u);
+  }
 }
 
 hipError_t launch_nnz_order(int64_t T, int K, const int32_t* row_nnz, const uint8_t* row_ovf, int32_t* order,
@@ -724,10 +758,15 @@ __global__ __launch_bounds__(1024) void k_ovf_list(int64_t T, int32_t cap, const
   int64_t base = 0;
   for (int64_t r0 = 0; r0 < T; r0 += 1024 * kOvfRowsPerThread) {
     const int64_t t0 = r0 + (int64_t)tid * kOvfRowsPerThread;
+    // every flag load is issued (a row past the batch re-reads row T - 1), so that all 16
+    // are in flight together
+    uint8_t fl[kOvfRowsPerThread];
+#pragma unroll
+    for (int k = 0; k < kOvfRowsPerThread; ++k) fl[k] = row_ovf[min(t0 + k, T - 1)];
     uint32_t bits = 0;
 #pragma unroll
     for (int k = 0; k < kOvfRowsPerThread; ++k)
-      if (t0 + k < T && row_ovf[t0 + k]) bits |= 1u << k;
+      if (t0 + k < T && fl[k]) bits |= 1u << k;
     const int c = __popc(bits);
     const int incl = wave_incl_scan(c);
     if (l == 63) wsum[w] = incl;
