@@ -130,20 +130,28 @@ __global__ __launch_bounds__(1024) void k_col_ptr(int64_t f, const int32_t* __re
 // (d) fill: entry (t, e) with unit n goes to position colstart[n] + (offset of t's block
 // in n's list) + (the block's earlier tokens that activate n: the mask's bits below t),
 // i.e. each unit's list in token order. Every entry is placed independently (one wave
-// per token). Up to three per-entry values go beside the token (fp32 sources [T][K];
-// value 0 may come from the bf16 ELL values).
+// per token) as one 16-byte record: the token, then up to three per-entry values (fp32
+// sources [T][K]; value 0 may come from the bf16 ELL values; an unused one is 0). The
+// positions are scattered, so one store per entry rather than one per array matters.
+// The sources are read for every entry of a pass: v[1] always, v[0] and v[2] when gated,
+// hb when not.
 struct FillValues {
   const bf16_t* hb;    // when non-null: value 0 from these bf16 entries
   const float* v[3];   // fp32 sources (null: unused)
-  float* out[3];       // [T K] destinations in list order
 };
 
+// GATED: the three values from fp32 sources; else h from the bf16 ELL values and dz
+// (value 3 is 0). A wave takes 4 x 64 of its token's entries per pass: their indices and
+// values are loaded together, then the list offsets of their units, then the records
+// are stored (an entry past the row re-reads its last entry and stores nothing).
+template <bool GATED>
 __global__ __launch_bounds__(256) void k_blk_fill(int64_t T, int K, int64_t f, const uint16_t* __restrict__ ell_idx,
                                                   const int32_t* __restrict__ row_nnz,
                                                   const uint8_t* __restrict__ row_ovf,
                                                   const uint64_t* __restrict__ bm, const int32_t* __restrict__ bc,
-                                                  const int32_t* __restrict__ colstart, int32_t* __restrict__ csc_tok,
+                                                  const int32_t* __restrict__ colstart, u32x4_t* __restrict__ csc_rec,
                                                   FillValues fv) {
+  constexpr int U = 4;
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int l = threadIdx.x & 63;
   if (t >= T || row_ovf[t]) return;
@@ -151,14 +159,37 @@ __global__ __launch_bounds__(256) void k_blk_fill(int64_t T, int K, int64_t f, c
   const int tt = (int)(t % kBlkTok);
   const uint64_t below = (1ull << tt) - 1ull;
   const int nnz = row_nnz[t];
-  for (int e = l; e < nnz; e += 64) {
-    const int64_t src = t * (int64_t)K + e;
-    const int64_t n = ell_idx[src];
-    const int pos = colstart[n] + bc[b * f + n] + __popcll(bm[b * f + n] & below);
-    csc_tok[pos] = (int32_t)t;
-    if (fv.out[0]) fv.out[0][pos] = fv.hb ? bf16_to_f32(fv.hb[src]) : fv.v[0][src];
-    if (fv.out[1]) fv.out[1][pos] = fv.v[1][src];
-    if (fv.out[2]) fv.out[2][pos] = fv.v[2][src];
+  for (int e0 = 0; e0 < nnz; e0 += U * 64) {
+    int64_t src[U];
+    int n[U];
+    float v0[U], v1[U], v2[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      src[u] = t * (int64_t)K + min(e0 + u * 64 + l, nnz - 1);
+      n[u] = ell_idx[src[u]];
+      v0[u] = GATED ? fv.v[0][src[u]] : bf16_to_f32(fv.hb[src[u]]);
+      v1[u] = fv.v[1][src[u]];
+      v2[u] = GATED ? fv.v[2][src[u]] : 0.f;
+    }
+    int cs[U], cb[U];
+    uint64_t mk[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      cs[u] = colstart[n[u]];
+      cb[u] = bc[b * f + n[u]];
+      mk[u] = bm[b * f + n[u]];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (e0 + u * 64 + l < nnz) {
+        u32x4_t r;
+        r[0] = (uint32_t)t;
+        r[1] = __float_as_uint(v0[u]);
+        r[2] = __float_as_uint(v1[u]);
+        r[3] = __float_as_uint(v2[u]);
+        csc_rec[cs[u] + cb[u] + __popcll(mk[u] & below)] = r;
+      }
+    }
   }
 }
 
@@ -215,10 +246,7 @@ struct BwdPlan {
   int32_t* uorder = nullptr;  // [f] the units by descending list length
   int32_t* order = nullptr;   // [T] the tokens by descending row count (token-group walks)
   int32_t* colstart = nullptr; // [f] list start of each unit
-  int32_t* csc_tok = nullptr; // [T K]
-  float* csc_h = nullptr;     // [T K] h
-  float* csc_z = nullptr;     // [T K] dz (gated: dh_u)
-  float* csc_g = nullptr;     // [T K] gated: dh_g
+  u32x4_t* csc_rec = nullptr; // [T K] records: token, h, dz (gated: dh_u), gated: dh_g
   float* dWuT = nullptr;      // [f][d]
   float* dWgT = nullptr;      // gated: [f][d]
   void* WupT = nullptr;       // [f][d] when neither W_upT nor W_up_packed is given
@@ -266,10 +294,7 @@ BwdPlan plan_backward(const sfl_ffn_bwd_args_t& a, void* ws) {
   p.uorder = (int32_t*)take((size_t)f * 4);
   p.order = (int32_t*)take((size_t)T * 4);
   p.colstart = (int32_t*)take((size_t)f * 4);
-  p.csc_tok = (int32_t*)take((size_t)T * K * 4);
-  p.csc_h = (float*)take((size_t)T * K * 4);
-  p.csc_z = (float*)take((size_t)T * K * 4);
-  if (gated) p.csc_g = (float*)take((size_t)T * K * 4);
+  p.csc_rec = (u32x4_t*)take((size_t)T * K * 16);
   p.dWuT = (float*)take((size_t)f * d * 4);
   if (gated) p.dWgT = (float*)take((size_t)f * d * 4);
   if (!a.W_upT && !a.W_up_packed) p.WupT = take((size_t)f * d * 2);
@@ -448,23 +473,28 @@ sfl_status_t backward_run(const sfl_ffn_bwd_args_t* a, hipStream_t s) {
     fv.v[0] = p.hf;
     fv.v[1] = p.dz;  // dh_u
     fv.v[2] = p.dhg;
-    fv.out[2] = p.csc_g;
   }
-  fv.out[0] = p.csc_h;
-  fv.out[1] = p.csc_z;
-  hipLaunchKernelGGL(k_blk_fill, dim3((unsigned)cdiv(T, 4)), dim3(256), 0, s, T, K, f, sv.ell_idx, sv.row_nnz,
-                     sv.row_ovf, p.bm, p.bc, p.colstart, p.csc_tok, fv);
+  if (gated)
+    hipLaunchKernelGGL(k_blk_fill<true>, dim3((unsigned)cdiv(T, 4)), dim3(256), 0, s, T, K, f, sv.ell_idx,
+                       sv.row_nnz, sv.row_ovf, p.bm, p.bc, p.colstart, p.csc_rec, fv);
+  else
+    hipLaunchKernelGGL(k_blk_fill<false>, dim3((unsigned)cdiv(T, 4)), dim3(256), 0, s, T, K, f, sv.ell_idx,
+                       sv.row_nnz, sv.row_ovf, p.bm, p.bc, p.colstart, p.csc_rec, fv);
   SFL_HIPB(hipGetLastError());
   rec(3);
   // 4. weight gradients of the sparse rows: per-unit gathers over slice-major dY and X
   SFL_HIPB(launch_pack_down(dY, p.dYP, T, d, s));
   SFL_HIPB(launch_pack_down(X, p.XP, T, d, s));
   const int64_t mean_bound = cdiv(T * (int64_t)K, f);  // the lists hold at most T K entries
-  SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, p.csc_tok, p.csc_h, mean_bound, p.dYP, a->dW_down, s, p.uorder));
-  SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, p.csc_tok, p.csc_z, mean_bound, p.XP, p.dWuT, s, p.uorder));
+  const int32_t* csc_tok = (const int32_t*)p.csc_rec;
+  const float* csc_val = (const float*)p.csc_rec;  // h at word 1, dz (dh_u) at 2, dh_g at 3
+  SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, csc_tok, csc_val + 1, mean_bound, p.dYP, a->dW_down, s, p.uorder,
+                             4));
+  SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, csc_tok, csc_val + 2, mean_bound, p.XP, p.dWuT, s, p.uorder, 4));
   SFL_HIPB(launch_transpose(p.dWuT, a->dW_up, f, d, 4, s));
   if (gated) {
-    SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, p.csc_tok, p.csc_g, mean_bound, p.XP, p.dWgT, s, p.uorder));
+    SFL_HIPB(launch_csc_gather(f, d, T, p.col_ptr, csc_tok, csc_val + 3, mean_bound, p.XP, p.dWgT, s, p.uorder,
+                               4));
     SFL_HIPB(launch_transpose(p.dWgT, a->dW_gate, f, d, 4, s));
   }
   rec(4);

@@ -791,7 +791,8 @@ __global__ __launch_bounds__(256) void k_gated_h(int64_t T, int K, const bf16_t*
 }
 
 // ---- per-unit gathers of the backward (dW_down, dW_up^T) ---------------------------------
-// out[n, :] = sum over unit n's list e in [ptr[n], ptr[n+1]) of val[e] * G[tok[e], :], fp32,
+// out[n, :] = sum over unit n's list e in [ptr[n], ptr[n+1]) of val[e s] * G[tok[e s], :], fp32
+// (s: the entries' stride in 4-byte words),
 // with G ([R][d] rows: dY or X) in the slice-major copy [d/SLICE][R][SLICE]. The same slice
 // walk as the down-projection gather (XCD x covers slices x, x+8, ...; a slice of G stays in
 // its L2 while the XCD's units stream through it); the lists are read straight from global
@@ -802,7 +803,7 @@ template <bool TG>
 __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_units, int64_t d, int64_t R,
                                                                   const int32_t* __restrict__ ptr,
                                                                   const int32_t* __restrict__ tok,
-                                                                  const float* __restrict__ val,
+                                                                  const float* __restrict__ val, int stride,
                                                                   const bf16_t* __restrict__ G, float* __restrict__ out,
                                                                   int n_slices, int upw, int lds_pairs,
                                                                   const int32_t* __restrict__ out_rows) {
@@ -831,8 +832,8 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_unit
       for (int u = 0; u < SU; ++u) {
         const int e = e0 + u * (int)blockDim.x;
         if (e < n_ent) {
-          tk[u] = tok[pb + e];
-          vl[u] = val[pb + e];
+          tk[u] = tok[(int64_t)(pb + e) * stride];
+          vl[u] = val[(int64_t)(pb + e) * stride];
         }
       }
 #pragma unroll
@@ -919,8 +920,8 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_csc_gather(int64_t n_unit
         for (int u = 0; u < GU; ++u) {
           const int e = q + u * NGRP + grp;
           const bool ok = e < cnt;
-          v[u] = ok ? val[p0 + e] : 0.f;
-          const uint32_t off = ok ? (uint32_t)tok[p0 + e] * row_b + col_b : 0x80000000u;
+          v[u] = ok ? val[(int64_t)(p0 + e) * stride] : 0.f;
+          const uint32_t off = ok ? (uint32_t)tok[(int64_t)(p0 + e) * stride] * row_b + col_b : 0x80000000u;
           w[u] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(gr, (int)off, 0, 0));
         }
 #pragma unroll
@@ -1091,7 +1092,8 @@ hipError_t launch_gather_down_packed(int64_t T, int64_t d, int64_t f, int K, con
 
 hipError_t launch_csc_gather(int64_t n_units, int64_t d, int64_t R, const int32_t* ptr, const int32_t* tok,
                              const float* val, int64_t mean_bound, const void* Gp, float* out, hipStream_t s,
-                             const int32_t* out_rows) {
+                             const int32_t* out_rows, int stride) {
+  if (stride < 1) return hipErrorInvalidValue;
   if (n_units == 0) return hipSuccess;
   if (d % (8 * SLICE2) != 0) return hipErrorInvalidValue;
   // units per block: lists of mean_bound entries (an upper bound of the mean list length)
@@ -1122,10 +1124,10 @@ hipError_t launch_csc_gather(int64_t n_units, int64_t d, int64_t R, const int32_
   }
   const dim3 grid((unsigned)(8 * blocks)), block(GATHER_WAVES * 64);
   if (groups)
-    hipLaunchKernelGGL(k_csc_gather<true>, grid, block, lds, s, n_units, d, R, ptr, tok, val,
+    hipLaunchKernelGGL(k_csc_gather<true>, grid, block, lds, s, n_units, d, R, ptr, tok, val, stride,
                        (const bf16_t*)Gp, out, (int)(d / SLICE2), upw, stage_pairs, out_rows);
   else
-    hipLaunchKernelGGL(k_csc_gather<false>, grid, block, lds, s, n_units, d, R, ptr, tok, val,
+    hipLaunchKernelGGL(k_csc_gather<false>, grid, block, lds, s, n_units, d, R, ptr, tok, val, stride,
                        (const bf16_t*)Gp, out, (int)(d / SLICE2), upw, stage_pairs, out_rows);
   return hipGetLastError();
 }

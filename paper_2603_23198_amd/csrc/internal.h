@@ -236,12 +236,14 @@ hipError_t launch_pack_down(const void* W, void* out, int64_t f, int64_t d, hipS
 hipError_t launch_gated_updot(int64_t T, int64_t d, int64_t f, int K, const uint16_t* ell_idx, const int32_t* row_nnz,
                               const uint8_t* row_ovf, const void* X, const void* WuP, float* part_u, hipStream_t s,
                               const int32_t* order = nullptr);
-// Backward per-unit gathers: out[r][:] = sum_e val[e] G[tok[e]][:] over list k's entries
-// [ptr[k], ptr[k+1]), r = out_rows[k] (or k when null), G slice-major [d/64][R][64] bf16,
-// out fp32 [n_units][d]; mean_bound bounds the mean list length (sizes the blocks).
+// Backward per-unit gathers: out[r][:] = sum_e val[e stride] G[tok[e stride]][:] over list
+// k's entries e in [ptr[k], ptr[k+1]), r = out_rows[k] (or k when null), G slice-major
+// [d/64][R][64] bf16, out fp32 [n_units][d]; stride: the entries' spacing in 4-byte words
+// (records of a token and several values); mean_bound bounds the mean list length (sizes
+// the blocks).
 hipError_t launch_csc_gather(int64_t n_units, int64_t d, int64_t R, const int32_t* ptr, const int32_t* tok,
                              const float* val, int64_t mean_bound, const void* Gp, float* out, hipStream_t s,
-                             const int32_t* out_rows = nullptr);
+                             const int32_t* out_rows = nullptr, int stride = 1);
 // out[t][e] = sum of the 8 partials [8][T][K] + add on the sparse rows' entries (fp32).
 hipError_t launch_sum_parts(int64_t T, int K, const int32_t* row_nnz, const uint8_t* row_ovf, const float* part,
                             float add, float* out, hipStream_t s);
