@@ -607,7 +607,7 @@ __host__ __device__ inline int updot_copies(int tpw, int nsl) { return tpw < GAT
 // takes entry q + u * NGRP + g; each lane dots its 8 columns (bf16 dot2), the group sums
 // its 8 lanes, lane 0 of the group adds that to the entry's LDS sum. A token is always
 // handled by the same wave, so each entry's sum is updated in slice order.
-template <int U>
+template <int U, bool XS>
 __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gated_updot(
     int64_t T, int64_t d, int64_t f, int K, const uint16_t* __restrict__ ell_idx, const int32_t* __restrict__ row_nnz,
     const uint8_t* __restrict__ row_ovf, const bf16_t* __restrict__ X, const bf16_t* __restrict__ WuP,
@@ -630,12 +630,35 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gated_updot(
     return q < T ? (order ? (int64_t)order[q] : q) : T;
   };
   int* tok_s = cnt_s + tpw;
+  // with XS, the block's activation segments of all the XCD's slices, [tpw][nsl][64]
+  // bf16 after the token rows: read from memory once at the start (each is used once per
+  // XCD, so they always come from HBM), with the entries, not one at a time per item
+  bf16_t* xs = (bf16_t*)(((uintptr_t)(tok_s + tpw) + 15) & ~(uintptr_t)15);
   for (int i = threadIdx.x; i < tpw; i += blockDim.x) {
     const int64_t t = tok(i);
     cnt_s[i] = (t < T && !row_ovf[t]) ? row_nnz[t] : -1;
     tok_s[i] = (int)t;
   }
   __syncthreads();
+  constexpr int XU = 4;  // 16-byte chunks per thread and pass
+  const int nxc = XS ? tpw * nsl * 8 : 0;
+  u32x4_t xc[XU];
+  if constexpr (XS)
+  for (int q0 = threadIdx.x; q0 < nxc; q0 += (int)blockDim.x * XU) {
+    // a chunk past the end, or of a skipped token, re-reads row 0's and is not stored
+#pragma unroll
+    for (int u = 0; u < XU; ++u) {
+      const int q = min(q0 + u * (int)blockDim.x, nxc - 1);
+      const int i = q / (nsl * 8), r = q % (nsl * 8);
+      const int64_t t = cnt_s[i] > 0 ? tok_s[i] : 0;
+      xc[u] = *(const u32x4_t*)(X + t * d + (int64_t)(xcd + 8 * (r >> 3)) * SLICE2 + (r & 7) * 8);
+    }
+#pragma unroll
+    for (int u = 0; u < XU; ++u) {
+      const int q = q0 + u * (int)blockDim.x;
+      if (q < nxc) *(u32x4_t*)(xs + (size_t)q * 8) = xc[u];
+    }
+  }
   // rows of whole 8-entry chunks, 16-byte aligned: the chunks are dealt over all threads,
   // four loads in flight per thread (one round of latency, as in the token-group gather)
   const bool flat = K % 8 == 0 && (((uintptr_t)ell_idx) & 15) == 0;
@@ -690,7 +713,9 @@ __global__ __launch_bounds__(GATHER_WAVES * 64) void k_gated_updot(
     const int nnz = __builtin_amdgcn_readfirstlane(cnt_s[i]);
     if (nnz <= 0) return;
     // this lane's 8 columns of x[t] in the slice, as bf16 pairs
-    const u32x4_t xv = *(const u32x4_t*)(X + tok(i) * d + (int64_t)slice * SLICE2 + sub * 8);
+    u32x4_t xv;
+    if constexpr (XS) xv = *(const u32x4_t*)(xs + ((size_t)i * nsl + sl) * SLICE2 + sub * 8);
+    else xv = *(const u32x4_t*)(X + tok(i) * d + (int64_t)slice * SLICE2 + sub * 8);
     const uint32_t* er = ent + i * K;
     for (int q = 0; q < nnz; q += NGRP * U) {
       u32x4_t w[U];
@@ -1170,22 +1195,37 @@ hipError_t launch_gated_updot(int64_t T, int64_t d, int64_t f, int K, const uint
   const int tpw = slice_walk_tpw(T, per_tok);
   const int64_t blocks = cdiv(T, tpw);
   const int nsl_max = (int)cdiv(d / SLICE2, 8);
-  const size_t lds = (size_t)tpw * per_tok + (size_t)(updot_copies(tpw, nsl_max) - 1) * tpw * std::max(K, 1) * 4;
+  size_t lds = (size_t)tpw * per_tok + (size_t)(updot_copies(tpw, nsl_max) - 1) * tpw * std::max(K, 1) * 4;
   if (lds > 160 * 1024) return hipErrorInvalidValue;
-  const bool short_rows = use_short_unroll(K, (int64_t)lds);
-  const void* kern = short_rows ? (const void*)k_gated_updot<GU_SHORT> : (const void*)k_gated_updot<GU>;
-  if (lds > 65536) {
-    const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
+  // the activation segments staged too where that costs no workgroup per CU (read one item
+  // at a time, the dz up-dot at the training shape spent about 0.19 of its 1.27 ms waiting
+  // on them; with one workgroup per CU instead of two or three the gated blocks were 10 %
+  // slower), and not for decode-sized blocks (the loads then add a round before the walk)
+  const size_t xbytes = (size_t)tpw * nsl_max * SLICE2 * 2 + 16;
+  const size_t lds_cu = 160 * 1024;
+  const int xstage =
+      updot_copies(tpw, nsl_max) == 1 && lds + xbytes <= lds_cu && lds_cu / (lds + xbytes) >= lds_cu / lds ? 1 : 0;
+  const bool short_rows = use_short_unroll(K, (int64_t)lds);  // on the entries' share, as before
+  if (xstage) lds += xbytes;
+#define SFL_UPDOT(U_, XS_)                                                                                         \
+  do {                                                                                                           \
+    if (lds > 65536) {                                                                                           \
+      const hipError_t e = hipFuncSetAttribute((const void*)k_gated_updot<U_, XS_>,                              \
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);            \
+      if (e != hipSuccess) return e;                                                                             \
+    }                                                                                                            \
+    hipLaunchKernelGGL((k_gated_updot<U_, XS_>), dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), lds, s, T, \
+                       d, f, K, ell_idx, row_nnz, row_ovf, (const bf16_t*)X, (const bf16_t*)WuP, part_u,          \
+                       (int)(d / SLICE2), tpw, order);                                                            \
+  } while (0)
+  if (short_rows) {
+    if (xstage) SFL_UPDOT(GU_SHORT, true);
+    else SFL_UPDOT(GU_SHORT, false);
+  } else {
+    if (xstage) SFL_UPDOT(GU, true);
+    else SFL_UPDOT(GU, false);
   }
-  if (short_rows)
-    hipLaunchKernelGGL(k_gated_updot<GU_SHORT>, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), lds, s, T, d, f,
-                       K, ell_idx, row_nnz, row_ovf, (const bf16_t*)X, (const bf16_t*)WuP, part_u, (int)(d / SLICE2),
-                       tpw, order);
-  else
-    hipLaunchKernelGGL(k_gated_updot<GU>, dim3((unsigned)(8 * blocks)), dim3(GATHER_WAVES * 64), lds, s, T, d, f, K,
-                       ell_idx, row_nnz, row_ovf, (const bf16_t*)X, (const bf16_t*)WuP, part_u, (int)(d / SLICE2), tpw,
-                       order);
+#undef SFL_UPDOT
   return hipGetLastError();
 }
 
