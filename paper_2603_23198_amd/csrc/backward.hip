@@ -102,27 +102,38 @@ __global__ __launch_bounds__(256) void k_blk_scan(int64_t nb, int64_t f, int32_t
 __global__ __launch_bounds__(1024) void k_col_ptr(int64_t f, const int32_t* __restrict__ col_cnt,
                                                   const int32_t* __restrict__ uorder, int32_t* __restrict__ col_ptr,
                                                   int32_t* __restrict__ colstart) {
+  // a pass covers kColPer x 1024 positions, position r0 + j 1024 + tid for thread tid: the
+  // units, then their counts, of all of them are loaded together (coalesced; positions past
+  // f re-read the last one and count 0), then the kColPer block scans run from registers
+  constexpr int kColPer = 16;
   __shared__ int wsum[16];
   const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
   int base = 0;
-  for (int64_t r0 = 0; r0 < f; r0 += 1024) {
-    const int64_t k = r0 + tid;
-    const int64_t n = k < f ? uorder[k] : 0;
-    const int c = k < f ? col_cnt[n] : 0;
-    const int incl = wave_incl_scan(c);
-    if (l == 63) wsum[w] = incl;
-    __syncthreads();
-    int before = 0, all = 0;
-    for (int i = 0; i < 16; ++i) {
-      before += (i < w) ? wsum[i] : 0;
-      all += wsum[i];
+  for (int64_t r0 = 0; r0 < f; r0 += 1024 * kColPer) {
+    int n[kColPer], c[kColPer];
+#pragma unroll
+    for (int j = 0; j < kColPer; ++j) n[j] = uorder[min(r0 + j * 1024 + tid, f - 1)];
+#pragma unroll
+    for (int j = 0; j < kColPer; ++j) c[j] = col_cnt[n[j]];
+#pragma unroll
+    for (int j = 0; j < kColPer; ++j) {
+      const int64_t k = r0 + j * 1024 + tid;
+      const int cj = k < f ? c[j] : 0;
+      const int incl = wave_incl_scan(cj);
+      if (l == 63) wsum[w] = incl;
+      __syncthreads();
+      int before = 0, all = 0;
+      for (int i = 0; i < 16; ++i) {
+        before += (i < w) ? wsum[i] : 0;
+        all += wsum[i];
+      }
+      if (k < f) {
+        col_ptr[k] = base + before + incl - cj;
+        colstart[n[j]] = base + before + incl - cj;
+      }
+      base += all;
+      __syncthreads();
     }
-    if (k < f) {
-      col_ptr[k] = base + before + incl - c;
-      colstart[n] = base + before + incl - c;
-    }
-    base += all;
-    __syncthreads();
   }
   if (tid == 0) col_ptr[f] = base;
 }
