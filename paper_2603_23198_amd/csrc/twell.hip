@@ -333,7 +333,7 @@ __global__ __launch_bounds__(256) void k_classify_wide(int64_t T, int NT, int S,
 // several rows per wave amortise the per-block statistics, but the walk is latency bound:
 // keep about 4096 waves (16 per CU) in flight before packing rows
 int classify_rows_per_wave(int64_t T) {
-  return (int)std::max<int64_t>(1, std::min<int64_t>(kClassifyRowsPerWave, T / 4096));
+  return (int)std::max<int64_t>(1, std::min<int64_t>(kClassifyRowsPerWave, T / 8192));
 }
 int64_t classify_grid(int64_t T, int64_t f, int Tn) {
   const int NT = (int)cdiv(f, Tn);

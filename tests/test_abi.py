@@ -83,7 +83,7 @@ def _need_lists(cap):
 
 def _cls_parts(T, f, Tn=256):
     # the classification's per-block statistics, 16 bytes a block, summed by the list kernel
-    rpw = max(1, min(8, T // 4096))
+    rpw = max(1, min(8, T // 8192))
     grid = -(-T // 4) if -(-f // Tn) > 512 else -(-T // (16 * rpw))
     return _al(16 * grid)
 
