@@ -875,7 +875,21 @@ __global__ __launch_bounds__(1024) void k_dense_decision(int64_t T, int64_t f, i
                                                          int32_t* __restrict__ flags) {
   __shared__ long long part[16];
   long long sum = 0;
-  for (int64_t t = threadIdx.x; t < T; t += 1024) sum += row_ovf[t] ? 0 : row_nnz[t];
+  // eight rows per thread and pass, their counts and flags loaded together (a row past the
+  // batch re-reads row T - 1 and adds nothing)
+  constexpr int P = 8;
+  for (int64_t t0 = threadIdx.x; t0 < T; t0 += 1024 * P) {
+    int nz[P];
+    uint8_t ov[P];
+#pragma unroll
+    for (int u = 0; u < P; ++u) {
+      const int64_t t = min(t0 + 1024 * u, T - 1);
+      nz[u] = row_nnz[t];
+      ov[u] = row_ovf[t];
+    }
+#pragma unroll
+    for (int u = 0; u < P; ++u) sum += (t0 + 1024 * u < T && !ov[u]) ? nz[u] : 0;
+  }
   sum = wave_sum<long long>(sum);
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = sum;
   __syncthreads();
