@@ -637,17 +637,20 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
     SFL_HIP(launch_classify(T, f, vb, a->cfg.tile_cols, a->cfg.tile_slots, a->cfg.ell_width, tw.val, tw.idx,
                             tw.cnt, tw.row_nnz, tw.row_ovf, tw.ell_val, tw.ell_idx, a->stats, s, l1_vals,
                             packed_layout(a->cfg), cls_part));
-  // the dense-backup row list: up to 64 rows the gather's first block builds it (nothing
-  // before the dense-backup stage reads it), else its own kernel
+  // the dense-backup row list (nothing before the dense-backup stage reads it): up to 64
+  // rows the gather's first block builds it, with the token order a second workgroup of
+  // the order kernel, else its own kernel
   OvfList late_list;
-  if (list_by_gather(*a)) {
+  const bool list_by_order = !list_by_gather(*a) && packed_gather(*a) && nnz_token_order(*a);
+  const int n_cls_part = cls_part ? (int)classify_grid(T, f, a->cfg.tile_cols) : 0;
+  if (list_by_gather(*a) || list_by_order) {
     late_list.rows = tw.ovf_rows;
     late_list.n = tw.n_ovf;
     late_list.cap = (int32_t)cap;
     late_list.stats = a->stats;
   } else {
     SFL_HIP(launch_ovf_list(T, (int32_t)cap, tw.row_ovf, tw.ovf_rows, tw.n_ovf, a->stats, s, cls_part,
-                            cls_part ? (int)classify_grid(T, f, a->cfg.tile_cols) : 0));
+                            n_cls_part));
   }
   ev.record(2, s);
   if (plan.H) {
@@ -675,7 +678,9 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
   if (packed_gather(*a)) {
     const int32_t* order = nullptr;
     if (nnz_token_order(*a)) {
-      SFL_HIP(launch_nnz_order(T, a->cfg.ell_width, tw.row_nnz, tw.row_ovf, plan.order, s));
+      // with a second workgroup building the dense-backup row list
+      SFL_HIP(launch_nnz_order(T, a->cfg.ell_width, tw.row_nnz, tw.row_ovf, plan.order, s,
+                               list_by_order ? &late_list : nullptr, cls_part, n_cls_part));
       order = plan.order;
     }
     const void* WdP = a->W_down_packed;
@@ -713,7 +718,8 @@ sfl_status_t forward_run(const sfl_ffn_args_t* a, void* ws, size_t ws_bytes, hip
     const bool form_h = a->gated && T <= kGatherFormsH;
     SFL_HIP(launch_gather_down_packed(T, d, f, a->cfg.ell_width, hv, tw.ell_idx, tw.row_nnz, tw.row_ovf, WdP, a->Y,
                                       s, 0, 0, nullptr, order, plan.dense_flags ? plan.dense_flags + 1 : nullptr,
-                                      form_h ? plan.part_u : nullptr, form_h ? a->stats : nullptr, late_list));
+                                      form_h ? plan.part_u : nullptr, form_h ? a->stats : nullptr,
+                                      list_by_order ? OvfList{} : late_list));
   } else {
     SFL_HIP(launch_gather_down(vb, T, d, a->cfg.ell_width, tw.ell_val, tw.ell_idx, tw.row_nnz, tw.row_ovf,
                                a->W_down, a->Y, s));

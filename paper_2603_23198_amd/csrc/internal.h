@@ -169,13 +169,6 @@ hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32
                            int n_parts = 0);
 // Zeroes the statistics (if given) and n_zero counters from zero.
 hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s, int32_t* zero = nullptr, int n_zero = 0);
-// order[0 .. T): the sparse rows by descending row_nnz, then the dense-backup rows (one
-// workgroup, counting sort over K + 2 buckets; order within a bucket unspecified; with
-// row_ovf null every row counts as sparse and counts above K share the first bucket).
-// Fails with hipErrorInvalidValue when K + 2 buckets do not fit the kernel's LDS histogram.
-bool nnz_order_supported(int K);
-hipError_t launch_nnz_order(int64_t T, int K, const int32_t* row_nnz, const uint8_t* row_ovf, int32_t* order,
-                            hipStream_t s);
 // Dense-backup rows whose tiles kept every value, rebuilt from the TwELL slabs; the others
 // are listed (need_rows: token rows, need_slots: their ovf_dense rows, *n_need: their number,
 // which must be zero before the call; list order unspecified) for the GEMM. With l1_part
@@ -210,6 +203,17 @@ struct OvfList {
   int32_t cap = 0;
   sfl_stats_t* stats = nullptr;
 };
+// order[0 .. T): the sparse rows by descending row_nnz, then the dense-backup rows (one
+// workgroup, counting sort over K + 2 buckets; order within a bucket unspecified; with
+// row_ovf null every row counts as sparse and counts above K share the first bucket).
+// Given list (row_ovf then required), a second workgroup of the same launch writes the
+// dense-backup row list as launch_ovf_list does (with the classification's n_parts
+// per-block statistics at parts, if given).
+// Fails with hipErrorInvalidValue when K + 2 buckets do not fit the kernel's LDS histogram.
+bool nnz_order_supported(int K);
+hipError_t launch_nnz_order(int64_t T, int K, const int32_t* row_nnz, const uint8_t* row_ovf, int32_t* order,
+                            hipStream_t s, const OvfList* list = nullptr, const ClassifyPart* parts = nullptr,
+                            int n_parts = 0);
 // bf16, d % 512 == 0: same sum from the slice-major copy of W_down (persistent, XCD-aware).
 // out_mode 0: bf16 Y; 1: fp32 Yf; 2: bf16 Y of (sum + Yf) (val_f32 only for 1 and 2).
 // With ol.rows (at most 64 rows): block 0 also builds the dense-backup row list from row_ovf

@@ -625,98 +625,15 @@ hipError_t launch_stats_init(sfl_stats_t* stats, hipStream_t s, int32_t* zero, i
   return hipGetLastError();
 }
 
-// Processing order of the tokens for the sparse down projection: the sparse rows by
-// descending row count, then the dense-backup rows (which the gathers skip; row_ovf may
-// be null: no such rows, and counts above K share the first bucket). A counting
-// sort in one workgroup: bucket K - n for a sparse row of n entries (n <= K), bucket K + 1
-// for a dense-backup row; histogram in LDS, exclusive scan over the buckets, then each
-// token placed at its bucket's cursor (LDS atomics, so the order within a bucket varies;
-// the gathers' results do not depend on it).
-constexpr int kOrderMaxBuckets = 16384;
-constexpr int kOrderPer = 8;  // tokens per thread and pass of k_nnz_order
-bool nnz_order_supported(int K) { return K >= 0 && K + 2 <= kOrderMaxBuckets; }
-
-__global__ __launch_bounds__(1024) void k_nnz_order(int64_t T, int K, const int32_t* __restrict__ row_nnz,
-                                                    const uint8_t* __restrict__ row_ovf, int32_t* __restrict__ order) {
-  __shared__ int hist[kOrderMaxBuckets];
-  __shared__ int wsum[16];
-  const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
-  const int nb = K + 2;
-  for (int i = tid; i < nb; i += 1024) hist[i] = 0;
-  __syncthreads();
-  // passes of kOrderPer tokens per thread, their counts (and flags) loaded together, with
-  // no load under a condition (a token past the batch reads token T - 1 and counts
-  // nothing); a single pass keeps the buckets for the placement below
-  int bk[kOrderPer];
-  auto buckets = [&](int64_t t0) {
-    int nz[kOrderPer];
-    if (row_ovf) {
-      uint8_t ov[kOrderPer];
-#pragma unroll
-      for (int u = 0; u < kOrderPer; ++u) {
-        const int64_t t = min(t0 + 1024 * u, T - 1);
-        nz[u] = row_nnz[t];
-        ov[u] = row_ovf[t];
-      }
-#pragma unroll
-      for (int u = 0; u < kOrderPer; ++u) bk[u] = ov[u] ? K + 1 : K - min(max(nz[u], 0), K);
-    } else {
-#pragma unroll
-      for (int u = 0; u < kOrderPer; ++u) nz[u] = row_nnz[min(t0 + 1024 * u, T - 1)];
-#pragma unroll
-      for (int u = 0; u < kOrderPer; ++u) bk[u] = K - min(max(nz[u], 0), K);
-    }
-  };
-  for (int64_t t0 = tid; t0 < T; t0 += 1024 * kOrderPer) {
-    buckets(t0);
-#pragma unroll
-    for (int u = 0; u < kOrderPer; ++u)
-      if (t0 + 1024 * u < T) atomicAdd(&hist[bk[u]], 1);
-  }
-  __syncthreads();
-  // exclusive scan: thread j owns buckets [j per, (j + 1) per)
-  const int per = (nb + 1023) / 1024;
-  const int b0 = min(nb, tid * per), b1 = min(nb, b0 + per);
-  int local = 0;
-  for (int b = b0; b < b1; ++b) local += hist[b];
-  const int incl = wave_incl_scan(local);
-  if (l == 63) wsum[w] = incl;
-  __syncthreads();
-  int before = 0;
-  for (int i = 0; i < w; ++i) before += wsum[i];
-  int run = before + incl - local;
-  for (int b = b0; b < b1; ++b) {
-    const int c = hist[b];
-    hist[b] = run;
-    run += c;
-  }
-  __syncthreads();
-  const bool one_pass = T <= 1024 * kOrderPer;
-  for (int64_t t0 = tid; t0 < T; t0 += 1024 * kOrderPer) {
-    if (!one_pass) buckets(t0);
-#pragma unroll
-    for (int u = 0; u < kOrderPer; ++u)
-      if (t0 + 1024 * u < T) order[atomicAdd(&hist[bk[u]], 1)] = (int32_t)(t0 + 1024 * u);
-  }
-}
-
-hipError_t launch_nnz_order(int64_t T, int K, const int32_t* row_nnz, const uint8_t* row_ovf, int32_t* order,
-                            hipStream_t s) {
-  if (T == 0) return hipSuccess;
-  if (!nnz_order_supported(K) || T > INT32_MAX) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_nnz_order, dim3(1), dim3(1024), 0, s, T, K, row_nnz, row_ovf, order);
-  return hipGetLastError();
-}
-
 // One workgroup of 1024 threads; each pass covers 1024 x 16 rows, thread i taking 16
 // consecutive rows (their flags loaded together), so a pass costs one round of loads.
 // An exclusive scan of the threads' counts (wave scans + a scan of the 16 wave totals)
 // places each thread's rows, in ascending row order.
 constexpr int kOvfRowsPerThread = 16;
-__global__ __launch_bounds__(1024) void k_ovf_list(int64_t T, int32_t cap, const uint8_t* __restrict__ row_ovf,
-                                                   int32_t* __restrict__ ovf_rows, int32_t* __restrict__ n_ovf,
-                                                   sfl_stats_t* __restrict__ stats,
-                                                   const ClassifyPart* __restrict__ parts, int n_parts) {
+__device__ __forceinline__ void ovf_list_block(int64_t T, int32_t cap, const uint8_t* __restrict__ row_ovf,
+                                               int32_t* __restrict__ ovf_rows, int32_t* __restrict__ n_ovf,
+                                               sfl_stats_t* __restrict__ stats,
+                                               const ClassifyPart* __restrict__ parts, int n_parts) {
   __shared__ int wsum[16];
   const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
   if (parts && stats) {
@@ -792,10 +709,111 @@ __global__ __launch_bounds__(1024) void k_ovf_list(int64_t T, int32_t cap, const
   }
 }
 
+__global__ __launch_bounds__(1024) void k_ovf_list(int64_t T, int32_t cap, const uint8_t* __restrict__ row_ovf,
+                                                   int32_t* __restrict__ ovf_rows, int32_t* __restrict__ n_ovf,
+                                                   sfl_stats_t* __restrict__ stats,
+                                                   const ClassifyPart* __restrict__ parts, int n_parts) {
+  ovf_list_block(T, cap, row_ovf, ovf_rows, n_ovf, stats, parts, n_parts);
+}
+
 hipError_t launch_ovf_list(int64_t T, int32_t cap, const uint8_t* row_ovf, int32_t* ovf_rows, int32_t* n_ovf,
                            sfl_stats_t* stats, hipStream_t s, const ClassifyPart* parts, int n_parts) {
   hipLaunchKernelGGL(k_ovf_list, dim3(1), dim3(1024), 0, s, T, cap, row_ovf, ovf_rows, n_ovf, stats, parts,
                      n_parts);
+  return hipGetLastError();
+}
+
+// Processing order of the tokens for the sparse down projection: the sparse rows by
+// descending row count, then the dense-backup rows (which the gathers skip; row_ovf may
+// be null: no such rows, and counts above K share the first bucket). A counting
+// sort in one workgroup: bucket K - n for a sparse row of n entries (n <= K), bucket K + 1
+// for a dense-backup row; histogram in LDS, exclusive scan over the buckets, then each
+// token placed at its bucket's cursor (LDS atomics, so the order within a bucket varies;
+// the gathers' results do not depend on it). Given the dense-backup list's outputs, a
+// second workgroup builds that list (as k_ovf_list) beside the first, in the same launch.
+constexpr int kOrderMaxBuckets = 16384;
+constexpr int kOrderPer = 8;  // tokens per thread and pass of k_nnz_order
+bool nnz_order_supported(int K) { return K >= 0 && K + 2 <= kOrderMaxBuckets; }
+
+__global__ __launch_bounds__(1024) void k_nnz_order(int64_t T, int K, const int32_t* __restrict__ row_nnz,
+                                                    const uint8_t* __restrict__ row_ovf, int32_t* __restrict__ order,
+                                                    int32_t cap, int32_t* __restrict__ ovf_rows,
+                                                    int32_t* __restrict__ n_ovf, sfl_stats_t* __restrict__ stats,
+                                                    const ClassifyPart* __restrict__ parts, int n_parts) {
+  if (blockIdx.x == 1) {
+    ovf_list_block(T, cap, row_ovf, ovf_rows, n_ovf, stats, parts, n_parts);
+    return;
+  }
+  __shared__ int hist[kOrderMaxBuckets];
+  __shared__ int wsum[16];
+  const int tid = threadIdx.x, l = tid & 63, w = tid >> 6;
+  const int nb = K + 2;
+  for (int i = tid; i < nb; i += 1024) hist[i] = 0;
+  __syncthreads();
+  // passes of kOrderPer tokens per thread, their counts (and flags) loaded together, with
+  // no load under a condition (a token past the batch reads token T - 1 and counts
+  // nothing); a single pass keeps the buckets for the placement below
+  int bk[kOrderPer];
+  auto buckets = [&](int64_t t0) {
+    int nz[kOrderPer];
+    if (row_ovf) {
+      uint8_t ov[kOrderPer];
+#pragma unroll
+      for (int u = 0; u < kOrderPer; ++u) {
+        const int64_t t = min(t0 + 1024 * u, T - 1);
+        nz[u] = row_nnz[t];
+        ov[u] = row_ovf[t];
+      }
+#pragma unroll
+      for (int u = 0; u < kOrderPer; ++u) bk[u] = ov[u] ? K + 1 : K - min(max(nz[u], 0), K);
+    } else {
+#pragma unroll
+      for (int u = 0; u < kOrderPer; ++u) nz[u] = row_nnz[min(t0 + 1024 * u, T - 1)];
+#pragma unroll
+      for (int u = 0; u < kOrderPer; ++u) bk[u] = K - min(max(nz[u], 0), K);
+    }
+  };
+  for (int64_t t0 = tid; t0 < T; t0 += 1024 * kOrderPer) {
+    buckets(t0);
+#pragma unroll
+    for (int u = 0; u < kOrderPer; ++u)
+      if (t0 + 1024 * u < T) atomicAdd(&hist[bk[u]], 1);
+  }
+  __syncthreads();
+  // exclusive scan: thread j owns buckets [j per, (j + 1) per)
+  const int per = (nb + 1023) / 1024;
+  const int b0 = min(nb, tid * per), b1 = min(nb, b0 + per);
+  int local = 0;
+  for (int b = b0; b < b1; ++b) local += hist[b];
+  const int incl = wave_incl_scan(local);
+  if (l == 63) wsum[w] = incl;
+  __syncthreads();
+  int before = 0;
+  for (int i = 0; i < w; ++i) before += wsum[i];
+  int run = before + incl - local;
+  for (int b = b0; b < b1; ++b) {
+    const int c = hist[b];
+    hist[b] = run;
+    run += c;
+  }
+  __syncthreads();
+  const bool one_pass = T <= 1024 * kOrderPer;
+  for (int64_t t0 = tid; t0 < T; t0 += 1024 * kOrderPer) {
+    if (!one_pass) buckets(t0);
+#pragma unroll
+    for (int u = 0; u < kOrderPer; ++u)
+      if (t0 + 1024 * u < T) order[atomicAdd(&hist[bk[u]], 1)] = (int32_t)(t0 + 1024 * u);
+  }
+}
+
+hipError_t launch_nnz_order(int64_t T, int K, const int32_t* row_nnz, const uint8_t* row_ovf, int32_t* order,
+                            hipStream_t s, const OvfList* list, const ClassifyPart* parts, int n_parts) {
+  if (T == 0) return hipSuccess;
+  if (!nnz_order_supported(K) || T > INT32_MAX) return hipErrorInvalidValue;
+  if (list && (!list->rows || !list->n || !row_ovf)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_nnz_order, dim3(list ? 2 : 1), dim3(1024), 0, s, T, K, row_nnz, row_ovf, order,
+                     list ? list->cap : 0, list ? list->rows : nullptr, list ? list->n : nullptr,
+                     list ? list->stats : nullptr, list ? parts : nullptr, list ? n_parts : 0);
   return hipGetLastError();
 }
 
