@@ -425,8 +425,10 @@ sfl_status_t sfl_track_active_units(const sfl_twell_t* tw, int64_t T, int64_t f,
  * the units are its columns (W_gate or W_up [d][f]), 1 when they are its rows (a
  * transposed copy [f][d]). noise: device float32 array of W's shape holding standard
  * normal draws from the caller's generator. Computed in fp32 (one multiply, one fused
- * multiply-add), bf16 results rounded to nearest even. Errors: SFL_E_ARG for NULL
- * pointers (non-empty W), lam outside [0, 1], sigma < 0 or units_on_rows not 0/1. */
+ * multiply-add), bf16 results rounded to nearest even. A live unit costs one read of
+ * its record. Errors: SFL_E_ARG for NULL pointers (non-empty W), lam outside [0, 1],
+ * sigma < 0 or units_on_rows not 0/1; SFL_E_UNSUPPORTED for more than 2^31 - 1 rows
+ * (units on rows) or more than 65535 x 64 rows (units on columns). */
 sfl_status_t sfl_reinit_dead_units(void* W, sfl_dtype_t dtype, int64_t rows, int64_t cols, int32_t units_on_rows,
                                    const int64_t* last_active, int64_t step, float lam, float sigma,
                                    const float* noise, sfl_stream_t stream);

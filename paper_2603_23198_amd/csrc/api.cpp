@@ -929,6 +929,7 @@ sfl_status_t sfl_reinit_dead_units(void* W, sfl_dtype_t dtype, int64_t rows, int
   if (!(lam >= 0.f && lam <= 1.f) || !(sigma >= 0.f)) return SFL_E_ARG;
   if (rows * cols == 0) return SFL_OK;
   if (!W || !last_active || !noise) return SFL_E_ARG;
+  if (!reinit_supported(rows, cols, units_on_rows)) return SFL_E_UNSUPPORTED;
   SFL_HIP(launch_reinit_units(W, dtype == SFL_BF16, rows, cols, units_on_rows, last_active, step, lam, sigma, noise,
                               (hipStream_t)stream));
   return SFL_OK;

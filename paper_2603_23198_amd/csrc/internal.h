@@ -275,6 +275,9 @@ hipError_t launch_track_units(int64_t T, int64_t f, int n_tiles, int S, const in
                               int64_t* last, hipStream_t s);
 // W [rows][cols] (bf16 or fp32): for unit u (row or column) with last[u] < step,
 // w <- (1 - lam) w + lam sigma noise, noise fp32 of W's shape.
+// Shapes the re-initialisation's grid covers (units on rows: at most 2^31 - 1 rows; on
+// columns: at most 65535 chunks of 64 rows).
+bool reinit_supported(int64_t rows, int64_t cols, int units_on_rows);
 hipError_t launch_reinit_units(void* W, int val_bf16, int64_t rows, int64_t cols, int units_on_rows,
                                const int64_t* last, int64_t step, float lam, float sigma, const float* noise,
                                hipStream_t s);

@@ -48,18 +48,42 @@ __device__ __forceinline__ void store_w(float* W, int64_t i, float v) { W[i] = v
 __device__ __forceinline__ void store_w(bf16_t* W, int64_t i, float v) { W[i] = f32_to_bf16(v); }
 
 // W [rows][cols]; unit u = units_on_rows ? r : c. Dead units: w = a w + b z (fp32 FMA,
-// then the storage rounding), with a = 1 - lam and b = lam sigma.
+// then the storage rounding), with a = 1 - lam and b = lam sigma. A thread reads its
+// unit's record once and a live unit's thread does nothing more, so a step with few dead
+// units costs little more than the launch. Units on columns: thread = column (a wave's
+// columns are consecutive, so its row accesses coalesce), block y = a chunk of
+// kReinitRows rows. Units on rows: block = one row (the unit), threads over its columns.
+constexpr int kReinitRows = 64;
 template <typename V>
-__global__ __launch_bounds__(256) void k_reinit(V* __restrict__ W, int64_t rows, int64_t cols, int units_on_rows,
-                                                const int64_t* __restrict__ last, int64_t step, float a, float b,
-                                                const float* __restrict__ noise) {
-  const int64_t total = rows * cols;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
-    const int64_t u = units_on_rows ? i / cols : i % cols;
-    if (last[u] < step) store_w(W, i, fmaf(b, noise[i], a * load_w(W, i)));
+__global__ __launch_bounds__(256) void k_reinit_cols(V* __restrict__ W, int64_t rows, int64_t cols,
+                                                     const int64_t* __restrict__ last, int64_t step, float a, float b,
+                                                     const float* __restrict__ noise) {
+  const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (c >= cols || last[c] >= step) return;
+  const int64_t r1 = min((int64_t)(blockIdx.y + 1) * kReinitRows, rows);
+  for (int64_t r = (int64_t)blockIdx.y * kReinitRows; r < r1; ++r) {
+    const int64_t i = r * cols + c;
+    store_w(W, i, fmaf(b, noise[i], a * load_w(W, i)));
+  }
+}
+template <typename V>
+__global__ __launch_bounds__(256) void k_reinit_rows(V* __restrict__ W, int64_t cols, const int64_t* __restrict__ last,
+                                                     int64_t step, float a, float b, const float* __restrict__ noise) {
+  const int64_t r = blockIdx.x;
+  if (last[r] >= step) return;  // uniform over the block
+  for (int64_t c = threadIdx.x; c < cols; c += 256) {
+    const int64_t i = r * cols + c;
+    store_w(W, i, fmaf(b, noise[i], a * load_w(W, i)));
   }
 }
 
+}  // namespace
+
+bool reinit_supported(int64_t rows, int64_t cols, int units_on_rows) {
+  return units_on_rows ? rows <= INT32_MAX : cdiv(rows, kReinitRows) <= 65535 && cdiv(cols, 256) <= INT32_MAX;
+}
+
+namespace {
 unsigned grid_for(int64_t n) { return (unsigned)std::max<int64_t>(1, std::min<int64_t>(cdiv(n, 256), 4096)); }
 
 }  // namespace
@@ -89,13 +113,24 @@ hipError_t launch_reinit_units(void* W, int val_bf16, int64_t rows, int64_t cols
   const int64_t total = rows * cols;
   if (total == 0) return hipSuccess;
   const float a = 1.0f - lam, b = lam * sigma;
-  const unsigned grid = grid_for(total);
-  if (val_bf16)
-    hipLaunchKernelGGL(k_reinit<bf16_t>, dim3(grid), dim3(256), 0, s, (bf16_t*)W, rows, cols, units_on_rows, last,
-                       step, a, b, noise);
-  else
-    hipLaunchKernelGGL(k_reinit<float>, dim3(grid), dim3(256), 0, s, (float*)W, rows, cols, units_on_rows, last,
-                       step, a, b, noise);
+  if (units_on_rows) {
+    if (!reinit_supported(rows, cols, units_on_rows)) return hipErrorInvalidValue;
+    if (val_bf16)
+      hipLaunchKernelGGL(k_reinit_rows<bf16_t>, dim3((unsigned)rows), dim3(256), 0, s, (bf16_t*)W, cols, last, step,
+                         a, b, noise);
+    else
+      hipLaunchKernelGGL(k_reinit_rows<float>, dim3((unsigned)rows), dim3(256), 0, s, (float*)W, cols, last, step, a,
+                         b, noise);
+  } else {
+    if (!reinit_supported(rows, cols, units_on_rows)) return hipErrorInvalidValue;
+    const int64_t gy = cdiv(rows, kReinitRows);
+    const dim3 grid((unsigned)cdiv(cols, 256), (unsigned)gy);
+    if (val_bf16)
+      hipLaunchKernelGGL(k_reinit_cols<bf16_t>, grid, dim3(256), 0, s, (bf16_t*)W, rows, cols, last, step, a, b,
+                         noise);
+    else
+      hipLaunchKernelGGL(k_reinit_cols<float>, grid, dim3(256), 0, s, (float*)W, rows, cols, last, step, a, b, noise);
+  }
   return hipGetLastError();
 }
 
