@@ -973,14 +973,29 @@ __global__ __launch_bounds__(256) void k_ovf_fill(int64_t f, int NT, int Tn, int
         for (int x = threadIdx.x; x < w; x += 256) row_s[x] = V(0);
       __syncthreads();
       const int j0 = (int)(c0 / Tn), nt = (w + Tn - 1) / Tn;
-      for (int q = threadIdx.x; q < nt * S; q += 256) {
-        const int j = j0 + q / S, slot = q % S;
-        if (slot < sl.count(j)) {
-          V v;
-          uint16_t col;
-          sl.slot(j, slot, v, col);
-          row_s[(int)(col - c0)] = v;
-          if (l1_part) l1 += VT<V>::load(&v, 0);
+      // four slots per thread and pass: their tiles' counts and the slots themselves are
+      // loaded before any is used (a slot past the window re-reads the last one, and a
+      // slot at or past its tile's count holds no entry: neither is stored)
+      constexpr int FU = 4;
+      const int nq = nt * S;
+      for (int q0 = threadIdx.x; q0 < nq; q0 += 256 * FU) {
+        int cj[FU];
+        V v[FU];
+        uint16_t col[FU];
+#pragma unroll
+        for (int u = 0; u < FU; ++u) {
+          const int q = min(q0 + u * 256, nq - 1);
+          const int j = j0 + q / S;
+          cj[u] = sl.count(j);
+          sl.slot(j, q % S, v[u], col[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < FU; ++u) {
+          const int q = q0 + u * 256;
+          if (q < nq && q % S < cj[u]) {
+            row_s[(int)(col[u] - c0)] = v[u];
+            if (l1_part) l1 += VT<V>::load(&v[u], 0);
+          }
         }
       }
       __syncthreads();
