@@ -76,23 +76,43 @@ __global__ __launch_bounds__(1024) void k_blk_mask(int64_t T, int K, int64_t f, 
 
 // (b) per unit: exclusive scan over the blocks (in place: bc[b][n] becomes the offset of
 // block b within unit n's list) and the unit's total; 16 blocks' counts are read at a
-// time so that their loads overlap.
+// time so that their loads overlap (a count past a range re-reads its last one and adds 0).
 __global__ __launch_bounds__(256) void k_blk_scan(int64_t nb, int64_t f, int32_t* __restrict__ bc,
                                                   int32_t* __restrict__ col_cnt) {
-  const int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (n >= f) return;
-  int run = 0;
-  for (int64_t b0 = 0; b0 < nb; b0 += 16) {
+  // 64 units per block; wave p takes the p-th quarter of the blocks of each unit (so four
+  // times as many waves wait on memory at once as with one thread per unit): a pass sums
+  // the quarter, the quarters' sums give each wave its start through LDS, a second pass
+  // (its reads now hitting the cache) writes the offsets
+  __shared__ int qsum[4][64];
+  const int l = threadIdx.x & 63, p = threadIdx.x >> 6;
+  const int64_t n = (int64_t)blockIdx.x * 64 + l;
+  const bool ok = n < f;
+  const int64_t nn = ok ? n : f - 1;
+  const int64_t per = (nb + 3) / 4;
+  const int64_t b_lo = min(nb, p * per), b_hi = min(nb, b_lo + per);
+  int sum = 0;
+  for (int64_t b0 = b_lo; b0 < b_hi; b0 += 16) {
     int c[16];
 #pragma unroll
-    for (int q = 0; q < 16; ++q) c[q] = b0 + q < nb ? bc[(b0 + q) * f + n] : 0;
+    for (int q = 0; q < 16; ++q) c[q] = bc[min(b0 + q, b_hi - 1) * f + nn];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) sum += b0 + q < b_hi ? c[q] : 0;
+  }
+  qsum[p][l] = sum;
+  __syncthreads();
+  int run = 0;
+  for (int i = 0; i < p; ++i) run += qsum[i][l];
+  if (ok && p == 3) col_cnt[n] = run + sum;
+  for (int64_t b0 = b_lo; b0 < b_hi; b0 += 16) {
+    int c[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) c[q] = bc[min(b0 + q, b_hi - 1) * f + nn];
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
-      if (b0 + q < nb) bc[(b0 + q) * f + n] = run;
-      run += c[q];
+      if (ok && b0 + q < b_hi) bc[(b0 + q) * f + n] = run;
+      run += b0 + q < b_hi ? c[q] : 0;
     }
   }
-  col_cnt[n] = run;
 }
 
 // (c) the units' lists laid out in the processing order uorder (the units by descending
@@ -467,7 +487,7 @@ sfl_status_t backward_run(const sfl_ffn_bwd_args_t* a, hipStream_t s) {
                        sv.ell_idx, sv.row_nnz, sv.row_ovf, p.bm, p.bc);
     SFL_HIPB(hipGetLastError());
   }
-  hipLaunchKernelGGL(k_blk_scan, dim3((unsigned)cdiv(f, 256)), dim3(256), 0, s, nb, f, p.bc, p.col_cnt);
+  hipLaunchKernelGGL(k_blk_scan, dim3((unsigned)cdiv(f, 64)), dim3(256), 0, s, nb, f, p.bc, p.col_cnt);
   SFL_HIPB(hipGetLastError());
   // units by descending list length; lists of more than four times the bound on the mean
   // length (T K / f) share the first bucket (fewer buckets: a shorter scan in the sort)
