@@ -57,14 +57,30 @@ __global__ __launch_bounds__(1024) void k_blk_mask(int64_t T, int K, int64_t f, 
   for (int i = threadIdx.x; i < nu; i += 1024) mask_s[i] = 0ull;
   __syncthreads();
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
-  for (int tt = w; tt < kBlkTok; tt += 16) {
-    const int64_t t = b * kBlkTok + tt;
-    if (t >= T || row_ovf[t]) continue;
-    const int nnz = row_nnz[t];
-    for (int e = l; e < nnz; e += 64) {
-      const int64_t n = ell_idx[t * (int64_t)K + e] - u0;
-      if (n >= 0 && n < nu) atomicOr(&mask_s[n], 1ull << tt);
+  // each wave takes kBlkTok / 16 tokens: their counts and flags, then 64 entries of each
+  // per pass, are loaded together (positions past a row or the batch re-read a valid one
+  // and set nothing)
+  constexpr int TW = kBlkTok / 16;
+  int nz[TW];
+#pragma unroll
+  for (int k = 0; k < TW; ++k) {
+    const int64_t t = min(b * kBlkTok + w + 16 * k, T - 1);
+    nz[k] = row_nnz[t];
+    nz[k] = (b * kBlkTok + w + 16 * k < T && !row_ovf[t]) ? nz[k] : 0;
+  }
+  int emax = 0;
+#pragma unroll
+  for (int k = 0; k < TW; ++k) emax = max(emax, nz[k]);
+  for (int e0 = 0; e0 < emax; e0 += 64) {
+    int64_t n[TW];
+#pragma unroll
+    for (int k = 0; k < TW; ++k) {
+      const int64_t t = min(b * kBlkTok + w + 16 * k, T - 1);
+      n[k] = (int64_t)ell_idx[t * (int64_t)K + min(e0 + l, K - 1)] - u0;
     }
+#pragma unroll
+    for (int k = 0; k < TW; ++k)
+      if (e0 + l < nz[k] && n[k] >= 0 && n[k] < nu) atomicOr(&mask_s[n[k]], 1ull << (w + 16 * k));
   }
   __syncthreads();
   for (int i = threadIdx.x; i < nu; i += 1024) {
