@@ -412,11 +412,13 @@ def test_all_active_and_all_inactive_rows():
     assert rel_l2(to_f64(Y), Yref) <= 2e-2
 
 
-@pytest.mark.parametrize("T,d,copies", [(128, 256, False), (48, 512, True), (48, 512, False)])
+@pytest.mark.parametrize("T,d,copies", [(128, 256, False), (48, 512, True), (48, 512, False), (1536, 512, False)])
 def test_capacity_exceeded_flag_then_enough_capacity(T, d, copies):
     """More dense-backup rows than the capacity: the flag, the count and the first `capacity`
     rows of the ascending list, which at most 64 rows with a slice-major gather are built by
-    the gather's first block instead of the list kernel."""
+    the gather's first block, from 1024 rows (tokens sorted by row count) by a second
+    workgroup of the sort's launch, else by the list kernel; the entry total, which the
+    classification's blocks leave to whichever of them builds the list."""
     w = wl.make_ffn("capacity", "bf16", T, d, 512, seed=4, sparsity=0.95, ell_width=16)
     w.shift_t[::4] = 100.0    # T / 4 dense-backup rows
     w.cfg["ovf_capacity"] = 10
@@ -426,6 +428,7 @@ def test_capacity_exceeded_flag_then_enough_capacity(T, d, copies):
     got = twell_views(bufs, w.T, w.f, cfg)
     flagged = np.nonzero(got["row_ovf"])[0]
     assert got["n_ovf"] == st["n_ovf_rows"] == len(flagged)
+    assert st["total_nnz"] == int(got["row_nnz"].astype(np.int64).sum())
     np.testing.assert_array_equal(got["ovf_rows"][:10], flagged[:10])  # ascending, the first `capacity`
     Yref, _ = oracle_rows(w, np.arange(w.T))
     done = got["ovf_rows"][:10]
